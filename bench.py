@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Benchmark of the continual convolution step on one MI355X.
+
+A step is one forward_step call: every one of the B streams consumes one
+frame, the per-step contraction runs, the partial-sum ring is updated and the
+completed output frame is emitted (for the depthwise workload a step is the
+depthwise convolution step followed by the continual average-pool step).
+Inputs (the whole synthetic clip, split into contiguous frames), weights and
+the state are resident in HBM before timing starts; runs longer than the clip
+cycle through its frames, continuing the same state (streams are infinite).
+
+Prints one JSON line: stream-frames/s (B x steps / s, eager forward_step
+calls), the roofline of the dominant kernel measured with HIP events around
+each of its launches, the same steps replayed from a HIP graph and through
+forward_steps, and the CPU oracle timed on a bounded sample of the same
+workload on the host cores.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+DEFAULT_WORKLOAD = "conv3d_b1_c24_k3_56x56_f32"
+METRIC = "stream-frames/sec for CoConv3d forward_step; % of MFMA peak or HBM GB/s"
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+# Non-packed fp32 FMA on the vector ALUs: 256 CUs x 4 SIMDs x 16 lanes x 2
+# FLOP x 2.4 GHz (packed fp32 instructions are not used).
+PEAK_VALU_F32_TFLOPS = 78.6
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--algo", default="auto")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="bounded CPU-oracle sample (seconds of oracle work)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-modes", action="store_true", help="skip graph / forward_steps modes")
+    return ap.parse_args()
+
+
+def per_step_work(c, Ho, Wo):
+    """Algorithmic FLOPs and bytes of one conv step (eager partial sums, stride 1):
+    FLOPs = 2 B Ho Wo C_out kT (C_in/G) kH kW;
+    bytes = |x_n| + |W| + 2 (kT - 1) |Y frame| * 4 (float32 ring RMW) + |y|."""
+    kT, kH, kW = (tuple(c.kernel) + (1, 1))[:3]
+    esz = 2 if c.dtype == "bf16" else 4
+    cg = c.in_channels // c.groups
+    S = 1
+    for s in c.in_size:
+        S *= s
+    So = Ho * Wo
+    flops = 2 * c.batch * So * c.out_channels * kT * cg * kH * kW
+    x_bytes = c.batch * c.in_channels * S * esz
+    w_bytes = c.out_channels * cg * kT * kH * kW * esz
+    ring_bytes = 2 * (kT - 1) * c.batch * c.out_channels * So * 4
+    y_bytes = c.batch * c.out_channels * So * esz
+    return flops, x_bytes + w_bytes + ring_bytes + y_bytes
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU sharding is "
+                                   "not built (streams would shard over the batch)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2204_03418_amd import coinf, synth
+
+    wl = synth.WORKLOADS[args.workload]
+    c = wl.conv
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    x, w, b = synth.workload_inputs(args.workload)
+    T = x.shape[2]
+    frames = [x[:, :, t].contiguous().to(dev) for t in range(T)]
+    co = coinf.CoConv(w.to(dev), b.to(dev) if b is not None else None, batch=c.batch,
+                      in_size=c.in_size, stride=c.stride, padding=c.padding,
+                      dilation=c.dilation, groups=c.groups, algo=args.algo)
+    y = co.new_output()
+    po = None
+    if wl.pool is not None:
+        pl = wl.pool
+        po = coinf.CoPool(pl.kind, batch=pl.batch, channels=pl.channels, kernel=pl.kernel,
+                          in_size=pl.in_size, stride=pl.stride, padding=pl.padding,
+                          count_include_pad=pl.count_include_pad,
+                          dtype=synth.torch_dtype(pl.dtype), device=dev)
+        z = torch.empty(po.out_frame_shape(), dtype=synth.torch_dtype(pl.dtype), device=dev)
+
+    fptr = [ctypes.c_void_p(f.data_ptr()) for f in frames]
+    yptr = ctypes.c_void_p(y.data_ptr())
+    zptr = ctypes.c_void_p(z.data_ptr()) if po is not None else None
+    conv_step = coinf.co_conv_forward_step
+    pool_step = coinf.co_pool_forward_step
+    hconv = co.handle
+    hpool = po.handle if po is not None else None
+
+    def run(n0, count, stream_ptr):
+        for i in range(n0, n0 + count):
+            st = conv_step(hconv, fptr[i % T], yptr, 1, stream_ptr)
+            if hpool is not None and st == coinf.CO_OK:
+                pool_step(hpool, yptr, zptr, 1, stream_ptr)
+
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    # warm-up: past the delay so every timed step emits
+    warm = max(args.warmup, co.delay + (po.delay if po is not None else 0) + 2)
+    run(0, warm, sp)
+    torch.cuda.synchronize()
+    n = warm
+
+    # (i) eager forward_step calls: the headline number
+    K = args.steps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    run(n, K, sp)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    n += K
+    ms = e0.elapsed_time(e1)
+    ms_per_step = ms / K
+    value = c.batch * K / (ms / 1e3)
+
+    # dominant kernel: the conv step, timed with an event pair around each launch
+    Ho, Wo = (tuple(co.out_size) + (1, 1))[:2]
+    flops, nbytes = per_step_work(c, Ho, Wo)
+    Kk = min(K, 1000)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(Kk)]
+    for i in range(Kk):
+        evs[i][0].record(stream)
+        conv_step(hconv, fptr[(n + i) % T], yptr, 1, sp)
+        evs[i][1].record(stream)
+        if hpool is not None:
+            pool_step(hpool, yptr, zptr, 1, sp)
+    torch.cuda.synchronize()
+    n += Kk
+    kern_ms = float(np.mean([a.elapsed_time(b_) for a, b_ in evs]))
+    if c.dtype == "bf16" or co.algo.startswith("gemm"):
+        bound_compute = "mfma"
+        peak_c = PEAK_MFMA_TFLOPS[c.dtype]
+    else:
+        bound_compute = "alu"
+        peak_c = PEAK_VALU_F32_TFLOPS
+    ai = flops / nbytes
+    ridge = peak_c * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if ai >= ridge:
+        achieved = flops / (kern_ms / 1e3) / 1e12
+        roof = {"bound": bound_compute, "achieved": round(achieved, 3), "peak": peak_c,
+                "unit": "TFLOP/s", "frac": round(achieved / peak_c, 5), "traffic": None}
+    else:
+        achieved = nbytes / (kern_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": None}
+    roof.update({"kernel": f"conv step ({co.algo})", "kernel_avg_us": round(kern_ms * 1e3, 3),
+                 "flops_per_launch": flops, "bytes_per_launch": nbytes})
+
+    modes = {"eager_forward_step": round(value, 1)}
+    if not args.no_modes:
+        # (ii) the same steps replayed from a HIP graph: one schedule period
+        # (ring slots x stride) per capture, so replays keep the state coherent
+        period = co.info.ring_slots * c.stride[0]
+        if po is not None:
+            period *= po.info.fifo_slots * wl.pool.stride[0]
+        reps = max(1, K // period)
+        gstream = torch.cuda.Stream()
+        gstream.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(gstream):
+            with torch.cuda.graph(graph, stream=gstream):
+                gp = ctypes.c_void_p(gstream.cuda_stream)
+                run(n, period, gp)
+        n += period
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(reps):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        modes["graph_replay"] = round(c.batch * reps * period / (g0.elapsed_time(g1) / 1e3), 1)
+        # (iii) forward_steps over the resident clip
+        if po is None:
+            xc = x.to(dev)
+            calls = max(1, K // T)
+            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            co.forward_steps(xc)
+            torch.cuda.synchronize()
+            s0.record(stream)
+            for _ in range(calls):
+                co.forward_steps(xc)
+            s1.record(stream)
+            torch.cuda.synchronize()
+            modes["forward_steps"] = round(c.batch * calls * T / (s0.elapsed_time(s1) / 1e3), 1)
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(wl, x, w, b, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "stream-frames/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": warm,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": c.dtype,
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": c.batch, "in_channels": c.in_channels,
+                   "out_channels": c.out_channels, "groups": c.groups,
+                   "kernel": list(c.kernel), "in_size": list(c.in_size),
+                   "padding": list(c.padding), "frames": T, "algo": co.algo,
+                   "pool": None if wl.pool is None else
+                   {"kind": wl.pool.kind, "kernel": list(wl.pool.kernel),
+                    "stride": list(wl.pool.stride)}},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "modes": modes,
+    }
+    print(json.dumps(out))
+
+
+def cpu_baseline(wl, x, w, b, seconds):
+    """The oracle's sliding-window driver stepping the same frames on the host
+    cores (float64, OpenMP over (b, o)); bounded to about `seconds` of work."""
+    import numpy as np
+
+    import oracle
+
+    c = wl.conv
+    xs = x.float().double().numpy()
+    co = oracle.ContinualConv(w.float().double().numpy(),
+                              None if b is None else b.float().double().numpy(),
+                              stride=c.stride, padding=c.padding, dilation=c.dilation,
+                              groups=c.groups)
+    po = None
+    if wl.pool is not None:
+        po = oracle.ContinualPool(wl.pool.kind, wl.pool.kernel, wl.pool.stride, wl.pool.padding,
+                                  count_include_pad=wl.pool.count_include_pad,
+                                  spatial_dims=len(wl.pool.in_size))
+    T = xs.shape[2]
+
+    def step(i):
+        y = co.forward_step(xs[:, :, i % T])
+        if po is not None and y is not None:
+            po.forward_step(y)
+
+    for i in range(co.delay + (po.delay if po else 0) + 1):
+        step(i)
+    i0 = co.delay + (po.delay if po else 0) + 1
+    t0 = time.perf_counter()
+    k = 0
+    while time.perf_counter() - t0 < seconds or k == 0:
+        step(i0 + k)
+        k += 1
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": round(c.batch * k / dt, 3), "unit": "stream-frames/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{k} steps of the same workload after the delay ({dt:.1f} s, float64, "
+                      f"OpenMP over (b, o)); cpu: {cpu_model}"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,303 @@
+/*
+ * coinf.h -- continual convolution and pooling steps on AMD MI355X (gfx950).
+ *
+ * C ABI of libcoinf.so.  The operations follow the statement of Continual
+ * Inference Networks in Hedegaard & Iosifidis, "Continual Inference: A Library
+ * for Efficient Online Inference with Deep Neural Networks in PyTorch"
+ * (arXiv 2204.03418):
+ *
+ *   - Definition 1 (section 2): step inference equals batch inference for
+ *     identical receptive fields, with one set of parameters;
+ *   - Principle 1 (section 3.1): forward, weights and constructor arguments as
+ *     PyTorch's nn.ConvNd / nn.AvgPoolNd / nn.MaxPoolNd;
+ *   - Assumption 1 (section 3.1): clip tensors are (B, C, T, S1, S2), step
+ *     tensors are (B, C, S1, S2);
+ *   - Principle 2 (section 3.1): the call modes forward, forward_step and
+ *     forward_steps;
+ *   - Principle 3 (section 3.1): state rules (steps use and update state,
+ *     update_state = 0 computes without updating, forward is stateless,
+ *     clean_state wipes, outputs are empty until the delay has elapsed);
+ *   - Principle 4 (section 3.1): delay d = f - p - 1, f the receptive field and
+ *     p the temporal padding; padding reduces the delay and end padding is
+ *     only applied on request (pad_end);
+ *   - Principle 5 (section 3.1): a temporal stride s gives one non-empty output
+ *     every s steps.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Every tensor argument is a DEVICE pointer to contiguous memory in
+ * the layout stated at the function.  The caller allocates and frees all
+ * device memory (inputs, outputs, weights, bias and the state buffer, whose
+ * size *_query reports).  The library allocates only the small host handle
+ * (freed by *_destroy) and, in co_conv_forward_steps / co_pool_forward_steps
+ * with update_state = 0, a stream-ordered temporary copy of the state that it
+ * frees on the same stream.  It keeps the state pointer until destroy and no
+ * other pointer past the call.
+ *
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  All device
+ * work is enqueued on it; no call synchronises the host except
+ * *_attach_state, which reads the state header back.
+ *
+ * Status.  CO_OK: an output frame was written.  CO_EMPTY: the call was valid
+ * and produced no output (before the delay, or between strided outputs);
+ * the output buffer is untouched and the state advanced if update_state.
+ * Negative values: nothing was enqueued and the handle is unchanged.  The
+ * OK/EMPTY decision depends only on the step counter, so it is known on
+ * return, before the device work runs.
+ *
+ * Dtypes.  CO_F32 and CO_BF16 name the dtype of x, y, weight and bias.
+ * Accumulation and the state are float32 in both cases; bf16 results are
+ * rounded to nearest-even once, when written.
+ *
+ * Threads.  A handle is not thread-safe; distinct handles are independent.
+ * Concurrent calls on one state buffer race.
+ */
+#ifndef COINF_H
+#define COINF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t co_status;
+#define CO_OK        0   /* output written */
+#define CO_EMPTY     1   /* valid call, no output (Figure 1: empty outputs) */
+#define CO_EINVAL   -1   /* invalid argument or descriptor */
+#define CO_ENOTSUP  -2   /* valid but unsupported (e.g. a forced algorithm) */
+#define CO_ESTATE   -3   /* state buffer too small or not made for this descriptor */
+#define CO_EHIP     -4   /* the HIP runtime reported an error */
+
+#define CO_F32   0
+#define CO_BF16  1
+
+/* Algorithm choice for a convolution (all compute the same result). */
+#define CO_ALGO_AUTO       0   /* library heuristic */
+#define CO_ALGO_DIRECT     1   /* generic direct kernel, any shape */
+#define CO_ALGO_GEMM       2   /* implicit GEMM on MFMA (groups = 1) */
+#define CO_ALGO_DEPTHWISE  3   /* depthwise stencil (groups = C_in = C_out) */
+
+#define CO_POOL_AVG  0
+#define CO_POOL_MAX  1
+
+#define CO_MAX_TAPS  64        /* largest temporal kernel size kT */
+
+/* Per-tap actions of one convolution step (see co_conv_plan_step). */
+#define CO_TAP_NONE        0   /* tap inactive this step */
+#define CO_TAP_START       1   /* first contribution: ring slot := partial */
+#define CO_TAP_ACC         2   /* ring slot += partial */
+#define CO_TAP_EMIT        3   /* y := ring slot + partial + bias (output completes) */
+#define CO_TAP_EMIT_FRESH  4   /* y := partial + bias (the output's only real tap) */
+
+/*
+ * Convolution descriptor (Principle 1: the nn.ConvNd constructor arguments).
+ * spatial_dims 0, 1, 2 selects Conv1d, Conv2d, Conv3d; the first axis of
+ * kernel/stride/padding/dilation is time, the rest are spatial.  Unused
+ * spatial axes must have in_size 1, kernel 1, stride 1, padding 0, dilation 1.
+ * Temporal padding must satisfy 0 <= padding[0] <= f - 1 (non-negative
+ * delay, Principle 4); spatial padding is ordinary zero padding per frame.
+ */
+typedef struct co_conv_desc {
+  int32_t spatial_dims;
+  int32_t batch;                  /* B independent streams, one shared clock (Principle 7) */
+  int32_t in_channels;
+  int32_t out_channels;
+  int32_t groups;
+  int32_t in_size[2];             /* S1, S2 */
+  int32_t kernel[3];
+  int32_t stride[3];
+  int32_t padding[3];
+  int32_t dilation[3];
+  int32_t has_bias;
+  int32_t dtype;                  /* CO_F32 | CO_BF16 */
+  int32_t algo;                   /* CO_ALGO_* */
+} co_conv_desc;
+
+typedef struct co_conv_info {
+  int32_t receptive_field;        /* f = dilation[0] * (kernel[0] - 1) + 1 */
+  int32_t delay;                  /* d = f - padding[0] - 1 (Principle 4) */
+  int32_t out_size[2];            /* spatial output sizes, unused axes 1 */
+  int32_t ring_slots;             /* partial-sum frames kept in the state */
+  int32_t algo;                   /* algorithm resolved from desc->algo */
+  int64_t state_bytes;            /* size of the caller-allocated state buffer */
+} co_conv_info;
+
+/* What one step does, as decided on the host from the step counter alone. */
+typedef struct co_step_plan {
+  int32_t emit;                   /* 1 when the step outputs a frame */
+  int32_t n_taps;                 /* kernel[0] */
+  int64_t out_index;              /* index of the emitted output frame, -1 if none */
+  int8_t  action[CO_MAX_TAPS];    /* CO_TAP_* per temporal tap j */
+  int32_t slot[CO_MAX_TAPS];      /* ring slot the tap touches, -1 if none */
+  int64_t target[CO_MAX_TAPS];    /* output frame the tap contributes to, -1 if none */
+} co_step_plan;
+
+typedef struct co_conv_handle co_conv_handle;
+
+/* Human-readable name of a status code (static string). */
+const char* co_status_str(co_status s);
+
+/*
+ * Validate a descriptor and report receptive field, delay (Principle 4),
+ * spatial output sizes and the state size.  Host only; touches no device.
+ * Returns CO_EINVAL for an invalid descriptor, CO_ENOTSUP when a forced
+ * algorithm cannot run it.
+ */
+co_status co_conv_query(const co_conv_desc* desc, co_conv_info* info);
+
+/*
+ * The schedule of step n (0-based count of frames consumed since a clean
+ * state): which temporal taps of the newly arrived frame are active, the
+ * output frame each feeds and its ring slot, and whether an output completes
+ * (Principles 3-5).  update_state = 0 keeps only the completing tap, since
+ * nothing else may change the state.  The plan of an end-padding frame
+ * (pad_end) is the plan of its step.  Host only; touches no device.
+ */
+co_status co_conv_plan_step(const co_conv_desc* desc, int64_t n, int32_t update_state,
+                            co_step_plan* plan);
+
+/*
+ * Create a handle over a caller-allocated state buffer of at least
+ * info.state_bytes bytes.  Packs `weight` (C_out, C_in/groups, kT[, kH[, kW]],
+ * desc->dtype) and `bias` (C_out, desc->dtype; may be NULL when !has_bias)
+ * into the state -- one set of parameters for step and clip inference
+ * (Definition 1) -- and starts from a clean state (step counter 0, the
+ * padding "pre-saturating" the state as described after Example 2).  The
+ * weight and bias buffers are read on `stream` and may be freed once that
+ * work has completed.
+ */
+co_status co_conv_init_state(const co_conv_desc* desc, const void* weight, const void* bias,
+                             void* state, int64_t state_bytes, void* stream,
+                             co_conv_handle** out);
+
+/*
+ * forward_step (Principle 2): consume one frame x_t (B, C_in, S1, S2) and,
+ * when the schedule emits, write the completed output y_t (B, C_out, So1, So2)
+ * for the output frame delayed by `delay` steps.  Returns CO_OK or CO_EMPTY.
+ * update_state = 0 computes the same output without changing the state
+ * (Principle 3).
+ */
+co_status co_conv_forward_step(co_conv_handle* h, const void* x_t, void* y_t,
+                               int32_t update_state, void* stream);
+
+/*
+ * forward_steps (Principle 2): consume T frames of x (B, C_in, T, S1, S2) as
+ * T forward_step calls and write the non-empty outputs, in order, into
+ * y (B, C_out, y_cap_frames, So1, So2) starting at frame 0.  pad_end = 1
+ * appends padding[0] end-padding zero frames (Principle 4 text).  *n_out
+ * receives the number of frames written.  CO_EINVAL (nothing enqueued) when
+ * more than y_cap_frames outputs would be produced.  update_state = 0 leaves
+ * the state as it was before the call.
+ */
+co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, void* y,
+                                int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
+                                void* stream, int32_t* n_out);
+
+/*
+ * forward (Principle 2, clip mode): the regular convolution of the clip
+ * x (B, C_in, T, S1, S2) with symmetric temporal padding padding[0], written
+ * to y (B, C_out, T_out, So1, So2), T_out = floor((T + 2p - f)/s) + 1 (0 when
+ * negative: nothing is written).  Stateless (Principle 3): no handle.
+ */
+co_status co_conv_forward(const co_conv_desc* desc, const void* weight, const void* bias,
+                          const void* x, int32_t T, void* y, void* stream);
+
+/* Number of T_out frames co_conv_forward produces for a clip of T frames. */
+co_status co_conv_clip_frames(const co_conv_desc* desc, int32_t T, int32_t* t_out);
+
+/* clean_state (Principle 3): wipe the state; the next step is step 0. */
+co_status co_conv_clean_state(co_conv_handle* h, void* stream);
+
+/* Step counter n of the handle (frames consumed since the last clean state). */
+co_status co_conv_get_steps(const co_conv_handle* h, int64_t* n);
+
+/*
+ * Resume from a state buffer that co_conv_init_state prepared for the same
+ * descriptor, after its step-counter value `n` (e.g. a copy saved mid-stream).
+ * Nothing is zeroed or re-packed.  Reads the state header back synchronously;
+ * CO_ESTATE when it does not match the descriptor.
+ */
+co_status co_conv_attach_state(const co_conv_desc* desc, void* state, int64_t state_bytes,
+                               int64_t n, void* stream, co_conv_handle** out);
+
+/* Free the host handle (the state buffer stays the caller's). */
+co_status co_conv_destroy(co_conv_handle* h);
+
+/* Name of the kernel family a handle runs ("direct", "gemm_bf16", ...). */
+const char* co_conv_algo_name(const co_conv_handle* h);
+
+/*
+ * Pool descriptor (Principle 1: nn.AvgPoolNd / nn.MaxPoolNd arguments;
+ * stride must be given explicitly, ceil_mode is not supported).  Padding on
+ * each axis is at most kernel/2 as in PyTorch; dilation is only allowed for
+ * CO_POOL_MAX.  Average pooling counts pads in the divisor when
+ * count_include_pad is set (PyTorch's default); maximum pooling ignores pads.
+ */
+typedef struct co_pool_desc {
+  int32_t kind;                   /* CO_POOL_AVG | CO_POOL_MAX */
+  int32_t spatial_dims;
+  int32_t batch;
+  int32_t channels;
+  int32_t in_size[2];
+  int32_t kernel[3];
+  int32_t stride[3];
+  int32_t padding[3];
+  int32_t dilation[3];
+  int32_t count_include_pad;
+  int32_t dtype;
+} co_pool_desc;
+
+typedef struct co_pool_info {
+  int32_t receptive_field;
+  int32_t delay;
+  int32_t out_size[2];
+  int32_t fifo_slots;             /* spatially pooled frames kept in the state */
+  int32_t reserved;
+  int64_t state_bytes;
+} co_pool_info;
+
+/* One pool step: the FIFO slot written and, when emitting, the window read. */
+typedef struct co_pool_plan {
+  int32_t emit;
+  int32_t n_taps;
+  int64_t out_index;
+  int32_t write_slot;             /* slot of the newly arrived frame */
+  int32_t reserved;
+  int32_t src[CO_MAX_TAPS];       /* per tap: slot, -1 = start padding, -2 = this frame */
+} co_pool_plan;
+
+typedef struct co_pool_handle co_pool_handle;
+
+co_status co_pool_query(const co_pool_desc* desc, co_pool_info* info);
+co_status co_pool_plan_step(const co_pool_desc* desc, int64_t n, co_pool_plan* plan);
+
+/* Clean state over a caller-allocated buffer of info.state_bytes bytes. */
+co_status co_pool_init_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
+                             void* stream, co_pool_handle** out);
+
+/* forward_step of a continual pool: x_t (B, C, S1, S2) -> y_t (B, C, So1, So2). */
+co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
+                               int32_t update_state, void* stream);
+
+/* forward_steps of a continual pool; same conventions as co_conv_forward_steps. */
+co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, void* y,
+                                int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
+                                void* stream, int32_t* n_out);
+
+/* Clip-mode pooling with symmetric temporal padding; stateless. */
+co_status co_pool_forward(const co_pool_desc* desc, const void* x, int32_t T, void* y,
+                          void* stream);
+co_status co_pool_clip_frames(const co_pool_desc* desc, int32_t T, int32_t* t_out);
+
+co_status co_pool_clean_state(co_pool_handle* h, void* stream);
+co_status co_pool_get_steps(const co_pool_handle* h, int64_t* n);
+co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
+                               int64_t n, void* stream, co_pool_handle** out);
+co_status co_pool_destroy(co_pool_handle* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COINF_H */

@@ -1,0 +1,438 @@
+// C ABI of libcoinf: validation, handle bookkeeping and the step loops.
+// Every entry point validates on the host before it enqueues anything, so a
+// negative status means nothing ran and the handle is unchanged.
+#include <new>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+using namespace coinf;
+
+struct co_conv_handle {
+  ConvGeom g;
+  ConvLayout L;
+  char* state;
+  int64_t n;  // frames consumed since the last clean state
+};
+
+struct co_pool_handle {
+  PoolGeom g;
+  PoolLayout L;
+  char* state;
+  int64_t n;
+};
+
+namespace {
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_EHIP; }
+
+bool any_tap(const co_step_plan& p) {
+  for (int j = 0; j < p.n_taps; ++j)
+    if (p.action[j] != CO_TAP_NONE) return true;
+  return false;
+}
+
+co_status read_header(const void* state, hipStream_t s, StateHeader* h) {
+  if (hipMemcpyAsync(h, state, sizeof(*h), hipMemcpyDeviceToHost, s) != hipSuccess)
+    return CO_EHIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return CO_EHIP;
+  return CO_OK;
+}
+
+// Stream-ordered backup of a byte range, restored by restore_range.
+struct Backup {
+  void* tmp = nullptr;
+  int64_t bytes = 0;
+};
+
+co_status backup_range(char* src, int64_t bytes, hipStream_t s, Backup* b) {
+  b->bytes = bytes;
+  if (bytes == 0) return CO_OK;
+  if (hipMallocAsync(&b->tmp, size_t(bytes), s) != hipSuccess) return CO_EHIP;
+  if (hipMemcpyAsync(b->tmp, src, size_t(bytes), hipMemcpyDeviceToDevice, s) != hipSuccess)
+    return CO_EHIP;
+  return CO_OK;
+}
+
+co_status restore_range(char* dst, hipStream_t s, Backup* b) {
+  if (b->bytes == 0) return CO_OK;
+  co_status st = CO_OK;
+  if (hipMemcpyAsync(dst, b->tmp, size_t(b->bytes), hipMemcpyDeviceToDevice, s) != hipSuccess)
+    st = CO_EHIP;
+  if (hipFreeAsync(b->tmp, s) != hipSuccess) st = CO_EHIP;
+  b->tmp = nullptr;
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* co_status_str(co_status s) {
+  switch (s) {
+    case CO_OK: return "CO_OK";
+    case CO_EMPTY: return "CO_EMPTY";
+    case CO_EINVAL: return "CO_EINVAL: invalid argument";
+    case CO_ENOTSUP: return "CO_ENOTSUP: unsupported configuration";
+    case CO_ESTATE: return "CO_ESTATE: state buffer too small or made for another descriptor";
+    case CO_EHIP: return "CO_EHIP: HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+// ---------------------------------------------------------------- convolution
+
+co_status co_conv_query(const co_conv_desc* desc, co_conv_info* info) {
+  if (!info) return CO_EINVAL;
+  ConvGeom g;
+  const co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const ConvLayout L = conv_layout(g);
+  info->receptive_field = g.f;
+  info->delay = g.d;
+  info->out_size[0] = g.Ho;
+  info->out_size[1] = g.Wo;
+  info->ring_slots = g.R;
+  info->algo = g.algo;
+  info->state_bytes = L.total;
+  return CO_OK;
+}
+
+co_status co_conv_plan_step(const co_conv_desc* desc, int64_t n, int32_t update_state,
+                            co_step_plan* plan) {
+  if (!plan || n < 0) return CO_EINVAL;
+  ConvGeom g;
+  const co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  conv_plan(g, n, update_state != 0, plan);
+  return CO_OK;
+}
+
+co_status co_conv_init_state(const co_conv_desc* desc, const void* weight, const void* bias,
+                             void* state, int64_t state_bytes, void* stream,
+                             co_conv_handle** out) {
+  if (!out || !state || !weight) return CO_EINVAL;
+  ConvGeom g;
+  co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (g.has_bias && !bias) return CO_EINVAL;
+  const ConvLayout L = conv_layout(g);
+  if (state_bytes < L.total) return CO_ESTATE;
+  StateHeader hdr{kConvMagic, kStateVersion, conv_hash(g), L.total, g.algo, g.R};
+  co_conv_handle* h = new (std::nothrow) co_conv_handle{g, L, static_cast<char*>(state), 0};
+  if (!h) return CO_EINVAL;
+  st = hip_status(launch_conv_init(g, L, h->state, weight, bias, hdr, as_stream(stream)));
+  if (st != CO_OK) {
+    delete h;
+    return st;
+  }
+  *out = h;
+  return CO_OK;
+}
+
+co_status co_conv_forward_step(co_conv_handle* h, const void* x_t, void* y_t,
+                               int32_t update_state, void* stream) {
+  if (!h || !x_t) return CO_EINVAL;
+  co_step_plan plan;
+  conv_plan(h->g, h->n, update_state != 0, &plan);
+  if (plan.emit && !y_t) return CO_EINVAL;
+  if (any_tap(plan)) {
+    const StepIO io{x_t, h->g.S(), y_t, h->g.So()};
+    const co_status st =
+        hip_status(launch_conv_step(h->g, h->L, h->state, io, plan, false, as_stream(stream)));
+    if (st != CO_OK) return st;
+  }
+  if (update_state) ++h->n;
+  return plan.emit ? CO_OK : CO_EMPTY;
+}
+
+co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, void* y,
+                                int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
+                                void* stream, int32_t* n_out) {
+  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  const ConvGeom& g = h->g;
+  const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  const int64_t n_emit = conv_emissions(g, h->n, count);
+  if (n_emit > y_cap_frames) return CO_EINVAL;
+  if (n_emit > 0 && !y) return CO_EINVAL;
+  hipStream_t s = as_stream(stream);
+  const int64_t n0 = h->n;
+  Backup bk;
+  const int64_t ring_bytes = int64_t(g.R) * h->L.ring_slot_elems * 4;
+  if (!update_state) {
+    const co_status st = backup_range(h->state + h->L.ring, ring_bytes, s, &bk);
+    if (st != CO_OK) return st;
+  }
+  const int64_t S = g.S(), So = g.So();
+  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  int64_t k = 0;
+  co_status st = CO_OK;
+  for (int64_t t = 0; t < count; ++t) {
+    co_step_plan plan;
+    conv_plan(g, h->n, true, &plan);
+    const bool pad = t >= T;
+    if (any_tap(plan)) {
+      const StepIO io{pad ? nullptr : static_cast<const char*>(x) + size_t(t * S) * esz,
+                      int64_t(T) * S,
+                      plan.emit ? static_cast<char*>(y) + size_t(k * So) * esz : nullptr,
+                      int64_t(y_cap_frames) * So};
+      st = hip_status(launch_conv_step(g, h->L, h->state, io, plan, pad, s));
+      if (st != CO_OK) break;
+    }
+    if (plan.emit) ++k;
+    ++h->n;
+  }
+  if (!update_state) {
+    const co_status r = restore_range(h->state + h->L.ring, s, &bk);
+    if (st == CO_OK) st = r;
+    h->n = n0;
+  }
+  *n_out = int32_t(k);
+  return st;
+}
+
+co_status co_conv_clip_frames(const co_conv_desc* desc, int32_t T, int32_t* t_out) {
+  if (!t_out || T < 0) return CO_EINVAL;
+  ConvGeom g;
+  const co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  *t_out = int32_t(axis_out_len(T, g.kT, g.sT, g.pT, g.dT));
+  return CO_OK;
+}
+
+co_status co_conv_forward(const co_conv_desc* desc, const void* weight, const void* bias,
+                          const void* x, int32_t T, void* y, void* stream) {
+  ConvGeom g;
+  co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (T < 0 || !weight || (g.has_bias && !bias)) return CO_EINVAL;
+  const int64_t T_out = axis_out_len(T, g.kT, g.sT, g.pT, g.dT);
+  if (T_out == 0) return CO_OK;
+  if (!x || !y) return CO_EINVAL;
+  if (int64_t(g.B) * g.Cout * T_out * g.So() > (int64_t(1) << 40)) return CO_EINVAL;
+  return hip_status(launch_conv_clip(g, T, int32_t(T_out), weight, bias, x, y, as_stream(stream)));
+}
+
+co_status co_conv_clean_state(co_conv_handle* h, void* stream) {
+  (void)stream;
+  if (!h) return CO_EINVAL;
+  // Every partial sum is started by the first real tap of its output before
+  // anything reads it, so a clean state needs no device work.
+  h->n = 0;
+  return CO_OK;
+}
+
+co_status co_conv_get_steps(const co_conv_handle* h, int64_t* n) {
+  if (!h || !n) return CO_EINVAL;
+  *n = h->n;
+  return CO_OK;
+}
+
+co_status co_conv_attach_state(const co_conv_desc* desc, void* state, int64_t state_bytes,
+                               int64_t n, void* stream, co_conv_handle** out) {
+  if (!out || !state || n < 0) return CO_EINVAL;
+  ConvGeom g;
+  co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const ConvLayout L = conv_layout(g);
+  if (state_bytes < L.total) return CO_ESTATE;
+  StateHeader hdr;
+  st = read_header(state, as_stream(stream), &hdr);
+  if (st != CO_OK) return st;
+  if (hdr.magic != kConvMagic || hdr.version != kStateVersion || hdr.desc_hash != conv_hash(g) ||
+      hdr.bytes != L.total || hdr.algo != g.algo || hdr.slots != g.R)
+    return CO_ESTATE;
+  co_conv_handle* h = new (std::nothrow) co_conv_handle{g, L, static_cast<char*>(state), n};
+  if (!h) return CO_EINVAL;
+  *out = h;
+  return CO_OK;
+}
+
+co_status co_conv_destroy(co_conv_handle* h) {
+  if (!h) return CO_EINVAL;
+  delete h;
+  return CO_OK;
+}
+
+const char* co_conv_algo_name(const co_conv_handle* h) {
+  if (!h) return "none";
+  switch (h->g.algo) {
+    case CO_ALGO_DEPTHWISE: return "depthwise";
+    case CO_ALGO_GEMM: return h->g.dtype == CO_BF16 ? "gemm_bf16" : "gemm_f32";
+    default: return "direct";
+  }
+}
+
+// -------------------------------------------------------------------- pooling
+
+co_status co_pool_query(const co_pool_desc* desc, co_pool_info* info) {
+  if (!info) return CO_EINVAL;
+  PoolGeom g;
+  const co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const PoolLayout L = pool_layout(g);
+  info->receptive_field = g.f;
+  info->delay = g.d;
+  info->out_size[0] = g.Ho;
+  info->out_size[1] = g.Wo;
+  info->fifo_slots = g.R;
+  info->reserved = 0;
+  info->state_bytes = L.total;
+  return CO_OK;
+}
+
+co_status co_pool_plan_step(const co_pool_desc* desc, int64_t n, co_pool_plan* plan) {
+  if (!plan || n < 0) return CO_EINVAL;
+  PoolGeom g;
+  const co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  pool_plan(g, n, plan);
+  return CO_OK;
+}
+
+co_status co_pool_init_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
+                             void* stream, co_pool_handle** out) {
+  if (!out || !state) return CO_EINVAL;
+  PoolGeom g;
+  co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const PoolLayout L = pool_layout(g);
+  if (state_bytes < L.total) return CO_ESTATE;
+  StateHeader hdr{kPoolMagic, kStateVersion, pool_hash(g), L.total, 0, g.R};
+  co_pool_handle* h = new (std::nothrow) co_pool_handle{g, L, static_cast<char*>(state), 0};
+  if (!h) return CO_EINVAL;
+  st = hip_status(launch_pool_init(g, L, h->state, hdr, as_stream(stream)));
+  if (st != CO_OK) {
+    delete h;
+    return st;
+  }
+  *out = h;
+  return CO_OK;
+}
+
+co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
+                               int32_t update_state, void* stream) {
+  if (!h || !x_t) return CO_EINVAL;
+  co_pool_plan plan;
+  pool_plan(h->g, h->n, &plan);
+  if (plan.emit && !y_t) return CO_EINVAL;
+  if (plan.emit || update_state) {
+    const StepIO io{x_t, h->g.S(), y_t, h->g.So()};
+    const co_status st = hip_status(launch_pool_step(h->g, h->L, h->state, io, plan,
+                                                     update_state != 0, false, as_stream(stream)));
+    if (st != CO_OK) return st;
+  }
+  if (update_state) ++h->n;
+  return plan.emit ? CO_OK : CO_EMPTY;
+}
+
+co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, void* y,
+                                int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
+                                void* stream, int32_t* n_out) {
+  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  const PoolGeom& g = h->g;
+  const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  const int64_t n_emit = pool_emissions(g, h->n, count);
+  if (n_emit > y_cap_frames) return CO_EINVAL;
+  if (n_emit > 0 && !y) return CO_EINVAL;
+  hipStream_t s = as_stream(stream);
+  const int64_t n0 = h->n;
+  Backup bk;
+  // FIFO and validity flags are contiguous from L.valid to the end
+  const int64_t bytes = h->L.total - h->L.valid;
+  if (!update_state) {
+    const co_status st = backup_range(h->state + h->L.valid, bytes, s, &bk);
+    if (st != CO_OK) return st;
+  }
+  const int64_t S = g.S(), So = g.So();
+  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  int64_t k = 0;
+  co_status st = CO_OK;
+  for (int64_t t = 0; t < count; ++t) {
+    co_pool_plan plan;
+    pool_plan(g, h->n, &plan);
+    const bool pad = t >= T;
+    const StepIO io{pad ? nullptr : static_cast<const char*>(x) + size_t(t * S) * esz,
+                    int64_t(T) * S,
+                    plan.emit ? static_cast<char*>(y) + size_t(k * So) * esz : nullptr,
+                    int64_t(y_cap_frames) * So};
+    st = hip_status(launch_pool_step(g, h->L, h->state, io, plan, true, pad, s));
+    if (st != CO_OK) break;
+    if (plan.emit) ++k;
+    ++h->n;
+  }
+  if (!update_state) {
+    const co_status r = restore_range(h->state + h->L.valid, s, &bk);
+    if (st == CO_OK) st = r;
+    h->n = n0;
+  }
+  *n_out = int32_t(k);
+  return st;
+}
+
+co_status co_pool_clip_frames(const co_pool_desc* desc, int32_t T, int32_t* t_out) {
+  if (!t_out || T < 0) return CO_EINVAL;
+  PoolGeom g;
+  const co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  *t_out = int32_t(axis_out_len(T, g.kT, g.sT, g.pT, g.dT));
+  return CO_OK;
+}
+
+co_status co_pool_forward(const co_pool_desc* desc, const void* x, int32_t T, void* y,
+                          void* stream) {
+  PoolGeom g;
+  co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (T < 0) return CO_EINVAL;
+  const int64_t T_out = axis_out_len(T, g.kT, g.sT, g.pT, g.dT);
+  if (T_out == 0) return CO_OK;
+  if (!x || !y) return CO_EINVAL;
+  return hip_status(launch_pool_clip(g, T, int32_t(T_out), x, y, as_stream(stream)));
+}
+
+co_status co_pool_clean_state(co_pool_handle* h, void* stream) {
+  (void)stream;
+  if (!h) return CO_EINVAL;
+  // The FIFO is only read for frames written since the last clean state.
+  h->n = 0;
+  return CO_OK;
+}
+
+co_status co_pool_get_steps(const co_pool_handle* h, int64_t* n) {
+  if (!h || !n) return CO_EINVAL;
+  *n = h->n;
+  return CO_OK;
+}
+
+co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
+                               int64_t n, void* stream, co_pool_handle** out) {
+  if (!out || !state || n < 0) return CO_EINVAL;
+  PoolGeom g;
+  co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const PoolLayout L = pool_layout(g);
+  if (state_bytes < L.total) return CO_ESTATE;
+  StateHeader hdr;
+  st = read_header(state, as_stream(stream), &hdr);
+  if (st != CO_OK) return st;
+  if (hdr.magic != kPoolMagic || hdr.version != kStateVersion || hdr.desc_hash != pool_hash(g) ||
+      hdr.bytes != L.total || hdr.slots != g.R)
+    return CO_ESTATE;
+  co_pool_handle* h = new (std::nothrow) co_pool_handle{g, L, static_cast<char*>(state), n};
+  if (!h) return CO_EINVAL;
+  *out = h;
+  return CO_OK;
+}
+
+co_status co_pool_destroy(co_pool_handle* h) {
+  if (!h) return CO_EINVAL;
+  delete h;
+  return CO_OK;
+}
+
+}  // extern "C"

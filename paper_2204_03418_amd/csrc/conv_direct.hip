@@ -1,0 +1,219 @@
+// Generic continual convolution kernels: the direct step kernel (any groups,
+// stride, padding, dilation), the end-padding step, clip-mode convolution and
+// the init-time packing of bias, weights and the state header.
+//
+// The step realises the eager evaluation the paper describes in section 3.1
+// (before Principle 3): when a frame arrives, its contribution through every
+// temporal tap j is computed at once and stored as a partial sum of the output
+// frame that tap feeds; the output whose last tap this frame is completes and
+// is emitted.  Partial sums live in a float32 ring of R output frames inside
+// the caller's state buffer, laid out (slot, B, C_out, Ho, Wo).
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace coinf {
+
+namespace {
+
+// One thread per output element (b, o, i, j); taps in an outer loop so the
+// kernel handles any kT without a register array.
+template <typename T, bool ZERO>
+__global__ __launch_bounds__(kBlock) void conv_step_direct_kernel(
+    ConvGeom g, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y, int64_t y_bc,
+    const float* __restrict__ w, const float* __restrict__ bias, float* __restrict__ ring,
+    int64_t ring_slot, TapTable tt) {
+  const int32_t So = g.Ho * g.Wo;
+  const int32_t total = g.B * g.Cout * So;
+  const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  if (idx >= total) return;
+  const int32_t p = idx % So;
+  const int32_t bo = idx / So;
+  const int32_t o = bo % g.Cout;
+  const int32_t b = bo / g.Cout;
+  const int32_t i = p / g.Wo, jo = p % g.Wo;
+  const int32_t grp = o / g.Og;
+  const T* xb = x + (int64_t(b) * g.Cin + int64_t(grp) * g.Cg) * x_bc;
+  const int32_t kHW = g.kH * g.kW;
+  for (int32_t j = 0; j < g.kT; ++j) {
+    const int act = tt.action[j];
+    if (act == CO_TAP_NONE) continue;
+    float acc = 0.f;
+    if (!ZERO) {
+      for (int32_t c = 0; c < g.Cg; ++c) {
+        const T* xc = xb + int64_t(c) * x_bc;
+        const float* wc = w + (int64_t(o) * g.Cg + c) * g.kT * kHW + int64_t(j) * kHW;
+        for (int32_t u = 0; u < g.kH; ++u) {
+          const int32_t hi = i * g.sH + u * g.dH - g.pH;
+          if (hi < 0 || hi >= g.H) continue;
+          for (int32_t v = 0; v < g.kW; ++v) {
+            const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+            if (wi < 0 || wi >= g.W) continue;
+            acc = fmaf(wc[u * g.kW + v], to_f32<T>(xc[hi * g.W + wi]), acc);
+          }
+        }
+      }
+    }
+    float* r = ring + int64_t(tt.slot[j] < 0 ? 0 : tt.slot[j]) * ring_slot + idx;
+    const int64_t yi = int64_t(bo) * y_bc + p;
+    switch (act) {
+      case CO_TAP_START: *r = acc; break;
+      case CO_TAP_ACC: *r = *r + acc; break;
+      case CO_TAP_EMIT: y[yi] = from_f32<T>(*r + acc + bias[o]); break;
+      case CO_TAP_EMIT_FRESH: y[yi] = from_f32<T>(acc + bias[o]); break;
+      default: break;
+    }
+  }
+}
+
+// Clip-mode regular convolution: one thread per output element.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void conv_clip_direct_kernel(
+    ConvGeom g, int32_t T_in, int32_t T_out, const T* __restrict__ x, const T* __restrict__ w,
+    const T* __restrict__ bias, T* __restrict__ y) {
+  const int64_t So = int64_t(g.Ho) * g.Wo;
+  const int64_t total = int64_t(g.B) * g.Cout * T_out * So;
+  const int64_t idx = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx >= total) return;
+  const int64_t p = idx % So;
+  const int64_t t = (idx / So) % T_out;
+  const int64_t bo = idx / (So * T_out);
+  const int32_t o = int32_t(bo % g.Cout);
+  const int32_t b = int32_t(bo / g.Cout);
+  const int32_t i = int32_t(p / g.Wo), jo = int32_t(p % g.Wo);
+  const int32_t grp = o / g.Og;
+  const int64_t S = int64_t(g.H) * g.W;
+  float acc = 0.f;
+  for (int32_t c = 0; c < g.Cg; ++c) {
+    const T* xc = x + (int64_t(b) * g.Cin + int64_t(grp) * g.Cg + c) * T_in * S;
+    for (int32_t a = 0; a < g.kT; ++a) {
+      const int64_t ti = t * g.sT + int64_t(a) * g.dT - g.pT;
+      if (ti < 0 || ti >= T_in) continue;
+      for (int32_t u = 0; u < g.kH; ++u) {
+        const int32_t hi = i * g.sH + u * g.dH - g.pH;
+        if (hi < 0 || hi >= g.H) continue;
+        for (int32_t v = 0; v < g.kW; ++v) {
+          const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+          if (wi < 0 || wi >= g.W) continue;
+          const float wv = to_f32<T>(w[(((int64_t(o) * g.Cg + c) * g.kT + a) * g.kH + u) * g.kW + v]);
+          acc = fmaf(wv, to_f32<T>(xc[ti * S + hi * g.W + wi]), acc);
+        }
+      }
+    }
+  }
+  if (g.has_bias) acc += to_f32<T>(bias[o]);
+  y[idx] = from_f32<T>(acc);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void pack_bias_kernel(int32_t n, int32_t has_bias,
+                                                           const T* __restrict__ src,
+                                                           float* __restrict__ dst) {
+  const int32_t i = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  if (i < n) dst[i] = has_bias ? to_f32<T>(src[i]) : 0.f;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void pack_f32_kernel(int64_t n, const T* __restrict__ src,
+                                                          float* __restrict__ dst) {
+  const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (i < n) dst[i] = to_f32<T>(src[i]);
+}
+
+__global__ void write_header_kernel(StateHeader h, StateHeader* dst) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *dst = h;
+}
+
+template <typename T>
+hipError_t step_direct_t(const ConvGeom& g, const ConvLayout& L, char* state, const StepIO& io,
+                         const co_step_plan& plan, bool zero_frame, hipStream_t s) {
+  TapTable tt;
+  for (int j = 0; j < CO_MAX_TAPS; ++j) {
+    tt.action[j] = plan.action[j];
+    tt.slot[j] = plan.slot[j];
+  }
+  const float* w = reinterpret_cast<const float*>(state + L.weight);
+  const float* bias = reinterpret_cast<const float*>(state + L.bias);
+  float* ring = reinterpret_cast<float*>(state + L.ring);
+  const unsigned grid = grid_for(g.out_frame_elems());
+  if (zero_frame)
+    hipLaunchKernelGGL((conv_step_direct_kernel<T, true>), dim3(grid), dim3(kBlock), 0, s, g,
+                       static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc, w,
+                       bias, ring, L.ring_slot_elems, tt);
+  else
+    hipLaunchKernelGGL((conv_step_direct_kernel<T, false>), dim3(grid), dim3(kBlock), 0, s, g,
+                       static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc, w,
+                       bias, ring, L.ring_slot_elems, tt);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char* state,
+                                   const StepIO& io, const co_step_plan& plan, bool zero_frame,
+                                   hipStream_t s) {
+  if (g.dtype == CO_BF16) return step_direct_t<bf16_t>(g, L, state, io, plan, zero_frame, s);
+  return step_direct_t<float>(g, L, state, io, plan, zero_frame, s);
+}
+
+hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,
+                            const StepIO& io, const co_step_plan& plan, bool zero_frame,
+                            hipStream_t s) {
+  // An end-padding frame contributes exactly zero: every algorithm shares the
+  // ring layout, so the direct kernel's no-contraction path serves them all.
+  if (zero_frame) return launch_conv_step_direct(g, L, state, io, plan, true, s);
+  switch (g.algo) {
+    case CO_ALGO_DEPTHWISE: return launch_conv_step_depthwise(g, L, state, io, plan, s);
+    case CO_ALGO_GEMM: return launch_conv_step_gemm(g, L, state, io, plan, s);
+    default: return launch_conv_step_direct(g, L, state, io, plan, false, s);
+  }
+}
+
+hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
+                            const void* weight, const void* bias, const StateHeader& hdr,
+                            hipStream_t s) {
+  float* bdst = reinterpret_cast<float*>(state + L.bias);
+  if (g.dtype == CO_BF16)
+    hipLaunchKernelGGL(pack_bias_kernel<bf16_t>, dim3(grid_for(g.Cout)), dim3(kBlock), 0, s,
+                       g.Cout, g.has_bias, static_cast<const bf16_t*>(bias), bdst);
+  else
+    hipLaunchKernelGGL(pack_bias_kernel<float>, dim3(grid_for(g.Cout)), dim3(kBlock), 0, s,
+                       g.Cout, g.has_bias, static_cast<const float*>(bias), bdst);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (g.algo == CO_ALGO_GEMM) {
+    e = launch_pack_gemm(g, L, state, weight, s);
+  } else {
+    const int64_t n = int64_t(g.Cout) * g.Cg * g.kT * g.kH * g.kW;
+    float* wdst = reinterpret_cast<float*>(state + L.weight);
+    if (g.dtype == CO_BF16)
+      hipLaunchKernelGGL(pack_f32_kernel<bf16_t>, dim3(grid_for(n)), dim3(kBlock), 0, s, n,
+                         static_cast<const bf16_t*>(weight), wdst);
+    else
+      hipLaunchKernelGGL(pack_f32_kernel<float>, dim3(grid_for(n)), dim3(kBlock), 0, s, n,
+                         static_cast<const float*>(weight), wdst);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, s, hdr,
+                     reinterpret_cast<StateHeader*>(state + L.header));
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_clip(const ConvGeom& g, int32_t T, int32_t T_out, const void* weight,
+                            const void* bias, const void* x, void* y, hipStream_t s) {
+  const int64_t total = int64_t(g.B) * g.Cout * T_out * g.So();
+  if (total == 0) return hipSuccess;
+  if (g.dtype == CO_BF16)
+    hipLaunchKernelGGL(conv_clip_direct_kernel<bf16_t>, dim3(grid_for(total)), dim3(kBlock), 0,
+                       s, g, T, T_out, static_cast<const bf16_t*>(x),
+                       static_cast<const bf16_t*>(weight), static_cast<const bf16_t*>(bias),
+                       static_cast<bf16_t*>(y));
+  else
+    hipLaunchKernelGGL(conv_clip_direct_kernel<float>, dim3(grid_for(total)), dim3(kBlock), 0,
+                       s, g, T, T_out, static_cast<const float*>(x),
+                       static_cast<const float*>(weight), static_cast<const float*>(bias),
+                       static_cast<float*>(y));
+  return hipGetLastError();
+}
+
+}  // namespace coinf

@@ -1,0 +1,58 @@
+// Kernel launchers of libcoinf (host side of the HIP kernels).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "schedule.hpp"
+
+namespace coinf {
+
+// Where one step reads its frame and writes its output.  x_bc / y_bc are the
+// element strides between consecutive (batch, channel) planes: S for a single
+// frame (B, C, S1, S2), T*S when the frame is read in place from a clip
+// (B, C, T, S1, S2).
+struct StepIO {
+  const void* x;
+  int64_t x_bc;
+  void* y;
+  int64_t y_bc;
+};
+
+// One convolution step with the handle's algorithm.  zero_frame runs an
+// end-padding frame, which contributes exactly zero (no contraction).
+hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,
+                            const StepIO& io, const co_step_plan& plan, bool zero_frame,
+                            hipStream_t stream);
+
+// Pack bias and weights into the state and write its header.
+hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
+                            const void* weight, const void* bias, const StateHeader& hdr,
+                            hipStream_t stream);
+
+// Clip-mode regular convolution (symmetric temporal padding).
+hipError_t launch_conv_clip(const ConvGeom& g, int32_t T, int32_t T_out, const void* weight,
+                            const void* bias, const void* x, void* y, hipStream_t stream);
+
+hipError_t launch_pool_step(const PoolGeom& g, const PoolLayout& L, char* state,
+                            const StepIO& io, const co_pool_plan& plan, bool update_state,
+                            bool pad_frame, hipStream_t stream);
+
+hipError_t launch_pool_init(const PoolGeom& g, const PoolLayout& L, char* state,
+                            const StateHeader& hdr, hipStream_t stream);
+
+hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const void* x, void* y,
+                            hipStream_t stream);
+
+// Per-algorithm step launchers (defined next to their kernels).
+hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char* state,
+                                   const StepIO& io, const co_step_plan& plan, bool zero_frame,
+                                   hipStream_t stream);
+hipError_t launch_conv_step_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
+                                      const StepIO& io, const co_step_plan& plan,
+                                      hipStream_t stream);
+hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
+                                 const StepIO& io, const co_step_plan& plan, hipStream_t stream);
+hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
+                            const void* weight, hipStream_t stream);
+
+}  // namespace coinf

@@ -1,0 +1,173 @@
+// Continual average / maximum pooling kernels.
+//
+// A pooling window factorises into a spatial reduction of each frame and a
+// temporal reduction over the window's frames.  The state keeps the spatially
+// reduced frames of the last f input frames in a FIFO of float32 frames
+// (slot, B, C, Ho, Wo) plus one validity flag per slot (0 for end-padding
+// frames).  Each step reduces the arriving frame once -- the intermediate
+// result future outputs need, computed eagerly as section 3.1 describes
+// before Principle 3 -- and, when the schedule emits, reduces the window's
+// kT slots into the output.  Average pooling stores window sums (pads add 0)
+// and divides once at emission; maximum pooling stores window maxima (pads
+// are -inf).
+#include <math.h>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace coinf {
+
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void pool_step_kernel(
+    PoolGeom g, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y, int64_t y_bc,
+    float* __restrict__ fifo, int64_t fifo_slot, float* __restrict__ valid, int32_t write_slot,
+    int32_t update, int32_t emit, int32_t pad_frame, PoolTaps taps) {
+  const int32_t So = g.Ho * g.Wo;
+  const int32_t total = g.B * g.C * So;
+  const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  if (idx >= total) return;
+  const int32_t p = idx % So;
+  const int32_t bc = idx / So;
+  const int32_t i = p / g.Wo, jo = p % g.Wo;
+  const bool is_max = g.kind == CO_POOL_MAX;
+  // spatial reduction of the arriving frame
+  float val = is_max ? -INFINITY : 0.f;
+  int32_t scount = 0;
+  for (int32_t u = 0; u < g.kH; ++u) {
+    const int32_t hi = i * g.sH + u * g.dH - g.pH;
+    if (hi < 0 || hi >= g.H) continue;
+    for (int32_t v = 0; v < g.kW; ++v) {
+      const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+      if (wi < 0 || wi >= g.W) continue;
+      ++scount;
+      if (!pad_frame) {
+        const float e = to_f32<T>(x[int64_t(bc) * x_bc + hi * g.W + wi]);
+        val = is_max ? fmaxf(val, e) : val + e;
+      }
+    }
+  }
+  if (update) {
+    fifo[int64_t(write_slot) * fifo_slot + idx] = val;
+    if (idx == 0) valid[write_slot] = pad_frame ? 0.f : 1.f;
+  }
+  if (!emit) return;
+  float acc = is_max ? -INFINITY : 0.f;
+  int32_t tcount = 0;
+  for (int32_t j = 0; j < g.kT; ++j) {
+    const int32_t s = taps.src[j];
+    float e;
+    int32_t ok;
+    if (s == -1) {  // start padding
+      continue;
+    } else if (s == -2) {  // the arriving frame
+      e = val;
+      ok = pad_frame ? 0 : 1;
+    } else {
+      e = fifo[int64_t(s) * fifo_slot + idx];
+      ok = valid[s] != 0.f ? 1 : 0;
+    }
+    acc = is_max ? fmaxf(acc, e) : acc + e;
+    tcount += ok;
+  }
+  float out;
+  if (is_max) {
+    out = acc;
+  } else {
+    const int32_t div = g.count_include_pad ? g.kT * g.kH * g.kW : tcount * scount;
+    out = div > 0 ? acc / float(div) : 0.f;
+  }
+  y[int64_t(bc) * y_bc + p] = from_f32<T>(out);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void pool_clip_kernel(PoolGeom g, int32_t T_in,
+                                                           int32_t T_out,
+                                                           const T* __restrict__ x,
+                                                           T* __restrict__ y) {
+  const int64_t So = int64_t(g.Ho) * g.Wo;
+  const int64_t total = int64_t(g.B) * g.C * T_out * So;
+  const int64_t idx = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx >= total) return;
+  const int64_t p = idx % So;
+  const int64_t t = (idx / So) % T_out;
+  const int64_t bc = idx / (So * T_out);
+  const int32_t i = int32_t(p / g.Wo), jo = int32_t(p % g.Wo);
+  const int64_t S = int64_t(g.H) * g.W;
+  const bool is_max = g.kind == CO_POOL_MAX;
+  float acc = is_max ? -INFINITY : 0.f;
+  int32_t count = 0;
+  for (int32_t a = 0; a < g.kT; ++a) {
+    const int64_t ti = t * g.sT + int64_t(a) * g.dT - g.pT;
+    if (ti < 0 || ti >= T_in) continue;
+    for (int32_t u = 0; u < g.kH; ++u) {
+      const int32_t hi = i * g.sH + u * g.dH - g.pH;
+      if (hi < 0 || hi >= g.H) continue;
+      for (int32_t v = 0; v < g.kW; ++v) {
+        const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+        if (wi < 0 || wi >= g.W) continue;
+        const float e = to_f32<T>(x[(bc * T_in + ti) * S + hi * g.W + wi]);
+        acc = is_max ? fmaxf(acc, e) : acc + e;
+        ++count;
+      }
+    }
+  }
+  float out;
+  if (is_max) {
+    out = acc;
+  } else {
+    const int32_t div = g.count_include_pad ? g.kT * g.kH * g.kW : count;
+    out = div > 0 ? acc / float(div) : 0.f;
+  }
+  y[idx] = from_f32<T>(out);
+}
+
+__global__ void pool_header_kernel(StateHeader h, StateHeader* dst) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *dst = h;
+}
+
+template <typename T>
+hipError_t pool_step_t(const PoolGeom& g, const PoolLayout& L, char* state, const StepIO& io,
+                       const co_pool_plan& plan, bool update, bool pad, hipStream_t s) {
+  PoolTaps taps;
+  for (int j = 0; j < CO_MAX_TAPS; ++j) taps.src[j] = plan.src[j];
+  float* fifo = reinterpret_cast<float*>(state + L.fifo);
+  float* valid = reinterpret_cast<float*>(state + L.valid);
+  hipLaunchKernelGGL(pool_step_kernel<T>, dim3(grid_for(g.out_frame_elems())), dim3(kBlock), 0,
+                     s, g, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
+                     fifo, L.fifo_slot_elems, valid, plan.write_slot, update ? 1 : 0, plan.emit,
+                     pad ? 1 : 0, taps);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pool_step(const PoolGeom& g, const PoolLayout& L, char* state,
+                            const StepIO& io, const co_pool_plan& plan, bool update_state,
+                            bool pad_frame, hipStream_t s) {
+  if (g.dtype == CO_BF16) return pool_step_t<bf16_t>(g, L, state, io, plan, update_state, pad_frame, s);
+  return pool_step_t<float>(g, L, state, io, plan, update_state, pad_frame, s);
+}
+
+hipError_t launch_pool_init(const PoolGeom& g, const PoolLayout& L, char* state,
+                            const StateHeader& hdr, hipStream_t s) {
+  hipLaunchKernelGGL(pool_header_kernel, dim3(1), dim3(64), 0, s, hdr,
+                     reinterpret_cast<StateHeader*>(state + L.header));
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const void* x, void* y,
+                            hipStream_t s) {
+  const int64_t total = int64_t(g.B) * g.C * T_out * g.So();
+  if (total == 0) return hipSuccess;
+  if (g.dtype == CO_BF16)
+    hipLaunchKernelGGL(pool_clip_kernel<bf16_t>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, T,
+                       T_out, static_cast<const bf16_t*>(x), static_cast<bf16_t*>(y));
+  else
+    hipLaunchKernelGGL(pool_clip_kernel<float>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, T,
+                       T_out, static_cast<const float*>(x), static_cast<float*>(y));
+  return hipGetLastError();
+}
+
+}  // namespace coinf

@@ -1,0 +1,109 @@
+// Host-side scheduler of the continual convolution / pooling steps.
+//
+// Pure C++ (no HIP): descriptor validation, receptive field and delay
+// (Principle 4), the per-step tap schedule (Principles 3-5) and the layout of
+// the caller-owned state buffer.  The device code consumes what this file
+// decides; nothing here touches the GPU.
+#pragma once
+
+#include <cstdint>
+
+#include "../../include/coinf.h"
+
+namespace coinf {
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t m) { return ceil_div(a, m) * m; }
+
+// floor((L + 2p - d(k-1) - 1)/s) + 1, or 0 when no window fits.
+inline int64_t axis_out_len(int64_t L, int64_t k, int64_t s, int64_t p, int64_t d) {
+  const int64_t span = L + 2 * p - d * (k - 1) - 1;
+  return span < 0 ? 0 : span / s + 1;
+}
+
+// Everything a convolution kernel needs to know about the layer, resolved
+// once from the descriptor.  Spatial axes are always two (unused ones are 1).
+struct ConvGeom {
+  int32_t spatial_dims;
+  int32_t B, Cin, Cout, G, Cg, Og;
+  int32_t H, W, Ho, Wo;
+  int32_t kT, kH, kW;
+  int32_t sT, sH, sW;
+  int32_t pT, pH, pW;
+  int32_t dT, dH, dW;
+  int32_t f, d, R;          // receptive field, delay, ring slots
+  int32_t has_bias, dtype, algo;
+  int64_t S() const { return int64_t(H) * W; }
+  int64_t So() const { return int64_t(Ho) * Wo; }
+  int64_t out_frame_elems() const { return int64_t(B) * Cout * So(); }
+};
+
+// Layout of a convolution state buffer (byte offsets).
+struct ConvLayout {
+  int64_t header, bias, weight, ring;
+  int64_t weight_bytes;
+  int64_t ring_slot_elems;  // floats between consecutive ring slots
+  int64_t total;
+};
+
+struct PoolGeom {
+  int32_t kind, spatial_dims;
+  int32_t B, C;
+  int32_t H, W, Ho, Wo;
+  int32_t kT, kH, kW;
+  int32_t sT, sH, sW;
+  int32_t pT, pH, pW;
+  int32_t dT, dH, dW;
+  int32_t f, d, R;          // receptive field, delay, FIFO slots
+  int32_t count_include_pad, dtype;
+  int64_t S() const { return int64_t(H) * W; }
+  int64_t So() const { return int64_t(Ho) * Wo; }
+  int64_t out_frame_elems() const { return int64_t(B) * C * So(); }
+};
+
+struct PoolLayout {
+  int64_t header, valid, fifo;
+  int64_t fifo_slot_elems;
+  int64_t total;
+};
+
+constexpr int64_t kHeaderBytes = 256;
+constexpr int64_t kAlign = 256;
+constexpr uint32_t kConvMagic = 0x564E4F43u;  // "CONV"
+constexpr uint32_t kPoolMagic = 0x4C4F4F50u;  // "POOL"
+constexpr uint32_t kStateVersion = 1;
+
+// State header, written at init and checked on attach.
+struct StateHeader {
+  uint32_t magic;
+  uint32_t version;
+  uint64_t desc_hash;
+  int64_t bytes;
+  int32_t algo;
+  int32_t slots;
+};
+
+// Validate a convolution descriptor, resolve the algorithm and fill g.
+co_status conv_geom(const co_conv_desc* desc, ConvGeom* g);
+ConvLayout conv_layout(const ConvGeom& g);
+// Hash of the validated descriptor and resolved algorithm (FNV-1a).
+uint64_t conv_hash(const ConvGeom& g);
+// Tap plan of step n (see co_conv_plan_step).
+void conv_plan(const ConvGeom& g, int64_t n, bool update_state, co_step_plan* plan);
+// Number of non-empty outputs of steps n .. n + count - 1.
+int64_t conv_emissions(const ConvGeom& g, int64_t n, int64_t count);
+
+co_status pool_geom(const co_pool_desc* desc, PoolGeom* g);
+PoolLayout pool_layout(const PoolGeom& g);
+uint64_t pool_hash(const PoolGeom& g);
+void pool_plan(const PoolGeom& g, int64_t n, co_pool_plan* plan);
+int64_t pool_emissions(const PoolGeom& g, int64_t n, int64_t count);
+
+// Whether the implicit-GEMM / depthwise kernels accept a geometry.
+bool gemm_supported(const ConvGeom& g);
+bool depthwise_supported(const ConvGeom& g);
+
+// Bytes of packed weights for an algorithm.
+int64_t packed_weight_bytes(const ConvGeom& g);
+
+}  // namespace coinf

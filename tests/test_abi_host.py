@@ -1,0 +1,249 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+* libcoinf.so loads and exports every function include/coinf.h declares;
+* descriptor validation returns the documented status codes;
+* the step schedule (co_conv_plan_step / co_pool_plan_step) is checked
+  symbolically on an exhaustive grid: replaying the plans on a model ring of
+  "which (frame, tap) products each slot holds" must deliver, for every
+  emitted output, exactly the set of real-frame taps that the ordinary
+  convolution of its window sums -- and the emission steps must match the
+  oracle's sliding-window driver.
+"""
+import ctypes
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2204_03418_amd import coinf as C
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "coinf.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(co_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 20
+    lib = ctypes.CDLL(C.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings():
+    for s in (C.CO_OK, C.CO_EMPTY, C.CO_EINVAL, C.CO_ENOTSUP, C.CO_ESTATE, C.CO_EHIP):
+        assert C.co_status_str(s).decode().startswith("CO_")
+
+
+def desc1d(k=3, s=1, p=0, d=1, cin=2, cout=3, groups=1, B=1, **kw):
+    return C.conv_desc(B, cin, cout, (k,), (), (s,), (p,), (d,), groups, True, C.CO_F32, **kw)
+
+
+def test_query_delay_and_receptive_field_example1():
+    # Example 1: co.Conv3d(4, 8, 3) has delay 2 and receptive field 3
+    d = C.conv_desc(2, 4, 8, (3, 3, 3), (6, 7))
+    info = C.conv_query(d)
+    assert (info.delay, info.receptive_field) == (2, 3)
+    assert tuple(info.out_size) == (4, 5)
+
+
+@pytest.mark.parametrize("k,p,dil,expect_d", [(3, 0, 1, 2), (3, 2, 1, 0), (3, 1, 1, 1),
+                                               (3, 0, 2, 4), (1, 0, 1, 0), (9, 0, 1, 8)])
+def test_query_principle4_delay(k, p, dil, expect_d):
+    info = C.conv_query(desc1d(k=k, p=p, d=dil))
+    assert info.delay == expect_d
+    assert info.receptive_field == dil * (k - 1) + 1
+
+
+def _status(desc):
+    info = C.ConvInfo()
+    return C.co_conv_query(ctypes.byref(desc), ctypes.byref(info))
+
+
+def test_invalid_descriptors():
+    assert _status(desc1d(p=3)) == C.CO_EINVAL              # negative delay
+    assert _status(desc1d(cin=3, groups=2)) == C.CO_EINVAL  # groups do not divide
+    assert _status(desc1d(cout=3, cin=2, groups=2)) == C.CO_EINVAL
+    assert _status(desc1d(k=0)) == C.CO_EINVAL
+    assert _status(desc1d(s=0)) == C.CO_EINVAL
+    assert _status(desc1d(d=0)) == C.CO_EINVAL
+    assert _status(desc1d(B=0)) == C.CO_EINVAL
+    assert _status(desc1d(k=65)) == C.CO_EINVAL             # more taps than CO_MAX_TAPS
+    d = desc1d()
+    d.dtype = 7
+    assert _status(d) == C.CO_EINVAL
+    d = desc1d()
+    d.in_size[1] = 2                                          # unused axis must be 1
+    assert _status(d) == C.CO_EINVAL
+    d = C.conv_desc(1, 2, 2, (3, 5), (4,))                    # spatial window does not fit
+    assert _status(d) == C.CO_EINVAL
+    d = desc1d()
+    d.algo = 9
+    assert _status(d) == C.CO_EINVAL
+
+
+def test_forced_algorithm_not_supported():
+    d = desc1d(cin=4, cout=4, groups=2, algo="depthwise")
+    assert _status(d) == C.CO_ENOTSUP
+
+
+def test_auto_algorithm_choice():
+    dw = C.conv_desc(2, 8, 8, (3, 3, 3), (7, 7), padding=(0, 1, 1), groups=8)
+    assert C.conv_query(dw).algo == C.CO_ALGO_DEPTHWISE
+    g = C.conv_desc(1, 2, 3, (3,), ())
+    assert C.conv_query(g).algo in (C.CO_ALGO_DIRECT, C.CO_ALGO_GEMM)
+
+
+def test_null_and_small_buffers_rejected_without_device():
+    d = desc1d()
+    info = C.conv_query(d)
+    h = ctypes.c_void_p()
+    fake = ctypes.c_void_p(0x1000)
+    assert C.co_conv_init_state(ctypes.byref(d), fake, fake, None, info.state_bytes, None,
+                                ctypes.byref(h)) == C.CO_EINVAL
+    assert C.co_conv_init_state(ctypes.byref(d), None, fake, fake, info.state_bytes, None,
+                                ctypes.byref(h)) == C.CO_EINVAL
+    assert C.co_conv_init_state(ctypes.byref(d), fake, None, fake, info.state_bytes, None,
+                                ctypes.byref(h)) == C.CO_EINVAL      # has_bias without bias
+    assert C.co_conv_init_state(ctypes.byref(d), fake, fake, fake, info.state_bytes - 1, None,
+                                ctypes.byref(h)) == C.CO_ESTATE
+    assert C.co_conv_attach_state(ctypes.byref(d), fake, info.state_bytes - 4, 0, None,
+                                  ctypes.byref(h)) == C.CO_ESTATE
+    assert C.co_conv_attach_state(ctypes.byref(d), fake, info.state_bytes, -1, None,
+                                  ctypes.byref(h)) == C.CO_EINVAL
+    assert C.co_conv_forward_step(None, fake, fake, 1, None) == C.CO_EINVAL
+    n = C.i32()
+    assert C.co_conv_forward_steps(None, fake, 4, fake, 4, 0, 1, None, ctypes.byref(n)) == C.CO_EINVAL
+    assert C.co_conv_destroy(None) == C.CO_EINVAL
+    assert C.co_conv_forward(ctypes.byref(d), None, fake, fake, 5, fake, None) == C.CO_EINVAL
+    # a clip too short for one window writes nothing and succeeds without the device
+    assert C.co_conv_forward(ctypes.byref(d), fake, fake, fake, 2, fake, None) == C.CO_OK
+    t = C.i32()
+    assert C.co_conv_clip_frames(ctypes.byref(d), 7, ctypes.byref(t)) == C.CO_OK and t.value == 5
+
+
+def _real_taps(tau, k, s, p, dil):
+    """(real frame, tap) pairs that the ordinary convolution of output tau sums."""
+    out = set()
+    for j in range(k):
+        r = tau * s + j * dil - p
+        if r >= 0:
+            out.add((r, j))
+    return out
+
+
+PLAN_GRID = [(k, s, dil, p) for k in (1, 2, 3, 4, 5) for s in (1, 2, 3) for dil in (1, 2, 3)
+             for p in range(0, dil * (k - 1) + 1)]
+
+
+@pytest.mark.parametrize("k,s,dil,p", PLAN_GRID)
+def test_conv_plan_delivers_exact_window(k, s, dil, p):
+    d = desc1d(k=k, s=s, p=p, d=dil)
+    info = C.conv_query(d)
+    R = info.ring_slots
+    f = dil * (k - 1) + 1
+    assert R == -(-(f - 1) // s) + 1
+    ring = [None] * R           # slot -> (tau, set of (frame, tap)) or None
+    steps = 40
+    co = oracle.ContinualConv(np.ones((1, 1, k)), None, stride=s, padding=p, dilation=dil)
+    for n in range(steps):
+        plan = C.conv_plan(d, n, True)
+        ref = co.forward_step(np.ones((1, 1)))
+        assert bool(plan.emit) == (ref is not None), n
+        emitted = None
+        for j in range(k):
+            a, slot, tau = plan.action[j], plan.slot[j], plan.target[j]
+            if a == C.CO_TAP_NONE:
+                assert slot == -1 and tau == -1
+                continue
+            assert tau * s + j * dil == n + p       # the frame really feeds tap j of tau
+            if a == C.CO_TAP_START:
+                assert ring[slot] is None, (n, j, "slot still live")
+                ring[slot] = (tau, {(n, j)})
+            elif a == C.CO_TAP_ACC:
+                assert ring[slot] is not None and ring[slot][0] == tau
+                ring[slot][1].add((n, j))
+            elif a == C.CO_TAP_EMIT:
+                assert j == k - 1 and ring[slot] is not None and ring[slot][0] == tau
+                emitted = (tau, ring[slot][1] | {(n, j)})
+                ring[slot] = None
+            elif a == C.CO_TAP_EMIT_FRESH:
+                assert j == k - 1 and slot == -1
+                emitted = (tau, {(n, j)})
+        if plan.emit:
+            assert emitted is not None and emitted[0] == plan.out_index
+            assert emitted[1] == _real_taps(plan.out_index, k, s, p, dil)
+        else:
+            assert emitted is None and plan.out_index == -1
+
+
+@pytest.mark.parametrize("k,s,dil,p", PLAN_GRID[::3])
+def test_conv_plan_update_state_false_keeps_only_completing_tap(k, s, dil, p):
+    d = desc1d(k=k, s=s, p=p, d=dil)
+    for n in range(20):
+        a = C.conv_plan(d, n, True)
+        b = C.conv_plan(d, n, False)
+        assert a.emit == b.emit and a.out_index == b.out_index
+        for j in range(k):
+            if j == k - 1:
+                assert a.action[j] == b.action[j] and a.slot[j] == b.slot[j]
+            else:
+                assert b.action[j] == C.CO_TAP_NONE
+
+
+POOL_PLAN_GRID = [(k, s, dil, p) for k in (1, 2, 3, 4, 7) for s in (1, 2, 3) for dil in (1, 2)
+                  for p in range(0, k // 2 + 1)]
+
+
+@pytest.mark.parametrize("k,s,dil,p", POOL_PLAN_GRID)
+def test_pool_plan_reads_the_window(k, s, dil, p):
+    d = C.pool_desc("max", 1, 1, (k,), (), (s,), (p,), (dil,))
+    info = C.pool_query(d)
+    f = dil * (k - 1) + 1
+    assert info.fifo_slots == f and info.delay == f - p - 1
+    fifo = {}
+    for n in range(40):
+        plan = C.pool_plan(d, n)
+        if plan.emit:
+            tau = plan.out_index
+            assert tau * s + f - 1 - p == n
+            for j in range(k):
+                r = tau * s + j * dil - p
+                src = plan.src[j]
+                if r < 0:
+                    assert src == -1
+                elif r == n:
+                    assert src == -2
+                else:
+                    assert fifo.get(src) == r, (n, j)
+        fifo[plan.write_slot] = n
+
+
+def test_pool_validation():
+    info = C.PoolInfo()
+    bad = C.pool_desc("avg", 1, 1, (3, 3, 3), (5, 5), (1, 1, 1), (0, 2, 0))  # pad > k/2
+    assert C.co_pool_query(ctypes.byref(bad), ctypes.byref(info)) == C.CO_EINVAL
+    bad = C.pool_desc("avg", 1, 1, (3,), (), (1,), (0,), (2,))               # avg dilation
+    assert C.co_pool_query(ctypes.byref(bad), ctypes.byref(info)) == C.CO_ENOTSUP
+    ok = C.pool_desc("avg", 16, 432, (4, 7, 7), (7, 7), (1, 7, 7))
+    assert C.co_pool_query(ctypes.byref(ok), ctypes.byref(info)) == C.CO_OK
+    assert info.delay == 3 and tuple(info.out_size) == (1, 1)
+
+
+def test_emission_count_matches_oracle_formula():
+    for k, s, p in itertools.product((1, 3, 4), (1, 2, 3), (0, 1, 2)):
+        if p > k - 1:
+            continue
+        d = desc1d(k=k, s=s, p=p)
+        # forward_steps over T frames emits floor((T + p - f)/s) + 1 outputs
+        for T in range(0, 12):
+            emitted = sum(C.conv_plan(d, n).emit for n in range(T))
+            expect = (T + p - k) // s + 1 if T + p >= k else 0
+            assert emitted == expect

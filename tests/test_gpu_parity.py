@@ -1,0 +1,295 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle.
+
+Every case draws seeded inputs once on the host, feeds the identical values
+to the oracle (float64) and to the GPU, and compares element by element with
+the normwise bound of parity_util.TOL.  Sizes span several thread blocks and
+leave ragged tails; edge cases cover kT = 1, delay 0, all-empty streams,
+strides, dilations, groups, end padding and both dtypes.
+"""
+import itertools
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2204_03418_amd import synth
+from parity_util import TOL, assert_close, np64, oracle_conv, relerr, say
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2204_03418_amd import coinf
+DEV = "cuda"
+
+
+def _fuzz_cases():
+    rng = np.random.default_rng(2204)
+    out = []
+    for idx in range(36):
+        sd = idx % 3
+        nd = sd + 1
+        k = tuple(int(v) for v in rng.integers(1, 4, nd))
+        s = (int(rng.integers(1, 3)),) + tuple(int(v) for v in rng.integers(1, 3, sd))
+        dil = tuple(int(v) for v in rng.integers(1, 3, nd))
+        p = tuple(int(rng.integers(0, dil[i] * (k[i] - 1) + 1)) for i in range(nd))
+        G = int(rng.choice([1, 1, 2, 3]))
+        cin = G * int(rng.integers(1, 4))
+        cout = G * int(rng.integers(1, 6))
+        size = tuple(max(int(v), dil[i + 1] * (k[i + 1] - 1) + 1)
+                     for i, v in enumerate(rng.integers(3, 12, sd)))
+        B = int(rng.integers(1, 4))
+        T = int(rng.integers(1, 13))
+        dt = "bf16" if idx % 4 == 3 else "f32"
+        out.append((idx, B, cin, cout, G, k, s, p, dil, size, T, dt))
+    return out
+
+
+@pytest.mark.parametrize("case", _fuzz_cases(), ids=lambda c: f"fuzz{c[0]}")
+def test_fuzz_conv_steps_and_clip(case):
+    idx, B, cin, cout, G, k, s, p, dil, size, T, dt = case
+    say("fuzz", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          stride=s, padding=p, dilation=dil, groups=G, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, T, 50000 + 10 * idx, "normal")
+    tdt = synth.torch_dtype(dt)
+    for algo in ("direct", "auto"):
+        co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=s, padding=p,
+                          dilation=dil, groups=G, algo=algo)
+        ref = oracle_conv(w, b, s, p, dil, G)
+        ys = co.forward_steps(x.to(DEV), pad_end=True)
+        r = ref.forward_steps(np64(x), pad_end=True)
+        if r is None:
+            assert ys is None
+        else:
+            assert_close(np64(ys), r, tdt, f"steps {algo}")
+        clip = co.forward(x.to(DEV))
+        rc = oracle.conv_forward(np64(x), np64(w), np64(b), s, p, dil, G)
+        assert tuple(clip.shape) == rc.shape
+        if rc.size:
+            assert_close(np64(clip), rc, tdt, f"clip {algo}")
+
+
+def _run_steps(co, x):
+    """forward_step per frame (the benchmark's launch configuration)."""
+    outs = []
+    for t in range(x.shape[2]):
+        y = co.forward_step(x[:, :, t].contiguous())
+        if y is not None:
+            outs.append(y.clone())
+    return outs
+
+
+@pytest.mark.parametrize("name", ["conv1d_b1_c4to8_k3_f32", "conv3d_b1_c24_k3_56x56_f32"])
+def test_workload_full_clip(name):
+    """Whole clip, every output element, forward_step per frame."""
+    wl = synth.WORKLOADS[name]
+    c = wl.conv
+    say("workload", name)
+    x, w, b = synth.workload_inputs(name)
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size, stride=c.stride,
+                      padding=c.padding, dilation=c.dilation, groups=c.groups)
+    outs = _run_steps(co, x.to(DEV))
+    torch.cuda.synchronize()
+    ref = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x))
+    got = np.stack([np64(o) for o in outs], axis=2)
+    assert_close(got, ref, synth.torch_dtype(c.dtype), name)
+
+
+@pytest.mark.parametrize("name,streams,frames", [
+    ("conv3d_b64_c192_k3_14x14_bf16", (0, 37, 63), 8),
+    ("conv2d_b32_c64to256_k9x1_v25_f32", (0, 31), 300),
+    ("conv2d_b32_c64to256_k9x1_v25_bf16", (5, 17), 300),
+])
+def test_workload_sampled_streams(name, streams, frames):
+    """Full-size run on the GPU; the oracle recomputes sampled streams (the B
+    streams are independent, one shared clock) over the first `frames` frames."""
+    wl = synth.WORKLOADS[name]
+    c = wl.conv
+    say("workload", name, "streams", streams, "frames", frames)
+    x, w, b = synth.workload_inputs(name)
+    x = x[:, :, :frames].contiguous()
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size, stride=c.stride,
+                      padding=c.padding, dilation=c.dilation, groups=c.groups)
+    outs = _run_steps(co, x.to(DEV))
+    torch.cuda.synchronize()
+    sel = list(streams)
+    got = np.stack([np64(o[sel]) for o in outs], axis=2)
+    ref = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x[sel]))
+    assert_close(got, ref, synth.torch_dtype(c.dtype), name)
+
+
+def test_workload_depthwise_then_pool():
+    name = "dwconv3d_b16_c432_k3_7x7_avgpool_bf16"
+    wl = synth.WORKLOADS[name]
+    c, pl = wl.conv, wl.pool
+    say("workload", name)
+    x, w, b = synth.workload_inputs(name)
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size, padding=c.padding,
+                      groups=c.groups)
+    assert co.algo == "depthwise"
+    po = coinf.CoPool("avg", batch=pl.batch, channels=pl.channels, kernel=pl.kernel,
+                      in_size=pl.in_size, stride=pl.stride, dtype=torch.bfloat16)
+    assert co.delay + po.delay == 5
+    xd = x.to(DEV)
+    conv_outs, pool_outs = [], []
+    for t in range(x.shape[2]):
+        y = co.forward_step(xd[:, :, t].contiguous())
+        if y is None:
+            continue
+        conv_outs.append(y.clone())
+        z = po.forward_step(y)
+        if z is not None:
+            pool_outs.append(z.clone())
+    torch.cuda.synchronize()
+    ref_c = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x))
+    got_c = np.stack([np64(o) for o in conv_outs], axis=2)
+    assert_close(got_c, ref_c, torch.bfloat16, "depthwise conv")
+    # the pool oracle chains on the oracle's own (float64) conv outputs; the
+    # GPU pool sees the bf16-rounded conv outputs, within the bf16 bound
+    rp = oracle.ContinualPool("avg", pl.kernel, pl.stride).forward_steps(ref_c)
+    got_p = np.stack([np64(o) for o in pool_outs], axis=2)
+    assert got_p.shape == rp.shape
+    assert_close(got_p, rp, torch.bfloat16, "avg pool")
+    # the chain's output count: T - 5 frames after a delay of 5
+    assert got_p.shape[2] == x.shape[2] - 5
+
+
+def _pool_cases():
+    out = []
+    for i, (kind, k, s, p, d, cip, sd) in enumerate(itertools.product(
+            ("avg", "max"), (1, 3, 4), (1, 2), (0, 1), (1, 2), (True, False), (0, 1, 2))):
+        if kind == "avg" and d == 2:
+            continue
+        if kind == "max" and not cip:
+            continue
+        if p > k // 2:
+            continue
+        out.append((i, kind, k, s, p, d, cip, sd))
+    return out
+
+
+@pytest.mark.parametrize("case", _pool_cases(), ids=lambda c: f"pool{c[0]}")
+def test_pool_fuzz(case):
+    i, kind, k, s, p, d, cip, sd = case
+    say("pool", case)
+    size = {0: (), 1: (9,), 2: (7, 6)}[sd]
+    ks = (k,) + ((3, 2) if sd == 2 else (3,) if sd == 1 else ())
+    ss = (s,) + ((2, 1) if sd == 2 else (2,) if sd == 1 else ())
+    ps = (p,) + ((1, 0) if sd == 2 else (1,) if sd == 1 else ())
+    ds = (d,) + ((1, 2) if (sd == 2 and kind == "max") else (1,) * sd)
+    dt = torch.bfloat16 if i % 3 == 0 else torch.float32
+    x = synth.normal((3, 5, 11) + size, 7000 + i, dtype="bf16" if dt == torch.bfloat16 else "f32")
+    po = coinf.CoPool(kind, batch=3, channels=5, kernel=ks, in_size=size, stride=ss, padding=ps,
+                      dilation=ds, count_include_pad=cip, dtype=dt)
+    ys = po.forward_steps(x.to(DEV), pad_end=True)
+    r = oracle.ContinualPool(kind, ks, ss, ps, ds, cip, spatial_dims=sd).forward_steps(
+        np64(x), pad_end=True)
+    assert_close(np64(ys), r, dt, "pool steps")
+    clip = po.forward(x.to(DEV))
+    rc = oracle.pool_forward(kind, np64(x), ks, ss, ps, ds, cip)
+    assert_close(np64(clip), rc, dt, "pool clip")
+
+
+def _small_conv(algo="auto", dtype="f32", **kw):
+    spec = synth.ConvSpec(batch=2, in_channels=6, out_channels=10, kernel=(3, 3, 3),
+                          in_size=(9, 11), padding=kw.get("padding", (1, 1, 1)), dtype=dtype)
+    x, w, b = synth.conv_inputs(spec, 12, 90000, "normal")
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=2, in_size=(9, 11), padding=spec.padding,
+                      algo=algo)
+    return co, x.to(DEV), w, b, spec
+
+
+def test_update_state_false_leaves_state_bitwise():
+    say("update_state=False")
+    co, x, *_ = _small_conv()
+    for t in range(5):
+        co.forward_step(x[:, :, t].contiguous())
+    torch.cuda.synchronize()
+    before = co.state.clone()
+    n = co.steps
+    peek = co.forward_step(x[:, :, 5].contiguous(), update_state=False)
+    torch.cuda.synchronize()
+    assert co.steps == n
+    assert torch.equal(co.state, before)
+    real = co.forward_step(x[:, :, 5].contiguous())
+    assert torch.equal(peek, real)
+    # forward_steps with update_state=False: same outputs, state restored
+    torch.cuda.synchronize()
+    before = co.state.clone()
+    n = co.steps
+    a = co.forward_steps(x[:, :, 6:].contiguous(), update_state=False)
+    torch.cuda.synchronize()
+    assert co.steps == n and torch.equal(co.state, before)
+    bb = co.forward_steps(x[:, :, 6:].contiguous())
+    assert torch.equal(a, bb)
+
+
+def test_clean_state_replay_and_determinism():
+    say("clean_state replay")
+    co, x, *_ = _small_conv()
+    y1 = co.forward_steps(x).clone()
+    co.clean_state()
+    assert co.steps == 0
+    y2 = co.forward_steps(x).clone()
+    assert torch.equal(y1, y2)
+
+
+def test_snapshot_attach_resume_bitwise():
+    say("snapshot/attach")
+    co, x, w, b, spec = _small_conv()
+    T = x.shape[2]
+    co.forward_steps(x[:, :, :5].contiguous())
+    snap = co.state.clone()
+    n = co.steps
+    rest = co.forward_steps(x[:, :, 5:].contiguous()).clone()
+    del co
+    co2 = coinf.CoConv(w.to(DEV), b.to(DEV), batch=2, in_size=(9, 11), padding=spec.padding,
+                       state=snap, attach_steps=n)
+    assert co2.steps == n
+    rest2 = co2.forward_steps(x[:, :, 5:T].contiguous())
+    assert torch.equal(rest, rest2)
+
+
+def test_attach_rejects_foreign_state():
+    say("attach mismatch")
+    co, x, w, b, spec = _small_conv()
+    torch.cuda.synchronize()
+    with pytest.raises(coinf.CoinfError) as e:
+        coinf.CoConv(w.to(DEV), b.to(DEV), batch=2, in_size=(9, 11), padding=(0, 1, 1),
+                     state=co.state, attach_steps=0)
+    assert e.value.status == coinf.CO_ESTATE
+
+
+@pytest.mark.parametrize("k,p,s,dil", [(1, 0, 1, 1), (3, 2, 1, 1), (4, 0, 3, 2), (2, 1, 2, 3),
+                                       (5, 3, 1, 2)])
+def test_temporal_edge_cases(k, p, s, dil):
+    """kT = 1 (no ring), delay 0, stride > kT with dilation, end padding."""
+    say("edge", k, p, s, dil)
+    spec = synth.ConvSpec(batch=3, in_channels=5, out_channels=7, kernel=(k, 3), in_size=(13,),
+                          stride=(s, 1), padding=(p, 1), dilation=(dil, 1))
+    x, w, b = synth.conv_inputs(spec, 17, 31000 + k * 100 + p * 10 + s, "normal")
+    ref = oracle_conv(w, b, spec.stride, spec.padding, spec.dilation, 1)
+    for algo in ("direct", "auto"):
+        co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=3, in_size=(13,), stride=spec.stride,
+                          padding=spec.padding, dilation=spec.dilation, algo=algo)
+        ref.clean_state()
+        r = ref.forward_steps(np64(x), pad_end=True)
+        ys = co.forward_steps(x.to(DEV), pad_end=True)
+        assert_close(np64(ys), r, torch.float32, f"edge {algo}")
+
+
+def test_all_empty_and_zero_length():
+    say("all empty")
+    spec = synth.ConvSpec(batch=1, in_channels=2, out_channels=3, kernel=(5,), dtype="f32")
+    x, w, b = synth.conv_inputs(spec, 3, 123, "normal")
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=1)
+    assert co.forward_steps(x.to(DEV)) is None          # 3 frames < delay 4
+    assert co.steps == 3
+    assert co.forward_steps(x[:, :, :0].contiguous().to(DEV)) is None
+    assert co.steps == 3
+    y = co.forward_step(x[:, :, 0].contiguous().to(DEV))
+    assert y is None                                     # step 3 < delay 4
+    y = co.forward_step(x[:, :, 1].contiguous().to(DEV))  # step 4 emits
+    assert y is not None
