@@ -7,7 +7,7 @@
 // temporal tap j is computed at once and stored as a partial sum of the output
 // frame that tap feeds; the output whose last tap this frame is completes and
 // is emitted.  Partial sums live in a float32 ring of R output frames inside
-// the caller's state buffer, laid out (slot, B, C_out, Ho, Wo).
+// the caller's state buffer, laid out (slot, C_out, B, Ho, Wo).
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -34,6 +34,9 @@ __global__ __launch_bounds__(kBlock) void conv_step_direct_kernel(
   const int32_t grp = o / g.Og;
   const T* xb = x + (int64_t(b) * g.Cin + int64_t(grp) * g.Cg) * x_bc;
   const int32_t kHW = g.kH * g.kW;
+  // ring layout (slot, C_out, B, Ho, Wo): channel-major so that consecutive
+  // output pixels of all streams are contiguous for every kernel family
+  const int32_t ridx = (o * g.B + b) * So + p;
   for (int32_t j = 0; j < g.kT; ++j) {
     const int act = tt.action[j];
     if (act == CO_TAP_NONE) continue;
@@ -53,7 +56,7 @@ __global__ __launch_bounds__(kBlock) void conv_step_direct_kernel(
         }
       }
     }
-    float* r = ring + int64_t(tt.slot[j] < 0 ? 0 : tt.slot[j]) * ring_slot + idx;
+    float* r = ring + int64_t(tt.slot[j] < 0 ? 0 : tt.slot[j]) * ring_slot + ridx;
     const int64_t yi = int64_t(bo) * y_bc + p;
     switch (act) {
       case CO_TAP_START: *r = acc; break;

@@ -5,8 +5,8 @@
 // matrix cores.  One thread owns one output element (b, c, i, j): it loads the
 // stencil's input neighbourhood once into registers, evaluates every active
 // tap from it, and updates that element's partial sums in the float32 ring
-// (slot, B, C, Ho, Wo).  Consecutive threads own consecutive output pixels, so
-// ring and output traffic is fully coalesced; the step is bound by HBM.
+// (slot, C, B, Ho, Wo).  Consecutive threads own consecutive output pixels, so
+// ring and output traffic is coalesced; the step is bound by HBM.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -41,6 +41,7 @@ __global__ __launch_bounds__(kBlock) void conv_step_dw_kernel(
   }
   const float* wc = w + int64_t(c) * g.kT * (KH * KW);
   const int64_t yi = int64_t(bc) * y_bc + p;
+  const int32_t ridx = (c * g.B + bc / g.Cout) * So + p;  // ring (slot, C, B, Ho, Wo)
   for (int32_t j = 0; j < g.kT; ++j) {
     const int act = tt.action[j];
     if (act == CO_TAP_NONE) continue;
@@ -48,7 +49,7 @@ __global__ __launch_bounds__(kBlock) void conv_step_dw_kernel(
     float acc = 0.f;
 #pragma unroll
     for (int e = 0; e < KH * KW; ++e) acc = fmaf(wj[e], xv[e], acc);
-    float* r = ring + int64_t(tt.slot[j] < 0 ? 0 : tt.slot[j]) * ring_slot + idx;
+    float* r = ring + int64_t(tt.slot[j] < 0 ? 0 : tt.slot[j]) * ring_slot + ridx;
     switch (act) {
       case CO_TAP_START: *r = acc; break;
       case CO_TAP_ACC: *r = *r + acc; break;

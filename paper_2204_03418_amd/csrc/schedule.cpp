@@ -1,6 +1,8 @@
 // Host-side scheduler: validation, delay, tap plans and state layouts.
 #include "schedule.hpp"
 
+#include <algorithm>
+#include <cmath>
 #include <cstring>
 
 namespace coinf {
@@ -37,23 +39,106 @@ bool depthwise_supported(const ConvGeom& g) {
   return g.G == g.Cin && g.G == g.Cout && shape && g.kT <= CO_MAX_TAPS;
 }
 
-bool gemm_supported(const ConvGeom& g) {
-  (void)g;
-  return false;
+namespace {
+
+struct GemmShape {
+  int32_t dtype, WM, WN, NWM, NWN, KL;
+};
+
+// Instantiated tile shapes (the kernel file instantiates the same table).
+constexpr GemmShape kGemmShapes[kGemmConfigs] = {
+    {CO_BF16, 7, 4, 4, 1, 8},  // 448 x 64: large M and N, many channels
+    {CO_BF16, 2, 2, 1, 4, 8},  // 32 x 128: small K, wide N
+    {CO_F32, 2, 2, 1, 4, 4},   // 32 x 128
+    {CO_F32, 1, 1, 4, 1, 4},   // 64 x 16: small N, fills the chip with waves
+};
+
+// Input rows a tile of output pixels [m0, m1) needs, over all of its images.
+int64_t tile_slots(const ConvGeom& g, int64_t m0, int64_t m1) {
+  const int64_t So = g.So();
+  const int64_t r0 = m0 / g.Wo, r1 = (m1 - 1) / g.Wo;  // flattened output rows
+  const int64_t b0 = r0 / g.Ho, i0 = r0 % g.Ho;
+  const int64_t b1 = r1 / g.Ho, i1 = r1 % g.Ho;
+  (void)So;
+  int64_t q0 = b0 * g.H + std::max<int64_t>(0, i0 - g.pH);
+  int64_t q1 = b1 * g.H + std::min<int64_t>(g.H - 1, i1 + g.kH - 1 - g.pH);
+  return q1 >= q0 ? q1 - q0 + 1 : 1;
 }
+
+}  // namespace
+
+bool gemm_geometry_ok(const ConvGeom& g) {
+  const bool taps = (g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1);
+  return g.G == 1 && taps && g.sH == 1 && g.sW == 1 && g.dH == 1 && g.dW == 1 &&
+         g.W + 2 * g.pW <= 256;
+}
+
+bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
+  if (id < 0 || id >= kGemmConfigs || !gemm_geometry_ok(g)) return false;
+  const GemmShape& s = kGemmShapes[id];
+  if (s.dtype != g.dtype) return false;
+  GemmConfig r{};
+  r.id = id;
+  r.dtype = s.dtype;
+  r.WM = s.WM;
+  r.WN = s.WN;
+  r.NWM = s.NWM;
+  r.NWN = s.NWN;
+  r.KL = s.KL;
+  r.CK = 4 * s.KL;
+  r.M_WG = 16 * s.WM * s.NWM;
+  r.N_WG = 16 * s.WN * s.NWN;
+  const int64_t M = int64_t(g.B) * g.So();
+  const int64_t N = int64_t(g.kT) * g.Cout;
+  r.m_tiles = int32_t(ceil_div(M, r.M_WG));
+  r.n_tiles = int32_t(ceil_div(N, r.N_WG));
+  r.n_chunks = int32_t(ceil_div(g.Cin, r.CK));
+  r.cols = g.W + 2 * g.pW;
+  int64_t slots = 1;
+  for (int64_t t = 0; t < r.m_tiles; ++t)
+    slots = std::max(slots, tile_slots(g, t * r.M_WG, std::min<int64_t>(M, (t + 1) * r.M_WG)));
+  r.max_slots = int32_t(slots);
+  // A: (slots + zero row) x cols pixels x 64 B; B: kH*kW x N_WG x 64 B
+  r.lds_bytes = (slots + 1) * r.cols * 64 + int64_t(g.kH) * g.kW * r.N_WG * 64;
+  if (r.lds_bytes > kLdsBytes) return false;
+  *c = r;
+  return true;
+}
+
+int gemm_pick(const ConvGeom& g) {
+  int best = -1;
+  double best_cost = 0;
+  for (int id = 0; id < kGemmConfigs; ++id) {
+    GemmConfig c;
+    if (!gemm_config(g, id, &c)) continue;
+    // cycles of one wave: MFMA issue (bf16 16x16x32: 16 clk per fragment pair
+    // per 32 channels; f32 16x16x4: 4 x 32 clk per 16 channels), plus staging
+    // per chunk and the epilogue; waves beyond one per SIMD run in rounds
+    const double mfma = c.dtype == CO_BF16 ? 16.0 : 128.0;
+    const double wave = double(c.WM) * c.WN * c.n_chunks * g.kH * g.kW * mfma +
+                        300.0 * c.n_chunks + 100.0 * c.WM * c.WN;
+    const double waves = double(c.m_tiles) * c.n_tiles * c.NWM * c.NWN;
+    const double cost = std::ceil(waves / 1024.0) * wave;
+    if (best < 0 || cost < best_cost) {
+      best = id;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+bool gemm_supported(const ConvGeom& g) { return gemm_pick(g) >= 0; }
 
 int64_t packed_weight_bytes(const ConvGeom& g) {
   const int64_t n = int64_t(g.Cout) * g.Cg * g.kT * g.kH * g.kW;
-  switch (g.algo) {
-    case CO_ALGO_GEMM: {
-      // [kT][C_out][K_pad] in the io dtype, K padded to the MFMA K step
-      const int64_t K = int64_t(g.Cg) * g.kH * g.kW;
-      const int64_t kstep = g.dtype == CO_BF16 ? 32 : 8;
-      return int64_t(g.kT) * g.Cout * round_up(K, kstep) * (g.dtype == CO_BF16 ? 2 : 4);
-    }
-    default:
-      return n * 4;  // float32, PyTorch order
+  if (g.algo == CO_ALGO_GEMM) {
+    // [n_tile][chunk][kH*kW][N_WG][CK] in the io dtype, zero padded
+    GemmConfig c;
+    if (!gemm_config(g, g.cfg, &c)) return 0;
+    return int64_t(c.n_tiles) * c.n_chunks * g.kH * g.kW * c.N_WG * c.CK *
+           (g.dtype == CO_BF16 ? 2 : 4);
   }
+  return n * 4;  // float32, PyTorch order
 }
 
 co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
@@ -119,17 +204,22 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
   r.has_bias = d.has_bias;
   r.dtype = d.dtype;
 
+  r.cfg = -1;
   int32_t algo = d.algo;
+  // multiply-accumulates of one step: tiny layers stay on the direct kernel,
+  // whose single pass costs less than staging tiles through LDS
+  const double macs = double(r.B) * r.So() * r.Cout * r.kT * r.Cg * r.kH * r.kW;
   if (algo == CO_ALGO_AUTO) {
     if (depthwise_supported(r))
       algo = CO_ALGO_DEPTHWISE;
     else
-      algo = gemm_supported(r) ? CO_ALGO_GEMM : CO_ALGO_DIRECT;
+      algo = (macs >= 1.0e5 && gemm_supported(r)) ? CO_ALGO_GEMM : CO_ALGO_DIRECT;
   } else if (algo == CO_ALGO_DEPTHWISE) {
     if (!depthwise_supported(r)) return CO_ENOTSUP;
   } else if (algo == CO_ALGO_GEMM) {
     if (!gemm_supported(r)) return CO_ENOTSUP;
   }
+  if (algo == CO_ALGO_GEMM) r.cfg = gemm_pick(r);
   r.algo = algo;
   *g = r;
   return CO_OK;

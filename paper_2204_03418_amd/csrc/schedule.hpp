@@ -33,10 +33,32 @@ struct ConvGeom {
   int32_t dT, dH, dW;
   int32_t f, d, R;          // receptive field, delay, ring slots
   int32_t has_bias, dtype, algo;
+  int32_t cfg;              // implicit-GEMM tile configuration (-1: none)
   int64_t S() const { return int64_t(H) * W; }
   int64_t So() const { return int64_t(Ho) * Wo; }
   int64_t out_frame_elems() const { return int64_t(B) * Cout * So(); }
 };
+
+// Tile configuration of the implicit-GEMM step kernel.  The GEMM is
+// C[M = B*Ho*Wo output pixels][N = kT*C_out (tap, channel)] over
+// K = kH*kW*C_in (spatial tap, channel; channels innermost).  Each wave owns
+// WM x WN fragments of 16x16; a workgroup has NWM x NWN waves.
+struct GemmConfig {
+  int32_t id;          // kernel instantiation
+  int32_t dtype;       // CO_F32 | CO_BF16
+  int32_t WM, WN;      // fragments per wave along M and N
+  int32_t NWM, NWN;    // waves per workgroup along M and N
+  int32_t KL;          // elements per lane per 16-byte operand read
+  int32_t CK;          // input channels per LDS chunk (= 4 * KL)
+  int32_t M_WG, N_WG;  // workgroup tile
+  int32_t m_tiles, n_tiles, n_chunks;
+  int32_t cols;        // staged pixels per input row (W + 2 pW)
+  int32_t max_slots;   // staged input rows per tile (one zero row follows)
+  int64_t lds_bytes;
+};
+
+constexpr int kGemmConfigs = 4;
+constexpr int64_t kLdsBytes = 160 * 1024;
 
 // Layout of a convolution state buffer (byte offsets).
 struct ConvLayout {
@@ -99,8 +121,15 @@ uint64_t pool_hash(const PoolGeom& g);
 void pool_plan(const PoolGeom& g, int64_t n, co_pool_plan* plan);
 int64_t pool_emissions(const PoolGeom& g, int64_t n, int64_t count);
 
+// Fill the derived sizes of tile configuration `id` for a geometry; false
+// when it does not apply (dtype, LDS) .
+bool gemm_config(const ConvGeom& g, int id, GemmConfig* c);
+// The configuration the library picks for a geometry (-1: none fits).
+int gemm_pick(const ConvGeom& g);
+
 // Whether the implicit-GEMM / depthwise kernels accept a geometry.
 bool gemm_supported(const ConvGeom& g);
+bool gemm_geometry_ok(const ConvGeom& g);
 bool depthwise_supported(const ConvGeom& g);
 
 // Bytes of packed weights for an algorithm.

@@ -293,3 +293,57 @@ def test_all_empty_and_zero_length():
     assert y is None                                     # step 3 < delay 4
     y = co.forward_step(x[:, :, 1].contiguous().to(DEV))  # step 4 emits
     assert y is not None
+
+
+GEMM_CASES = [
+    # B, Cin, Cout, kT, (kH, kW), in_size, (pH, pW), sT, pT, dT, dtype
+    (3, 40, 24, 3, (3, 3), (9, 11), (1, 1), 1, 0, 1, "bf16"),    # 2 channel chunks, ragged
+    (2, 20, 36, 2, (3, 3), (7, 6), (0, 1), 1, 1, 1, "f32"),      # valid rows, ragged N
+    (5, 64, 48, 4, (1,), (25,), (0,), 1, 0, 1, "f32"),           # (kT, 1) over joints
+    (5, 64, 48, 4, (1,), (25,), (0,), 1, 2, 1, "bf16"),
+    (20, 8, 16, 3, (3, 3), (4, 4), (1, 1), 1, 0, 1, "bf16"),     # many streams per tile
+    (2, 33, 40, 3, (3, 3), (10, 9), (1, 1), 2, 1, 2, "f32"),     # temporal stride + dilation
+    (1, 24, 24, 3, (3, 3), (56, 56), (1, 1), 1, 0, 1, "f32"),    # the 56x56 stem block
+    (4, 96, 80, 5, (3, 3), (14, 14), (1, 1), 1, 2, 1, "bf16"),
+    (3, 16, 16, 1, (3, 3), (8, 8), (1, 1), 1, 0, 1, "f32"),      # kT = 1: no ring
+]
+
+
+@pytest.mark.parametrize("case", GEMM_CASES, ids=lambda c: "gemm_" + "_".join(map(str, c[:4])) + c[-1])
+def test_gemm_forced(case):
+    B, cin, cout, kT, ks, size, ps, sT, pT, dT, dt = case
+    say("gemm", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=(kT,) + ks,
+                          in_size=size, stride=(sT,) + (1,) * len(size),
+                          padding=(pT,) + ps, dilation=(dT,) + (1,) * len(size), dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 11, 61000 + cin * 7 + cout, "kaiming")
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=spec.stride,
+                      padding=spec.padding, dilation=spec.dilation, algo="gemm")
+    assert co.algo.startswith("gemm")
+    ref = oracle_conv(w, b, spec.stride, spec.padding, spec.dilation, 1)
+    xd = x.to(DEV)
+    tdt = synth.torch_dtype(dt)
+    # steps through forward_step (with update_state=False peeks in between)
+    outs, peeks = [], []
+    for t in range(x.shape[2]):
+        fr = xd[:, :, t].contiguous()
+        pk = co.forward_step(fr, update_state=False)
+        if pk is not None:
+            peeks.append(pk.clone())
+        y = co.forward_step(fr)
+        if y is not None:
+            outs.append(y.clone())
+    r = ref.forward_steps(np64(x))
+    if r is None:
+        assert not outs
+        return
+    got = np.stack([np64(o) for o in outs], axis=2)
+    assert_close(got, r, tdt, "gemm steps")
+    assert len(peeks) == len(outs)
+    for a, bb in zip(peeks, outs):
+        assert torch.equal(a, bb)
+    # forward_steps with end padding from a clean state
+    co.clean_state()
+    ref.clean_state()
+    ys = co.forward_steps(xd, pad_end=True)
+    assert_close(np64(ys), ref.forward_steps(np64(x), pad_end=True), tdt, "gemm steps pad_end")
