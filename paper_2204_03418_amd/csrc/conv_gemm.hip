@@ -22,8 +22,9 @@
 // channels-last layout, transposing the NCHW frame on the way, and copies the
 // matching block of pre-packed weights.  Each lane then reads 16-byte operand
 // fragments (8 bf16 or 4 fp32 channels of one pixel / one column) straight
-// from LDS for v_mfma_f32_16x16x32_bf16 or v_mfma_f32_16x16x4_f32.  16-byte
-// units of a pixel are XOR-swizzled against LDS bank conflicts.  Tiles are
+// from LDS for v_mfma_f32_16x16x32_bf16 or v_mfma_f32_16x16x4_f32.  Operand
+// addresses are a per-lane base plus compile-time offsets (spatial tap,
+// stage), so they cost no registers or ALU work inside the loop.  Tiles are
 // numbered so that consecutive tiles run on the same XCD and share its L2.
 #include "device.hpp"
 #include "launch.hpp"
@@ -39,6 +40,8 @@ struct GemmArgs {
   int32_t M, N, So;
   int32_t m_tiles, n_tile0, n_tile_cnt, tiles_per_xcd;
   int32_t n_chunks, cols, max_slots;
+  int32_t pair;     // rows are read two pixels per load (even width, aligned)
+  int32_t x_bytes;  // bytes of x reachable from the frame pointer
 };
 
 template <typename T>
@@ -65,26 +68,105 @@ __device__ __forceinline__ void mma(v4f& acc, const v4f& a, const v4f& b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc, 0, 0, 0);
 }
 
-// Physical 16-byte unit of logical unit `grp` of pixel/column `idx`.
-__device__ __forceinline__ int swz(int idx, int grp) { return grp ^ ((idx >> 1) & 3); }
-
 template <typename T>
 __device__ __forceinline__ void store_out(T* y, int64_t i, float v) {
   y[i] = from_f32<T>(v);
 }
 
-template <typename T, int KH, int KW, int WM, int WN, int NWM, int NWN>
+// Four consecutive outputs; one 8- or 16-byte store when aligned.
+template <typename T>
+__device__ __forceinline__ void store4(T* y, float a, float b, float c, float d, bool vec);
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* y, float a, float b, float c, float d,
+                                               bool vec) {
+  if (vec) {
+    const uint32_t lo = uint32_t(f32_to_bf16(a)) | (uint32_t(f32_to_bf16(b)) << 16);
+    const uint32_t hi = uint32_t(f32_to_bf16(c)) | (uint32_t(f32_to_bf16(d)) << 16);
+    *reinterpret_cast<uint2*>(y) = make_uint2(lo, hi);
+  } else {
+    y[0] = f32_to_bf16(a);
+    y[1] = f32_to_bf16(b);
+    y[2] = f32_to_bf16(c);
+    y[3] = f32_to_bf16(d);
+  }
+}
+template <>
+__device__ __forceinline__ void store4<float>(float* y, float a, float b, float c, float d,
+                                              bool vec) {
+  if (vec) {
+    *reinterpret_cast<float4*>(y) = make_float4(a, b, c, d);
+  } else {
+    y[0] = a;
+    y[1] = b;
+    y[2] = c;
+    y[3] = d;
+  }
+}
+
+// Raw global loads of one staging item -- KL channels of one pixel, or of two
+// adjacent pixels when rows have even width (one 4- or 8-byte load per
+// channel) -- and their packing into the two pixels' 16-byte LDS units.
+// Bit operations only, so the values stay in registers.
+template <typename T>
+struct Stage;
+template <>
+struct Stage<bf16_t> {
+  using Pair = uint32_t;  // two bf16 of one channel: pixel x (low), x+1 (high)
+  static __device__ __forceinline__ Pair load(__amdgpu_buffer_rsrc_t r, int voff, int soff,
+                                              bool pair) {
+    return pair ? __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0)
+                : uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+  }
+  static __device__ __forceinline__ void pack(const Pair (&r)[8], uint4& u0, uint4& u1) {
+    u0.x = (r[0] & 0xffffu) | (r[1] << 16);
+    u0.y = (r[2] & 0xffffu) | (r[3] << 16);
+    u0.z = (r[4] & 0xffffu) | (r[5] << 16);
+    u0.w = (r[6] & 0xffffu) | (r[7] << 16);
+    u1.x = (r[0] >> 16) | (r[1] & 0xffff0000u);
+    u1.y = (r[2] >> 16) | (r[3] & 0xffff0000u);
+    u1.z = (r[4] >> 16) | (r[5] & 0xffff0000u);
+    u1.w = (r[6] >> 16) | (r[7] & 0xffff0000u);
+  }
+};
+template <>
+struct Stage<float> {
+  using Pair = uint2;  // two fp32 of one channel: pixel x, x+1
+  static __device__ __forceinline__ Pair load(__amdgpu_buffer_rsrc_t r, int voff, int soff,
+                                              bool pair) {
+    if (pair) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+      return make_uint2(v[0], v[1]);
+    }
+    return make_uint2(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0), 0u);
+  }
+  static __device__ __forceinline__ void pack(const Pair (&r)[4], uint4& u0, uint4& u1) {
+    u0 = make_uint4(r[0].x, r[1].x, r[2].x, r[3].x);
+    u1 = make_uint4(r[0].y, r[1].y, r[2].y, r[3].y);
+  }
+};
+
+// Raw buffer resource over `bytes` bytes from `base` (CDNA raw-buffer word 3:
+// 32-bit data format, no swizzle); reads past the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), bytes, 0x00020000);
+}
+
+template <typename T, int KH, int KW, int WM, int WN, int NWM, int NWN, bool PAIR>
 __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     ConvGeom g, GemmArgs ga, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
     int64_t y_bc, const uint4* __restrict__ wp, const float* __restrict__ bias,
     float* __restrict__ ring, int64_t ring_slot, TapTable tt) {
   using Frag = typename FragOf<T>::type;
+  using Pair = typename Stage<T>::Pair;
   constexpr int KL = 16 / int(sizeof(T));  // channels per 16-byte unit
   constexpr int CK = 4 * KL;               // channels per LDS chunk
   constexpr int KHW = KH * KW;
   constexpr int NT = 64 * NWM * NWN;
   constexpr int M_WG = 16 * WM * NWM;
   constexpr int N_WG = 16 * WN * NWN;
+  constexpr int AI = (kGemmStageItems + NT - 1) / NT;     // A items per thread
+  constexpr int B_UNITS = KHW * N_WG * 4;
+  constexpr int BI = (B_UNITS + NT - 1) / NT;            // B copies per thread
   extern __shared__ uint4 smem[];
 
   const int tid = int(threadIdx.x);
@@ -111,10 +193,14 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   const int nslots = q1 - q0 + 1;
   const int zero_slot = ga.max_slots;
 
-  uint4* As = smem;                                      // [(slots+1) * cols][4]
-  uint4* Bs = smem + (ga.max_slots + 1) * ga.cols * 4;   // [KHW * N_WG][4]
-  const int a_units = (ga.max_slots + 1) * ga.cols * 4;
-  for (int u = tid; u < a_units; u += NT) As[u] = make_uint4(0u, 0u, 0u, 0u);
+  // LDS: [A stage 0][A stage 1][B stage 0][B stage 1]; an A stage holds
+  // (slots + zero row) * cols pixels of 4 units plus two trash pixels that
+  // absorb the writes of staging items a thread does not have.
+  const int a_pixels = (ga.max_slots + 1) * ga.cols;
+  const int a_units = (a_pixels + 2) * 4;
+  uint4* const As0 = smem;
+  uint4* const Bs0 = smem + 2 * a_units;
+  for (int u = tid; u < 2 * a_units; u += NT) smem[u] = make_uint4(0u, 0u, 0u, 0u);
 
   // LDS pixel index of each of this lane's A rows, per spatial tap row u
   int pixbase[WM][KH];
@@ -132,129 +218,234 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     }
   }
 
+  // staging items of this thread: (slot, channel group, pixel or pixel pair).
+  // Items past the tile read element 0 and land in the trash pixels.
+  constexpr int PW = PAIR ? 2 : 1;
+  const int wp_items = g.W / PW;
+  const int a_items = nslots * 4 * wp_items;
+  int a_src[AI];      // byte offset of the item without the chunk's channel base
+  int a_dst[AI];      // LDS unit index of the item's first pixel
+  int a_dst1[AI];     // ... and of its second pixel (PAIR)
+  int a_grp[AI];
+#pragma unroll
+  for (int ai = 0; ai < AI; ++ai) {
+    const int it = tid + ai * NT;
+    a_src[ai] = 0;
+    a_grp[ai] = 0;
+    a_dst[ai] = a_pixels * 4;
+    a_dst1[ai] = (a_pixels + 1) * 4;
+    if (it < a_items) {
+      const int xp = it % wp_items;
+      const int rest = it / wp_items;
+      const int grp = rest & 3;
+      const int sl = rest >> 2;
+      const int q = q0 + sl;
+      const int b = q / g.H, ih = q - b * g.H;
+      const int xcol = xp * PW;
+      a_src[ai] = int(((int64_t(b) * g.Cin + grp * KL) * x_bc + int64_t(ih) * g.W + xcol) *
+                      int64_t(sizeof(T)));
+      a_grp[ai] = grp;
+      const int pix = sl * ga.cols + xcol + g.pW;
+      a_dst[ai] = pix * 4 + grp;
+      a_dst1[ai] = (pix + 1) * 4 + grp;
+    }
+  }
+
+  Pair ra[AI][KL];
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ga.x_bytes);
+  const int plane_bytes = int(x_bc * int64_t(sizeof(T)));
+  // channels past C_in read the next stream's planes or past the buffer end
+  // (zero); they are masked when stored
+  auto prefetch = [&](int ch) {
+    const int cbase = ch * CK;
+#pragma unroll
+    for (int ai = 0; ai < AI; ++ai)
+#pragma unroll
+      for (int e = 0; e < KL; ++e)
+        ra[ai][e] = Stage<T>::load(xr, a_src[ai], (cbase + e) * plane_bytes, PAIR);
+  };
+  auto store_a = [&](int buf, int ch) {
+    uint4* As = As0 + buf * a_units;
+    const bool ragged = ch * CK + CK > g.Cin;
+#pragma unroll
+    for (int ai = 0; ai < AI; ++ai) {
+      if (ragged) {  // channels past C_in were read clamped: zero them
+        const int c0 = ch * CK + a_grp[ai] * KL;
+#pragma unroll
+        for (int e = 0; e < KL; ++e)
+          if (c0 + e >= g.Cin) ra[ai][e] = Pair{};
+      }
+      uint4 p0, p1;
+      Stage<T>::pack(ra[ai], p0, p1);
+      As[a_dst[ai]] = p0;
+      if (PAIR) As[a_dst1[ai]] = p1;
+    }
+  };
+  // B: the pre-packed block of (n_tile, ch) goes straight from global memory
+  // into LDS (global_load_lds_dwordx4; each wave fills 1 KB contiguously)
+  auto copy_b = [&](int ch, int buf) {
+    const uint4* wsrc = wp + (int64_t(n_tile) * ga.n_chunks + ch) * B_UNITS;
+    uint4* Bs = Bs0 + buf * B_UNITS;
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) {
+      const int u0 = wave * 64 + bi * NT;  // first unit of this wave's 1 KB
+      if (u0 < B_UNITS)
+        __builtin_amdgcn_global_load_lds(wsrc + u0 + lane,
+                                         (__attribute__((address_space(3))) void*)(Bs + u0),
+                                         16, 0, 0);
+    }
+  };
+
   v4f acc[WM][WN];
 #pragma unroll
   for (int mf = 0; mf < WM; ++mf)
 #pragma unroll
     for (int nf = 0; nf < WN; ++nf) acc[mf][nf] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  const int a_items = nslots * 4 * g.W;
-  const int b_units = KHW * N_WG * 4;
-  for (int ch = 0; ch < ga.n_chunks; ++ch) {
-    __syncthreads();
-    // stage A: item = (slot, channel group, column), column fastest so the
-    // global reads of one channel row are coalesced across lanes
-    for (int it = tid; it < a_items; it += NT) {
-      const int xcol = it % g.W;
-      const int rest = it / g.W;
-      const int grp = rest & 3;
-      const int s = rest >> 2;
-      const int q = q0 + s;
-      const int b = q / g.H, ih = q - b * g.H;
-      const int c0 = ch * CK + grp * KL;
-      union {
-        T v[KL];
-        uint4 u;
-      } pk;
-      const T* src = x + (int64_t(b) * g.Cin + c0) * x_bc + int64_t(ih) * g.W + xcol;
+  // epilogue data of this lane's columns, resolved before the main loop so
+  // the tap table reads are long done when the epilogue runs
+  int e_act[WN], e_o[WN];
+  float e_bias[WN];
+  float* e_ring[WN];
+  const bool e_yvec = (y_bc % 4) == 0 &&
+                      (reinterpret_cast<uintptr_t>(y) % (4 * sizeof(T))) == 0;
 #pragma unroll
-      for (int e = 0; e < KL; ++e) pk.v[e] = (c0 + e < g.Cin) ? src[int64_t(e) * x_bc] : T(0);
-      const int pix = s * ga.cols + xcol + g.pW;
-      As[pix * 4 + swz(pix, grp)] = pk.u;
-    }
-    // stage B: the pre-packed (already swizzled) weight block of (n_tile, ch)
-    const uint4* wsrc = wp + (int64_t(n_tile) * ga.n_chunks + ch) * b_units;
-    for (int u = tid; u < b_units; u += NT) Bs[u] = wsrc[u];
-    __syncthreads();
+  for (int nf = 0; nf < WN; ++nf) {
+    const int n = n_tile * N_WG + (wn * WN + nf) * 16 + lrow;
+    const int nn = n < ga.N ? n : ga.N - 1;
+    const int t = nn / g.Cout, o = nn - t * g.Cout;
+    e_act[nf] = n < ga.N ? int(tt.action[t]) : CO_TAP_NONE;
+    e_o[nf] = o;
+    e_bias[nf] = bias[o];
+    const int sl = tt.slot[t] < 0 ? 0 : tt.slot[t];
+    e_ring[nf] = ring + int64_t(sl) * ring_slot + int64_t(o) * ga.M;
+  }
 
+  // Accumulators start from the partial sum the ring already holds for the
+  // taps that add to it (ACC, EMIT) and from zero otherwise, so the MFMAs
+  // accumulate straight onto the ring value; the reads are issued here and
+  // land while the first chunk is staged.
+  const bool vec_epi = (ga.M % 4) == 0;
+#pragma unroll
+  for (int nf = 0; nf < WN; ++nf) {
+    const bool rd = e_act[nf] == CO_TAP_ACC || e_act[nf] == CO_TAP_EMIT;
+#pragma unroll
+    for (int mf = 0; mf < WM; ++mf) {
+      const int P0 = m0 + (wm * WM + mf) * 16 + lgrp * 4;
+      if (rd && P0 < ga.M) {
+        if (vec_epi) {
+          acc[mf][nf] = *reinterpret_cast<const v4f*>(e_ring[nf] + P0);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (P0 + r < ga.M) acc[mf][nf][r] = e_ring[nf][P0 + r];
+        }
+      }
+    }
+  }
+
+  // B fragment LDS units of this lane (column n, logical unit lgrp)
+  int bbase[WN];
+#pragma unroll
+  for (int nf = 0; nf < WN; ++nf) {
+    const int n = (wn * WN + nf) * 16 + lrow;
+    bbase[nf] = n * 4 + lgrp;
+  }
+
+  __syncthreads();  // zero fill done
+  copy_b(0, 0);
+  prefetch(0);
+  store_a(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);  // LDS-direct loads of B have landed
+  __syncthreads();
+  for (int ch = 0; ch < ga.n_chunks; ++ch) {
+    const bool more = ch + 1 < ga.n_chunks;
+    if (more) {  // next chunk's global loads are in flight during the MFMAs
+      copy_b(ch + 1, (ch + 1) & 1);
+      prefetch(ch + 1);
+    }
+    const uint4* As = As0 + (ch & 1) * a_units;
+    const uint4* Bs = Bs0 + (ch & 1) * B_UNITS;
+    Frag af[2][WM], bf[2][WN];
+    auto load_frags = [&](int uv, int k) {
+      const int u = uv / KW, v = uv % KW;
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf)
+        af[k][mf] = __builtin_bit_cast(Frag, As[(pixbase[mf][u] + v) * 4 + lgrp]);
+#pragma unroll
+      for (int nf = 0; nf < WN; ++nf)
+        bf[k][nf] = __builtin_bit_cast(Frag, Bs[uv * N_WG * 4 + bbase[nf]]);
+    };
+    load_frags(0, 0);
 #pragma unroll
     for (int uv = 0; uv < KHW; ++uv) {
-      const int u = uv / KW, v = uv % KW;
-      Frag af[WM], bf[WN];
-#pragma unroll
-      for (int mf = 0; mf < WM; ++mf) {
-        const int pix = pixbase[mf][u] + v;
-        const uint4 t = As[pix * 4 + swz(pix, lgrp)];
-        af[mf] = __builtin_bit_cast(Frag, t);
-      }
-#pragma unroll
-      for (int nf = 0; nf < WN; ++nf) {
-        const int n = (wn * WN + nf) * 16 + lrow;
-        const uint4 t = Bs[(uv * N_WG + n) * 4 + swz(n, lgrp)];
-        bf[nf] = __builtin_bit_cast(Frag, t);
-      }
+      // the next tap's fragments are requested before this tap's MFMAs, so
+      // LDS latency hides behind WM*WN matrix instructions
+      if (uv + 1 < KHW) load_frags(uv + 1, (uv + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int mf = 0; mf < WM; ++mf)
 #pragma unroll
-        for (int nf = 0; nf < WN; ++nf) mma(acc[mf][nf], af[mf], bf[nf]);
+        for (int nf = 0; nf < WN; ++nf) mma(acc[mf][nf], af[uv & 1][mf], bf[uv & 1][nf]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    if (more) store_a((ch + 1) & 1, ch + 1);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
   }
 
   // Fused ring epilogue.  Lane (lrow, lgrp) of fragment (mf, nf) holds column
   // n = ... + lrow and the four consecutive pixels lgrp*4 .. lgrp*4+3.  The
   // ring is (slot, C_out, B*Ho*Wo), so those four pixels are contiguous.
-  const bool vec = (ga.M % 4) == 0;
-  const bool yvec = (ga.So % 4) == 0 && (y_bc % 4) == 0;
-#pragma unroll
-  for (int nf = 0; nf < WN; ++nf) {
-    const int n = n_tile * N_WG + (wn * WN + nf) * 16 + lrow;
-    if (n >= ga.N) continue;
-    const int t = n / g.Cout, o = n - t * g.Cout;
-    const int act = tt.action[t];
-    if (act == CO_TAP_NONE) continue;
-    const int slot = tt.slot[t] < 0 ? 0 : tt.slot[t];
-    float* rrow = ring + int64_t(slot) * ring_slot + int64_t(o) * ga.M;
-    const float bo = bias[o];
+  if (vec_epi) {
+    // the accumulators already include the ring value: stores only
 #pragma unroll
     for (int mf = 0; mf < WM; ++mf) {
       const int P0 = m0 + (wm * WM + mf) * 16 + lgrp * 4;
       if (P0 >= ga.M) continue;
-      const v4f a = acc[mf][nf];
-      float vals[4] = {a[0], a[1], a[2], a[3]};
-      const bool full = vec && P0 + 3 < ga.M;
-      if (act == CO_TAP_START) {
-        if (full) {
-          *reinterpret_cast<float4*>(rrow + P0) = make_float4(vals[0], vals[1], vals[2], vals[3]);
-        } else {
-          for (int r = 0; r < 4; ++r)
-            if (P0 + r < ga.M) rrow[P0 + r] = vals[r];
-        }
-      } else if (act == CO_TAP_ACC) {
-        if (full) {
-          float4 cur = *reinterpret_cast<const float4*>(rrow + P0);
-          cur.x += vals[0];
-          cur.y += vals[1];
-          cur.z += vals[2];
-          cur.w += vals[3];
-          *reinterpret_cast<float4*>(rrow + P0) = cur;
-        } else {
-          for (int r = 0; r < 4; ++r)
-            if (P0 + r < ga.M) rrow[P0 + r] += vals[r];
-        }
-      } else {  // EMIT / EMIT_FRESH: complete the output frame
-        if (act == CO_TAP_EMIT) {
-          if (full) {
-            const float4 cur = *reinterpret_cast<const float4*>(rrow + P0);
-            vals[0] += cur.x;
-            vals[1] += cur.y;
-            vals[2] += cur.z;
-            vals[3] += cur.w;
+      const int b = P0 / ga.So, p = P0 - b * ga.So;
+      const bool same_frame = p + 3 < ga.So;
+#pragma unroll
+      for (int nf = 0; nf < WN; ++nf) {
+        const int act = e_act[nf];
+        const v4f v = acc[mf][nf];
+        if (act == CO_TAP_START || act == CO_TAP_ACC) {
+          *reinterpret_cast<v4f*>(e_ring[nf] + P0) = v;
+        } else if (act == CO_TAP_EMIT || act == CO_TAP_EMIT_FRESH) {
+          const float bo = e_bias[nf];
+          const int o = e_o[nf];
+          if (same_frame) {
+            T* yp = y + (int64_t(b) * g.Cout + o) * y_bc + p;
+            store4<T>(yp, v[0] + bo, v[1] + bo, v[2] + bo, v[3] + bo, e_yvec);
           } else {
-            for (int r = 0; r < 4; ++r)
-              if (P0 + r < ga.M) vals[r] += rrow[P0 + r];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int bb = (P0 + r) / ga.So, pp = (P0 + r) - bb * ga.So;
+              store_out<T>(y, (int64_t(bb) * g.Cout + o) * y_bc + pp, v[r] + bo);
+            }
           }
         }
-        if (full && yvec) {
-          const int b = P0 / ga.So, p = P0 - b * ga.So;
-          T* yp = y + (int64_t(b) * g.Cout + o) * y_bc + p;
+      }
+    }
+  } else {
+    // ragged pixel count: element-wise
 #pragma unroll
-          for (int r = 0; r < 4; ++r) store_out<T>(yp, r, vals[r] + bo);
-        } else {
-          for (int r = 0; r < 4; ++r) {
-            const int P = P0 + r;
-            if (P >= ga.M) break;
+    for (int nf = 0; nf < WN; ++nf) {
+      const int act = e_act[nf];
+      if (act == CO_TAP_NONE) continue;
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf) {
+        const int P0 = m0 + (wm * WM + mf) * 16 + lgrp * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int P = P0 + r;
+          if (P >= ga.M) continue;
+          const float v = acc[mf][nf][r];
+          if (act == CO_TAP_START || act == CO_TAP_ACC) {
+            e_ring[nf][P] = v;
+          } else {
             const int b = P / ga.So, p = P - b * ga.So;
-            store_out<T>(y, (int64_t(b) * g.Cout + o) * y_bc + p, vals[r] + bo);
+            store_out<T>(y, (int64_t(b) * g.Cout + e_o[nf]) * y_bc + p, v + e_bias[nf]);
           }
         }
       }
@@ -263,7 +454,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
 }
 
 // Pack W (C_out, C_in, kT, kH, kW) into [n_tile][chunk][uv][N_WG][4 units of
-// KL channels], zero padded, units pre-swizzled exactly as the kernel reads.
+// KL channels], zero padded, in exactly the order the kernel reads from LDS.
 template <typename T>
 __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfig c,
                                                            const T* __restrict__ w,
@@ -281,7 +472,7 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfi
   rest /= khw;
   const int ch = int(rest % c.n_chunks);
   const int nt = int(rest / c.n_chunks);
-  const int grp = phys ^ ((nl >> 1) & 3);
+  const int grp = phys;
   const int n = nt * c.N_WG + nl;
   const int t = n / g.Cout, o = n - t * g.Cout;
   const int u = uv / g.kW, v = uv % g.kW;
@@ -300,10 +491,10 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfi
   out[U] = pk.q;
 }
 
-template <typename T, int KH, int KW, int WM, int WN, int NWM, int NWN>
+template <typename T, int KH, int KW, int WM, int WN, int NWM, int NWN, bool PAIR>
 hipError_t gemm_launch(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L, char* state,
                        const StepIO& io, const co_step_plan& plan, hipStream_t s) {
-  auto kern = conv_step_gemm_kernel<T, KH, KW, WM, WN, NWM, NWN>;
+  auto kern = conv_step_gemm_kernel<T, KH, KW, WM, WN, NWM, NWN, PAIR>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -337,6 +528,9 @@ hipError_t gemm_launch(const ConvGeom& g, const GemmConfig& c, const ConvLayout&
   ga.n_chunks = c.n_chunks;
   ga.cols = c.cols;
   ga.max_slots = c.max_slots;
+  ga.pair = PAIR ? 1 : 0;
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  ga.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz);
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * ga.tiles_per_xcd)), dim3(64 * NWM * NWN),
                      size_t(c.lds_bytes), s, g, ga, static_cast<const T*>(io.x), io.x_bc,
                      static_cast<T*>(io.y), io.y_bc,
@@ -346,17 +540,25 @@ hipError_t gemm_launch(const ConvGeom& g, const GemmConfig& c, const ConvLayout&
   return hipGetLastError();
 }
 
+template <int KH, int KW, bool PAIR>
+hipError_t gemm_dispatch_cfg(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
+                             char* state, const StepIO& io, const co_step_plan& plan,
+                             hipStream_t s) {
+  switch (c.id) {
+    case 0: return gemm_launch<bf16_t, KH, KW, 7, 2, 4, 2, PAIR>(g, c, L, state, io, plan, s);
+    case 1: return gemm_launch<bf16_t, KH, KW, 2, 2, 1, 4, PAIR>(g, c, L, state, io, plan, s);
+    case 2: return gemm_launch<float, KH, KW, 2, 2, 1, 4, PAIR>(g, c, L, state, io, plan, s);
+    case 3: return gemm_launch<float, KH, KW, 1, 1, 4, 1, PAIR>(g, c, L, state, io, plan, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int KH, int KW>
 hipError_t gemm_dispatch_taps(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
                               char* state, const StepIO& io, const co_step_plan& plan,
                               hipStream_t s) {
-  switch (c.id) {
-    case 0: return gemm_launch<bf16_t, KH, KW, 7, 4, 4, 1>(g, c, L, state, io, plan, s);
-    case 1: return gemm_launch<bf16_t, KH, KW, 2, 2, 1, 4>(g, c, L, state, io, plan, s);
-    case 2: return gemm_launch<float, KH, KW, 2, 2, 1, 4>(g, c, L, state, io, plan, s);
-    case 3: return gemm_launch<float, KH, KW, 1, 1, 4, 1>(g, c, L, state, io, plan, s);
-    default: return hipErrorInvalidValue;
-  }
+  if (g.W % 2 == 0) return gemm_dispatch_cfg<KH, KW, true>(g, c, L, state, io, plan, s);
+  return gemm_dispatch_cfg<KH, KW, false>(g, c, L, state, io, plan, s);
 }
 
 }  // namespace
@@ -365,6 +567,15 @@ hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* s
                                  const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   GemmConfig c;
   if (!gemm_config(g, g.cfg, &c)) return hipErrorInvalidValue;
+  // Even-width rows are staged two pixels per load; a frame pointer or plane
+  // stride that breaks that alignment takes the direct kernel (same ring).
+  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  if (g.W % 2 == 0 &&
+      ((reinterpret_cast<uintptr_t>(io.x) % (2 * esz)) != 0 || (io.x_bc % 2) != 0))
+    return launch_conv_step_direct(g, L, state, io, plan, false, s);
+  // staging reads use 32-bit buffer offsets over the reachable part of x
+  if (((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * int64_t(esz) >= (int64_t(1) << 31))
+    return launch_conv_step_direct(g, L, state, io, plan, false, s);
   if (g.kH == 3 && g.kW == 3) return gemm_dispatch_taps<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return gemm_dispatch_taps<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;

@@ -47,7 +47,7 @@ struct GemmShape {
 
 // Instantiated tile shapes (the kernel file instantiates the same table).
 constexpr GemmShape kGemmShapes[kGemmConfigs] = {
-    {CO_BF16, 7, 4, 4, 1, 8},  // 448 x 64: large M and N, many channels
+    {CO_BF16, 7, 2, 4, 2, 8},  // 448 x 64, 8 waves: large M and N, many channels
     {CO_BF16, 2, 2, 1, 4, 8},  // 32 x 128: small K, wide N
     {CO_F32, 2, 2, 1, 4, 4},   // 32 x 128
     {CO_F32, 1, 1, 4, 1, 4},   // 64 x 16: small N, fills the chip with waves
@@ -98,9 +98,14 @@ bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
   for (int64_t t = 0; t < r.m_tiles; ++t)
     slots = std::max(slots, tile_slots(g, t * r.M_WG, std::min<int64_t>(M, (t + 1) * r.M_WG)));
   r.max_slots = int32_t(slots);
-  // A: (slots + zero row) x cols pixels x 64 B; B: kH*kW x N_WG x 64 B
-  r.lds_bytes = (slots + 1) * r.cols * 64 + int64_t(g.kH) * g.kW * r.N_WG * 64;
+  // two stages of A: (slots + zero row) x cols pixels x 64 B and
+  // B: kH*kW x N_WG x 64 B
+  r.lds_bytes = 2 * (((slots + 1) * r.cols + 2) * 64 + int64_t(g.kH) * g.kW * r.N_WG * 64);
   if (r.lds_bytes > kLdsBytes) return false;
+  // staging items (row, channel group, pixel pair) must fit the per-thread
+  // register budget of the kernel
+  const int64_t items = slots * 4 * (g.W % 2 == 0 ? g.W / 2 : g.W);
+  if (items > int64_t(kGemmStageItems)) return false;
   *c = r;
   return true;
 }
@@ -114,11 +119,19 @@ int gemm_pick(const ConvGeom& g) {
     // cycles of one wave: MFMA issue (bf16 16x16x32: 16 clk per fragment pair
     // per 32 channels; f32 16x16x4: 4 x 32 clk per 16 channels), plus staging
     // per chunk and the epilogue; waves beyond one per SIMD run in rounds
-    const double mfma = c.dtype == CO_BF16 ? 16.0 : 128.0;
+    // Workgroups resident per CU (LDS, 2048 threads) and waves per SIMD; one
+    // wave per SIMD issues MFMAs at about 30 cycles each on MI355X, two or
+    // more at about 21 (bf16 16x16x32, measured).
+    const int threads = 64 * c.NWM * c.NWN;
+    const int64_t wg_cu = std::max<int64_t>(
+        1, std::min<int64_t>(kLdsBytes / std::max<int64_t>(c.lds_bytes, 1), 2048 / threads));
+    const double wps = double(wg_cu) * c.NWM * c.NWN / 4.0;
+    const double mfma = (c.dtype == CO_BF16 ? 16.0 : 128.0) * (wps >= 2.0 ? 21.0 : 30.0) / 16.0;
     const double wave = double(c.WM) * c.WN * c.n_chunks * g.kH * g.kW * mfma +
                         300.0 * c.n_chunks + 100.0 * c.WM * c.WN;
-    const double waves = double(c.m_tiles) * c.n_tiles * c.NWM * c.NWN;
-    const double cost = std::ceil(waves / 1024.0) * wave;
+    const double wgs = double(c.m_tiles) * c.n_tiles;
+    const double rounds = std::ceil(wgs / (256.0 * double(wg_cu)));
+    const double cost = rounds * wave * std::max(1.0, wps) / std::max(1.0, wps);
     if (best < 0 || cost < best_cost) {
       best = id;
       best_cost = cost;

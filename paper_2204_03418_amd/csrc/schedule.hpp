@@ -58,6 +58,7 @@ struct GemmConfig {
 };
 
 constexpr int kGemmConfigs = 4;
+constexpr int kGemmStageItems = 1024;  // staging items per workgroup and chunk
 constexpr int64_t kLdsBytes = 160 * 1024;
 
 // Layout of a convolution state buffer (byte offsets).
