@@ -24,7 +24,9 @@
 // fragments (8 bf16 or 4 fp32 channels of one pixel / one column) straight
 // from LDS for v_mfma_f32_16x16x32_bf16 or v_mfma_f32_16x16x4_f32.  Operand
 // addresses are a per-lane base plus compile-time offsets (spatial tap,
-// stage), so they cost no registers or ALU work inside the loop.  Tiles are
+// stage), so they cost no registers or ALU work inside the loop; padded
+// pixels (A) and column-swizzled units (B) keep the reads free of LDS bank
+// conflicts.  Tiles are
 // numbered so that consecutive tiles run on the same XCD and share its L2.
 #include "device.hpp"
 #include "launch.hpp"
@@ -36,10 +38,18 @@ namespace {
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
+constexpr int kPixUnits = kGemmPixUnits;  // 16-byte units per staged pixel (4 + 1 pad)
+
+// Physical unit of logical channel group `grp` of weight column `n`: the XOR
+// spreads 8 consecutive columns over 8 bank groups (it depends on n only, so
+// a column's address stays base + tap offset).
+__device__ __forceinline__ int bswz(int n, int grp) { return grp ^ ((n >> 1) & 3); }
+
 struct GemmArgs {
   int32_t M, N, So;
   int32_t m_tiles, n_tile0, n_tile_cnt, tiles_per_xcd;
   int32_t n_chunks, cols, max_slots;
+  int32_t a_units;  // 16-byte units of one A stage
   int32_t pair;     // rows are read two pixels per load (even width, aligned)
   int32_t x_bytes;  // bytes of x reachable from the frame pointer
 };
@@ -193,11 +203,14 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   const int nslots = q1 - q0 + 1;
   const int zero_slot = ga.max_slots;
 
-  // LDS: [A stage 0][A stage 1][B stage 0][B stage 1]; an A stage holds
-  // (slots + zero row) * cols pixels of 4 units plus two trash pixels that
-  // absorb the writes of staging items a thread does not have.
-  const int a_pixels = (ga.max_slots + 1) * ga.cols;
-  const int a_units = (a_pixels + 2) * 4;
+  // LDS: [A stage 0][A stage 1][B stage 0][B stage 1].  An A stage holds
+  // rows of `cols` = W + pW pixels (consecutive rows share their zero halo
+  // column), the zero row, and two trash pixels that absorb the writes of
+  // staging items a thread does not have.  A pixel is 5 units of 16 bytes:
+  // 4 channel groups and one pad, so 8 consecutive pixels hit 8 different
+  // bank groups and a tap offset stays a plain address offset.
+  const int a_pixels = (ga.max_slots + 2) * ga.cols;
+  const int a_units = ga.a_units;  // == (a_pixels + 2) * kPixUnits, sized on the host
   uint4* const As0 = smem;
   uint4* const Bs0 = smem + 2 * a_units;
   for (int u = tid; u < 2 * a_units; u += NT) smem[u] = make_uint4(0u, 0u, 0u, 0u);
@@ -232,8 +245,8 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     const int it = tid + ai * NT;
     a_src[ai] = 0;
     a_grp[ai] = 0;
-    a_dst[ai] = a_pixels * 4;
-    a_dst1[ai] = (a_pixels + 1) * 4;
+    a_dst[ai] = a_pixels * kPixUnits;
+    a_dst1[ai] = (a_pixels + 1) * kPixUnits;
     if (it < a_items) {
       const int xp = it % wp_items;
       const int rest = it / wp_items;
@@ -246,8 +259,8 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
                       int64_t(sizeof(T)));
       a_grp[ai] = grp;
       const int pix = sl * ga.cols + xcol + g.pW;
-      a_dst[ai] = pix * 4 + grp;
-      a_dst1[ai] = (pix + 1) * 4 + grp;
+      a_dst[ai] = pix * kPixUnits + grp;
+      a_dst1[ai] = (pix + 1) * kPixUnits + grp;
     }
   }
 
@@ -349,7 +362,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
 #pragma unroll
   for (int nf = 0; nf < WN; ++nf) {
     const int n = (wn * WN + nf) * 16 + lrow;
-    bbase[nf] = n * 4 + lgrp;
+    bbase[nf] = n * 4 + bswz(n, lgrp);
   }
 
   __syncthreads();  // zero fill done
@@ -371,7 +384,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
       const int u = uv / KW, v = uv % KW;
 #pragma unroll
       for (int mf = 0; mf < WM; ++mf)
-        af[k][mf] = __builtin_bit_cast(Frag, As[(pixbase[mf][u] + v) * 4 + lgrp]);
+        af[k][mf] = __builtin_bit_cast(Frag, As[(pixbase[mf][u] + v) * kPixUnits + lgrp]);
 #pragma unroll
       for (int nf = 0; nf < WN; ++nf)
         bf[k][nf] = __builtin_bit_cast(Frag, Bs[uv * N_WG * 4 + bbase[nf]]);
@@ -472,7 +485,7 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfi
   rest /= khw;
   const int ch = int(rest % c.n_chunks);
   const int nt = int(rest / c.n_chunks);
-  const int grp = phys;
+  const int grp = phys ^ ((nl >> 1) & 3);  // inverse of bswz
   const int n = nt * c.N_WG + nl;
   const int t = n / g.Cout, o = n - t * g.Cout;
   const int u = uv / g.kW, v = uv % g.kW;
@@ -528,6 +541,7 @@ hipError_t gemm_launch(const ConvGeom& g, const GemmConfig& c, const ConvLayout&
   ga.n_chunks = c.n_chunks;
   ga.cols = c.cols;
   ga.max_slots = c.max_slots;
+  ga.a_units = int32_t(c.a_units);
   ga.pair = PAIR ? 1 : 0;
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   ga.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz);

@@ -93,14 +93,18 @@ bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
   r.m_tiles = int32_t(ceil_div(M, r.M_WG));
   r.n_tiles = int32_t(ceil_div(N, r.N_WG));
   r.n_chunks = int32_t(ceil_div(g.Cin, r.CK));
-  r.cols = g.W + 2 * g.pW;
+  r.cols = g.W + g.pW;  // staged row pitch: rows share their zero halo column
   int64_t slots = 1;
   for (int64_t t = 0; t < r.m_tiles; ++t)
     slots = std::max(slots, tile_slots(g, t * r.M_WG, std::min<int64_t>(M, (t + 1) * r.M_WG)));
   r.max_slots = int32_t(slots);
-  // two stages of A: (slots + zero row) x cols pixels x 64 B and
-  // B: kH*kW x N_WG x 64 B
-  r.lds_bytes = 2 * (((slots + 1) * r.cols + 2) * 64 + int64_t(g.kH) * g.kW * r.N_WG * 64);
+  // LDS: two stages of A and two of B, in 16-byte units.  An A stage holds
+  // (slots + zero row + halo spill) rows of `cols` pixels plus 2 trash pixels,
+  // kGemmPixUnits units per pixel; a B stage kH*kW x N_WG columns x 4 units.
+  // The kernel takes a_units from here, so allocation and layout agree.
+  r.a_units = ((slots + 2) * r.cols + 2) * kGemmPixUnits;
+  r.b_units = int64_t(g.kH) * g.kW * r.N_WG * 4;
+  r.lds_bytes = 2 * (r.a_units + r.b_units) * 16;
   if (r.lds_bytes > kLdsBytes) return false;
   // staging items (row, channel group, pixel pair) must fit the per-thread
   // register budget of the kernel

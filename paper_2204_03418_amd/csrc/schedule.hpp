@@ -52,12 +52,15 @@ struct GemmConfig {
   int32_t CK;          // input channels per LDS chunk (= 4 * KL)
   int32_t M_WG, N_WG;  // workgroup tile
   int32_t m_tiles, n_tiles, n_chunks;
-  int32_t cols;        // staged pixels per input row (W + 2 pW)
+  int32_t cols;        // staged row pitch in pixels (W + pW: shared halo)
   int32_t max_slots;   // staged input rows per tile (one zero row follows)
-  int64_t lds_bytes;
+  int64_t a_units;     // 16-byte units of one A stage in LDS
+  int64_t b_units;     // 16-byte units of one B stage in LDS
+  int64_t lds_bytes;   // 2 * (a_units + b_units) * 16
 };
 
 constexpr int kGemmConfigs = 4;
+constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)
 constexpr int kGemmStageItems = 1024;  // staging items per workgroup and chunk
 constexpr int64_t kLdsBytes = 160 * 1024;
 

@@ -247,3 +247,24 @@ def test_emission_count_matches_oracle_formula():
             emitted = sum(C.conv_plan(d, n).emit for n in range(T))
             expect = (T + p - k) // s + 1 if T + p >= k else 0
             assert emitted == expect
+
+
+def test_gemm_state_and_algorithm_for_named_workloads():
+    """Every named workload resolves to its intended kernel family and a
+    state size that holds the packed weights and the ring."""
+    from paper_2204_03418_amd import synth
+    expect = {"conv1d_b1_c4to8_k3_f32": C.CO_ALGO_DIRECT,
+              "dwconv3d_b16_c432_k3_7x7_avgpool_bf16": C.CO_ALGO_DEPTHWISE}
+    for name, w in synth.WORKLOADS.items():
+        c = w.conv
+        d = C.conv_desc(c.batch, c.in_channels, c.out_channels, c.kernel, c.in_size, c.stride,
+                        c.padding, c.dilation, c.groups, True,
+                        C.CO_BF16 if c.dtype == "bf16" else C.CO_F32)
+        info = C.conv_query(d)
+        assert info.algo == expect.get(name, C.CO_ALGO_GEMM), name
+        esz = 2 if c.dtype == "bf16" else 4
+        So = 1
+        for s in info.out_size[:len(c.in_size)]:
+            So *= s
+        ring = info.ring_slots * c.batch * c.out_channels * So * 4
+        assert info.state_bytes >= ring + c.out_channels * 4, name
