@@ -155,12 +155,6 @@ struct Stage<float> {
   }
 };
 
-// Raw buffer resource over `bytes` bytes from `base` (CDNA raw-buffer word 3:
-// 32-bit data format, no swizzle); reads past the end return zero.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), bytes, 0x00020000);
-}
-
 template <typename T, int KH, int KW, int WM, int WN, int NWM, int NWN, bool PAIR>
 __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     ConvGeom g, GemmArgs ga, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,

@@ -50,6 +50,32 @@ struct PoolTaps {
 
 constexpr int kBlock = 256;
 
+// Raw buffer resource over `bytes` bytes from `base` (CDNA raw-buffer word 3:
+// 32-bit data format, no swizzle).  Reads at offsets past `bytes` return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), bytes, 0x00020000);
+}
+
+// Byte offset that lies past every buffer this library builds (< 2^31), so a
+// read from it returns 0: out-of-frame stencil taps load through it instead of
+// branching around the load.
+constexpr int kOutOfRange = 0x7ffffff0;
+
+// Element `e` of a T buffer, or 0.0 when !in (no branch: the offset moves out
+// of range and the hardware returns zero).
+template <typename T>
+__device__ __forceinline__ float load_or_zero(__amdgpu_buffer_rsrc_t r, int e, bool in);
+template <>
+__device__ __forceinline__ float load_or_zero<bf16_t>(__amdgpu_buffer_rsrc_t r, int e, bool in) {
+  const int off = in ? e * 2 : kOutOfRange;
+  return bf16_to_f32(bf16_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)));
+}
+template <>
+__device__ __forceinline__ float load_or_zero<float>(__amdgpu_buffer_rsrc_t r, int e, bool in) {
+  const int off = in ? e * 4 : kOutOfRange;
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
 inline unsigned grid_for(int64_t n, int block = kBlock) {
   return unsigned((n + block - 1) / block);
 }

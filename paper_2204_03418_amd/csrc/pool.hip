@@ -9,8 +9,11 @@
 // before Principle 3 -- and, when the schedule emits, reduces the window's
 // kT slots into the output.  Average pooling stores window sums (pads add 0)
 // and divides once at emission; maximum pooling stores window maxima (pads
-// are -inf).
+// are -inf).  Groups of lanes share each output element (see
+// pool_step_kernel), so a window of 49 positions is loaded in one round.
 #include <math.h>
+
+#include <algorithm>
 
 #include "device.hpp"
 #include "launch.hpp"
@@ -19,64 +22,108 @@ namespace coinf {
 
 namespace {
 
-template <typename T>
+// Reduction of v over the G lanes of a lane group (G a power of two <= 64).
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+  for (int m = G / 2; m > 0; m >>= 1) v += __shfl_xor(v, m, G);
+  return v;
+}
+template <int G>
+__device__ __forceinline__ float group_max(float v) {
+#pragma unroll
+  for (int m = G / 2; m > 0; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, G));
+  return v;
+}
+
+// One pool step.  G lanes share one output element (b, c, i, j): they load
+// the spatial window together (lane r takes window elements r, r + G, ...,
+// with clamped addresses so all loads are in flight at once) and reduce it
+// with cross-lane shuffles; the FIFO slot is written by lane 0; when the
+// schedule emits, lane j of the group fetches temporal tap j and the group
+// reduces again.  No thread ever waits on a chain of dependent loads.
+template <typename T, int G>
 __global__ __launch_bounds__(kBlock) void pool_step_kernel(
     PoolGeom g, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y, int64_t y_bc,
     float* __restrict__ fifo, int64_t fifo_slot, float* __restrict__ valid, int32_t write_slot,
     int32_t update, int32_t emit, int32_t pad_frame, PoolTaps taps) {
   const int32_t So = g.Ho * g.Wo;
   const int32_t total = g.B * g.C * So;
-  const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
-  if (idx >= total) return;
-  const int32_t p = idx % So;
-  const int32_t bc = idx / So;
+  const int64_t gid = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  const int32_t idx = int32_t(gid / G);  // output element of this lane's group
+  const int32_t r = int32_t(gid % G);    // lane within the group
+  const bool live = idx < total;         // whole groups are live or not
+  const int32_t e_idx = live ? idx : 0;
+  const int32_t p = e_idx % So;
+  const int32_t bc = e_idx / So;
   const int32_t i = p / g.Wo, jo = p % g.Wo;
   const bool is_max = g.kind == CO_POOL_MAX;
-  // spatial reduction of the arriving frame
+  const int32_t kHW = g.kH * g.kW;
+
+  // spatial reduction of the arriving frame (out-of-frame positions read an
+  // out-of-range buffer offset: zero, no branch around the load)
   float val = is_max ? -INFINITY : 0.f;
-  int32_t scount = 0;
-  for (int32_t u = 0; u < g.kH; ++u) {
+  const int x_extent =
+      pad_frame ? 0 : int(((int64_t(g.B) * g.C - 1) * x_bc + g.H * g.W) * int64_t(sizeof(T)));
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, x_extent);
+  const int plane = int(int64_t(bc) * x_bc);
+  for (int32_t e = r; e < kHW; e += G) {
+    const int32_t u = e / g.kW, v = e - u * g.kW;
     const int32_t hi = i * g.sH + u * g.dH - g.pH;
-    if (hi < 0 || hi >= g.H) continue;
-    for (int32_t v = 0; v < g.kW; ++v) {
-      const int32_t wi = jo * g.sW + v * g.dW - g.pW;
-      if (wi < 0 || wi >= g.W) continue;
-      ++scount;
-      if (!pad_frame) {
-        const float e = to_f32<T>(x[int64_t(bc) * x_bc + hi * g.W + wi]);
-        val = is_max ? fmaxf(val, e) : val + e;
-      }
-    }
+    const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+    const bool in = hi >= 0 && hi < g.H && wi >= 0 && wi < g.W && !pad_frame;
+    const float xv = load_or_zero<T>(xr, plane + hi * g.W + wi, in);
+    if (in) val = is_max ? fmaxf(val, xv) : val + xv;
   }
-  if (update) {
+  val = is_max ? group_max<G>(val) : group_sum<G>(val);
+  if (!live) return;
+
+  if (update && r == 0) {
     fifo[int64_t(write_slot) * fifo_slot + idx] = val;
     if (idx == 0) valid[write_slot] = pad_frame ? 0.f : 1.f;
   }
   if (!emit) return;
+
+  // temporal reduction over the window's kT frames, spread over the group
   float acc = is_max ? -INFINITY : 0.f;
-  int32_t tcount = 0;
-  for (int32_t j = 0; j < g.kT; ++j) {
-    const int32_t s = taps.src[j];
-    float e;
-    int32_t ok;
-    if (s == -1) {  // start padding
-      continue;
-    } else if (s == -2) {  // the arriving frame
-      e = val;
-      ok = pad_frame ? 0 : 1;
+  float tcount = 0.f;
+  for (int32_t t = r; t < g.kT; t += G) {
+    const int32_t s = taps.src[t];
+    if (s == -1) continue;  // start padding: ignored by max, adds 0 to a sum
+    float ev, ok;
+    if (s == -2) {          // the arriving frame
+      ev = val;
+      ok = pad_frame ? 0.f : 1.f;
     } else {
-      e = fifo[int64_t(s) * fifo_slot + idx];
-      ok = valid[s] != 0.f ? 1 : 0;
+      ev = fifo[int64_t(s) * fifo_slot + idx];
+      ok = valid[s];
     }
-    acc = is_max ? fmaxf(acc, e) : acc + e;
+    acc = is_max ? fmaxf(acc, ev) : acc + ev;
     tcount += ok;
   }
+  if (is_max) {
+    acc = group_max<G>(acc);
+  } else {
+    acc = group_sum<G>(acc);
+    tcount = group_sum<G>(tcount);
+  }
+  if (r != 0) return;
   float out;
   if (is_max) {
     out = acc;
   } else {
-    const int32_t div = g.count_include_pad ? g.kT * g.kH * g.kW : tcount * scount;
-    out = div > 0 ? acc / float(div) : 0.f;
+    // spatial positions inside the frame (count_include_pad = 0 divisor)
+    int32_t vh = 0, vw = 0;
+    for (int32_t u = 0; u < g.kH; ++u) {
+      const int32_t hi = i * g.sH + u * g.dH - g.pH;
+      vh += (hi >= 0 && hi < g.H) ? 1 : 0;
+    }
+    for (int32_t v = 0; v < g.kW; ++v) {
+      const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+      vw += (wi >= 0 && wi < g.W) ? 1 : 0;
+    }
+    const float div = g.count_include_pad ? float(g.kT * kHW) : tcount * float(vh * vw);
+    out = div > 0.f ? acc / div : 0.f;
   }
   y[int64_t(bc) * y_bc + p] = from_f32<T>(out);
 }
@@ -127,18 +174,29 @@ __global__ void pool_header_kernel(StateHeader h, StateHeader* dst) {
   if (threadIdx.x == 0 && blockIdx.x == 0) *dst = h;
 }
 
-template <typename T>
-hipError_t pool_step_t(const PoolGeom& g, const PoolLayout& L, char* state, const StepIO& io,
+template <typename T, int G>
+hipError_t pool_step_g(const PoolGeom& g, const PoolLayout& L, char* state, const StepIO& io,
                        const co_pool_plan& plan, bool update, bool pad, hipStream_t s) {
   PoolTaps taps;
   for (int j = 0; j < CO_MAX_TAPS; ++j) taps.src[j] = plan.src[j];
   float* fifo = reinterpret_cast<float*>(state + L.fifo);
   float* valid = reinterpret_cast<float*>(state + L.valid);
-  hipLaunchKernelGGL(pool_step_kernel<T>, dim3(grid_for(g.out_frame_elems())), dim3(kBlock), 0,
-                     s, g, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
-                     fifo, L.fifo_slot_elems, valid, plan.write_slot, update ? 1 : 0, plan.emit,
-                     pad ? 1 : 0, taps);
+  hipLaunchKernelGGL((pool_step_kernel<T, G>), dim3(grid_for(g.out_frame_elems() * G)),
+                     dim3(kBlock), 0, s, g, static_cast<const T*>(io.x), io.x_bc,
+                     static_cast<T*>(io.y), io.y_bc, fifo, L.fifo_slot_elems, valid,
+                     plan.write_slot, update ? 1 : 0, plan.emit, pad ? 1 : 0, taps);
   return hipGetLastError();
+}
+
+// Lanes per output element: enough to cover the spatial window (and the
+// temporal taps) in about one load each.
+template <typename T>
+hipError_t pool_step_t(const PoolGeom& g, const PoolLayout& L, char* state, const StepIO& io,
+                       const co_pool_plan& plan, bool update, bool pad, hipStream_t s) {
+  const int work = std::max(g.kH * g.kW, g.kT);
+  if (work > 16) return pool_step_g<T, 64>(g, L, state, io, plan, update, pad, s);
+  if (work > 4) return pool_step_g<T, 16>(g, L, state, io, plan, update, pad, s);
+  return pool_step_g<T, 4>(g, L, state, io, plan, update, pad, s);
 }
 
 }  // namespace
