@@ -55,16 +55,52 @@ def parse():
 
 
 def copy_calibration(mib, steps):
-    """A plain device-to-device copy of a known size, for scaling FETCH_SIZE and
-    WRITE_SIZE counter readings to bytes."""
+    """Plain device copies of a known size -- the runtime's copy kernel
+    (Tensor.copy_) and an elementwise kernel (torch.neg) -- for scaling
+    FETCH_SIZE and WRITE_SIZE counter readings to bytes."""
     import torch
     n = int(mib * 1024 * 1024 / 4)
     a = torch.randn(n, device="cuda")
     b = torch.empty_like(a)
     for _ in range(steps):
         b.copy_(a)
+    for _ in range(steps):
+        torch.neg(a, out=b)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes": n * 4, "steps": steps}))
+    print(json.dumps({"copy_bytes": n * 4, "steps": steps, "kernels": ["copy_", "neg"]}))
+
+
+def sources_digest():
+    """sha256 prefix over the library's kernel sources (sorted file names and
+    contents): the key under which measured counters stay valid."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2204_03418_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        h.update(name.encode())
+        with open(os.path.join(d, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the workload's dominant kernel, from the
+    rocprofv3 FETCH_SIZE / WRITE_SIZE passes summarised in profiles/traffic.txt
+    (already scaled by the plain-copy calibration); None when the kernel
+    sources changed after those counters were taken, or none were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    try:
+        with open(path) as f:
+            lines = [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+    except OSError:
+        return None
+    kv = {ln[0]: ln[1] for ln in lines if len(ln) == 2}
+    if kv.get("sources") != sources_digest():
+        return None
+    for ln in lines:
+        if len(ln) == 5 and ln[0] == workload:
+            return int(ln[4])
+    return None
 
 
 def per_step_work(c, Ho, Wo):
@@ -188,6 +224,7 @@ def main():
         achieved = nbytes / (kern_ms / 1e3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": None}
+    roof["traffic"] = measured_traffic(args.workload)
     roof.update({"kernel": f"conv step ({co.algo})", "kernel_avg_us": round(kern_ms * 1e3, 3),
                  "flops_per_launch": flops, "bytes_per_launch": nbytes})
 
