@@ -77,6 +77,8 @@ typedef int32_t co_status;
 #define CO_ALGO_DIRECT     1   /* generic direct kernel, any shape */
 #define CO_ALGO_GEMM       2   /* implicit GEMM on MFMA (groups = 1) */
 #define CO_ALGO_DEPTHWISE  3   /* depthwise stencil (groups = C_in = C_out) */
+#define CO_ALGO_GEMM_REG   4   /* implicit GEMM on MFMA with register operands
+                                  (groups = 1, small kH*kW*C_in) */
 
 #define CO_POOL_AVG  0
 #define CO_POOL_MAX  1

@@ -262,6 +262,7 @@ const char* co_conv_algo_name(const co_conv_handle* h) {
   switch (h->g.algo) {
     case CO_ALGO_DEPTHWISE: return "depthwise";
     case CO_ALGO_GEMM: return h->g.dtype == CO_BF16 ? "gemm_bf16" : "gemm_f32";
+    case CO_ALGO_GEMM_REG: return h->g.dtype == CO_BF16 ? "gemm_reg_bf16" : "gemm_reg_f32";
     default: return "direct";
   }
 }

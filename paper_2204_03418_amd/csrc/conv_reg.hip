@@ -1,0 +1,450 @@
+// Register-operand implicit-GEMM continual convolution step (groups = 1,
+// small reduction depth K = kH*kW*C_in).
+//
+// The per-step contraction is the same GEMM as in the LDS-tiled kernel
+// (m = output pixel of a stream, n = (temporal tap, output channel),
+// k = (spatial tap, input channel)), and the same fused ring epilogue follows
+// it (section 3.1: the arriving frame's contribution to every future output
+// is computed at once and kept as a partial sum).  For layers whose K is
+// small, staging tiles through LDS costs more than it saves: the step is a
+// few hundred cycles of matrix work behind several dependent trips to
+// memory.  Here one wave owns a tile of 16 output pixels x 16*WN columns and
+// keeps every k-step's operands in registers:
+//
+//   * input pixels are gathered straight from the NCHW frame with buffer
+//     loads, one value (fp32) or eight channels (bf16) per lane and k-step,
+//     in the lane order of the matrix instruction; taps outside the frame
+//     read an out-of-range offset, which returns zero, so every load issues
+//     at once;
+//   * weights were packed at init as 16-byte units in the exact lane order
+//     of the instruction, so each lane fetches them with 16-byte loads;
+//   * the ring partial sums the tile continues are requested with them.
+//
+// The wave then runs its MFMAs back to back onto the seeded accumulators and
+// stores the ring / output.  No LDS and no barrier: one round trip to memory
+// plus the matrix work.  Each lane computes its own input address, so any
+// stride, dilation and spatial padding is handled.
+#include <type_traits>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace coinf {
+
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+constexpr int kRegWaves = 4;  // independent waves per workgroup
+
+constexpr int kRegMaxTaps = 9;  // largest kH*kW an instantiation holds
+
+struct RegArgs {
+  int32_t M, N, So;
+  int32_t m_frags, nf0, n_grps;  // column groups of WN fragments from fragment nf0
+  int32_t blocks_per_xcd;
+  int32_t ntaps, CS, CSU;        // spatial taps, channel blocks, weight units per tap
+  int32_t dh[kRegMaxTaps], dw[kRegMaxTaps];  // input row / column offset of each tap
+  int32_t x_bytes, w_bytes;
+  int32_t ring_slot, ring_bytes;  // floats between ring slots; bytes of all slots
+  int32_t y_bc, y_bytes;          // y plane stride (elements); bytes of y
+};
+
+// Per-tap action and ring slot as one dword each (action | slot << 8), so
+// the kernel reads them with scalar loads (there is no scalar byte load).
+struct RegTaps {
+  int32_t as[CO_MAX_TAPS];
+};
+
+// 32-bit byte offset of element `e` of a T buffer, or an out-of-range offset
+// (the load returns zero) when !ok.
+template <typename T>
+__device__ __forceinline__ int elem_off(uint32_t e, bool ok) {
+  return ok ? int(e * uint32_t(sizeof(T))) : kOutOfRange;
+}
+
+// VEC: M % 4 == 0 (whole 16-byte ring stores).  EXACT: the layer has exactly
+// CSMAX channel blocks and C_in is a multiple of the block width, so no
+// k-step is idle and no lane reads past C_in (no per-k-step selects).
+template <typename T, int WN, int TAPS, int CSMAX, bool VEC, bool EXACT>
+__global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
+    ConvGeom g, RegArgs ra, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
+    int64_t y_bc, const uint4* __restrict__ wp, const float* __restrict__ bias,
+    float* __restrict__ ring, RegTaps tt) {
+  constexpr bool kBF = sizeof(T) == 2;
+  constexpr int CL = kBF ? 8 : 1;  // input channels per lane and k-step
+  constexpr int CKS = 4 * CL;      // input channels per k-step (channel block)
+  // 16-byte weight units per tap: fp32 packs four channel blocks per unit
+  constexpr int CSUMAX = kBF ? CSMAX : (CSMAX + 3) / 4;
+  const int lane = int(threadIdx.x) & 63;
+  // wave index as a scalar, so everything derived from the tile stays uniform
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  const int lrow = lane & 15, lgrp = lane >> 4;
+
+  // XCD-aware numbering: blocks are dealt to the 8 XCDs round-robin, so
+  // consecutive logical blocks (neighbouring tiles) share an XCD's L2.
+  const int bid = int(blockIdx.x);
+  const int lb = (bid & 7) * ra.blocks_per_xcd + (bid >> 3);
+  const int tile = lb * kRegWaves + wave;
+  if (tile >= ra.m_frags * ra.n_grps) return;  // whole waves; no barriers follow
+  const int mf = tile / ra.n_grps;
+  const int nfb = ra.nf0 + (tile - mf * ra.n_grps) * WN;
+
+  // ---- epilogue data ------------------------------------------------------
+  // lane (lrow, lgrp) of fragment f holds column n = (nfb+f)*16 + lrow and
+  // the four consecutive pixels mf*16 + lgrp*4 .. +3 of the result.  The
+  // taps a fragment spans are read with wave-uniform (scalar) loads, so the
+  // ring reads issue in the same batch as the operand gathers.
+  int e_act[WN], e_o[WN], e_off[WN];  // action, channel, ring element offset
+  float e_bias[WN];
+  const __amdgpu_buffer_rsrc_t br = make_rsrc(bias, g.Cout * 4);
+  // column n = t*C_out + o: decode the wave's first column once, then step 16
+  // columns per fragment (C_out >= 16, so o wraps at most once per step)
+  const int n0 = nfb * 16;
+  int tq = n0 / g.Cout, oq = n0 - tq * g.Cout;  // wave-uniform: fragment f's first column
+#pragma unroll
+  for (int f = 0; f < WN; ++f) {
+    const int n = (nfb + f) * 16 + lrow;
+    int t = tq, o = oq + lrow;
+    if (o >= g.Cout) {  // per lane: the fragment crosses into the next tap
+      o -= g.Cout;
+      ++t;
+    }
+    // the fragment spans taps tq and tq + 1 at most: two scalar reads
+    const int a0 = tt.as[min(tq, g.kT - 1)], a1 = tt.as[min(tq + 1, g.kT - 1)];
+    const int as = t == tq ? a0 : a1;
+    const bool in = n < ra.N;
+    e_act[f] = in ? (as & 0xff) : CO_TAP_NONE;
+    o = in ? o : 0;
+    e_o[f] = o;
+    e_off[f] = (as >> 8) * ra.ring_slot + o * ra.M;
+    e_bias[f] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(br, o * 4, 0, 0));
+    oq += 16;
+    if (oq >= g.Cout) {  // uniform
+      oq -= g.Cout;
+      ++tq;
+    }
+  }
+  const int P0 = mf * 16 + lgrp * 4;
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(ring, ra.ring_bytes);
+
+  // ---- one batch of loads: ring partial sums, bias, then the operands ----
+  // The ring holds a partial sum for taps that add to it (ACC, EMIT); other
+  // taps read an out-of-range offset (zero).  The values are added after the
+  // matrix work, so no instruction waits for them before the last MFMA.
+  v4f prev[WN];
+#pragma unroll
+  for (int f = 0; f < WN; ++f) {
+    // one 16-byte read per lane (slots end with four floats of padding, so a
+    // ragged frame's last pixels stay in range; pixels past M are not stored)
+    const bool rd = ((e_act[f] == CO_TAP_ACC) | (e_act[f] == CO_TAP_EMIT)) & (P0 < ra.M);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(
+        rr, rd ? (e_off[f] + P0) * 4 : kOutOfRange, 0, 0);
+    prev[f] = v4f{__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
+                  __uint_as_float(v[3])};
+  }
+
+  // ---- operand gathers --------------------------------------------------
+  // k-step (tap tp, channel block cb): lane (lrow, lgrp) supplies row m =
+  // pixel lrow and channel(s) cb*CKS + lgrp*CL (+ 0..CL-1).  The tap's
+  // per-lane offset and frame test are computed once per tap; a k-step adds
+  // a uniform channel-block offset.  Taps outside the frame and channels past
+  // C_in read an out-of-range offset (zero), so every load is in bounds.
+  const int P = mf * 16 + lrow;
+  const bool pvalid = P < ra.M;
+  const int Pc = pvalid ? P : 0;
+  const int b = Pc / ra.So, p = Pc - b * ra.So;
+  const int i = p / g.Wo, j = p - i * g.Wo;
+  const int hb = i * g.sH - g.pH, wb = j * g.sW - g.pW;
+  const int lane_c = lgrp * CL;
+  constexpr uint32_t esz = sizeof(T);
+  const uint32_t plane_b = uint32_t(x_bc) * esz;
+  const uint32_t lane_b = (uint32_t(b) * uint32_t(g.Cin) + uint32_t(lane_c)) * plane_b;
+  // channels of this lane inside the last channel block (it may be partial)
+  const int nv_last = min(max(g.Cin - ((ra.CS - 1) * CKS + lane_c), 0), CL);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ra.x_bytes);
+
+  using AReg = typename std::conditional<kBF, uint4, float>::type;
+  AReg areg[TAPS][CSMAX];
+#pragma unroll
+  for (int tp = 0; tp < TAPS; ++tp) {
+    // per-lane offset of the tap's pixel in channel block 0, or out of range;
+    // a channel block adds a wave-uniform offset through the instruction's
+    // scalar operand.  In the last block lanes past C_in read out of range.
+    const int hi = hb + ra.dh[tp], wi = wb + ra.dw[tp];
+    const bool ok = (tp < ra.ntaps) & pvalid & (unsigned(hi) < unsigned(g.H)) &
+                    (unsigned(wi) < unsigned(g.W));
+    const int vt = ok ? int(lane_b + (uint32_t(hi) * uint32_t(g.W) + uint32_t(wi)) * esz)
+                      : kOutOfRange;
+    if constexpr (kBF) {
+      int vlast[8];  // last block: element e exists iff e < nv_last
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        vlast[e] = ok & (e < nv_last) ? vt + int(uint32_t(e) * plane_b) : kOutOfRange;
+#pragma unroll
+      for (int cb = 0; cb < CSMAX; ++cb) {
+        const bool live = EXACT || cb < ra.CS;  // wave-uniform
+        const bool last = !EXACT && cb == ra.CS - 1;
+        const int sb = int(uint32_t(cb * CKS) * plane_b);
+        uint32_t r[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int v = !live ? kOutOfRange : last ? vlast[e] : vt;
+          const int so = last ? sb : sb + int(uint32_t(e) * plane_b);
+          r[e] = __builtin_amdgcn_raw_buffer_load_b16(xr, v, so, 0);
+        }
+        areg[tp][cb] = make_uint4(r[0] | (r[1] << 16), r[2] | (r[3] << 16),
+                                  r[4] | (r[5] << 16), r[6] | (r[7] << 16));
+      }
+    } else {
+      const int vl = nv_last > 0 ? vt : kOutOfRange;
+#pragma unroll
+      for (int cb = 0; cb < CSMAX; ++cb) {
+        const bool live = EXACT || cb < ra.CS;  // wave-uniform
+        const bool last = !EXACT && cb == ra.CS - 1;
+        const int v = !live ? kOutOfRange : last ? vl : vt;
+        areg[tp][cb] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+            xr, v, int(uint32_t(cb * CKS) * plane_b), 0));
+      }
+    }
+  }
+
+  // weights: unit (fragment nf, tap tp, unit cq) of this lane at
+  // (((nf * ntaps + tp) * CSU + cq) * 64 + lane) * 16 bytes
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(wp, ra.w_bytes);
+  uint4 breg[WN][TAPS][CSUMAX];
+#pragma unroll
+  for (int f = 0; f < WN; ++f)
+#pragma unroll
+    for (int tp = 0; tp < TAPS; ++tp)
+#pragma unroll
+      for (int cq = 0; cq < CSUMAX; ++cq) {
+        const bool okw = (tp < ra.ntaps) & (cq < ra.CSU);
+        const int off = ((((nfb + f) * ra.ntaps + tp) * ra.CSU + cq) << 10) + lane * 16;
+        const auto w4 =
+            __builtin_amdgcn_raw_buffer_load_b128(wr, okw ? off : kOutOfRange, 0, 0);
+        breg[f][tp][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+
+  // ---- matrix work --------------------------------------------------------
+  // Straight-line MFMAs over every k-step the instantiation holds (k-steps
+  // past the layer's taps / channel blocks multiply zeros): with no branch
+  // here the loads above stay one batch, and each instruction waits only for
+  // its own operands.
+  __builtin_amdgcn_sched_barrier(0);
+  v4f acc[WN];
+#pragma unroll
+  for (int f = 0; f < WN; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int tp = 0; tp < TAPS; ++tp) {
+#pragma unroll
+    for (int cb = 0; cb < CSMAX; ++cb) {
+#pragma unroll
+      for (int f = 0; f < WN; ++f) {
+        if constexpr (kBF) {
+          acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(v8bf, areg[tp][cb]), __builtin_bit_cast(v8bf, breg[f][tp][cb]),
+              acc[f], 0, 0, 0);
+        } else {
+          const uint4 u4 = breg[f][tp][cb / 4];
+          const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
+          acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[tp][cb], __uint_as_float(bw), acc[f],
+                                                        0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // ---- fused ring epilogue (branch-free) ----------------------------------
+  // Stores go through buffer resources; a lane that must not store uses an
+  // out-of-range offset, which the hardware drops.  With no branch after the
+  // tile test the compiler cannot move any load of the batch down here.
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ra.y_bytes);
+  constexpr int yesz = int(sizeof(T));
+  const int pb = P0 / ra.So, pp = P0 - pb * ra.So;  // frame and pixel of the lane's first row
+#pragma unroll
+  for (int f = 0; f < WN; ++f) {
+    const int act = e_act[f];
+    const bool to_ring = (act == CO_TAP_START) | (act == CO_TAP_ACC);
+    const bool to_y = (act == CO_TAP_EMIT) | (act == CO_TAP_EMIT_FRESH);
+    const v4f v = acc[f] + prev[f];
+    if constexpr (VEC) {  // M % 4 == 0: a lane's four pixels are all valid or none
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(v4u, v), rr, to_ring & (P0 < ra.M) ? (e_off[f] + P0) * 4 : kOutOfRange,
+          0, 0);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        __builtin_amdgcn_raw_buffer_store_b32(
+            __float_as_uint(v[r]), rr,
+            to_ring & (P0 + r < ra.M) ? (e_off[f] + P0 + r) * 4 : kOutOfRange, 0, 0);
+    }
+    const int o = e_o[f];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int bq = pb, pq = pp + r;
+      if (ra.So >= 4) {  // uniform: four consecutive pixels cross at most one frame edge
+        const bool wrap = pq >= ra.So;
+        bq += wrap ? 1 : 0;
+        pq -= wrap ? ra.So : 0;
+      } else {
+        bq = (P0 + r) / ra.So;
+        pq = P0 + r - bq * ra.So;
+      }
+      const int yo = ((bq * g.Cout + o) * ra.y_bc + pq) * yesz;
+      const int off = to_y & (P0 + r < ra.M) ? yo : kOutOfRange;
+      const float val = v[r] + e_bias[f];
+      if constexpr (sizeof(T) == 2)
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)), yr, off,
+                                              0, 0);
+      else
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, off, 0, 0);
+    }
+  }
+}
+
+// Pack W (C_out, C_in, kT, kH, kW) as [fragment][tap][unit][lane] 16-byte
+// units, in the order the kernel loads them: an fp32 unit holds channel
+// blocks 4cq .. 4cq+3 of one tap (one channel per lane each), a bf16 unit
+// holds channel block cq (eight channels per lane); lane (lrow, lgrp) holds
+// column n = nf*16 + lrow and the channels the same lane gathers from x.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void pack_reg_kernel(ConvGeom g, RegConfig c,
+                                                          const T* __restrict__ w,
+                                                          uint4* __restrict__ out) {
+  constexpr bool kBF = sizeof(T) == 2;
+  const int ntaps = g.kH * g.kW;
+  const int64_t total = int64_t(c.n_frags) * c.U * 64;
+  const int64_t idx = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (idx >= total) return;
+  const int lane = int(idx % 64);
+  int64_t rest = idx / 64;
+  const int cq = int(rest % c.CSU);
+  rest /= c.CSU;
+  const int tp = int(rest % ntaps);
+  const int nf = int(rest / ntaps);
+  const int n = nf * 16 + (lane & 15), lgrp = lane >> 4;
+  const int t = n / g.Cout, o = n - t * g.Cout;
+  const int u = tp / g.kW, v = tp - u * g.kW;
+  const bool ncol = n < g.kT * g.Cout;
+  auto weight = [&](int cb, int c_in) -> T {
+    if (!ncol || cb >= c.CS || c_in >= g.Cin) return T(0);
+    return w[(((int64_t(o) * g.Cin + c_in) * g.kT + t) * g.kH + u) * g.kW + v];
+  };
+  uint32_t word[4] = {0u, 0u, 0u, 0u};
+  if constexpr (kBF) {
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const uint32_t lo = weight(cq, cq * 32 + lgrp * 8 + e);
+      const uint32_t hi = weight(cq, cq * 32 + lgrp * 8 + e + 1);
+      word[e / 2] = lo | (hi << 16);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int cb = 4 * cq + e;
+      word[e] = __float_as_uint(weight(cb, cb * 4 + lgrp));
+    }
+  }
+  out[idx] = make_uint4(word[0], word[1], word[2], word[3]);
+}
+
+template <typename T, int WN, int TAPS, int CSMAX>
+hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L, char* state,
+                      const StepIO& io, const co_step_plan& plan, hipStream_t s) {
+  RegTaps tt;
+  int t_lo = CO_MAX_TAPS, t_hi = -1;
+  for (int t = 0; t < CO_MAX_TAPS; ++t) {
+    const int sl = plan.slot[t] < 0 ? 0 : plan.slot[t];
+    tt.as[t] = int32_t(plan.action[t]) | (sl << 8);
+    if (plan.action[t] != CO_TAP_NONE) {
+      t_lo = t < t_lo ? t : t_lo;
+      t_hi = t;
+    }
+  }
+  if (t_hi < 0) return hipSuccess;
+  RegArgs ra;
+  ra.M = int32_t(int64_t(g.B) * g.So());
+  ra.N = g.kT * g.Cout;
+  ra.So = int32_t(g.So());
+  ra.m_frags = c.m_frags;
+  // only the column fragments holding active taps
+  ra.nf0 = (t_lo * g.Cout) / 16;
+  const int nf_end = int(ceil_div(int64_t(t_hi + 1) * g.Cout, 16));
+  ra.n_grps = int32_t(ceil_div(nf_end - ra.nf0, WN));
+  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegWaves);
+  ra.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
+  ra.ntaps = g.kH * g.kW;
+  ra.CS = c.CS;
+  ra.CSU = c.CSU;
+  for (int tp = 0; tp < kRegMaxTaps; ++tp) {
+    const int u = tp < ra.ntaps ? tp / g.kW : 0, v = tp < ra.ntaps ? tp % g.kW : 0;
+    ra.dh[tp] = u * g.dH;
+    ra.dw[tp] = v * g.dW;
+  }
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  ra.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz);
+  ra.w_bytes = int32_t(L.weight_bytes);
+  ra.ring_slot = int32_t(L.ring_slot_elems);
+  ra.y_bc = int32_t(io.y_bc);
+  ra.y_bytes = int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz);
+  ra.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
+  const bool exact = c.CS == CSMAX && g.Cin % c.CKS == 0;
+  auto kern = ra.M % 4 == 0
+                  ? (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, true, true>
+                           : conv_step_reg_kernel<T, WN, TAPS, CSMAX, true, false>)
+                  : (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, false, true>
+                           : conv_step_reg_kernel<T, WN, TAPS, CSMAX, false, false>);
+  hipLaunchKernelGGL(kern, dim3(unsigned(8 * ra.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g,
+                     ra, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
+                     reinterpret_cast<const uint4*>(state + L.weight),
+                     reinterpret_cast<const float*>(state + L.bias),
+                     reinterpret_cast<float*>(state + L.ring), tt);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* state,
+                                const StepIO& io, const co_step_plan& plan, hipStream_t s) {
+  RegConfig c;
+  if (!reg_config(g, g.cfg, &c)) return hipErrorInvalidValue;
+  // 32-bit buffer offsets: input extent and packed weights below 2^31 bytes
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  if (((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz >= (int64_t(1) << 31) ||
+      L.weight_bytes >= (int64_t(1) << 30) || int64_t(c.m_frags) * c.n_frags >= (int64_t(1) << 30) ||
+      int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31) ||
+      ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31))
+    return launch_conv_step_direct(g, L, state, io, plan, false, s);
+  switch (c.id) {
+    case 0: return reg_launch<float, 4, 1, 16>(g, c, L, state, io, plan, s);
+    case 1: return reg_launch<float, 2, 1, 32>(g, c, L, state, io, plan, s);
+    case 2: return reg_launch<float, 1, 9, 6>(g, c, L, state, io, plan, s);
+    case 3: return reg_launch<float, 2, 9, 3>(g, c, L, state, io, plan, s);
+    case 4: return reg_launch<bf16_t, 4, 1, 2>(g, c, L, state, io, plan, s);
+    case 5: return reg_launch<bf16_t, 2, 1, 4>(g, c, L, state, io, plan, s);
+    case 6: return reg_launch<bf16_t, 1, 1, 16>(g, c, L, state, io, plan, s);
+    case 7: return reg_launch<bf16_t, 1, 9, 2>(g, c, L, state, io, plan, s);
+    case 8: return reg_launch<bf16_t, 2, 9, 1>(g, c, L, state, io, plan, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,
+                           const void* weight, hipStream_t s) {
+  RegConfig c;
+  if (!reg_config(g, g.cfg, &c)) return hipErrorInvalidValue;
+  const int64_t total = int64_t(c.n_frags) * c.U * 64;
+  uint4* out = reinterpret_cast<uint4*>(state + L.weight);
+  if (g.dtype == CO_BF16)
+    hipLaunchKernelGGL(pack_reg_kernel<bf16_t>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
+                       static_cast<const bf16_t*>(weight), out);
+  else
+    hipLaunchKernelGGL(pack_reg_kernel<float>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
+                       static_cast<const float*>(weight), out);
+  return hipGetLastError();
+}
+
+}  // namespace coinf

@@ -146,6 +146,87 @@ int gemm_pick(const ConvGeom& g) {
 
 bool gemm_supported(const ConvGeom& g) { return gemm_pick(g) >= 0; }
 
+namespace {
+
+struct RegShape {
+  int32_t dtype, WN, TAPS, CSMAX;
+};
+
+// Instantiated register-GEMM shapes (the kernel file instantiates the same
+// table): spatial taps x channel blocks held per lane (the matrix work covers
+// all of them, so shapes are sized to common layers: 3x3 taps with up to 24
+// fp32 channels, 1x1 with up to 64 or 128), operand registers per lane near
+// or below 128 in every shape.
+constexpr RegShape kRegShapes[kRegConfigs] = {
+    {CO_F32, 4, 1, 16}, {CO_F32, 2, 1, 32}, {CO_F32, 1, 9, 6}, {CO_F32, 2, 9, 3},
+    {CO_BF16, 4, 1, 2}, {CO_BF16, 2, 1, 4},  {CO_BF16, 1, 1, 16}, {CO_BF16, 1, 9, 2},
+    {CO_BF16, 2, 9, 1},
+};
+
+}  // namespace
+
+bool reg_config(const ConvGeom& g, int id, RegConfig* c) {
+  // C_out >= 16 keeps every 16-column fragment within two temporal taps
+  if (id < 0 || id >= kRegConfigs || g.G != 1 || g.Cout < 16) return false;
+  const RegShape& s = kRegShapes[id];
+  if (s.dtype != g.dtype) return false;
+  RegConfig r{};
+  r.id = id;
+  r.dtype = s.dtype;
+  r.WN = s.WN;
+  r.TAPS = s.TAPS;
+  r.CSMAX = s.CSMAX;
+  r.CKS = g.dtype == CO_BF16 ? 32 : 4;
+  r.CS = int32_t(ceil_div(g.Cin, r.CKS));
+  const int taps = g.kH * g.kW;
+  if (taps > s.TAPS || r.CS > s.CSMAX) return false;
+  r.CSU = g.dtype == CO_BF16 ? r.CS : int32_t(ceil_div(r.CS, 4));
+  r.KS = taps * r.CS;
+  r.U = taps * r.CSU;
+  r.m_frags = int32_t(ceil_div(int64_t(g.B) * g.So(), 16));
+  r.n_frags = int32_t(ceil_div(int64_t(g.kT) * g.Cout, 16));
+  *c = r;
+  return true;
+}
+
+int reg_pick(const ConvGeom& g) {
+  // Prefer the widest wave tile (fewer re-reads of the input pixels) that
+  // still gives every SIMD a wave; among equal widths the smallest register
+  // footprint (taps x channel blocks).
+  int best = -1;
+  int64_t best_waves = 0;
+  int best_wn = 0, best_k = 0;
+  for (int id = 0; id < kRegConfigs; ++id) {
+    RegConfig c;
+    if (!reg_config(g, id, &c)) continue;
+    const int64_t waves = int64_t(c.m_frags) * ceil_div(c.n_frags, c.WN);
+    const bool fills = waves >= 1024;
+    bool better;
+    if (best < 0) {
+      better = true;
+    } else {
+      const bool best_fills = best_waves >= 1024;
+      if (fills != best_fills)
+        better = fills;
+      else if (fills && c.WN != best_wn)
+        better = c.WN > best_wn;
+      else if (!fills && waves != best_waves)
+        better = waves > best_waves;
+      else
+        better = c.TAPS * c.CSMAX < best_k;
+    }
+    if (better) {
+      best = id;
+      best_waves = waves;
+      best_wn = c.WN;
+      best_k = c.TAPS * c.CSMAX;
+    }
+  }
+  return best;
+}
+
+bool reg_supported(const ConvGeom& g) { return reg_pick(g) >= 0; }
+
 int64_t packed_weight_bytes(const ConvGeom& g) {
   const int64_t n = int64_t(g.Cout) * g.Cg * g.kT * g.kH * g.kW;
   if (g.algo == CO_ALGO_GEMM) {
@@ -154,6 +235,12 @@ int64_t packed_weight_bytes(const ConvGeom& g) {
     if (!gemm_config(g, g.cfg, &c)) return 0;
     return int64_t(c.n_tiles) * c.n_chunks * g.kH * g.kW * c.N_WG * c.CK *
            (g.dtype == CO_BF16 ? 2 : 4);
+  }
+  if (g.algo == CO_ALGO_GEMM_REG) {
+    // [fragment][unit][lane] of 16 bytes, in the matrix instruction's order
+    RegConfig c;
+    if (!reg_config(g, g.cfg, &c)) return 0;
+    return int64_t(c.n_frags) * c.U * 64 * 16;
   }
   return n * 4;  // float32, PyTorch order
 }
@@ -166,7 +253,7 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
   if (d.in_channels % d.groups || d.out_channels % d.groups) return CO_EINVAL;
   if (d.dtype != CO_F32 && d.dtype != CO_BF16) return CO_EINVAL;
   if (d.has_bias != 0 && d.has_bias != 1) return CO_EINVAL;
-  if (d.algo < CO_ALGO_AUTO || d.algo > CO_ALGO_DEPTHWISE) return CO_EINVAL;
+  if (d.algo < CO_ALGO_AUTO || d.algo > CO_ALGO_GEMM_REG) return CO_EINVAL;
   for (int a = 0; a < 3; ++a) {
     if (d.kernel[a] < 1 || d.stride[a] < 1 || d.dilation[a] < 1 || d.padding[a] < 0)
       return CO_EINVAL;
@@ -227,16 +314,24 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
   // whose single pass costs less than staging tiles through LDS
   const double macs = double(r.B) * r.So() * r.Cout * r.kT * r.Cg * r.kH * r.kW;
   if (algo == CO_ALGO_AUTO) {
+    // depthwise stencil; else matrix cores, with operands in registers when
+    // the reduction is shallow enough (one memory round trip per step) and
+    // staged through LDS otherwise; tiny layers on the direct kernel
     if (depthwise_supported(r))
       algo = CO_ALGO_DEPTHWISE;
+    else if (reg_supported(r))
+      algo = CO_ALGO_GEMM_REG;
     else
       algo = (macs >= 1.0e5 && gemm_supported(r)) ? CO_ALGO_GEMM : CO_ALGO_DIRECT;
   } else if (algo == CO_ALGO_DEPTHWISE) {
     if (!depthwise_supported(r)) return CO_ENOTSUP;
   } else if (algo == CO_ALGO_GEMM) {
     if (!gemm_supported(r)) return CO_ENOTSUP;
+  } else if (algo == CO_ALGO_GEMM_REG) {
+    if (!reg_supported(r)) return CO_ENOTSUP;
   }
   if (algo == CO_ALGO_GEMM) r.cfg = gemm_pick(r);
+  if (algo == CO_ALGO_GEMM_REG) r.cfg = reg_pick(r);
   r.algo = algo;
   *g = r;
   return CO_OK;
@@ -249,7 +344,9 @@ ConvLayout conv_layout(const ConvGeom& g) {
   L.weight = L.bias + round_up(int64_t(g.Cout) * 4, kAlign);
   L.weight_bytes = packed_weight_bytes(g);
   L.ring = L.weight + round_up(L.weight_bytes, kAlign);
-  L.ring_slot_elems = round_up(g.out_frame_elems(), kAlign / 4);
+  // four floats past the frame keep a 16-byte read of the last four pixels
+  // of a ragged frame inside the slot
+  L.ring_slot_elems = round_up(g.out_frame_elems() + 4, kAlign / 4);
   L.total = L.ring + int64_t(g.R) * L.ring_slot_elems * 4;
   return L;
 }

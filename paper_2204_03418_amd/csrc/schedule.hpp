@@ -33,7 +33,7 @@ struct ConvGeom {
   int32_t dT, dH, dW;
   int32_t f, d, R;          // receptive field, delay, ring slots
   int32_t has_bias, dtype, algo;
-  int32_t cfg;              // implicit-GEMM tile configuration (-1: none)
+  int32_t cfg;              // GEMM / register-GEMM instantiation (-1: none)
   int64_t S() const { return int64_t(H) * W; }
   int64_t So() const { return int64_t(Ho) * Wo; }
   int64_t out_frame_elems() const { return int64_t(B) * Cout * So(); }
@@ -58,6 +58,28 @@ struct GemmConfig {
   int64_t b_units;     // 16-byte units of one B stage in LDS
   int64_t lds_bytes;   // 2 * (a_units + b_units) * 16
 };
+
+// Register-operand implicit GEMM (small K): one wave per 16-pixel x
+// 16*WN-column tile holds every k-step's operands in registers.  A k-step is
+// one spatial tap (u, v) and one block of CKS input channels: 4 for fp32
+// (v_mfma_f32_16x16x4_f32, one channel per lane) and 32 for bf16
+// (v_mfma_f32_16x16x32_bf16, eight channels per lane).
+struct RegConfig {
+  int32_t id;       // kernel instantiation
+  int32_t dtype;    // CO_F32 | CO_BF16
+  int32_t WN;       // 16-column fragments per wave
+  int32_t TAPS;     // spatial taps (kH*kW) the instantiation holds
+  int32_t CSMAX;    // channel blocks per tap the instantiation holds
+  int32_t CKS;      // input channels per k-step (channel block)
+  int32_t CS;       // channel blocks per spatial tap, ceil(C_in / CKS)
+  int32_t CSU;      // 16-byte weight units per lane, fragment and tap
+  int32_t KS;       // k-steps: kH * kW * CS
+  int32_t U;        // 16-byte weight units per lane and fragment: kH * kW * CSU
+  int32_t m_frags;  // 16-pixel fragments, ceil(B*Ho*Wo / 16)
+  int32_t n_frags;  // 16-column fragments, ceil(kT*C_out / 16)
+};
+
+constexpr int kRegConfigs = 9;
 
 constexpr int kGemmConfigs = 4;
 constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)
@@ -130,6 +152,12 @@ int64_t pool_emissions(const PoolGeom& g, int64_t n, int64_t count);
 bool gemm_config(const ConvGeom& g, int id, GemmConfig* c);
 // The configuration the library picks for a geometry (-1: none fits).
 int gemm_pick(const ConvGeom& g);
+
+// Register-operand GEMM: derived sizes of instantiation `id` (false when it
+// does not apply) and the one the library picks (-1: none holds K).
+bool reg_config(const ConvGeom& g, int id, RegConfig* c);
+int reg_pick(const ConvGeom& g);
+bool reg_supported(const ConvGeom& g);
 
 // Whether the implicit-GEMM / depthwise kernels accept a geometry.
 bool gemm_supported(const ConvGeom& g);

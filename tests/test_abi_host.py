@@ -98,7 +98,7 @@ def test_auto_algorithm_choice():
     dw = C.conv_desc(2, 8, 8, (3, 3, 3), (7, 7), padding=(0, 1, 1), groups=8)
     assert C.conv_query(dw).algo == C.CO_ALGO_DEPTHWISE
     g = C.conv_desc(1, 2, 3, (3,), ())
-    assert C.conv_query(g).algo in (C.CO_ALGO_DIRECT, C.CO_ALGO_GEMM)
+    assert C.conv_query(g).algo in (C.CO_ALGO_DIRECT, C.CO_ALGO_GEMM, C.CO_ALGO_GEMM_REG)
 
 
 def test_null_and_small_buffers_rejected_without_device():
@@ -254,7 +254,10 @@ def test_gemm_state_and_algorithm_for_named_workloads():
     state size that holds the packed weights and the ring."""
     from paper_2204_03418_amd import synth
     expect = {"conv1d_b1_c4to8_k3_f32": C.CO_ALGO_DIRECT,
-              "dwconv3d_b16_c432_k3_7x7_avgpool_bf16": C.CO_ALGO_DEPTHWISE}
+              "dwconv3d_b16_c432_k3_7x7_avgpool_bf16": C.CO_ALGO_DEPTHWISE,
+              "conv3d_b1_c24_k3_56x56_f32": C.CO_ALGO_GEMM_REG,
+              "conv2d_b32_c64to256_k9x1_v25_f32": C.CO_ALGO_GEMM_REG,
+              "conv2d_b32_c64to256_k9x1_v25_bf16": C.CO_ALGO_GEMM_REG}
     for name, w in synth.WORKLOADS.items():
         c = w.conv
         d = C.conv_desc(c.batch, c.in_channels, c.out_channels, c.kernel, c.in_size, c.stride,
@@ -268,3 +271,18 @@ def test_gemm_state_and_algorithm_for_named_workloads():
             So *= s
         ring = info.ring_slots * c.batch * c.out_channels * So * 4
         assert info.state_bytes >= ring + c.out_channels * 4, name
+
+
+def test_register_gemm_shapes():
+    """The register-operand GEMM holds K = kH*kW*C_in in registers: it takes
+    small-K layers with C_out >= 16 and refuses the rest when forced."""
+    ok = C.conv_desc(1, 24, 24, (3, 3, 3), (56, 56), padding=(0, 1, 1), algo="gemm_reg")
+    assert C.conv_query(ok).algo == C.CO_ALGO_GEMM_REG
+    bf = C.conv_desc(32, 64, 256, (9, 1), (25,), dtype=C.CO_BF16, algo="gemm_reg")
+    assert C.conv_query(bf).algo == C.CO_ALGO_GEMM_REG
+    deep = C.conv_desc(2, 192, 192, (3, 3, 3), (14, 14), padding=(0, 1, 1), algo="gemm_reg")
+    assert _status(deep) == C.CO_ENOTSUP          # K = 1728: too deep for registers
+    narrow = C.conv_desc(1, 4, 8, (3,), (), algo="gemm_reg")
+    assert _status(narrow) == C.CO_ENOTSUP        # C_out < 16
+    grouped = C.conv_desc(1, 32, 32, (3, 3, 3), (8, 8), groups=2, algo="gemm_reg")
+    assert _status(grouped) == C.CO_ENOTSUP

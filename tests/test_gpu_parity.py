@@ -347,3 +347,61 @@ def test_gemm_forced(case):
     ref.clean_state()
     ys = co.forward_steps(xd, pad_end=True)
     assert_close(np64(ys), ref.forward_steps(np64(x), pad_end=True), tdt, "gemm steps pad_end")
+
+
+REG_CASES = [
+    # B, Cin, Cout, kernel (time first), in_size, stride, padding, dilation, dtype
+    (1, 24, 24, (3, 3, 3), (56, 56), (1, 1, 1), (0, 1, 1), (1, 1, 1), "f32"),   # 56x56 stem block
+    (3, 7, 20, (2, 3, 3), (9, 11), (1, 1, 1), (1, 1, 1), (1, 1, 1), "f32"),     # ragged C and M
+    (2, 10, 33, (3, 3, 2), (8, 7), (2, 2, 1), (2, 1, 0), (2, 1, 2), "f32"),     # strides, dilation
+    (5, 64, 48, (4, 1), (25,), (1, 1), (0, 0), (1, 1), "f32"),                  # (kT, 1) over joints
+    (5, 64, 48, (4, 1), (25,), (1, 1), (2, 0), (1, 1), "bf16"),
+    (2, 40, 24, (3, 1, 3), (9, 11), (1, 1, 1), (0, 0, 1), (1, 1, 1), "bf16"),   # ragged channel block
+    (4, 16, 16, (1, 3, 3), (8, 8), (1, 1, 1), (0, 1, 1), (1, 1, 1), "f32"),     # kT = 1: no ring
+    (3, 5, 17, (3,), (), (1,), (0,), (1,), "f32"),                              # Conv1d, M = B
+    (2, 100, 32, (2, 1, 1), (6, 5), (1, 1, 1), (1, 0, 0), (1, 1, 1), "bf16"),   # 4 channel blocks
+    (3, 12, 40, (5, 3, 3), (7, 9), (2, 2, 2), (3, 1, 1), (1, 2, 1), "bf16"),    # stride 2 everywhere
+]
+
+
+@pytest.mark.parametrize("case", REG_CASES, ids=lambda c: "reg_" + "_".join(map(str, c[:3])) + c[-1])
+def test_gemm_reg_forced(case):
+    """Register-operand GEMM step (forced) against the oracle: forward_step with
+    update_state=False peeks, then forward_steps with end padding."""
+    B, cin, cout, k, size, s, p, dil, dt = case
+    say("gemm_reg", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          stride=s, padding=p, dilation=dil, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 13, 71000 + cin * 7 + cout, "kaiming")
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=s, padding=p,
+                      dilation=dil, algo="gemm_reg")
+    assert co.algo.startswith("gemm_reg")
+    ref = oracle_conv(w, b, s, p, dil, 1)
+    xd = x.to(DEV)
+    tdt = synth.torch_dtype(dt)
+    outs, peeks = [], []
+    for t in range(x.shape[2]):
+        fr = xd[:, :, t].contiguous()
+        pk = co.forward_step(fr, update_state=False)
+        if pk is not None:
+            peeks.append(pk.clone())
+        y = co.forward_step(fr)
+        if y is not None:
+            outs.append(y.clone())
+    r = ref.forward_steps(np64(x))
+    if r is None:
+        assert not outs
+    else:
+        got = np.stack([np64(o) for o in outs], axis=2)
+        assert_close(got, r, tdt, "gemm_reg steps")
+        assert len(peeks) == len(outs)
+        for a, bb in zip(peeks, outs):
+            assert torch.equal(a, bb)
+    co.clean_state()
+    ref.clean_state()
+    ys = co.forward_steps(xd, pad_end=True)
+    rp = ref.forward_steps(np64(x), pad_end=True)
+    if rp is None:
+        assert ys is None
+    else:
+        assert_close(np64(ys), rp, tdt, "gemm_reg steps pad_end")
