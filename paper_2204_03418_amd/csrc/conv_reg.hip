@@ -39,7 +39,7 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 constexpr int kRegWaves = 4;  // independent waves per workgroup
 
-constexpr int kRegMaxTaps = 9;  // largest kH*kW an instantiation holds
+constexpr int kRegMaxTaps = 16;  // tap offsets passed (>= taps per wave x waves per tile)
 
 struct RegArgs {
   int32_t M, N, So;
@@ -58,17 +58,14 @@ struct RegTaps {
   int32_t as[CO_MAX_TAPS];
 };
 
-// 32-bit byte offset of element `e` of a T buffer, or an out-of-range offset
-// (the load returns zero) when !ok.
-template <typename T>
-__device__ __forceinline__ int elem_off(uint32_t e, bool ok) {
-  return ok ? int(e * uint32_t(sizeof(T))) : kOutOfRange;
-}
-
-// VEC: M % 4 == 0 (whole 16-byte ring stores).  EXACT: the layer has exactly
-// CSMAX channel blocks and C_in is a multiple of the block width, so no
-// k-step is idle and no lane reads past C_in (no per-k-step selects).
-template <typename T, int WN, int TAPS, int CSMAX, bool VEC, bool EXACT>
+// TAPS: spatial taps one wave holds.  KSPLIT: waves sharing one tile; wave h
+// of a tile takes taps h*TAPS .. h*TAPS + TAPS - 1 and the partial sums meet
+// in LDS, which halves each wave's serial gathers and MFMAs when a layer has
+// too few tiles to give every SIMD more than one wave.  VEC: M % 4 == 0
+// (whole 16-byte ring stores).  EXACT: the layer has exactly CSMAX channel
+// blocks and C_in is a multiple of the block width, so no k-step is idle and
+// no lane reads past C_in (no per-k-step selects).
+template <typename T, int WN, int TAPS, int CSMAX, int KSPLIT, bool VEC, bool EXACT>
 __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
     ConvGeom g, RegArgs ra, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
     int64_t y_bc, const uint4* __restrict__ wp, const float* __restrict__ bias,
@@ -87,8 +84,18 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   // consecutive logical blocks (neighbouring tiles) share an XCD's L2.
   const int bid = int(blockIdx.x);
   const int lb = (bid & 7) * ra.blocks_per_xcd + (bid >> 3);
-  const int tile = lb * kRegWaves + wave;
-  if (tile >= ra.m_frags * ra.n_grps) return;  // whole waves; no barriers follow
+  constexpr int TPW = kRegWaves / KSPLIT;  // tiles per workgroup
+  const int h = wave % KSPLIT, wslot = wave / KSPLIT;
+  const int tile_raw = lb * TPW + wslot;
+  const int tiles = ra.m_frags * ra.n_grps;
+  if constexpr (KSPLIT == 1) {
+    if (tile_raw >= tiles) return;  // whole waves; no barrier follows
+  }
+  // with a split, waves past the last tile keep to the barrier: they redo
+  // tile 0 with every store masked
+  const bool live = tile_raw < tiles;
+  const int tile = live ? tile_raw : 0;
+  const bool owner = live & (h == 0);  // the wave that stores the tile
   const int mf = tile / ra.n_grps;
   const int nfb = ra.nf0 + (tile - mf * ra.n_grps) * WN;
 
@@ -139,7 +146,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   for (int f = 0; f < WN; ++f) {
     // one 16-byte read per lane (slots end with four floats of padding, so a
     // ragged frame's last pixels stay in range; pixels past M are not stored)
-    const bool rd = ((e_act[f] == CO_TAP_ACC) | (e_act[f] == CO_TAP_EMIT)) & (P0 < ra.M);
+    const bool rd = ((e_act[f] == CO_TAP_ACC) | (e_act[f] == CO_TAP_EMIT)) & (P0 < ra.M) & owner;
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(
         rr, rd ? (e_off[f] + P0) * 4 : kOutOfRange, 0, 0);
     prev[f] = v4f{__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
@@ -168,8 +175,10 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
 
   using AReg = typename std::conditional<kBF, uint4, float>::type;
   AReg areg[TAPS][CSMAX];
+  const int tp0 = h * TAPS;  // first tap of this wave
 #pragma unroll
-  for (int tp = 0; tp < TAPS; ++tp) {
+  for (int i = 0; i < TAPS; ++i) {
+    const int tp = tp0 + i;
     // per-lane offset of the tap's pixel in channel block 0, or out of range;
     // a channel block adds a wave-uniform offset through the instruction's
     // scalar operand.  In the last block lanes past C_in read out of range.
@@ -195,8 +204,8 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
           const int so = last ? sb : sb + int(uint32_t(e) * plane_b);
           r[e] = __builtin_amdgcn_raw_buffer_load_b16(xr, v, so, 0);
         }
-        areg[tp][cb] = make_uint4(r[0] | (r[1] << 16), r[2] | (r[3] << 16),
-                                  r[4] | (r[5] << 16), r[6] | (r[7] << 16));
+        areg[i][cb] = make_uint4(r[0] | (r[1] << 16), r[2] | (r[3] << 16),
+                                 r[4] | (r[5] << 16), r[6] | (r[7] << 16));
       }
     } else {
       const int vl = nv_last > 0 ? vt : kOutOfRange;
@@ -205,7 +214,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
         const bool live = EXACT || cb < ra.CS;  // wave-uniform
         const bool last = !EXACT && cb == ra.CS - 1;
         const int v = !live ? kOutOfRange : last ? vl : vt;
-        areg[tp][cb] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        areg[i][cb] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
             xr, v, int(uint32_t(cb * CKS) * plane_b), 0));
       }
     }
@@ -218,14 +227,15 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
 #pragma unroll
   for (int f = 0; f < WN; ++f)
 #pragma unroll
-    for (int tp = 0; tp < TAPS; ++tp)
+    for (int i = 0; i < TAPS; ++i)
 #pragma unroll
       for (int cq = 0; cq < CSUMAX; ++cq) {
+        const int tp = tp0 + i;
         const bool okw = (tp < ra.ntaps) & (cq < ra.CSU);
         const int off = ((((nfb + f) * ra.ntaps + tp) * ra.CSU + cq) << 10) + lane * 16;
         const auto w4 =
             __builtin_amdgcn_raw_buffer_load_b128(wr, okw ? off : kOutOfRange, 0, 0);
-        breg[f][tp][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        breg[f][i][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
 
   // ---- matrix work --------------------------------------------------------
@@ -257,6 +267,17 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
     }
   }
 
+  if constexpr (KSPLIT == 2) {
+    // the two waves of a tile exchange partial sums through LDS; both end
+    // with the full sum, the owner stores it
+    __shared__ v4f red[TPW][2][WN][64];
+#pragma unroll
+    for (int f = 0; f < WN; ++f) red[wslot][h][f][lane] = acc[f];
+    __syncthreads();
+#pragma unroll
+    for (int f = 0; f < WN; ++f) acc[f] += red[wslot][1 - h][f][lane];
+  }
+
   // ---- fused ring epilogue (branch-free) ----------------------------------
   // Stores go through buffer resources; a lane that must not store uses an
   // out-of-range offset, which the hardware drops.  With no branch after the
@@ -267,8 +288,8 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
 #pragma unroll
   for (int f = 0; f < WN; ++f) {
     const int act = e_act[f];
-    const bool to_ring = (act == CO_TAP_START) | (act == CO_TAP_ACC);
-    const bool to_y = (act == CO_TAP_EMIT) | (act == CO_TAP_EMIT_FRESH);
+    const bool to_ring = ((act == CO_TAP_START) | (act == CO_TAP_ACC)) & owner;
+    const bool to_y = ((act == CO_TAP_EMIT) | (act == CO_TAP_EMIT_FRESH)) & owner;
     const v4f v = acc[f] + prev[f];
     if constexpr (VEC) {  // M % 4 == 0: a lane's four pixels are all valid or none
       __builtin_amdgcn_raw_buffer_store_b128(
@@ -351,7 +372,7 @@ __global__ __launch_bounds__(kBlock) void pack_reg_kernel(ConvGeom g, RegConfig 
   out[idx] = make_uint4(word[0], word[1], word[2], word[3]);
 }
 
-template <typename T, int WN, int TAPS, int CSMAX>
+template <typename T, int WN, int TAPS, int CSMAX, int KSPLIT>
 hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L, char* state,
                       const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   RegTaps tt;
@@ -374,7 +395,7 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   ra.nf0 = (t_lo * g.Cout) / 16;
   const int nf_end = int(ceil_div(int64_t(t_hi + 1) * g.Cout, 16));
   ra.n_grps = int32_t(ceil_div(nf_end - ra.nf0, WN));
-  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegWaves);
+  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegWaves / KSPLIT);
   ra.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
   ra.ntaps = g.kH * g.kW;
   ra.CS = c.CS;
@@ -393,10 +414,10 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   ra.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
   const bool exact = c.CS == CSMAX && g.Cin % c.CKS == 0;
   auto kern = ra.M % 4 == 0
-                  ? (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, true, true>
-                           : conv_step_reg_kernel<T, WN, TAPS, CSMAX, true, false>)
-                  : (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, false, true>
-                           : conv_step_reg_kernel<T, WN, TAPS, CSMAX, false, false>);
+                  ? (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, true, true>
+                           : conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, true, false>)
+                  : (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, false, true>
+                           : conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, false, false>);
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * ra.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g,
                      ra, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
                      reinterpret_cast<const uint4*>(state + L.weight),
@@ -419,15 +440,16 @@ hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* st
       ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31))
     return launch_conv_step_direct(g, L, state, io, plan, false, s);
   switch (c.id) {
-    case 0: return reg_launch<float, 4, 1, 16>(g, c, L, state, io, plan, s);
-    case 1: return reg_launch<float, 2, 1, 32>(g, c, L, state, io, plan, s);
-    case 2: return reg_launch<float, 1, 9, 6>(g, c, L, state, io, plan, s);
-    case 3: return reg_launch<float, 2, 9, 3>(g, c, L, state, io, plan, s);
-    case 4: return reg_launch<bf16_t, 4, 1, 2>(g, c, L, state, io, plan, s);
-    case 5: return reg_launch<bf16_t, 2, 1, 4>(g, c, L, state, io, plan, s);
-    case 6: return reg_launch<bf16_t, 1, 1, 16>(g, c, L, state, io, plan, s);
-    case 7: return reg_launch<bf16_t, 1, 9, 2>(g, c, L, state, io, plan, s);
-    case 8: return reg_launch<bf16_t, 2, 9, 1>(g, c, L, state, io, plan, s);
+    case 0: return reg_launch<float, 4, 1, 16, 1>(g, c, L, state, io, plan, s);
+    case 1: return reg_launch<float, 2, 1, 32, 1>(g, c, L, state, io, plan, s);
+    case 2: return reg_launch<float, 1, 9, 6, 1>(g, c, L, state, io, plan, s);
+    case 3: return reg_launch<float, 2, 9, 3, 1>(g, c, L, state, io, plan, s);
+    case 4: return reg_launch<float, 1, 5, 6, 2>(g, c, L, state, io, plan, s);
+    case 5: return reg_launch<bf16_t, 4, 1, 2, 1>(g, c, L, state, io, plan, s);
+    case 6: return reg_launch<bf16_t, 2, 1, 4, 1>(g, c, L, state, io, plan, s);
+    case 7: return reg_launch<bf16_t, 1, 1, 16, 1>(g, c, L, state, io, plan, s);
+    case 8: return reg_launch<bf16_t, 1, 9, 2, 1>(g, c, L, state, io, plan, s);
+    case 9: return reg_launch<bf16_t, 2, 9, 1, 1>(g, c, L, state, io, plan, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -149,18 +149,20 @@ bool gemm_supported(const ConvGeom& g) { return gemm_pick(g) >= 0; }
 namespace {
 
 struct RegShape {
-  int32_t dtype, WN, TAPS, CSMAX;
+  int32_t dtype, WN, TAPS, CSMAX, KSPLIT;
 };
 
 // Instantiated register-GEMM shapes (the kernel file instantiates the same
-// table): spatial taps x channel blocks held per lane (the matrix work covers
+// table): spatial taps x channel blocks held per tile (the matrix work covers
 // all of them, so shapes are sized to common layers: 3x3 taps with up to 24
 // fp32 channels, 1x1 with up to 64 or 128), operand registers per lane near
-// or below 128 in every shape.
+// or below 128 in every shape.  The split shape gives a 3x3 layer with few
+// output tiles two waves per tile.
 constexpr RegShape kRegShapes[kRegConfigs] = {
-    {CO_F32, 4, 1, 16}, {CO_F32, 2, 1, 32}, {CO_F32, 1, 9, 6}, {CO_F32, 2, 9, 3},
-    {CO_BF16, 4, 1, 2}, {CO_BF16, 2, 1, 4},  {CO_BF16, 1, 1, 16}, {CO_BF16, 1, 9, 2},
-    {CO_BF16, 2, 9, 1},
+    {CO_F32, 4, 1, 16, 1}, {CO_F32, 2, 1, 32, 1}, {CO_F32, 1, 9, 6, 1},
+    {CO_F32, 2, 9, 3, 1},  {CO_F32, 1, 10, 6, 2}, {CO_BF16, 4, 1, 2, 1},
+    {CO_BF16, 2, 1, 4, 1}, {CO_BF16, 1, 1, 16, 1}, {CO_BF16, 1, 9, 2, 1},
+    {CO_BF16, 2, 9, 1, 1},
 };
 
 }  // namespace
@@ -175,6 +177,7 @@ bool reg_config(const ConvGeom& g, int id, RegConfig* c) {
   r.dtype = s.dtype;
   r.WN = s.WN;
   r.TAPS = s.TAPS;
+  r.KSPLIT = s.KSPLIT;
   r.CSMAX = s.CSMAX;
   r.CKS = g.dtype == CO_BF16 ? 32 : 4;
   r.CS = int32_t(ceil_div(g.Cin, r.CKS));
@@ -190,17 +193,20 @@ bool reg_config(const ConvGeom& g, int id, RegConfig* c) {
 }
 
 int reg_pick(const ConvGeom& g) {
-  // Prefer the widest wave tile (fewer re-reads of the input pixels) that
-  // still gives every SIMD a wave; among equal widths the smallest register
-  // footprint (taps x channel blocks).
+  // Waves (tiles x waves per tile) should cover the 1024 SIMDs; among shapes
+  // that do, the widest wave tile (fewer re-reads of the input pixels), then
+  // no split, then the smallest register footprint.  When none covers the
+  // chip, the one with the most waves.
   int best = -1;
   int64_t best_waves = 0;
-  int best_wn = 0, best_k = 0;
+  int best_wn = 0, best_split = 0, best_k = 0;
   for (int id = 0; id < kRegConfigs; ++id) {
     RegConfig c;
     if (!reg_config(g, id, &c)) continue;
-    const int64_t waves = int64_t(c.m_frags) * ceil_div(c.n_frags, c.WN);
+    const int64_t tiles = int64_t(c.m_frags) * ceil_div(c.n_frags, c.WN);
+    const int64_t waves = tiles * c.KSPLIT;
     const bool fills = waves >= 1024;
+    const int k = c.TAPS * c.CSMAX;
     bool better;
     if (best < 0) {
       better = true;
@@ -208,18 +214,21 @@ int reg_pick(const ConvGeom& g) {
       const bool best_fills = best_waves >= 1024;
       if (fills != best_fills)
         better = fills;
-      else if (fills && c.WN != best_wn)
-        better = c.WN > best_wn;
       else if (!fills && waves != best_waves)
         better = waves > best_waves;
+      else if (c.WN != best_wn)
+        better = c.WN > best_wn;
+      else if (c.KSPLIT != best_split)
+        better = c.KSPLIT < best_split;
       else
-        better = c.TAPS * c.CSMAX < best_k;
+        better = k < best_k;
     }
     if (better) {
       best = id;
       best_waves = waves;
       best_wn = c.WN;
-      best_k = c.TAPS * c.CSMAX;
+      best_split = c.KSPLIT;
+      best_k = k;
     }
   }
   return best;

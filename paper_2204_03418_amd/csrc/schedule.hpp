@@ -68,7 +68,8 @@ struct RegConfig {
   int32_t id;       // kernel instantiation
   int32_t dtype;    // CO_F32 | CO_BF16
   int32_t WN;       // 16-column fragments per wave
-  int32_t TAPS;     // spatial taps (kH*kW) the instantiation holds
+  int32_t TAPS;     // spatial taps (kH*kW) the instantiation holds (all waves of a tile)
+  int32_t KSPLIT;   // waves sharing one tile (each takes TAPS / KSPLIT taps)
   int32_t CSMAX;    // channel blocks per tap the instantiation holds
   int32_t CKS;      // input channels per k-step (channel block)
   int32_t CS;       // channel blocks per spatial tap, ceil(C_in / CKS)
@@ -79,7 +80,7 @@ struct RegConfig {
   int32_t n_frags;  // 16-column fragments, ceil(kT*C_out / 16)
 };
 
-constexpr int kRegConfigs = 9;
+constexpr int kRegConfigs = 10;
 
 constexpr int kGemmConfigs = 4;
 constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)

@@ -361,6 +361,7 @@ REG_CASES = [
     (3, 5, 17, (3,), (), (1,), (0,), (1,), "f32"),                              # Conv1d, M = B
     (2, 100, 32, (2, 1, 1), (6, 5), (1, 1, 1), (1, 0, 0), (1, 1, 1), "bf16"),   # 4 channel blocks
     (3, 12, 40, (5, 3, 3), (7, 9), (2, 2, 2), (3, 1, 1), (1, 2, 1), "bf16"),    # stride 2 everywhere
+    (8, 24, 24, (2, 3, 3), (28, 28), (1, 1, 1), (1, 1, 1), (1, 1, 1), "f32"),   # enough tiles: no split
 ]
 
 
