@@ -168,6 +168,7 @@ hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,
     case CO_ALGO_DEPTHWISE: return launch_conv_step_depthwise(g, L, state, io, plan, s);
     case CO_ALGO_GEMM: return launch_conv_step_gemm(g, L, state, io, plan, s);
     case CO_ALGO_GEMM_REG: return launch_conv_step_reg(g, L, state, io, plan, s);
+    case CO_ALGO_GEMM_IMG: return launch_conv_step_img(g, L, state, io, plan, s);
     default: return launch_conv_step_direct(g, L, state, io, plan, false, s);
   }
 }
@@ -188,6 +189,8 @@ hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
     e = launch_pack_gemm(g, L, state, weight, s);
   } else if (g.algo == CO_ALGO_GEMM_REG) {
     e = launch_pack_reg(g, L, state, weight, s);
+  } else if (g.algo == CO_ALGO_GEMM_IMG) {
+    e = launch_pack_img(g, L, state, weight, s);
   } else {
     const int64_t n = int64_t(g.Cout) * g.Cg * g.kT * g.kH * g.kW;
     float* wdst = reinterpret_cast<float*>(state + L.weight);

@@ -56,6 +56,10 @@ hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* st
                                 const StepIO& io, const co_step_plan& plan, hipStream_t stream);
 hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,
                            const void* weight, hipStream_t stream);
+hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* state,
+                                const StepIO& io, const co_step_plan& plan, hipStream_t stream);
+hipError_t launch_pack_img(const ConvGeom& g, const ConvLayout& L, char* state,
+                           const void* weight, hipStream_t stream);
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, hipStream_t stream);
 
