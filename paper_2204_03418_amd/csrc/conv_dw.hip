@@ -22,6 +22,7 @@ constexpr int kDwTaps = 4;  // active taps handled per pass (ring reads in fligh
 // Active taps of one step, compacted: tap index, action, ring slot.
 struct ActiveTaps {
   int32_t n;
+  FastDiv fd_So, fd_Cout, fd_Wo;  // dividers: pixels per frame, C_out, Wo
   int32_t tap[CO_MAX_TAPS];
   int32_t act[CO_MAX_TAPS];
   int32_t slot[CO_MAX_TAPS];
@@ -36,12 +37,13 @@ __global__ __launch_bounds__(kBlock) void conv_step_dw_kernel(
   const int32_t total = g.B * g.Cout * So;
   const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
   if (idx >= total) return;
-  const int32_t p = idx % So;
-  const int32_t bc = idx / So;
-  const int32_t c = bc % g.Cout;
-  const int32_t i = p / g.Wo, jo = p % g.Wo;
+  const int32_t bc = fdiv(idx, at.fd_So);
+  const int32_t p = idx - bc * So;
+  const int32_t bq = fdiv(bc, at.fd_Cout);
+  const int32_t c = bc - bq * g.Cout;
+  const int32_t i = fdiv(p, at.fd_Wo), jo = p - i * g.Wo;
   const int64_t yi = int64_t(bc) * y_bc + p;
-  const int32_t ridx = (c * g.B + bc / g.Cout) * So + p;  // ring (slot, C, B, Ho, Wo)
+  const int32_t ridx = (c * g.B + bq) * So + p;  // ring (slot, C, B, Ho, Wo)
 
   // stencil of the arriving frame: buffer loads whose out-of-frame taps
   // read zero from an out-of-range offset, so all loads issue together
@@ -103,6 +105,9 @@ hipError_t dw_launch(const ConvGeom& g, const ConvLayout& L, char* state, const 
     ++at.n;
   }
   if (at.n == 0) return hipSuccess;
+  at.fd_So = make_fastdiv(uint32_t(g.So()));
+  at.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  at.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   hipLaunchKernelGGL((conv_step_dw_kernel<T, KH, KW>), dim3(grid_for(g.out_frame_elems())),
                      dim3(kBlock), 0, s, g, static_cast<const T*>(io.x), io.x_bc,
                      static_cast<T*>(io.y), io.y_bc,

@@ -52,6 +52,8 @@ struct GemmArgs {
   int32_t a_units;  // 16-byte units of one A stage
   int32_t pair;     // rows are read two pixels per load (even width, aligned)
   int32_t x_bytes;  // bytes of x reachable from the frame pointer
+  // dividers: pixels per frame, Wo, Ho, H, C_out, column tiles, staging items per row
+  FastDiv fd_So, fd_Wo, fd_Ho, fd_H, fd_Cout, fd_ntc, fd_wpi;
 };
 
 template <typename T>
@@ -183,15 +185,15 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   const int bid = int(blockIdx.x);
   const int L = (bid & 7) * ga.tiles_per_xcd + (bid >> 3);
   if (L >= ga.m_tiles * ga.n_tile_cnt) return;
-  const int m_tile = L / ga.n_tile_cnt;
-  const int n_tile = ga.n_tile0 + L % ga.n_tile_cnt;
+  const int m_tile = fdiv(L, ga.fd_ntc);
+  const int n_tile = ga.n_tile0 + (L - m_tile * ga.n_tile_cnt);
   const int m0 = m_tile * M_WG;
   const int m1 = min(m0 + M_WG, ga.M);
 
   // input rows of the tile: flattened (stream, row) index q in [q0, q1]
-  const int r0 = m0 / g.Wo, r1 = (m1 - 1) / g.Wo;
-  const int b0 = r0 / g.Ho, i0 = r0 % g.Ho;
-  const int b1 = r1 / g.Ho, i1 = r1 % g.Ho;
+  const int r0 = fdiv(m0, ga.fd_Wo), r1 = fdiv(m1 - 1, ga.fd_Wo);
+  const int b0 = fdiv(r0, ga.fd_Ho), i0 = r0 - b0 * g.Ho;
+  const int b1 = fdiv(r1, ga.fd_Ho), i1 = r1 - b1 * g.Ho;
   const int q0 = b0 * g.H + max(0, i0 - g.pH);
   const int q1 = b1 * g.H + min(g.H - 1, i1 + KH - 1 - g.pH);
   const int nslots = q1 - q0 + 1;
@@ -215,8 +217,9 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   for (int mf = 0; mf < WM; ++mf) {
     const int P = m0 + (wm * WM + mf) * 16 + lrow;
     const bool valid = P < ga.M;
-    const int b = P / ga.So, p = P % ga.So;
-    const int i = p / g.Wo, j = p % g.Wo;
+    const int Pc = valid ? P : 0;
+    const int b = fdiv(Pc, ga.fd_So), p = Pc - b * ga.So;
+    const int i = fdiv(p, ga.fd_Wo), j = p - i * g.Wo;
 #pragma unroll
     for (int u = 0; u < KH; ++u) {
       const int ih = i + u - g.pH;
@@ -242,12 +245,12 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     a_dst[ai] = a_pixels * kPixUnits;
     a_dst1[ai] = (a_pixels + 1) * kPixUnits;
     if (it < a_items) {
-      const int xp = it % wp_items;
-      const int rest = it / wp_items;
+      const int rest = fdiv(it, ga.fd_wpi);
+      const int xp = it - rest * wp_items;
       const int grp = rest & 3;
       const int sl = rest >> 2;
       const int q = q0 + sl;
-      const int b = q / g.H, ih = q - b * g.H;
+      const int b = fdiv(q, ga.fd_H), ih = q - b * g.H;
       const int xcol = xp * PW;
       a_src[ai] = int(((int64_t(b) * g.Cin + grp * KL) * x_bc + int64_t(ih) * g.W + xcol) *
                       int64_t(sizeof(T)));
@@ -320,7 +323,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   for (int nf = 0; nf < WN; ++nf) {
     const int n = n_tile * N_WG + (wn * WN + nf) * 16 + lrow;
     const int nn = n < ga.N ? n : ga.N - 1;
-    const int t = nn / g.Cout, o = nn - t * g.Cout;
+    const int t = fdiv(nn, ga.fd_Cout), o = nn - t * g.Cout;
     e_act[nf] = n < ga.N ? int(tt.action[t]) : CO_TAP_NONE;
     e_o[nf] = o;
     e_bias[nf] = bias[o];
@@ -410,7 +413,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     for (int mf = 0; mf < WM; ++mf) {
       const int P0 = m0 + (wm * WM + mf) * 16 + lgrp * 4;
       if (P0 >= ga.M) continue;
-      const int b = P0 / ga.So, p = P0 - b * ga.So;
+      const int b = fdiv(P0, ga.fd_So), p = P0 - b * ga.So;
       const bool same_frame = p + 3 < ga.So;
 #pragma unroll
       for (int nf = 0; nf < WN; ++nf) {
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
           } else {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const int bb = (P0 + r) / ga.So, pp = (P0 + r) - bb * ga.So;
+              const int bb = fdiv(P0 + r, ga.fd_So), pp = (P0 + r) - bb * ga.So;
               store_out<T>(y, (int64_t(bb) * g.Cout + o) * y_bc + pp, v[r] + bo);
             }
           }
@@ -451,7 +454,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
           if (act == CO_TAP_START || act == CO_TAP_ACC) {
             e_ring[nf][P] = v;
           } else {
-            const int b = P / ga.So, p = P - b * ga.So;
+            const int b = fdiv(P, ga.fd_So), p = P - b * ga.So;
             store_out<T>(y, (int64_t(b) * g.Cout + e_o[nf]) * y_bc + p, v + e_bias[nf]);
           }
         }
@@ -539,6 +542,13 @@ hipError_t gemm_launch(const ConvGeom& g, const GemmConfig& c, const ConvLayout&
   ga.pair = PAIR ? 1 : 0;
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   ga.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz);
+  ga.fd_So = make_fastdiv(uint32_t(ga.So));
+  ga.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  ga.fd_Ho = make_fastdiv(uint32_t(g.Ho));
+  ga.fd_H = make_fastdiv(uint32_t(g.H));
+  ga.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  ga.fd_ntc = make_fastdiv(uint32_t(ga.n_tile_cnt));
+  ga.fd_wpi = make_fastdiv(uint32_t(PAIR ? g.W / 2 : g.W));
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * ga.tiles_per_xcd)), dim3(64 * NWM * NWN),
                      size_t(c.lds_bytes), s, g, ga, static_cast<const T*>(io.x), io.x_bc,
                      static_cast<T*>(io.y), io.y_bc,

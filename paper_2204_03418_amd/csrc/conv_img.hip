@@ -52,6 +52,7 @@ struct ImgArgs {
   int32_t pair;              // even width: two pixels per staging load
   int32_t x_bytes, ring_bytes, y_bytes;  // buffer extents (bytes)
   int32_t ring_slot;         // floats between ring slots
+  FastDiv fd_pairs, fd_wq, fd_Cout, fd_Wo, fd_slabs;  // dividers of the index decompositions
 };
 
 // Per-tap action and ring slot as one dword each (action | slot << 8), read
@@ -98,7 +99,7 @@ conv_step_img_kernel(ConvGeom g, ImgArgs ia, const bf16_t* __restrict__ x, int64
   const int bid = int(blockIdx.x);
   const int lb = (bid & 7) * ia.blocks_per_xcd + (bid >> 3);
   if (lb >= ia.wgs) return;  // whole workgroups: no barrier is skipped
-  const int b = lb / ia.slab_cnt;
+  const int b = fdiv(lb, ia.fd_slabs);
   const int slab = ia.slab0 + (lb - b * ia.slab_cnt);
 
   uint4* const As = smem;
@@ -117,8 +118,8 @@ conv_step_img_kernel(ConvGeom g, ImgArgs ia, const bf16_t* __restrict__ x, int64
     const int it = tid + ii * kImgThreads;
     const bool ok = it < ia.items;
     const int itc = ok ? it : 0;
-    const int co = itc / ia.pairs, pp = itc - co * ia.pairs;
-    const int r = pp / ia.wq, c = (pp - r * ia.wq) * pw;
+    const int co = fdiv(itc, ia.fd_pairs), pp = itc - co * ia.pairs;
+    const int r = fdiv(pp, ia.fd_wq), c = (pp - r * ia.wq) * pw;
     a_dst[ii] = ok ? ((r + g.pH) * ia.cols + c + g.pW) * ia.pix_units + co : -1;
     const int src = ok ? int(uint32_t((b * g.Cin + co * 8)) * uint32_t(plane_b) +
                              uint32_t(r * g.W + c) * 2u)
@@ -185,7 +186,7 @@ conv_step_img_kernel(ConvGeom g, ImgArgs ia, const bf16_t* __restrict__ x, int64
   };
   auto col_info = [&](int col) {
     const int n0 = slab * NS + col * 16;  // uniform
-    const int t0 = n0 / g.Cout;
+    const int t0 = fdiv(n0, ia.fd_Cout);
     const int o0 = n0 - t0 * g.Cout;
     const int as0 = tt.as[min(t0, g.kT - 1)], as1 = tt.as[min(t0 + 1, g.kT - 1)];
     int o = o0 + lrow;
@@ -243,7 +244,7 @@ conv_step_img_kernel(ConvGeom g, ImgArgs ia, const bf16_t* __restrict__ x, int64
   for (int i = 0; i < NA; ++i) {
     const int row = i < MO ? pr * MO + i : 4 * MO;
     const int p = min(row * 16 + lrow, ia.So - 1);
-    const int pi = p / g.Wo, pj = p - pi * g.Wo;
+    const int pi = fdiv(p, ia.fd_Wo), pj = p - pi * g.Wo;
     abase[i] = (pi * ia.cols + pj) * ia.pix_units + lgrp;
   }
   // weight unit of column lrow of a fragment, channel group lgrp (swizzled
@@ -447,6 +448,11 @@ hipError_t img_launch(const ConvGeom& g, const ImgConfig& c, const ConvLayout& L
   ia.wq = c.pair ? g.W / 2 : g.W;
   ia.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * 2);
   ia.ring_slot = int32_t(L.ring_slot_elems);
+  ia.fd_pairs = make_fastdiv(uint32_t(c.pairs));
+  ia.fd_wq = make_fastdiv(uint32_t(ia.wq));
+  ia.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  ia.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  ia.fd_slabs = make_fastdiv(uint32_t(ia.slab_cnt));
   ia.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
   ia.y_bytes = int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * 2);
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * ia.blocks_per_xcd)), dim3(kImgThreads),

@@ -50,6 +50,7 @@ struct RegArgs {
   int32_t x_bytes, w_bytes;
   int32_t ring_slot, ring_bytes;  // floats between ring slots; bytes of all slots
   int32_t y_bc, y_bytes;          // y plane stride (elements); bytes of y
+  FastDiv fd_So, fd_Wo, fd_Cout, fd_ngrps;  // dividers: pixels per frame, Wo, C_out, n_grps
 };
 
 // Per-tap action and ring slot as one dword each (action | slot << 8), so
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   const bool live = tile_raw < tiles;
   const int tile = live ? tile_raw : 0;
   const bool owner = live & (h == 0);  // the wave that stores the tile
-  const int mf = tile / ra.n_grps;
+  const int mf = fdiv(tile, ra.fd_ngrps);
   const int nfb = ra.nf0 + (tile - mf * ra.n_grps) * WN;
 
   // ---- epilogue data ------------------------------------------------------
@@ -110,7 +111,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   // column n = t*C_out + o: decode the wave's first column once, then step 16
   // columns per fragment (C_out >= 16, so o wraps at most once per step)
   const int n0 = nfb * 16;
-  int tq = n0 / g.Cout, oq = n0 - tq * g.Cout;  // wave-uniform: fragment f's first column
+  int tq = fdiv(n0, ra.fd_Cout), oq = n0 - tq * g.Cout;  // wave-uniform: fragment f's first column
 #pragma unroll
   for (int f = 0; f < WN; ++f) {
     const int n = (nfb + f) * 16 + lrow;
@@ -162,8 +163,8 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   const int P = mf * 16 + lrow;
   const bool pvalid = P < ra.M;
   const int Pc = pvalid ? P : 0;
-  const int b = Pc / ra.So, p = Pc - b * ra.So;
-  const int i = p / g.Wo, j = p - i * g.Wo;
+  const int b = fdiv(Pc, ra.fd_So), p = Pc - b * ra.So;
+  const int i = fdiv(p, ra.fd_Wo), j = p - i * g.Wo;
   const int hb = i * g.sH - g.pH, wb = j * g.sW - g.pW;
   const int lane_c = lgrp * CL;
   constexpr uint32_t esz = sizeof(T);
@@ -284,7 +285,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   // tile test the compiler cannot move any load of the batch down here.
   const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ra.y_bytes);
   constexpr int yesz = int(sizeof(T));
-  const int pb = P0 / ra.So, pp = P0 - pb * ra.So;  // frame and pixel of the lane's first row
+  const int pb = fdiv(P0, ra.fd_So), pp = P0 - pb * ra.So;  // frame and pixel of the lane's first row
 #pragma unroll
   for (int f = 0; f < WN; ++f) {
     const int act = e_act[f];
@@ -311,7 +312,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
         bq += wrap ? 1 : 0;
         pq -= wrap ? ra.So : 0;
       } else {
-        bq = (P0 + r) / ra.So;
+        bq = fdiv(P0 + r, ra.fd_So);
         pq = P0 + r - bq * ra.So;
       }
       const int yo = ((bq * g.Cout + o) * ra.y_bc + pq) * yesz;
@@ -412,6 +413,10 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   ra.y_bc = int32_t(io.y_bc);
   ra.y_bytes = int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz);
   ra.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
+  ra.fd_So = make_fastdiv(uint32_t(ra.So));
+  ra.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  ra.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  ra.fd_ngrps = make_fastdiv(uint32_t(ra.n_grps));
   const bool exact = c.CS == CSMAX && g.Cin % c.CKS == 0;
   auto kern = ra.M % 4 == 0
                   ? (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, true, true>

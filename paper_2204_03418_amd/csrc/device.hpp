@@ -37,6 +37,11 @@ __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <>
 __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
+// n / f.d for 0 <= n < 2^31 (see FastDiv).
+__device__ __forceinline__ int fdiv(int n, const FastDiv& f) {
+  return int((uint64_t(uint32_t(n)) * f.m) >> f.s);
+}
+
 // Per-tap actions and ring slots of one step, passed to kernels by value.
 struct TapTable {
   int8_t action[CO_MAX_TAPS];

@@ -46,7 +46,8 @@ template <typename T, int G>
 __global__ __launch_bounds__(kBlock) void pool_step_kernel(
     PoolGeom g, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y, int64_t y_bc,
     float* __restrict__ fifo, int64_t fifo_slot, float* __restrict__ valid, int32_t write_slot,
-    int32_t update, int32_t emit, int32_t pad_frame, PoolTaps taps) {
+    int32_t update, int32_t emit, int32_t pad_frame, PoolTaps taps, FastDiv fd_So, FastDiv fd_Wo,
+    FastDiv fd_kW) {
   const int32_t So = g.Ho * g.Wo;
   const int32_t total = g.B * g.C * So;
   const int64_t gid = int64_t(blockIdx.x) * kBlock + threadIdx.x;
@@ -54,9 +55,9 @@ __global__ __launch_bounds__(kBlock) void pool_step_kernel(
   const int32_t r = int32_t(gid % G);    // lane within the group
   const bool live = idx < total;         // whole groups are live or not
   const int32_t e_idx = live ? idx : 0;
-  const int32_t p = e_idx % So;
-  const int32_t bc = e_idx / So;
-  const int32_t i = p / g.Wo, jo = p % g.Wo;
+  const int32_t bc = fdiv(e_idx, fd_So);
+  const int32_t p = e_idx - bc * So;
+  const int32_t i = fdiv(p, fd_Wo), jo = p - i * g.Wo;
   const bool is_max = g.kind == CO_POOL_MAX;
   const int32_t kHW = g.kH * g.kW;
 
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(kBlock) void pool_step_kernel(
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, x_extent);
   const int plane = int(int64_t(bc) * x_bc);
   for (int32_t e = r; e < kHW; e += G) {
-    const int32_t u = e / g.kW, v = e - u * g.kW;
+    const int32_t u = fdiv(e, fd_kW), v = e - u * g.kW;
     const int32_t hi = i * g.sH + u * g.dH - g.pH;
     const int32_t wi = jo * g.sW + v * g.dW - g.pW;
     const bool in = hi >= 0 && hi < g.H && wi >= 0 && wi < g.W && !pad_frame;
@@ -184,7 +185,9 @@ hipError_t pool_step_g(const PoolGeom& g, const PoolLayout& L, char* state, cons
   hipLaunchKernelGGL((pool_step_kernel<T, G>), dim3(grid_for(g.out_frame_elems() * G)),
                      dim3(kBlock), 0, s, g, static_cast<const T*>(io.x), io.x_bc,
                      static_cast<T*>(io.y), io.y_bc, fifo, L.fifo_slot_elems, valid,
-                     plan.write_slot, update ? 1 : 0, plan.emit, pad ? 1 : 0, taps);
+                     plan.write_slot, update ? 1 : 0, plan.emit, pad ? 1 : 0, taps,
+                     make_fastdiv(uint32_t(g.So())), make_fastdiv(uint32_t(g.Wo)),
+                     make_fastdiv(uint32_t(g.kW)));
   return hipGetLastError();
 }
 

@@ -23,6 +23,22 @@ inline int64_t axis_out_len(int64_t L, int64_t k, int64_t s, int64_t p, int64_t 
 
 // Everything a convolution kernel needs to know about the layer, resolved
 // once from the descriptor.  Spatial axes are always two (unused ones are 1).
+// Division by a divisor known on the host: for 0 <= n < 2^31 and
+// 1 <= d < 2^31, n / d == (n * m) >> s with l = ceil(log2 d), s = 31 + l and
+// m = ceil(2^s / d) (< 2^32).  The product's error n*(m - 2^s/d)/2^s is below
+// 2^-l <= 1/d, which cannot carry past the next multiple of d.  Kernels take
+// index decompositions this way instead of emulating integer division.
+struct FastDiv {
+  uint32_t d, m, s;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((uint64_t(1) << l) < d) ++l;
+  const uint64_t m = ((uint64_t(1) << (31 + l)) + d - 1) / d;
+  return FastDiv{d, uint32_t(m), 31 + l};
+}
+
 struct ConvGeom {
   int32_t spatial_dims;
   int32_t B, Cin, Cout, G, Cg, Og;
