@@ -255,19 +255,25 @@ def main():
         g1.record(stream)
         torch.cuda.synchronize()
         modes["graph_replay"] = round(c.batch * reps * period / (g0.elapsed_time(g1) / 1e3), 1)
-        # (iii) forward_steps over the resident clip
-        if po is None:
-            xc = x.to(dev)
-            calls = max(1, K // T)
-            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            co.forward_steps(xc)
-            torch.cuda.synchronize()
-            s0.record(stream)
-            for _ in range(calls):
-                co.forward_steps(xc)
-            s1.record(stream)
-            torch.cuda.synchronize()
-            modes["forward_steps"] = round(c.batch * calls * T / (s0.elapsed_time(s1) / 1e3), 1)
+        # (iii) forward_steps over the resident clip (the depthwise workload
+        # chains the convolution's output clip into the pool's forward_steps)
+        xc = x.to(dev)
+        calls = max(1, K // T)
+
+        def clip_pass():
+            yc = co.forward_steps(xc)
+            if po is not None and yc is not None:
+                po.forward_steps(yc)
+
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        clip_pass()
+        torch.cuda.synchronize()
+        s0.record(stream)
+        for _ in range(calls):
+            clip_pass()
+        s1.record(stream)
+        torch.cuda.synchronize()
+        modes["forward_steps"] = round(c.batch * calls * T / (s0.elapsed_time(s1) / 1e3), 1)
 
     cpu = None
     if not args.no_cpu:

@@ -160,6 +160,17 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
   if (n_emit > 0 && !y) return CO_EINVAL;
   hipStream_t s = as_stream(stream);
   const int64_t n0 = h->n;
+  if (count > 0 && dw_steps_supported(g, T, y_cap_frames)) {
+    // one persistent launch: partial sums stay in registers across frames;
+    // with update_state = 0 the state is simply not written back
+    const co_status st = hip_status(launch_conv_steps_depthwise(
+        g, h->L, h->state, x, int64_t(T) * g.S(), T, int32_t(count), y,
+        int64_t(y_cap_frames) * g.So(), n0, update_state != 0, s));
+    if (st != CO_OK) return st;
+    if (update_state) h->n += count;
+    *n_out = int32_t(n_emit);
+    return CO_OK;
+  }
   Backup bk;
   const int64_t ring_bytes = int64_t(g.R) * h->L.ring_slot_elems * 4;
   if (!update_state) {
@@ -343,6 +354,17 @@ co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, voi
   if (n_emit > 0 && !y) return CO_EINVAL;
   hipStream_t s = as_stream(stream);
   const int64_t n0 = h->n;
+  if (count > 0 && pool_steps_supported(g)) {
+    // one persistent launch: the FIFO stays in registers across frames; with
+    // update_state = 0 the state is simply not written back
+    const co_status st = hip_status(launch_pool_steps(
+        g, h->L, h->state, x, int64_t(T) * g.S(), T, int32_t(count), y,
+        int64_t(y_cap_frames) * g.So(), n0, update_state != 0, s));
+    if (st != CO_OK) return st;
+    if (update_state) h->n += count;
+    *n_out = int32_t(n_emit);
+    return CO_OK;
+  }
   Backup bk;
   // FIFO and validity flags are contiguous from L.valid to the end
   const int64_t bytes = h->L.total - h->L.valid;

@@ -127,12 +127,223 @@ hipError_t dw_dispatch(const ConvGeom& g, const ConvLayout& L, char* state, cons
   return hipErrorInvalidValue;
 }
 
+// ---- persistent forward_steps -------------------------------------------
+//
+// A clip of `count` frames in one launch (temporal stride 1 and dilation 1):
+// the thread of output element (b, c, i, j) keeps the channel's kT stencils
+// and the kT - 1 partial sums of its live outputs in registers for the whole
+// clip.  The float32 ring is read once at the start and written back once at
+// the end (not at all when the state is not to be updated), so per frame
+// only the frame's stencil is read and the completed output written.
+//
+// Register acc[q] holds output tau = v - (KT - 1) + q, where v = n + pT is
+// the virtual time of the arriving frame n; tap j feeds acc[KT - 1 - j].  The
+// tap actions are those of the host schedule: an output's first tap on a
+// real frame starts it, later taps add, tap kT - 1 completes it (section
+// 3.1, Principles 3-5).
+struct DwSteps {
+  int32_t v0;       // virtual time n0 + pT of the first frame, capped at 2^29 (the
+                    // schedule only depends on it near the start of a stream)
+  int32_t slot0;    // ring slot of output v0 - (kT - 1): (n0 + pT - kT + 1) mod kT
+  int32_t count;    // frames: T real, then end padding (zero frames)
+  int32_t T;
+  int32_t k0;       // output frame index of the call's first frame: n0 - max(n0, d)
+  int32_t update;   // write the live partial sums back
+  int32_t x_bytes, y_bytes;  // buffer extents from the clip pointers
+  FastDiv fd_So, fd_Cout, fd_Wo;
+};
+
+constexpr int PF = 2;  // frames in flight per thread
+
+template <typename T, int KH, int KW, int KT>
+__global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
+    ConvGeom g, DwSteps ds, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
+    int64_t y_bc, const float* __restrict__ w, const float* __restrict__ bias,
+    float* __restrict__ ring, int64_t ring_slot) {
+  constexpr int NS = KH * KW;
+  constexpr uint32_t esz = sizeof(T);
+  const int32_t So = g.Ho * g.Wo;
+  const int32_t total = g.B * g.Cout * So;
+  const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  if (idx >= total) return;
+  const int32_t bc = fdiv(idx, ds.fd_So);
+  const int32_t p = idx - bc * So;
+  const int32_t bq = fdiv(bc, ds.fd_Cout);
+  const int32_t c = bc - bq * g.Cout;
+  const int32_t i = fdiv(p, ds.fd_Wo), jo = p - i * g.Wo;
+  const int32_t ridx = (c * g.B + bq) * So + p;  // ring (slot, C, B, Ho, Wo)
+
+  float wr[KT][NS];
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+#pragma unroll
+    for (int e = 0; e < NS; ++e) wr[j][e] = w[(c * KT + j) * NS + e];
+  const float bo = bias[c];
+
+  // live partial sums at the start: outputs v0 - KT + 1 .. v0 - 1, in ring
+  // slots slot0, slot0 + 1, ... (mod KT)
+  float acc[KT];
+#pragma unroll
+  for (int q = 0; q < KT; ++q) {
+    const int tau = ds.v0 - (KT - 1) + q;
+    const int sl = (ds.slot0 + q) % KT;
+    acc[q] = (q < KT - 1 && tau >= 0) ? ring[sl * ring_slot + ridx] : 0.f;
+  }
+
+  // stencil byte offsets inside the (b, c) plane of a frame; out-of-frame
+  // taps read an out-of-range offset (zero)
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ds.x_bytes);
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ds.y_bytes);
+  const uint32_t plane = uint32_t(bc) * uint32_t(x_bc) * esz;
+  int32_t soff[NS];
+#pragma unroll
+  for (int u = 0; u < KH; ++u) {
+    const int32_t hi = i * g.sH + u * g.dH - g.pH;
+#pragma unroll
+    for (int v = 0; v < KW; ++v) {
+      const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+      const bool in = hi >= 0 && hi < g.H && wi >= 0 && wi < g.W;
+      soff[u * KW + v] = in ? int(plane + uint32_t(hi * g.W + wi) * esz) : kOutOfRange;
+    }
+  }
+  const int32_t fstride = g.H * g.W * int32_t(esz);  // bytes between frames
+  const int32_t yoff = int32_t((uint32_t(bc) * uint32_t(y_bc) + uint32_t(p)) * esz);
+
+  // the stencil of frame t, zero for end-padding frames (t >= T); the frame
+  // offset is wave-uniform and always inside the clip, out-of-frame taps
+  // carry the out-of-range offset in their per-lane part
+  auto load_frame = [&](int t, float (&xv)[NS]) {
+    if (t < ds.T) {
+#pragma unroll
+      for (int e = 0; e < NS; ++e) xv[e] = load_or_zero_at<T>(xr, soff[e], t * fstride);
+    } else {
+#pragma unroll
+      for (int e = 0; e < NS; ++e) xv[e] = 0.f;
+    }
+  };
+  // frame t's stencil sits in register set t % PF; the next PF - 1 frames'
+  // are in flight while frame t is evaluated
+  float xq[PF][NS];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) load_frame(u, xq[u]);
+  for (int t0 = 0; t0 < ds.count; t0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int t = t0 + u;
+      if (t >= ds.count) break;
+      const int v = ds.v0 + t;
+#pragma unroll
+      for (int j = KT - 1; j >= 0; --j) {
+        const int q = KT - 1 - j;
+        const int tau = v - j;
+        if (tau < 0) continue;  // no such output (uniform)
+        const int first = tau >= g.pT ? 0 : g.pT - tau;  // first tap on a real frame
+        float a = (j == first) ? 0.f : acc[q];  // a start overwrites the slot
+#pragma unroll
+        for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xq[u][e], a);
+        if (j == KT - 1)
+          store_at(yr, yoff, (ds.k0 + t) * So * int32_t(esz), from_f32<T>(a + bo));
+        else
+          acc[q] = a;
+      }
+      // the oldest output is complete: shift the others down one place
+#pragma unroll
+      for (int q = 0; q + 1 < KT; ++q) acc[q] = acc[q + 1];
+      load_frame(t + PF, xq[u]);
+    }
+  }
+  if (ds.update) {
+    // live outputs after the clip: v1 - KT + 1 .. v1 - 1, slots continuing
+    // from slot0 + count
+    const int v1 = ds.v0 + ds.count;
+#pragma unroll
+    for (int q = 0; q + 1 < KT; ++q) {
+      const int tau = v1 - (KT - 1) + q;
+      const int sl = (ds.slot0 + ds.count + q) % KT;
+      if (tau >= 0) ring[sl * ring_slot + ridx] = acc[q];
+    }
+  }
+}
+
+template <typename T, int KH, int KW, int KT>
+hipError_t dw_steps_launch(const ConvGeom& g, const ConvLayout& L, char* state, const void* x,
+                           int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                           int64_t n0, bool update, hipStream_t s) {
+  DwSteps ds;
+  const int64_t v0 = n0 + g.pT;
+  ds.v0 = int32_t(v0 < (int64_t(1) << 29) ? v0 : (int64_t(1) << 29));
+  ds.slot0 = int32_t(((v0 - (g.kT - 1)) % g.kT + g.kT) % g.kT);
+  ds.count = count;
+  ds.T = nreal;
+  // output frame of step n: n - max(n0, d) (valid only for emitting steps)
+  ds.k0 = int32_t(n0 - (n0 > g.d ? n0 : g.d));
+  ds.update = update ? 1 : 0;
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  ds.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  ds.y_bytes = int32_t(((int64_t(g.B) * g.Cout - 1) * y_bc + y_bc) * esz);
+  ds.fd_So = make_fastdiv(uint32_t(g.So()));
+  ds.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  hipLaunchKernelGGL((conv_steps_dw_kernel<T, KH, KW, KT>), dim3(grid_for(g.out_frame_elems())),
+                     dim3(kBlock), 0, s, g, ds, static_cast<const T*>(x), x_bc,
+                     static_cast<T*>(y), y_bc, reinterpret_cast<const float*>(state + L.weight),
+                     reinterpret_cast<const float*>(state + L.bias),
+                     reinterpret_cast<float*>(state + L.ring), L.ring_slot_elems);
+  return hipGetLastError();
+}
+
+template <typename T, int KH, int KW>
+hipError_t dw_steps_kt(const ConvGeom& g, const ConvLayout& L, char* state, const void* x,
+                       int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc, int64_t n0,
+                       bool update, hipStream_t s) {
+  switch (g.kT) {
+    case 1: return dw_steps_launch<T, KH, KW, 1>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 2: return dw_steps_launch<T, KH, KW, 2>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 3: return dw_steps_launch<T, KH, KW, 3>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 4: return dw_steps_launch<T, KH, KW, 4>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 5: return dw_steps_launch<T, KH, KW, 5>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t dw_steps_dispatch(const ConvGeom& g, const ConvLayout& L, char* state, const void* x,
+                             int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                             int64_t n0, bool update, hipStream_t s) {
+  if (g.kH == 3 && g.kW == 3)
+    return dw_steps_kt<T, 3, 3>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  if (g.kH == 1 && g.kW == 1)
+    return dw_steps_kt<T, 1, 1>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 hipError_t launch_conv_step_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
                                       const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   if (g.dtype == CO_BF16) return dw_dispatch<bf16_t>(g, L, state, io, plan, s);
   return dw_dispatch<float>(g, L, state, io, plan, s);
+}
+
+}  // namespace coinf
+
+namespace coinf {
+
+bool dw_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  const bool fits = int64_t(g.B) * g.Cin * x_frames * g.S() * esz < (int64_t(1) << 31) &&
+                    int64_t(g.B) * g.Cout * y_frames * g.So() * esz < (int64_t(1) << 31);
+  return g.algo == CO_ALGO_DEPTHWISE && g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 &&
+         ((g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1)) && fits;
+}
+
+hipError_t launch_conv_steps_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
+                                       const void* x, int64_t x_bc, int32_t nreal, int32_t count,
+                                       void* y, int64_t y_bc, int64_t n0, bool update,
+                                       hipStream_t s) {
+  if (g.dtype == CO_BF16)
+    return dw_steps_dispatch<bf16_t>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  return dw_steps_dispatch<float>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
 }
 
 }  // namespace coinf

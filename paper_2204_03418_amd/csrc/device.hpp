@@ -81,6 +81,29 @@ __device__ __forceinline__ float load_or_zero<float>(__amdgpu_buffer_rsrc_t r, i
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 
+// Element at byte offset voff + soff of a T buffer as float; 0.0 when the
+// offset lies past the buffer (out-of-range reads return zero).
+template <typename T>
+__device__ __forceinline__ float load_or_zero_at(__amdgpu_buffer_rsrc_t r, int voff, int soff);
+template <>
+__device__ __forceinline__ float load_or_zero_at<bf16_t>(__amdgpu_buffer_rsrc_t r, int voff,
+                                                         int soff) {
+  return bf16_to_f32(bf16_t(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0)));
+}
+template <>
+__device__ __forceinline__ float load_or_zero_at<float>(__amdgpu_buffer_rsrc_t r, int voff,
+                                                        int soff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
+// Store v at byte offset voff + soff of a T buffer.
+__device__ __forceinline__ void store_at(__amdgpu_buffer_rsrc_t r, int voff, int soff, bf16_t v) {
+  __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
+}
+__device__ __forceinline__ void store_at(__amdgpu_buffer_rsrc_t r, int voff, int soff, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
+}
+
 inline unsigned grid_for(int64_t n, int block = kBlock) {
   return unsigned((n + block - 1) / block);
 }

@@ -40,6 +40,13 @@ hipError_t launch_pool_step(const PoolGeom& g, const PoolLayout& L, char* state,
 hipError_t launch_pool_init(const PoolGeom& g, const PoolLayout& L, char* state,
                             const StateHeader& hdr, hipStream_t stream);
 
+// Persistent forward_steps of a pool (same conventions as the depthwise one):
+// temporal stride 1 and dilation 1, kT <= 5, a spatial window of at most 64.
+bool pool_steps_supported(const PoolGeom& g);
+hipError_t launch_pool_steps(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                             int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                             int64_t n0, bool update, hipStream_t stream);
+
 hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const void* x, void* y,
                             hipStream_t stream);
 
@@ -50,6 +57,16 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
 hipError_t launch_conv_step_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
                                       const StepIO& io, const co_step_plan& plan,
                                       hipStream_t stream);
+
+// Persistent forward_steps of the depthwise step: `count` frames (the first T
+// read from the clip x with plane stride x_bc, the rest end-padding zero
+// frames) in one launch, starting at step counter n0; emitted frames go to
+// y in order.  Temporal stride 1 and dilation 1, kT <= 5, 3x3 or 1x1 stencils.
+bool dw_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames);
+hipError_t launch_conv_steps_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
+                                       const void* x, int64_t x_bc, int32_t T, int32_t count,
+                                       void* y, int64_t y_bc, int64_t n0, bool update,
+                                       hipStream_t stream);
 hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                                  const StepIO& io, const co_step_plan& plan, hipStream_t stream);
 hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* state,

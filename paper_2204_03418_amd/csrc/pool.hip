@@ -171,6 +171,155 @@ __global__ __launch_bounds__(kBlock) void pool_clip_kernel(PoolGeom g, int32_t T
   y[idx] = from_f32<T>(out);
 }
 
+// ---- persistent forward_steps -------------------------------------------
+//
+// A clip of `count` frames in one launch (temporal stride 1 and dilation 1,
+// a spatial window of at most G positions): the G lanes of output element
+// (b, c, i, j) reduce each frame's window (one load per lane, the next
+// frame's requested before the current one is reduced) and keep the last kT
+// reduced frames and their validity in registers; when the schedule emits
+// they reduce the window's frames into the output.  The FIFO is read at the
+// start and written back at the end; the validity flags of the call's
+// frames are written by the host afterwards.
+struct PoolSteps {
+  int64_t n0;     // step counter before the first frame
+  int32_t count;  // frames: T real, then end padding
+  int32_t T;
+  int64_t emit0;  // first emitting step of the call: max(n0, d)
+  int32_t update;
+  FastDiv fd_So, fd_Wo, fd_kW;
+};
+
+template <typename T, int G, int KT>
+__global__ __launch_bounds__(kBlock) void pool_steps_kernel(
+    PoolGeom g, PoolSteps ps, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
+    int64_t y_bc, float* __restrict__ fifo, int64_t fifo_slot, const float* __restrict__ valid) {
+  const int32_t So = g.Ho * g.Wo;
+  const int32_t total = g.B * g.C * So;
+  const int64_t gid = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  const int32_t idx = int32_t(gid / G);  // output element of this lane's group
+  const int32_t r = int32_t(gid % G);    // lane within the group
+  const bool live = idx < total;         // whole groups are live or not
+  if (!live) return;                     // (no barrier follows)
+  const int32_t bc = fdiv(idx, ps.fd_So);
+  const int32_t p = idx - bc * So;
+  const int32_t i = fdiv(p, ps.fd_Wo), jo = p - i * g.Wo;
+  const bool is_max = g.kind == CO_POOL_MAX;
+  const float neutral = is_max ? -INFINITY : 0.f;
+  const int32_t kHW = g.kH * g.kW;
+
+  // this lane's window position (at most one: kH*kW <= G)
+  int32_t soff = -1;
+  if (r < kHW) {
+    const int32_t u = fdiv(r, ps.fd_kW), v = r - u * g.kW;
+    const int32_t hi = i * g.sH + u * g.dH - g.pH;
+    const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+    if (hi >= 0 && hi < g.H && wi >= 0 && wi < g.W) soff = hi * g.W + wi;
+  }
+  // divisor of an average with count_include_pad = 0: spatial positions in the frame
+  int32_t vh = 0, vw = 0;
+  for (int32_t u = 0; u < g.kH; ++u) {
+    const int32_t hi = i * g.sH + u * g.dH - g.pH;
+    vh += (hi >= 0 && hi < g.H) ? 1 : 0;
+  }
+  for (int32_t v = 0; v < g.kW; ++v) {
+    const int32_t wi = jo * g.sW + v * g.dW - g.pW;
+    vw += (wi >= 0 && wi < g.W) ? 1 : 0;
+  }
+
+  // fv[q], fok[q]: reduced value and validity of real frame n - (KT - 1) + q
+  // at frame n; frames before the stream began are start padding
+  float fv[KT], fok[KT];
+#pragma unroll
+  for (int q = 0; q + 1 < KT; ++q) {
+    const int64_t rf = ps.n0 - (KT - 1) + q;
+    const bool have = rf >= 0;
+    fv[q] = have ? fifo[(rf % KT) * fifo_slot + idx] : neutral;
+    fok[q] = have ? valid[rf % KT] : 0.f;
+  }
+  const int64_t S = int64_t(g.H) * g.W;
+  const T* xb = x + int64_t(bc) * x_bc;
+  T* yb = y + int64_t(bc) * y_bc + p;
+  auto load = [&](int t) {
+    return (t < ps.T && soff >= 0) ? to_f32<T>(xb[int64_t(t) * S + soff]) : neutral;
+  };
+  // frame t's window element sits in xq[t % PF]; the next PF - 1 frames'
+  // are in flight while frame t is reduced
+  constexpr int PF = 4;
+  float xq[PF];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) xq[u] = load(u);
+  for (int t0 = 0; t0 < ps.count; t0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int t = t0 + u;
+      if (t >= ps.count) break;
+      const float val = is_max ? group_max<G>(xq[u]) : group_sum<G>(xq[u]);
+      xq[u] = load(t + PF);
+      fv[KT - 1] = val;
+      fok[KT - 1] = t < ps.T ? 1.f : 0.f;
+      const int64_t n = ps.n0 + t;
+      if (n >= g.d) {
+        // the window's frames as the per-step kernel combines them (tap q in
+        // lane q of a lane group, then an xor-shuffle tree), so both paths
+        // give the same bits; start padding contributes nothing
+        float tv[8], tc[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const bool in = q < KT && n - (KT - 1) + q >= 0;
+          tv[q] = in ? fv[q < KT ? q : 0] : neutral;
+          tc[q] = in ? fok[q < KT ? q : 0] : 0.f;
+        }
+#pragma unroll
+        for (int m = 4; m > 0; m >>= 1) {
+          float nv[8], nc[8];
+#pragma unroll
+          for (int l = 0; l < 8; ++l) {
+            nv[l] = is_max ? fmaxf(tv[l], tv[l ^ m]) : tv[l] + tv[l ^ m];
+            nc[l] = tc[l] + tc[l ^ m];
+          }
+#pragma unroll
+          for (int l = 0; l < 8; ++l) {
+            tv[l] = nv[l];
+            tc[l] = nc[l];
+          }
+        }
+        const float acc = tv[0], tcount = tc[0];
+        if (r == 0) {
+          float out;
+          if (is_max) {
+            out = acc;
+          } else {
+            const float div = g.count_include_pad ? float(KT * kHW) : tcount * float(vh * vw);
+            out = div > 0.f ? acc / div : 0.f;
+          }
+          yb[(n - ps.emit0) * So] = from_f32<T>(out);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q + 1 < KT; ++q) {
+        fv[q] = fv[q + 1];
+        fok[q] = fok[q + 1];
+      }
+    }
+  }
+  if (ps.update && r == 0) {
+    const int64_t n1 = ps.n0 + ps.count;
+#pragma unroll
+    for (int q = 0; q + 1 < KT; ++q) {
+      const int64_t rf = n1 - (KT - 1) + q;
+      if (rf >= 0) fifo[(rf % KT) * fifo_slot + idx] = fv[q];
+    }
+  }
+}
+
+// Validity flags of the FIFO slots the call's frames went to (one thread).
+__global__ void pool_valid_kernel(float* valid, int32_t R, int64_t n0, int32_t count, int32_t T) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int32_t first = count > R ? count - R : 0;
+  for (int32_t t = first; t < count; ++t) valid[(n0 + t) % R] = t < T ? 1.f : 0.f;
+}
+
 __global__ void pool_header_kernel(StateHeader h, StateHeader* dst) {
   if (threadIdx.x == 0 && blockIdx.x == 0) *dst = h;
 }
@@ -229,6 +378,70 @@ hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const v
     hipLaunchKernelGGL(pool_clip_kernel<float>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, T,
                        T_out, static_cast<const float*>(x), static_cast<float*>(y));
   return hipGetLastError();
+}
+
+namespace {
+
+template <typename T, int G, int KT>
+hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                             int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                             int64_t n0, bool update, hipStream_t s) {
+  PoolSteps ps;
+  ps.n0 = n0;
+  ps.count = count;
+  ps.T = nreal;
+  ps.emit0 = n0 > g.d ? n0 : g.d;
+  ps.update = update ? 1 : 0;
+  ps.fd_So = make_fastdiv(uint32_t(g.So()));
+  ps.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  ps.fd_kW = make_fastdiv(uint32_t(g.kW));
+  float* fifo = reinterpret_cast<float*>(state + L.fifo);
+  float* valid = reinterpret_cast<float*>(state + L.valid);
+  hipLaunchKernelGGL((pool_steps_kernel<T, G, KT>), dim3(grid_for(g.out_frame_elems() * G)),
+                     dim3(kBlock), 0, s, g, ps, static_cast<const T*>(x), x_bc,
+                     static_cast<T*>(y), y_bc, fifo, L.fifo_slot_elems, valid);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !update) return e;
+  hipLaunchKernelGGL(pool_valid_kernel, dim3(1), dim3(64), 0, s, valid, g.R, n0, count, nreal);
+  return hipGetLastError();
+}
+
+template <typename T, int G>
+hipError_t pool_steps_kt(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                         int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                         int64_t n0, bool update, hipStream_t s) {
+  switch (g.kT) {
+    case 1: return pool_steps_launch<T, G, 1>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 2: return pool_steps_launch<T, G, 2>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 3: return pool_steps_launch<T, G, 3>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 4: return pool_steps_launch<T, G, 4>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    case 5: return pool_steps_launch<T, G, 5>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t pool_steps_t(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                        int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                        int64_t n0, bool update, hipStream_t s) {
+  const int kHW = g.kH * g.kW;
+  if (kHW > 16) return pool_steps_kt<T, 64>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  if (kHW > 4) return pool_steps_kt<T, 16>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  return pool_steps_kt<T, 4>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+}
+
+}  // namespace
+
+bool pool_steps_supported(const PoolGeom& g) {
+  return g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64;  // (kT <= 8: tree)
+}
+
+hipError_t launch_pool_steps(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                             int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                             int64_t n0, bool update, hipStream_t s) {
+  if (g.dtype == CO_BF16)
+    return pool_steps_t<bf16_t>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  return pool_steps_t<float>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
 }
 
 }  // namespace coinf

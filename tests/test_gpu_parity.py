@@ -464,3 +464,120 @@ def test_gemm_img_forced(case):
         assert ys is None
     else:
         assert_close(np64(ys), rp, torch.bfloat16, "gemm_img steps pad_end")
+
+
+DW_STEPS_CASES = [
+    # B, C, kT, (kH, kW), in_size, (pT, pH, pW), dtype
+    (3, 20, 3, (3, 3), (7, 7), (0, 1, 1), "bf16"),    # the X3D-style block, small
+    (2, 12, 1, (3, 3), (6, 5), (0, 1, 1), "f32"),     # kT = 1: no ring
+    (2, 9, 2, (3, 3), (5, 8), (1, 0, 1), "f32"),      # delay 0, valid rows
+    (4, 16, 4, (1, 1), (3, 3), (3, 0, 0), "bf16"),    # pointwise taps, full padding
+    (1, 33, 5, (3, 3), (9, 4), (2, 1, 1), "f32"),     # ragged, kT = 5
+]
+
+
+@pytest.mark.parametrize("case", DW_STEPS_CASES, ids=lambda c: "dwsteps_" + "_".join(map(str, c[:3])))
+def test_depthwise_forward_steps_persistent(case):
+    """The depthwise forward_steps runs as one persistent launch (partial sums
+    in registers across frames).  Against the oracle with end padding, and
+    bitwise against the per-frame step kernel (same arithmetic order), also
+    when a clip continues a state left by single steps, after clean_state
+    (stale ring contents) and with update_state=False."""
+    B, C, kT, ks, size, p, dt = case
+    say("depthwise steps", case)
+    spec = synth.ConvSpec(batch=B, in_channels=C, out_channels=C, kernel=(kT,) + ks, in_size=size,
+                          padding=p, groups=C, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 14, 91000 + 13 * C + kT, "kaiming")
+    tdt = synth.torch_dtype(dt)
+    xd = x.to(DEV)
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=p, groups=C)
+
+    co = make()
+    assert co.algo == "depthwise"
+    ref = oracle_conv(w, b, (1, 1, 1), p, (1, 1, 1), C)
+    ys = co.forward_steps(xd, pad_end=True)
+    rp = ref.forward_steps(np64(x), pad_end=True)
+    assert_close(np64(ys), rp, tdt, "persistent depthwise steps")
+    # bitwise against single steps
+    co2 = make()
+    outs = [co2.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
+    outs = [o.clone() for o in outs if o is not None]
+    co.clean_state()
+    ys2 = co.forward_steps(xd)                      # after clean_state: stale ring contents
+    if outs:
+        assert torch.equal(ys2, torch.stack(outs, dim=2))
+    # a clip that continues single steps, and single steps after a clip
+    co3, co4 = make(), make()
+    for t in range(3):
+        co3.forward_step(xd[:, :, t].contiguous())
+    mid = co3.forward_steps(xd[:, :, 3:9].contiguous())
+    tail = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(9, x.shape[2])]
+    seq = [co4.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
+    seq = [s_.clone() for s_ in seq if s_ is not None]
+    got = ([mid[:, :, k] for k in range(mid.shape[2])] if mid is not None else []) + \
+        [t_ for t_ in tail if t_ is not None]
+    n_first = sum(1 for t in range(3) if t >= co3.delay)
+    assert len(got) == len(seq) - n_first
+    for g_, s_ in zip(got, seq[n_first:]):
+        assert torch.equal(g_, s_)
+    # update_state=False: same outputs, state bitwise unchanged
+    torch.cuda.synchronize()
+    before, n = co3.state.clone(), co3.steps
+    peek = co3.forward_steps(xd[:, :, 2:10].contiguous(), update_state=False)
+    torch.cuda.synchronize()
+    assert co3.steps == n and torch.equal(co3.state, before)
+    real = co3.forward_steps(xd[:, :, 2:10].contiguous())
+    assert torch.equal(peek, real)
+
+
+POOL_STEPS_CASES = [
+    # kind, kernel (time first), in_size, stride, padding, count_include_pad, dtype
+    ("avg", (4, 7, 7), (7, 7), (1, 7, 7), (0, 0, 0), True, "bf16"),   # the X3D-style pool
+    ("avg", (3, 3, 2), (7, 6), (1, 2, 1), (1, 1, 0), False, "f32"),
+    ("max", (5, 3, 3), (6, 5), (1, 1, 1), (2, 1, 1), True, "f32"),
+    ("max", (1, 2, 2), (4, 4), (1, 2, 2), (0, 0, 0), True, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", POOL_STEPS_CASES, ids=lambda c: "poolsteps_" + c[0] + str(c[1][0]))
+def test_pool_forward_steps_persistent(case):
+    """Pool forward_steps as one persistent launch against the oracle (end
+    padding), bitwise against per-frame steps, continuing a state left by
+    single steps, and with update_state=False."""
+    kind, ks, size, ss, ps, cip, dt = case
+    say("pool steps", case)
+    tdt = synth.torch_dtype(dt)
+    x = synth.normal((3, 6, 12) + size, 7700 + ks[0], dtype=dt)
+    xd = x.to(DEV)
+
+    def make():
+        return coinf.CoPool(kind, batch=3, channels=6, kernel=ks, in_size=size, stride=ss,
+                            padding=ps, count_include_pad=cip, dtype=tdt)
+
+    po = make()
+    ys = po.forward_steps(xd, pad_end=True)
+    r = oracle.ContinualPool(kind, ks, ss, ps, (1, 1, 1), cip, spatial_dims=2).forward_steps(
+        np64(x), pad_end=True)
+    assert_close(np64(ys), r, tdt, "persistent pool steps")
+    po2, po3 = make(), make()
+    seq = [po2.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
+    seq = [s_.clone() for s_ in seq if s_ is not None]
+    for t in range(2):
+        po3.forward_step(xd[:, :, t].contiguous())
+    mid = po3.forward_steps(xd[:, :, 2:8].contiguous())
+    tail = [po3.forward_step(xd[:, :, t].contiguous()) for t in range(8, x.shape[2])]
+    got = ([mid[:, :, k] for k in range(mid.shape[2])] if mid is not None else []) + \
+        [t_ for t_ in tail if t_ is not None]
+    n_first = sum(1 for t in range(2) if t >= po3.delay)
+    assert len(got) == len(seq) - n_first
+    for g_, s_ in zip(got, seq[n_first:]):
+        assert torch.equal(g_, s_)
+    torch.cuda.synchronize()
+    before, n = po3.state.clone(), po3.steps
+    peek = po3.forward_steps(xd[:, :, 1:9].contiguous(), pad_end=True, update_state=False)
+    torch.cuda.synchronize()
+    assert po3.steps == n and torch.equal(po3.state, before)
+    real = po3.forward_steps(xd[:, :, 1:9].contiguous(), pad_end=True)
+    assert torch.equal(peek, real)
