@@ -200,6 +200,16 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
                                 void* stream, int32_t* n_out);
 
 /*
+ * How co_conv_forward_steps runs a call over T frames into y_cap_frames
+ * output frames: *fused = 1 when the whole call is one persistent kernel
+ * launch that keeps the partial sums on chip across frames (temporal stride
+ * and dilation 1, on the depthwise and register-GEMM kernel families), 0 when
+ * it enqueues one step per frame.  Both give the same outputs.  Host-only.
+ */
+co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_frames,
+                              int32_t* fused);
+
+/*
  * forward (Principle 2, clip mode): the regular convolution of the clip
  * x (B, C_in, T, S1, S2) with symmetric temporal padding padding[0], written
  * to y (B, C_out, T_out, So1, So2), T_out = floor((T + 2p - f)/s) + 1 (0 when
@@ -289,6 +299,10 @@ co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
 co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, void* y,
                                 int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                                 void* stream, int32_t* n_out);
+
+/* As co_conv_steps_fused, for co_pool_forward_steps. */
+co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_frames,
+                              int32_t* fused);
 
 /* Clip-mode pooling with symmetric temporal padding; stateless. */
 co_status co_pool_forward(const co_pool_desc* desc, const void* x, int32_t T, void* y,

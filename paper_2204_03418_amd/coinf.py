@@ -97,6 +97,7 @@ co_conv_get_steps = _sig("co_conv_get_steps", i32, [vp, pi64])
 co_conv_attach_state = _sig("co_conv_attach_state", i32, [CD, vp, i64, i64, vp, pvp])
 co_conv_destroy = _sig("co_conv_destroy", i32, [vp])
 co_conv_algo_name = _sig("co_conv_algo_name", ctypes.c_char_p, [vp])
+co_conv_steps_fused = _sig("co_conv_steps_fused", i32, [vp, i32, i32, pi32])
 co_pool_query = _sig("co_pool_query", i32, [PD, PI])
 co_pool_plan_step = _sig("co_pool_plan_step", i32, [PD, i64, ctypes.POINTER(PoolPlan)])
 co_pool_init_state = _sig("co_pool_init_state", i32, [PD, vp, i64, vp, pvp])
@@ -104,6 +105,7 @@ co_pool_forward_step = _sig("co_pool_forward_step", i32, [vp, vp, vp, i32, vp])
 co_pool_forward_steps = _sig("co_pool_forward_steps", i32,
                              [vp, vp, i32, vp, i32, i32, i32, vp, pi32])
 co_pool_forward = _sig("co_pool_forward", i32, [PD, vp, i32, vp, vp])
+co_pool_steps_fused = _sig("co_pool_steps_fused", i32, [vp, i32, i32, pi32])
 co_pool_clip_frames = _sig("co_pool_clip_frames", i32, [PD, i32, pi32])
 co_pool_clean_state = _sig("co_pool_clean_state", i32, [vp, vp])
 co_pool_get_steps = _sig("co_pool_get_steps", i32, [vp, pi64])
@@ -313,6 +315,13 @@ class CoConv:
             return None
         return y[:, :, :n.value]
 
+    def steps_fused(self, T, pad_end=False):
+        """True when forward_steps over T frames runs as one persistent launch."""
+        cap = T + (self.desc.padding[0] if pad_end else 0)
+        f = i32()
+        check(co_conv_steps_fused(self.handle, T, cap, ctypes.byref(f)), "co_conv_steps_fused")
+        return bool(f.value)
+
     def forward(self, x):
         """Principle 2 forward (clip mode), stateless."""
         return conv_forward(self.desc, self.weight, self.bias, x)
@@ -412,6 +421,13 @@ class CoPool:
         if n.value == 0:
             return None
         return y[:, :, :n.value]
+
+    def steps_fused(self, T, pad_end=False):
+        """True when forward_steps over T frames runs as one persistent launch."""
+        cap = T + (self.desc.padding[0] if pad_end else 0)
+        f = i32()
+        check(co_pool_steps_fused(self.handle, T, cap, ctypes.byref(f)), "co_pool_steps_fused")
+        return bool(f.value)
 
     def forward(self, x):
         T = x.shape[2]

@@ -160,12 +160,14 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
   if (n_emit > 0 && !y) return CO_EINVAL;
   hipStream_t s = as_stream(stream);
   const int64_t n0 = h->n;
-  if (count > 0 && dw_steps_supported(g, T, y_cap_frames)) {
+  const bool dw = dw_steps_supported(g, T, y_cap_frames);
+  if (count > 0 && (dw || reg_steps_supported(g, T, y_cap_frames))) {
     // one persistent launch: partial sums stay in registers across frames;
     // with update_state = 0 the state is simply not written back
-    const co_status st = hip_status(launch_conv_steps_depthwise(
-        g, h->L, h->state, x, int64_t(T) * g.S(), T, int32_t(count), y,
-        int64_t(y_cap_frames) * g.So(), n0, update_state != 0, s));
+    const auto launch = dw ? launch_conv_steps_depthwise : launch_conv_steps_reg;
+    const co_status st = hip_status(launch(g, h->L, h->state, x, int64_t(T) * g.S(), T,
+                                           int32_t(count), y, int64_t(y_cap_frames) * g.So(),
+                                           n0, update_state != 0, s));
     if (st != CO_OK) return st;
     if (update_state) h->n += count;
     *n_out = int32_t(n_emit);
@@ -203,6 +205,15 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
   }
   *n_out = int32_t(k);
   return st;
+}
+
+co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_frames,
+                              int32_t* fused) {
+  if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
+  *fused = dw_steps_supported(h->g, T, y_cap_frames) || reg_steps_supported(h->g, T, y_cap_frames)
+               ? 1
+               : 0;
+  return CO_OK;
 }
 
 co_status co_conv_clip_frames(const co_conv_desc* desc, int32_t T, int32_t* t_out) {
@@ -340,6 +351,13 @@ co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
   }
   if (update_state) ++h->n;
   return plan.emit ? CO_OK : CO_EMPTY;
+}
+
+co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_frames,
+                              int32_t* fused) {
+  if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
+  *fused = pool_steps_supported(h->g) ? 1 : 0;
+  return CO_OK;
 }
 
 co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, void* y,

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
       int vlast[8];  // last block: element e exists iff e < nv_last
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        vlast[e] = ok & (e < nv_last) ? vt + int(uint32_t(e) * plane_b) : kOutOfRange;
+        vlast[e] = (ok & (e < nv_last)) ? vt + int(uint32_t(e) * plane_b) : kOutOfRange;
 #pragma unroll
       for (int cb = 0; cb < CSMAX; ++cb) {
         const bool live = EXACT || cb < ra.CS;  // wave-uniform
@@ -294,14 +294,14 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
     const v4f v = acc[f] + prev[f];
     if constexpr (VEC) {  // M % 4 == 0: a lane's four pixels are all valid or none
       __builtin_amdgcn_raw_buffer_store_b128(
-          __builtin_bit_cast(v4u, v), rr, to_ring & (P0 < ra.M) ? (e_off[f] + P0) * 4 : kOutOfRange,
+          __builtin_bit_cast(v4u, v), rr, (to_ring & (P0 < ra.M)) ? (e_off[f] + P0) * 4 : kOutOfRange,
           0, 0);
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         __builtin_amdgcn_raw_buffer_store_b32(
             __float_as_uint(v[r]), rr,
-            to_ring & (P0 + r < ra.M) ? (e_off[f] + P0 + r) * 4 : kOutOfRange, 0, 0);
+            (to_ring & (P0 + r < ra.M)) ? (e_off[f] + P0 + r) * 4 : kOutOfRange, 0, 0);
     }
     const int o = e_o[f];
 #pragma unroll
@@ -316,7 +316,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
         pq = P0 + r - bq * ra.So;
       }
       const int yo = ((bq * g.Cout + o) * ra.y_bc + pq) * yesz;
-      const int off = to_y & (P0 + r < ra.M) ? yo : kOutOfRange;
+      const int off = (to_y & (P0 + r < ra.M)) ? yo : kOutOfRange;
       const float val = v[r] + e_bias[f];
       if constexpr (sizeof(T) == 2)
         __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)), yr, off,
@@ -431,6 +431,326 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   return hipGetLastError();
 }
 
+// ---- persistent forward_steps -------------------------------------------
+//
+// Temporal stride and dilation 1: at virtual time v = n + pT the arriving
+// frame feeds output v - j through temporal tap j, and output v - (kT - 1) is
+// complete.  A wave owns 16 output pixels x 16 output channels for every
+// temporal tap, so the kT - 1 partial sums it continues are its own: they
+// stay in registers for the whole clip (the ring is read at the start and
+// written back at the end), and only the frames and the emitted outputs move
+// through memory.  Weights stay in registers too.  Per frame and tap the
+// products are summed over the k-steps in the order of the step kernel of
+// the same instantiation (split halves added first half + second), then
+// added to the partial sum, so forward_steps reproduces forward_step.
+struct RegSteps {
+  int32_t M, So, m_frags, o_frags, blocks_per_xcd;
+  int32_t ntaps, CS, CSU;
+  int32_t dh[kRegMaxTaps], dw[kRegMaxTaps];
+  int32_t x_bytes, w_bytes, ring_bytes, ring_slot, y_bytes;
+  int32_t fstride;  // bytes between consecutive frames of the clip
+  int32_t y_bc;     // elements between (stream, channel) planes of y
+  int32_t v0;       // virtual time of the first frame, capped at 2^29
+  int32_t slot_v0;  // v0 mod R (uncapped)
+  int32_t count, T, k0, update;
+  FastDiv fd_So, fd_Wo, fd_ofr;
+};
+
+template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM>
+__global__ __launch_bounds__(64 * kRegWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
+                           T* __restrict__ y, const uint4* __restrict__ wp,
+                           const float* __restrict__ bias, float* __restrict__ ring) {
+  constexpr bool kBF = sizeof(T) == 2;
+  constexpr int CL = kBF ? 8 : 1;
+  constexpr int CKS = 4 * CL;
+  constexpr int CSUMAX = kBF ? CSMAX : (CSMAX + 3) / 4;
+  constexpr int TH = TAPS / KSPLIT;  // spatial taps per partial chain
+  constexpr int AREGS = TAPS * CSMAX * (kBF ? 4 : 1);
+  constexpr int PF = AREGS <= 16 ? 4 : 2;  // frames in flight
+  using AReg = typename std::conditional<kBF, uint4, float>::type;
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int bid = int(blockIdx.x);
+  const int lb = (bid & 7) * rs.blocks_per_xcd + (bid >> 3);
+  const int tile = lb * kRegWaves + wave;
+  if (tile >= rs.m_frags * rs.o_frags) return;  // whole waves; no barrier follows
+  const int mf = fdiv(tile, rs.fd_ofr);
+  const int of = tile - mf * rs.o_frags;
+  const int kT = g.kT;
+
+  // ---- weights, once: column (tap j, channel o) of the step kernel's packing
+  const int o = of * 16 + lrow;
+  const bool ocol = o < g.Cout;
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(wp, rs.w_bytes);
+  uint4 wreg[KTM][TAPS][CSUMAX];
+#pragma unroll
+  for (int j = 0; j < KTM; ++j) {
+    const int n = j * g.Cout + o;
+    const int nf = n >> 4, r = n & 15;
+#pragma unroll
+    for (int tp = 0; tp < TAPS; ++tp)
+#pragma unroll
+      for (int cq = 0; cq < CSUMAX; ++cq) {
+        const bool ok = ocol & (j < kT) & (tp < rs.ntaps) & (cq < rs.CSU);
+        const int off = (((nf * rs.ntaps + tp) * rs.CSU + cq) << 10) + (lgrp * 16 + r) * 16;
+        const auto w4 = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? off : kOutOfRange, 0, 0);
+        wreg[j][tp][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+  }
+  const __amdgpu_buffer_rsrc_t br = make_rsrc(bias, g.Cout * 4);
+  const float bo = __uint_as_float(
+      __builtin_amdgcn_raw_buffer_load_b32(br, ocol ? o * 4 : kOutOfRange, 0, 0));
+
+  // ---- output rows of this lane: pixels P0 .. P0 + 3 of channel o
+  const int P0 = mf * 16 + lgrp * 4;
+  constexpr uint32_t esz = sizeof(T);
+  int yoff[4];  // byte offset of (b, o, frame 0, p) in y, or out of range
+  int roff[4];  // float offset of (o, P) inside a ring slot, or -1
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int P = P0 + r;
+    const bool ok = ocol & (P < rs.M);
+    const int b = fdiv(ok ? P : 0, rs.fd_So), p = (ok ? P : 0) - b * rs.So;
+    yoff[r] = ok ? int((uint32_t(b * g.Cout + o) * uint32_t(rs.y_bc) + uint32_t(p)) * esz)
+                 : kOutOfRange;
+    roff[r] = ok ? o * rs.M + P : -1;
+  }
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, rs.y_bytes);
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(ring, rs.ring_bytes);
+  const int R = g.R;
+
+  // ---- partial sums: part[j] continues output v - j (1 <= j <= kT - 1)
+  v4f part[KTM];
+#pragma unroll
+  for (int j = 1; j < KTM; ++j) {
+    part[j] = v4f{0.f, 0.f, 0.f, 0.f};
+    const int tau = rs.v0 - j;
+    if (j < kT && tau >= 0) {  // uniform
+      const int sl = (rs.slot_v0 - j + R) % R;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        part[j][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+            rr, roff[r] >= 0 ? (sl * rs.ring_slot + roff[r]) * 4 : kOutOfRange, 0, 0));
+    }
+  }
+
+  // ---- operand gathers of one frame (as in the step kernel; the frame
+  // offset rides in the wave-uniform scalar operand)
+  const int P = mf * 16 + lrow;
+  const bool pvalid = P < rs.M;
+  const int Pc = pvalid ? P : 0;
+  const int b = fdiv(Pc, rs.fd_So), p = Pc - b * rs.So;
+  const int i = fdiv(p, rs.fd_Wo), jw = p - i * g.Wo;
+  const int hb = i * g.sH - g.pH, wb = jw * g.sW - g.pW;
+  const int lane_c = lgrp * CL;
+  const uint32_t plane_b = uint32_t(x_bc) * esz;
+  const uint32_t lane_b = (uint32_t(b) * uint32_t(g.Cin) + uint32_t(lane_c)) * plane_b;
+  const int nv_last = min(max(g.Cin - ((rs.CS - 1) * CKS + lane_c), 0), CL);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, rs.x_bytes);
+  int vt[TAPS];
+#pragma unroll
+  for (int tp = 0; tp < TAPS; ++tp) {
+    const int hi = hb + rs.dh[tp], wi = wb + rs.dw[tp];
+    const bool ok = (tp < rs.ntaps) & pvalid & (unsigned(hi) < unsigned(g.H)) &
+                    (unsigned(wi) < unsigned(g.W));
+    vt[tp] = ok ? int(lane_b + (uint32_t(hi) * uint32_t(g.W) + uint32_t(wi)) * esz) : kOutOfRange;
+  }
+  auto load_frame = [&](int t, AReg (&a)[TAPS][CSMAX]) {
+    if (t < rs.T) {  // uniform; end-padding frames are zero
+      const int fo = t * rs.fstride;
+#pragma unroll
+      for (int tp = 0; tp < TAPS; ++tp)
+#pragma unroll
+        for (int cb = 0; cb < CSMAX; ++cb) {
+          const bool live = cb < rs.CS, last = cb == rs.CS - 1;  // uniform
+          const int sb = int(uint32_t(cb * CKS) * plane_b) + fo;
+          if constexpr (kBF) {
+            uint32_t r8[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int v = live & (!last | (e < nv_last)) ? vt[tp] : kOutOfRange;
+              r8[e] = __builtin_amdgcn_raw_buffer_load_b16(xr, v, sb + int(uint32_t(e) * plane_b), 0);
+            }
+            a[tp][cb] = make_uint4(r8[0] | (r8[1] << 16), r8[2] | (r8[3] << 16),
+                                   r8[4] | (r8[5] << 16), r8[6] | (r8[7] << 16));
+          } else {
+            const int v = live & (!last | (nv_last > 0)) ? vt[tp] : kOutOfRange;
+            a[tp][cb] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xr, v, sb, 0));
+          }
+        }
+    } else {
+#pragma unroll
+      for (int tp = 0; tp < TAPS; ++tp)
+#pragma unroll
+        for (int cb = 0; cb < CSMAX; ++cb) {
+          if constexpr (kBF)
+            a[tp][cb] = make_uint4(0u, 0u, 0u, 0u);
+          else
+            a[tp][cb] = 0.f;
+        }
+    }
+  };
+
+  AReg areg[PF][TAPS][CSMAX];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) load_frame(u, areg[u]);
+
+  for (int t0 = 0; t0 < rs.count; t0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int t = t0 + u;
+      if (t >= rs.count) break;
+      const int v = rs.v0 + t;
+      // products of every temporal tap, each as KSPLIT chains over k-steps
+      v4f c[KTM][KSPLIT];
+#pragma unroll
+      for (int j = 0; j < KTM; ++j)
+#pragma unroll
+        for (int h = 0; h < KSPLIT; ++h) c[j][h] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i2 = 0; i2 < TH; ++i2)
+#pragma unroll
+        for (int cb = 0; cb < CSMAX; ++cb)
+#pragma unroll
+          for (int h = 0; h < KSPLIT; ++h)
+#pragma unroll
+            for (int j = 0; j < KTM; ++j) {
+              if (j >= kT) continue;  // uniform
+              const int tp = h * TH + i2;
+              if constexpr (kBF) {
+                c[j][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(v8bf, areg[u][tp][cb]),
+                    __builtin_bit_cast(v8bf, wreg[j][tp][cb]), c[j][h], 0, 0, 0);
+              } else {
+                const uint4 u4 = wreg[j][tp][cb / 4];
+                const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
+                c[j][h] = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[u][tp][cb], __uint_as_float(bw),
+                                                               c[j][h], 0, 0, 0);
+              }
+            }
+      // the next frames' operands are requested before this frame's epilogue
+      load_frame(t + PF, areg[u]);
+      // fold each product into its output: tap j completes v - (kT - 1),
+      // starts at the first tap on a real frame, continues otherwise
+      v4f nxt[KTM];
+#pragma unroll
+      for (int j = 0; j < KTM; ++j) {
+        nxt[j] = v4f{0.f, 0.f, 0.f, 0.f};
+        if (j >= kT) continue;
+        const int tau = v - j;
+        if (tau < 0) continue;  // no such output (uniform)
+        const int first = tau >= g.pT ? 0 : g.pT - tau;
+        v4f sum = c[j][0];
+        if constexpr (KSPLIT == 2) sum = sum + c[j][1];
+        const v4f a = (j == first) ? sum : sum + part[j];
+        if (j == kT - 1) {
+          const int fo = (rs.k0 + t) * rs.So * int(esz);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float val = a[r] + bo;
+            if constexpr (kBF)
+              __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)),
+                                                    yr, yoff[r], fo, 0);
+            else
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, yoff[r], fo, 0);
+          }
+        } else {
+          nxt[j] = a;
+        }
+      }
+      // output v - j continues as v + 1 - (j + 1)
+#pragma unroll
+      for (int j = KTM - 1; j >= 1; --j) part[j] = nxt[j - 1];
+    }
+  }
+
+  if (rs.update) {
+    const int v1 = rs.v0 + rs.count;
+    const int s1 = (rs.slot_v0 + rs.count) % R;
+#pragma unroll
+    for (int j = 1; j < KTM; ++j) {
+      const int tau = v1 - j;
+      if (j < kT && tau >= 0) {  // uniform
+        const int sl = (s1 - j + R) % R;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          __builtin_amdgcn_raw_buffer_store_b32(
+              __float_as_uint(part[j][r]), rr,
+              roff[r] >= 0 ? (sl * rs.ring_slot + roff[r]) * 4 : kOutOfRange, 0, 0);
+      }
+    }
+  }
+}
+
+// Instantiations: (step-kernel shape id, largest kT).  Registers hold
+// kT x taps x channel blocks of weights, so deep temporal kernels go with
+// 1x1 spatial taps only.
+struct RegStepsShape {
+  int32_t cfg, ktm;
+};
+// (Step shapes 7 and 8 hold too many operand registers to add weights for
+// even three temporal taps without spilling; their forward_steps loop over
+// single steps.)
+constexpr RegStepsShape kRegStepsShapes[] = {
+    {0, 3}, {0, 9}, {1, 3}, {2, 3}, {3, 3}, {4, 3}, {5, 3}, {5, 9}, {6, 3}, {6, 9}, {9, 3},
+};
+
+int reg_steps_ktm(const ConvGeom& g) {
+  int best = 0;
+  for (const auto& sh : kRegStepsShapes)
+    if (sh.cfg == g.cfg && g.kT <= sh.ktm && (best == 0 || sh.ktm < best)) best = sh.ktm;
+  return best;
+}
+
+template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM>
+hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L,
+                            char* state, const void* x, int64_t x_bc, int32_t nreal,
+                            int32_t count, void* y, int64_t y_bc, int64_t n0, bool update,
+                            hipStream_t s) {
+  RegSteps rs;
+  rs.M = int32_t(int64_t(g.B) * g.So());
+  rs.So = int32_t(g.So());
+  rs.m_frags = c.m_frags;
+  rs.o_frags = int32_t(ceil_div(g.Cout, 16));
+  const int64_t blocks = ceil_div(int64_t(rs.m_frags) * rs.o_frags, kRegWaves);
+  rs.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
+  rs.ntaps = g.kH * g.kW;
+  rs.CS = c.CS;
+  rs.CSU = c.CSU;
+  for (int tp = 0; tp < kRegMaxTaps; ++tp) {
+    const int u = tp < rs.ntaps ? tp / g.kW : 0, v = tp < rs.ntaps ? tp % g.kW : 0;
+    rs.dh[tp] = u * g.dH;
+    rs.dw[tp] = v * g.dW;
+  }
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  rs.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  rs.w_bytes = int32_t(L.weight_bytes);
+  rs.ring_slot = int32_t(L.ring_slot_elems);
+  rs.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
+  rs.y_bytes = int32_t(int64_t(g.B) * g.Cout * y_bc * esz);
+  rs.fstride = int32_t(g.S() * esz);
+  rs.y_bc = int32_t(y_bc);
+  const int64_t v0 = n0 + g.pT;
+  rs.v0 = int32_t(v0 < (int64_t(1) << 29) ? v0 : (int64_t(1) << 29));
+  rs.slot_v0 = int32_t(v0 % g.R);
+  rs.count = count;
+  rs.T = nreal;
+  rs.k0 = int32_t(n0 - (n0 > g.d ? n0 : g.d));
+  rs.update = update ? 1 : 0;
+  rs.fd_So = make_fastdiv(uint32_t(rs.So));
+  rs.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  rs.fd_ofr = make_fastdiv(uint32_t(rs.o_frags));
+  hipLaunchKernelGGL((conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM>),
+                     dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g, rs,
+                     static_cast<const T*>(x), x_bc, static_cast<T*>(y),
+                     reinterpret_cast<const uint4*>(state + L.weight),
+                     reinterpret_cast<const float*>(state + L.bias),
+                     reinterpret_cast<float*>(state + L.ring));
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* state,
@@ -457,6 +777,44 @@ hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* st
     case 9: return reg_launch<bf16_t, 2, 9, 1, 1>(g, c, L, state, io, plan, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+bool reg_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
+  if (g.algo != CO_ALGO_GEMM_REG || g.sT != 1 || g.dT != 1 || reg_steps_ktm(g) == 0) return false;
+  RegConfig c;
+  if (!reg_config(g, g.cfg, &c)) return false;
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  const int64_t lim = int64_t(1) << 31;
+  return int64_t(g.B) * g.Cin * x_frames * g.S() * esz < lim &&
+         int64_t(g.B) * g.Cout * y_frames * g.So() * esz < lim &&
+         int64_t(g.R) * int64_t(conv_layout(g).ring_slot_elems) * 4 < lim &&
+         conv_layout(g).weight_bytes < (int64_t(1) << 30);
+}
+
+hipError_t launch_conv_steps_reg(const ConvGeom& g, const ConvLayout& L, char* state,
+                                 const void* x, int64_t x_bc, int32_t nreal, int32_t count,
+                                 void* y, int64_t y_bc, int64_t n0, bool update, hipStream_t s) {
+  RegConfig c;
+  if (!reg_config(g, g.cfg, &c)) return hipErrorInvalidValue;
+  const int ktm = reg_steps_ktm(g);
+#define CO_STEPS(TY, TAPS, CSMAX, KSPLIT, KTM) \
+  reg_steps_launch<TY, TAPS, CSMAX, KSPLIT, KTM>(g, c, L, state, x, x_bc, nreal, count, y, y_bc, \
+                                                 n0, update, s)
+  switch (c.id * 16 + ktm) {
+    case 0 * 16 + 3: return CO_STEPS(float, 1, 16, 1, 3);
+    case 0 * 16 + 9: return CO_STEPS(float, 1, 16, 1, 9);
+    case 1 * 16 + 3: return CO_STEPS(float, 1, 32, 1, 3);
+    case 2 * 16 + 3: return CO_STEPS(float, 9, 6, 1, 3);
+    case 3 * 16 + 3: return CO_STEPS(float, 9, 3, 1, 3);
+    case 4 * 16 + 3: return CO_STEPS(float, 10, 6, 2, 3);
+    case 5 * 16 + 3: return CO_STEPS(bf16_t, 1, 2, 1, 3);
+    case 5 * 16 + 9: return CO_STEPS(bf16_t, 1, 2, 1, 9);
+    case 6 * 16 + 3: return CO_STEPS(bf16_t, 1, 4, 1, 3);
+    case 6 * 16 + 9: return CO_STEPS(bf16_t, 1, 4, 1, 9);
+    case 9 * 16 + 3: return CO_STEPS(bf16_t, 9, 1, 1, 3);
+    default: return hipErrorInvalidValue;
+  }
+#undef CO_STEPS
 }
 
 hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,

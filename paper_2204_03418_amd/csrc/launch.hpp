@@ -71,6 +71,13 @@ hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* s
                                  const StepIO& io, const co_step_plan& plan, hipStream_t stream);
 hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* state,
                                 const StepIO& io, const co_step_plan& plan, hipStream_t stream);
+// Persistent forward_steps of the register-GEMM step (same conventions as
+// the depthwise one): temporal stride 1 and dilation 1, kT within what the
+// step kernel's instantiation can hold in registers.
+bool reg_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames);
+hipError_t launch_conv_steps_reg(const ConvGeom& g, const ConvLayout& L, char* state,
+                                 const void* x, int64_t x_bc, int32_t T, int32_t count, void* y,
+                                 int64_t y_bc, int64_t n0, bool update, hipStream_t stream);
 hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,
                            const void* weight, hipStream_t stream);
 hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* state,

@@ -532,6 +532,108 @@ def test_depthwise_forward_steps_persistent(case):
     assert torch.equal(peek, real)
 
 
+def _check_fused_steps(make, x, ref, tdt, what):
+    """forward_steps as one persistent launch: against the oracle with end
+    padding; bitwise against per-frame forward_step (same per-tap arithmetic
+    order), also after clean_state (stale ring contents); a clip continuing a
+    state left by single steps and single steps continuing a clip; and
+    update_state=False (same outputs, state unchanged)."""
+    xd = x.to(DEV)
+    T = x.shape[2]
+    co = make()
+    assert co.steps_fused(T, pad_end=True), (what, co.algo)
+    ys = co.forward_steps(xd, pad_end=True)
+    rp = ref.forward_steps(np64(x), pad_end=True)
+    assert_close(np64(ys), rp, tdt, what)
+    co2 = make()
+    outs = [co2.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    outs = [o.clone() for o in outs if o is not None]
+    co.clean_state()
+    ys2 = co.forward_steps(xd)
+    if outs:
+        assert torch.equal(ys2, torch.stack(outs, dim=2)), what
+    co3, co4 = make(), make()
+    for t in range(3):
+        co3.forward_step(xd[:, :, t].contiguous())
+    mid = co3.forward_steps(xd[:, :, 3:9].contiguous())
+    tail = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(9, T)]
+    seq = [co4.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    seq = [s_.clone() for s_ in seq if s_ is not None]
+    got = ([mid[:, :, k] for k in range(mid.shape[2])] if mid is not None else []) + \
+        [t_ for t_ in tail if t_ is not None]
+    n_first = sum(1 for t in range(3) if t >= co3.delay)
+    assert len(got) == len(seq) - n_first
+    for g_, s_ in zip(got, seq[n_first:]):
+        assert torch.equal(g_, s_), what
+    torch.cuda.synchronize()
+    before, n = co3.state.clone(), co3.steps
+    peek = co3.forward_steps(xd[:, :, 2:10].contiguous(), update_state=False)
+    torch.cuda.synchronize()
+    assert co3.steps == n and torch.equal(co3.state, before), what
+    real = co3.forward_steps(xd[:, :, 2:10].contiguous())
+    assert (peek is None and real is None) or torch.equal(peek, real), what
+
+
+REG_STEPS_CASES = [
+    # B, C_in, C_out, kernel (time first), in_size, padding, dtype, frames
+    (1, 24, 24, (3, 3, 3), (20, 20), (0, 1, 1), "f32", 12),   # 3x3, two waves per tile
+    (2, 20, 32, (3, 3, 3), (40, 40), (1, 1, 1), "f32", 12),   # 3x3, one wave per tile
+    (4, 12, 32, (3, 3, 3), (40, 40), (1, 1, 1), "f32", 12),   # 3x3, two columns per wave
+    (4, 32, 32, (3, 3, 3), (40, 40), (2, 1, 1), "bf16", 12),  # bf16 3x3
+    (3, 40, 20, (3, 1), (13,), (1, 0), "f32", 14),            # 1x1 spatial, small
+    (32, 96, 128, (9, 1), (25,), (4, 0), "bf16", 14),         # deep temporal kernel, bf16
+    (2, 7, 17, (1, 3, 3), (6, 9), (0, 1, 1), "f32", 12),      # kT = 1: no ring
+]
+
+
+@pytest.mark.parametrize("case", REG_STEPS_CASES, ids=lambda c: "regsteps_" + "_".join(
+    map(str, c[:3])) + "_" + c[6])
+def test_reg_forward_steps_persistent(case):
+    """The register-GEMM forward_steps as one persistent launch (partial sums
+    in accumulator registers across frames)."""
+    B, cin, cout, k, size, p, dt, T = case
+    say("reg steps", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          padding=p, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, T, 93000 + 7 * cin + cout, "kaiming")
+    tdt = synth.torch_dtype(dt)
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=p)
+
+    assert make().algo.startswith("gemm_reg")
+    ones = (1,) * len(k)
+    _check_fused_steps(make, x, oracle_conv(w, b, ones, p, ones, 1), tdt, "reg steps")
+
+
+@pytest.mark.parametrize("name,streams", [
+    ("conv3d_b1_c24_k3_56x56_f32", None),
+    ("conv2d_b32_c64to256_k9x1_v25_f32", (0, 13, 31)),
+    ("conv2d_b32_c64to256_k9x1_v25_bf16", (2, 29)),
+])
+def test_workload_forward_steps_fused(name, streams):
+    """Full-size forward_steps as one launch over the workload's clip: the
+    oracle recomputes every stream or sampled ones; bitwise against the
+    per-frame step kernel."""
+    wl = synth.WORKLOADS[name]
+    c = wl.conv
+    say("workload forward_steps", name)
+    x, w, b = synth.workload_inputs(name)
+    x = x[:, :, :40].contiguous()
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size, stride=c.stride,
+                      padding=c.padding, dilation=c.dilation, groups=c.groups)
+    assert co.steps_fused(x.shape[2])
+    xd = x.to(DEV)
+    ys = co.forward_steps(xd)
+    co2 = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size, stride=c.stride,
+                       padding=c.padding, dilation=c.dilation, groups=c.groups)
+    outs = _run_steps(co2, xd)
+    assert torch.equal(ys, torch.stack(outs, dim=2))
+    sel = list(streams) if streams else list(range(c.batch))
+    ref = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x[sel]))
+    assert_close(np64(ys[sel]), ref, synth.torch_dtype(c.dtype), name)
+
+
 POOL_STEPS_CASES = [
     # kind, kernel (time first), in_size, stride, padding, count_include_pad, dtype
     ("avg", (4, 7, 7), (7, 7), (1, 7, 7), (0, 0, 0), True, "bf16"),   # the X3D-style pool
