@@ -266,13 +266,17 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   const int plane_bytes = int(x_bc * int64_t(sizeof(T)));
   // channels past C_in read the next stream's planes or past the buffer end
   // (zero); they are masked when stored
-  auto prefetch = [&](int ch) {
+  // `part` < 0: all of chunk ch's loads; else the share issued during
+  // spatial tap `part`, so the loads trickle out between the matrix
+  // instructions instead of queueing all at once in front of them
+  auto prefetch = [&](int ch, int part) {
     const int cbase = ch * CK;
 #pragma unroll
     for (int ai = 0; ai < AI; ++ai)
 #pragma unroll
       for (int e = 0; e < KL; ++e)
-        ra[ai][e] = Stage<T>::load(xr, a_src[ai], (cbase + e) * plane_bytes, PAIR);
+        if (part < 0 || (ai * KL + e) % KHW == part)
+          ra[ai][e] = Stage<T>::load(xr, a_src[ai], (cbase + e) * plane_bytes, PAIR);
   };
   auto store_a = [&](int buf, int ch) {
     uint4* As = As0 + buf * a_units;
@@ -293,13 +297,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   };
   // B: the pre-packed block of (n_tile, ch) goes straight from global memory
   // into LDS (global_load_lds_dwordx4; each wave fills 1 KB contiguously)
-  auto copy_b = [&](int ch, int buf) {
+  auto copy_b = [&](int ch, int buf, int part) {
     const uint4* wsrc = wp + (int64_t(n_tile) * ga.n_chunks + ch) * B_UNITS;
     uint4* Bs = Bs0 + buf * B_UNITS;
 #pragma unroll
     for (int bi = 0; bi < BI; ++bi) {
       const int u0 = wave * 64 + bi * NT;  // first unit of this wave's 1 KB
-      if (u0 < B_UNITS)
+      if ((part < 0 || bi % KHW == part) && u0 < B_UNITS)
         __builtin_amdgcn_global_load_lds(wsrc + u0 + lane,
                                          (__attribute__((address_space(3))) void*)(Bs + u0),
                                          16, 0, 0);
@@ -363,17 +367,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   }
 
   __syncthreads();  // zero fill done
-  copy_b(0, 0);
-  prefetch(0);
+  copy_b(0, 0, -1);
+  prefetch(0, -1);
   store_a(0, 0);
   __builtin_amdgcn_s_waitcnt(0);  // LDS-direct loads of B have landed
   __syncthreads();
   for (int ch = 0; ch < ga.n_chunks; ++ch) {
     const bool more = ch + 1 < ga.n_chunks;
-    if (more) {  // next chunk's global loads are in flight during the MFMAs
-      copy_b(ch + 1, (ch + 1) & 1);
-      prefetch(ch + 1);
-    }
     const uint4* As = As0 + (ch & 1) * a_units;
     const uint4* Bs = Bs0 + (ch & 1) * B_UNITS;
     Frag af[2][WM], bf[2][WN];
@@ -392,6 +392,10 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
       // the next tap's fragments are requested before this tap's MFMAs, so
       // LDS latency hides behind WM*WN matrix instructions
       if (uv + 1 < KHW) load_frags(uv + 1, (uv + 1) & 1);
+      if (more) {  // next chunk's global loads are in flight during the MFMAs
+        copy_b(ch + 1, (ch + 1) & 1, uv);
+        prefetch(ch + 1, uv);
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int mf = 0; mf < WM; ++mf)
