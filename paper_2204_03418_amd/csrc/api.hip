@@ -26,6 +26,12 @@ namespace {
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
+// The persistent direct kernel indexes y with 64-bit offsets; its element
+// index per (stream, channel) plane stays 32-bit.
+bool y_steps_fit(const ConvGeom& g, int64_t y_frames) {
+  return int64_t(g.B) * g.Cout * y_frames * g.So() < (int64_t(1) << 31);
+}
+
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_EHIP; }
 
 bool any_tap(const co_step_plan& p) {
@@ -161,10 +167,12 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
   hipStream_t s = as_stream(stream);
   const int64_t n0 = h->n;
   const bool dw = dw_steps_supported(g, T, y_cap_frames);
-  if (count > 0 && (dw || reg_steps_supported(g, T, y_cap_frames))) {
+  const bool dir = direct_steps_supported(g, T) && y_steps_fit(g, y_cap_frames);
+  if (count > 0 && (dw || dir || reg_steps_supported(g, T, y_cap_frames))) {
     // one persistent launch: partial sums stay in registers across frames;
     // with update_state = 0 the state is simply not written back
-    const auto launch = dw ? launch_conv_steps_depthwise : launch_conv_steps_reg;
+    const auto launch = dw ? launch_conv_steps_depthwise
+                           : dir ? launch_conv_steps_direct : launch_conv_steps_reg;
     const co_status st = hip_status(launch(g, h->L, h->state, x, int64_t(T) * g.S(), T,
                                            int32_t(count), y, int64_t(y_cap_frames) * g.So(),
                                            n0, update_state != 0, s));
@@ -210,7 +218,10 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
 co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused) {
   if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
-  *fused = dw_steps_supported(h->g, T, y_cap_frames) || reg_steps_supported(h->g, T, y_cap_frames)
+  const ConvGeom& g = h->g;
+  *fused = dw_steps_supported(g, T, y_cap_frames) ||
+                   (direct_steps_supported(g, T) && y_steps_fit(g, y_cap_frames)) ||
+                   reg_steps_supported(g, T, y_cap_frames)
                ? 1
                : 0;
   return CO_OK;

@@ -149,6 +149,158 @@ hipError_t step_direct_t(const ConvGeom& g, const ConvLayout& L, char* state, co
   return hipGetLastError();
 }
 
+// Persistent forward_steps for small direct layers (temporal stride and
+// dilation 1): one thread per output element keeps its weights, the kT - 1
+// partial sums it continues and the next frames' inputs in registers for the
+// whole clip.  Positions e = (c, u, v) of the reduction are fixed; taps
+// outside the frame read zero, which leaves the sum unchanged, so each
+// temporal tap's sum runs in the step kernel's order and forward_steps
+// matches repeated forward_step.
+struct DirSteps {
+  int32_t v0;       // virtual time of the first frame, capped at 2^29
+  int32_t slot_v0;  // v0 mod R (uncapped)
+  int32_t count, T, k0, update;
+  int32_t x_bytes;
+  int32_t fstride;  // bytes between consecutive frames of the clip
+  FastDiv fd_So, fd_Cout, fd_Wo;
+};
+
+constexpr int kDirStepsKX = 16;  // reduction positions C_in/G * kH * kW held in registers
+constexpr int kDirStepsKT = 4;   // temporal taps held in registers
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
+    ConvGeom g, DirSteps ds, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
+    int64_t y_bc, const float* __restrict__ w, const float* __restrict__ bias,
+    float* __restrict__ ring, int64_t ring_slot) {
+  constexpr int KX = kDirStepsKX, KTM = kDirStepsKT, PF = 4;
+  constexpr uint32_t esz = sizeof(T);
+  const int32_t So = g.Ho * g.Wo;
+  const int32_t total = g.B * g.Cout * So;
+  const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  if (idx >= total) return;
+  const int32_t bo = fdiv(idx, ds.fd_So);
+  const int32_t p = idx - bo * So;
+  const int32_t b = fdiv(bo, ds.fd_Cout);
+  const int32_t o = bo - b * g.Cout;
+  const int32_t i = fdiv(p, ds.fd_Wo), jo = p - i * g.Wo;
+  const int32_t grp = o / g.Og;
+  const int32_t kHW = g.kH * g.kW;
+  const int32_t kT = g.kT;
+  const int32_t nk = g.Cg * kHW;
+  const int32_t ridx = (o * g.B + b) * So + p;
+
+  // byte offset of each reduction position inside frame 0 of the clip (or
+  // out of range), and its weight for every temporal tap
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ds.x_bytes);
+  const uint32_t plane = (uint32_t(b) * uint32_t(g.Cin) + uint32_t(grp * g.Cg)) * uint32_t(x_bc);
+  int xoff[KX];
+  float wr[KX][KTM];
+#pragma unroll
+  for (int e = 0; e < KX; ++e) {
+    const int c = e / (kHW > 0 ? kHW : 1), uv = e - c * kHW;
+    const int u = uv / g.kW, v = uv - u * g.kW;
+    const int hi = i * g.sH + u * g.dH - g.pH, wi = jo * g.sW + v * g.dW - g.pW;
+    const bool in = e < nk && hi >= 0 && hi < g.H && wi >= 0 && wi < g.W;
+    xoff[e] = in ? int((plane + uint32_t(c) * uint32_t(x_bc) + uint32_t(hi * g.W + wi)) * esz)
+                 : kOutOfRange;
+#pragma unroll
+    for (int j = 0; j < KTM; ++j)
+      wr[e][j] = (e < nk && j < kT) ? w[(int64_t(o) * g.Cg + c) * kT * kHW + int64_t(j) * kHW + uv]
+                                    : 0.f;
+  }
+  const float bo_ = bias[o];
+  const int R = g.R;
+  float part[KTM];
+#pragma unroll
+  for (int j = 1; j < KTM; ++j) {
+    part[j] = 0.f;
+    const int tau = ds.v0 - j;
+    if (j < kT && tau >= 0) part[j] = ring[int64_t((ds.slot_v0 - j + R) % R) * ring_slot + ridx];
+  }
+
+  const int fstride = ds.fstride;
+  auto load_frame = [&](int t, float (&xv)[KX]) {
+    if (t < ds.T) {  // uniform; end-padding frames are zero
+#pragma unroll
+      for (int e = 0; e < KX; ++e) xv[e] = load_or_zero_at<T>(xr, xoff[e], t * fstride);
+    } else {
+#pragma unroll
+      for (int e = 0; e < KX; ++e) xv[e] = 0.f;
+    }
+  };
+  float xq[PF][KX];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) load_frame(u, xq[u]);
+  T* yb = y + int64_t(bo) * y_bc + p;
+  for (int t0 = 0; t0 < ds.count; t0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int t = t0 + u;
+      if (t >= ds.count) break;
+      const int v = ds.v0 + t;
+      float cj[KTM];
+#pragma unroll
+      for (int j = 0; j < KTM; ++j) cj[j] = 0.f;
+#pragma unroll
+      for (int e = 0; e < KX; ++e)
+#pragma unroll
+        for (int j = 0; j < KTM; ++j) cj[j] = fmaf(wr[e][j], xq[u][e], cj[j]);
+      load_frame(t + PF, xq[u]);
+      float nxt[KTM];
+#pragma unroll
+      for (int j = 0; j < KTM; ++j) {
+        nxt[j] = 0.f;
+        const int tau = v - j;
+        if (j >= kT || tau < 0) continue;  // uniform
+        const int first = tau >= g.pT ? 0 : g.pT - tau;
+        const float a = (j == first) ? cj[j] : part[j] + cj[j];
+        if (j == kT - 1)
+          yb[int64_t(ds.k0 + t) * So] = from_f32<T>(a + bo_);
+        else
+          nxt[j] = a;
+      }
+#pragma unroll
+      for (int j = KTM - 1; j >= 1; --j) part[j] = nxt[j - 1];
+    }
+  }
+  if (ds.update) {
+    const int v1 = ds.v0 + ds.count;
+    const int s1 = (ds.slot_v0 + ds.count) % R;
+#pragma unroll
+    for (int j = 1; j < KTM; ++j) {
+      const int tau = v1 - j;
+      if (j < kT && tau >= 0) ring[int64_t((s1 - j + R) % R) * ring_slot + ridx] = part[j];
+    }
+  }
+}
+
+template <typename T>
+hipError_t direct_steps_t(const ConvGeom& g, const ConvLayout& L, char* state, const void* x,
+                          int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                          int64_t n0, bool update, hipStream_t s) {
+  DirSteps ds;
+  const int64_t v0 = n0 + g.pT;
+  ds.v0 = int32_t(v0 < (int64_t(1) << 29) ? v0 : (int64_t(1) << 29));
+  ds.slot_v0 = int32_t(v0 % g.R);
+  ds.count = count;
+  ds.T = nreal;
+  ds.k0 = int32_t(n0 - (n0 > g.d ? n0 : g.d));
+  ds.update = update ? 1 : 0;
+  const int64_t esz = sizeof(T);
+  ds.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  ds.fstride = int32_t(g.S() * esz);
+  ds.fd_So = make_fastdiv(uint32_t(g.So()));
+  ds.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  hipLaunchKernelGGL(conv_steps_direct_kernel<T>, dim3(grid_for(g.out_frame_elems())),
+                     dim3(kBlock), 0, s, g, ds, static_cast<const T*>(x), x_bc,
+                     static_cast<T*>(y), y_bc, reinterpret_cast<const float*>(state + L.weight),
+                     reinterpret_cast<const float*>(state + L.bias),
+                     reinterpret_cast<float*>(state + L.ring), L.ring_slot_elems);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char* state,
@@ -156,6 +308,22 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
                                    hipStream_t s) {
   if (g.dtype == CO_BF16) return step_direct_t<bf16_t>(g, L, state, io, plan, zero_frame, s);
   return step_direct_t<float>(g, L, state, io, plan, zero_frame, s);
+}
+
+bool direct_steps_supported(const ConvGeom& g, int64_t x_frames) {
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  return g.algo == CO_ALGO_DIRECT && g.sT == 1 && g.dT == 1 && g.kT <= kDirStepsKT &&
+         int64_t(g.Cg) * g.kH * g.kW <= kDirStepsKX &&
+         int64_t(g.B) * g.Cin * x_frames * g.S() * esz < (int64_t(1) << 31);
+}
+
+hipError_t launch_conv_steps_direct(const ConvGeom& g, const ConvLayout& L, char* state,
+                                    const void* x, int64_t x_bc, int32_t nreal, int32_t count,
+                                    void* y, int64_t y_bc, int64_t n0, bool update,
+                                    hipStream_t s) {
+  if (g.dtype == CO_BF16)
+    return direct_steps_t<bf16_t>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  return direct_steps_t<float>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
 }
 
 hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,

@@ -54,6 +54,14 @@ hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const v
 hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char* state,
                                    const StepIO& io, const co_step_plan& plan, bool zero_frame,
                                    hipStream_t stream);
+// Persistent forward_steps of small direct layers (same conventions as the
+// depthwise one): temporal stride 1 and dilation 1, kT <= 4 and
+// C_in/G * kH * kW <= 16.
+bool direct_steps_supported(const ConvGeom& g, int64_t x_frames);
+hipError_t launch_conv_steps_direct(const ConvGeom& g, const ConvLayout& L, char* state,
+                                    const void* x, int64_t x_bc, int32_t T, int32_t count,
+                                    void* y, int64_t y_bc, int64_t n0, bool update,
+                                    hipStream_t stream);
 hipError_t launch_conv_step_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
                                       const StepIO& io, const co_step_plan& plan,
                                       hipStream_t stream);

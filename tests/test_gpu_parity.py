@@ -606,7 +606,38 @@ def test_reg_forward_steps_persistent(case):
     _check_fused_steps(make, x, oracle_conv(w, b, ones, p, ones, 1), tdt, "reg steps")
 
 
+DIRECT_STEPS_CASES = [
+    # B, C_in, C_out, groups, kernel (time first), in_size, stride, padding, dilation, dtype
+    (1, 4, 8, 1, (3,), (), (1,), (0,), (1,), "f32"),                       # 1-D, no spatial axes
+    (2, 6, 9, 3, (2, 3), (7,), (1, 1), (1, 1), (1, 1), "bf16"),            # grouped
+    (3, 4, 4, 2, (4, 2, 2), (5, 6), (1, 1, 1), (3, 0, 1), (1, 1, 1), "f32"),  # kT = 4, delay 0
+    (2, 16, 5, 1, (1, 1, 1), (4, 4), (1, 1, 1), (0, 0, 0), (1, 1, 1), "f32"),  # 16 positions, kT = 1
+    (2, 1, 4, 1, (3, 3, 3), (9, 8), (1, 2, 1), (1, 1, 0), (1, 1, 2), "f32"),  # spatial stride, dilation
+]
+
+
+@pytest.mark.parametrize("case", DIRECT_STEPS_CASES, ids=lambda c: "dirsteps_" + "_".join(
+    map(str, c[:4])) + "_" + c[9])
+def test_direct_forward_steps_persistent(case):
+    """The direct family's forward_steps as one persistent launch (small
+    layers: weights, partial sums and prefetched inputs in registers)."""
+    B, cin, cout, G, k, size, st, p, dil, dt = case
+    say("direct steps", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          stride=st, padding=p, dilation=dil, groups=G, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 13, 95000 + 11 * cin + cout, "normal")
+    tdt = synth.torch_dtype(dt)
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=st, padding=p,
+                            dilation=dil, groups=G, algo="direct")
+
+    assert make().algo == "direct"
+    _check_fused_steps(make, x, oracle_conv(w, b, st, p, dil, G), tdt, "direct steps")
+
+
 @pytest.mark.parametrize("name,streams", [
+    ("conv1d_b1_c4to8_k3_f32", None),
     ("conv3d_b1_c24_k3_56x56_f32", None),
     ("conv2d_b32_c64to256_k9x1_v25_f32", (0, 13, 31)),
     ("conv2d_b32_c64to256_k9x1_v25_bf16", (2, 29)),
