@@ -220,16 +220,16 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
   }
 
   const int fstride = ds.fstride;
-  auto load_frame = [&](int t, float (&xv)[KX]) {
+  auto load_frame = [&](int t, uint32_t (&xv)[KX]) {
     if (t < ds.T) {  // uniform; end-padding frames are zero
 #pragma unroll
-      for (int e = 0; e < KX; ++e) xv[e] = load_or_zero_at<T>(xr, xoff[e], t * fstride);
+      for (int e = 0; e < KX; ++e) xv[e] = load_raw_at<T>(xr, xoff[e], t * fstride);
     } else {
 #pragma unroll
-      for (int e = 0; e < KX; ++e) xv[e] = 0.f;
+      for (int e = 0; e < KX; ++e) xv[e] = 0u;
     }
   };
-  float xq[PF][KX];
+  uint32_t xq[PF][KX];  // raw bits, converted when the frame is evaluated
 #pragma unroll
   for (int u = 0; u < PF; ++u) load_frame(u, xq[u]);
   T* yb = y + int64_t(bo) * y_bc + p;
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
 #pragma unroll
       for (int e = 0; e < KX; ++e)
 #pragma unroll
-        for (int j = 0; j < KTM; ++j) cj[j] = fmaf(wr[e][j], xq[u][e], cj[j]);
+        for (int j = 0; j < KTM; ++j) cj[j] = fmaf(wr[e][j], raw_to_f32<T>(xq[u][e]), cj[j]);
       load_frame(t + PF, xq[u]);
       float nxt[KTM];
 #pragma unroll

@@ -153,7 +153,7 @@ struct DwSteps {
   FastDiv fd_So, fd_Cout, fd_Wo;
 };
 
-constexpr int PF = 2;  // frames in flight per thread
+constexpr int PF = 4;  // frames in flight per thread
 
 template <typename T, int KH, int KW, int KT>
 __global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
@@ -212,18 +212,18 @@ __global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
   // the stencil of frame t, zero for end-padding frames (t >= T); the frame
   // offset is wave-uniform and always inside the clip, out-of-frame taps
   // carry the out-of-range offset in their per-lane part
-  auto load_frame = [&](int t, float (&xv)[NS]) {
+  auto load_frame = [&](int t, uint32_t (&xv)[NS]) {
     if (t < ds.T) {
 #pragma unroll
-      for (int e = 0; e < NS; ++e) xv[e] = load_or_zero_at<T>(xr, soff[e], t * fstride);
+      for (int e = 0; e < NS; ++e) xv[e] = load_raw_at<T>(xr, soff[e], t * fstride);
     } else {
 #pragma unroll
-      for (int e = 0; e < NS; ++e) xv[e] = 0.f;
+      for (int e = 0; e < NS; ++e) xv[e] = 0u;
     }
   };
   // frame t's stencil sits in register set t % PF; the next PF - 1 frames'
   // are in flight while frame t is evaluated
-  float xq[PF][NS];
+  uint32_t xq[PF][NS];  // raw bits, converted when the frame is evaluated
 #pragma unroll
   for (int u = 0; u < PF; ++u) load_frame(u, xq[u]);
   for (int t0 = 0; t0 < ds.count; t0 += PF) {
@@ -240,7 +240,7 @@ __global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
         const int first = tau >= g.pT ? 0 : g.pT - tau;  // first tap on a real frame
         float a = (j == first) ? 0.f : acc[q];  // a start overwrites the slot
 #pragma unroll
-        for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xq[u][e], a);
+        for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], raw_to_f32<T>(xq[u][e]), a);
         if (j == KT - 1)
           store_at(yr, yoff, (ds.k0 + t) * So * int32_t(esz), from_f32<T>(a + bo));
         else

@@ -466,7 +466,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   constexpr int CKS = 4 * CL;
   constexpr int CSUMAX = kBF ? CSMAX : (CSMAX + 3) / 4;
   constexpr int TH = TAPS / KSPLIT;  // spatial taps per partial chain
-  constexpr int AREGS = TAPS * CSMAX * (kBF ? 4 : 1);
+  constexpr int AREGS = TAPS * CSMAX * CL;  // raw registers per frame
   constexpr int PF = AREGS <= 16 ? 4 : 2;  // frames in flight
   using AReg = typename std::conditional<kBF, uint4, float>::type;
   const int lane = int(threadIdx.x) & 63;
@@ -557,7 +557,10 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
                     (unsigned(wi) < unsigned(g.W));
     vt[tp] = ok ? int(lane_b + (uint32_t(hi) * uint32_t(g.W) + uint32_t(wi)) * esz) : kOutOfRange;
   }
-  auto load_frame = [&](int t, AReg (&a)[TAPS][CSMAX]) {
+  // Raw loaded bits (eight bf16 channels or one fp32 per lane and k-step),
+  // packed into operands only when the frame is multiplied: packing right
+  // after the loads would make the wave wait for them there.
+  auto load_frame = [&](int t, uint32_t (&a)[TAPS][CSMAX][CL]) {
     if (t < rs.T) {  // uniform; end-padding frames are zero
       const int fo = t * rs.fstride;
 #pragma unroll
@@ -566,36 +569,32 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
         for (int cb = 0; cb < CSMAX; ++cb) {
           const bool live = cb < rs.CS, last = cb == rs.CS - 1;  // uniform
           const int sb = int(uint32_t(cb * CKS) * plane_b) + fo;
-          if constexpr (kBF) {
-            uint32_t r8[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int v = live & (!last | (e < nv_last)) ? vt[tp] : kOutOfRange;
-              r8[e] = __builtin_amdgcn_raw_buffer_load_b16(xr, v, sb + int(uint32_t(e) * plane_b), 0);
-            }
-            a[tp][cb] = make_uint4(r8[0] | (r8[1] << 16), r8[2] | (r8[3] << 16),
-                                   r8[4] | (r8[5] << 16), r8[6] | (r8[7] << 16));
-          } else {
-            const int v = live & (!last | (nv_last > 0)) ? vt[tp] : kOutOfRange;
-            a[tp][cb] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xr, v, sb, 0));
+          for (int e = 0; e < CL; ++e) {
+            const int v = (live & (!last | (e < nv_last))) ? vt[tp] : kOutOfRange;
+            a[tp][cb][e] = load_raw_at<T>(xr, v, sb + int(uint32_t(e) * plane_b));
           }
         }
     } else {
 #pragma unroll
       for (int tp = 0; tp < TAPS; ++tp)
 #pragma unroll
-        for (int cb = 0; cb < CSMAX; ++cb) {
-          if constexpr (kBF)
-            a[tp][cb] = make_uint4(0u, 0u, 0u, 0u);
-          else
-            a[tp][cb] = 0.f;
-        }
+        for (int cb = 0; cb < CSMAX; ++cb)
+#pragma unroll
+          for (int e = 0; e < CL; ++e) a[tp][cb][e] = 0u;
     }
   };
+  auto operand = [&](const uint32_t (&r)[CL]) -> AReg {
+    if constexpr (kBF)
+      return make_uint4(r[0] | (r[1] << 16), r[2] | (r[3] << 16), r[4] | (r[5] << 16),
+                        r[6] | (r[7] << 16));
+    else
+      return __uint_as_float(r[0]);
+  };
 
-  AReg areg[PF][TAPS][CSMAX];
+  uint32_t araw[PF][TAPS][CSMAX][CL];
 #pragma unroll
-  for (int u = 0; u < PF; ++u) load_frame(u, areg[u]);
+  for (int u = 0; u < PF; ++u) load_frame(u, araw[u]);
 
   for (int t0 = 0; t0 < rs.count; t0 += PF) {
 #pragma unroll
@@ -619,19 +618,20 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
             for (int j = 0; j < KTM; ++j) {
               if (j >= kT) continue;  // uniform
               const int tp = h * TH + i2;
+              const AReg av = operand(araw[u][tp][cb]);
               if constexpr (kBF) {
                 c[j][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(v8bf, areg[u][tp][cb]),
+                    __builtin_bit_cast(v8bf, av),
                     __builtin_bit_cast(v8bf, wreg[j][tp][cb]), c[j][h], 0, 0, 0);
               } else {
                 const uint4 u4 = wreg[j][tp][cb / 4];
                 const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
-                c[j][h] = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[u][tp][cb], __uint_as_float(bw),
+                c[j][h] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, __uint_as_float(bw),
                                                                c[j][h], 0, 0, 0);
               }
             }
       // the next frames' operands are requested before this frame's epilogue
-      load_frame(t + PF, areg[u]);
+      load_frame(t + PF, araw[u]);
       // fold each product into its output: tap j completes v - (kT - 1),
       // starts at the first tap on a real frame, continues otherwise
       v4f nxt[KTM];

@@ -96,6 +96,26 @@ __device__ __forceinline__ float load_or_zero_at<float>(__amdgpu_buffer_rsrc_t r
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
 
+// Raw bits of the T element at byte offset voff + soff (0 when the offset
+// lies past the buffer): the 16-bit pattern of a bf16, the 32-bit pattern of
+// an fp32.  Prefetch buffers hold raw bits and convert them when the frame is
+// used: an instruction that touched a loaded value right after its load
+// would make the wave wait for that load there.
+template <typename T>
+__device__ __forceinline__ uint32_t load_raw_at(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  if constexpr (sizeof(T) == 2)
+    return uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+  else
+    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+template <typename T>
+__device__ __forceinline__ float raw_to_f32(uint32_t raw) {
+  if constexpr (sizeof(T) == 2)
+    return __uint_as_float(raw << 16);
+  else
+    return __uint_as_float(raw);
+}
+
 // Store v at byte offset voff + soff of a T buffer.
 __device__ __forceinline__ void store_at(__amdgpu_buffer_rsrc_t r, int voff, int soff, bf16_t v) {
   __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);

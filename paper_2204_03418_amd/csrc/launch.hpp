@@ -41,8 +41,9 @@ hipError_t launch_pool_init(const PoolGeom& g, const PoolLayout& L, char* state,
                             const StateHeader& hdr, hipStream_t stream);
 
 // Persistent forward_steps of a pool (same conventions as the depthwise one):
-// temporal stride 1 and dilation 1, kT <= 5, a spatial window of at most 64.
-bool pool_steps_supported(const PoolGeom& g);
+// temporal stride 1 and dilation 1, kT <= 5, a spatial window of at most 64,
+// clips below 2^31 bytes.
+bool pool_steps_supported(const PoolGeom& g, int64_t x_frames);
 hipError_t launch_pool_steps(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
                              int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
                              int64_t n0, bool update, hipStream_t stream);

@@ -187,6 +187,8 @@ struct PoolSteps {
   int32_t T;
   int64_t emit0;  // first emitting step of the call: max(n0, d)
   int32_t update;
+  int32_t x_bytes;  // bytes of the clip reachable from x
+  int32_t fstride;  // bytes between consecutive frames
   FastDiv fd_So, fd_Wo, fd_kW;
 };
 
@@ -237,16 +239,23 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
     fv[q] = have ? fifo[(rf % KT) * fifo_slot + idx] : neutral;
     fok[q] = have ? valid[rf % KT] : 0.f;
   }
-  const int64_t S = int64_t(g.H) * g.W;
-  const T* xb = x + int64_t(bc) * x_bc;
   T* yb = y + int64_t(bc) * y_bc + p;
-  auto load = [&](int t) {
-    return (t < ps.T && soff >= 0) ? to_f32<T>(xb[int64_t(t) * S + soff]) : neutral;
+  // raw bits of this lane's window element of frame t (converted when the
+  // frame is reduced, so the loads stay in flight); positions outside the
+  // frame read the out-of-range offset and become the neutral value at use
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ps.x_bytes);
+  const int loff = soff >= 0 ? int((uint32_t(bc) * uint32_t(x_bc) + uint32_t(soff)) * sizeof(T))
+                             : kOutOfRange;
+  auto load = [&](int t) -> uint32_t {
+    return t < ps.T ? load_raw_at<T>(xr, loff, t * ps.fstride) : 0u;
+  };
+  auto value = [&](int t, uint32_t raw) {
+    return (t < ps.T && soff >= 0) ? raw_to_f32<T>(raw) : neutral;
   };
   // frame t's window element sits in xq[t % PF]; the next PF - 1 frames'
   // are in flight while frame t is reduced
   constexpr int PF = 4;
-  float xq[PF];
+  uint32_t xq[PF];
 #pragma unroll
   for (int u = 0; u < PF; ++u) xq[u] = load(u);
   for (int t0 = 0; t0 < ps.count; t0 += PF) {
@@ -254,7 +263,8 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
     for (int u = 0; u < PF; ++u) {
       const int t = t0 + u;
       if (t >= ps.count) break;
-      const float val = is_max ? group_max<G>(xq[u]) : group_sum<G>(xq[u]);
+      const float xv = value(t, xq[u]);
+      const float val = is_max ? group_max<G>(xv) : group_sum<G>(xv);
       xq[u] = load(t + PF);
       fv[KT - 1] = val;
       fok[KT - 1] = t < ps.T ? 1.f : 0.f;
@@ -392,6 +402,9 @@ hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state
   ps.T = nreal;
   ps.emit0 = n0 > g.d ? n0 : g.d;
   ps.update = update ? 1 : 0;
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  ps.x_bytes = int32_t(((int64_t(g.B) * g.C - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  ps.fstride = int32_t(g.S() * esz);
   ps.fd_So = make_fastdiv(uint32_t(g.So()));
   ps.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   ps.fd_kW = make_fastdiv(uint32_t(g.kW));
@@ -432,8 +445,10 @@ hipError_t pool_steps_t(const PoolGeom& g, const PoolLayout& L, char* state, con
 
 }  // namespace
 
-bool pool_steps_supported(const PoolGeom& g) {
-  return g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64;  // (kT <= 8: tree)
+bool pool_steps_supported(const PoolGeom& g, int64_t x_frames) {
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  return g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64 &&  // (kT <= 8: tree)
+         int64_t(g.B) * g.C * x_frames * g.S() * esz < (int64_t(1) << 31);
 }
 
 hipError_t launch_pool_steps(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
