@@ -168,11 +168,14 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
   const int64_t n0 = h->n;
   const bool dw = dw_steps_supported(g, T, y_cap_frames);
   const bool dir = direct_steps_supported(g, T) && y_steps_fit(g, y_cap_frames);
-  if (count > 0 && (dw || dir || reg_steps_supported(g, T, y_cap_frames))) {
-    // one persistent launch: partial sums stay in registers across frames;
-    // with update_state = 0 the state is simply not written back
-    const auto launch = dw ? launch_conv_steps_depthwise
-                           : dir ? launch_conv_steps_direct : launch_conv_steps_reg;
+  const bool gem = gemm_steps_supported(g, T, y_cap_frames, x);
+  if (count > 0 && (dw || dir || gem || reg_steps_supported(g, T, y_cap_frames))) {
+    // one persistent launch: partial sums stay on chip across frames; with
+    // update_state = 0 the state is simply not written back
+    const auto launch = dw    ? launch_conv_steps_depthwise
+                        : dir ? launch_conv_steps_direct
+                        : gem ? launch_conv_steps_gemm
+                              : launch_conv_steps_reg;
     const co_status st = hip_status(launch(g, h->L, h->state, x, int64_t(T) * g.S(), T,
                                            int32_t(count), y, int64_t(y_cap_frames) * g.So(),
                                            n0, update_state != 0, s));
@@ -219,8 +222,12 @@ co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_
                               int32_t* fused) {
   if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
   const ConvGeom& g = h->g;
+  // (the GEMM family also needs 4-byte aligned pixel pairs in x; an
+  // allocation from the caching allocator always is)
+  static const uint32_t aligned_probe = 0;
   *fused = dw_steps_supported(g, T, y_cap_frames) ||
                    (direct_steps_supported(g, T) && y_steps_fit(g, y_cap_frames)) ||
+                   gemm_steps_supported(g, T, y_cap_frames, &aligned_probe) ||
                    reg_steps_supported(g, T, y_cap_frames)
                ? 1
                : 0;

@@ -355,6 +355,7 @@ hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
   if (e != hipSuccess) return e;
   if (g.algo == CO_ALGO_GEMM) {
     e = launch_pack_gemm(g, L, state, weight, s);
+    if (e == hipSuccess && L.steps_weight_bytes > 0) e = launch_pack_gemm_steps(g, L, state, weight, s);
   } else if (g.algo == CO_ALGO_GEMM_REG) {
     e = launch_pack_reg(g, L, state, weight, s);
   } else if (g.algo == CO_ALGO_GEMM_IMG) {

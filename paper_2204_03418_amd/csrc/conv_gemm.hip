@@ -264,19 +264,22 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
   Pair ra[AI][KL];
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ga.x_bytes);
   const int plane_bytes = int(x_bc * int64_t(sizeof(T)));
-  // channels past C_in read the next stream's planes or past the buffer end
-  // (zero); they are masked when stored
-  // `part` < 0: all of chunk ch's loads; else the share issued during
-  // spatial tap `part`, so the loads trickle out between the matrix
-  // instructions instead of queueing all at once in front of them
+  // Channels past C_in (a ragged last chunk) read the out-of-range offset
+  // (zero) and are masked again when stored.  `part` < 0: all of chunk ch's
+  // loads; else the share issued during spatial tap `part`, so the loads
+  // trickle out between the matrix instructions instead of queueing all at
+  // once in front of them.
   auto prefetch = [&](int ch, int part) {
     const int cbase = ch * CK;
 #pragma unroll
     for (int ai = 0; ai < AI; ++ai)
 #pragma unroll
       for (int e = 0; e < KL; ++e)
-        if (part < 0 || (ai * KL + e) % KHW == part)
-          ra[ai][e] = Stage<T>::load(xr, a_src[ai], (cbase + e) * plane_bytes, PAIR);
+        if (part < 0 || (ai * KL + e) % KHW == part) {
+          const bool cin = cbase + a_grp[ai] * KL + e < g.Cin;
+          ra[ai][e] = Stage<T>::load(xr, cin ? a_src[ai] : kOutOfRange,
+                                     (cbase + e) * plane_bytes, PAIR);
+        }
   };
   auto store_a = [&](int buf, int ch) {
     uint4* As = As0 + buf * a_units;
@@ -505,6 +508,454 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfi
   out[U] = pk.q;
 }
 
+// ---- persistent forward_steps (bf16) -----------------------------------
+//
+// Temporal stride and dilation 1: the frame at virtual time v feeds output
+// v - j through temporal tap j.  A workgroup owns M_WG pixels x O_WG output
+// channels for every tap (column c = t * O_WG + o_local), so the partial sums
+// of its outputs never leave its registers: the ring is read once at the
+// start of a call and written once at the end.  Each wave holds WM pixel
+// fragments x one channel fragment x every tap.  A frame is the step kernel's
+// GEMM with the same k order (32-channel chunks outer, spatial taps inner),
+// and each tap's accumulators start from the partial sum exactly as the step
+// kernel starts them from the ring, so the results equal stepping bit for
+// bit.
+//
+// Pipeline: input chunks are staged as in the step kernel (double buffered);
+// weights stream in stages of one chunk x one kernel row (triple buffered,
+// requested two stages ahead with global_load_lds).  At the end of a stage a
+// wave waits until at most the memory requests it issued in that stage are
+// outstanding -- the next stage's weights, requested a stage earlier, have
+// then landed -- and the workgroup meets at a barrier.
+
+struct GemmSteps {
+  int32_t M, So;
+  int32_t m_tiles, o_tiles, tiles_per_xcd;
+  int32_t n_chunks, cols, max_slots, a_units;
+  int32_t x_bytes;
+  int32_t fstride;    // bytes between consecutive frames of the clip
+  int32_t y_bc;       // y elements between (stream, channel) planes
+  int32_t ring_slot;  // floats between ring slots
+  int32_t v0;         // virtual time of the first frame, capped at 2^29
+  int32_t slot_v0;    // v0 mod R (uncapped)
+  int32_t count, T, k0, update;
+  int32_t yvec;       // four outputs of a lane can go out as one 8-byte store
+  FastDiv fd_So, fd_Wo, fd_Ho, fd_H, fd_ot, fd_wpi;
+};
+
+// s_waitcnt immediate: wait until at most n vector memory requests are
+// outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14; expcnt and
+// lgkmcnt at their maxima, i.e. not waited for).
+constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+template <int KH, int KW, bool PAIR>
+__global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_kernel(
+    ConvGeom g, GemmSteps gs, const bf16_t* __restrict__ x, int64_t x_bc,
+    bf16_t* __restrict__ y, const uint4* __restrict__ wp, const float* __restrict__ bias,
+    float* __restrict__ ring) {
+  using T = bf16_t;
+  using Frag = v8bf;
+  using Pair = typename Stage<T>::Pair;
+  constexpr int WM = kStepsWM, NWM = kStepsNWM, NWN = kStepsNWN, KTM = kStepsKT;
+  constexpr int KL = 8, CK = 32;
+  constexpr int NT = 64 * NWM * NWN;
+  constexpr int M_WG = 16 * WM * NWM;
+  constexpr int O_WG = 16 * NWN;
+  constexpr int N_WG = KTM * O_WG;
+  constexpr int AI = (kStepsStageItems + NT - 1) / NT;
+  constexpr int B_UNITS = KW * N_WG * 4;        // one weight stage
+  constexpr int BI = (B_UNITS + NT - 1) / NT;  // weight copies per thread and stage
+  constexpr int ALOADS = AI * KL;              // input loads per thread and chunk
+  static_assert(B_UNITS >= NT && B_UNITS % 64 == 0, "weight stage shape");
+  extern __shared__ uint4 smem[];
+
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % NWM, wn = wave / NWM;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int bid = int(blockIdx.x);
+  const int L = (bid & 7) * gs.tiles_per_xcd + (bid >> 3);
+  if (L >= gs.m_tiles * gs.o_tiles) return;
+  const int m_tile = fdiv(L, gs.fd_ot);
+  const int o_tile = L - m_tile * gs.o_tiles;
+  const int m0 = m_tile * M_WG;
+  const int m1 = min(m0 + M_WG, gs.M);
+  const int kT = g.kT;
+
+  // input rows of the tile: flattened (stream, row) index q in [q0, q1]
+  const int r0 = fdiv(m0, gs.fd_Wo), r1 = fdiv(m1 - 1, gs.fd_Wo);
+  const int b0 = fdiv(r0, gs.fd_Ho), i0 = r0 - b0 * g.Ho;
+  const int b1 = fdiv(r1, gs.fd_Ho), i1 = r1 - b1 * g.Ho;
+  const int q0 = b0 * g.H + max(0, i0 - g.pH);
+  const int q1 = b1 * g.H + min(g.H - 1, i1 + KH - 1 - g.pH);
+  const int nslots = q1 - q0 + 1;
+  const int zero_slot = gs.max_slots;
+
+  // LDS: [A stage 0][A stage 1][B stage 0][B stage 1][B stage 2], the A
+  // stages laid out as in the step kernel
+  const int a_pixels = (gs.max_slots + 2) * gs.cols;
+  const int a_units = gs.a_units;
+  uint4* const As0 = smem;
+  uint4* const Bs0 = smem + 2 * a_units;
+  for (int u = tid; u < 2 * a_units; u += NT) smem[u] = make_uint4(0u, 0u, 0u, 0u);
+
+  int pixbase[WM][KH];
+#pragma unroll
+  for (int mf = 0; mf < WM; ++mf) {
+    const int P = m0 + (wm * WM + mf) * 16 + lrow;
+    const bool valid = P < gs.M;
+    const int Pc = valid ? P : 0;
+    const int b = fdiv(Pc, gs.fd_So), p = Pc - b * gs.So;
+    const int i = fdiv(p, gs.fd_Wo), j = p - i * g.Wo;
+#pragma unroll
+    for (int u = 0; u < KH; ++u) {
+      const int ih = i + u - g.pH;
+      const int slot = (valid && ih >= 0 && ih < g.H) ? b * g.H + ih - q0 : zero_slot;
+      pixbase[mf][u] = slot * gs.cols + j;
+    }
+  }
+
+  constexpr int PW = PAIR ? 2 : 1;
+  const int wp_items = g.W / PW;
+  const int a_items = nslots * 4 * wp_items;
+  int a_src[AI], a_dst[AI], a_dst1[AI], a_grp[AI];
+#pragma unroll
+  for (int ai = 0; ai < AI; ++ai) {
+    const int it = tid + ai * NT;
+    a_src[ai] = 0;
+    a_grp[ai] = 0;
+    a_dst[ai] = a_pixels * kPixUnits;
+    a_dst1[ai] = (a_pixels + 1) * kPixUnits;
+    if (it < a_items) {
+      const int rest = fdiv(it, gs.fd_wpi);
+      const int xp = it - rest * wp_items;
+      const int grp = rest & 3;
+      const int sl = rest >> 2;
+      const int q = q0 + sl;
+      const int b = fdiv(q, gs.fd_H), ih = q - b * g.H;
+      const int xcol = xp * PW;
+      a_src[ai] = int(((int64_t(b) * g.Cin + grp * KL) * x_bc + int64_t(ih) * g.W + xcol) *
+                      int64_t(sizeof(T)));
+      a_grp[ai] = grp;
+      const int pix = sl * gs.cols + xcol + g.pW;
+      a_dst[ai] = pix * kPixUnits + grp;
+      a_dst1[ai] = (pix + 1) * kPixUnits + grp;
+    }
+  }
+
+  Pair ra[AI][KL];
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, gs.x_bytes);
+  const int plane_bytes = int(x_bc * int64_t(sizeof(T)));
+  // input loads of chunk ch of frame t; end-padding frames stage zeros and
+  // issue nothing (the return value says whether loads went out)
+  auto prefetch = [&](int t, int ch) -> bool {
+    if (t >= gs.T) {
+#pragma unroll
+      for (int ai = 0; ai < AI; ++ai)
+#pragma unroll
+        for (int e = 0; e < KL; ++e) ra[ai][e] = Pair{};
+      return false;
+    }
+    const int cbase = ch * CK;
+    const int fo = t * gs.fstride;
+#pragma unroll
+    for (int ai = 0; ai < AI; ++ai)
+#pragma unroll
+      for (int e = 0; e < KL; ++e) {
+        const bool cin = cbase + a_grp[ai] * KL + e < g.Cin;
+        ra[ai][e] = Stage<T>::load(xr, cin ? a_src[ai] : kOutOfRange,
+                                   (cbase + e) * plane_bytes + fo, PAIR);
+      }
+    return true;
+  };
+  auto store_a = [&](int buf, int ch) {
+    uint4* As = As0 + buf * a_units;
+    const bool ragged = ch * CK + CK > g.Cin;
+#pragma unroll
+    for (int ai = 0; ai < AI; ++ai) {
+      if (ragged) {
+        const int c0 = ch * CK + a_grp[ai] * KL;
+#pragma unroll
+        for (int e = 0; e < KL; ++e)
+          if (c0 + e >= g.Cin) ra[ai][e] = Pair{};
+      }
+      uint4 p0, p1;
+      Stage<T>::pack(ra[ai], p0, p1);
+      As[a_dst[ai]] = p0;
+      if (PAIR) As[a_dst1[ai]] = p1;
+    }
+  };
+  // weight stage st (chunk st / KH, kernel row st % KH) into buffer buf; every
+  // wave issues BI copies (a copy past the stage repeats one inside it, with
+  // identical data), so the outstanding-request counts below are uniform
+  auto copy_b = [&](int st, int buf) {
+    const uint4* wsrc = wp + (int64_t(o_tile) * gs.n_chunks * KH + st) * B_UNITS;
+    uint4* Bs = Bs0 + buf * B_UNITS;
+#pragma unroll
+    for (int bi = 0; bi < BI; ++bi) {
+      int u0 = wave * 64 + bi * NT;
+      if (u0 >= B_UNITS) u0 -= NT;
+      __builtin_amdgcn_global_load_lds(wsrc + u0 + lane,
+                                       (__attribute__((address_space(3))) void*)(Bs + u0), 16,
+                                       0, 0);
+    }
+  };
+  auto wait_stage = [&](bool a, bool b) {
+    if (a) {
+      if (b)
+        __builtin_amdgcn_s_waitcnt(vm_wait(ALOADS + BI));
+      else
+        __builtin_amdgcn_s_waitcnt(vm_wait(ALOADS));
+    } else {
+      if (b)
+        __builtin_amdgcn_s_waitcnt(vm_wait(BI));
+      else
+        __builtin_amdgcn_s_waitcnt(0);
+    }
+  };
+
+  // this lane's output channel, B columns, outputs and partial sums
+  const int o = o_tile * O_WG + wn * 16 + lrow;
+  const bool ocol = o < g.Cout;
+  const float bo = ocol ? bias[o] : 0.f;
+  int bcol[KTM];
+#pragma unroll
+  for (int j = 0; j < KTM; ++j) {
+    const int cc = j * O_WG + wn * 16 + lrow;
+    bcol[j] = cc * 4 + bswz(cc, lgrp);
+  }
+  // first of the four pixels of fragment mf this lane holds (recomputed
+  // where needed rather than kept in registers across the frame loop)
+  auto pix0 = [&](int mf) { return m0 + (wm * WM + mf) * 16 + lgrp * 4; };
+  const int R = g.R;
+  // part[mf][j - 1]: partial sum of output v - j, continued by tap j >= 1
+  v4f part[WM][KTM - 1];
+#pragma unroll
+  for (int j = 1; j < KTM; ++j)
+#pragma unroll
+    for (int mf = 0; mf < WM; ++mf) {
+      part[mf][j - 1] = v4f{0.f, 0.f, 0.f, 0.f};
+      const int tau = gs.v0 - j;
+      if (j < kT && tau >= 0) {
+        const int sl = (gs.slot_v0 - j + R) % R;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (ocol && pix0(mf) + r < gs.M)
+            part[mf][j - 1][r] =
+                ring[int64_t(sl) * gs.ring_slot + int64_t(o) * gs.M + pix0(mf) + r];
+      }
+    }
+
+  const int spf = gs.n_chunks * KH;  // weight stages per frame
+  const int total_stages = gs.count * spf;
+  __syncthreads();  // zero fill done
+  copy_b(0, 0);
+  if (total_stages > 1) copy_b(1 % spf, 1);
+  prefetch(0, 0);
+  store_a(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  v4f c[WM][KTM];
+  int gst = 0;  // stages done
+  int gch = 0;  // chunks done
+  for (int t = 0; t < gs.count; ++t) {
+    const int v = gs.v0 + t;
+    // accumulators start from the partial sum of the output each tap
+    // continues, or from zero where the tap starts it (as the step kernel)
+#pragma unroll
+    for (int j = 0; j < KTM; ++j) {
+      const int tau = v - j;
+      const int first = tau >= g.pT ? 0 : g.pT - tau;
+      // (tap 0 always starts its output: v >= pT)
+      const bool seed = j >= 1 && j < kT && tau >= 0 && j != first;
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf)
+        c[mf][j] = seed ? part[mf][j > 0 ? j - 1 : 0] : v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int ch = 0; ch < gs.n_chunks; ++ch, ++gch) {
+      const uint4* As = As0 + (gch & 1) * a_units;
+      const bool lastc = ch + 1 == gs.n_chunks;
+      const int nch = lastc ? 0 : ch + 1;
+      const int ntf = lastc ? t + 1 : t;
+      const bool anext = ntf < gs.count;
+#pragma unroll
+      for (int u = 0; u < KH; ++u, ++gst) {
+        bool aload = false;
+        if (u == 0 && anext) aload = prefetch(ntf, nch);
+        const bool b2 = gst + 2 < total_stages;
+        if (b2) copy_b((gst + 2) % spf, (gst + 2) % 3);
+        const uint4* Bs = Bs0 + (gst % 3) * B_UNITS;
+        // a tap's pixel fragments are requested one tap ahead; its weight
+        // fragments (shared by all WM rows) just before use
+        Frag af[2][WM], bf[KTM];
+        auto load_a = [&](int vv, int k) {
+#pragma unroll
+          for (int mf = 0; mf < WM; ++mf)
+            af[k][mf] = __builtin_bit_cast(Frag, As[(pixbase[mf][u] + vv) * kPixUnits + lgrp]);
+        };
+        load_a(0, 0);
+#pragma unroll
+        for (int vv = 0; vv < KW; ++vv) {
+#pragma unroll
+          for (int j = 0; j < KTM; ++j)
+            bf[j] = __builtin_bit_cast(Frag, Bs[vv * N_WG * 4 + bcol[j]]);
+          // weights before the next tap's pixels: LDS reads complete in
+          // order, so the matrix instructions wait for these three only
+          __builtin_amdgcn_sched_barrier(0);
+          if (vv + 1 < KW) load_a(vv + 1, (vv + 1) & 1);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int j = 0; j < KTM; ++j)
+#pragma unroll
+            for (int mf = 0; mf < WM; ++mf) mma(c[mf][j], af[vv & 1][mf], bf[j]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (u == KH - 1 && anext) store_a((gch + 1) & 1, nch);
+        wait_stage(aload, b2);
+        __syncthreads();
+      }
+    }
+    // the output tap kT - 1 completes goes out with the bias; the others'
+    // sums carry on as the partial sums of the next frame
+    const int ko = gs.k0 + t;
+#pragma unroll
+    for (int j = 0; j < KTM; ++j) {
+      if (j != kT - 1 || v - j < 0) continue;  // uniform
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf) {
+        const int p0 = pix0(mf);
+        if (!ocol || p0 >= gs.M) continue;
+        const v4f a = c[mf][j];
+        if (gs.yvec) {  // the four pixels lie in one stream's frame
+          const int b = fdiv(p0, gs.fd_So), p = p0 - b * gs.So;
+          bf16_t* yp = y + (int64_t(b) * g.Cout + o) * gs.y_bc + int64_t(ko) * gs.So + p;
+          store4<T>(yp, a[0] + bo, a[1] + bo, a[2] + bo, a[3] + bo, true);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int P = p0 + r;
+            if (P >= gs.M) continue;
+            const int b = fdiv(P, gs.fd_So), p = P - b * gs.So;
+            store_out<T>(y, (int64_t(b) * g.Cout + o) * gs.y_bc + int64_t(ko) * gs.So + p,
+                         a[r] + bo);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int j = KTM - 1; j >= 1; --j) {
+      const bool carry = j - 1 < kT - 1 && v - (j - 1) >= 0;
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf)
+        part[mf][j - 1] = carry ? c[mf][j - 1] : v4f{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
+  if (gs.update) {
+    const int v1 = gs.v0 + gs.count;
+    const int s1 = (gs.slot_v0 + gs.count) % R;
+#pragma unroll
+    for (int j = 1; j < KTM; ++j) {
+      if (j >= kT || v1 - j < 0) continue;  // uniform
+      const int sl = (s1 - j + R) % R;
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (ocol && pix0(mf) + r < gs.M)
+            ring[int64_t(sl) * gs.ring_slot + int64_t(o) * gs.M + pix0(mf) + r] = part[mf][j - 1][r];
+    }
+  }
+}
+
+// Pack W (C_out, C_in, kT, kH, kW) into [o_tile][chunk][u][v][column][4 units]
+// (column = t * O_WG + o_local), zero padded, with the units swizzled as the
+// persistent kernel reads them.
+__global__ __launch_bounds__(kBlock) void pack_gemm_steps_kernel(ConvGeom g, GemmStepsConfig c,
+                                                                 const bf16_t* __restrict__ w,
+                                                                 uint4* __restrict__ out) {
+  const int64_t total = c.weight_bytes / 16;
+  const int64_t U = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (U >= total) return;
+  const int phys = int(U % 4);
+  int64_t rest = U / 4;
+  const int col = int(rest % c.N_WG);
+  rest /= c.N_WG;
+  const int v = int(rest % g.kW);
+  rest /= g.kW;
+  const int u = int(rest % g.kH);
+  rest /= g.kH;
+  const int ch = int(rest % c.n_chunks);
+  const int ot = int(rest / c.n_chunks);
+  const int grp = phys ^ ((col >> 1) & 3);  // inverse of bswz
+  const int t = col / c.O_WG, o = ot * c.O_WG + col % c.O_WG;
+  union {
+    bf16_t v[8];
+    uint4 q;
+  } pk;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int cc = ch * 32 + grp * 8 + e;
+    bf16_t val = 0;
+    if (t < g.kT && o < g.Cout && cc < g.Cin)
+      val = w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * g.kH + u) * g.kW) + v];
+    pk.v[e] = val;
+  }
+  out[U] = pk.q;
+}
+
+template <int KH, int KW, bool PAIR>
+hipError_t gemm_steps_launch(const ConvGeom& g, const GemmStepsConfig& c, const ConvLayout& L,
+                             char* state, const void* x, int64_t x_bc, int32_t nreal,
+                             int32_t count, void* y, int64_t y_bc, int64_t n0, bool update,
+                             hipStream_t s) {
+  auto kern = conv_steps_gemm_kernel<KH, KW, PAIR>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       int(kLdsBytes));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  GemmSteps gs;
+  gs.M = int32_t(int64_t(g.B) * g.So());
+  gs.So = int32_t(g.So());
+  gs.m_tiles = c.m_tiles;
+  gs.o_tiles = c.o_tiles;
+  gs.tiles_per_xcd = int32_t(ceil_div(int64_t(c.m_tiles) * c.o_tiles, 8));
+  gs.n_chunks = c.n_chunks;
+  gs.cols = c.cols;
+  gs.max_slots = c.max_slots;
+  gs.a_units = int32_t(c.a_units);
+  gs.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * x_bc + int64_t(nreal) * g.S()) * 2);
+  gs.fstride = int32_t(g.S() * 2);
+  gs.y_bc = int32_t(y_bc);
+  gs.ring_slot = int32_t(L.ring_slot_elems);
+  const int64_t v0 = n0 + g.pT;
+  gs.v0 = int32_t(v0 < (int64_t(1) << 29) ? v0 : (int64_t(1) << 29));
+  gs.slot_v0 = int32_t(v0 % g.R);
+  gs.count = count;
+  gs.T = nreal;
+  gs.k0 = int32_t(n0 - (n0 > g.d ? n0 : g.d));
+  gs.update = update ? 1 : 0;
+  gs.yvec = (g.So() % 4 == 0 && (reinterpret_cast<uintptr_t>(y) % 8) == 0) ? 1 : 0;
+  gs.fd_So = make_fastdiv(uint32_t(gs.So));
+  gs.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  gs.fd_Ho = make_fastdiv(uint32_t(g.Ho));
+  gs.fd_H = make_fastdiv(uint32_t(g.H));
+  gs.fd_ot = make_fastdiv(uint32_t(c.o_tiles));
+  gs.fd_wpi = make_fastdiv(uint32_t(PAIR ? g.W / 2 : g.W));
+  hipLaunchKernelGGL(kern, dim3(unsigned(8 * gs.tiles_per_xcd)),
+                     dim3(64 * kStepsNWM * kStepsNWN), size_t(c.lds_bytes), s, g, gs,
+                     static_cast<const bf16_t*>(x), x_bc, static_cast<bf16_t*>(y),
+                     reinterpret_cast<const uint4*>(state + L.steps_weight),
+                     reinterpret_cast<const float*>(state + L.bias),
+                     reinterpret_cast<float*>(state + L.ring));
+  return hipGetLastError();
+}
+
 template <typename T, int KH, int KW, int WM, int WN, int NWM, int NWN, bool PAIR>
 hipError_t gemm_launch(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L, char* state,
                        const StepIO& io, const co_step_plan& plan, hipStream_t s) {
@@ -601,6 +1052,46 @@ hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* s
   if (g.kH == 3 && g.kW == 3) return gemm_dispatch_taps<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return gemm_dispatch_taps<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;
+}
+
+bool gemm_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames,
+                          const void* x) {
+  GemmStepsConfig c;
+  if (!gemm_steps_config(g, &c)) return false;
+  const int64_t x_bc = x_frames * g.S();
+  // even rows are staged two pixels per load: 4-byte aligned pixel pairs
+  if (g.W % 2 == 0 && ((x_bc % 2) != 0 || (reinterpret_cast<uintptr_t>(x) % 4) != 0))
+    return false;
+  const int64_t lim = int64_t(1) << 31;
+  return (int64_t(g.B) * g.Cin * x_bc) * 2 < lim && int64_t(g.B) * g.Cout * y_frames * g.So() < lim &&
+         int64_t(g.R) * conv_layout(g).ring_slot_elems < lim;
+}
+
+hipError_t launch_conv_steps_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
+                                  const void* x, int64_t x_bc, int32_t nreal, int32_t count,
+                                  void* y, int64_t y_bc, int64_t n0, bool update, hipStream_t s) {
+  GemmStepsConfig c;
+  if (!gemm_steps_config(g, &c) || L.steps_weight_bytes != c.weight_bytes)
+    return hipErrorInvalidValue;
+  const bool pair = g.W % 2 == 0;
+  if (g.kH == 3 && g.kW == 3)
+    return pair ? gemm_steps_launch<3, 3, true>(g, c, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s)
+                : gemm_steps_launch<3, 3, false>(g, c, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  if (g.kH == 1 && g.kW == 1)
+    return pair ? gemm_steps_launch<1, 1, true>(g, c, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s)
+                : gemm_steps_launch<1, 1, false>(g, c, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* state,
+                                  const void* weight, hipStream_t s) {
+  GemmStepsConfig c;
+  if (!gemm_steps_config(g, &c)) return hipSuccess;
+  const int64_t total = c.weight_bytes / 16;
+  hipLaunchKernelGGL(pack_gemm_steps_kernel, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
+                     static_cast<const bf16_t*>(weight),
+                     reinterpret_cast<uint4*>(state + L.steps_weight));
+  return hipGetLastError();
 }
 
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,

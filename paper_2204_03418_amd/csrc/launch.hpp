@@ -93,6 +93,16 @@ hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* st
                                 const StepIO& io, const co_step_plan& plan, hipStream_t stream);
 hipError_t launch_pack_img(const ConvGeom& g, const ConvLayout& L, char* state,
                            const void* weight, hipStream_t stream);
+// Persistent forward_steps of the LDS-tiled GEMM (bf16; same conventions as
+// the depthwise one): temporal stride 1 and dilation 1, kT <= 3, 3x3 or 1x1
+// taps, tiles within the LDS and staging budgets.  x is the clip pointer
+// (pixel pairs must be 4-byte aligned when rows are even).
+bool gemm_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames, const void* x);
+hipError_t launch_conv_steps_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
+                                  const void* x, int64_t x_bc, int32_t T, int32_t count, void* y,
+                                  int64_t y_bc, int64_t n0, bool update, hipStream_t stream);
+hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* state,
+                                  const void* weight, hipStream_t stream);
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, hipStream_t stream);
 

@@ -114,6 +114,35 @@ bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
   return true;
 }
 
+bool gemm_steps_config(const ConvGeom& g, GemmStepsConfig* c) {
+  if (g.algo != CO_ALGO_GEMM || g.dtype != CO_BF16 || !gemm_geometry_ok(g) || g.sT != 1 ||
+      g.dT != 1 || g.kT > kStepsKT)
+    return false;
+  GemmStepsConfig r{};
+  r.M_WG = 16 * kStepsWM * kStepsNWM;
+  r.O_WG = 16 * kStepsNWN;
+  r.N_WG = kStepsKT * r.O_WG;
+  const int64_t M = int64_t(g.B) * g.So();
+  r.m_tiles = int32_t(ceil_div(M, r.M_WG));
+  r.o_tiles = int32_t(ceil_div(g.Cout, r.O_WG));
+  r.n_chunks = int32_t(ceil_div(g.Cin, 32));
+  r.cols = g.W + g.pW;
+  int64_t slots = 1;
+  for (int64_t t = 0; t < r.m_tiles; ++t)
+    slots = std::max(slots, tile_slots(g, t * r.M_WG, std::min<int64_t>(M, (t + 1) * r.M_WG)));
+  r.max_slots = int32_t(slots);
+  r.a_units = ((slots + 2) * r.cols + 2) * kGemmPixUnits;
+  r.b_units = int64_t(g.kW) * r.N_WG * 4;
+  r.lds_bytes = (2 * r.a_units + 3 * r.b_units) * 16;
+  if (r.lds_bytes > kLdsBytes) return false;
+  const int64_t items = slots * 4 * (g.W % 2 == 0 ? g.W / 2 : g.W);
+  if (items > int64_t(kStepsStageItems)) return false;
+  r.weight_bytes = int64_t(r.o_tiles) * r.n_chunks * g.kH * r.b_units * 16;
+  if (r.weight_bytes >= (int64_t(1) << 31)) return false;
+  *c = r;
+  return true;
+}
+
 int gemm_pick(const ConvGeom& g) {
   int best = -1;
   double best_cost = 0;
@@ -403,7 +432,10 @@ ConvLayout conv_layout(const ConvGeom& g) {
   L.bias = kHeaderBytes;
   L.weight = L.bias + round_up(int64_t(g.Cout) * 4, kAlign);
   L.weight_bytes = packed_weight_bytes(g);
-  L.ring = L.weight + round_up(L.weight_bytes, kAlign);
+  L.steps_weight = L.weight + round_up(L.weight_bytes, kAlign);
+  GemmStepsConfig sc;
+  L.steps_weight_bytes = gemm_steps_config(g, &sc) ? sc.weight_bytes : 0;
+  L.ring = L.steps_weight + round_up(L.steps_weight_bytes, kAlign);
   // four floats past the frame keep a 16-byte read of the last four pixels
   // of a ragged frame inside the slot
   L.ring_slot_elems = round_up(g.out_frame_elems() + 4, kAlign / 4);

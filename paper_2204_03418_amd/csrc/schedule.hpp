@@ -132,10 +132,31 @@ constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)
 constexpr int kGemmStageItems = 1024;  // staging items per workgroup and chunk
 constexpr int64_t kLdsBytes = 160 * 1024;
 
+// Persistent forward_steps of the LDS-tiled GEMM (bf16, temporal stride and
+// dilation 1, kT <= kStepsKT): a workgroup of kStepsNWM x kStepsNWN waves
+// owns M_WG = 16 * kStepsWM * kStepsNWM output pixels x O_WG = 16 * kStepsNWN
+// output channels for every temporal tap (N_WG = kStepsKT * O_WG columns),
+// so the partial sums its outputs continue stay in its registers across
+// frames.  Per frame it stages the input in chunks of 32 channels (double
+// buffered) and streams the weights in stages of one chunk x one kernel row
+// (triple buffered).
+struct GemmStepsConfig {
+  int32_t M_WG, O_WG, N_WG;
+  int32_t m_tiles, o_tiles, n_chunks;
+  int32_t cols, max_slots;
+  int64_t a_units;       // 16-byte units of one input stage
+  int64_t b_units;       // 16-byte units of one weight stage (kW x N_WG x 4)
+  int64_t lds_bytes;     // (2 * a_units + 3 * b_units) * 16
+  int64_t weight_bytes;  // packed weights: o_tiles x n_chunks x kH stages
+};
+constexpr int kStepsWM = 5, kStepsNWM = 2, kStepsNWN = 4, kStepsKT = 3;
+constexpr int kStepsStageItems = 512;  // input staging items per workgroup and chunk
+
 // Layout of a convolution state buffer (byte offsets).
 struct ConvLayout {
   int64_t header, bias, weight, ring;
   int64_t weight_bytes;
+  int64_t steps_weight, steps_weight_bytes;  // second packing for persistent forward_steps (0: none)
   int64_t ring_slot_elems;  // floats between consecutive ring slots
   int64_t total;
 };
@@ -209,6 +230,7 @@ bool reg_supported(const ConvGeom& g);
 // Whether the implicit-GEMM / depthwise kernels accept a geometry.
 bool gemm_supported(const ConvGeom& g);
 bool gemm_geometry_ok(const ConvGeom& g);
+bool gemm_steps_config(const ConvGeom& g, GemmStepsConfig* c);
 bool depthwise_supported(const ConvGeom& g);
 
 // Bytes of packed weights for an algorithm.

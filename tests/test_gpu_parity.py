@@ -636,7 +636,38 @@ def test_direct_forward_steps_persistent(case):
     _check_fused_steps(make, x, oracle_conv(w, b, st, p, dil, G), tdt, "direct steps")
 
 
+GEMM_STEPS_CASES = [
+    # B, C_in, C_out, kernel (time first), in_size, padding
+    (3, 40, 80, (3, 3, 3), (9, 10), (1, 1, 1)),   # ragged channel chunk and channel tile
+    (2, 32, 64, (2, 3, 3), (7, 7), (0, 1, 1)),    # odd width (single-pixel staging), kT = 2
+    (4, 64, 48, (1, 1, 1), (6, 8), (0, 0, 0)),    # 1x1, kT = 1
+    (2, 96, 64, (3, 1, 1), (5, 6), (2, 0, 0)),    # 1x1 spatial, delay 0
+    (5, 32, 64, (3, 3, 3), (14, 14), (0, 1, 1)),  # tiles spanning streams
+]
+
+
+@pytest.mark.parametrize("case", GEMM_STEPS_CASES, ids=lambda c: "gemmsteps_" + "_".join(
+    map(str, c[:3])) + f"_k{c[3][0]}")
+def test_gemm_forward_steps_persistent(case):
+    """The LDS-tiled GEMM's forward_steps as one persistent launch (bf16):
+    a workgroup owns pixels x output channels x every temporal tap, the
+    partial sums stay in its registers across frames."""
+    B, cin, cout, k, size, p = case
+    say("gemm steps", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          padding=p, dtype="bf16")
+    x, w, b = synth.conv_inputs(spec, 12, 97000 + 5 * cin + cout, "kaiming")
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=p, algo="gemm")
+
+    assert make().algo == "gemm_bf16"
+    _check_fused_steps(make, x, oracle_conv(w, b, (1, 1, 1), p, (1, 1, 1), 1), torch.bfloat16,
+                       "gemm steps")
+
+
 @pytest.mark.parametrize("name,streams", [
+    ("conv3d_b64_c192_k3_14x14_bf16", (0, 37, 63)),
     ("conv1d_b1_c4to8_k3_f32", None),
     ("conv3d_b1_c24_k3_56x56_f32", None),
     ("conv2d_b32_c64to256_k9x1_v25_f32", (0, 13, 31)),
