@@ -10,6 +10,8 @@
 // from registers and updates that element's partial sums in the float32 ring
 // (slot, C, B, Ho, Wo).  Consecutive threads own consecutive output pixels,
 // so ring and output traffic is coalesced; the step is bound by HBM.
+#include <algorithm>
+
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -265,6 +267,167 @@ __global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
   }
 }
 
+// Small planes (Ho * Wo <= 64): one wave per (stream, channel) plane and one
+// lane per output pixel.  A plane's frames lie contiguously in the clip, so
+// the wave moves a block of F frames with a couple of 16-byte loads per lane
+// (aligned down to 16 bytes; the buffer returns zero past its end) into its
+// own LDS region, and each lane reads its stencil from there.  The
+// thread-per-output kernel above issues one 2-byte gather per tap, output
+// and frame instead.  Double buffered: block k + 1 sits in registers while
+// block k is evaluated.  The taps, partial sums and summation order are those
+// of the thread-per-output kernel.
+constexpr int kDwpWaves = 4;   // planes per workgroup
+constexpr int kDwpLoads = 2;   // 16-byte loads per lane and block
+constexpr int kDwpUnits = 64 * kDwpLoads;  // 16-byte LDS units per wave and buffer
+
+struct DwpArgs {
+  int32_t F;        // frames per block: (F * S * esz + 31) <= 16 * kDwpUnits
+  int32_t nblk;     // blocks: ceil(count / F)
+  int32_t frame_bytes;
+};
+
+template <typename T, int KH, int KW, int KT>
+__global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
+    ConvGeom g, DwSteps ds, DwpArgs pa, const T* __restrict__ x, int64_t x_bc,
+    T* __restrict__ y, int64_t y_bc, const float* __restrict__ w,
+    const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot) {
+  constexpr int NS = KH * KW;
+  constexpr uint32_t esz = sizeof(T);
+  __shared__ uint4 lds[kDwpWaves][2][kDwpUnits];
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  const int BC = g.B * g.Cout;
+  const int bc_raw = int(blockIdx.x) * kDwpWaves + wave;
+  const bool wlive = bc_raw < BC;  // whole waves; idle ones still meet the barriers
+  const int bc = wlive ? bc_raw : 0;
+  const int So = g.Ho * g.Wo;
+  const bool pl = wlive && lane < So;
+  const int p = lane < So ? lane : 0;
+  const int bq = fdiv(bc, ds.fd_Cout), c = bc - bq * g.Cout;
+  const int i = fdiv(p, ds.fd_Wo), jo = p - i * g.Wo;
+  const int ridx = (c * g.B + bq) * So + p;
+
+  float wr[KT][NS];
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+#pragma unroll
+    for (int e = 0; e < NS; ++e) wr[j][e] = w[(c * KT + j) * NS + e];
+  const float bo = bias[c];
+  float acc[KT];
+#pragma unroll
+  for (int q = 0; q < KT; ++q) {
+    const int tau = ds.v0 - (KT - 1) + q;
+    const int sl = (ds.slot0 + q) % KT;
+    acc[q] = (pl && q < KT - 1 && tau >= 0) ? ring[sl * ring_slot + ridx] : 0.f;
+  }
+  // stencil: element offset inside a frame, or -1 outside it
+  int soff[NS];
+#pragma unroll
+  for (int u = 0; u < KH; ++u) {
+    const int hi = i * g.sH + u * g.dH - g.pH;
+#pragma unroll
+    for (int v = 0; v < KW; ++v) {
+      const int wi = jo * g.sW + v * g.dW - g.pW;
+      const bool in = hi >= 0 && hi < g.H && wi >= 0 && wi < g.W;
+      soff[u * KW + v] = in ? hi * g.W + wi : -1;
+    }
+  }
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ds.x_bytes);
+  const int plane0 = int(uint32_t(bc) * uint32_t(x_bc) * esz);  // byte offset of the plane's clip
+  // block k: real frames [k F, min(k F + F, T)) of the plane, from the
+  // 16-byte boundary at or below their first byte
+  auto fetch = [&](int k, uint4 (&rb)[kDwpLoads]) {
+    const int t0 = k * pa.F;
+    const int nr = min(max(ds.T - t0, 0), pa.F);
+    const int s0 = plane0 + t0 * pa.frame_bytes;
+    const int a0 = s0 & ~15;
+    const int nunits = nr > 0 ? (s0 + nr * pa.frame_bytes - a0 + 15) >> 4 : 0;
+#pragma unroll
+    for (int l = 0; l < kDwpLoads; ++l) {
+      const int u = l * 64 + lane;
+      const int off = a0 + u * 16;
+      if (!wlive || u >= nunits) {
+        rb[l] = make_uint4(0u, 0u, 0u, 0u);
+      } else if (off + 16 <= ds.x_bytes) {
+        const auto v4 = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+        rb[l] = make_uint4(v4[0], v4[1], v4[2], v4[3]);
+      } else {
+        // the unit that runs past the end of the clip: 2-byte reads, each
+        // inside the buffer or at the out-of-range offset
+        uint32_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          h[e] = __builtin_amdgcn_raw_buffer_load_b16(
+              xr, off + 2 * e + 2 <= ds.x_bytes ? off + 2 * e : kOutOfRange, 0, 0);
+        rb[l] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                           h[6] | (h[7] << 16));
+      }
+    }
+  };
+  auto stash = [&](int buf, const uint4 (&rb)[kDwpLoads]) {
+#pragma unroll
+    for (int l = 0; l < kDwpLoads; ++l) lds[wave][buf][l * 64 + lane] = rb[l];
+  };
+
+  T* yb = y + int64_t(bc) * y_bc + p;
+  uint4 rb[kDwpLoads];
+  fetch(0, rb);
+  stash(0, rb);
+  if (pa.nblk > 1) fetch(1, rb);
+  __syncthreads();
+  for (int k = 0; k < pa.nblk; ++k) {
+    const int buf = k & 1;
+    const int t0 = k * pa.F;
+    const int shift = ((plane0 + t0 * pa.frame_bytes) & 15) / int(esz);  // elements
+    const T* fr = reinterpret_cast<const T*>(&lds[wave][buf][0]) + shift;
+    for (int f = 0; f < pa.F; ++f) {
+      const int t = t0 + f;
+      if (t >= ds.count) break;  // uniform
+      const bool real = t < ds.T;
+      float xv[NS];
+#pragma unroll
+      for (int e = 0; e < NS; ++e)
+        xv[e] = (real && soff[e] >= 0) ? to_f32<T>(fr[f * (pa.frame_bytes / int(esz)) + soff[e]])
+                                       : 0.f;
+      const int v = ds.v0 + t;
+#pragma unroll
+      for (int j = KT - 1; j >= 0; --j) {
+        const int q = KT - 1 - j;
+        const int tau = v - j;
+        if (tau < 0) continue;
+        const int first = tau >= g.pT ? 0 : g.pT - tau;
+        float a = (j == first) ? 0.f : acc[q];
+#pragma unroll
+        for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
+        if (j == KT - 1) {
+          if (pl) yb[int64_t(ds.k0 + t) * So] = from_f32<T>(a + bo);
+        } else {
+          acc[q] = a;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q + 1 < KT; ++q) acc[q] = acc[q + 1];
+    }
+    if (k + 1 < pa.nblk) {
+      // block k + 1 into the buffer block k - 1 used (every wave left it at
+      // the last barrier), then block k + 2 into registers
+      stash(buf ^ 1, rb);
+      if (k + 2 < pa.nblk) fetch(k + 2, rb);
+    }
+    __syncthreads();
+  }
+  if (ds.update && pl) {
+    const int v1 = ds.v0 + ds.count;
+#pragma unroll
+    for (int q = 0; q + 1 < KT; ++q) {
+      const int tau = v1 - (KT - 1) + q;
+      const int sl = (ds.slot0 + ds.count + q) % KT;
+      if (tau >= 0) ring[sl * ring_slot + ridx] = acc[q];
+    }
+  }
+}
+
 template <typename T, int KH, int KW, int KT>
 hipError_t dw_steps_launch(const ConvGeom& g, const ConvLayout& L, char* state, const void* x,
                            int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
@@ -284,6 +447,21 @@ hipError_t dw_steps_launch(const ConvGeom& g, const ConvLayout& L, char* state, 
   ds.fd_So = make_fastdiv(uint32_t(g.So()));
   ds.fd_Cout = make_fastdiv(uint32_t(g.Cout));
   ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  const int64_t fbytes = g.S() * esz;
+  if (g.So() <= 64 && fbytes + 31 <= 16 * kDwpUnits) {
+    DwpArgs pa;
+    pa.F = int32_t(std::min<int64_t>(16, (16 * kDwpUnits - 31) / fbytes));
+    pa.nblk = int32_t((int64_t(count) + pa.F - 1) / pa.F);
+    pa.frame_bytes = int32_t(fbytes);
+    const int64_t planes = int64_t(g.B) * g.Cout;
+    hipLaunchKernelGGL((conv_steps_dwp_kernel<T, KH, KW, KT>),
+                       dim3(unsigned((planes + kDwpWaves - 1) / kDwpWaves)), dim3(64 * kDwpWaves),
+                       0, s, g, ds, pa, static_cast<const T*>(x), x_bc, static_cast<T*>(y), y_bc,
+                       reinterpret_cast<const float*>(state + L.weight),
+                       reinterpret_cast<const float*>(state + L.bias),
+                       reinterpret_cast<float*>(state + L.ring), L.ring_slot_elems);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((conv_steps_dw_kernel<T, KH, KW, KT>), dim3(grid_for(g.out_frame_elems())),
                      dim3(kBlock), 0, s, g, ds, static_cast<const T*>(x), x_bc,
                      static_cast<T*>(y), y_bc, reinterpret_cast<const float*>(state + L.weight),

@@ -473,6 +473,8 @@ DW_STEPS_CASES = [
     (2, 9, 2, (3, 3), (5, 8), (1, 0, 1), "f32"),      # delay 0, valid rows
     (4, 16, 4, (1, 1), (3, 3), (3, 0, 0), "bf16"),    # pointwise taps, full padding
     (1, 33, 5, (3, 3), (9, 4), (2, 1, 1), "f32"),     # ragged, kT = 5
+    (1, 3, 3, (3, 3), (5, 5), (1, 1, 1), "bf16"),     # clip bytes not a multiple of 16
+    (2, 8, 3, (3, 3), (10, 9), (1, 1, 1), "bf16"),    # 90 output pixels: thread per output
 ]
 
 
@@ -668,6 +670,7 @@ def test_gemm_forward_steps_persistent(case):
 
 @pytest.mark.parametrize("name,streams", [
     ("conv3d_b64_c192_k3_14x14_bf16", (0, 37, 63)),
+    ("dwconv3d_b16_c432_k3_7x7_avgpool_bf16", (0, 9, 15)),
     ("conv1d_b1_c4to8_k3_f32", None),
     ("conv3d_b1_c24_k3_56x56_f32", None),
     ("conv2d_b32_c64to256_k9x1_v25_f32", (0, 13, 31)),
