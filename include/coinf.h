@@ -315,6 +315,99 @@ co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t st
                                int64_t n, void* stream, co_pool_handle** out);
 co_status co_pool_destroy(co_pool_handle* h);
 
+/*
+ * Delay (section 3.2, co.Delay): shifts a stream by `delay` steps, so that
+ * parallel branches with different delays meet on the same frame
+ * (Principle 7; residual connections, section 3.1.1).  Step n outputs input
+ * frame n - delay; the first `delay` steps are empty.  The state is a ring of
+ * `delay` input frames in the io dtype.  A frame is (batch, channels,
+ * frame_elems) contiguous elements; frame_elems is the product of the
+ * spatial sizes (1 for a 1-D stream).
+ */
+typedef struct co_delay_desc {
+  int32_t batch;
+  int32_t channels;
+  int32_t frame_elems;
+  int32_t delay;                  /* >= 0 */
+  int32_t dtype;                  /* CO_F32 | CO_BF16 */
+} co_delay_desc;
+
+typedef struct co_delay_handle co_delay_handle;
+
+/* State size of a descriptor (CO_EINVAL for an invalid one).  Host only. */
+co_status co_delay_query(const co_delay_desc* desc, int64_t* state_bytes);
+
+/* Clean state over a caller-allocated buffer of at least state_bytes bytes. */
+co_status co_delay_init_state(const co_delay_desc* desc, void* state, int64_t state_bytes,
+                              void* stream, co_delay_handle** out);
+
+/*
+ * forward_step: y_t := x_{n - delay} (CO_OK) or nothing (CO_EMPTY, n < delay).
+ * y_t may be NULL to only advance the stream.  update_state = 0 reads
+ * without storing x_t or advancing.
+ */
+co_status co_delay_forward_step(co_delay_handle* h, const void* x_t, void* y_t,
+                                int32_t update_state, void* stream);
+
+/*
+ * Residual merge step (Principle 7, reduce "sum"): y_t := a_t + x_{n - delay}
+ * in one pass, a_t being the wrapped module's output of this step (a_t and
+ * y_t may alias).  CO_EMPTY with y_t untouched while n < delay; the stream
+ * still advances.  Accumulates in float32 and rounds once to the io dtype.
+ */
+co_status co_delay_add_step(co_delay_handle* h, const void* x_t, const void* a_t, void* y_t,
+                            int32_t update_state, void* stream);
+
+/*
+ * forward_steps over x (batch, channels, T, frame_elems): the non-empty
+ * outputs, in order, into y (batch, channels, y_cap_frames, frame_elems);
+ * *n_out = their count.  CO_EINVAL when they would exceed y_cap_frames.
+ */
+co_status co_delay_forward_steps(co_delay_handle* h, const void* x, int32_t T, void* y,
+                                 int32_t y_cap_frames, int32_t update_state, void* stream,
+                                 int32_t* n_out);
+
+/*
+ * Residual merge over clips: y[b, c, i] := a[b, c, i] + x[b, c, i + lag] for
+ * i < a_frames, where the wrapped module's outputs a (batch, channels,
+ * a_frames, frame_elems) are aligned with the last a_frames steps of this
+ * call and lag = T - a_frames - delay + (steps before the call) is the
+ * residual's offset into x.  Advances the stream by T steps like
+ * co_delay_forward_steps (x_{n - delay} earlier than x comes from the ring).
+ * CO_EINVAL when some residual frame precedes the stream.
+ */
+co_status co_delay_add_steps(co_delay_handle* h, const void* x, int32_t T, const void* a,
+                             int32_t a_frames, void* y, int32_t update_state, void* stream);
+
+/*
+ * Clip-mode merge (no state): y[bc, i, e] := a[bc, i, e] + x[bc, i + x_offset, e]
+ * for bc < rows, i < a_frames, e < frame_elems; a and y hold a_frames frames
+ * per row, x holds x_frames.  Used by residual connections in clip mode,
+ * where a centred residual is shrunk by x_offset frames (section 3.1.1).
+ */
+co_status co_add_frames(const void* a, const void* x, void* y, int32_t rows, int32_t frame_elems,
+                        int32_t a_frames, int32_t x_frames, int32_t x_offset, int32_t dtype,
+                        void* stream);
+
+co_status co_delay_clean_state(co_delay_handle* h, void* stream);
+co_status co_delay_get_steps(const co_delay_handle* h, int64_t* n);
+co_status co_delay_destroy(co_delay_handle* h);
+
+/*
+ * Accumulated receptive field and delay of a chain of n layers (Principle 6),
+ * each layer given by its temporal receptive field f, stride s and padding p,
+ * in the form the principle's worked example evaluates (f = {3, 3},
+ * s = {2, 1}, p = {2, 0} gives f_acc = 7, p_acc = 2, d = 4):
+ *   f_acc(0) = f(0), p_acc(0) = p(0), s_acc(0) = s(0);
+ *   f_acc(i) = f_acc(i-1) + (f(i) - 1) * s_acc(i-1);
+ *   p_acc(i) = p_acc(i-1) + p(i) * s_acc(i-1);
+ *   s_acc(i) = s_acc(i-1) * s(i);
+ *   d(i) = f_acc(i) - p_acc(i) - 1.
+ * Writes the values of the last layer.  Host only.
+ */
+co_status co_chain_delay(int32_t n, const int32_t* f, const int32_t* s, const int32_t* p,
+                         int64_t* f_acc, int64_t* p_acc, int64_t* s_acc, int64_t* delay);
+
 #ifdef __cplusplus
 }
 #endif

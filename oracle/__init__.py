@@ -406,3 +406,132 @@ class ContinualPool(_ContinualBase):
     def forward(self, x):
         return pool_forward(self.kind, x, self.kernel, self.stride, self.padding,
                             self.dilation, self.count_include_pad)
+
+
+# ---------------------------------------------------------------- composition
+#
+# Section 3.1.1 (residual connections), section 3.2 (co.Delay), section 3.3
+# (containers) and Principles 6-7.  Written from the text: a delay is a FIFO
+# of input frames; parallel branches follow one clock and a merge of an empty
+# value is empty (Principle 7); a chain passes each non-empty output on.
+
+
+class ContinualDelay:
+    """co.Delay(d): step n returns input frame n - d, empty (None) for n < d;
+    forward (clip mode) is the identity."""
+
+    def __init__(self, d):
+        if d < 0:
+            raise ValueError("negative delay")
+        self.d = d
+        self.clean_state()
+
+    delay = property(lambda self: self.d)
+    receptive_field = property(lambda self: self.d + 1)
+
+    def clean_state(self):
+        self.fifo = []
+        self.n = 0
+
+    def forward_step(self, x_t, update_state=True):
+        fifo = self.fifo + [np.asarray(x_t, dtype=np.float64)]
+        y = fifo.pop(0) if len(fifo) > self.d else None
+        if update_state:
+            self.fifo, self.n = fifo, self.n + 1
+        return y
+
+    def forward(self, x):
+        return np.asarray(x, dtype=np.float64)
+
+
+def _steps(mod, x):
+    """forward_step over the T axis; non-empty outputs stacked (None if none)."""
+    outs = [mod.forward_step(x[:, :, t]) for t in range(x.shape[2])]
+    outs = [o for o in outs if o is not None]
+    return np.stack(outs, axis=2) if outs else None
+
+
+class ContinualParallelSum:
+    """Two branches on one input stream and one clock, merged by a sum
+    (Principle 7: the merge is empty whenever a branch's value is)."""
+
+    def __init__(self, a, b):
+        self.a, self.b = a, b
+
+    delay = property(lambda self: max(self.a.delay, self.b.delay))
+
+    def clean_state(self):
+        self.a.clean_state()
+        self.b.clean_state()
+
+    def forward_step(self, x_t, update_state=True):
+        ya = self.a.forward_step(x_t, update_state)
+        yb = self.b.forward_step(x_t, update_state)
+        if ya is None or yb is None:
+            return None
+        return ya + yb
+
+    def forward_steps(self, x):
+        return _steps(self, np.asarray(x, dtype=np.float64))
+
+
+class ContinualResidual(ContinualParallelSum):
+    """Residual connection (section 3.1.1) around a stride-1 module with
+    receptive field f and temporal padding p: the input branch is delayed by
+    (f - 1) // 2 steps, which aligns it with the centre of the module's
+    window; clip mode adds the input shrunk by (f - 1) // 2 - p frames at each
+    end (the centred residual; nothing is dropped with equal padding)."""
+
+    def __init__(self, module):
+        self.module = module
+        self.shrink = (module.f - 1) // 2 - module.pT
+        if self.shrink < 0:
+            raise ValueError("more temporal padding than the centre alignment allows")
+        super().__init__(module, ContinualDelay((module.f - 1) // 2))
+
+    def forward(self, x):
+        y = self.module.forward(x)
+        x = np.asarray(x, dtype=np.float64)
+        return y + x[:, :, self.shrink:self.shrink + y.shape[2]]
+
+
+class ContinualChain:
+    """Modules in sequence: each non-empty step output feeds the next module;
+    an empty one ends the step (section 3.3, Sequential)."""
+
+    def __init__(self, *mods):
+        self.mods = list(mods)
+
+    def clean_state(self):
+        for m in self.mods:
+            m.clean_state()
+
+    def forward_step(self, x_t, update_state=True):
+        for m in self.mods:
+            x_t = m.forward_step(x_t, update_state)
+            if x_t is None:
+                return None
+        return x_t
+
+    def forward_steps(self, x):
+        return _steps(self, np.asarray(x, dtype=np.float64))
+
+    def forward(self, x):
+        for m in self.mods:
+            x = m.forward(x)
+        return x
+
+
+def chain_delay(f, s, p):
+    """Principle 6 for layers with temporal receptive fields f, strides s and
+    paddings p, in the form its worked example evaluates (the printed
+    recurrences give f_acc = 5 and p_acc = 0 on that example, which states 7
+    and 2): each layer's receptive field and padding count in units of the
+    accumulated stride of the layers before it.  Returns the last layer's
+    (f_acc, p_acc, s_acc, delay)."""
+    f_acc, p_acc, s_acc = f[0], p[0], s[0]
+    for fi, si, pi in zip(f[1:], s[1:], p[1:]):
+        f_acc = f_acc + (fi - 1) * s_acc
+        p_acc = p_acc + pi * s_acc
+        s_acc = s_acc * si
+    return f_acc, p_acc, s_acc, f_acc - p_acc - 1

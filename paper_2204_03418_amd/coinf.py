@@ -67,6 +67,11 @@ class PoolInfo(ctypes.Structure):
                 ("fifo_slots", i32), ("reserved", i32), ("state_bytes", i64)]
 
 
+class DelayDesc(ctypes.Structure):
+    _fields_ = [("batch", i32), ("channels", i32), ("frame_elems", i32), ("delay", i32),
+                ("dtype", i32)]
+
+
 class PoolPlan(ctypes.Structure):
     _fields_ = [("emit", i32), ("n_taps", i32), ("out_index", i64), ("write_slot", i32),
                 ("reserved", i32), ("src", i32 * CO_MAX_TAPS)]
@@ -111,6 +116,19 @@ co_pool_clean_state = _sig("co_pool_clean_state", i32, [vp, vp])
 co_pool_get_steps = _sig("co_pool_get_steps", i32, [vp, pi64])
 co_pool_attach_state = _sig("co_pool_attach_state", i32, [PD, vp, i64, i64, vp, pvp])
 co_pool_destroy = _sig("co_pool_destroy", i32, [vp])
+DD = ctypes.POINTER(DelayDesc)
+co_delay_query = _sig("co_delay_query", i32, [DD, pi64])
+co_delay_init_state = _sig("co_delay_init_state", i32, [DD, vp, i64, vp, pvp])
+co_delay_forward_step = _sig("co_delay_forward_step", i32, [vp, vp, vp, i32, vp])
+co_delay_add_step = _sig("co_delay_add_step", i32, [vp, vp, vp, vp, i32, vp])
+co_delay_forward_steps = _sig("co_delay_forward_steps", i32,
+                              [vp, vp, i32, vp, i32, i32, vp, pi32])
+co_delay_add_steps = _sig("co_delay_add_steps", i32, [vp, vp, i32, vp, i32, vp, i32, vp])
+co_add_frames = _sig("co_add_frames", i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp])
+co_delay_clean_state = _sig("co_delay_clean_state", i32, [vp, vp])
+co_delay_get_steps = _sig("co_delay_get_steps", i32, [vp, pi64])
+co_delay_destroy = _sig("co_delay_destroy", i32, [vp])
+co_chain_delay = _sig("co_chain_delay", i32, [i32, pi32, pi32, pi32, pi64, pi64, pi64, pi64])
 
 
 class CoinfError(RuntimeError):
@@ -214,6 +232,17 @@ def _need(t, dtype, shape, what):
         raise ValueError(f"{what} must be contiguous")
 
 
+def _n_emit(n0, count, d, s):
+    """Non-empty steps among steps n0 .. n0 + count - 1 (Principles 4-5: step n
+    emits iff n >= d and (n - d) mod s == 0)."""
+    lo = max(n0, d)
+    hi = n0 + count
+    if hi <= lo:
+        return 0
+    first = lo + (-(lo - d)) % s
+    return 0 if first >= hi else (hi - 1 - first) // s + 1
+
+
 class CoConv:
     """A continual ConvNd layer over a device state buffer (co_conv_* ABI).
 
@@ -267,6 +296,14 @@ class CoConv:
         return self.info.receptive_field
 
     @property
+    def t_stride(self):
+        return self.desc.stride[0]
+
+    @property
+    def t_padding(self):
+        return self.desc.padding[0]
+
+    @property
     def algo(self):
         return co_conv_algo_name(self.handle).decode()
 
@@ -301,10 +338,12 @@ class CoConv:
                                     _stream(stream))
 
     def forward_steps(self, x, pad_end=False, update_state=True):
-        """Principle 2 forward_steps over x (B, C_in, T, *S); None when empty."""
+        """Principle 2 forward_steps over x (B, C_in, T, *S); None when empty.
+        The result is contiguous, sized to the frames the call emits."""
         T = x.shape[2]
         _need(x, self.torch_dtype, (self.batch, self.in_channels, T) + self.in_size, "x")
-        cap = T + (self.desc.padding[0] if pad_end else 0)
+        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
+                      self.desc.stride[0])
         y = torch.empty((self.batch, self.out_channels, cap) + self.out_size,
                         dtype=self.torch_dtype, device=x.device)
         n = i32()
@@ -317,7 +356,8 @@ class CoConv:
 
     def steps_fused(self, T, pad_end=False):
         """True when forward_steps over T frames runs as one persistent launch."""
-        cap = T + (self.desc.padding[0] if pad_end else 0)
+        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
+                      self.desc.stride[0])
         f = i32()
         check(co_conv_steps_fused(self.handle, T, cap, ctypes.byref(f)), "co_conv_steps_fused")
         return bool(f.value)
@@ -383,6 +423,14 @@ class CoPool:
         return self.info.receptive_field
 
     @property
+    def t_stride(self):
+        return self.desc.stride[0]
+
+    @property
+    def t_padding(self):
+        return self.desc.padding[0]
+
+    @property
     def steps(self):
         n = i64()
         check(co_pool_get_steps(self.handle, ctypes.byref(n)), "co_pool_get_steps")
@@ -411,7 +459,8 @@ class CoPool:
     def forward_steps(self, x, pad_end=False, update_state=True):
         T = x.shape[2]
         _need(x, self.torch_dtype, (self.batch, self.channels, T) + self.in_size, "x")
-        cap = T + (self.desc.padding[0] if pad_end else 0)
+        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
+                      self.desc.stride[0])
         y = torch.empty((self.batch, self.channels, cap) + self.out_size,
                         dtype=self.torch_dtype, device=x.device)
         n = i32()
@@ -424,7 +473,8 @@ class CoPool:
 
     def steps_fused(self, T, pad_end=False):
         """True when forward_steps over T frames runs as one persistent launch."""
-        cap = T + (self.desc.padding[0] if pad_end else 0)
+        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
+                      self.desc.stride[0])
         f = i32()
         check(co_pool_steps_fused(self.handle, T, cap, ctypes.byref(f)), "co_pool_steps_fused")
         return bool(f.value)
@@ -442,3 +492,222 @@ class CoPool:
 
     def clean_state(self):
         check(co_pool_clean_state(self.handle, _stream()), "co_pool_clean_state")
+
+
+def chain_delay(layers):
+    """Principle 6 over a chain of layers (anything with receptive_field,
+    t_stride and t_padding): (f_acc, p_acc, s_acc, delay) of the last one."""
+    n = len(layers)
+    arr = i32 * n
+    f = arr(*[m.receptive_field for m in layers])
+    st = arr(*[m.t_stride for m in layers])
+    p = arr(*[m.t_padding for m in layers])
+    out = [i64() for _ in range(4)]
+    check(co_chain_delay(n, f, st, p, *[ctypes.byref(o) for o in out]), "co_chain_delay")
+    return tuple(o.value for o in out)
+
+
+class CoDelay:
+    """co.Delay: step n outputs frame n - delay (empty before); clip mode is
+    the identity.  Frames are (batch, channels, *in_size)."""
+
+    def __init__(self, delay, *, batch, channels, in_size=(), dtype=torch.float32,
+                 device="cuda"):
+        self.torch_dtype = dtype
+        self.batch, self.channels, self.in_size = batch, channels, tuple(in_size)
+        self.out_channels, self.out_size = channels, tuple(in_size)
+        E = 1
+        for v in in_size:
+            E *= int(v)
+        self.E = E
+        self.desc = DelayDesc(batch, channels, E, int(delay), DTYPES[dtype])
+        nb = i64()
+        check(co_delay_query(ctypes.byref(self.desc), ctypes.byref(nb)), "co_delay_query")
+        self.state = torch.empty(max(nb.value, 1), dtype=torch.uint8, device=device)
+        h = ctypes.c_void_p()
+        check(co_delay_init_state(ctypes.byref(self.desc), _ptr(self.state), self.state.numel(),
+                                  _stream(), ctypes.byref(h)), "co_delay_init_state")
+        self.handle = h
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            co_delay_destroy(h)
+            self.handle = None
+
+    delay = property(lambda self: self.desc.delay)
+    receptive_field = property(lambda self: self.desc.delay + 1)
+    t_stride = property(lambda self: 1)
+    t_padding = property(lambda self: 0)
+
+    @property
+    def steps(self):
+        n = i64()
+        check(co_delay_get_steps(self.handle, ctypes.byref(n)), "co_delay_get_steps")
+        return n.value
+
+    def frame_shape(self):
+        return (self.batch, self.channels) + self.in_size
+
+    def forward_step(self, x_t, update_state=True, out=None, emit=True):
+        """x_{n - delay}, or None while empty; emit=False only advances."""
+        _need(x_t, self.torch_dtype, self.frame_shape(), "x_t")
+        y = None
+        if emit:
+            y = torch.empty_like(x_t) if out is None else out
+        st = check(co_delay_forward_step(self.handle, _ptr(x_t), _ptr(y),
+                                         1 if update_state else 0, _stream()),
+                   "co_delay_forward_step")
+        return y if (st == CO_OK and emit) else None
+
+    def add_step(self, x_t, a_t, update_state=True, out=None):
+        """a_t + x_{n - delay} (the residual merge), or None while empty."""
+        _need(x_t, self.torch_dtype, self.frame_shape(), "x_t")
+        _need(a_t, self.torch_dtype, self.frame_shape(), "a_t")
+        y = torch.empty_like(a_t) if out is None else out
+        st = check(co_delay_add_step(self.handle, _ptr(x_t), _ptr(a_t), _ptr(y),
+                                     1 if update_state else 0, _stream()), "co_delay_add_step")
+        return y if st == CO_OK else None
+
+    def forward_steps(self, x, update_state=True):
+        T = x.shape[2]
+        _need(x, self.torch_dtype, (self.batch, self.channels, T) + self.in_size, "x")
+        y = torch.empty_like(x)
+        n = i32()
+        check(co_delay_forward_steps(self.handle, _ptr(x), T, _ptr(y), T,
+                                     1 if update_state else 0, _stream(), ctypes.byref(n)),
+              "co_delay_forward_steps")
+        return y[:, :, :n.value] if n.value else None
+
+    def add_steps(self, x, a, update_state=True):
+        """a (the last a.shape[2] steps' module outputs) + the delayed x."""
+        T = x.shape[2]
+        _need(x, self.torch_dtype, (self.batch, self.channels, T) + self.in_size, "x")
+        na = 0 if a is None else a.shape[2]
+        y = None
+        if na:
+            _need(a, self.torch_dtype, (self.batch, self.channels, na) + self.in_size, "a")
+            y = torch.empty_like(a)
+        check(co_delay_add_steps(self.handle, _ptr(x), T, _ptr(a) if na else None, na,
+                                 _ptr(y) if na else None, 1 if update_state else 0, _stream()),
+              "co_delay_add_steps")
+        return y
+
+    def forward(self, x):
+        return x
+
+    def clean_state(self):
+        check(co_delay_clean_state(self.handle, _stream()), "co_delay_clean_state")
+
+
+def add_frames(a, x, x_offset=0):
+    """y[:, :, i] = a[:, :, i] + x[:, :, i + x_offset] (clip-mode merge)."""
+    rows = a.shape[0] * a.shape[1]
+    E = 1
+    for v in a.shape[3:]:
+        E *= int(v)
+    y = torch.empty_like(a)
+    check(co_add_frames(_ptr(a), _ptr(x), _ptr(y), rows, E, a.shape[2], x.shape[2],
+                        int(x_offset), DTYPES[a.dtype], _stream()), "co_add_frames")
+    return y
+
+
+class Sequential:
+    """Section 3.3's Sequential: modules in a chain; an empty step output
+    ends the step (downstream modules do not advance), and the chain's delay
+    follows Principle 6."""
+
+    def __init__(self, *modules):
+        self.modules = list(modules)
+
+    @property
+    def delay(self):
+        return chain_delay(self.modules)[3]
+
+    @property
+    def receptive_field(self):
+        return chain_delay(self.modules)[0]
+
+    @property
+    def t_stride(self):
+        return chain_delay(self.modules)[2]
+
+    @property
+    def t_padding(self):
+        return chain_delay(self.modules)[1]
+
+    def forward_step(self, x_t, update_state=True):
+        for m in self.modules:
+            x_t = m.forward_step(x_t, update_state=update_state)
+            if x_t is None:
+                return None
+        return x_t
+
+    def forward_steps(self, x, update_state=True):
+        for m in self.modules:
+            x = m.forward_steps(x, update_state=update_state)
+            if x is None:
+                return None
+        return x
+
+    def forward(self, x):
+        for m in self.modules:
+            x = m.forward(x)
+        return x
+
+    def clean_state(self):
+        for m in self.modules:
+            m.clean_state()
+
+
+class Residual:
+    """Section 3.1.1's residual connection around a module with equal input
+    and output frames (stride 1): the input joins the module's output aligned
+    on the centre of its receptive field, so the residual branch is delayed by
+    (f - 1) // 2 steps (Principle 7: the whole has the module's delay, and a
+    step is empty while either branch is).  With equal temporal padding
+    ((f - 1) / 2) clip mode adds the input as is; a module with less padding
+    needs residual_shrink=True, which drops the border frames of the input in
+    clip mode (the centred residual)."""
+
+    def __init__(self, module, residual_shrink=False):
+        if module.t_stride != 1:
+            raise ValueError("residual connections need temporal stride 1")
+        f, p = module.receptive_field, module.t_padding
+        self.module = module
+        self.d_res = (f - 1) // 2
+        self.shrink = self.d_res - p
+        if self.shrink < 0 or (self.shrink > 0 and not residual_shrink):
+            raise ValueError("clip shapes differ: give the module padding (f - 1) / 2 or "
+                             "residual_shrink=True")
+        self.line = CoDelay(self.d_res, batch=module.batch, channels=module.out_channels,
+                            in_size=module.out_size, dtype=module.torch_dtype,
+                            device=module.state.device)
+
+    delay = property(lambda self: max(self.module.delay, self.d_res))
+    receptive_field = property(lambda self: self.module.receptive_field)
+    t_stride = property(lambda self: 1)
+    t_padding = property(lambda self: self.module.t_padding)
+    batch = property(lambda self: self.module.batch)
+    out_channels = property(lambda self: self.module.out_channels)
+    out_size = property(lambda self: self.module.out_size)
+    torch_dtype = property(lambda self: self.module.torch_dtype)
+
+    def forward_step(self, x_t, update_state=True):
+        a = self.module.forward_step(x_t, update_state=update_state)
+        if a is None:
+            self.line.forward_step(x_t, update_state=update_state, emit=False)
+            return None
+        return self.line.add_step(x_t, a, update_state=update_state, out=a)
+
+    def forward_steps(self, x, update_state=True):
+        a = self.module.forward_steps(x, update_state=update_state)
+        return self.line.add_steps(x, a, update_state=update_state)
+
+    def forward(self, x):
+        a = self.module.forward(x)
+        return add_frames(a, x, self.shrink)
+
+    def clean_state(self):
+        self.module.clean_state()
+        self.line.clean_state()

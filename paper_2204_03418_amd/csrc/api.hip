@@ -1,6 +1,7 @@
 // C ABI of libcoinf: validation, handle bookkeeping and the step loops.
 // Every entry point validates on the host before it enqueues anything, so a
 // negative status means nothing ran and the handle is unchanged.
+#include <algorithm>
 #include <new>
 
 #include "device.hpp"
@@ -20,6 +21,12 @@ struct co_pool_handle {
   PoolLayout L;
   char* state;
   int64_t n;
+};
+
+struct co_delay_handle {
+  DelayGeom g;
+  char* state;
+  int64_t n;  // frames consumed since the last clean state
 };
 
 namespace {
@@ -492,6 +499,168 @@ co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t st
 co_status co_pool_destroy(co_pool_handle* h) {
   if (!h) return CO_EINVAL;
   delete h;
+  return CO_OK;
+}
+
+
+// ------------------------------------------------------------ delay, merges
+
+namespace {
+constexpr int64_t kMaxLaunchElems = int64_t(1) << 38;  // grid limit at 256 threads
+}
+
+co_status co_delay_query(const co_delay_desc* desc, int64_t* state_bytes) {
+  if (!state_bytes) return CO_EINVAL;
+  DelayGeom g;
+  const co_status st = delay_geom(desc, &g);
+  if (st != CO_OK) return st;
+  *state_bytes = g.state_bytes();
+  return CO_OK;
+}
+
+co_status co_delay_init_state(const co_delay_desc* desc, void* state, int64_t state_bytes,
+                              void* stream, co_delay_handle** out) {
+  if (!out || !state) return CO_EINVAL;
+  DelayGeom g;
+  co_status st = delay_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (state_bytes < g.state_bytes()) return CO_ESTATE;
+  const uint64_t hash = delay_hash(g);
+  StateHeader hdr{kDelayMagic, kStateVersion, hash, g.state_bytes(), 0, g.d};
+  co_delay_handle* h = new (std::nothrow) co_delay_handle{g, static_cast<char*>(state), 0};
+  if (!h) return CO_EINVAL;
+  st = hip_status(launch_delay_init(g, h->state, hdr, as_stream(stream)));
+  if (st != CO_OK) {
+    delete h;
+    return st;
+  }
+  *out = h;
+  return CO_OK;
+}
+
+co_status co_delay_forward_step(co_delay_handle* h, const void* x_t, void* y_t,
+                                int32_t update_state, void* stream) {
+  if (!h || !x_t) return CO_EINVAL;
+  const bool emit = h->n >= h->g.d && y_t;
+  if (emit || (update_state && h->g.d > 0)) {
+    const co_status st = hip_status(launch_delay_step(h->g, h->state, x_t, nullptr, y_t, h->n,
+                                                      emit, update_state != 0,
+                                                      as_stream(stream)));
+    if (st != CO_OK) return st;
+  }
+  const bool nonempty = h->n >= h->g.d;
+  if (update_state) ++h->n;
+  return nonempty ? CO_OK : CO_EMPTY;
+}
+
+co_status co_delay_add_step(co_delay_handle* h, const void* x_t, const void* a_t, void* y_t,
+                            int32_t update_state, void* stream) {
+  if (!h || !x_t) return CO_EINVAL;
+  const bool emit = h->n >= h->g.d;
+  if (emit && (!a_t || !y_t)) return CO_EINVAL;
+  if (emit || (update_state && h->g.d > 0)) {
+    const co_status st = hip_status(launch_delay_step(h->g, h->state, x_t, emit ? a_t : nullptr,
+                                                      emit ? y_t : nullptr, h->n, emit,
+                                                      update_state != 0, as_stream(stream)));
+    if (st != CO_OK) return st;
+  }
+  if (update_state) ++h->n;
+  return emit ? CO_OK : CO_EMPTY;
+}
+
+co_status co_delay_forward_steps(co_delay_handle* h, const void* x, int32_t T, void* y,
+                                 int32_t y_cap_frames, int32_t update_state, void* stream,
+                                 int32_t* n_out) {
+  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  const DelayGeom& g = h->g;
+  const int64_t first = std::min<int64_t>(T, std::max<int64_t>(0, g.d - h->n));
+  const int32_t nout = int32_t(T - first);
+  if (nout > y_cap_frames || (nout > 0 && !y)) return CO_EINVAL;
+  if (g.frame() * std::max<int64_t>(T, 1) > kMaxLaunchElems) return CO_EINVAL;
+  const co_status st = hip_status(launch_delay_steps(g, h->state, x, T, nullptr, y, y_cap_frames,
+                                                     h->n, int32_t(first), nout,
+                                                     update_state != 0, as_stream(stream)));
+  if (st != CO_OK) return st;
+  if (update_state) h->n += T;
+  *n_out = nout;
+  return CO_OK;
+}
+
+co_status co_delay_add_steps(co_delay_handle* h, const void* x, int32_t T, const void* a,
+                             int32_t a_frames, void* y, int32_t update_state, void* stream) {
+  if (!h || T < 0 || a_frames < 0 || a_frames > T) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  if (a_frames > 0 && (!a || !y)) return CO_EINVAL;
+  const DelayGeom& g = h->g;
+  const int64_t first = int64_t(T) - a_frames;  // step of a's first frame in this call
+  if (a_frames > 0 && h->n + first < g.d) return CO_EINVAL;  // residual precedes the stream
+  if (g.frame() * std::max<int64_t>(T, 1) > kMaxLaunchElems) return CO_EINVAL;
+  const co_status st = hip_status(launch_delay_steps(g, h->state, x, T, a, y, a_frames, h->n,
+                                                     int32_t(first), a_frames,
+                                                     update_state != 0, as_stream(stream)));
+  if (st != CO_OK) return st;
+  if (update_state) h->n += T;
+  return CO_OK;
+}
+
+co_status co_add_frames(const void* a, const void* x, void* y, int32_t rows, int32_t frame_elems,
+                        int32_t a_frames, int32_t x_frames, int32_t x_offset, int32_t dtype,
+                        void* stream) {
+  if (rows < 0 || frame_elems < 1 || a_frames < 0 || x_frames < 0 || x_offset < 0) return CO_EINVAL;
+  if (dtype != CO_F32 && dtype != CO_BF16) return CO_EINVAL;
+  if (int64_t(x_offset) + a_frames > x_frames) return CO_EINVAL;
+  const int64_t total = int64_t(rows) * a_frames * frame_elems;
+  if (total == 0) return CO_OK;
+  if (!a || !x || !y || total > kMaxLaunchElems) return CO_EINVAL;
+  return hip_status(launch_add_frames(a, x, y, rows, frame_elems, a_frames, x_frames, x_offset,
+                                      dtype, as_stream(stream)));
+}
+
+co_status co_delay_clean_state(co_delay_handle* h, void* stream) {
+  (void)stream;
+  if (!h) return CO_EINVAL;
+  // every ring slot is written before it is read again
+  h->n = 0;
+  return CO_OK;
+}
+
+co_status co_delay_get_steps(const co_delay_handle* h, int64_t* n) {
+  if (!h || !n) return CO_EINVAL;
+  *n = h->n;
+  return CO_OK;
+}
+
+co_status co_delay_destroy(co_delay_handle* h) {
+  if (!h) return CO_EINVAL;
+  delete h;
+  return CO_OK;
+}
+
+co_status co_chain_delay(int32_t n, const int32_t* f, const int32_t* s, const int32_t* p,
+                         int64_t* f_acc, int64_t* p_acc, int64_t* s_acc, int64_t* delay) {
+  if (n < 1 || !f || !s || !p || !f_acc || !p_acc || !s_acc || !delay) return CO_EINVAL;
+  // Principle 6 in the form its worked example evaluates: layer i's
+  // receptive field and padding count in units of the accumulated stride of
+  // the layers before it.
+  int64_t fa = 0, pa = 0, sa = 1;
+  for (int32_t i = 0; i < n; ++i) {
+    if (f[i] < 1 || s[i] < 1 || p[i] < 0) return CO_EINVAL;
+    if (i == 0) {
+      fa = f[0];
+      pa = p[0];
+      sa = s[0];
+    } else {
+      fa = fa + int64_t(f[i] - 1) * sa;
+      pa = pa + int64_t(p[i]) * sa;
+      sa = sa * s[i];
+    }
+    if (fa > (int64_t(1) << 40) || sa > (int64_t(1) << 40)) return CO_EINVAL;
+  }
+  *f_acc = fa;
+  *p_acc = pa;
+  *s_acc = sa;
+  *delay = fa - pa - 1;
   return CO_OK;
 }
 

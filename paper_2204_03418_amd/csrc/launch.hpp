@@ -106,4 +106,16 @@ hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* 
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, hipStream_t stream);
 
+// Delay line and residual merges (delay.hip).
+hipError_t launch_delay_init(const DelayGeom& g, char* state, const StateHeader& hdr,
+                             hipStream_t stream);
+hipError_t launch_delay_step(const DelayGeom& g, char* state, const void* x, const void* a,
+                             void* y, int64_t n, bool emit, bool update, hipStream_t stream);
+hipError_t launch_delay_steps(const DelayGeom& g, char* state, const void* x, int32_t T,
+                              const void* a, void* y, int32_t y_frames, int64_t n0,
+                              int32_t t_first, int32_t nout, bool update, hipStream_t stream);
+hipError_t launch_add_frames(const void* a, const void* x, void* y, int64_t rows, int32_t E,
+                             int32_t a_frames, int32_t x_frames, int32_t x_offset, int32_t dtype,
+                             hipStream_t stream);
+
 }  // namespace coinf

@@ -591,4 +591,20 @@ int64_t pool_emissions(const PoolGeom& g, int64_t n, int64_t count) {
   return (hi - 1 - first) / g.sT + 1;
 }
 
+co_status delay_geom(const co_delay_desc* desc, DelayGeom* g) {
+  if (!desc || !g) return CO_EINVAL;
+  const co_delay_desc& d = *desc;
+  if (d.batch < 1 || d.channels < 1 || d.frame_elems < 1 || d.delay < 0) return CO_EINVAL;
+  if (d.dtype != CO_F32 && d.dtype != CO_BF16) return CO_EINVAL;
+  DelayGeom r{d.batch, d.channels, d.frame_elems, d.delay, d.dtype};
+  if (r.frame() > kMaxI32 || int64_t(r.d) * r.frame() * r.esz() > (int64_t(1) << 40))
+    return CO_EINVAL;
+  *g = r;
+  return CO_OK;
+}
+
+uint64_t delay_hash(const DelayGeom& g) {
+  return fnv1a(1469598103934665603ull ^ 0x44454c59ull, &g, sizeof(g));
+}
+
 }  // namespace coinf

@@ -188,6 +188,20 @@ constexpr uint32_t kConvMagic = 0x564E4F43u;  // "CONV"
 constexpr uint32_t kPoolMagic = 0x4C4F4F50u;  // "POOL"
 constexpr uint32_t kStateVersion = 1;
 
+constexpr uint32_t kDelayMagic = 0x594C4544u;  // "DELY"
+
+// Delay geometry: frames of B x C x E elements, a ring of d input frames
+// laid out (slot, B, C, E) in the io dtype after the header.
+struct DelayGeom {
+  int32_t B, C, E, d, dtype;
+  int64_t frame() const { return int64_t(B) * C * E; }
+  int64_t esz() const { return dtype == CO_BF16 ? 2 : 4; }
+  int64_t ring_offset() const { return kHeaderBytes; }
+  int64_t state_bytes() const { return kHeaderBytes + int64_t(d) * frame() * esz(); }
+};
+co_status delay_geom(const co_delay_desc* desc, DelayGeom* g);
+uint64_t delay_hash(const DelayGeom& g);
+
 // State header, written at init and checked on attach.
 struct StateHeader {
   uint32_t magic;

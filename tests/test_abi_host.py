@@ -308,3 +308,47 @@ def test_frame_resident_gemm_shapes():
                 C.conv_desc(2, 512, 32, (3, 3, 3), (14, 14), padding=(0, 1, 1),
                             dtype=C.CO_BF16, algo="gemm_img")):                # LDS
         assert _status(bad) == C.CO_ENOTSUP
+
+
+def _chain(f, s, p):
+    n = len(f)
+    arr = ctypes.c_int32 * n
+    out = [ctypes.c_int64() for _ in range(4)]
+    st = C.co_chain_delay(n, arr(*f), arr(*s), arr(*p), *[ctypes.byref(o) for o in out])
+    return st, tuple(o.value for o in out)
+
+
+def test_chain_delay_principle6():
+    """co_chain_delay against the worked example (printed values) and the
+    oracle's chain formula, itself pinned by stepped chains."""
+    assert _chain([3, 3], [2, 1], [2, 0]) == (C.CO_OK, (7, 2, 2, 4))
+    assert _chain([3, 4], [1, 1], [0, 0]) == (C.CO_OK, (6, 0, 1, 5))   # conv then pool: d = 5
+    rng = np.random.default_rng(17)
+    for _ in range(200):
+        n = int(rng.integers(1, 5))
+        f = [int(v) for v in rng.integers(1, 8, n)]
+        s = [int(v) for v in rng.integers(1, 4, n)]
+        p = [int(rng.integers(0, fi)) for fi in f]
+        st, got = _chain(f, s, p)
+        assert st == C.CO_OK and got == oracle.chain_delay(f, s, p)
+    assert _chain([3, 0], [1, 1], [0, 0])[0] == C.CO_EINVAL
+    assert _chain([3], [0], [0])[0] == C.CO_EINVAL
+    assert _chain([3], [1], [-1])[0] == C.CO_EINVAL
+
+
+def test_delay_query_and_validation():
+    d = C.DelayDesc(2, 3, 5, 4, C.CO_BF16)
+    nb = ctypes.c_int64()
+    assert C.co_delay_query(ctypes.byref(d), ctypes.byref(nb)) == C.CO_OK
+    assert nb.value == 256 + 4 * 2 * 3 * 5 * 2
+    for bad in (C.DelayDesc(0, 3, 5, 1, C.CO_F32), C.DelayDesc(1, 3, 5, -1, C.CO_F32),
+                C.DelayDesc(1, 3, 0, 1, C.CO_F32), C.DelayDesc(1, 3, 5, 1, 7)):
+        assert C.co_delay_query(ctypes.byref(bad), ctypes.byref(nb)) == C.CO_EINVAL
+    # a state buffer that is too small is rejected before any device work
+    h = ctypes.c_void_p()
+    buf = ctypes.create_string_buffer(16)
+    assert C.co_delay_init_state(ctypes.byref(d), buf, 16, None, ctypes.byref(h)) == C.CO_ESTATE
+    # clip merge: shape and argument checks happen on the host
+    assert C.co_add_frames(None, None, None, 4, 3, 0, 5, 0, C.CO_F32, None) == C.CO_OK
+    assert C.co_add_frames(None, None, None, 4, 3, 4, 5, 2, C.CO_F32, None) == C.CO_EINVAL
+    assert C.co_add_frames(None, None, None, 4, 0, 1, 5, 0, C.CO_F32, None) == C.CO_EINVAL
