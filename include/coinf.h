@@ -316,6 +316,35 @@ co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t st
 co_status co_pool_destroy(co_pool_handle* h);
 
 /*
+ * Fused step of a depthwise convolution and the pool that consumes its output
+ * (sections 3.2-3.3; the X3D bottleneck closes with such a pair), when the
+ * pool's spatial window is the whole output plane (kernel = stride = the
+ * plane, no spatial padding: a 1x1 pooled frame), the plane has at most 64
+ * pixels and the kernels are 3x3 or 1x1.  The fused handle borrows the two
+ * handles (it neither owns nor frees them) and advances their states and
+ * step counters exactly as co_conv_forward_step followed, when the
+ * convolution emits, by co_pool_forward_step would: the results are
+ * identical, and fused and separate calls can be mixed.  The intermediate
+ * frame is not written anywhere.  CO_ENOTSUP when the pair does not fit.
+ */
+typedef struct co_convpool_handle co_convpool_handle;
+
+co_status co_convpool_bind(co_conv_handle* conv, co_pool_handle* pool, co_convpool_handle** out);
+
+/* One step: x_t (B, C, S1, S2) in; the pool's output z_t (B, C, 1, 1) when
+ * both emit (CO_OK), else CO_EMPTY with z_t untouched. */
+co_status co_convpool_forward_step(co_convpool_handle* h, const void* x_t, void* z_t,
+                                   int32_t update_state, void* stream);
+
+/* T steps over x (B, C, T, S1, S2); the non-empty outputs, in order, into
+ * z (B, C, z_cap_frames, 1, 1); *n_out = their count. */
+co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_t T, void* z,
+                                    int32_t z_cap_frames, int32_t update_state, void* stream,
+                                    int32_t* n_out);
+
+co_status co_convpool_destroy(co_convpool_handle* h);
+
+/*
  * Delay (section 3.2, co.Delay): shifts a stream by `delay` steps, so that
  * parallel branches with different delays meet on the same frame
  * (Principle 7; residual connections, section 3.1.1).  Step n outputs input

@@ -129,6 +129,11 @@ co_delay_clean_state = _sig("co_delay_clean_state", i32, [vp, vp])
 co_delay_get_steps = _sig("co_delay_get_steps", i32, [vp, pi64])
 co_delay_destroy = _sig("co_delay_destroy", i32, [vp])
 co_chain_delay = _sig("co_chain_delay", i32, [i32, pi32, pi32, pi32, pi64, pi64, pi64, pi64])
+co_convpool_bind = _sig("co_convpool_bind", i32, [vp, vp, pvp])
+co_convpool_forward_step = _sig("co_convpool_forward_step", i32, [vp, vp, vp, i32, vp])
+co_convpool_forward_steps = _sig("co_convpool_forward_steps", i32,
+                                 [vp, vp, i32, vp, i32, i32, vp, pi32])
+co_convpool_destroy = _sig("co_convpool_destroy", i32, [vp])
 
 
 class CoinfError(RuntimeError):
@@ -612,13 +617,91 @@ def add_frames(a, x, x_offset=0):
     return y
 
 
+class ConvPool:
+    """A depthwise CoConv followed by a CoPool over its whole output plane,
+    stepped as one launch (co_convpool_*).  Both modules keep their states and
+    step counters, and the outputs equal stepping them separately."""
+
+    def __init__(self, conv, pool):
+        h = ctypes.c_void_p()
+        check(co_convpool_bind(conv.handle, pool.handle, ctypes.byref(h)), "co_convpool_bind")
+        self.conv, self.pool, self.handle = conv, pool, h
+
+    @staticmethod
+    def fits(conv, pool):
+        h = ctypes.c_void_p()
+        if co_convpool_bind(conv.handle, pool.handle, ctypes.byref(h)) != CO_OK:
+            return False
+        co_convpool_destroy(h)
+        return True
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            co_convpool_destroy(h)
+            self.handle = None
+
+    delay = property(lambda self: chain_delay([self.conv, self.pool])[3])
+    receptive_field = property(lambda self: chain_delay([self.conv, self.pool])[0])
+    t_stride = property(lambda self: chain_delay([self.conv, self.pool])[2])
+    t_padding = property(lambda self: chain_delay([self.conv, self.pool])[1])
+
+    def _out(self, frames, device):
+        return torch.empty((self.pool.batch, self.pool.channels, frames) + self.pool.out_size,
+                           dtype=self.pool.torch_dtype, device=device)
+
+    def forward_step(self, x_t, update_state=True):
+        _need(x_t, self.conv.torch_dtype, self.conv.frame_shape(), "x_t")
+        z = torch.empty(self.pool.out_frame_shape(), dtype=self.pool.torch_dtype,
+                        device=x_t.device)
+        st = check(co_convpool_forward_step(self.handle, _ptr(x_t), _ptr(z),
+                                            1 if update_state else 0, _stream()),
+                   "co_convpool_forward_step")
+        return z if st == CO_OK else None
+
+    def forward_steps(self, x, update_state=True):
+        T = x.shape[2]
+        c, p = self.conv, self.pool
+        _need(x, c.torch_dtype, (c.batch, c.in_channels, T) + c.in_size, "x")
+        n_c = _n_emit(c.steps, T, c.delay, c.t_stride)
+        cap = _n_emit(p.steps, n_c, p.delay, p.t_stride)
+        z = self._out(cap, x.device)
+        n = i32()
+        check(co_convpool_forward_steps(self.handle, _ptr(x), T, _ptr(z), cap,
+                                        1 if update_state else 0, _stream(), ctypes.byref(n)),
+              "co_convpool_forward_steps")
+        return z if n.value else None
+
+    def forward(self, x):
+        return self.pool.forward(self.conv.forward(x))
+
+    def clean_state(self):
+        self.conv.clean_state()
+        self.pool.clean_state()
+
+
 class Sequential:
     """Section 3.3's Sequential: modules in a chain; an empty step output
     ends the step (downstream modules do not advance), and the chain's delay
-    follows Principle 6."""
+    follows Principle 6.  With fuse (the default) a depthwise CoConv directly
+    followed by a CoPool over its whole output plane runs as one ConvPool
+    launch per step, with identical results."""
 
-    def __init__(self, *modules):
-        self.modules = list(modules)
+    def __init__(self, *modules, fuse=True):
+        mods = list(modules)
+        if fuse:
+            out, i = [], 0
+            while i < len(mods):
+                a = mods[i]
+                b = mods[i + 1] if i + 1 < len(mods) else None
+                if isinstance(a, CoConv) and isinstance(b, CoPool) and ConvPool.fits(a, b):
+                    out.append(ConvPool(a, b))
+                    i += 2
+                else:
+                    out.append(a)
+                    i += 1
+            mods = out
+        self.modules = mods
 
     @property
     def delay(self):

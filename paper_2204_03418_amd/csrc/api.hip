@@ -23,6 +23,11 @@ struct co_pool_handle {
   int64_t n;
 };
 
+struct co_convpool_handle {
+  co_conv_handle* conv;
+  co_pool_handle* pool;
+};
+
 struct co_delay_handle {
   DelayGeom g;
   char* state;
@@ -661,6 +666,107 @@ co_status co_chain_delay(int32_t n, const int32_t* f, const int32_t* s, const in
   *p_acc = pa;
   *s_acc = sa;
   *delay = fa - pa - 1;
+  return CO_OK;
+}
+
+
+// -------------------------------------------------- fused depthwise + pool
+
+co_status co_convpool_bind(co_conv_handle* conv, co_pool_handle* pool, co_convpool_handle** out) {
+  if (!conv || !pool || !out) return CO_EINVAL;
+  if (!convpool_supported(conv->g, pool->g)) return CO_ENOTSUP;
+  co_convpool_handle* h = new (std::nothrow) co_convpool_handle{conv, pool};
+  if (!h) return CO_EINVAL;
+  *out = h;
+  return CO_OK;
+}
+
+namespace {
+
+// One fused step at the handles' counters, reading frame planes x_bc
+// elements apart; *emitted says whether z was written.
+co_status convpool_step(co_convpool_handle* h, const void* x_t, int64_t x_bc, void* z,
+                        int64_t z_bc, bool update, hipStream_t s, bool* emitted) {
+  co_conv_handle* c = h->conv;
+  co_pool_handle* p = h->pool;
+  co_step_plan cplan;
+  conv_plan(c->g, c->n, update, &cplan);
+  co_pool_plan pplan;
+  if (cplan.emit) pool_plan(p->g, p->n, &pplan);
+  const bool pemit = cplan.emit && pplan.emit;
+  if (pemit && !z) return CO_EINVAL;
+  if (any_tap(cplan) || cplan.emit) {
+    const co_status st = hip_status(launch_convpool_step(c->g, c->L, c->state, p->g, p->L,
+                                                         p->state, x_t, x_bc, z, z_bc, cplan,
+                                                         cplan.emit ? &pplan : nullptr, update, s));
+    if (st != CO_OK) return st;
+  }
+  if (update) {
+    ++c->n;
+    if (cplan.emit) ++p->n;
+  }
+  *emitted = pemit;
+  return CO_OK;
+}
+
+}  // namespace
+
+co_status co_convpool_forward_step(co_convpool_handle* h, const void* x_t, void* z_t,
+                                   int32_t update_state, void* stream) {
+  if (!h || !x_t) return CO_EINVAL;
+  bool emitted = false;
+  const co_status st = convpool_step(h, x_t, h->conv->g.S(), z_t, 1, update_state != 0,
+                                     as_stream(stream), &emitted);
+  if (st != CO_OK) return st;
+  return emitted ? CO_OK : CO_EMPTY;
+}
+
+co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_t T, void* z,
+                                    int32_t z_cap_frames, int32_t update_state, void* stream,
+                                    int32_t* n_out) {
+  if (!h || T < 0 || z_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  co_conv_handle* c = h->conv;
+  co_pool_handle* p = h->pool;
+  // the pool steps once per emitted convolution frame
+  const int64_t conv_out = conv_emissions(c->g, c->n, T);
+  const int64_t n_emit = pool_emissions(p->g, p->n, conv_out);
+  if (n_emit > z_cap_frames || (n_emit > 0 && !z)) return CO_EINVAL;
+  const int64_t x_bc = int64_t(T) * c->g.S();
+  const size_t esz = c->g.dtype == CO_BF16 ? 2 : 4;
+  if ((int64_t(c->g.B) * c->g.Cin * x_bc) * int64_t(esz) >= (int64_t(1) << 31)) return CO_EINVAL;
+  hipStream_t s = as_stream(stream);
+  Backup bk_ring, bk_fifo;
+  const int64_t n0c = c->n, n0p = p->n;
+  if (!update_state) {
+    co_status st = backup_range(c->state + c->L.ring, int64_t(c->g.R) * c->L.ring_slot_elems * 4,
+                                s, &bk_ring);
+    if (st == CO_OK)
+      st = backup_range(p->state + p->L.valid, p->L.total - p->L.valid, s, &bk_fifo);
+    if (st != CO_OK) return st;
+  }
+  co_status st = CO_OK;
+  int64_t k = 0;
+  for (int32_t t = 0; t < T && st == CO_OK; ++t) {
+    bool emitted = false;
+    st = convpool_step(h, static_cast<const char*>(x) + size_t(t) * c->g.S() * esz, x_bc,
+                       static_cast<char*>(z) + size_t(k) * esz, z_cap_frames, true, s, &emitted);
+    if (emitted) ++k;
+  }
+  if (!update_state) {
+    const co_status r1 = restore_range(c->state + c->L.ring, s, &bk_ring);
+    const co_status r2 = restore_range(p->state + p->L.valid, s, &bk_fifo);
+    if (st == CO_OK) st = r1 != CO_OK ? r1 : r2;
+    c->n = n0c;
+    p->n = n0p;
+  }
+  *n_out = int32_t(k);
+  return st;
+}
+
+co_status co_convpool_destroy(co_convpool_handle* h) {
+  if (!h) return CO_EINVAL;
+  delete h;
   return CO_OK;
 }
 

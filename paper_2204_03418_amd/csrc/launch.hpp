@@ -106,6 +106,18 @@ hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* 
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, hipStream_t stream);
 
+// Fused depthwise convolution step + global spatial pool step (convpool.hip):
+// one launch per step; pplan is null when the convolution does not emit
+// (the pool does not step); x_bc is the element stride between frame planes.
+// The pair must satisfy convpool_supported, and the planes reachable from x
+// must span fewer than 2^31 bytes.
+bool convpool_supported(const ConvGeom& g, const PoolGeom& pg);
+hipError_t launch_convpool_step(const ConvGeom& g, const ConvLayout& L, char* cstate,
+                                const PoolGeom& pg, const PoolLayout& PL, char* pstate,
+                                const void* x, int64_t x_bc, void* z, int64_t z_bc,
+                                const co_step_plan& cplan, const co_pool_plan* pplan, bool update,
+                                hipStream_t stream);
+
 // Delay line and residual merges (delay.hip).
 hipError_t launch_delay_init(const DelayGeom& g, char* state, const StateHeader& hdr,
                              hipStream_t stream);

@@ -107,15 +107,16 @@ def test_x3d_bottleneck_sequential():
     w2 = synth.normal((C, 1, 3, 3, 3), 4402, std=0.3, dtype="bf16")
     b2 = synth.normal((C,), 4403, std=0.1, dtype="bf16")
 
-    def make():
+    def make(fuse=True):
         return coinf.Sequential(
             coinf.CoConv(w1.to(DEV), None, batch=B, in_size=(7, 7)),
             coinf.CoConv(w2.to(DEV), b2.to(DEV), batch=B, in_size=(7, 7), padding=(1, 1, 1),
                          groups=C),
             coinf.CoPool("avg", batch=B, channels=C, kernel=(4, 7, 7), in_size=(7, 7),
-                         stride=(1, 7, 7), dtype=tdt))
+                         stride=(1, 7, 7), dtype=tdt), fuse=fuse)
 
     seq = make()
+    assert isinstance(seq.modules[1], coinf.ConvPool) and len(seq.modules) == 2
     assert seq.delay == 4
     ref = oracle.ContinualChain(
         oracle.ContinualConv(np64(w1), None),
@@ -131,3 +132,110 @@ def test_x3d_bottleneck_sequential():
     assert_close(np64(got), r, tdt, "bottleneck steps")
     ys = make().forward_steps(xd)
     assert torch.equal(ys, got)
+    # the unfused chain gives the same bits
+    assert torch.equal(make(fuse=False).forward_steps(xd), got)
+
+
+CONVPOOL_CASES = [
+    # B, C, kernel (time first), in_size, conv padding, pool kind, pool kT, cip, dtype
+    (4, 24, (3, 3, 3), (7, 7), (0, 1, 1), "avg", 4, True, "bf16"),   # the X3D block
+    (3, 10, (2, 3, 3), (5, 6), (1, 1, 1), "max", 3, True, "f32"),
+    (2, 7, (3, 1, 1), (4, 4), (2, 0, 0), "avg", 2, False, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", CONVPOOL_CASES, ids=lambda c: f"convpool_{c[5]}_{c[8]}")
+def test_fused_depthwise_pool_step(case):
+    """co_convpool: one launch per step equals the depthwise conv step
+    followed by the pool step bit for bit (steps, clips, mixing fused and
+    separate calls, update_state=False), and the oracle chain."""
+    B, C, k, size, pad, kind, pk, cip, dt = case
+    say("convpool", case)
+    tdt = synth.torch_dtype(dt)
+    T = 14
+    x = synth.normal((B, C, T) + size, 4500 + C, dtype=dt)
+    w = synth.normal((C, 1) + k, 4501 + C, std=0.3, dtype=dt)
+    b = synth.normal((C,), 4502 + C, std=0.1, dtype=dt)
+    xd = x.to(DEV)
+    ho, wo = size[0] - k[1] + 1 + 2 * pad[1], size[1] - k[2] + 1 + 2 * pad[2]
+
+    def pair():
+        conv = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=pad, groups=C)
+        pool = coinf.CoPool(kind, batch=B, channels=C, kernel=(pk, ho, wo), in_size=(ho, wo),
+                            stride=(1, ho, wo), count_include_pad=cip, dtype=tdt)
+        return conv, pool
+
+    def separate(conv, pool, t):
+        y = conv.forward_step(xd[:, :, t].contiguous())
+        return None if y is None else pool.forward_step(y)
+
+    c1, p1 = pair()
+    ref = [separate(c1, p1, t) for t in range(T)]
+    c2, p2 = pair()
+    fused = coinf.ConvPool(c2, p2)
+    got = [fused.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    assert [g is None for g in got] == [r is None for r in ref]
+    for g_, r_ in zip(got, ref):
+        if r_ is not None:
+            assert torch.equal(g_, r_)
+    seq = [r_ for r_ in ref if r_ is not None]
+    # a clip in one call
+    c3, p3 = pair()
+    zc = coinf.ConvPool(c3, p3).forward_steps(xd)
+    assert torch.equal(zc, torch.stack(seq, dim=2))
+    # fused steps continuing separate ones, and the other way round
+    c4, p4 = pair()
+    f4 = coinf.ConvPool(c4, p4)
+    mix = [separate(c4, p4, t) for t in range(5)] + [f4.forward_step(xd[:, :, t].contiguous())
+                                                       for t in range(5, 10)]
+    mix += [separate(c4, p4, t) for t in range(10, T)]
+    for g_, r_ in zip(mix, ref):
+        assert (g_ is None and r_ is None) or torch.equal(g_, r_)
+    # update_state=False leaves both states and counters as they were
+    torch.cuda.synchronize()
+    cs, ps, n = c4.state.clone(), p4.state.clone(), (c4.steps, p4.steps)
+    f4.forward_steps(xd[:, :, :6].contiguous(), update_state=False)
+    f4.forward_step(xd[:, :, 0].contiguous(), update_state=False)
+    torch.cuda.synchronize()
+    assert torch.equal(c4.state, cs) and torch.equal(p4.state, ps)
+    assert (c4.steps, p4.steps) == n
+    # the oracle chain
+    ch = oracle.ContinualChain(
+        oracle.ContinualConv(np64(w), np64(b), padding=pad, groups=C),
+        oracle.ContinualPool(kind, (pk, ho, wo), stride=(1, ho, wo), count_include_pad=cip))
+    assert_close(np64(zc), ch.forward_steps(np64(x)), tdt, "convpool vs oracle")
+
+
+def test_fused_depthwise_pool_workload():
+    """The X3D-style workload at full size: fused clip call against separate
+    steps (bitwise) and the oracle on sampled streams."""
+    name = "dwconv3d_b16_c432_k3_7x7_avgpool_bf16"
+    wl = synth.WORKLOADS[name]
+    c, pl = wl.conv, wl.pool
+    say("convpool workload")
+    x, w, b = synth.workload_inputs(name)
+    x = x[:, :, :20].contiguous()
+    xd = x.to(DEV)
+
+    def pair():
+        conv = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size,
+                            padding=c.padding, groups=c.groups)
+        pool = coinf.CoPool("avg", batch=pl.batch, channels=pl.channels, kernel=pl.kernel,
+                            in_size=pl.in_size, stride=pl.stride, dtype=torch.bfloat16)
+        return conv, pool
+
+    z = coinf.ConvPool(*pair()).forward_steps(xd)
+    conv, pool = pair()
+    outs = []
+    for t in range(x.shape[2]):
+        y = conv.forward_step(xd[:, :, t].contiguous())
+        if y is not None:
+            zz = pool.forward_step(y)
+            if zz is not None:
+                outs.append(zz)
+    assert torch.equal(z, torch.stack(outs, dim=2))
+    sel = [0, 7, 15]
+    ch = oracle.ContinualChain(
+        oracle.ContinualConv(np64(w), np64(b), padding=c.padding, groups=c.groups),
+        oracle.ContinualPool("avg", pl.kernel, stride=pl.stride))
+    assert_close(np64(z[sel]), ch.forward_steps(np64(x[sel])), torch.bfloat16, "workload")
