@@ -275,6 +275,34 @@ def main():
         torch.cuda.synchronize()
         modes["forward_steps"] = round(c.batch * calls * T / (s0.elapsed_time(s1) / 1e3), 1)
 
+        # (iv) a depthwise convolution feeding a global pool: the fused step
+        # (one launch per step, the same results as the two-launch chain)
+        if po is not None and coinf.ConvPool.fits(co, po):
+            cp = coinf.ConvPool(co, po)
+            cp_step = coinf.co_convpool_forward_step
+            for i in range(2 * T):
+                cp_step(cp.handle, fptr[(n + i) % T], zptr, 1, sp)
+            n += 2 * T
+            f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            f0.record(stream)
+            for i in range(K):
+                cp_step(cp.handle, fptr[(n + i) % T], zptr, 1, sp)
+            f1.record(stream)
+            torch.cuda.synchronize()
+            n += K
+            modes["fused_convpool_step"] = round(c.batch * K / (f0.elapsed_time(f1) / 1e3), 1)
+            # and the fused clip: one launch per forward_steps call where it fits
+            cp.forward_steps(xc)
+            torch.cuda.synchronize()
+            f0.record(stream)
+            for _ in range(calls):
+                cp.forward_steps(xc)
+            f1.record(stream)
+            torch.cuda.synchronize()
+            modes["fused_convpool_forward_steps"] = round(
+                c.batch * calls * T / (f0.elapsed_time(f1) / 1e3), 1)
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl, x, w, b, args.cpu_seconds)

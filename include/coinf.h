@@ -337,7 +337,11 @@ co_status co_convpool_forward_step(co_convpool_handle* h, const void* x_t, void*
                                    int32_t update_state, void* stream);
 
 /* T steps over x (B, C, T, S1, S2); the non-empty outputs, in order, into
- * z (B, C, z_cap_frames, 1, 1); *n_out = their count. */
+ * z (B, C, z_cap_frames, 1, 1); *n_out = their count.  With temporal stride
+ * and dilation 1 in both modules, both kT <= 5 and a padded input plane of
+ * at most 128 elements the clip runs as one launch that keeps both states in
+ * registers; otherwise as one fused launch per frame.  Same results either
+ * way, and the same results as stepping. */
 co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_t T, void* z,
                                     int32_t z_cap_frames, int32_t update_state, void* stream,
                                     int32_t* n_out);

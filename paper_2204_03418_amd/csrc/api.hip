@@ -736,8 +736,21 @@ co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_
   const size_t esz = c->g.dtype == CO_BF16 ? 2 : 4;
   if ((int64_t(c->g.B) * c->g.Cin * x_bc) * int64_t(esz) >= (int64_t(1) << 31)) return CO_EINVAL;
   hipStream_t s = as_stream(stream);
-  Backup bk_ring, bk_fifo;
   const int64_t n0c = c->n, n0p = p->n;
+  if (T > 0 && convpool_steps_supported(c->g, p->g, T)) {
+    // one persistent launch; with update_state = 0 it writes no state
+    const co_status st = hip_status(launch_convpool_steps(c->g, c->L, c->state, p->g, p->L,
+                                                          p->state, x, T, z, z_cap_frames, n0c,
+                                                          n0p, update_state != 0, s));
+    if (st != CO_OK) return st;
+    if (update_state) {
+      c->n += T;
+      p->n += conv_out;
+    }
+    *n_out = int32_t(n_emit);
+    return CO_OK;
+  }
+  Backup bk_ring, bk_fifo;
   if (!update_state) {
     co_status st = backup_range(c->state + c->L.ring, int64_t(c->g.R) * c->L.ring_slot_elems * 4,
                                 s, &bk_ring);

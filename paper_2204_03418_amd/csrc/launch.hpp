@@ -44,6 +44,10 @@ hipError_t launch_pool_init(const PoolGeom& g, const PoolLayout& L, char* state,
 // temporal stride 1 and dilation 1, kT <= 5, a spatial window of at most 64,
 // clips below 2^31 bytes.
 bool pool_steps_supported(const PoolGeom& g, int64_t x_frames);
+// Validity flags of the FIFO slots that pool steps n0 .. n0 + count - 1 wrote
+// (the first T real frames, the rest end padding).
+hipError_t launch_pool_valid(float* valid, int32_t R, int64_t n0, int32_t count, int32_t T,
+                             hipStream_t stream);
 hipError_t launch_pool_steps(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
                              int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
                              int64_t n0, bool update, hipStream_t stream);
@@ -117,6 +121,15 @@ hipError_t launch_convpool_step(const ConvGeom& g, const ConvLayout& L, char* cs
                                 const void* x, int64_t x_bc, void* z, int64_t z_bc,
                                 const co_step_plan& cplan, const co_pool_plan* pplan, bool update,
                                 hipStream_t stream);
+// The same pair over a clip x (B, C, T, H, W) in one launch, from the
+// handles' step counters n0c (convolution) and n0p (pool): the pooled
+// outputs go to z (B, C, z_cap, 1, 1) from frame 0; with update the ring, the
+// FIFO and the FIFO's validity flags advance (the host advances the counters).
+bool convpool_steps_supported(const ConvGeom& g, const PoolGeom& pg, int64_t T);
+hipError_t launch_convpool_steps(const ConvGeom& g, const ConvLayout& L, char* cstate,
+                                 const PoolGeom& pg, const PoolLayout& PL, char* pstate,
+                                 const void* x, int32_t T, void* z, int64_t z_cap, int64_t n0c,
+                                 int64_t n0p, bool update, hipStream_t stream);
 
 // Delay line and residual merges (delay.hip).
 hipError_t launch_delay_init(const DelayGeom& g, char* state, const StateHeader& hdr,

@@ -445,6 +445,12 @@ hipError_t pool_steps_t(const PoolGeom& g, const PoolLayout& L, char* state, con
 
 }  // namespace
 
+hipError_t launch_pool_valid(float* valid, int32_t R, int64_t n0, int32_t count, int32_t T,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(pool_valid_kernel, dim3(1), dim3(64), 0, s, valid, R, n0, count, T);
+  return hipGetLastError();
+}
+
 bool pool_steps_supported(const PoolGeom& g, int64_t x_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   return g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64 &&  // (kT <= 8: tree)

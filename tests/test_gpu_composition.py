@@ -141,6 +141,8 @@ CONVPOOL_CASES = [
     (4, 24, (3, 3, 3), (7, 7), (0, 1, 1), "avg", 4, True, "bf16"),   # the X3D block
     (3, 10, (2, 3, 3), (5, 6), (1, 1, 1), "max", 3, True, "f32"),
     (2, 7, (3, 1, 1), (4, 4), (2, 0, 0), "avg", 2, False, "f32"),
+    # a padded plane too large for the one-launch clip: per-frame fused launches
+    (2, 5, (3, 3, 3), (10, 10), (1, 0, 0), "avg", 3, False, "bf16"),
 ]
 
 
@@ -183,6 +185,11 @@ def test_fused_depthwise_pool_step(case):
     c3, p3 = pair()
     zc = coinf.ConvPool(c3, p3).forward_steps(xd)
     assert torch.equal(zc, torch.stack(seq, dim=2))
+    # the clip in two calls: the second continues the state the first left
+    c5, p5 = pair()
+    f5 = coinf.ConvPool(c5, p5)
+    za, zb = f5.forward_steps(xd[:, :, :7].contiguous()), f5.forward_steps(xd[:, :, 7:].contiguous())
+    assert torch.equal(torch.cat([z_ for z_ in (za, zb) if z_ is not None], dim=2), zc)
     # fused steps continuing separate ones, and the other way round
     c4, p4 = pair()
     f4 = coinf.ConvPool(c4, p4)
