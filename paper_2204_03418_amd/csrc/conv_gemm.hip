@@ -869,6 +869,303 @@ __global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_ke
   }
 }
 
+// The same persistent frame loop with the weight fragments read from global
+// memory (L2) straight into registers instead of through LDS.  Measured on
+// MI355X, streaming the 0.5 MB of weights a workgroup uses per frame through
+// LDS made LDS bandwidth the limit: every weight byte was written once and
+// read twice there, on top of the pixel fragments.  Read from memory, the two
+// waves that share a weight fragment meet in L1, LDS carries only the staged
+// input rows, and the workgroup meets at one barrier per 32-channel chunk
+// instead of one per kernel row.  Each lane keeps a ring of kStepsBRing
+// weight fragment sets, requested kStepsBDist k-steps ahead of use (across
+// chunk and frame boundaries: every frame reads the same weights).
+//
+// Arithmetic is the step kernel's: 16x16x32 bf16 MFMAs in the same k order
+// (32-channel chunks outer, spatial taps inner), accumulators seeded with the
+// partial sums, so a clip gives the bits of stepping frame by frame.  The
+// partial sums stay in the accumulators across frames: after the completing
+// tap's output goes out, tap j's accumulators become tap j + 1's.
+constexpr int kStepsBRing = 3;  // weight fragment sets in flight per lane
+constexpr int kStepsBDist = 2;  // k-steps between a weight request and its use
+
+template <int KH, int KW, bool PAIR>
+__global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_wreg_kernel(
+    ConvGeom g, GemmSteps gs, const bf16_t* __restrict__ x, int64_t x_bc,
+    bf16_t* __restrict__ y, const uint4* __restrict__ wp, const float* __restrict__ bias,
+    float* __restrict__ ring) {
+  using T = bf16_t;
+  using Frag = v8bf;
+  using Pair = typename Stage<T>::Pair;
+  constexpr int WM = kStepsWM, NWM = kStepsNWM, NWN = kStepsNWN, KTM = kStepsKT;
+  constexpr int KL = 8, CK = 32;
+  constexpr int KHW = KH * KW;  // k-steps per chunk
+  constexpr int NT = 64 * NWM * NWN;
+  constexpr int M_WG = 16 * WM * NWM;
+  constexpr int O_WG = 16 * NWN;
+  constexpr int N_WG = KTM * O_WG;
+  constexpr int AI = (kStepsStageItems + NT - 1) / NT;
+  constexpr int NB = kStepsBRing, DB = kStepsBDist;
+  static_assert(KHW % NB == 0 && DB < NB, "weight ring: a chunk's k-steps fill whole rounds");
+  static_assert(AI * KL <= KHW, "input loads: at most one per k-step");
+  extern __shared__ uint4 smem[];
+
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % NWM, wn = wave / NWM;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int bid = int(blockIdx.x);
+  const int L = (bid & 7) * gs.tiles_per_xcd + (bid >> 3);
+  if (L >= gs.m_tiles * gs.o_tiles) return;
+  const int m_tile = fdiv(L, gs.fd_ot);
+  const int o_tile = L - m_tile * gs.o_tiles;
+  const int m0 = m_tile * M_WG;
+  const int m1 = min(m0 + M_WG, gs.M);
+  const int kT = g.kT;
+
+  // input rows of the tile: flattened (stream, row) index q in [q0, q1]
+  const int r0 = fdiv(m0, gs.fd_Wo), r1 = fdiv(m1 - 1, gs.fd_Wo);
+  const int b0 = fdiv(r0, gs.fd_Ho), i0 = r0 - b0 * g.Ho;
+  const int b1 = fdiv(r1, gs.fd_Ho), i1 = r1 - b1 * g.Ho;
+  const int q0 = b0 * g.H + max(0, i0 - g.pH);
+  const int q1 = b1 * g.H + min(g.H - 1, i1 + KH - 1 - g.pH);
+  const int nslots = q1 - q0 + 1;
+  const int zero_slot = gs.max_slots;
+
+  // LDS: [A stage 0][A stage 1], laid out as in the step kernel
+  const int a_pixels = (gs.max_slots + 2) * gs.cols;
+  const int a_units = gs.a_units;
+  uint4* const As0 = smem;
+  for (int u = tid; u < 2 * a_units; u += NT) smem[u] = make_uint4(0u, 0u, 0u, 0u);
+
+  int pixbase[WM][KH];
+#pragma unroll
+  for (int mf = 0; mf < WM; ++mf) {
+    const int P = m0 + (wm * WM + mf) * 16 + lrow;
+    const bool valid = P < gs.M;
+    const int Pc = valid ? P : 0;
+    const int b = fdiv(Pc, gs.fd_So), p = Pc - b * gs.So;
+    const int i = fdiv(p, gs.fd_Wo), j = p - i * g.Wo;
+#pragma unroll
+    for (int u = 0; u < KH; ++u) {
+      const int ih = i + u - g.pH;
+      const int slot = (valid && ih >= 0 && ih < g.H) ? b * g.H + ih - q0 : zero_slot;
+      pixbase[mf][u] = slot * gs.cols + j;
+    }
+  }
+
+  constexpr int PW = PAIR ? 2 : 1;
+  const int wp_items = g.W / PW;
+  const int a_items = nslots * 4 * wp_items;
+  int a_src[AI], a_dst[AI], a_dst1[AI], a_grp[AI];
+#pragma unroll
+  for (int ai = 0; ai < AI; ++ai) {
+    const int it = tid + ai * NT;
+    a_src[ai] = 0;
+    a_grp[ai] = 0;
+    a_dst[ai] = a_pixels * kPixUnits;
+    a_dst1[ai] = (a_pixels + 1) * kPixUnits;
+    if (it < a_items) {
+      const int rest = fdiv(it, gs.fd_wpi);
+      const int xp = it - rest * wp_items;
+      const int grp = rest & 3;
+      const int sl = rest >> 2;
+      const int q = q0 + sl;
+      const int b = fdiv(q, gs.fd_H), ih = q - b * g.H;
+      const int xcol = xp * PW;
+      a_src[ai] = int(((int64_t(b) * g.Cin + grp * KL) * x_bc + int64_t(ih) * g.W + xcol) *
+                      int64_t(sizeof(T)));
+      a_grp[ai] = grp;
+      const int pix = sl * gs.cols + xcol + g.pW;
+      a_dst[ai] = pix * kPixUnits + grp;
+      a_dst1[ai] = (pix + 1) * kPixUnits + grp;
+    }
+  }
+
+  Pair ra[AI][KL];
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, gs.x_bytes);
+  const int plane_bytes = int(x_bc * int64_t(sizeof(T)));
+  // input load e of chunk ch of frame t (one per k-step, so they trickle out
+  // between the matrix instructions).  Branch-free: end-padding frames and
+  // frames past the call read the out-of-range offset, i.e. zeros.
+  auto prefetch_one = [&](int t, int ch, int e) {
+    const int cbase = ch * CK;
+    const bool live = t < gs.T;  // uniform
+#pragma unroll
+    for (int ai = 0; ai < AI; ++ai)
+#pragma unroll
+      for (int ee = 0; ee < KL; ++ee) {
+        if (ai * KL + ee != e) continue;
+        const bool cin = live && cbase + a_grp[ai] * KL + ee < g.Cin;
+        ra[ai][ee] = Stage<T>::load(xr, cin ? a_src[ai] : kOutOfRange,
+                                    live ? (cbase + ee) * plane_bytes + t * gs.fstride : 0, PAIR);
+      }
+  };
+  auto store_a = [&](int buf, int ch) {
+    uint4* As = As0 + buf * a_units;
+    const bool ragged = ch * CK + CK > g.Cin;
+#pragma unroll
+    for (int ai = 0; ai < AI; ++ai) {
+      if (ragged) {
+        const int c0 = ch * CK + a_grp[ai] * KL;
+#pragma unroll
+        for (int e = 0; e < KL; ++e)
+          if (c0 + e >= g.Cin) ra[ai][e] = Pair{};
+      }
+      uint4 p0, p1;
+      Stage<T>::pack(ra[ai], p0, p1);
+      As[a_dst[ai]] = p0;
+      if (PAIR) As[a_dst1[ai]] = p1;
+    }
+  };
+
+  // weights of this workgroup's channel tile: k-step ks = ch * KHW + uv is a
+  // block of N_WG columns x 4 units; lane (lrow, lgrp) reads its column's unit
+  // of logical channel group lgrp (the packing swizzles units within a column)
+  const int steps_per_frame = gs.n_chunks * KHW;
+  const int wblk_bytes = N_WG * 64;
+  const __amdgpu_buffer_rsrc_t wr =
+      make_rsrc(wp + int64_t(o_tile) * steps_per_frame * N_WG * 4, steps_per_frame * wblk_bytes);
+  int boff[KTM];
+#pragma unroll
+  for (int j = 0; j < KTM; ++j) {
+    const int cc = j * O_WG + wn * 16 + lrow;
+    boff[j] = (cc * 4 + bswz(cc, lgrp)) * 16;
+  }
+  Frag bq[NB][KTM];
+  auto load_b = [&](int ks, int slot) {
+    const int so = ks * wblk_bytes;
+#pragma unroll
+    for (int j = 0; j < KTM; ++j)
+      bq[slot][j] = __builtin_bit_cast(Frag, __builtin_amdgcn_raw_buffer_load_b128(wr, boff[j], so, 0));
+  };
+
+  // this lane's output channel and the first of its four pixels per fragment
+  const int o = o_tile * O_WG + wn * 16 + lrow;
+  const bool ocol = o < g.Cout;
+  const float bo = ocol ? bias[o] : 0.f;
+  auto pix0 = [&](int mf) { return m0 + (wm * WM + mf) * 16 + lgrp * 4; };
+  const int R = g.R;
+
+  // c[mf][j]: the running sum of output v - j (v = virtual time of the frame
+  // being processed).  On entry, taps j >= 1 continue the ring's partial sums
+  // unless the stream is at its first frame (then every output starts there).
+  v4f c[WM][KTM];
+#pragma unroll
+  for (int j = 0; j < KTM; ++j)
+#pragma unroll
+    for (int mf = 0; mf < WM; ++mf) {
+      c[mf][j] = v4f{0.f, 0.f, 0.f, 0.f};
+      const int tau = gs.v0 - j;
+      if (j >= 1 && j < kT && tau >= 0 && gs.v0 > g.pT) {
+        const int sl = (gs.slot_v0 - j + R) % R;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (ocol && pix0(mf) + r < gs.M)
+            c[mf][j][r] = ring[int64_t(sl) * gs.ring_slot + int64_t(o) * gs.M + pix0(mf) + r];
+      }
+    }
+
+  __syncthreads();  // zero fill done
+#pragma unroll
+  for (int d = 0; d < DB; ++d) load_b(d % steps_per_frame, d);
+#pragma unroll
+  for (int e = 0; e < AI * KL; ++e) prefetch_one(0, 0, e);
+  store_a(0, 0);
+  __syncthreads();
+
+  int gch = 0;  // chunks done
+  for (int t = 0; t < gs.count; ++t) {
+    const int v = gs.v0 + t;
+#pragma unroll 1
+    for (int ch = 0; ch < gs.n_chunks; ++ch, ++gch) {
+      const uint4* As = As0 + (gch & 1) * a_units;
+      const bool lastc = ch + 1 == gs.n_chunks;
+      const int nch = lastc ? 0 : ch + 1;
+      const int ntf = lastc ? t + 1 : t;
+      const int ks0 = ch * KHW;
+      Frag af[2][WM];
+      auto load_a = [&](int uv, int k) {
+        const int u = uv / KW, vv = uv % KW;
+#pragma unroll
+        for (int mf = 0; mf < WM; ++mf)
+          af[k][mf] = __builtin_bit_cast(Frag, As[(pixbase[mf][u] + vv) * kPixUnits + lgrp]);
+      };
+      load_a(0, 0);
+#pragma unroll
+      for (int uv = 0; uv < KHW; ++uv) {
+        // weights DB k-steps ahead (wrapping into the next frame's first
+        // chunk), the next chunk's input share, then the next tap's pixels
+        int ks = ks0 + uv + DB;
+        if (ks >= steps_per_frame) ks -= steps_per_frame;
+        load_b(ks, (uv + DB) % NB);
+        if (uv < AI * KL) prefetch_one(ntf, nch, uv);
+        if (uv + 1 < KHW) load_a(uv + 1, (uv + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < KTM; ++j)
+#pragma unroll
+          for (int mf = 0; mf < WM; ++mf) mma(c[mf][j], af[uv & 1][mf], bq[uv % NB][j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // unconditional, also after the call's last chunk (into a buffer no
+      // one reads again): a store under a branch lets the compiler sink the
+      // input loads from their k-steps into that branch, right before it,
+      // which exposes a full memory round trip per chunk
+      store_a((gch + 1) & 1, nch);
+      __syncthreads();
+    }
+    // the output tap kT - 1 completes goes out with the bias
+    const int ko = gs.k0 + t;
+#pragma unroll
+    for (int j = 0; j < KTM; ++j) {
+      if (j != kT - 1 || v - j < 0) continue;  // uniform
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf) {
+        const int p0 = pix0(mf);
+        if (!ocol || p0 >= gs.M) continue;
+        const v4f a = c[mf][j];
+        if (gs.yvec) {  // the four pixels lie in one stream's frame
+          const int b = fdiv(p0, gs.fd_So), p = p0 - b * gs.So;
+          bf16_t* yp = y + (int64_t(b) * g.Cout + o) * gs.y_bc + int64_t(ko) * gs.So + p;
+          store4<T>(yp, a[0] + bo, a[1] + bo, a[2] + bo, a[3] + bo, true);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int P = p0 + r;
+            if (P >= gs.M) continue;
+            const int b = fdiv(P, gs.fd_So), p = P - b * gs.So;
+            store_out<T>(y, (int64_t(b) * g.Cout + o) * gs.y_bc + int64_t(ko) * gs.So + p,
+                         a[r] + bo);
+          }
+        }
+      }
+    }
+    // tap j's running sums carry on as tap j + 1's; tap 0 starts afresh
+#pragma unroll
+    for (int j = KTM - 1; j >= 1; --j)
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf) c[mf][j] = c[mf][j - 1];
+#pragma unroll
+    for (int mf = 0; mf < WM; ++mf) c[mf][0] = v4f{0.f, 0.f, 0.f, 0.f};
+  }
+
+  if (gs.update) {
+    const int v1 = gs.v0 + gs.count;
+    const int s1 = (gs.slot_v0 + gs.count) % R;
+#pragma unroll
+    for (int j = 1; j < KTM; ++j) {
+      if (j >= kT || v1 - j < 0) continue;  // uniform
+      const int sl = (s1 - j + R) % R;
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (ocol && pix0(mf) + r < gs.M)
+            ring[int64_t(sl) * gs.ring_slot + int64_t(o) * gs.M + pix0(mf) + r] = c[mf][j][r];
+    }
+  }
+}
+
 // Pack W (C_out, C_in, kT, kH, kW) into [o_tile][chunk][u][v][column][4 units]
 // (column = t * O_WG + o_local), zero padded, with the units swizzled as the
 // persistent kernel reads them.
@@ -910,7 +1207,15 @@ hipError_t gemm_steps_launch(const ConvGeom& g, const GemmStepsConfig& c, const 
                              char* state, const void* x, int64_t x_bc, int32_t nreal,
                              int32_t count, void* y, int64_t y_bc, int64_t n0, bool update,
                              hipStream_t s) {
-  auto kern = conv_steps_gemm_kernel<KH, KW, PAIR>;
+  // the register-weight kernel wherever a chunk's k-steps fill whole rounds
+  // of its weight ring (3x3 kernels), else weights through LDS
+  constexpr bool wreg = (KH * KW) % kStepsBRing == 0;
+  auto kern = [] {
+    if constexpr (wreg)
+      return conv_steps_gemm_wreg_kernel<KH, KW, PAIR>;
+    else
+      return conv_steps_gemm_kernel<KH, KW, PAIR>;
+  }();
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -947,8 +1252,10 @@ hipError_t gemm_steps_launch(const ConvGeom& g, const GemmStepsConfig& c, const 
   gs.fd_H = make_fastdiv(uint32_t(g.H));
   gs.fd_ot = make_fastdiv(uint32_t(c.o_tiles));
   gs.fd_wpi = make_fastdiv(uint32_t(PAIR ? g.W / 2 : g.W));
+  // the register-weight kernel keeps only the two input stages in LDS
+  const size_t lds = wreg ? size_t(2 * c.a_units * 16) : size_t(c.lds_bytes);
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * gs.tiles_per_xcd)),
-                     dim3(64 * kStepsNWM * kStepsNWN), size_t(c.lds_bytes), s, g, gs,
+                     dim3(64 * kStepsNWM * kStepsNWN), lds, s, g, gs,
                      static_cast<const bf16_t*>(x), x_bc, static_cast<bf16_t*>(y),
                      reinterpret_cast<const uint4*>(state + L.steps_weight),
                      reinterpret_cast<const float*>(state + L.bias),
