@@ -24,7 +24,7 @@ constexpr int kDwTaps = 4;  // active taps handled per pass (ring reads in fligh
 // Active taps of one step, compacted: tap index, action, ring slot.
 struct ActiveTaps {
   int32_t n;
-  FastDiv fd_So, fd_Cout, fd_Wo;  // dividers: pixels per frame, C_out, Wo
+  FastDiv fd_So, fd_B, fd_Wo;  // dividers: pixels per frame, streams, Wo
   int32_t tap[CO_MAX_TAPS];
   int32_t act[CO_MAX_TAPS];
   int32_t slot[CO_MAX_TAPS];
@@ -39,13 +39,16 @@ __global__ __launch_bounds__(kBlock) void conv_step_dw_kernel(
   const int32_t total = g.B * g.Cout * So;
   const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
   if (idx >= total) return;
-  const int32_t bc = fdiv(idx, at.fd_So);
-  const int32_t p = idx - bc * So;
-  const int32_t bq = fdiv(bc, at.fd_Cout);
-  const int32_t c = bc - bq * g.Cout;
+  // threads in ring order (c, b, pixel): the ring is most of a step's bytes,
+  // so its reads and writes are the ones kept contiguous across a wave
+  const int32_t cb = fdiv(idx, at.fd_So);
+  const int32_t p = idx - cb * So;
+  const int32_t c = fdiv(cb, at.fd_B);
+  const int32_t bq = cb - c * g.B;
+  const int32_t bc = bq * g.Cout + c;
   const int32_t i = fdiv(p, at.fd_Wo), jo = p - i * g.Wo;
   const int64_t yi = int64_t(bc) * y_bc + p;
-  const int32_t ridx = (c * g.B + bq) * So + p;  // ring (slot, C, B, Ho, Wo)
+  const int32_t ridx = idx;  // ring (slot, C, B, Ho, Wo)
 
   // stencil of the arriving frame: buffer loads whose out-of-frame taps
   // read zero from an out-of-range offset, so all loads issue together
@@ -108,7 +111,7 @@ hipError_t dw_launch(const ConvGeom& g, const ConvLayout& L, char* state, const 
   }
   if (at.n == 0) return hipSuccess;
   at.fd_So = make_fastdiv(uint32_t(g.So()));
-  at.fd_Cout = make_fastdiv(uint32_t(g.Cout));
+  at.fd_B = make_fastdiv(uint32_t(g.B));
   at.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   hipLaunchKernelGGL((conv_step_dw_kernel<T, KH, KW>), dim3(grid_for(g.out_frame_elems())),
                      dim3(kBlock), 0, s, g, static_cast<const T*>(io.x), io.x_bc,
