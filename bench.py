@@ -103,6 +103,10 @@ def measured_traffic(workload):
     return None
 
 
+def kT_of(c):
+    return (tuple(c.kernel) + (1, 1))[0]
+
+
 def per_step_work(c, Ho, Wo):
     """Algorithmic FLOPs and bytes of one conv step (eager partial sums, stride 1):
     FLOPs = 2 B Ho Wo C_out kT (C_in/G) kH kW;
@@ -229,6 +233,7 @@ def main():
                  "flops_per_launch": flops, "bytes_per_launch": nbytes})
 
     modes = {"eager_forward_step": round(value, 1)}
+    modes_roof = {}
     if not args.no_modes:
         # (ii) the same steps replayed from a HIP graph: one schedule period
         # (ring slots x stride) per capture, so replays keep the state coherent
@@ -274,6 +279,22 @@ def main():
         s1.record(stream)
         torch.cuda.synchronize()
         modes["forward_steps"] = round(c.batch * calls * T / (s0.elapsed_time(s1) / 1e3), 1)
+        # the same roofline terms for forward_steps: per frame the persistent
+        # launch does the step's FLOPs but moves only the frame and its output
+        # (the partial sums stay on chip), so it is priced on compute
+        us_frame = s0.elapsed_time(s1) * 1e3 / (calls * T)
+        io_bytes = nbytes - 2 * (kT_of(c) - 1) * c.batch * c.out_channels * Ho * Wo * 4
+        tf = flops / (us_frame * 1e-6) / 1e12
+        gbs = io_bytes / (us_frame * 1e-6) / 1e9
+        fs = {"persistent": bool(co.steps_fused(T)), "us_per_frame": round(us_frame, 3),
+              "flops_per_frame": flops, "io_bytes_per_frame": io_bytes}
+        if flops / io_bytes >= ridge:
+            fs.update({"bound": bound_compute, "achieved": round(tf, 3), "peak": peak_c,
+                       "unit": "TFLOP/s", "frac": round(tf / peak_c, 5)})
+        else:
+            fs.update({"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
+                       "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 5)})
+        modes_roof["forward_steps"] = fs
 
         # (iv) a depthwise convolution feeding a global pool: the fused step
         # (one launch per step, the same results as the two-launch chain)
@@ -330,6 +351,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "modes": modes,
+        "modes_roofline": modes_roof,
     }
     print(json.dumps(out))
 

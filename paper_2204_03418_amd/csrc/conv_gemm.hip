@@ -887,16 +887,22 @@ __global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_ke
 // tap's output goes out, tap j's accumulators become tap j + 1's.
 constexpr int kStepsBRing = 3;  // weight fragment sets in flight per lane
 constexpr int kStepsBDist = 2;  // k-steps between a weight request and its use
+// Wave layout of this kernel (the workgroup tile is the config's M_WG x O_WG)
+constexpr int kWregWM = kStepsWM, kWregNWM = kStepsNWM, kWregNWN = kStepsNWN;
+static_assert(16 * kWregWM * kWregNWM == 16 * kStepsWM * kStepsNWM &&
+                  kWregNWN == kStepsNWN,
+              "the register-weight kernel covers the config's workgroup tile");
+constexpr int kWregThreads = 64 * kWregNWM * kWregNWN;
 
 template <int KH, int KW, bool PAIR>
-__global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_wreg_kernel(
+__global__ __launch_bounds__(kWregThreads) void conv_steps_gemm_wreg_kernel(
     ConvGeom g, GemmSteps gs, const bf16_t* __restrict__ x, int64_t x_bc,
     bf16_t* __restrict__ y, const uint4* __restrict__ wp, const float* __restrict__ bias,
     float* __restrict__ ring) {
   using T = bf16_t;
   using Frag = v8bf;
   using Pair = typename Stage<T>::Pair;
-  constexpr int WM = kStepsWM, NWM = kStepsNWM, NWN = kStepsNWN, KTM = kStepsKT;
+  constexpr int WM = kWregWM, NWM = kWregNWM, NWN = kWregNWN, KTM = kStepsKT;
   constexpr int KL = 8, CK = 32;
   constexpr int KHW = KH * KW;  // k-steps per chunk
   constexpr int NT = 64 * NWM * NWN;
@@ -906,7 +912,8 @@ __global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_wr
   constexpr int AI = (kStepsStageItems + NT - 1) / NT;
   constexpr int NB = kStepsBRing, DB = kStepsBDist;
   static_assert(KHW % NB == 0 && DB < NB, "weight ring: a chunk's k-steps fill whole rounds");
-  static_assert(AI * KL <= KHW, "input loads: at most one per k-step");
+  constexpr int LPS = (AI * KL + KHW - 1) / KHW;  // input loads per k-step
+  static_assert(LPS * KHW >= AI * KL, "input loads spread over the chunk's k-steps");
   extern __shared__ uint4 smem[];
 
   const int tid = int(threadIdx.x);
@@ -1098,7 +1105,9 @@ __global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_wr
         int ks = ks0 + uv + DB;
         if (ks >= steps_per_frame) ks -= steps_per_frame;
         load_b(ks, (uv + DB) % NB);
-        if (uv < AI * KL) prefetch_one(ntf, nch, uv);
+#pragma unroll
+        for (int e = uv * LPS; e < uv * LPS + LPS; ++e)
+          if (e < AI * KL) prefetch_one(ntf, nch, e);
         if (uv + 1 < KHW) load_a(uv + 1, (uv + 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -1255,7 +1264,7 @@ hipError_t gemm_steps_launch(const ConvGeom& g, const GemmStepsConfig& c, const 
   // the register-weight kernel keeps only the two input stages in LDS
   const size_t lds = wreg ? size_t(2 * c.a_units * 16) : size_t(c.lds_bytes);
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * gs.tiles_per_xcd)),
-                     dim3(64 * kStepsNWM * kStepsNWN), lds, s, g, gs,
+                     dim3(wreg ? kWregThreads : 64 * kStepsNWM * kStepsNWN), lds, s, g, gs,
                      static_cast<const bf16_t*>(x), x_bc, static_cast<bf16_t*>(y),
                      reinterpret_cast<const uint4*>(state + L.steps_weight),
                      reinterpret_cast<const float*>(state + L.bias),
