@@ -245,10 +245,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
     a_dst[ai] = a_pixels * kPixUnits;
     a_dst1[ai] = (a_pixels + 1) * kPixUnits;
     if (it < a_items) {
+      // items run along a row, then down the tile's rows, then over the
+      // four channel groups: the lanes of one load instruction read
+      // consecutive rows of the same channel plane (a few whole cache lines)
       const int rest = fdiv(it, ga.fd_wpi);
       const int xp = it - rest * wp_items;
-      const int grp = rest & 3;
-      const int sl = rest >> 2;
+      const int grp = rest / nslots;
+      const int sl = rest - grp * nslots;
       const int q = q0 + sl;
       const int b = fdiv(q, ga.fd_H), ih = q - b * g.H;
       const int xcol = xp * PW;
@@ -627,10 +630,13 @@ __global__ __launch_bounds__(64 * kStepsNWM * kStepsNWN) void conv_steps_gemm_ke
     a_dst[ai] = a_pixels * kPixUnits;
     a_dst1[ai] = (a_pixels + 1) * kPixUnits;
     if (it < a_items) {
+      // items run along a row, then down the tile's rows, then over the
+      // four channel groups: the lanes of one load instruction read
+      // consecutive rows of the same channel plane (a few whole cache lines)
       const int rest = fdiv(it, gs.fd_wpi);
       const int xp = it - rest * wp_items;
-      const int grp = rest & 3;
-      const int sl = rest >> 2;
+      const int grp = rest / nslots;
+      const int sl = rest - grp * nslots;
       const int q = q0 + sl;
       const int b = fdiv(q, gs.fd_H), ih = q - b * g.H;
       const int xcol = xp * PW;
@@ -917,7 +923,9 @@ __global__ __launch_bounds__(kWregThreads) void conv_steps_gemm_wreg_kernel(
   extern __shared__ uint4 smem[];
 
   const int tid = int(threadIdx.x);
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  // wave index as a scalar: everything derived from it stays wave-uniform
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % NWM, wn = wave / NWM;
   const int lrow = lane & 15, lgrp = lane >> 4;
   const int bid = int(blockIdx.x);
@@ -972,10 +980,13 @@ __global__ __launch_bounds__(kWregThreads) void conv_steps_gemm_wreg_kernel(
     a_dst[ai] = a_pixels * kPixUnits;
     a_dst1[ai] = (a_pixels + 1) * kPixUnits;
     if (it < a_items) {
+      // items run along a row, then down the tile's rows, then over the
+      // four channel groups: the lanes of one load instruction read
+      // consecutive rows of the same channel plane (a few whole cache lines)
       const int rest = fdiv(it, gs.fd_wpi);
       const int xp = it - rest * wp_items;
-      const int grp = rest & 3;
-      const int sl = rest >> 2;
+      const int grp = rest / nslots;
+      const int sl = rest - grp * nslots;
       const int q = q0 + sl;
       const int b = fdiv(q, gs.fd_H), ih = q - b * g.H;
       const int xcol = xp * PW;
