@@ -246,3 +246,29 @@ def test_fused_depthwise_pool_workload():
         oracle.ContinualConv(np64(w), np64(b), padding=c.padding, groups=c.groups),
         oracle.ContinualPool("avg", pl.kernel, stride=pl.stride))
     assert_close(np64(z[sel]), ch.forward_steps(np64(x[sel])), torch.bfloat16, "workload")
+
+
+def test_expanded_temporal_average_pool():
+    """Temporal global average pooling expanded to 64 steps (the section on
+    performance comparisons: the receptive field of a continual 3D-CNN grows by
+    pooling 64 frames over time and the whole frame in space): against the
+    oracle, with delay 63, and stepping bitwise equal to forward_steps."""
+    B, C, T, H, W = 4, 48, 80, 7, 7
+    say("expanded pool")
+    x = synth.normal((B, C, T, H, W), 8800, dtype="bf16")
+    xd = x.to(DEV)
+
+    def make():
+        return coinf.CoPool("avg", batch=B, channels=C, kernel=(64, H, W), in_size=(H, W),
+                            stride=(1, H, W), dtype=torch.bfloat16)
+
+    po = make()
+    assert po.delay == 63
+    ys = po.forward_steps(xd)
+    assert ys.shape == (B, C, T - 63, 1, 1)
+    ref = oracle.ContinualPool("avg", (64, H, W), stride=(1, H, W)).forward_steps(np64(x))
+    assert_close(np64(ys), ref, torch.bfloat16, "expanded pool")
+    po2 = make()
+    outs = [po2.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    assert all(o is None for o in outs[:63])
+    assert torch.equal(torch.stack(outs[63:], dim=2), ys)
