@@ -442,7 +442,10 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
 // through memory.  Weights stay in registers too.  Per frame and tap the
 // products are summed over the k-steps in the order of the step kernel of
 // the same instantiation (split halves added first half + second), then
-// added to the partial sum, so forward_steps reproduces forward_step.
+// added to the partial sum, so forward_steps reproduces forward_step.  A
+// split instantiation (KSPLIT = 2) runs its two halves on two waves, which
+// meet in LDS once per frame: twice the waves, half the serial matrix work
+// per wave.
 struct RegSteps {
   int32_t M, So, m_frags, o_frags, blocks_per_xcd;
   int32_t ntaps, CS, CSU;
@@ -456,7 +459,7 @@ struct RegSteps {
   FastDiv fd_So, fd_Wo, fd_ofr;
 };
 
-template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM>
+template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL>
 __global__ __launch_bounds__(64 * kRegWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
                            T* __restrict__ y, const uint4* __restrict__ wp,
@@ -474,29 +477,47 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   const int lrow = lane & 15, lgrp = lane >> 4;
   const int bid = int(blockIdx.x);
   const int lb = (bid & 7) * rs.blocks_per_xcd + (bid >> 3);
-  const int tile = lb * kRegWaves + wave;
-  if (tile >= rs.m_frags * rs.o_frags) return;  // whole waves; no barrier follows
+  // With KSPLIT = 2 the two chains of a tile run on two waves (h = 0 takes
+  // spatial taps 0 .. TH - 1, h = 1 the rest); h = 1 hands its products to
+  // h = 0 through LDS every frame, and h = 0 adds them exactly as a single
+  // wave adds its two chains.  Waves past the last tile keep to the per-frame
+  // barrier: they redo tile 0 with every store masked.
+  constexpr int TPW = kRegWaves / KSPLIT;  // tiles per workgroup
+  const int h = wave % KSPLIT, wslot = wave / KSPLIT;
+  const int tile_raw = lb * TPW + wslot;
+  const bool live = tile_raw < rs.m_frags * rs.o_frags;
+  if constexpr (KSPLIT == 1) {
+    if (!live) return;  // whole waves; no barrier follows
+  }
+  const int tile = live ? tile_raw : 0;
+  const bool owner = live & (h == 0);  // the wave that keeps the sums and stores
   const int mf = fdiv(tile, rs.fd_ofr);
   const int of = tile - mf * rs.o_frags;
-  const int kT = g.kT;
+  // FULL: the layer uses every temporal tap of the instantiation (kT == KTM),
+  // so the per-tap tests below are compile-time and the frame loop is
+  // straight-line matrix work with no branch between the instructions
+  const int kT = FULL ? KTM : g.kT;
 
-  // ---- weights, once: column (tap j, channel o) of the step kernel's packing
+  // ---- weights of this wave's spatial taps, once: column (tap j, channel o)
+  // of the step kernel's packing
   const int o = of * 16 + lrow;
   const bool ocol = o < g.Cout;
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(wp, rs.w_bytes);
-  uint4 wreg[KTM][TAPS][CSUMAX];
+  const int tp0 = h * TH;  // first spatial tap of this wave's chain
+  uint4 wreg[KTM][TH][CSUMAX];
 #pragma unroll
   for (int j = 0; j < KTM; ++j) {
     const int n = j * g.Cout + o;
     const int nf = n >> 4, r = n & 15;
 #pragma unroll
-    for (int tp = 0; tp < TAPS; ++tp)
+    for (int i2 = 0; i2 < TH; ++i2)
 #pragma unroll
       for (int cq = 0; cq < CSUMAX; ++cq) {
+        const int tp = tp0 + i2;
         const bool ok = ocol & (j < kT) & (tp < rs.ntaps) & (cq < rs.CSU);
         const int off = (((nf * rs.ntaps + tp) * rs.CSU + cq) << 10) + (lgrp * 16 + r) * 16;
         const auto w4 = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? off : kOutOfRange, 0, 0);
-        wreg[j][tp][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        wreg[j][i2][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
   }
   const __amdgpu_buffer_rsrc_t br = make_rsrc(bias, g.Cout * 4);
@@ -511,7 +532,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int P = P0 + r;
-    const bool ok = ocol & (P < rs.M);
+    const bool ok = ocol & (P < rs.M) & owner;
     const int b = fdiv(ok ? P : 0, rs.fd_So), p = (ok ? P : 0) - b * rs.So;
     yoff[r] = ok ? int((uint32_t(b * g.Cout + o) * uint32_t(rs.y_bc) + uint32_t(p)) * esz)
                  : kOutOfRange;
@@ -549,39 +570,40 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   const uint32_t lane_b = (uint32_t(b) * uint32_t(g.Cin) + uint32_t(lane_c)) * plane_b;
   const int nv_last = min(max(g.Cin - ((rs.CS - 1) * CKS + lane_c), 0), CL);
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, rs.x_bytes);
-  int vt[TAPS];
+  int vt[TH];
 #pragma unroll
-  for (int tp = 0; tp < TAPS; ++tp) {
+  for (int i2 = 0; i2 < TH; ++i2) {
+    const int tp = tp0 + i2;
     const int hi = hb + rs.dh[tp], wi = wb + rs.dw[tp];
     const bool ok = (tp < rs.ntaps) & pvalid & (unsigned(hi) < unsigned(g.H)) &
                     (unsigned(wi) < unsigned(g.W));
-    vt[tp] = ok ? int(lane_b + (uint32_t(hi) * uint32_t(g.W) + uint32_t(wi)) * esz) : kOutOfRange;
+    vt[i2] = ok ? int(lane_b + (uint32_t(hi) * uint32_t(g.W) + uint32_t(wi)) * esz) : kOutOfRange;
   }
   // Raw loaded bits (eight bf16 channels or one fp32 per lane and k-step),
   // packed into operands only when the frame is multiplied: packing right
   // after the loads would make the wave wait for them there.
-  auto load_frame = [&](int t, uint32_t (&a)[TAPS][CSMAX][CL]) {
+  auto load_frame = [&](int t, uint32_t (&a)[TH][CSMAX][CL]) {
     if (t < rs.T) {  // uniform; end-padding frames are zero
       const int fo = t * rs.fstride;
 #pragma unroll
-      for (int tp = 0; tp < TAPS; ++tp)
+      for (int i2 = 0; i2 < TH; ++i2)
 #pragma unroll
         for (int cb = 0; cb < CSMAX; ++cb) {
-          const bool live = cb < rs.CS, last = cb == rs.CS - 1;  // uniform
+          const bool lv = cb < rs.CS, last = cb == rs.CS - 1;  // uniform
           const int sb = int(uint32_t(cb * CKS) * plane_b) + fo;
 #pragma unroll
           for (int e = 0; e < CL; ++e) {
-            const int v = (live & (!last | (e < nv_last))) ? vt[tp] : kOutOfRange;
-            a[tp][cb][e] = load_raw_at<T>(xr, v, sb + int(uint32_t(e) * plane_b));
+            const int v = (lv & (!last | (e < nv_last))) ? vt[i2] : kOutOfRange;
+            a[i2][cb][e] = load_raw_at<T>(xr, v, sb + int(uint32_t(e) * plane_b));
           }
         }
     } else {
 #pragma unroll
-      for (int tp = 0; tp < TAPS; ++tp)
+      for (int i2 = 0; i2 < TH; ++i2)
 #pragma unroll
         for (int cb = 0; cb < CSMAX; ++cb)
 #pragma unroll
-          for (int e = 0; e < CL; ++e) a[tp][cb][e] = 0u;
+          for (int e = 0; e < CL; ++e) a[i2][cb][e] = 0u;
     }
   };
   auto operand = [&](const uint32_t (&r)[CL]) -> AReg {
@@ -592,7 +614,9 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       return __uint_as_float(r[0]);
   };
 
-  uint32_t araw[PF][TAPS][CSMAX][CL];
+  uint32_t araw[PF][TH][CSMAX][CL];
+  // products handed from chain 1 to chain 0: [tile][frame parity][tap j][lane]
+  __shared__ v4f red[KSPLIT == 2 ? TPW : 1][2][KSPLIT == 2 ? KTM : 1][64];
 #pragma unroll
   for (int u = 0; u < PF; ++u) load_frame(u, araw[u]);
 
@@ -602,62 +626,74 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       const int t = t0 + u;
       if (t >= rs.count) break;
       const int v = rs.v0 + t;
-      // products of every temporal tap, each as KSPLIT chains over k-steps
-      v4f c[KTM][KSPLIT];
+      // products of every temporal tap over this wave's chain of k-steps
+      v4f c[KTM];
 #pragma unroll
-      for (int j = 0; j < KTM; ++j)
-#pragma unroll
-        for (int h = 0; h < KSPLIT; ++h) c[j][h] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < KTM; ++j) c[j] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int i2 = 0; i2 < TH; ++i2)
 #pragma unroll
         for (int cb = 0; cb < CSMAX; ++cb)
 #pragma unroll
-          for (int h = 0; h < KSPLIT; ++h)
-#pragma unroll
-            for (int j = 0; j < KTM; ++j) {
-              if (j >= kT) continue;  // uniform
-              const int tp = h * TH + i2;
-              const AReg av = operand(araw[u][tp][cb]);
-              if constexpr (kBF) {
-                c[j][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(v8bf, av),
-                    __builtin_bit_cast(v8bf, wreg[j][tp][cb]), c[j][h], 0, 0, 0);
-              } else {
-                const uint4 u4 = wreg[j][tp][cb / 4];
-                const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
-                c[j][h] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, __uint_as_float(bw),
-                                                               c[j][h], 0, 0, 0);
-              }
+          for (int j = 0; j < KTM; ++j) {
+            if (!FULL && j >= kT) continue;  // uniform
+            const AReg av = operand(araw[u][i2][cb]);
+            if constexpr (kBF) {
+              c[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(v8bf, av), __builtin_bit_cast(v8bf, wreg[j][i2][cb]), c[j],
+                  0, 0, 0);
+            } else {
+              const uint4 u4 = wreg[j][i2][cb / 4];
+              const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
+              c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, __uint_as_float(bw), c[j], 0, 0, 0);
             }
+          }
       // the next frames' operands are requested before this frame's epilogue
       load_frame(t + PF, araw[u]);
+      v4f c1[KTM];  // chain 1's products (KSPLIT = 2), as chain 0 adds them
+      if constexpr (KSPLIT == 2) {
+        if (h == 1) {
+#pragma unroll
+          for (int j = 0; j < KTM; ++j) red[wslot][t & 1][j][lane] = c[j];
+        }
+        __syncthreads();  // (a slot is rewritten two frames later, after another barrier)
+        // Both waves run the fold below: the helper's stores carry the
+        // out-of-range offset and are dropped.  A branch around it would
+        // give the two paths different counts of outstanding memory
+        // operations, and the compiler would then wait for all of them
+        // (the frames in flight included) before each frame's products.
+#pragma unroll
+        for (int j = 0; j < KTM; ++j) c1[j] = red[wslot][t & 1][j][lane];
+      }
       // fold each product into its output: tap j completes v - (kT - 1),
       // starts at the first tap on a real frame, continues otherwise
       v4f nxt[KTM];
 #pragma unroll
       for (int j = 0; j < KTM; ++j) {
         nxt[j] = v4f{0.f, 0.f, 0.f, 0.f};
-        if (j >= kT) continue;
+        if (!FULL && j >= kT) continue;
+        // output v - j exists once tau >= 0 (a uniform select, no branch:
+        // the stores of a missing output carry the out-of-range offset)
         const int tau = v - j;
-        if (tau < 0) continue;  // no such output (uniform)
+        const bool exists = tau >= 0;
         const int first = tau >= g.pT ? 0 : g.pT - tau;
-        v4f sum = c[j][0];
-        if constexpr (KSPLIT == 2) sum = sum + c[j][1];
+        v4f sum = c[j];
+        if constexpr (KSPLIT == 2) sum = sum + c1[j];
         const v4f a = (j == first) ? sum : sum + part[j];
         if (j == kT - 1) {
-          const int fo = (rs.k0 + t) * rs.So * int(esz);
+          const int fo = exists ? (rs.k0 + t) * rs.So * int(esz) : 0;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const float val = a[r] + bo;
+            const int yo = exists ? yoff[r] : kOutOfRange;
             if constexpr (kBF)
               __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)),
-                                                    yr, yoff[r], fo, 0);
+                                                    yr, yo, fo, 0);
             else
-              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, yoff[r], fo, 0);
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, yo, fo, 0);
           }
         } else {
-          nxt[j] = a;
+          nxt[j] = exists ? a : v4f{0.f, 0.f, 0.f, 0.f};
         }
       }
       // output v - j continues as v + 1 - (j + 1)
@@ -666,7 +702,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
     }
   }
 
-  if (rs.update) {
+  if (rs.update && h == 0) {
     const int v1 = rs.v0 + rs.count;
     const int s1 = (rs.slot_v0 + rs.count) % R;
 #pragma unroll
@@ -714,7 +750,7 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.So = int32_t(g.So());
   rs.m_frags = c.m_frags;
   rs.o_frags = int32_t(ceil_div(g.Cout, 16));
-  const int64_t blocks = ceil_div(int64_t(rs.m_frags) * rs.o_frags, kRegWaves);
+  const int64_t blocks = ceil_div(int64_t(rs.m_frags) * rs.o_frags, kRegWaves / KSPLIT);
   rs.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
   rs.ntaps = g.kH * g.kW;
   rs.CS = c.CS;
@@ -742,9 +778,10 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.fd_So = make_fastdiv(uint32_t(rs.So));
   rs.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   rs.fd_ofr = make_fastdiv(uint32_t(rs.o_frags));
-  hipLaunchKernelGGL((conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM>),
-                     dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g, rs,
-                     static_cast<const T*>(x), x_bc, static_cast<T*>(y),
+  auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true>
+                          : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g,
+                     rs, static_cast<const T*>(x), x_bc, static_cast<T*>(y),
                      reinterpret_cast<const uint4*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
                      reinterpret_cast<float*>(state + L.ring));
