@@ -241,13 +241,16 @@ __global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
       for (int j = KT - 1; j >= 0; --j) {
         const int q = KT - 1 - j;
         const int tau = v - j;
-        if (tau < 0) continue;  // no such output (uniform)
+        // output v - j exists once tau >= 0; no branch around the arithmetic
+        // (the sums of a missing output are never stored or written back)
+        const bool exists = tau >= 0;
         const int first = tau >= g.pT ? 0 : g.pT - tau;  // first tap on a real frame
         float a = (j == first) ? 0.f : acc[q];  // a start overwrites the slot
 #pragma unroll
         for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], raw_to_f32<T>(xq[u][e]), a);
         if (j == KT - 1)
-          store_at(yr, yoff, (ds.k0 + t) * So * int32_t(esz), from_f32<T>(a + bo));
+          store_at(yr, exists ? yoff : kOutOfRange,
+                   exists ? (ds.k0 + t) * So * int32_t(esz) : 0, from_f32<T>(a + bo));
         else
           acc[q] = a;
       }
@@ -398,13 +401,13 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
       for (int j = KT - 1; j >= 0; --j) {
         const int q = KT - 1 - j;
         const int tau = v - j;
-        if (tau < 0) continue;
+        const bool exists = tau >= 0;  // as above: only the store is guarded
         const int first = tau >= g.pT ? 0 : g.pT - tau;
         float a = (j == first) ? 0.f : acc[q];
 #pragma unroll
         for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
         if (j == KT - 1) {
-          if (pl) yb[int64_t(ds.k0 + t) * So] = from_f32<T>(a + bo);
+          if (pl && exists) yb[int64_t(ds.k0 + t) * So] = from_f32<T>(a + bo);
         } else {
           acc[q] = a;
         }
