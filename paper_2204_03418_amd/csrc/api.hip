@@ -40,10 +40,6 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
 // The persistent direct kernel indexes y with 64-bit offsets; its element
 // index per (stream, channel) plane stays 32-bit.
-bool y_steps_fit(const ConvGeom& g, int64_t y_frames) {
-  return int64_t(g.B) * g.Cout * y_frames * g.So() < (int64_t(1) << 31);
-}
-
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_EHIP; }
 
 bool any_tap(const co_step_plan& p) {
@@ -179,7 +175,7 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
   hipStream_t s = as_stream(stream);
   const int64_t n0 = h->n;
   const bool dw = dw_steps_supported(g, T, y_cap_frames);
-  const bool dir = direct_steps_supported(g, T) && y_steps_fit(g, y_cap_frames);
+  const bool dir = direct_steps_supported(g, T, y_cap_frames);
   const bool gem = gemm_steps_supported(g, T, y_cap_frames, x);
   if (count > 0 && (dw || dir || gem || reg_steps_supported(g, T, y_cap_frames))) {
     // one persistent launch: partial sums stay on chip across frames; with
@@ -238,7 +234,7 @@ co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_
   // allocation from the caching allocator always is)
   static const uint32_t aligned_probe = 0;
   *fused = dw_steps_supported(g, T, y_cap_frames) ||
-                   (direct_steps_supported(g, T) && y_steps_fit(g, y_cap_frames)) ||
+                   direct_steps_supported(g, T, y_cap_frames) ||
                    gemm_steps_supported(g, T, y_cap_frames, &aligned_probe) ||
                    reg_steps_supported(g, T, y_cap_frames)
                ? 1

@@ -160,7 +160,7 @@ struct DirSteps {
   int32_t v0;       // virtual time of the first frame, capped at 2^29
   int32_t slot_v0;  // v0 mod R (uncapped)
   int32_t count, T, k0, update;
-  int32_t x_bytes;
+  int32_t x_bytes, y_bytes;
   int32_t fstride;  // bytes between consecutive frames of the clip
   FastDiv fd_So, fd_Cout, fd_Wo;
 };
@@ -168,12 +168,15 @@ struct DirSteps {
 constexpr int kDirStepsKX = 16;  // reduction positions C_in/G * kH * kW held in registers
 constexpr int kDirStepsKT = 4;   // temporal taps held in registers
 
-template <typename T>
+// KX: reduction positions held (4, 8 or 16); PF: frames in flight (16, 8 or
+// 4, so a thread holds 64 raw inputs either way).  The loop is bound by the
+// latency of its frame loads, so a small layer keeps more frames in flight.
+template <typename T, int KX, int PF>
 __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
     ConvGeom g, DirSteps ds, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
     int64_t y_bc, const float* __restrict__ w, const float* __restrict__ bias,
     float* __restrict__ ring, int64_t ring_slot) {
-  constexpr int KX = kDirStepsKX, KTM = kDirStepsKT, PF = 4;
+  constexpr int KTM = kDirStepsKT;
   constexpr uint32_t esz = sizeof(T);
   const int32_t So = g.Ho * g.Wo;
   const int32_t total = g.B * g.Cout * So;
@@ -232,7 +235,8 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
   uint32_t xq[PF][KX];  // raw bits, converted when the frame is evaluated
 #pragma unroll
   for (int u = 0; u < PF; ++u) load_frame(u, xq[u]);
-  T* yb = y + int64_t(bo) * y_bc + p;
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ds.y_bytes);
+  const int yoff = int((uint32_t(bo) * uint32_t(y_bc) + uint32_t(p)) * esz);
   for (int t0 = 0; t0 < ds.count; t0 += PF) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
@@ -247,19 +251,24 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
 #pragma unroll
         for (int j = 0; j < KTM; ++j) cj[j] = fmaf(wr[e][j], raw_to_f32<T>(xq[u][e]), cj[j]);
       load_frame(t + PF, xq[u]);
+      // fold each tap's product into its output without a branch: a missing
+      // output (tau < 0) or an unused tap only selects zero, and the one
+      // store is always issued, to the out-of-range offset unless tap kT - 1
+      // completes an existing output (a store under a branch would make the
+      // compiler wait for every frame in flight before each frame)
       float nxt[KTM];
+      float yv = 0.f;
 #pragma unroll
       for (int j = 0; j < KTM; ++j) {
-        nxt[j] = 0.f;
         const int tau = v - j;
-        if (j >= kT || tau < 0) continue;  // uniform
         const int first = tau >= g.pT ? 0 : g.pT - tau;
         const float a = (j == first) ? cj[j] : part[j] + cj[j];
-        if (j == kT - 1)
-          yb[int64_t(ds.k0 + t) * So] = from_f32<T>(a + bo_);
-        else
-          nxt[j] = a;
+        yv = j == kT - 1 ? a : yv;
+        nxt[j] = (j < kT - 1 && tau >= 0) ? a : 0.f;
       }
+      const bool emits = v - (kT - 1) >= 0;  // uniform
+      store_at(yr, emits ? yoff : kOutOfRange, emits ? (ds.k0 + t) * So * int32_t(esz) : 0,
+               from_f32<T>(yv + bo_));
 #pragma unroll
       for (int j = KTM - 1; j >= 1; --j) part[j] = nxt[j - 1];
     }
@@ -289,11 +298,16 @@ hipError_t direct_steps_t(const ConvGeom& g, const ConvLayout& L, char* state, c
   ds.update = update ? 1 : 0;
   const int64_t esz = sizeof(T);
   ds.x_bytes = int32_t(((int64_t(g.B) * g.Cin - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  ds.y_bytes = int32_t(int64_t(g.B) * g.Cout * y_bc * esz);
   ds.fstride = int32_t(g.S() * esz);
   ds.fd_So = make_fastdiv(uint32_t(g.So()));
   ds.fd_Cout = make_fastdiv(uint32_t(g.Cout));
   ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
-  hipLaunchKernelGGL(conv_steps_direct_kernel<T>, dim3(grid_for(g.out_frame_elems())),
+  const int64_t nk = int64_t(g.Cg) * g.kH * g.kW;
+  auto kern = nk <= 4   ? conv_steps_direct_kernel<T, 4, 16>
+              : nk <= 8 ? conv_steps_direct_kernel<T, 8, 8>
+                        : conv_steps_direct_kernel<T, kDirStepsKX, 4>;
+  hipLaunchKernelGGL(kern, dim3(grid_for(g.out_frame_elems())),
                      dim3(kBlock), 0, s, g, ds, static_cast<const T*>(x), x_bc,
                      static_cast<T*>(y), y_bc, reinterpret_cast<const float*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
@@ -310,11 +324,12 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
   return step_direct_t<float>(g, L, state, io, plan, zero_frame, s);
 }
 
-bool direct_steps_supported(const ConvGeom& g, int64_t x_frames) {
+bool direct_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   return g.algo == CO_ALGO_DIRECT && g.sT == 1 && g.dT == 1 && g.kT <= kDirStepsKT &&
          int64_t(g.Cg) * g.kH * g.kW <= kDirStepsKX &&
-         int64_t(g.B) * g.Cin * x_frames * g.S() * esz < (int64_t(1) << 31);
+         int64_t(g.B) * g.Cin * x_frames * g.S() * esz < (int64_t(1) << 31) &&
+         int64_t(g.B) * g.Cout * y_frames * g.So() * esz < (int64_t(1) << 31);
 }
 
 hipError_t launch_conv_steps_direct(const ConvGeom& g, const ConvLayout& L, char* state,

@@ -62,7 +62,7 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
 // Persistent forward_steps of small direct layers (same conventions as the
 // depthwise one): temporal stride 1 and dilation 1, kT <= 4 and
 // C_in/G * kH * kW <= 16.
-bool direct_steps_supported(const ConvGeom& g, int64_t x_frames);
+bool direct_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames);
 hipError_t launch_conv_steps_direct(const ConvGeom& g, const ConvLayout& L, char* state,
                                     const void* x, int64_t x_bc, int32_t T, int32_t count,
                                     void* y, int64_t y_bc, int64_t n0, bool update,
