@@ -382,7 +382,7 @@ co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
 co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused) {
   if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
-  *fused = pool_steps_supported(h->g, T) ? 1 : 0;
+  *fused = pool_steps_supported(h->g, T, y_cap_frames) ? 1 : 0;
   return CO_OK;
 }
 
@@ -398,7 +398,7 @@ co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, voi
   if (n_emit > 0 && !y) return CO_EINVAL;
   hipStream_t s = as_stream(stream);
   const int64_t n0 = h->n;
-  if (count > 0 && pool_steps_supported(g, T)) {
+  if (count > 0 && pool_steps_supported(g, T, y_cap_frames)) {
     // one persistent launch: the FIFO stays in registers across frames; with
     // update_state = 0 the state is simply not written back
     const co_status st = hip_status(launch_pool_steps(

@@ -43,7 +43,7 @@ hipError_t launch_pool_init(const PoolGeom& g, const PoolLayout& L, char* state,
 // Persistent forward_steps of a pool (same conventions as the depthwise one):
 // temporal stride 1 and dilation 1, kT <= 5, a spatial window of at most 64,
 // clips below 2^31 bytes.
-bool pool_steps_supported(const PoolGeom& g, int64_t x_frames);
+bool pool_steps_supported(const PoolGeom& g, int64_t x_frames, int64_t y_frames);
 // Validity flags of the FIFO slots that pool steps n0 .. n0 + count - 1 wrote
 // (the first T real frames, the rest end padding).
 hipError_t launch_pool_valid(float* valid, int32_t R, int64_t n0, int32_t count, int32_t T,

@@ -188,6 +188,7 @@ struct PoolSteps {
   int64_t emit0;  // first emitting step of the call: max(n0, d)
   int32_t update;
   int32_t x_bytes;  // bytes of the clip reachable from x
+  int32_t y_bytes;  // bytes of the output clip
   int32_t fstride;  // bytes between consecutive frames
   FastDiv fd_So, fd_Wo, fd_kW;
 };
@@ -239,7 +240,12 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
     fv[q] = have ? fifo[(rf % KT) * fifo_slot + idx] : neutral;
     fok[q] = have ? valid[rf % KT] : 0.f;
   }
-  T* yb = y + int64_t(bc) * y_bc + p;
+  // the emitted value goes out through a buffer store that every lane issues
+  // every frame, to the out-of-range offset unless lane 0 of a group emits:
+  // a store under a branch would make the compiler wait for every frame in
+  // flight before each frame
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ps.y_bytes);
+  const int yoff = int((uint32_t(bc) * uint32_t(y_bc) + uint32_t(p)) * sizeof(T));
   // raw bits of this lane's window element of frame t (converted when the
   // frame is reduced, so the loads stay in flight); positions outside the
   // frame read the out-of-range offset and become the neutral value at use
@@ -253,8 +259,9 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
     return (t < ps.T && soff >= 0) ? raw_to_f32<T>(raw) : neutral;
   };
   // frame t's window element sits in xq[t % PF]; the next PF - 1 frames'
-  // are in flight while frame t is reduced
-  constexpr int PF = 4;
+  // are in flight while frame t is reduced (one register per frame, so the
+  // loop keeps many: it is bound by the latency of these loads)
+  constexpr int PF = 16;
   uint32_t xq[PF];
 #pragma unroll
   for (int u = 0; u < PF; ++u) xq[u] = load(u);
@@ -269,7 +276,7 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
       fv[KT - 1] = val;
       fok[KT - 1] = t < ps.T ? 1.f : 0.f;
       const int64_t n = ps.n0 + t;
-      if (n >= g.d) {
+      {
         // the window's frames as the per-step kernel combines them (tap q in
         // lane q of a lane group, then an xor-shuffle tree), so both paths
         // give the same bits; start padding contributes nothing
@@ -295,16 +302,16 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
           }
         }
         const float acc = tv[0], tcount = tc[0];
-        if (r == 0) {
-          float out;
-          if (is_max) {
-            out = acc;
-          } else {
-            const float div = g.count_include_pad ? float(KT * kHW) : tcount * float(vh * vw);
-            out = div > 0.f ? acc / div : 0.f;
-          }
-          yb[(n - ps.emit0) * So] = from_f32<T>(out);
+        float out;
+        if (is_max) {
+          out = acc;
+        } else {
+          const float div = g.count_include_pad ? float(KT * kHW) : tcount * float(vh * vw);
+          out = div > 0.f ? acc / div : 0.f;
         }
+        const bool emits = n >= g.d;  // uniform
+        store_at(yr, (emits && r == 0) ? yoff : kOutOfRange,
+                 emits ? int((n - ps.emit0) * So * int64_t(sizeof(T))) : 0, from_f32<T>(out));
       }
 #pragma unroll
       for (int q = 0; q + 1 < KT; ++q) {
@@ -404,6 +411,7 @@ hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state
   ps.update = update ? 1 : 0;
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   ps.x_bytes = int32_t(((int64_t(g.B) * g.C - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  ps.y_bytes = int32_t(int64_t(g.B) * g.C * y_bc * esz);
   ps.fstride = int32_t(g.S() * esz);
   ps.fd_So = make_fastdiv(uint32_t(g.So()));
   ps.fd_Wo = make_fastdiv(uint32_t(g.Wo));
@@ -451,10 +459,11 @@ hipError_t launch_pool_valid(float* valid, int32_t R, int64_t n0, int32_t count,
   return hipGetLastError();
 }
 
-bool pool_steps_supported(const PoolGeom& g, int64_t x_frames) {
+bool pool_steps_supported(const PoolGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   return g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64 &&  // (kT <= 8: tree)
-         int64_t(g.B) * g.C * x_frames * g.S() * esz < (int64_t(1) << 31);
+         int64_t(g.B) * g.C * x_frames * g.S() * esz < (int64_t(1) << 31) &&
+         int64_t(g.B) * g.C * y_frames * g.So() * esz < (int64_t(1) << 31);
 }
 
 hipError_t launch_pool_steps(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
