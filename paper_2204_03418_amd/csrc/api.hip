@@ -418,21 +418,40 @@ co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, voi
   }
   const int64_t S = g.S(), So = g.So();
   const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
-  int64_t k = 0;
+  // The pool step addresses a frame with 32-bit buffer offsets over
+  // everything reachable from the frame pointer.  A clip whose planes lie
+  // 2^31 bytes or more apart is stepped through a contiguous copy of each
+  // frame (B*C rows of S elements).
+  const bool staged =
+      T > 0 && ((int64_t(g.B) * g.C - 1) * T * S + S) * int64_t(esz) >= (int64_t(1) << 31);
+  void* frame = nullptr;
   co_status st = CO_OK;
-  for (int64_t t = 0; t < count; ++t) {
+  if (staged && hipMallocAsync(&frame, size_t(g.B) * g.C * S * esz, s) != hipSuccess)
+    st = CO_EHIP;
+  int64_t k = 0;
+  for (int64_t t = 0; t < count && st == CO_OK; ++t) {
     co_pool_plan plan;
     pool_plan(g, h->n, &plan);
     const bool pad = t >= T;
-    const StepIO io{pad ? nullptr : static_cast<const char*>(x) + size_t(t * S) * esz,
-                    int64_t(T) * S,
-                    plan.emit ? static_cast<char*>(y) + size_t(k * So) * esz : nullptr,
+    const char* xt = pad ? nullptr : static_cast<const char*>(x) + size_t(t * S) * esz;
+    int64_t x_bc = int64_t(T) * S;
+    if (staged && !pad) {
+      if (hipMemcpy2DAsync(frame, size_t(S) * esz, xt, size_t(T) * S * esz, size_t(S) * esz,
+                           size_t(g.B) * g.C, hipMemcpyDeviceToDevice, s) != hipSuccess) {
+        st = CO_EHIP;
+        break;
+      }
+      xt = static_cast<const char*>(frame);
+      x_bc = S;
+    }
+    const StepIO io{xt, x_bc, plan.emit ? static_cast<char*>(y) + size_t(k * So) * esz : nullptr,
                     int64_t(y_cap_frames) * So};
     st = hip_status(launch_pool_step(g, h->L, h->state, io, plan, true, pad, s));
     if (st != CO_OK) break;
     if (plan.emit) ++k;
     ++h->n;
   }
+  if (frame && hipFreeAsync(frame, s) != hipSuccess && st == CO_OK) st = CO_EHIP;
   if (!update_state) {
     const co_status r = restore_range(h->state + h->L.valid, s, &bk);
     if (st == CO_OK) st = r;

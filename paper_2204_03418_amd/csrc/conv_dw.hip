@@ -505,6 +505,13 @@ hipError_t dw_steps_dispatch(const ConvGeom& g, const ConvLayout& L, char* state
 
 hipError_t launch_conv_step_depthwise(const ConvGeom& g, const ConvLayout& L, char* state,
                                       const StepIO& io, const co_step_plan& plan, hipStream_t s) {
+  // The stencil loads use 32-bit buffer offsets over everything reachable
+  // from the frame pointer; a frame of a clip whose planes lie further apart
+  // (forward_steps over a clip of 2^31 bytes or more) takes the direct
+  // kernel, which shares the ring layout and the weight packing.
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  if (((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz >= (int64_t(1) << 31))
+    return launch_conv_step_direct(g, L, state, io, plan, false, s);
   if (g.dtype == CO_BF16) return dw_dispatch<bf16_t>(g, L, state, io, plan, s);
   return dw_dispatch<float>(g, L, state, io, plan, s);
 }

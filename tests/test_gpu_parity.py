@@ -748,3 +748,40 @@ def test_pool_forward_steps_persistent(case):
     assert po3.steps == n and torch.equal(po3.state, before)
     real = po3.forward_steps(xd[:, :, 1:9].contiguous(), pad_end=True)
     assert torch.equal(peek, real)
+
+
+@pytest.mark.parametrize("what", ["depthwise", "avgpool"])
+def test_forward_steps_clip_beyond_32bit_offsets(what):
+    """forward_steps over a clip of more than 2^31 bytes: the persistent kernels
+    decline it and the per-frame loop must still address every plane (the
+    depthwise step hands such frames to the 64-bit direct kernel, the pool loop
+    steps a contiguous copy of each frame).  The clip repeats a 7-frame seeded
+    block, so the oracle recomputes sampled output frames from 3-frame windows."""
+    B, C, H, W, T, P = 2, 32, 64, 64, 2100, 7
+    assert (B * C - 1) * T * H * W * 4 + H * W * 4 >= 2 ** 31
+    say("large clip", what, (B, C, T, H, W))
+    base = synth.normal((B, C, P, H, W), 9100)
+    if what == "depthwise":
+        w = synth.normal((C, 1, 3, 3, 3), 9101, std=0.2)
+        b = synth.normal((C,), 9102)
+        mod = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=(H, W), padding=(0, 1, 1),
+                           groups=C)
+        assert mod.algo == "depthwise"
+    else:
+        mod = coinf.CoPool("avg", batch=B, channels=C, kernel=(3, 3, 3), in_size=(H, W),
+                          stride=1)
+    assert mod.delay == 2 and not mod.steps_fused(T)
+    x = base.to(DEV).repeat(1, 1, T // P, 1, 1)
+    y = mod.forward_steps(x)
+    torch.cuda.synchronize()
+    del x
+    assert y.shape[2] == T - 2
+    for k in (0, 1, 5, 1234, T - 3):
+        win = np64(base[:, :, [(k + j) % P for j in range(3)]])
+        if what == "depthwise":
+            ref = oracle.conv_window(win, np.ones(3, np.uint8), np64(w), np64(b), C, 1, (1, 1),
+                                     (1, 1), (1, 1, 1))
+        else:
+            ref = oracle.pool_window("avg", win, np.ones(3, np.uint8), (3, 3, 3), (1, 1, 1),
+                                     (0, 0), (1, 1, 1), True)
+        assert_close(np64(y[:, :, k:k + 1]), ref, torch.float32, f"{what} frame {k}")
