@@ -324,6 +324,41 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
   return step_direct_t<float>(g, L, state, io, plan, zero_frame, s);
 }
 
+hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char* state,
+                                   const StepIO& io, const co_step_plan& plan, hipStream_t s) {
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  const int64_t S = g.S(), So = g.So(), lim = int64_t(1) << 31;
+  const int64_t xrows = int64_t(g.B) * g.Cin, yrows = int64_t(g.B) * g.Cout;
+  const bool y_far = io.y && ((yrows - 1) * io.y_bc + So) * esz >= lim;
+  // An input frame that is already contiguous and 16-byte aligned, with an
+  // output in 32-bit reach, is what the copies below would produce: the
+  // kernel has declined the geometry itself, and staging cannot help.
+  const bool x_plain = io.x_bc == S && reinterpret_cast<uintptr_t>(io.x) % 16 == 0;
+  if (!io.x || (x_plain && !y_far) || xrows * S * esz >= lim || yrows * So * esz >= lim)
+    return hipErrorInvalidValue;
+  void* xs = nullptr;
+  void* ys = nullptr;
+  hipError_t e = hipMallocAsync(&xs, size_t(xrows * S * esz), s);
+  if (e == hipSuccess && y_far) e = hipMallocAsync(&ys, size_t(yrows * So * esz), s);
+  if (e == hipSuccess)
+    e = hipMemcpy2DAsync(xs, size_t(S * esz), io.x, size_t(io.x_bc * esz), size_t(S * esz),
+                         size_t(xrows), hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess) {
+    const StepIO sio{static_cast<const char*>(xs), S, y_far ? static_cast<char*>(ys) : io.y,
+                     y_far || !io.y ? So : io.y_bc};
+    e = launch_conv_step(g, L, state, sio, plan, false, s);
+  }
+  if (e == hipSuccess && y_far)
+    e = hipMemcpy2DAsync(io.y, size_t(io.y_bc * esz), ys, size_t(So * esz), size_t(So * esz),
+                         size_t(yrows), hipMemcpyDeviceToDevice, s);
+  for (void* p : {xs, ys}) {
+    if (!p) continue;
+    const hipError_t f = hipFreeAsync(p, s);
+    if (e == hipSuccess) e = f;
+  }
+  return e;
+}
+
 bool direct_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   return g.algo == CO_ALGO_DIRECT && g.sT == 1 && g.dT == 1 && g.kT <= kDirStepsKT &&

@@ -1370,12 +1370,12 @@ hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* s
   // Even-width rows are staged two pixels per load; a frame pointer or plane
   // stride that breaks that alignment takes the direct kernel (same ring).
   const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
-  if (g.W % 2 == 0 &&
-      ((reinterpret_cast<uintptr_t>(io.x) % (2 * esz)) != 0 || (io.x_bc % 2) != 0))
-    return launch_conv_step_direct(g, L, state, io, plan, false, s);
-  // staging reads use 32-bit buffer offsets over the reachable part of x
-  if (((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * int64_t(esz) >= (int64_t(1) << 31))
-    return launch_conv_step_direct(g, L, state, io, plan, false, s);
+  // even rows are staged as aligned pixel pairs, and the staging reads use
+  // 32-bit buffer offsets over the reachable part of x
+  if ((g.W % 2 == 0 &&
+       ((reinterpret_cast<uintptr_t>(io.x) % (2 * esz)) != 0 || (io.x_bc % 2) != 0)) ||
+      ((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * int64_t(esz) >= (int64_t(1) << 31))
+    return launch_conv_step_staged(g, L, state, io, plan, s);
   if (g.kH == 3 && g.kW == 3) return gemm_dispatch_taps<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return gemm_dispatch_taps<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;

@@ -454,7 +454,7 @@ hipError_t img_launch(const ConvGeom& g, const ImgConfig& c, const ConvLayout& L
   ia.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   ia.fd_slabs = make_fastdiv(uint32_t(ia.slab_cnt));
   ia.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
-  ia.y_bytes = int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * 2);
+  ia.y_bytes = io.y ? int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * 2) : 0;
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * ia.blocks_per_xcd)), dim3(kImgThreads),
                      size_t(c.lds_bytes), s, g, ia, static_cast<const bf16_t*>(io.x), io.x_bc,
                      static_cast<bf16_t*>(io.y), io.y_bc,
@@ -490,9 +490,9 @@ hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* st
   const bool pair_ok = !c.pair || ((reinterpret_cast<uintptr_t>(io.x) & 3) == 0 &&
                                    (io.x_bc & 1) == 0);
   const int64_t y_extent = ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * 2;
-  if (x_extent >= (int64_t(1) << 31) || y_extent >= (int64_t(1) << 31) || !pair_ok ||
-      int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31))
-    return launch_conv_step_direct(g, L, state, io, plan, false, s);
+  if (int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+  if (x_extent >= (int64_t(1) << 31) || (io.y && y_extent >= (int64_t(1) << 31)) || !pair_ok)
+    return launch_conv_step_staged(g, L, state, io, plan, s);
   if (g.kH == 3 && g.kW == 3) return img_dispatch<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return img_dispatch<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;

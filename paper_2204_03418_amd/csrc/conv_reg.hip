@@ -411,7 +411,7 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   ra.w_bytes = int32_t(L.weight_bytes);
   ra.ring_slot = int32_t(L.ring_slot_elems);
   ra.y_bc = int32_t(io.y_bc);
-  ra.y_bytes = int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz);
+  ra.y_bytes = io.y ? int32_t(((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz) : 0;
   ra.ring_bytes = int32_t(int64_t(g.R) * L.ring_slot_elems * 4);
   ra.fd_So = make_fastdiv(uint32_t(ra.So));
   ra.fd_Wo = make_fastdiv(uint32_t(g.Wo));
@@ -794,13 +794,16 @@ hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* st
                                 const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   RegConfig c;
   if (!reg_config(g, g.cfg, &c)) return hipErrorInvalidValue;
-  // 32-bit buffer offsets: input extent and packed weights below 2^31 bytes
+  // 32-bit buffer offsets: the packed weights, the tile count and the ring
+  // are held in reach when the algorithm is chosen; the reach of a frame
+  // depends on its plane and output strides
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  if (L.weight_bytes >= (int64_t(1) << 30) || int64_t(c.m_frags) * c.n_frags >= (int64_t(1) << 30) ||
+      int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31))
+    return hipErrorInvalidValue;
   if (((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz >= (int64_t(1) << 31) ||
-      L.weight_bytes >= (int64_t(1) << 30) || int64_t(c.m_frags) * c.n_frags >= (int64_t(1) << 30) ||
-      int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31) ||
-      ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31))
-    return launch_conv_step_direct(g, L, state, io, plan, false, s);
+      (io.y && ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31)))
+    return launch_conv_step_staged(g, L, state, io, plan, s);
   switch (c.id) {
     case 0: return reg_launch<float, 4, 1, 16, 1>(g, c, L, state, io, plan, s);
     case 1: return reg_launch<float, 2, 1, 32, 1>(g, c, L, state, io, plan, s);

@@ -59,6 +59,13 @@ hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const v
 hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char* state,
                                    const StepIO& io, const co_step_plan& plan, bool zero_frame,
                                    hipStream_t stream);
+// One step of a GEMM-family layer whose frame the kernel cannot address in
+// place (an input plane stride or an output stride that takes the reach past
+// 2^31 bytes, or a misaligned input): the frame is copied into a contiguous
+// stream-ordered buffer, stepped, and an output staged the same way is
+// copied back.  Fails when the frame is already contiguous and aligned.
+hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char* state,
+                                   const StepIO& io, const co_step_plan& plan, hipStream_t stream);
 // Persistent forward_steps of small direct layers (same conventions as the
 // depthwise one): temporal stride 1 and dilation 1, kT <= 4 and
 // C_in/G * kH * kW <= 16.

@@ -67,10 +67,23 @@ int64_t tile_slots(const ConvGeom& g, int64_t m0, int64_t m1) {
 
 }  // namespace
 
+int64_t ring_slot_elems(const ConvGeom& g) {
+  // four floats past the frame keep a 16-byte read of the last four pixels
+  // of a ragged frame inside the slot
+  return round_up(g.out_frame_elems() + 4, kAlign / 4);
+}
+
+bool frame_offsets_fit(const ConvGeom& g) {
+  const int64_t lim = int64_t(1) << 31;
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  return int64_t(g.B) * g.Cin * g.S() * esz < lim && g.out_frame_elems() * esz < lim &&
+         int64_t(g.R) * ring_slot_elems(g) * 4 < lim;
+}
+
 bool gemm_geometry_ok(const ConvGeom& g) {
   const bool taps = (g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1);
   return g.G == 1 && taps && g.sH == 1 && g.sW == 1 && g.dH == 1 && g.dW == 1 &&
-         g.W + 2 * g.pW <= 256;
+         g.W + 2 * g.pW <= 256 && frame_offsets_fit(g);
 }
 
 bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
@@ -198,7 +211,8 @@ constexpr RegShape kRegShapes[kRegConfigs] = {
 
 bool reg_config(const ConvGeom& g, int id, RegConfig* c) {
   // C_out >= 16 keeps every 16-column fragment within two temporal taps
-  if (id < 0 || id >= kRegConfigs || g.G != 1 || g.Cout < 16) return false;
+  if (id < 0 || id >= kRegConfigs || g.G != 1 || g.Cout < 16 || !frame_offsets_fit(g))
+    return false;
   const RegShape& s = kRegShapes[id];
   if (s.dtype != g.dtype) return false;
   RegConfig r{};
@@ -217,6 +231,10 @@ bool reg_config(const ConvGeom& g, int id, RegConfig* c) {
   r.U = taps * r.CSU;
   r.m_frags = int32_t(ceil_div(int64_t(g.B) * g.So(), 16));
   r.n_frags = int32_t(ceil_div(int64_t(g.kT) * g.Cout, 16));
+  // packed weights and the tile count are addressed with 32-bit offsets
+  if (int64_t(r.n_frags) * r.U * 64 * 16 >= (int64_t(1) << 30) ||
+      int64_t(r.m_frags) * r.n_frags >= (int64_t(1) << 30))
+    return false;
   *c = r;
   return true;
 }
@@ -268,7 +286,7 @@ bool reg_supported(const ConvGeom& g) { return reg_pick(g) >= 0; }
 bool img_config(const ConvGeom& g, ImgConfig* c) {
   const bool taps = (g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1);
   if (g.dtype != CO_BF16 || g.G != 1 || !taps || g.sH != 1 || g.sW != 1 || g.dH != 1 ||
-      g.dW != 1 || g.Cin % 8 != 0)
+      g.dW != 1 || g.Cin % 8 != 0 || !frame_offsets_fit(g))
     return false;
   ImgConfig r{};
   const int64_t mf = ceil_div(g.So(), 16);
@@ -436,9 +454,7 @@ ConvLayout conv_layout(const ConvGeom& g) {
   GemmStepsConfig sc;
   L.steps_weight_bytes = gemm_steps_config(g, &sc) ? sc.weight_bytes : 0;
   L.ring = L.steps_weight + round_up(L.steps_weight_bytes, kAlign);
-  // four floats past the frame keep a 16-byte read of the last four pixels
-  // of a ragged frame inside the slot
-  L.ring_slot_elems = round_up(g.out_frame_elems() + 4, kAlign / 4);
+  L.ring_slot_elems = ring_slot_elems(g);
   L.total = L.ring + int64_t(g.R) * L.ring_slot_elems * 4;
   return L;
 }

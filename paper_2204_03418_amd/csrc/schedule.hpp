@@ -212,6 +212,13 @@ struct StateHeader {
   int32_t slots;
 };
 
+// Floats in one ring slot: the output frame, padded.
+int64_t ring_slot_elems(const ConvGeom& g);
+// Whether one input frame, one output frame (in the io dtype) and the whole
+// fp32 ring each stay below 2^31 bytes: the GEMM-family kernels address them
+// through 32-bit buffer offsets.
+bool frame_offsets_fit(const ConvGeom& g);
+
 // Validate a convolution descriptor, resolve the algorithm and fill g.
 co_status conv_geom(const co_conv_desc* desc, ConvGeom* g);
 ConvLayout conv_layout(const ConvGeom& g);

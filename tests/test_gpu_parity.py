@@ -750,38 +750,81 @@ def test_pool_forward_steps_persistent(case):
     assert torch.equal(peek, real)
 
 
-@pytest.mark.parametrize("what", ["depthwise", "avgpool"])
-def test_forward_steps_clip_beyond_32bit_offsets(what):
+# what, B, C, (H, W), dtype, frames: (B*C - 1) planes of T*H*W elements reach past 2^31 bytes
+LARGE_CLIP_CASES = [
+    ("depthwise", 2, 32, (64, 64), "f32", 2100),
+    ("avgpool", 2, 32, (64, 64), "f32", 2100),
+    ("gemm", 2, 32, (64, 64), "f32", 2100),
+    ("gemm_reg", 2, 24, (64, 64), "f32", 2800),
+    ("gemm_img", 8, 32, (14, 14), "bf16", 21504),
+]
+
+
+@pytest.mark.parametrize("case", LARGE_CLIP_CASES, ids=lambda c: c[0])
+def test_forward_steps_clip_beyond_32bit_offsets(case):
     """forward_steps over a clip of more than 2^31 bytes: the persistent kernels
     decline it and the per-frame loop must still address every plane (the
-    depthwise step hands such frames to the 64-bit direct kernel, the pool loop
-    steps a contiguous copy of each frame).  The clip repeats a 7-frame seeded
-    block, so the oracle recomputes sampled output frames from 3-frame windows."""
-    B, C, H, W, T, P = 2, 32, 64, 64, 2100, 7
-    assert (B * C - 1) * T * H * W * 4 + H * W * 4 >= 2 ** 31
-    say("large clip", what, (B, C, T, H, W))
-    base = synth.normal((B, C, P, H, W), 9100)
-    if what == "depthwise":
-        w = synth.normal((C, 1, 3, 3, 3), 9101, std=0.2)
-        b = synth.normal((C,), 9102)
-        mod = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=(H, W), padding=(0, 1, 1),
-                           groups=C)
-        assert mod.algo == "depthwise"
-    else:
+    depthwise step hands such frames to the 64-bit direct kernel; the pool loop
+    and the GEMM-family steps work from a contiguous copy of each frame, the
+    GEMM family also emitting into a contiguous frame that is copied out).  The
+    clip repeats a 7-frame seeded block, so the oracle recomputes sampled output
+    frames from 3-frame windows."""
+    what, B, C, (H, W), dt, T = case
+    esz, P = (2 if dt == "bf16" else 4), 7
+    assert (B * C - 1) * T * H * W * esz + H * W * esz >= 2 ** 31
+    say("large clip", what, (B, C, T, H, W), dt)
+    tdt = synth.torch_dtype(dt)
+    base = synth.normal((B, C, P, H, W), 9100, dtype=dt)
+    if what == "avgpool":
         mod = coinf.CoPool("avg", batch=B, channels=C, kernel=(3, 3, 3), in_size=(H, W),
-                          stride=1)
+                           stride=1, dtype=tdt)
+    else:
+        groups = C if what == "depthwise" else 1
+        w = synth.normal((C, C // groups, 3, 3, 3), 9101, std=0.2 / (C // groups) ** 0.5,
+                         dtype=dt)
+        b = synth.normal((C,), 9102, dtype=dt)
+        mod = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=(H, W), padding=(0, 1, 1),
+                           groups=groups, algo="auto" if what == "depthwise" else what)
+        assert mod.algo.startswith(what)
     assert mod.delay == 2 and not mod.steps_fused(T)
     x = base.to(DEV).repeat(1, 1, T // P, 1, 1)
     y = mod.forward_steps(x)
     torch.cuda.synchronize()
     del x
     assert y.shape[2] == T - 2
-    for k in (0, 1, 5, 1234, T - 3):
+    for k in (0, 1234, T - 3):
         win = np64(base[:, :, [(k + j) % P for j in range(3)]])
-        if what == "depthwise":
-            ref = oracle.conv_window(win, np.ones(3, np.uint8), np64(w), np64(b), C, 1, (1, 1),
-                                     (1, 1), (1, 1, 1))
-        else:
+        if what == "avgpool":
             ref = oracle.pool_window("avg", win, np.ones(3, np.uint8), (3, 3, 3), (1, 1, 1),
                                      (0, 0), (1, 1, 1), True)
-        assert_close(np64(y[:, :, k:k + 1]), ref, torch.float32, f"{what} frame {k}")
+        else:
+            ref = oracle.conv_window(win, np.ones(3, np.uint8), np64(w), np64(b), groups, 1,
+                                     (1, 1), (1, 1), (1, 1, 1))
+        assert_close(np64(y[:, :, k:k + 1]), ref, tdt, f"{what} frame {k}")
+
+
+@pytest.mark.parametrize("algo,dt", [("gemm", "bf16"), ("gemm", "f32"), ("gemm_img", "bf16")])
+def test_misaligned_frame_is_staged(algo, dt):
+    """A frame that starts one element past an aligned address: the GEMM-family
+    step stages it into an aligned copy and still matches the oracle."""
+    say("misaligned frame", algo, dt)
+    spec = synth.ConvSpec(batch=2, in_channels=16, out_channels=24, kernel=(3, 3, 3),
+                          in_size=(8, 8), padding=(1, 1, 1), dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 6, 9200, "kaiming")
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=2, in_size=(8, 8), padding=spec.padding,
+                      algo=algo)
+    assert co.algo.startswith(algo)
+    n = 2 * 16 * 8 * 8
+    buf = torch.zeros(n + 1, dtype=x.dtype, device=DEV)
+    outs = []
+    for t in range(x.shape[2]):
+        buf[1:].copy_(x[:, :, t].reshape(-1).to(DEV))
+        fr = buf[1:].view(2, 16, 8, 8)
+        assert fr.data_ptr() % 16 != 0
+        y = co.forward_step(fr)
+        if y is not None:
+            outs.append(y.clone())
+    torch.cuda.synchronize()
+    got = np.stack([np64(o) for o in outs], axis=2)
+    ref = oracle_conv(w, b, spec.stride, spec.padding, spec.dilation, 1).forward_steps(np64(x))
+    assert_close(got, ref, synth.torch_dtype(dt), f"{algo} misaligned")
