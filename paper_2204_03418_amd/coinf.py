@@ -286,10 +286,13 @@ class CoConv:
                   "co_conv_attach_state")
         self.handle = h
 
-    def __del__(self):
+    # the destroy function is bound as a default so that objects collected
+    # during interpreter shutdown, after the module globals are cleared, still
+    # release their handles
+    def __del__(self, _destroy=co_conv_destroy):
         h = getattr(self, "handle", None)
         if h is not None and h.value:
-            co_conv_destroy(h)
+            _destroy(h)
             self.handle = None
 
     @property
@@ -413,10 +416,13 @@ class CoPool:
                   "co_pool_attach_state")
         self.handle = h
 
-    def __del__(self):
+    # the destroy function is bound as a default so that objects collected
+    # during interpreter shutdown, after the module globals are cleared, still
+    # release their handles
+    def __del__(self, _destroy=co_pool_destroy):
         h = getattr(self, "handle", None)
         if h is not None and h.value:
-            co_pool_destroy(h)
+            _destroy(h)
             self.handle = None
 
     @property
@@ -534,10 +540,13 @@ class CoDelay:
                                   _stream(), ctypes.byref(h)), "co_delay_init_state")
         self.handle = h
 
-    def __del__(self):
+    # the destroy function is bound as a default so that objects collected
+    # during interpreter shutdown, after the module globals are cleared, still
+    # release their handles
+    def __del__(self, _destroy=co_delay_destroy):
         h = getattr(self, "handle", None)
         if h is not None and h.value:
-            co_delay_destroy(h)
+            _destroy(h)
             self.handle = None
 
     delay = property(lambda self: self.desc.delay)
@@ -635,10 +644,13 @@ class ConvPool:
         co_convpool_destroy(h)
         return True
 
-    def __del__(self):
+    # the destroy function is bound as a default so that objects collected
+    # during interpreter shutdown, after the module globals are cleared, still
+    # release their handles
+    def __del__(self, _destroy=co_convpool_destroy):
         h = getattr(self, "handle", None)
         if h is not None and h.value:
-            co_convpool_destroy(h)
+            _destroy(h)
             self.handle = None
 
     delay = property(lambda self: chain_delay([self.conv, self.pool])[3])
