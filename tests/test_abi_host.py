@@ -101,6 +101,30 @@ def test_auto_algorithm_choice():
     assert C.conv_query(g).algo in (C.CO_ALGO_DIRECT, C.CO_ALGO_GEMM, C.CO_ALGO_GEMM_REG)
 
 
+def test_frames_past_32bit_offsets_keep_to_64bit_kernels():
+    """The GEMM-family kernels address one frame and the ring with 32-bit byte
+    offsets: an input or output frame of 2^31 bytes (within the element limit)
+    rules them out when the algorithm is chosen, one stream fewer keeps them."""
+    f32 = dict(padding=(0, 1, 1), dtype=C.CO_F32)
+    # input frame 128 x 256 x 128 x 128 fp32 = 2^31 bytes
+    d = C.conv_desc(128, 256, 16, (1, 3, 3), (128, 128), algo="gemm", **f32)
+    assert _status(d) == C.CO_ENOTSUP
+    d = C.conv_desc(128, 256, 16, (1, 3, 3), (128, 128), **f32)
+    assert C.conv_query(d).algo == C.CO_ALGO_DIRECT
+    d = C.conv_desc(127, 256, 16, (1, 3, 3), (128, 128), algo="gemm", **f32)
+    assert C.conv_query(d).algo == C.CO_ALGO_GEMM
+    # output frame 128 x 256 x 128 x 128 fp32
+    d = C.conv_desc(128, 16, 256, (1, 3, 3), (128, 128), algo="gemm", **f32)
+    assert _status(d) == C.CO_ENOTSUP
+    d = C.conv_desc(127, 16, 256, (1, 3, 3), (128, 128), algo="gemm", **f32)
+    assert C.conv_query(d).algo == C.CO_ALGO_GEMM
+    # register GEMM, bf16 1x1: input frame 1024 x 64 x 128 x 128 bf16 = 2^31 bytes
+    d = C.conv_desc(1024, 64, 16, (1, 1, 1), (128, 128), dtype=C.CO_BF16, algo="gemm_reg")
+    assert _status(d) == C.CO_ENOTSUP
+    d = C.conv_desc(1023, 64, 16, (1, 1, 1), (128, 128), dtype=C.CO_BF16, algo="gemm_reg")
+    assert C.conv_query(d).algo == C.CO_ALGO_GEMM_REG
+
+
 def test_null_and_small_buffers_rejected_without_device():
     d = desc1d()
     info = C.conv_query(d)
