@@ -30,14 +30,18 @@ struct ActiveTaps {
   int32_t slot[CO_MAX_TAPS];
 };
 
+// Threads per workgroup of the step kernel: one wave per workgroup measures
+// fastest for these latency-bound steps.
+constexpr int kDwStepBlock = 64;
+
 template <typename T, int KH, int KW>
-__global__ __launch_bounds__(kBlock) void conv_step_dw_kernel(
+__global__ __launch_bounds__(kDwStepBlock) void conv_step_dw_kernel(
     ConvGeom g, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y, int64_t y_bc,
     const float* __restrict__ w, const float* __restrict__ bias, float* __restrict__ ring,
     int64_t ring_slot, ActiveTaps at) {
   const int32_t So = g.Ho * g.Wo;
   const int32_t total = g.B * g.Cout * So;
-  const int32_t idx = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  const int32_t idx = int32_t(blockIdx.x) * kDwStepBlock + int32_t(threadIdx.x);
   if (idx >= total) return;
   // threads in ring order (c, b, pixel): the ring is most of a step's bytes,
   // so its reads and writes are the ones kept contiguous across a wave
@@ -113,9 +117,9 @@ hipError_t dw_launch(const ConvGeom& g, const ConvLayout& L, char* state, const 
   at.fd_So = make_fastdiv(uint32_t(g.So()));
   at.fd_B = make_fastdiv(uint32_t(g.B));
   at.fd_Wo = make_fastdiv(uint32_t(g.Wo));
-  hipLaunchKernelGGL((conv_step_dw_kernel<T, KH, KW>), dim3(grid_for(g.out_frame_elems())),
-                     dim3(kBlock), 0, s, g, static_cast<const T*>(io.x), io.x_bc,
-                     static_cast<T*>(io.y), io.y_bc,
+  hipLaunchKernelGGL((conv_step_dw_kernel<T, KH, KW>),
+                     dim3(grid_for(g.out_frame_elems(), kDwStepBlock)), dim3(kDwStepBlock), 0, s, g,
+                     static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
                      reinterpret_cast<const float*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
                      reinterpret_cast<float*>(state + L.ring), L.ring_slot_elems, at);

@@ -37,7 +37,12 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
-constexpr int kRegWaves = 4;  // independent waves per workgroup
+constexpr int kRegWaves = 4;  // independent waves per workgroup (persistent kernel)
+// Tiles per workgroup of the step kernel.  One tile (one wave, or the
+// KSPLIT waves that share it) per workgroup measures fastest: these steps
+// are bound by launch and memory latency, and small workgroups are
+// dispatched and retired as soon as their own tile is done.
+constexpr int kRegStepTiles = 1;
 
 constexpr int kRegMaxTaps = 16;  // tap offsets passed (>= taps per wave x waves per tile)
 
@@ -67,7 +72,7 @@ struct RegTaps {
 // blocks and C_in is a multiple of the block width, so no k-step is idle and
 // no lane reads past C_in (no per-k-step selects).
 template <typename T, int WN, int TAPS, int CSMAX, int KSPLIT, bool VEC, bool EXACT>
-__global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
+__global__ __launch_bounds__(64 * KSPLIT * kRegStepTiles) void conv_step_reg_kernel(
     ConvGeom g, RegArgs ra, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
     int64_t y_bc, const uint4* __restrict__ wp, const float* __restrict__ bias,
     float* __restrict__ ring, RegTaps tt) {
@@ -85,7 +90,7 @@ __global__ __launch_bounds__(64 * kRegWaves) void conv_step_reg_kernel(
   // consecutive logical blocks (neighbouring tiles) share an XCD's L2.
   const int bid = int(blockIdx.x);
   const int lb = (bid & 7) * ra.blocks_per_xcd + (bid >> 3);
-  constexpr int TPW = kRegWaves / KSPLIT;  // tiles per workgroup
+  constexpr int TPW = kRegStepTiles;  // tiles per workgroup
   const int h = wave % KSPLIT, wslot = wave / KSPLIT;
   const int tile_raw = lb * TPW + wslot;
   const int tiles = ra.m_frags * ra.n_grps;
@@ -396,7 +401,7 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   ra.nf0 = (t_lo * g.Cout) / 16;
   const int nf_end = int(ceil_div(int64_t(t_hi + 1) * g.Cout, 16));
   ra.n_grps = int32_t(ceil_div(nf_end - ra.nf0, WN));
-  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegWaves / KSPLIT);
+  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegStepTiles);
   ra.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
   ra.ntaps = g.kH * g.kW;
   ra.CS = c.CS;
@@ -423,8 +428,8 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
                            : conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, true, false>)
                   : (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, false, true>
                            : conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, false, false>);
-  hipLaunchKernelGGL(kern, dim3(unsigned(8 * ra.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g,
-                     ra, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
+  hipLaunchKernelGGL(kern, dim3(unsigned(8 * ra.blocks_per_xcd)),
+                     dim3(64 * KSPLIT * kRegStepTiles), 0, s, g, ra, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
                      reinterpret_cast<const uint4*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
                      reinterpret_cast<float*>(state + L.ring), tt);
