@@ -15,8 +15,16 @@ namespace coinf {
 
 namespace {
 
-// One thread per output element (b, o, i, j); taps in an outer loop so the
-// kernel handles any kT without a register array.
+// Taps handled per pass of the step kernel: their ring reads are issued
+// together and one sweep over the frame's window feeds all their sums.
+constexpr int kDirStepTaps = 4;
+
+// One thread per output element (b, o, i, j).  Every temporal tap contracts
+// the same window of the arriving frame, so the taps of a pass share one
+// sweep over (c, u, v): each input value is loaded once for up to
+// kDirStepTaps sums, and the ring partials those taps continue are requested
+// before the sweep.  Each tap's sum runs over (c, u, v) in the same order as
+// a tap computed alone, so the results do not depend on the pass width.
 template <typename T, bool ZERO>
 __global__ __launch_bounds__(kBlock) void conv_step_direct_kernel(
     ConvGeom g, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y, int64_t y_bc,
@@ -37,33 +45,46 @@ __global__ __launch_bounds__(kBlock) void conv_step_direct_kernel(
   // ring layout (slot, C_out, B, Ho, Wo): channel-major so that consecutive
   // output pixels of all streams are contiguous for every kernel family
   const int32_t ridx = (o * g.B + b) * So + p;
-  for (int32_t j = 0; j < g.kT; ++j) {
-    const int act = tt.action[j];
-    if (act == CO_TAP_NONE) continue;
-    float acc = 0.f;
+  const int64_t yi = int64_t(bo) * y_bc + p;
+  for (int32_t j0 = 0; j0 < g.kT; j0 += kDirStepTaps) {
+    int act[kDirStepTaps];
+    float* r[kDirStepTaps];
+    float prev[kDirStepTaps], acc[kDirStepTaps];
+#pragma unroll
+    for (int k = 0; k < kDirStepTaps; ++k) {
+      const int32_t j = j0 + k;
+      act[k] = j < g.kT ? int(tt.action[j]) : CO_TAP_NONE;
+      r[k] = ring + int64_t(j < g.kT && tt.slot[j] >= 0 ? tt.slot[j] : 0) * ring_slot + ridx;
+      prev[k] = (act[k] == CO_TAP_ACC || act[k] == CO_TAP_EMIT) ? *r[k] : 0.f;
+      acc[k] = 0.f;
+    }
     if (!ZERO) {
       for (int32_t c = 0; c < g.Cg; ++c) {
         const T* xc = xb + int64_t(c) * x_bc;
-        const float* wc = w + (int64_t(o) * g.Cg + c) * g.kT * kHW + int64_t(j) * kHW;
+        const float* wc = w + (int64_t(o) * g.Cg + c) * g.kT * kHW + int64_t(j0) * kHW;
         for (int32_t u = 0; u < g.kH; ++u) {
           const int32_t hi = i * g.sH + u * g.dH - g.pH;
           if (hi < 0 || hi >= g.H) continue;
           for (int32_t v = 0; v < g.kW; ++v) {
             const int32_t wi = jo * g.sW + v * g.dW - g.pW;
             if (wi < 0 || wi >= g.W) continue;
-            acc = fmaf(wc[u * g.kW + v], to_f32<T>(xc[hi * g.W + wi]), acc);
+            const float xv = to_f32<T>(xc[hi * g.W + wi]);
+#pragma unroll
+            for (int k = 0; k < kDirStepTaps; ++k)
+              if (act[k] != CO_TAP_NONE) acc[k] = fmaf(wc[k * kHW + u * g.kW + v], xv, acc[k]);
           }
         }
       }
     }
-    float* r = ring + int64_t(tt.slot[j] < 0 ? 0 : tt.slot[j]) * ring_slot + ridx;
-    const int64_t yi = int64_t(bo) * y_bc + p;
-    switch (act) {
-      case CO_TAP_START: *r = acc; break;
-      case CO_TAP_ACC: *r = *r + acc; break;
-      case CO_TAP_EMIT: y[yi] = from_f32<T>(*r + acc + bias[o]); break;
-      case CO_TAP_EMIT_FRESH: y[yi] = from_f32<T>(acc + bias[o]); break;
-      default: break;
+#pragma unroll
+    for (int k = 0; k < kDirStepTaps; ++k) {
+      switch (act[k]) {
+        case CO_TAP_START: *r[k] = acc[k]; break;
+        case CO_TAP_ACC: *r[k] = prev[k] + acc[k]; break;
+        case CO_TAP_EMIT: y[yi] = from_f32<T>(prev[k] + acc[k] + bias[o]); break;
+        case CO_TAP_EMIT_FRESH: y[yi] = from_f32<T>(acc[k] + bias[o]); break;
+        default: break;
+      }
     }
   }
 }
