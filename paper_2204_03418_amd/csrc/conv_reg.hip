@@ -37,12 +37,13 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
-constexpr int kRegWaves = 4;  // independent waves per workgroup (persistent kernel)
-// Tiles per workgroup of the step kernel.  One tile (one wave, or the
-// KSPLIT waves that share it) per workgroup measures fastest: these steps
-// are bound by launch and memory latency, and small workgroups are
-// dispatched and retired as soon as their own tile is done.
-constexpr int kRegStepTiles = 1;
+// Tiles per workgroup of both kernels.  One tile (one wave, or the KSPLIT
+// waves that share it) per workgroup measures fastest: the steps are bound
+// by launch and memory latency, and small workgroups are dispatched and
+// retired as soon as their own tile is done; in the persistent kernel the
+// waves of a tile meet at the per-frame barrier without waiting for the
+// waves of other tiles.
+constexpr int kRegTiles = 1;
 
 constexpr int kRegMaxTaps = 16;  // tap offsets passed (>= taps per wave x waves per tile)
 
@@ -72,7 +73,7 @@ struct RegTaps {
 // blocks and C_in is a multiple of the block width, so no k-step is idle and
 // no lane reads past C_in (no per-k-step selects).
 template <typename T, int WN, int TAPS, int CSMAX, int KSPLIT, bool VEC, bool EXACT>
-__global__ __launch_bounds__(64 * KSPLIT * kRegStepTiles) void conv_step_reg_kernel(
+__global__ __launch_bounds__(64 * KSPLIT * kRegTiles) void conv_step_reg_kernel(
     ConvGeom g, RegArgs ra, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
     int64_t y_bc, const uint4* __restrict__ wp, const float* __restrict__ bias,
     float* __restrict__ ring, RegTaps tt) {
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(64 * KSPLIT * kRegStepTiles) void conv_step_reg_ker
   // consecutive logical blocks (neighbouring tiles) share an XCD's L2.
   const int bid = int(blockIdx.x);
   const int lb = (bid & 7) * ra.blocks_per_xcd + (bid >> 3);
-  constexpr int TPW = kRegStepTiles;  // tiles per workgroup
+  constexpr int TPW = kRegTiles;  // tiles per workgroup
   const int h = wave % KSPLIT, wslot = wave / KSPLIT;
   const int tile_raw = lb * TPW + wslot;
   const int tiles = ra.m_frags * ra.n_grps;
@@ -401,7 +402,7 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
   ra.nf0 = (t_lo * g.Cout) / 16;
   const int nf_end = int(ceil_div(int64_t(t_hi + 1) * g.Cout, 16));
   ra.n_grps = int32_t(ceil_div(nf_end - ra.nf0, WN));
-  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegStepTiles);
+  const int64_t blocks = ceil_div(int64_t(ra.m_frags) * ra.n_grps, kRegTiles);
   ra.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
   ra.ntaps = g.kH * g.kW;
   ra.CS = c.CS;
@@ -429,7 +430,8 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
                   : (exact ? conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, false, true>
                            : conv_step_reg_kernel<T, WN, TAPS, CSMAX, KSPLIT, false, false>);
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * ra.blocks_per_xcd)),
-                     dim3(64 * KSPLIT * kRegStepTiles), 0, s, g, ra, static_cast<const T*>(io.x), io.x_bc, static_cast<T*>(io.y), io.y_bc,
+                     dim3(64 * KSPLIT * kRegTiles), 0, s, g, ra, static_cast<const T*>(io.x),
+                     io.x_bc, static_cast<T*>(io.y), io.y_bc,
                      reinterpret_cast<const uint4*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
                      reinterpret_cast<float*>(state + L.ring), tt);
@@ -465,7 +467,7 @@ struct RegSteps {
 };
 
 template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL>
-__global__ __launch_bounds__(64 * kRegWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(64 * KSPLIT * kRegTiles) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
                            T* __restrict__ y, const uint4* __restrict__ wp,
                            const float* __restrict__ bias, float* __restrict__ ring) {
@@ -487,7 +489,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   // h = 0 through LDS every frame, and h = 0 adds them exactly as a single
   // wave adds its two chains.  Waves past the last tile keep to the per-frame
   // barrier: they redo tile 0 with every store masked.
-  constexpr int TPW = kRegWaves / KSPLIT;  // tiles per workgroup
+  constexpr int TPW = kRegTiles;  // tiles per workgroup
   const int h = wave % KSPLIT, wslot = wave / KSPLIT;
   const int tile_raw = lb * TPW + wslot;
   const bool live = tile_raw < rs.m_frags * rs.o_frags;
@@ -755,7 +757,7 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.So = int32_t(g.So());
   rs.m_frags = c.m_frags;
   rs.o_frags = int32_t(ceil_div(g.Cout, 16));
-  const int64_t blocks = ceil_div(int64_t(rs.m_frags) * rs.o_frags, kRegWaves / KSPLIT);
+  const int64_t blocks = ceil_div(int64_t(rs.m_frags) * rs.o_frags, kRegTiles);
   rs.blocks_per_xcd = int32_t(ceil_div(blocks, 8));
   rs.ntaps = g.kH * g.kW;
   rs.CS = c.CS;
@@ -785,8 +787,8 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.fd_ofr = make_fastdiv(uint32_t(rs.o_frags));
   auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true>
                           : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false>;
-  hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * kRegWaves), 0, s, g,
-                     rs, static_cast<const T*>(x), x_bc, static_cast<T*>(y),
+  hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * KSPLIT * kRegTiles),
+                     0, s, g, rs, static_cast<const T*>(x), x_bc, static_cast<T*>(y),
                      reinterpret_cast<const uint4*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
                      reinterpret_cast<float*>(state + L.ring));
