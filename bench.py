@@ -9,16 +9,28 @@ Inputs (the whole synthetic clip, split into contiguous frames), weights and
 the state are resident in HBM before timing starts; runs longer than the clip
 cycle through its frames, continuing the same state (streams are infinite).
 
-Prints one JSON line: stream-frames/s (B x steps / s, eager forward_step
-calls), the roofline of the dominant kernel (the convolution step, launched
-back to back and timed with HIP events around the region), the same steps
-replayed from a HIP graph and through forward_steps, and the CPU oracle timed
-on a bounded sample of the same workload on the host cores.
+The headline line is the 64-stream 192->192 3x3x3 14x14 bf16 layer, the
+largest of the named workloads.  Every timed region runs exactly --steps
+steps and is repeated (at least 5 times, and until the repetitions cover
+10 ms); the median repetition is reported.  The line carries:
+
+* value: stream-frames/s of eager forward_step calls (B x steps / s);
+* roofline: the convolution step kernel alone, launched back to back, timed
+  with HIP events on its launch stream (median repetition), priced on the
+  step's algorithmic FLOPs or bytes;
+* modes: the same steps replayed from a HIP graph, through forward_steps
+  over the resident clip, and (depthwise) through the fused conv+pool step;
+* workloads: the eager step, its kernel and forward_steps, with rooflines,
+  for every named workload;
+* cpu_baseline: the oracle timed on a bounded sample of the same workload on
+  the host cores, at the host's thread count and at one thread.
 """
 import argparse
 import ctypes
 import json
+import math
 import os
+import statistics
 import sys
 import time
 
@@ -26,7 +38,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-DEFAULT_WORKLOAD = "conv3d_b1_c24_k3_56x56_f32"
+DEFAULT_WORKLOAD = "conv3d_b64_c192_k3_14x14_bf16"
 METRIC = "stream-frames/sec for CoConv3d forward_step; % of MFMA peak or HBM GB/s"
 
 # MI355X published peaks
@@ -36,18 +48,26 @@ PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 # FLOP x 2.4 GHz (packed fp32 instructions are not used).
 PEAK_VALU_F32_TFLOPS = 78.6
 
+MIN_REPS = 5
+MIN_REGION_MS = 10.0
+WARM_MS = 250.0
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--algo", default="auto")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="bounded CPU-oracle sample (seconds of oracle work)")
+                    help="bounded CPU-oracle sample (seconds of oracle work per thread count)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-modes", action="store_true", help="skip graph / forward_steps modes")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the per-workload table (headline workload only)")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time the eager conv step rotating over >512 MB of layer states")
     ap.add_argument("--copy-mib", type=float, default=0.0,
                     help="instead of the benchmark, run --steps plain device copies of this many "
                          "MiB (calibrates the HBM traffic counters)")
@@ -126,6 +146,239 @@ def per_step_work(c, Ho, Wo):
     return flops, x_bytes + w_bytes + ring_bytes + y_bytes
 
 
+def timed(fn, stream, est_ms=None):
+    """Median wall time (ms, HIP events on `stream`) of repetitions of fn():
+    at least MIN_REPS, and enough that they cover MIN_REGION_MS together.
+    Returns (median ms, repetitions)."""
+    import torch
+    if est_ms is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        est_ms = max(e0.elapsed_time(e1), 1e-3)
+    reps = max(MIN_REPS, min(200, int(math.ceil(MIN_REGION_MS / est_ms))))
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in ev), reps
+
+
+class Workload:
+    """One named workload resident on the GPU: frames, layer handles and
+    output buffers; a running step counter keeps every timed step emitting."""
+
+    def __init__(self, name, dev, algo="auto"):
+        import torch
+
+        from paper_2204_03418_amd import coinf, synth
+
+        self.name = name
+        self.wl = wl = synth.WORKLOADS[name]
+        self.c = c = wl.conv
+        self.dev = dev
+        self.coinf = coinf
+        x, w, b = synth.workload_inputs(name)
+        self.x_cpu, self.w_cpu, self.b_cpu = x, w, b
+        self.T = x.shape[2]
+        self.frames = [x[:, :, t].contiguous().to(dev) for t in range(self.T)]
+        self.xc = x.to(dev)
+        self.w, self.b = w.to(dev), (b.to(dev) if b is not None else None)
+        self.algo = algo
+        self.co = self.new_conv()
+        self.y = self.co.new_output()
+        self.po = None
+        if wl.pool is not None:
+            pl = wl.pool
+            self.po = coinf.CoPool(pl.kind, batch=pl.batch, channels=pl.channels,
+                                   kernel=pl.kernel, in_size=pl.in_size, stride=pl.stride,
+                                   padding=pl.padding, count_include_pad=pl.count_include_pad,
+                                   dtype=synth.torch_dtype(pl.dtype), device=dev)
+            self.z = torch.empty(self.po.out_frame_shape(), dtype=synth.torch_dtype(pl.dtype),
+                                 device=dev)
+        self.fptr = [ctypes.c_void_p(f.data_ptr()) for f in self.frames]
+        self.yptr = ctypes.c_void_p(self.y.data_ptr())
+        self.zptr = ctypes.c_void_p(self.z.data_ptr()) if self.po is not None else None
+        self.stream = torch.cuda.current_stream()
+        self.sp = ctypes.c_void_p(self.stream.cuda_stream)
+        self.n = 0
+        Ho, Wo = (tuple(self.co.out_size) + (1, 1))[:2]
+        self.flops, self.nbytes = per_step_work(c, Ho, Wo)
+        self.io_bytes = self.nbytes - 2 * (kT_of(c) - 1) * c.batch * c.out_channels * Ho * Wo * 4
+        if c.dtype == "bf16" or self.co.algo.startswith("gemm"):
+            self.bound_compute, self.peak_c = "mfma", PEAK_MFMA_TFLOPS[c.dtype]
+        else:
+            self.bound_compute, self.peak_c = "alu", PEAK_VALU_F32_TFLOPS
+        self.ridge = self.peak_c * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+    def new_conv(self):
+        c = self.c
+        return self.coinf.CoConv(self.w, self.b, batch=c.batch, in_size=c.in_size,
+                                 stride=c.stride, padding=c.padding, dilation=c.dilation,
+                                 groups=c.groups, algo=self.algo)
+
+    @property
+    def delay(self):
+        return self.co.delay + (self.po.delay if self.po is not None else 0)
+
+    def steps(self, count, stream_ptr=None):
+        """`count` eager forward_step calls (conv, then pool when it emitted)."""
+        sp = self.sp if stream_ptr is None else stream_ptr
+        conv_step, pool_step = self.coinf.co_conv_forward_step, self.coinf.co_pool_forward_step
+        hc = self.co.handle
+        hp = self.po.handle if self.po is not None else None
+        for i in range(self.n, self.n + count):
+            st = conv_step(hc, self.fptr[i % self.T], self.yptr, 1, sp)
+            if hp is not None and st == self.coinf.CO_OK:
+                pool_step(hp, self.yptr, self.zptr, 1, sp)
+        self.n += count
+
+    def conv_steps(self, count):
+        """`count` convolution step launches alone (every one emits)."""
+        conv_step = self.coinf.co_conv_forward_step
+        hc = self.co.handle
+        for i in range(self.n, self.n + count):
+            conv_step(hc, self.fptr[i % self.T], self.yptr, 1, self.sp)
+        self.n += count
+
+    def roofline(self, us, flops=None, nbytes=None):
+        """Roofline entry of a kernel taking `us` per launch: compute-priced
+        when the arithmetic intensity on `nbytes` is above the ridge, else
+        HBM-priced."""
+        flops = self.flops if flops is None else flops
+        nbytes = self.nbytes if nbytes is None else nbytes
+        if flops / nbytes >= self.ridge:
+            a = flops / (us * 1e-6) / 1e12
+            return {"bound": self.bound_compute, "achieved": round(a, 3), "peak": self.peak_c,
+                    "unit": "TFLOP/s", "frac": round(a / self.peak_c, 5)}
+        a = nbytes / (us * 1e-6) / 1e9
+        return {"bound": "hbm", "achieved": round(a, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(a / PEAK_HBM_GBS, 5)}
+
+    def eager(self, K):
+        """Median ms of K eager steps; stream-frames/s."""
+        ms, reps = timed(lambda: self.steps(K), self.stream)
+        return ms, reps, self.c.batch * K / (ms / 1e3)
+
+    def kernel_us(self, K):
+        """The convolution step kernel alone, K launches back to back on its
+        stream, bracketed by HIP events: median µs per launch."""
+        ms, _ = timed(lambda: self.conv_steps(K), self.stream)
+        return ms * 1e3 / K
+
+    def forward_steps(self, K):
+        """forward_steps over the resident clip (the depthwise workload chains
+        the convolution's output clip into the pool's forward_steps): calls of
+        T frames covering at least K frames; median µs per frame."""
+        calls = max(1, -(-K // self.T))
+
+        def clip_pass():
+            for _ in range(calls):
+                yc = self.co.forward_steps(self.xc)
+                if self.po is not None and yc is not None:
+                    self.po.forward_steps(yc)
+
+        clip_pass()
+        ms, _ = timed(clip_pass, self.stream)
+        return ms * 1e3 / (calls * self.T)
+
+    def graph(self, K):
+        """The same eager steps replayed from a HIP graph of whole schedule
+        periods (ring slots x stride, at least 64 steps), so replays keep the
+        state coherent: stream-frames/s."""
+        import torch
+        period = self.co.info.ring_slots * self.c.stride[0]
+        if self.po is not None:
+            period *= self.po.info.fifo_slots * self.wl.pool.stride[0]
+        period *= max(1, -(-64 // period))
+        gstream = torch.cuda.Stream()
+        gstream.wait_stream(self.stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(gstream):
+            with torch.cuda.graph(graph, stream=gstream):
+                self.steps(period, ctypes.c_void_p(gstream.cuda_stream))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        reps = max(1, K // period)
+
+        def replay():
+            for _ in range(reps):
+                graph.replay()
+
+        ms, _ = timed(replay, self.stream)
+        return self.c.batch * reps * period / (ms / 1e3)
+
+    def fused_convpool(self, K):
+        """Depthwise conv + global pool fused into one launch per step, and
+        over the clip: stream-frames/s of each (None when the pair does not
+        fuse)."""
+        coinf = self.coinf
+        if self.po is None or not coinf.ConvPool.fits(self.co, self.po):
+            return None
+        co2 = self.new_conv()
+        c = self.wl.pool
+        po2 = coinf.CoPool(c.kind, batch=c.batch, channels=c.channels, kernel=c.kernel,
+                           in_size=c.in_size, stride=c.stride, padding=c.padding,
+                           count_include_pad=c.count_include_pad,
+                           dtype=self.z.dtype, device=self.dev)
+        cp = coinf.ConvPool(co2, po2)
+        cp_step = coinf.co_convpool_forward_step
+        state = {"n": 0}
+
+        def run(count):
+            for i in range(state["n"], state["n"] + count):
+                cp_step(cp.handle, self.fptr[i % self.T], self.zptr, 1, self.sp)
+            state["n"] += count
+
+        run(2 * self.T)
+        ms, _ = timed(lambda: run(K), self.stream)
+        step = self.c.batch * K / (ms / 1e3)
+        calls = max(1, -(-K // self.T))
+
+        def clip():
+            for _ in range(calls):
+                cp.forward_steps(self.xc)
+
+        clip()
+        ms, _ = timed(clip, self.stream)
+        return step, self.c.batch * calls * self.T / (ms / 1e3)
+
+    def cold(self, K):
+        """The eager conv step rotating over enough independent layer states
+        (rings and packed weights) that their footprint passes 512 MB, twice
+        the 256 MB Infinity Cache, so the ring's reads and writes come from
+        HBM rather than the cache; frames rotate too."""
+        nh = int(min(1024, max(2, -(-512 * 2**20 // self.co.info.state_bytes))))
+        cold = [self.new_conv() for _ in range(nh)]
+        ch = [cc.handle for cc in cold]
+        conv_step = self.coinf.co_conv_forward_step
+        for r in range(self.co.delay + 1):
+            for k in range(nh):
+                conv_step(ch[k], self.fptr[r % self.T], self.yptr, 1, self.sp)
+        Kc = max(K, 2 * nh)
+        state = {"i": 0}
+
+        def run():
+            for i in range(state["i"], state["i"] + Kc):
+                conv_step(ch[i % nh], self.fptr[(i // nh) % self.T], self.yptr, 1, self.sp)
+            state["i"] += Kc
+
+        ms, _ = timed(run, self.stream)
+        us = ms * 1e3 / Kc
+        out = {"states": nh, "footprint_mb": round(nh * self.co.info.state_bytes / 2**20, 1),
+               "kernel_avg_us": round(us, 3)}
+        out.update(self.roofline(us))
+        return self.c.batch / (us * 1e-6), out
+
+
 def main():
     args = parse()
     if args.copy_mib > 0:
@@ -137,233 +390,63 @@ def main():
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
-    import numpy as np
     import torch
 
-    from paper_2204_03418_amd import coinf, synth
+    from paper_2204_03418_amd import synth
 
-    wl = synth.WORKLOADS[args.workload]
-    c = wl.conv
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    x, w, b = synth.workload_inputs(args.workload)
-    T = x.shape[2]
-    frames = [x[:, :, t].contiguous().to(dev) for t in range(T)]
-    co = coinf.CoConv(w.to(dev), b.to(dev) if b is not None else None, batch=c.batch,
-                      in_size=c.in_size, stride=c.stride, padding=c.padding,
-                      dilation=c.dilation, groups=c.groups, algo=args.algo)
-    y = co.new_output()
-    po = None
-    if wl.pool is not None:
-        pl = wl.pool
-        po = coinf.CoPool(pl.kind, batch=pl.batch, channels=pl.channels, kernel=pl.kernel,
-                          in_size=pl.in_size, stride=pl.stride, padding=pl.padding,
-                          count_include_pad=pl.count_include_pad,
-                          dtype=synth.torch_dtype(pl.dtype), device=dev)
-        z = torch.empty(po.out_frame_shape(), dtype=synth.torch_dtype(pl.dtype), device=dev)
+    K = args.steps
 
-    fptr = [ctypes.c_void_p(f.data_ptr()) for f in frames]
-    yptr = ctypes.c_void_p(y.data_ptr())
-    zptr = ctypes.c_void_p(z.data_ptr()) if po is not None else None
-    conv_step = coinf.co_conv_forward_step
-    pool_step = coinf.co_pool_forward_step
-    hconv = co.handle
-    hpool = po.handle if po is not None else None
-
-    def run(n0, count, stream_ptr):
-        for i in range(n0, n0 + count):
-            st = conv_step(hconv, fptr[i % T], yptr, 1, stream_ptr)
-            if hpool is not None and st == coinf.CO_OK:
-                pool_step(hpool, yptr, zptr, 1, stream_ptr)
-
-    stream = torch.cuda.current_stream()
-    sp = ctypes.c_void_p(stream.cuda_stream)
-    # warm-up: past the delay so every timed step emits
-    warm = max(args.warmup, co.delay + (po.delay if po is not None else 0) + 2)
-    run(0, warm, sp)
-    torch.cuda.synchronize()
-    n = warm
+    wk = Workload(args.workload, dev, args.algo)
+    c = wk.c
+    # warm-up: past the delay so every timed step emits, and long enough
+    # (WARM_MS of steps) that the clocks have left their idle state
+    warm = warm_up(wk, args.warmup)
 
     # (i) eager forward_step calls: the headline number
-    K = args.steps
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    run(n, K, sp)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    n += K
-    ms = e0.elapsed_time(e1)
+    ms, reps, value = wk.eager(K)
     ms_per_step = ms / K
-    value = c.batch * K / (ms / 1e3)
 
     # dominant kernel: the conv step alone, launched back to back (every step
-    # emits, so each launch is one full contraction + ring update + emit);
-    # HIP events bracket the region on the launch stream
-    Ho, Wo = (tuple(co.out_size) + (1, 1))[:2]
-    flops, nbytes = per_step_work(c, Ho, Wo)
-    Kk = K
-    k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    k0.record(stream)
-    for i in range(Kk):
-        conv_step(hconv, fptr[(n + i) % T], yptr, 1, sp)
-    k1.record(stream)
-    torch.cuda.synchronize()
-    n += Kk
-    kern_ms = k0.elapsed_time(k1) / Kk
-    if c.dtype == "bf16" or co.algo.startswith("gemm"):
-        bound_compute = "mfma"
-        peak_c = PEAK_MFMA_TFLOPS[c.dtype]
-    else:
-        bound_compute = "alu"
-        peak_c = PEAK_VALU_F32_TFLOPS
-    ai = flops / nbytes
-    ridge = peak_c * 1e12 / (PEAK_HBM_GBS * 1e9)
-    if ai >= ridge:
-        achieved = flops / (kern_ms / 1e3) / 1e12
-        roof = {"bound": bound_compute, "achieved": round(achieved, 3), "peak": peak_c,
-                "unit": "TFLOP/s", "frac": round(achieved / peak_c, 5), "traffic": None}
-    else:
-        achieved = nbytes / (kern_ms / 1e3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": None}
+    # emits, so each launch is one full contraction + ring update + emit)
+    kern_us = wk.kernel_us(K)
+    roof = wk.roofline(kern_us)
     roof["traffic"] = measured_traffic(args.workload)
-    roof.update({"kernel": f"conv step ({co.algo})", "kernel_avg_us": round(kern_ms * 1e3, 3),
-                 "flops_per_launch": flops, "bytes_per_launch": nbytes})
+    roof.update({"kernel": f"conv step ({wk.co.algo})", "kernel_avg_us": round(kern_us, 3),
+                 "flops_per_launch": wk.flops, "bytes_per_launch": wk.nbytes,
+                 "launches_per_region": K, "regions": reps})
 
     modes = {"eager_forward_step": round(value, 1)}
     modes_roof = {}
     if not args.no_modes:
-        # (ii) the same steps replayed from a HIP graph: one schedule period
-        # (ring slots x stride) per capture, so replays keep the state coherent
-        period = co.info.ring_slots * c.stride[0]
-        if po is not None:
-            period *= po.info.fifo_slots * wl.pool.stride[0]
-        period *= max(1, -(-64 // period))  # at least 64 steps per replay
-        reps = max(1, K // period)
-        gstream = torch.cuda.Stream()
-        gstream.wait_stream(stream)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(gstream):
-            with torch.cuda.graph(graph, stream=gstream):
-                gp = ctypes.c_void_p(gstream.cuda_stream)
-                run(n, period, gp)
-        n += period
-        torch.cuda.synchronize()
-        graph.replay()
-        torch.cuda.synchronize()
-        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        g0.record(stream)
-        for _ in range(reps):
-            graph.replay()
-        g1.record(stream)
-        torch.cuda.synchronize()
-        modes["graph_replay"] = round(c.batch * reps * period / (g0.elapsed_time(g1) / 1e3), 1)
-        # (iii) forward_steps over the resident clip (the depthwise workload
-        # chains the convolution's output clip into the pool's forward_steps)
-        xc = x.to(dev)
-        calls = max(1, K // T)
-
-        def clip_pass():
-            yc = co.forward_steps(xc)
-            if po is not None and yc is not None:
-                po.forward_steps(yc)
-
-        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        clip_pass()
-        torch.cuda.synchronize()
-        s0.record(stream)
-        for _ in range(calls):
-            clip_pass()
-        s1.record(stream)
-        torch.cuda.synchronize()
-        modes["forward_steps"] = round(c.batch * calls * T / (s0.elapsed_time(s1) / 1e3), 1)
-        # the same roofline terms for forward_steps: per frame the persistent
-        # launch does the step's FLOPs but moves only the frame and its output
-        # (the partial sums stay on chip), so it is priced on compute
-        us_frame = s0.elapsed_time(s1) * 1e3 / (calls * T)
-        io_bytes = nbytes - 2 * (kT_of(c) - 1) * c.batch * c.out_channels * Ho * Wo * 4
-        tf = flops / (us_frame * 1e-6) / 1e12
-        gbs = io_bytes / (us_frame * 1e-6) / 1e9
-        fs = {"persistent": bool(co.steps_fused(T)), "us_per_frame": round(us_frame, 3),
-              "flops_per_frame": flops, "io_bytes_per_frame": io_bytes}
-        if flops / io_bytes >= ridge:
-            fs.update({"bound": bound_compute, "achieved": round(tf, 3), "peak": peak_c,
-                       "unit": "TFLOP/s", "frac": round(tf / peak_c, 5)})
-        else:
-            fs.update({"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
-                       "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 5)})
+        modes["graph_replay"] = round(wk.graph(K), 1)
+        us_frame = wk.forward_steps(K)
+        modes["forward_steps"] = round(c.batch / (us_frame * 1e-6), 1)
+        fs = {"persistent": bool(wk.co.steps_fused(wk.T)), "us_per_frame": round(us_frame, 3),
+              "flops_per_frame": wk.flops, "io_bytes_per_frame": wk.io_bytes}
+        # per frame the persistent launch does the step's FLOPs but moves only
+        # the frame and its output (the partial sums stay on chip)
+        fs.update(wk.roofline(us_frame, nbytes=wk.io_bytes))
         modes_roof["forward_steps"] = fs
+        fused = wk.fused_convpool(K)
+        if fused is not None:
+            modes["fused_convpool_step"] = round(fused[0], 1)
+            modes["fused_convpool_forward_steps"] = round(fused[1], 1)
+        if args.cold:
+            v, cr = wk.cold(K)
+            modes["cold_conv_step"] = round(v, 1)
+            modes_roof["cold_conv_step"] = cr
 
-        # (iv) a depthwise convolution feeding a global pool: the fused step
-        # (one launch per step, the same results as the two-launch chain)
-        if po is not None and coinf.ConvPool.fits(co, po):
-            cp = coinf.ConvPool(co, po)
-            cp_step = coinf.co_convpool_forward_step
-            for i in range(2 * T):
-                cp_step(cp.handle, fptr[(n + i) % T], zptr, 1, sp)
-            n += 2 * T
-            f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            f0.record(stream)
-            for i in range(K):
-                cp_step(cp.handle, fptr[(n + i) % T], zptr, 1, sp)
-            f1.record(stream)
-            torch.cuda.synchronize()
-            n += K
-            modes["fused_convpool_step"] = round(c.batch * K / (f0.elapsed_time(f1) / 1e3), 1)
-            # and the fused clip: one launch per forward_steps call where it fits
-            cp.forward_steps(xc)
-            torch.cuda.synchronize()
-            f0.record(stream)
-            for _ in range(calls):
-                cp.forward_steps(xc)
-            f1.record(stream)
-            torch.cuda.synchronize()
-            modes["fused_convpool_forward_steps"] = round(
-                c.batch * calls * T / (f0.elapsed_time(f1) / 1e3), 1)
-
-    if not args.no_modes:
-        # (v) cold: the same eager conv steps rotating over enough independent
-        # layer states (rings and packed weights) that their footprint passes
-        # 512 MB, twice the 256 MB Infinity Cache, so the ring's reads and
-        # writes come from HBM rather than the cache; frames rotate too
-        nh = int(min(1024, max(2, -(-512 * 2**20 // co.info.state_bytes))))
-        cold = [coinf.CoConv(w.to(dev), b.to(dev) if b is not None else None, batch=c.batch,
-                             in_size=c.in_size, stride=c.stride, padding=c.padding,
-                             dilation=c.dilation, groups=c.groups, algo=args.algo)
-                for _ in range(nh)]
-        ch = [cc.handle for cc in cold]
-        for r in range(co.delay + 1):  # past the delay: every timed step emits
-            for k in range(nh):
-                conv_step(ch[k], fptr[r % T], yptr, 1, sp)
-        Kc = max(K, 2 * nh)
-        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        c0.record(stream)
-        for i in range(Kc):
-            conv_step(ch[i % nh], fptr[(i // nh) % T], yptr, 1, sp)
-        c1.record(stream)
-        torch.cuda.synchronize()
-        cms = c0.elapsed_time(c1) / Kc
-        modes["cold_conv_step"] = round(c.batch / (cms / 1e3), 1)
-        cr = {"states": nh, "footprint_mb": round(nh * co.info.state_bytes / 2**20, 1),
-              "kernel_avg_us": round(cms * 1e3, 3)}
-        if roof["bound"] == "hbm":
-            cg = nbytes / (cms / 1e3) / 1e9
-            cr.update({"bound": "hbm", "achieved": round(cg, 2), "peak": PEAK_HBM_GBS,
-                       "unit": "GB/s", "frac": round(cg / PEAK_HBM_GBS, 5)})
-        else:
-            ct = flops / (cms / 1e3) / 1e12
-            cr.update({"bound": roof["bound"], "achieved": round(ct, 3), "peak": peak_c,
-                       "unit": "TFLOP/s", "frac": round(ct / peak_c, 5)})
-        modes_roof["cold_conv_step"] = cr
-        del cold, ch
+    table = {}
+    if not args.no_workloads:
+        for name in synth.WORKLOADS:
+            table[name] = workload_entry(wk if name == args.workload else None, name, dev, K,
+                                         args.algo, args.warmup)
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(wl, x, w, b, args.cpu_seconds)
+        cpu = cpu_baseline(wk, args.cpu_seconds)
 
     out = {
         "metric": METRIC,
@@ -381,53 +464,101 @@ def main():
         "config": {"workload": args.workload, "batch": c.batch, "in_channels": c.in_channels,
                    "out_channels": c.out_channels, "groups": c.groups,
                    "kernel": list(c.kernel), "in_size": list(c.in_size),
-                   "padding": list(c.padding), "frames": T, "algo": co.algo,
-                   "pool": None if wl.pool is None else
-                   {"kind": wl.pool.kind, "kernel": list(wl.pool.kernel),
-                    "stride": list(wl.pool.stride)}},
+                   "padding": list(c.padding), "frames": wk.T, "algo": wk.co.algo,
+                   "pool": None if wk.wl.pool is None else
+                   {"kind": wk.wl.pool.kind, "kernel": list(wk.wl.pool.kernel),
+                    "stride": list(wk.wl.pool.stride)},
+                   "timing": f"median of >= {MIN_REPS} repetitions of {K} steps "
+                             f"({reps} here), HIP events on the launch stream"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "modes": modes,
         "modes_roofline": modes_roof,
+        "workloads": table,
     }
     print(json.dumps(out))
 
 
-def cpu_baseline(wl, x, w, b, seconds):
-    """The oracle's sliding-window driver stepping the same frames on the host
-    cores (float64, OpenMP over (b, o)); bounded to about `seconds` of work."""
-    import numpy as np
+def warm_up(wk, steps):
+    """At least `steps` untimed steps, past the layer's delay, and more until
+    WARM_MS of them have run; returns the number of warm-up steps."""
+    import torch
+    n = max(steps, wk.delay + 2)
+    wk.steps(n)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < WARM_MS:
+        wk.steps(16)
+        n += 16
+        torch.cuda.synchronize()
+    return n
 
+
+def workload_entry(wk, name, dev, K, algo, warmup):
+    """Eager step, its convolution kernel and forward_steps of one named
+    workload, each with its roofline entry."""
+    import torch
+    if wk is None:
+        wk = Workload(name, dev, algo)
+        warm_up(wk, warmup)
+    ms, _, value = wk.eager(K)
+    kern_us = wk.kernel_us(K)
+    us_frame = wk.forward_steps(K)
+    e = {"batch": wk.c.batch, "algo": wk.co.algo, "dtype": wk.c.dtype,
+         "eager_forward_step": round(value, 1), "ms_per_step": round(ms / K, 6),
+         "kernel_avg_us": round(kern_us, 3), "flops_per_step": wk.flops,
+         "bytes_per_step": wk.nbytes, "roofline": wk.roofline(kern_us),
+         "forward_steps": round(wk.c.batch / (us_frame * 1e-6), 1),
+         "forward_steps_us_per_frame": round(us_frame, 3),
+         "forward_steps_persistent": bool(wk.co.steps_fused(wk.T)),
+         "forward_steps_roofline": wk.roofline(us_frame, nbytes=wk.io_bytes)}
+    traffic = measured_traffic(name)
+    if traffic is not None:
+        e["roofline"]["traffic"] = traffic
+    return e
+
+
+def cpu_baseline(wk, seconds):
+    """The oracle's sliding-window driver stepping the same frames on the host
+    cores (float64, OpenMP over (b, o)), bounded to about `seconds` of work:
+    all streams at the host's thread count, and one stream at one thread
+    (streams are independent, so one stream is 1/B of a step's work)."""
     import oracle
 
-    c = wl.conv
-    xs = x.float().double().numpy()
-    co = oracle.ContinualConv(w.float().double().numpy(),
-                              None if b is None else b.float().double().numpy(),
-                              stride=c.stride, padding=c.padding, dilation=c.dilation,
-                              groups=c.groups)
-    po = None
-    if wl.pool is not None:
-        po = oracle.ContinualPool(wl.pool.kind, wl.pool.kernel, wl.pool.stride, wl.pool.padding,
-                                  count_include_pad=wl.pool.count_include_pad,
-                                  spatial_dims=len(wl.pool.in_size))
+    wl, c = wk.wl, wk.c
+    xs = wk.x_cpu.float().double().numpy()
+    w = wk.w_cpu.float().double().numpy()
+    b = None if wk.b_cpu is None else wk.b_cpu.float().double().numpy()
     T = xs.shape[2]
 
-    def step(i):
-        y = co.forward_step(xs[:, :, i % T])
-        if po is not None and y is not None:
-            po.forward_step(y)
+    def driver():
+        co = oracle.ContinualConv(w, b, stride=c.stride, padding=c.padding,
+                                  dilation=c.dilation, groups=c.groups)
+        po = None
+        if wl.pool is not None:
+            po = oracle.ContinualPool(wl.pool.kind, wl.pool.kernel, wl.pool.stride,
+                                      wl.pool.padding, count_include_pad=wl.pool.count_include_pad,
+                                      spatial_dims=len(wl.pool.in_size))
+        return co, po
 
-    for i in range(co.delay + (po.delay if po else 0) + 1):
-        step(i)
-    i0 = co.delay + (po.delay if po else 0) + 1
-    t0 = time.perf_counter()
-    k = 0
-    while time.perf_counter() - t0 < seconds or k == 0:
-        step(i0 + k)
-        k += 1
-    dt = time.perf_counter() - t0
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    def run(frames, secs):
+        co, po = driver()
+
+        def step(i):
+            y = co.forward_step(frames[:, :, i % T])
+            if po is not None and y is not None:
+                po.forward_step(y)
+
+        i0 = co.delay + (po.delay if po else 0) + 1
+        for i in range(i0):
+            step(i)
+        t0 = time.perf_counter()
+        k = 0
+        while time.perf_counter() - t0 < secs or k == 0:
+            step(i0 + k)
+            k += 1
+        return k, time.perf_counter() - t0
+
     cpu_model = ""
     try:
         with open("/proc/cpuinfo") as f:
@@ -437,10 +568,21 @@ def cpu_baseline(wl, x, w, b, seconds):
                     break
     except OSError:
         pass
-    return {"value": round(c.batch * k / dt, 3), "unit": "stream-frames/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{k} steps of the same workload after the delay ({dt:.1f} s, float64, "
-                      f"OpenMP over (b, o)); cpu: {cpu_model}"}
+    threads = oracle.max_threads()
+    k, dt = run(xs, seconds)
+    out = {"value": round(c.batch * k / dt, 3), "unit": "stream-frames/s", "cores": threads,
+           "kind": "oracle",
+           "sample": f"{k} steps of all {c.batch} streams after the delay ({dt:.1f} s, float64, "
+                     f"OpenMP over (b, o), {threads} threads); cpu: {cpu_model}"}
+    oracle.set_threads(1)
+    try:
+        k1, dt1 = run(xs[:1], seconds)
+    finally:
+        oracle.set_threads(threads)
+    out["one_thread"] = {"value": round(k1 / dt1, 3), "unit": "stream-frames/s", "cores": 1,
+                         "sample": f"{k1} steps of one of the {c.batch} streams after the delay "
+                                   f"({dt1:.1f} s, float64, one thread)"}
+    return out
 
 
 if __name__ == "__main__":

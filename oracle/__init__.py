@@ -74,6 +74,10 @@ def _load():
                              + [i64] * 2 + [i64] * 3 + [ctypes.c_int32, dp])
     lib.ora_out_len.restype = i64
     lib.ora_out_len.argtypes = [i64] * 5
+    lib.ora_set_threads.restype = None
+    lib.ora_set_threads.argtypes = [ctypes.c_int32]
+    lib.ora_max_threads.restype = ctypes.c_int32
+    lib.ora_max_threads.argtypes = []
     _lib = lib
     return lib
 
@@ -84,6 +88,16 @@ def _dptr(a):
 
 def _u8ptr(a):
     return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the oracle's OpenMP loops (process-wide)."""
+    _load().ora_set_threads(int(n))
+
+
+def max_threads() -> int:
+    """Threads the oracle's OpenMP loops use now."""
+    return int(_load().ora_max_threads())
 
 
 def out_len(L: int, k: int, s: int, p: int, d: int) -> int:

@@ -21,8 +21,14 @@
  * output (B, C_out, To, Ho, Wo).  Conv1d/2d are the H = W = 1 / W = 1 cases.
  */
 #include <math.h>
+#include <omp.h>
 #include <stddef.h>
 #include <stdint.h>
+
+/* Thread count of the OpenMP loops below (the benchmark's CPU baseline times
+ * the oracle at the host's full thread count and at one thread). */
+void ora_set_threads(int32_t n) { omp_set_num_threads(n > 0 ? n : 1); }
+int32_t ora_max_threads(void) { return omp_get_max_threads(); }
 
 /* L_out = floor((L + 2p - d(k-1) - 1)/s) + 1, or 0 when the window does not fit. */
 static int64_t out_len(int64_t L, int64_t k, int64_t s, int64_t p, int64_t d) {

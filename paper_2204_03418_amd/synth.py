@@ -10,8 +10,9 @@ T = 300 frames of V = 25 joints) and 1-D signal workloads: the datasets and
 trained weights are not used.  Frames are i.i.d. N(0, 1); the kernels are
 data-oblivious, so the distribution affects numerics only, never cost.
 
-Draws are float32 from ``torch.Generator('cpu')`` seeded per workload:
-x with ``1000*c + 0``, weights ``1000*c + 1``, bias ``1000*c + 2``.  bfloat16
+Draws are float32 from ``torch.Generator('cpu')`` seeded per workload number
+c = 1..5 (in the order listed below; both skeleton precisions share 5): x with
+``1000*c + 0``, weights ``1000*c + 1``, bias ``1000*c + 2``.  bfloat16
 workloads round the float32 draws to nearest-even on the host, so the oracle
 and the GPU consume identical values.
 """
@@ -86,7 +87,7 @@ class PoolSpec:
 @dataclass(frozen=True)
 class Workload:
     name: str
-    index: int                     # seed base: 1000 * index
+    index: int                     # workload number 1..5; seed base 1000 * index
     frames: int                    # T of the synthetic clip
     conv: ConvSpec
     pool: PoolSpec = None
@@ -97,34 +98,34 @@ class Workload:
 WORKLOADS = {
     w.name: w for w in [
         Workload(
-            name="conv1d_b1_c4to8_k3_f32", index=0, frames=64,
+            name="conv1d_b1_c4to8_k3_f32", index=1, frames=64,
             conv=ConvSpec(batch=1, in_channels=4, out_channels=8, kernel=(3,), dtype="f32"),
             weight_init="normal",
             note="CoConv1d single stream, 1-D signal"),
         Workload(
-            name="conv3d_b1_c24_k3_56x56_f32", index=1, frames=16,
+            name="conv3d_b1_c24_k3_56x56_f32", index=2, frames=16,
             conv=ConvSpec(batch=1, in_channels=24, out_channels=24, kernel=(3, 3, 3),
                           in_size=(56, 56), padding=(0, 1, 1), dtype="f32"),
             note="CoConv3d single stream, X3D-S-like stem block"),
         Workload(
-            name="conv3d_b64_c192_k3_14x14_bf16", index=2, frames=32,
+            name="conv3d_b64_c192_k3_14x14_bf16", index=3, frames=32,
             conv=ConvSpec(batch=64, in_channels=192, out_channels=192, kernel=(3, 3, 3),
                           in_size=(14, 14), padding=(0, 1, 1), dtype="bf16"),
             note="CoConv3d, 64 independent streams"),
         Workload(
-            name="dwconv3d_b16_c432_k3_7x7_avgpool_bf16", index=3, frames=64,
+            name="dwconv3d_b16_c432_k3_7x7_avgpool_bf16", index=4, frames=64,
             conv=ConvSpec(batch=16, in_channels=432, out_channels=432, kernel=(3, 3, 3),
                           in_size=(7, 7), padding=(0, 1, 1), groups=432, dtype="bf16"),
             pool=PoolSpec(kind="avg", batch=16, channels=432, kernel=(4, 7, 7),
                           in_size=(7, 7), stride=(1, 7, 7), dtype="bf16"),
             note="X3D-style depthwise CoConv3d followed by continual AvgPool3d (4,7,7)"),
         Workload(
-            name="conv2d_b32_c64to256_k9x1_v25_f32", index=4, frames=300,
+            name="conv2d_b32_c64to256_k9x1_v25_f32", index=5, frames=300,
             conv=ConvSpec(batch=32, in_channels=64, out_channels=256, kernel=(9, 1),
                           in_size=(25,), dtype="f32"),
             note="ST-GCN-like temporal conv over T=300 frames of V=25 joints (fp32)"),
         Workload(
-            name="conv2d_b32_c64to256_k9x1_v25_bf16", index=4, frames=300,
+            name="conv2d_b32_c64to256_k9x1_v25_bf16", index=5, frames=300,
             conv=ConvSpec(batch=32, in_channels=64, out_channels=256, kernel=(9, 1),
                           in_size=(25,), dtype="bf16"),
             note="ST-GCN-like temporal conv over T=300 frames of V=25 joints (bf16)"),
