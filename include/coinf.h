@@ -68,6 +68,7 @@ typedef int32_t co_status;
 #define CO_ENOTSUP  -2   /* valid but unsupported (e.g. a forced algorithm) */
 #define CO_ESTATE   -3   /* state buffer too small or not made for this descriptor */
 #define CO_EHIP     -4   /* the HIP runtime reported an error */
+#define CO_ESCRATCH -5   /* the call needs more than the no-allocation scratch holds */
 
 #define CO_F32   0
 #define CO_BF16  1
@@ -198,6 +199,38 @@ co_status co_conv_forward_step(co_conv_handle* h, const void* x_t, void* y_t,
 co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, void* y,
                                 int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                                 void* stream, int32_t* n_out);
+
+/*
+ * forward_steps without device allocation, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Arguments, outputs, status and state semantics are those of
+ * co_conv_forward_steps; the two give bitwise equal outputs and states.
+ *
+ * Where co_conv_forward_steps makes stream-ordered allocations -- the
+ * backup of the ring for update_state = 0 when the call loops over step
+ * launches, and contiguous copies of a frame (or output) that a matrix-core
+ * step kernel cannot address in place (misaligned, or past 2^31 bytes of
+ * reach) -- this entry point uses a scratch array the library holds in
+ * device memory: 64 MiB per GPU (co_conv_scratch_bytes), allocated when the
+ * library's code object is loaded on that GPU and held until the process
+ * ends.  It calls no hipMalloc, hipFree or allocating library routine.
+ *
+ * Returns CO_ESCRATCH (nothing enqueued, handle unchanged) when the call
+ * needs more scratch than that: the ring's bytes (R x B x C_out x Ho x Wo x 4,
+ * rounded up to 256) with update_state = 0 on the looping path, plus the
+ * staged frame copies.  A call that runs as one persistent launch
+ * (co_conv_steps_fused) needs none.
+ *
+ * All calls on one GPU share that GPU's scratch, and each call leaves its
+ * contents behind: calls whose device work overlaps on one GPU (different
+ * streams, or threads) race.  Calls ordered on one stream do not.
+ */
+co_status co_conv_forward_steps_noalloc(co_conv_handle* h, const void* x, int32_t T, void* y,
+                                        int32_t y_cap_frames, int32_t pad_end,
+                                        int32_t update_state, void* stream, int32_t* n_out);
+
+/* Bytes of device scratch co_conv_forward_steps_noalloc holds per GPU.  Host-only. */
+co_status co_conv_scratch_bytes(int64_t* bytes);
 
 /*
  * How co_conv_forward_steps runs a call over T frames into y_cap_frames

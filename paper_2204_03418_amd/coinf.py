@@ -22,6 +22,7 @@ lib = ctypes.CDLL(LIB_PATH)
 
 # ---------------------------------------------------------------- constants
 CO_OK, CO_EMPTY, CO_EINVAL, CO_ENOTSUP, CO_ESTATE, CO_EHIP = 0, 1, -1, -2, -3, -4
+CO_ESCRATCH = -5
 CO_F32, CO_BF16 = 0, 1
 CO_ALGO_AUTO, CO_ALGO_DIRECT, CO_ALGO_GEMM, CO_ALGO_DEPTHWISE, CO_ALGO_GEMM_REG = 0, 1, 2, 3, 4
 CO_ALGO_GEMM_IMG = 5
@@ -103,6 +104,9 @@ co_conv_attach_state = _sig("co_conv_attach_state", i32, [CD, vp, i64, i64, vp, 
 co_conv_destroy = _sig("co_conv_destroy", i32, [vp])
 co_conv_algo_name = _sig("co_conv_algo_name", ctypes.c_char_p, [vp])
 co_conv_steps_fused = _sig("co_conv_steps_fused", i32, [vp, i32, i32, pi32])
+co_conv_forward_steps_noalloc = _sig("co_conv_forward_steps_noalloc", i32,
+                                     [vp, vp, i32, vp, i32, i32, i32, vp, pi32])
+co_conv_scratch_bytes = _sig("co_conv_scratch_bytes", i32, [pi64])
 co_pool_query = _sig("co_pool_query", i32, [PD, PI])
 co_pool_plan_step = _sig("co_pool_plan_step", i32, [PD, i64, ctypes.POINTER(PoolPlan)])
 co_pool_init_state = _sig("co_pool_init_state", i32, [PD, vp, i64, vp, pvp])

@@ -2,12 +2,20 @@
 // Every entry point validates on the host before it enqueues anything, so a
 // negative status means nothing ran and the handle is unchanged.
 #include <algorithm>
+#include <mutex>
 #include <new>
 
 #include "device.hpp"
 #include "launch.hpp"
 
 using namespace coinf;
+
+// Device scratch of co_conv_forward_steps_noalloc: each GPU the library runs
+// on holds its own copy until the process ends.  Host code never uses the
+// array's name as an address; it asks the runtime for the copy on the
+// current device (scratch_address below).
+constexpr int64_t kScratchBytes = int64_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 struct co_conv_handle {
   ConvGeom g;
@@ -80,6 +88,134 @@ co_status restore_range(char* dst, hipStream_t s, Backup* b) {
   return st;
 }
 
+// Device address of `scratch` on the device that runs `stream` (the current
+// device for the null stream), looked up once per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+co_status scratch_address(hipStream_t stream, void** out) {
+  int cur = 0, dev = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return CO_EHIP;
+  dev = cur;
+  if (stream && hipStreamGetDevice(stream, &dev) != hipSuccess) return CO_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return CO_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return CO_EHIP;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) return CO_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return CO_OK;
+}
+
+int64_t round256(int64_t n) { return (n + 255) & ~int64_t(255); }
+
+// Caller-side device workspace of a forward_steps call (null: the call makes
+// stream-ordered allocations instead).
+struct Scratch {
+  char* p;
+  int64_t bytes;
+};
+
+co_status conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, void* y,
+                             int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
+                             hipStream_t s, int32_t* n_out, const Scratch* sc) {
+  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  const ConvGeom& g = h->g;
+  const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  const int64_t n_emit = conv_emissions(g, h->n, count);
+  if (n_emit > y_cap_frames) return CO_EINVAL;
+  if (n_emit > 0 && !y) return CO_EINVAL;
+  const int64_t n0 = h->n;
+  const bool dw = dw_steps_supported(g, T, y_cap_frames);
+  const bool dir = direct_steps_supported(g, T, y_cap_frames);
+  const bool gem = gemm_steps_supported(g, T, y_cap_frames, x);
+  if (count > 0 && (dw || dir || gem || reg_steps_supported(g, T, y_cap_frames))) {
+    // one persistent launch: partial sums stay on chip across frames; with
+    // update_state = 0 the state is simply not written back
+    const auto launch = dw    ? launch_conv_steps_depthwise
+                        : dir ? launch_conv_steps_direct
+                        : gem ? launch_conv_steps_gemm
+                              : launch_conv_steps_reg;
+    const co_status st = hip_status(launch(g, h->L, h->state, x, int64_t(T) * g.S(), T,
+                                           int32_t(count), y, int64_t(y_cap_frames) * g.So(),
+                                           n0, update_state != 0, s));
+    if (st != CO_OK) return st;
+    if (update_state) h->n += count;
+    *n_out = int32_t(n_emit);
+    return CO_OK;
+  }
+  const int64_t S = g.S(), So = g.So();
+  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  const int64_t ring_bytes = int64_t(g.R) * h->L.ring_slot_elems * 4;
+  // With a caller workspace: the ring's backup first, then the staged copies
+  // of a frame the step kernel cannot read in place.  Whether a frame is
+  // staged depends on its pointer's alignment, which repeats every two
+  // frames, and on the plane strides, which every frame shares.
+  const int64_t backup = update_state ? 0 : round256(ring_bytes);
+  if (sc) {
+    int64_t stage = 0;
+    for (int64_t t = 0; t < std::min<int64_t>(T, 2); ++t) {
+      const StepIO io{static_cast<const char*>(x) + size_t(t * S) * esz, int64_t(T) * S,
+                      n_emit > 0 ? y : nullptr, int64_t(y_cap_frames) * So};
+      stage = std::max(stage, conv_step_staging_bytes(g, io));
+    }
+    if (backup + stage > sc->bytes) return CO_ESCRATCH;
+  }
+  Backup bk;
+  if (!update_state) {
+    if (sc) {
+      if (hipMemcpyAsync(sc->p, h->state + h->L.ring, size_t(ring_bytes),
+                         hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return CO_EHIP;
+    } else {
+      const co_status st = backup_range(h->state + h->L.ring, ring_bytes, s, &bk);
+      if (st != CO_OK) return st;
+    }
+  }
+  int64_t k = 0;
+  co_status st = CO_OK;
+  for (int64_t t = 0; t < count; ++t) {
+    co_step_plan plan;
+    conv_plan(g, h->n, true, &plan);
+    const bool pad = t >= T;
+    if (any_tap(plan)) {
+      StepIO io{pad ? nullptr : static_cast<const char*>(x) + size_t(t * S) * esz,
+                int64_t(T) * S,
+                plan.emit ? static_cast<char*>(y) + size_t(k * So) * esz : nullptr,
+                int64_t(y_cap_frames) * So};
+      if (sc) {
+        io.ws = sc->p + backup;
+        io.ws_bytes = sc->bytes - backup;
+      }
+      st = hip_status(launch_conv_step(g, h->L, h->state, io, plan, pad, s));
+      if (st != CO_OK) break;
+    }
+    if (plan.emit) ++k;
+    ++h->n;
+  }
+  if (!update_state) {
+    co_status r = CO_OK;
+    if (sc) {
+      if (hipMemcpyAsync(h->state + h->L.ring, sc->p, size_t(ring_bytes),
+                         hipMemcpyDeviceToDevice, s) != hipSuccess)
+        r = CO_EHIP;
+    } else {
+      r = restore_range(h->state + h->L.ring, s, &bk);
+    }
+    if (st == CO_OK) st = r;
+    h->n = n0;
+  }
+  *n_out = int32_t(k);
+  return st;
+}
+
 }  // namespace
 
 extern "C" {
@@ -92,6 +228,9 @@ const char* co_status_str(co_status s) {
     case CO_ENOTSUP: return "CO_ENOTSUP: unsupported configuration";
     case CO_ESTATE: return "CO_ESTATE: state buffer too small or made for another descriptor";
     case CO_EHIP: return "CO_EHIP: HIP runtime error";
+    case CO_ESCRATCH:
+      return "CO_ESCRATCH: the call needs more device scratch than the no-allocation entry "
+             "point holds";
     default: return "unknown status";
   }
 }
@@ -165,65 +304,26 @@ co_status co_conv_forward_step(co_conv_handle* h, const void* x_t, void* y_t,
 co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, void* y,
                                 int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                                 void* stream, int32_t* n_out) {
-  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
-  if (T > 0 && !x) return CO_EINVAL;
-  const ConvGeom& g = h->g;
-  const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
-  const int64_t n_emit = conv_emissions(g, h->n, count);
-  if (n_emit > y_cap_frames) return CO_EINVAL;
-  if (n_emit > 0 && !y) return CO_EINVAL;
-  hipStream_t s = as_stream(stream);
-  const int64_t n0 = h->n;
-  const bool dw = dw_steps_supported(g, T, y_cap_frames);
-  const bool dir = direct_steps_supported(g, T, y_cap_frames);
-  const bool gem = gemm_steps_supported(g, T, y_cap_frames, x);
-  if (count > 0 && (dw || dir || gem || reg_steps_supported(g, T, y_cap_frames))) {
-    // one persistent launch: partial sums stay on chip across frames; with
-    // update_state = 0 the state is simply not written back
-    const auto launch = dw    ? launch_conv_steps_depthwise
-                        : dir ? launch_conv_steps_direct
-                        : gem ? launch_conv_steps_gemm
-                              : launch_conv_steps_reg;
-    const co_status st = hip_status(launch(g, h->L, h->state, x, int64_t(T) * g.S(), T,
-                                           int32_t(count), y, int64_t(y_cap_frames) * g.So(),
-                                           n0, update_state != 0, s));
-    if (st != CO_OK) return st;
-    if (update_state) h->n += count;
-    *n_out = int32_t(n_emit);
-    return CO_OK;
-  }
-  Backup bk;
-  const int64_t ring_bytes = int64_t(g.R) * h->L.ring_slot_elems * 4;
-  if (!update_state) {
-    const co_status st = backup_range(h->state + h->L.ring, ring_bytes, s, &bk);
-    if (st != CO_OK) return st;
-  }
-  const int64_t S = g.S(), So = g.So();
-  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
-  int64_t k = 0;
-  co_status st = CO_OK;
-  for (int64_t t = 0; t < count; ++t) {
-    co_step_plan plan;
-    conv_plan(g, h->n, true, &plan);
-    const bool pad = t >= T;
-    if (any_tap(plan)) {
-      const StepIO io{pad ? nullptr : static_cast<const char*>(x) + size_t(t * S) * esz,
-                      int64_t(T) * S,
-                      plan.emit ? static_cast<char*>(y) + size_t(k * So) * esz : nullptr,
-                      int64_t(y_cap_frames) * So};
-      st = hip_status(launch_conv_step(g, h->L, h->state, io, plan, pad, s));
-      if (st != CO_OK) break;
-    }
-    if (plan.emit) ++k;
-    ++h->n;
-  }
-  if (!update_state) {
-    const co_status r = restore_range(h->state + h->L.ring, s, &bk);
-    if (st == CO_OK) st = r;
-    h->n = n0;
-  }
-  *n_out = int32_t(k);
-  return st;
+  return conv_forward_steps(h, x, T, y, y_cap_frames, pad_end, update_state, as_stream(stream),
+                            n_out, nullptr);
+}
+
+co_status co_conv_forward_steps_noalloc(co_conv_handle* h, const void* x, int32_t T, void* y,
+                                        int32_t y_cap_frames, int32_t pad_end,
+                                        int32_t update_state, void* stream, int32_t* n_out) {
+  if (!h) return CO_EINVAL;
+  void* p = nullptr;
+  const co_status st = scratch_address(as_stream(stream), &p);
+  if (st != CO_OK) return st;
+  const Scratch sc{static_cast<char*>(p), kScratchBytes};
+  return conv_forward_steps(h, x, T, y, y_cap_frames, pad_end, update_state, as_stream(stream),
+                            n_out, &sc);
+}
+
+co_status co_conv_scratch_bytes(int64_t* bytes) {
+  if (!bytes) return CO_EINVAL;
+  *bytes = kScratchBytes;
+  return CO_OK;
 }
 
 co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_frames,

@@ -345,12 +345,45 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
   return step_direct_t<float>(g, L, state, io, plan, zero_frame, s);
 }
 
+namespace {
+
+int64_t round256(int64_t n) { return (n + 255) & ~int64_t(255); }
+
+// The staged copies of one step: x (B*C_in contiguous planes) and, when the
+// output lies past 32-bit reach, y (B*C_out contiguous planes).
+struct StagedBytes {
+  int64_t x, y;
+};
+
+StagedBytes staged_bytes(const ConvGeom& g, const StepIO& io) {
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  const int64_t yrows = int64_t(g.B) * g.Cout;
+  const bool y_far = io.y && ((yrows - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31);
+  return {int64_t(g.B) * g.Cin * g.S() * esz, y_far ? yrows * g.So() * esz : 0};
+}
+
+}  // namespace
+
+int64_t conv_step_staging_bytes(const ConvGeom& g, const StepIO& io) {
+  bool staged = false;
+  switch (g.algo) {
+    case CO_ALGO_GEMM: staged = gemm_step_needs_staging(g, io); break;
+    case CO_ALGO_GEMM_REG: staged = reg_step_needs_staging(g, io); break;
+    case CO_ALGO_GEMM_IMG: staged = img_step_needs_staging(g, io); break;
+    default: return 0;  // the direct and depthwise kernels use 64-bit offsets
+  }
+  if (!staged) return 0;
+  const StagedBytes b = staged_bytes(g, io);
+  return round256(b.x) + round256(b.y);
+}
+
 hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char* state,
                                    const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   const int64_t S = g.S(), So = g.So(), lim = int64_t(1) << 31;
   const int64_t xrows = int64_t(g.B) * g.Cin, yrows = int64_t(g.B) * g.Cout;
-  const bool y_far = io.y && ((yrows - 1) * io.y_bc + So) * esz >= lim;
+  const StagedBytes sb = staged_bytes(g, io);
+  const bool y_far = sb.y > 0;
   // An input frame that is already contiguous and 16-byte aligned, with an
   // output in 32-bit reach, is what the copies below would produce: the
   // kernel has declined the geometry itself, and staging cannot help.
@@ -359,8 +392,16 @@ hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char*
     return hipErrorInvalidValue;
   void* xs = nullptr;
   void* ys = nullptr;
-  hipError_t e = hipMallocAsync(&xs, size_t(xrows * S * esz), s);
-  if (e == hipSuccess && y_far) e = hipMallocAsync(&ys, size_t(yrows * So * esz), s);
+  hipError_t e = hipSuccess;
+  const bool own = io.ws == nullptr;  // no workspace: stream-ordered allocations
+  if (own) {
+    e = hipMallocAsync(&xs, size_t(sb.x), s);
+    if (e == hipSuccess && y_far) e = hipMallocAsync(&ys, size_t(sb.y), s);
+  } else {
+    if (round256(sb.x) + round256(sb.y) > io.ws_bytes) return hipErrorInvalidValue;
+    xs = io.ws;
+    if (y_far) ys = static_cast<char*>(io.ws) + round256(sb.x);
+  }
   if (e == hipSuccess)
     e = hipMemcpy2DAsync(xs, size_t(S * esz), io.x, size_t(io.x_bc * esz), size_t(S * esz),
                          size_t(xrows), hipMemcpyDeviceToDevice, s);
@@ -372,10 +413,12 @@ hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char*
   if (e == hipSuccess && y_far)
     e = hipMemcpy2DAsync(io.y, size_t(io.y_bc * esz), ys, size_t(So * esz), size_t(So * esz),
                          size_t(yrows), hipMemcpyDeviceToDevice, s);
-  for (void* p : {xs, ys}) {
-    if (!p) continue;
-    const hipError_t f = hipFreeAsync(p, s);
-    if (e == hipSuccess) e = f;
+  if (own) {
+    for (void* p : {xs, ys}) {
+      if (!p) continue;
+      const hipError_t f = hipFreeAsync(p, s);
+      if (e == hipSuccess) e = f;
+    }
   }
   return e;
 }

@@ -1363,19 +1363,22 @@ hipError_t gemm_dispatch_taps(const ConvGeom& g, const GemmConfig& c, const Conv
 
 }  // namespace
 
+bool gemm_step_needs_staging(const ConvGeom& g, const StepIO& io) {
+  // even rows are read as aligned pixel pairs, and the staging reads use
+  // 32-bit buffer offsets over the reachable part of x
+  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  return (g.W % 2 == 0 &&
+          ((reinterpret_cast<uintptr_t>(io.x) % (2 * esz)) != 0 || (io.x_bc % 2) != 0)) ||
+         ((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * int64_t(esz) >= (int64_t(1) << 31);
+}
+
 hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                                  const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   GemmConfig c;
   if (!gemm_config(g, g.cfg, &c)) return hipErrorInvalidValue;
-  // Even-width rows are staged two pixels per load; a frame pointer or plane
-  // stride that breaks that alignment takes the direct kernel (same ring).
-  const size_t esz = g.dtype == CO_BF16 ? 2 : 4;
-  // even rows are staged as aligned pixel pairs, and the staging reads use
-  // 32-bit buffer offsets over the reachable part of x
-  if ((g.W % 2 == 0 &&
-       ((reinterpret_cast<uintptr_t>(io.x) % (2 * esz)) != 0 || (io.x_bc % 2) != 0)) ||
-      ((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * int64_t(esz) >= (int64_t(1) << 31))
-    return launch_conv_step_staged(g, L, state, io, plan, s);
+  // A frame pointer or plane stride that breaks the pixel-pair alignment, or
+  // a frame past 32-bit reach, is copied into a contiguous buffer first.
+  if (gemm_step_needs_staging(g, io)) return launch_conv_step_staged(g, L, state, io, plan, s);
   if (g.kH == 3 && g.kW == 3) return gemm_dispatch_taps<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return gemm_dispatch_taps<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;

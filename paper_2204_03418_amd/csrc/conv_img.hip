@@ -480,19 +480,24 @@ hipError_t img_dispatch(const ConvGeom& g, const ImgConfig& c, const ConvLayout&
 
 }  // namespace
 
-hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* state,
-                                const StepIO& io, const co_step_plan& plan, hipStream_t s) {
+bool img_step_needs_staging(const ConvGeom& g, const StepIO& io) {
   ImgConfig c;
-  if (!img_config(g, &c)) return hipErrorInvalidValue;
-  // 32-bit offsets: the reachable part of x and the ring below 2^31 bytes;
+  if (!img_config(g, &c)) return false;
+  // 32-bit offsets: the reachable part of x and of y below 2^31 bytes;
   // pixel pairs need 4-byte aligned rows
   const int64_t x_extent = ((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * 2;
   const bool pair_ok = !c.pair || ((reinterpret_cast<uintptr_t>(io.x) & 3) == 0 &&
                                    (io.x_bc & 1) == 0);
   const int64_t y_extent = ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * 2;
+  return x_extent >= (int64_t(1) << 31) || (io.y && y_extent >= (int64_t(1) << 31)) || !pair_ok;
+}
+
+hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* state,
+                                const StepIO& io, const co_step_plan& plan, hipStream_t s) {
+  ImgConfig c;
+  if (!img_config(g, &c)) return hipErrorInvalidValue;
   if (int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
-  if (x_extent >= (int64_t(1) << 31) || (io.y && y_extent >= (int64_t(1) << 31)) || !pair_ok)
-    return launch_conv_step_staged(g, L, state, io, plan, s);
+  if (img_step_needs_staging(g, io)) return launch_conv_step_staged(g, L, state, io, plan, s);
   if (g.kH == 3 && g.kW == 3) return img_dispatch<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return img_dispatch<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;

@@ -797,6 +797,12 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
 
 }  // namespace
 
+bool reg_step_needs_staging(const ConvGeom& g, const StepIO& io) {
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  return ((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz >= (int64_t(1) << 31) ||
+         (io.y && ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31));
+}
+
 hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* state,
                                 const StepIO& io, const co_step_plan& plan, hipStream_t s) {
   RegConfig c;
@@ -804,13 +810,10 @@ hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* st
   // 32-bit buffer offsets: the packed weights, the tile count and the ring
   // are held in reach when the algorithm is chosen; the reach of a frame
   // depends on its plane and output strides
-  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   if (L.weight_bytes >= (int64_t(1) << 30) || int64_t(c.m_frags) * c.n_frags >= (int64_t(1) << 30) ||
       int64_t(g.R) * L.ring_slot_elems * 4 >= (int64_t(1) << 31))
     return hipErrorInvalidValue;
-  if (((int64_t(g.B) * g.Cin - 1) * io.x_bc + g.S()) * esz >= (int64_t(1) << 31) ||
-      (io.y && ((int64_t(g.B) * g.Cout - 1) * io.y_bc + g.So()) * esz >= (int64_t(1) << 31)))
-    return launch_conv_step_staged(g, L, state, io, plan, s);
+  if (reg_step_needs_staging(g, io)) return launch_conv_step_staged(g, L, state, io, plan, s);
   switch (c.id) {
     case 0: return reg_launch<float, 4, 1, 16, 1>(g, c, L, state, io, plan, s);
     case 1: return reg_launch<float, 2, 1, 32, 1>(g, c, L, state, io, plan, s);

@@ -11,11 +11,15 @@ namespace coinf {
 // element strides between consecutive (batch, channel) planes: S for a single
 // frame (B, C, S1, S2), T*S when the frame is read in place from a clip
 // (B, C, T, S1, S2).
+// ws / ws_bytes: caller-provided device scratch for a step that has to stage
+// its frame (see launch_conv_step_staged); null lets the step allocate.
 struct StepIO {
   const void* x;
   int64_t x_bc;
   void* y;
   int64_t y_bc;
+  void* ws = nullptr;
+  int64_t ws_bytes = 0;
 };
 
 // One convolution step with the handle's algorithm.  zero_frame runs an
@@ -64,8 +68,19 @@ hipError_t launch_conv_step_direct(const ConvGeom& g, const ConvLayout& L, char*
 // 2^31 bytes, or a misaligned input): the frame is copied into a contiguous
 // stream-ordered buffer, stepped, and an output staged the same way is
 // copied back.  Fails when the frame is already contiguous and aligned.
+// With io.ws set the copies live there (io.ws_bytes must cover
+// conv_step_staging_bytes) and nothing is allocated.
 hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char* state,
                                    const StepIO& io, const co_step_plan& plan, hipStream_t stream);
+// Device bytes a step with this frame and output (io.x, io.x_bc, io.y,
+// io.y_bc) needs for staging: 0 when the handle's kernel reads the frame in
+// place.  Each staged buffer is rounded up to 256 bytes.
+int64_t conv_step_staging_bytes(const ConvGeom& g, const StepIO& io);
+// Whether the GEMM-family step kernels read this frame in place (false) or
+// have it staged (true).
+bool gemm_step_needs_staging(const ConvGeom& g, const StepIO& io);
+bool reg_step_needs_staging(const ConvGeom& g, const StepIO& io);
+bool img_step_needs_staging(const ConvGeom& g, const StepIO& io);
 // Persistent forward_steps of small direct layers (same conventions as the
 // depthwise one): temporal stride 1 and dilation 1, kT <= 4 and
 // C_in/G * kH * kW <= 16.
