@@ -51,6 +51,11 @@
  *
  * Threads.  A handle is not thread-safe; distinct handles are independent.
  * Concurrent calls on one state buffer race.
+ *
+ * Handles.  The library keeps a registry of the handles it has made and not
+ * yet destroyed: a call with a destroyed handle, a second destroy, or a
+ * handle of another kind returns CO_EINVAL.  A step counter stays below
+ * 2^62: a call that would pass it returns CO_EINVAL.
  */
 #ifndef COINF_H
 #define COINF_H
@@ -261,6 +266,17 @@ co_status co_conv_clean_state(co_conv_handle* h, void* stream);
 co_status co_conv_get_steps(const co_conv_handle* h, int64_t* n);
 
 /*
+ * Output frames a forward_steps call over T frames (plus padding[0] end
+ * frames when pad_end) emits when it starts at step counter n0: the steps
+ * m in [n0, n0 + count) with m >= delay and (m - delay) mod stride[0] == 0
+ * (Principles 4-5: the first output after `delay` steps, then one every
+ * temporal stride).  With n0 = co_conv_get_steps of a handle, the capacity
+ * co_conv_forward_steps needs.  Host-only.
+ */
+co_status co_conv_out_frames(const co_conv_desc* desc, int64_t n0, int32_t T, int32_t pad_end,
+                             int32_t* n_out);
+
+/*
  * Resume from a state buffer that co_conv_init_state prepared for the same
  * descriptor, after its step-counter value `n` (e.g. a copy saved mid-stream).
  * Nothing is zeroed or re-packed.  Reads the state header back synchronously;
@@ -276,8 +292,17 @@ co_status co_conv_destroy(co_conv_handle* h);
 const char* co_conv_algo_name(const co_conv_handle* h);
 
 /*
+ * Continual pooling (section 3.2, pooling; Principles 1-5).  The receptive
+ * field f = dilation[0] (kernel[0] - 1) + 1 and the delay f - padding[0] - 1
+ * follow Principle 4 as for convolutions.  Each arriving frame is reduced
+ * spatially once; the state keeps the last f reduced frames (a FIFO of
+ * fifo_slots float32 frames with a validity flag each), and an emitting step
+ * reduces the window's frames over time.  Layouts, ownership, streams,
+ * status and update_state are those of the convolution calls above.
+ *
  * Pool descriptor (Principle 1: nn.AvgPoolNd / nn.MaxPoolNd arguments;
- * stride must be given explicitly, ceil_mode is not supported).  Padding on
+ * stride must be given explicitly, ceil_mode is not supported).  An input
+ * frame (B x C x S1 x S2 elements) must stay below 2^31 bytes (CO_EINVAL).  Padding on
  * each axis is at most kernel/2 as in PyTorch; dilation is only allowed for
  * CO_POOL_MAX.  Average pooling counts pads in the divisor when
  * count_include_pad is set (PyTorch's default); maximum pooling ignores pads.
@@ -317,18 +342,32 @@ typedef struct co_pool_plan {
 
 typedef struct co_pool_handle co_pool_handle;
 
+/* Receptive field, delay (Principle 4), output frame size and state bytes of
+ * a descriptor; CO_EINVAL / CO_ENOTSUP as co_conv_query.  Host-only. */
 co_status co_pool_query(const co_pool_desc* desc, co_pool_info* info);
+
+/* The schedule of step n (Principles 3-5): whether it emits, which output,
+ * the FIFO slot the arriving frame takes and the slots the window reads.
+ * Host-only. */
 co_status co_pool_plan_step(const co_pool_desc* desc, int64_t n, co_pool_plan* plan);
 
-/* Clean state over a caller-allocated buffer of info.state_bytes bytes. */
+/* Clean state (Principle 3) over a caller-allocated buffer of
+ * info.state_bytes bytes: the header is written, the FIFO marked empty.
+ * CO_ESTATE when the buffer is too small. */
 co_status co_pool_init_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
                              void* stream, co_pool_handle** out);
 
-/* forward_step of a continual pool: x_t (B, C, S1, S2) -> y_t (B, C, So1, So2). */
+/* forward_step of a continual pool (Principle 2): x_t (B, C, S1, S2) ->
+ * y_t (B, C, So1, So2), written when the step emits (CO_OK), else CO_EMPTY
+ * with y_t untouched.  Average pools divide by the window volume (pads
+ * counted, count_include_pad) or by the valid positions; maximum pools skip
+ * pads.  update_state = 0 neither stores x_t nor advances the counter. */
 co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
                                int32_t update_state, void* stream);
 
-/* forward_steps of a continual pool; same conventions as co_conv_forward_steps. */
+/* forward_steps of a continual pool (Principle 2; pad_end appends padding[0]
+ * pad frames as at the end of Example 1's clip); same conventions as
+ * co_conv_forward_steps. */
 co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, void* y,
                                 int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                                 void* stream, int32_t* n_out);
@@ -337,15 +376,25 @@ co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, voi
 co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused);
 
-/* Clip-mode pooling with symmetric temporal padding; stateless. */
+/* forward (Principle 2, clip mode; Principle 1: the nn pool's result):
+ * pooling of x (B, C, T, S1, S2) with symmetric temporal padding into
+ * y (B, C, T_out, So1, So2); stateless. */
 co_status co_pool_forward(const co_pool_desc* desc, const void* x, int32_t T, void* y,
                           void* stream);
+/* Number of T_out frames co_pool_forward produces for a clip of T frames. */
 co_status co_pool_clip_frames(const co_pool_desc* desc, int32_t T, int32_t* t_out);
 
+/* clean_state (Principle 3): the next step is step 0; no device work. */
 co_status co_pool_clean_state(co_pool_handle* h, void* stream);
+/* Step counter n of the handle. */
 co_status co_pool_get_steps(const co_pool_handle* h, int64_t* n);
+/* As co_conv_out_frames (Principles 4-5), for co_pool_forward_steps. */
+co_status co_pool_out_frames(const co_pool_desc* desc, int64_t n0, int32_t T, int32_t pad_end,
+                             int32_t* n_out);
+/* Resume from a copied state after step n; as co_conv_attach_state. */
 co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
                                int64_t n, void* stream, co_pool_handle** out);
+/* Free the host handle (the state buffer stays the caller's). */
 co_status co_pool_destroy(co_pool_handle* h);
 
 /*
@@ -458,6 +507,21 @@ co_status co_add_frames(const void* a, const void* x, void* y, int32_t rows, int
 co_status co_delay_clean_state(co_delay_handle* h, void* stream);
 co_status co_delay_get_steps(const co_delay_handle* h, int64_t* n);
 co_status co_delay_destroy(co_delay_handle* h);
+
+/*
+ * Alignment of a residual connection (section 3.1.1, Principle 7) around a
+ * module of temporal receptive field f, stride s and padding p whose own
+ * delay is module_delay: the input joins the module's output on the centre
+ * of its receptive field, so the residual branch is delayed by
+ * *res_delay = floor((f - 1) / 2) steps; in clip mode the input's first and
+ * last *shrink = *res_delay - p frames have no module output to join;
+ * the whole's delay is *delay = max(module_delay, *res_delay) (a step is
+ * empty while either branch is).  CO_EINVAL unless s == 1 and
+ * 0 <= 2p <= f - 1 (a longer output than input cannot be joined).
+ * Host-only.
+ */
+co_status co_residual_align(int64_t f, int64_t s, int64_t p, int64_t module_delay,
+                            int64_t* res_delay, int64_t* shrink, int64_t* delay);
 
 /*
  * Accumulated receptive field and delay of a chain of n layers (Principle 6),

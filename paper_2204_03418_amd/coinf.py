@@ -107,6 +107,7 @@ co_conv_steps_fused = _sig("co_conv_steps_fused", i32, [vp, i32, i32, pi32])
 co_conv_forward_steps_noalloc = _sig("co_conv_forward_steps_noalloc", i32,
                                      [vp, vp, i32, vp, i32, i32, i32, vp, pi32])
 co_conv_scratch_bytes = _sig("co_conv_scratch_bytes", i32, [pi64])
+co_conv_out_frames = _sig("co_conv_out_frames", i32, [CD, i64, i32, i32, pi32])
 co_pool_query = _sig("co_pool_query", i32, [PD, PI])
 co_pool_plan_step = _sig("co_pool_plan_step", i32, [PD, i64, ctypes.POINTER(PoolPlan)])
 co_pool_init_state = _sig("co_pool_init_state", i32, [PD, vp, i64, vp, pvp])
@@ -115,6 +116,7 @@ co_pool_forward_steps = _sig("co_pool_forward_steps", i32,
                              [vp, vp, i32, vp, i32, i32, i32, vp, pi32])
 co_pool_forward = _sig("co_pool_forward", i32, [PD, vp, i32, vp, vp])
 co_pool_steps_fused = _sig("co_pool_steps_fused", i32, [vp, i32, i32, pi32])
+co_pool_out_frames = _sig("co_pool_out_frames", i32, [PD, i64, i32, i32, pi32])
 co_pool_clip_frames = _sig("co_pool_clip_frames", i32, [PD, i32, pi32])
 co_pool_clean_state = _sig("co_pool_clean_state", i32, [vp, vp])
 co_pool_get_steps = _sig("co_pool_get_steps", i32, [vp, pi64])
@@ -138,6 +140,7 @@ co_convpool_forward_step = _sig("co_convpool_forward_step", i32, [vp, vp, vp, i3
 co_convpool_forward_steps = _sig("co_convpool_forward_steps", i32,
                                  [vp, vp, i32, vp, i32, i32, vp, pi32])
 co_convpool_destroy = _sig("co_convpool_destroy", i32, [vp])
+co_residual_align = _sig("co_residual_align", i32, [i64, i64, i64, i64, pi64, pi64, pi64])
 
 
 class CoinfError(RuntimeError):
@@ -239,17 +242,6 @@ def _need(t, dtype, shape, what):
         raise ValueError(f"{what} has shape {tuple(t.shape)}, expected {tuple(shape)}")
     if not t.is_contiguous():
         raise ValueError(f"{what} must be contiguous")
-
-
-def _n_emit(n0, count, d, s):
-    """Non-empty steps among steps n0 .. n0 + count - 1 (Principles 4-5: step n
-    emits iff n >= d and (n - d) mod s == 0)."""
-    lo = max(n0, d)
-    hi = n0 + count
-    if hi <= lo:
-        return 0
-    first = lo + (-(lo - d)) % s
-    return 0 if first >= hi else (hi - 1 - first) // s + 1
 
 
 class CoConv:
@@ -354,8 +346,7 @@ class CoConv:
         The result is contiguous, sized to the frames the call emits."""
         T = x.shape[2]
         _need(x, self.torch_dtype, (self.batch, self.in_channels, T) + self.in_size, "x")
-        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
-                      self.desc.stride[0])
+        cap = self.out_frames(T, pad_end)
         y = torch.empty((self.batch, self.out_channels, cap) + self.out_size,
                         dtype=self.torch_dtype, device=x.device)
         n = i32()
@@ -366,12 +357,15 @@ class CoConv:
             return None
         return y[:, :, :n.value]
 
+    def out_frames(self, T, pad_end=False):
+        """Frames forward_steps over T frames emits from the current step."""
+        return conv_out_frames(self.desc, self.steps, T, pad_end)
+
     def steps_fused(self, T, pad_end=False):
         """True when forward_steps over T frames runs as one persistent launch."""
-        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
-                      self.desc.stride[0])
         f = i32()
-        check(co_conv_steps_fused(self.handle, T, cap, ctypes.byref(f)), "co_conv_steps_fused")
+        check(co_conv_steps_fused(self.handle, T, self.out_frames(T, pad_end), ctypes.byref(f)),
+              "co_conv_steps_fused")
         return bool(f.value)
 
     def forward(self, x):
@@ -380,6 +374,35 @@ class CoConv:
 
     def clean_state(self):
         check(co_conv_clean_state(self.handle, _stream()), "co_conv_clean_state")
+
+
+def conv_out_frames(desc, n0, T, pad_end=False):
+    """Frames forward_steps over T frames emits from step counter n0
+    (co_conv_out_frames)."""
+    n = i32()
+    check(co_conv_out_frames(ctypes.byref(desc), int(n0), int(T), 1 if pad_end else 0,
+                             ctypes.byref(n)), "co_conv_out_frames")
+    return n.value
+
+
+def pool_out_frames(desc, n0, T, pad_end=False):
+    """Frames a pool's forward_steps over T frames emits from step counter n0
+    (co_pool_out_frames)."""
+    n = i32()
+    check(co_pool_out_frames(ctypes.byref(desc), int(n0), int(T), 1 if pad_end else 0,
+                             ctypes.byref(n)), "co_pool_out_frames")
+    return n.value
+
+
+def residual_align(f, s, p, module_delay):
+    """(residual delay, clip shrink, delay of the whole) of a centred residual
+    (co_residual_align); None when the clip shapes cannot be joined."""
+    d_res, shrink, delay = i64(), i64(), i64()
+    st = co_residual_align(int(f), int(s), int(p), int(module_delay), ctypes.byref(d_res),
+                           ctypes.byref(shrink), ctypes.byref(delay))
+    if st != CO_OK:
+        return None
+    return d_res.value, shrink.value, delay.value
 
 
 def conv_forward(desc, weight, bias, x):
@@ -474,8 +497,7 @@ class CoPool:
     def forward_steps(self, x, pad_end=False, update_state=True):
         T = x.shape[2]
         _need(x, self.torch_dtype, (self.batch, self.channels, T) + self.in_size, "x")
-        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
-                      self.desc.stride[0])
+        cap = self.out_frames(T, pad_end)
         y = torch.empty((self.batch, self.channels, cap) + self.out_size,
                         dtype=self.torch_dtype, device=x.device)
         n = i32()
@@ -486,12 +508,15 @@ class CoPool:
             return None
         return y[:, :, :n.value]
 
+    def out_frames(self, T, pad_end=False):
+        """Frames forward_steps over T frames emits from the current step."""
+        return pool_out_frames(self.desc, self.steps, T, pad_end)
+
     def steps_fused(self, T, pad_end=False):
         """True when forward_steps over T frames runs as one persistent launch."""
-        cap = _n_emit(self.steps, T + (self.desc.padding[0] if pad_end else 0), self.delay,
-                      self.desc.stride[0])
         f = i32()
-        check(co_pool_steps_fused(self.handle, T, cap, ctypes.byref(f)), "co_pool_steps_fused")
+        check(co_pool_steps_fused(self.handle, T, self.out_frames(T, pad_end), ctypes.byref(f)),
+              "co_pool_steps_fused")
         return bool(f.value)
 
     def forward(self, x):
@@ -679,8 +704,8 @@ class ConvPool:
         T = x.shape[2]
         c, p = self.conv, self.pool
         _need(x, c.torch_dtype, (c.batch, c.in_channels, T) + c.in_size, "x")
-        n_c = _n_emit(c.steps, T, c.delay, c.t_stride)
-        cap = _n_emit(p.steps, n_c, p.delay, p.t_stride)
+        # the pool steps once per emitted convolution frame
+        cap = pool_out_frames(p.desc, p.steps, conv_out_frames(c.desc, c.steps, T))
         z = self._out(cap, x.device)
         n = i32()
         check(co_convpool_forward_steps(self.handle, _ptr(x), T, _ptr(z), cap,
@@ -772,18 +797,21 @@ class Residual:
     def __init__(self, module, residual_shrink=False):
         if module.t_stride != 1:
             raise ValueError("residual connections need temporal stride 1")
-        f, p = module.receptive_field, module.t_padding
+        al = residual_align(module.receptive_field, module.t_stride, module.t_padding,
+                            module.delay)
+        if al is None:
+            raise ValueError("clip shapes differ: the module's temporal padding exceeds "
+                             "(f - 1) / 2")
         self.module = module
-        self.d_res = (f - 1) // 2
-        self.shrink = self.d_res - p
-        if self.shrink < 0 or (self.shrink > 0 and not residual_shrink):
+        self.d_res, self.shrink, self._delay = al
+        if self.shrink > 0 and not residual_shrink:
             raise ValueError("clip shapes differ: give the module padding (f - 1) / 2 or "
                              "residual_shrink=True")
         self.line = CoDelay(self.d_res, batch=module.batch, channels=module.out_channels,
                             in_size=module.out_size, dtype=module.torch_dtype,
                             device=module.state.device)
 
-    delay = property(lambda self: max(self.module.delay, self.d_res))
+    delay = property(lambda self: self._delay)
     receptive_field = property(lambda self: self.module.receptive_field)
     t_stride = property(lambda self: 1)
     t_padding = property(lambda self: self.module.t_padding)

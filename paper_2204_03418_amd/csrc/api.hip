@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <mutex>
 #include <new>
+#include <unordered_map>
 
 #include "device.hpp"
 #include "launch.hpp"
@@ -49,6 +50,40 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 // The persistent direct kernel indexes y with 64-bit offsets; its element
 // index per (stream, channel) plane stays 32-bit.
 co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_EHIP; }
+
+// Live handles, by kind.  Every entry point checks its handle here, so a
+// destroyed handle, a second destroy, or a handle of another kind returns
+// CO_EINVAL without touching freed memory.
+enum class HKind : uint8_t { Conv, Pool, ConvPool, Delay };
+std::mutex g_live_mu;
+std::unordered_map<const void*, HKind>& live_map() {
+  static auto* m = new std::unordered_map<const void*, HKind>();  // kept past exit
+  return *m;
+}
+
+bool live(const void* h, HKind k) {
+  if (!h) return false;
+  std::lock_guard<std::mutex> lock(g_live_mu);
+  const auto it = live_map().find(h);
+  return it != live_map().end() && it->second == k;
+}
+
+template <typename H>
+co_status publish(H* h, HKind k, H** out) {
+  std::lock_guard<std::mutex> lock(g_live_mu);
+  live_map()[h] = k;
+  *out = h;
+  return CO_OK;
+}
+
+// Removes a live handle; false when it was not live (already destroyed).
+bool retire(const void* h, HKind k) {
+  std::lock_guard<std::mutex> lock(g_live_mu);
+  const auto it = live_map().find(h);
+  if (h == nullptr || it == live_map().end() || it->second != k) return false;
+  live_map().erase(it);
+  return true;
+}
 
 bool any_tap(const co_step_plan& p) {
   for (int j = 0; j < p.n_taps; ++j)
@@ -125,10 +160,11 @@ struct Scratch {
 co_status conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, void* y,
                              int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                              hipStream_t s, int32_t* n_out, const Scratch* sc) {
-  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (!live(h, HKind::Conv) || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
   if (T > 0 && !x) return CO_EINVAL;
   const ConvGeom& g = h->g;
   const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  if (count > kMaxSteps - h->n) return CO_EINVAL;
   const int64_t n_emit = conv_emissions(g, h->n, count);
   if (n_emit > y_cap_frames) return CO_EINVAL;
   if (n_emit > 0 && !y) return CO_EINVAL;
@@ -255,7 +291,7 @@ co_status co_conv_query(const co_conv_desc* desc, co_conv_info* info) {
 
 co_status co_conv_plan_step(const co_conv_desc* desc, int64_t n, int32_t update_state,
                             co_step_plan* plan) {
-  if (!plan || n < 0) return CO_EINVAL;
+  if (!plan || n < 0 || n >= kMaxSteps) return CO_EINVAL;
   ConvGeom g;
   const co_status st = conv_geom(desc, &g);
   if (st != CO_OK) return st;
@@ -281,13 +317,12 @@ co_status co_conv_init_state(const co_conv_desc* desc, const void* weight, const
     delete h;
     return st;
   }
-  *out = h;
-  return CO_OK;
+  return publish(h, HKind::Conv, out);
 }
 
 co_status co_conv_forward_step(co_conv_handle* h, const void* x_t, void* y_t,
                                int32_t update_state, void* stream) {
-  if (!h || !x_t) return CO_EINVAL;
+  if (!live(h, HKind::Conv) || !x_t || h->n >= kMaxSteps) return CO_EINVAL;
   co_step_plan plan;
   conv_plan(h->g, h->n, update_state != 0, &plan);
   if (plan.emit && !y_t) return CO_EINVAL;
@@ -311,7 +346,7 @@ co_status co_conv_forward_steps(co_conv_handle* h, const void* x, int32_t T, voi
 co_status co_conv_forward_steps_noalloc(co_conv_handle* h, const void* x, int32_t T, void* y,
                                         int32_t y_cap_frames, int32_t pad_end,
                                         int32_t update_state, void* stream, int32_t* n_out) {
-  if (!h) return CO_EINVAL;
+  if (!live(h, HKind::Conv)) return CO_EINVAL;
   void* p = nullptr;
   const co_status st = scratch_address(as_stream(stream), &p);
   if (st != CO_OK) return st;
@@ -328,7 +363,7 @@ co_status co_conv_scratch_bytes(int64_t* bytes) {
 
 co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused) {
-  if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
+  if (!live(h, HKind::Conv) || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
   const ConvGeom& g = h->g;
   // (the GEMM family also needs 4-byte aligned pixel pairs in x; an
   // allocation from the caching allocator always is)
@@ -366,7 +401,7 @@ co_status co_conv_forward(const co_conv_desc* desc, const void* weight, const vo
 
 co_status co_conv_clean_state(co_conv_handle* h, void* stream) {
   (void)stream;
-  if (!h) return CO_EINVAL;
+  if (!live(h, HKind::Conv)) return CO_EINVAL;
   // Every partial sum is started by the first real tap of its output before
   // anything reads it, so a clean state needs no device work.
   h->n = 0;
@@ -374,14 +409,26 @@ co_status co_conv_clean_state(co_conv_handle* h, void* stream) {
 }
 
 co_status co_conv_get_steps(const co_conv_handle* h, int64_t* n) {
-  if (!h || !n) return CO_EINVAL;
+  if (!live(h, HKind::Conv) || !n) return CO_EINVAL;
   *n = h->n;
+  return CO_OK;
+}
+
+co_status co_conv_out_frames(const co_conv_desc* desc, int64_t n0, int32_t T, int32_t pad_end,
+                             int32_t* n_out) {
+  if (!n_out || n0 < 0 || T < 0) return CO_EINVAL;
+  ConvGeom g;
+  const co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  if (n0 > kMaxSteps - count) return CO_EINVAL;
+  *n_out = int32_t(conv_emissions(g, n0, count));
   return CO_OK;
 }
 
 co_status co_conv_attach_state(const co_conv_desc* desc, void* state, int64_t state_bytes,
                                int64_t n, void* stream, co_conv_handle** out) {
-  if (!out || !state || n < 0) return CO_EINVAL;
+  if (!out || !state || n < 0 || n > kMaxSteps) return CO_EINVAL;
   ConvGeom g;
   co_status st = conv_geom(desc, &g);
   if (st != CO_OK) return st;
@@ -395,18 +442,17 @@ co_status co_conv_attach_state(const co_conv_desc* desc, void* state, int64_t st
     return CO_ESTATE;
   co_conv_handle* h = new (std::nothrow) co_conv_handle{g, L, static_cast<char*>(state), n};
   if (!h) return CO_EINVAL;
-  *out = h;
-  return CO_OK;
+  return publish(h, HKind::Conv, out);
 }
 
 co_status co_conv_destroy(co_conv_handle* h) {
-  if (!h) return CO_EINVAL;
+  if (!retire(h, HKind::Conv)) return CO_EINVAL;
   delete h;
   return CO_OK;
 }
 
 const char* co_conv_algo_name(const co_conv_handle* h) {
-  if (!h) return "none";
+  if (!live(h, HKind::Conv)) return "none";
   switch (h->g.algo) {
     case CO_ALGO_DEPTHWISE: return "depthwise";
     case CO_ALGO_GEMM: return h->g.dtype == CO_BF16 ? "gemm_bf16" : "gemm_f32";
@@ -435,7 +481,7 @@ co_status co_pool_query(const co_pool_desc* desc, co_pool_info* info) {
 }
 
 co_status co_pool_plan_step(const co_pool_desc* desc, int64_t n, co_pool_plan* plan) {
-  if (!plan || n < 0) return CO_EINVAL;
+  if (!plan || n < 0 || n >= kMaxSteps) return CO_EINVAL;
   PoolGeom g;
   const co_status st = pool_geom(desc, &g);
   if (st != CO_OK) return st;
@@ -459,13 +505,12 @@ co_status co_pool_init_state(const co_pool_desc* desc, void* state, int64_t stat
     delete h;
     return st;
   }
-  *out = h;
-  return CO_OK;
+  return publish(h, HKind::Pool, out);
 }
 
 co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
                                int32_t update_state, void* stream) {
-  if (!h || !x_t) return CO_EINVAL;
+  if (!live(h, HKind::Pool) || !x_t || h->n >= kMaxSteps) return CO_EINVAL;
   co_pool_plan plan;
   pool_plan(h->g, h->n, &plan);
   if (plan.emit && !y_t) return CO_EINVAL;
@@ -481,7 +526,7 @@ co_status co_pool_forward_step(co_pool_handle* h, const void* x_t, void* y_t,
 
 co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused) {
-  if (!h || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
+  if (!live(h, HKind::Pool) || !fused || T < 0 || y_cap_frames < 0) return CO_EINVAL;
   *fused = pool_steps_supported(h->g, T, y_cap_frames) ? 1 : 0;
   return CO_OK;
 }
@@ -489,10 +534,11 @@ co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_
 co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, void* y,
                                 int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                                 void* stream, int32_t* n_out) {
-  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (!live(h, HKind::Pool) || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
   if (T > 0 && !x) return CO_EINVAL;
   const PoolGeom& g = h->g;
   const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  if (count > kMaxSteps - h->n) return CO_EINVAL;
   const int64_t n_emit = pool_emissions(g, h->n, count);
   if (n_emit > y_cap_frames) return CO_EINVAL;
   if (n_emit > 0 && !y) return CO_EINVAL;
@@ -584,21 +630,33 @@ co_status co_pool_forward(const co_pool_desc* desc, const void* x, int32_t T, vo
 
 co_status co_pool_clean_state(co_pool_handle* h, void* stream) {
   (void)stream;
-  if (!h) return CO_EINVAL;
+  if (!live(h, HKind::Pool)) return CO_EINVAL;
   // The FIFO is only read for frames written since the last clean state.
   h->n = 0;
   return CO_OK;
 }
 
 co_status co_pool_get_steps(const co_pool_handle* h, int64_t* n) {
-  if (!h || !n) return CO_EINVAL;
+  if (!live(h, HKind::Pool) || !n) return CO_EINVAL;
   *n = h->n;
+  return CO_OK;
+}
+
+co_status co_pool_out_frames(const co_pool_desc* desc, int64_t n0, int32_t T, int32_t pad_end,
+                             int32_t* n_out) {
+  if (!n_out || n0 < 0 || T < 0) return CO_EINVAL;
+  PoolGeom g;
+  const co_status st = pool_geom(desc, &g);
+  if (st != CO_OK) return st;
+  const int64_t count = int64_t(T) + (pad_end ? g.pT : 0);
+  if (n0 > kMaxSteps - count) return CO_EINVAL;
+  *n_out = int32_t(pool_emissions(g, n0, count));
   return CO_OK;
 }
 
 co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t state_bytes,
                                int64_t n, void* stream, co_pool_handle** out) {
-  if (!out || !state || n < 0) return CO_EINVAL;
+  if (!out || !state || n < 0 || n > kMaxSteps) return CO_EINVAL;
   PoolGeom g;
   co_status st = pool_geom(desc, &g);
   if (st != CO_OK) return st;
@@ -612,12 +670,11 @@ co_status co_pool_attach_state(const co_pool_desc* desc, void* state, int64_t st
     return CO_ESTATE;
   co_pool_handle* h = new (std::nothrow) co_pool_handle{g, L, static_cast<char*>(state), n};
   if (!h) return CO_EINVAL;
-  *out = h;
-  return CO_OK;
+  return publish(h, HKind::Pool, out);
 }
 
 co_status co_pool_destroy(co_pool_handle* h) {
-  if (!h) return CO_EINVAL;
+  if (!retire(h, HKind::Pool)) return CO_EINVAL;
   delete h;
   return CO_OK;
 }
@@ -654,13 +711,12 @@ co_status co_delay_init_state(const co_delay_desc* desc, void* state, int64_t st
     delete h;
     return st;
   }
-  *out = h;
-  return CO_OK;
+  return publish(h, HKind::Delay, out);
 }
 
 co_status co_delay_forward_step(co_delay_handle* h, const void* x_t, void* y_t,
                                 int32_t update_state, void* stream) {
-  if (!h || !x_t) return CO_EINVAL;
+  if (!live(h, HKind::Delay) || !x_t || h->n >= kMaxSteps) return CO_EINVAL;
   const bool emit = h->n >= h->g.d && y_t;
   if (emit || (update_state && h->g.d > 0)) {
     const co_status st = hip_status(launch_delay_step(h->g, h->state, x_t, nullptr, y_t, h->n,
@@ -675,7 +731,7 @@ co_status co_delay_forward_step(co_delay_handle* h, const void* x_t, void* y_t,
 
 co_status co_delay_add_step(co_delay_handle* h, const void* x_t, const void* a_t, void* y_t,
                             int32_t update_state, void* stream) {
-  if (!h || !x_t) return CO_EINVAL;
+  if (!live(h, HKind::Delay) || !x_t || h->n >= kMaxSteps) return CO_EINVAL;
   const bool emit = h->n >= h->g.d;
   if (emit && (!a_t || !y_t)) return CO_EINVAL;
   if (emit || (update_state && h->g.d > 0)) {
@@ -691,8 +747,9 @@ co_status co_delay_add_step(co_delay_handle* h, const void* x_t, const void* a_t
 co_status co_delay_forward_steps(co_delay_handle* h, const void* x, int32_t T, void* y,
                                  int32_t y_cap_frames, int32_t update_state, void* stream,
                                  int32_t* n_out) {
-  if (!h || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (!live(h, HKind::Delay) || T < 0 || y_cap_frames < 0 || !n_out) return CO_EINVAL;
   if (T > 0 && !x) return CO_EINVAL;
+  if (T > kMaxSteps - h->n) return CO_EINVAL;
   const DelayGeom& g = h->g;
   const int64_t first = std::min<int64_t>(T, std::max<int64_t>(0, g.d - h->n));
   const int32_t nout = int32_t(T - first);
@@ -709,8 +766,9 @@ co_status co_delay_forward_steps(co_delay_handle* h, const void* x, int32_t T, v
 
 co_status co_delay_add_steps(co_delay_handle* h, const void* x, int32_t T, const void* a,
                              int32_t a_frames, void* y, int32_t update_state, void* stream) {
-  if (!h || T < 0 || a_frames < 0 || a_frames > T) return CO_EINVAL;
+  if (!live(h, HKind::Delay) || T < 0 || a_frames < 0 || a_frames > T) return CO_EINVAL;
   if (T > 0 && !x) return CO_EINVAL;
+  if (T > kMaxSteps - h->n) return CO_EINVAL;
   if (a_frames > 0 && (!a || !y)) return CO_EINVAL;
   const DelayGeom& g = h->g;
   const int64_t first = int64_t(T) - a_frames;  // step of a's first frame in this call
@@ -739,20 +797,20 @@ co_status co_add_frames(const void* a, const void* x, void* y, int32_t rows, int
 
 co_status co_delay_clean_state(co_delay_handle* h, void* stream) {
   (void)stream;
-  if (!h) return CO_EINVAL;
+  if (!live(h, HKind::Delay)) return CO_EINVAL;
   // every ring slot is written before it is read again
   h->n = 0;
   return CO_OK;
 }
 
 co_status co_delay_get_steps(const co_delay_handle* h, int64_t* n) {
-  if (!h || !n) return CO_EINVAL;
+  if (!live(h, HKind::Delay) || !n) return CO_EINVAL;
   *n = h->n;
   return CO_OK;
 }
 
 co_status co_delay_destroy(co_delay_handle* h) {
-  if (!h) return CO_EINVAL;
+  if (!retire(h, HKind::Delay)) return CO_EINVAL;
   delete h;
   return CO_OK;
 }
@@ -784,19 +842,38 @@ co_status co_chain_delay(int32_t n, const int32_t* f, const int32_t* s, const in
   return CO_OK;
 }
 
+co_status co_residual_align(int64_t f, int64_t s, int64_t p, int64_t module_delay,
+                            int64_t* res_delay, int64_t* shrink, int64_t* delay) {
+  if (!res_delay || !shrink || !delay) return CO_EINVAL;
+  if (f < 1 || s != 1 || p < 0 || 2 * p > f - 1 || module_delay < 0) return CO_EINVAL;
+  // the input joins the module's output on the centre of its receptive
+  // field: the residual branch waits (f - 1) / 2 frames (rounded down), clip
+  // mode drops the frames the module's padding does not restore, and the
+  // whole is empty while either branch is (Principle 7)
+  const int64_t c = (f - 1) / 2;
+  *res_delay = c;
+  *shrink = c - p;
+  *delay = std::max(module_delay, c);
+  return CO_OK;
+}
+
 
 // -------------------------------------------------- fused depthwise + pool
 
 co_status co_convpool_bind(co_conv_handle* conv, co_pool_handle* pool, co_convpool_handle** out) {
-  if (!conv || !pool || !out) return CO_EINVAL;
+  if (!live(conv, HKind::Conv) || !live(pool, HKind::Pool) || !out) return CO_EINVAL;
   if (!convpool_supported(conv->g, pool->g)) return CO_ENOTSUP;
   co_convpool_handle* h = new (std::nothrow) co_convpool_handle{conv, pool};
   if (!h) return CO_EINVAL;
-  *out = h;
-  return CO_OK;
+  return publish(h, HKind::ConvPool, out);
 }
 
 namespace {
+
+// A fused pair whose two handles are both still live.
+bool live_pair(const co_convpool_handle* h) {
+  return live(h, HKind::ConvPool) && live(h->conv, HKind::Conv) && live(h->pool, HKind::Pool);
+}
 
 // One fused step at the handles' counters, reading frame planes x_bc
 // elements apart; *emitted says whether z was written.
@@ -828,7 +905,7 @@ co_status convpool_step(co_convpool_handle* h, const void* x_t, int64_t x_bc, vo
 
 co_status co_convpool_forward_step(co_convpool_handle* h, const void* x_t, void* z_t,
                                    int32_t update_state, void* stream) {
-  if (!h || !x_t) return CO_EINVAL;
+  if (!live_pair(h) || !x_t || h->conv->n >= kMaxSteps) return CO_EINVAL;
   bool emitted = false;
   const co_status st = convpool_step(h, x_t, h->conv->g.S(), z_t, 1, update_state != 0,
                                      as_stream(stream), &emitted);
@@ -839,10 +916,11 @@ co_status co_convpool_forward_step(co_convpool_handle* h, const void* x_t, void*
 co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_t T, void* z,
                                     int32_t z_cap_frames, int32_t update_state, void* stream,
                                     int32_t* n_out) {
-  if (!h || T < 0 || z_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (!live_pair(h) || T < 0 || z_cap_frames < 0 || !n_out) return CO_EINVAL;
   if (T > 0 && !x) return CO_EINVAL;
   co_conv_handle* c = h->conv;
   co_pool_handle* p = h->pool;
+  if (T > kMaxSteps - c->n) return CO_EINVAL;
   // the pool steps once per emitted convolution frame
   const int64_t conv_out = conv_emissions(c->g, c->n, T);
   const int64_t n_emit = pool_emissions(p->g, p->n, conv_out);
@@ -893,7 +971,7 @@ co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_
 }
 
 co_status co_convpool_destroy(co_convpool_handle* h) {
-  if (!h) return CO_EINVAL;
+  if (!retire(h, HKind::ConvPool)) return CO_EINVAL;
   delete h;
   return CO_OK;
 }

@@ -529,8 +529,9 @@ bool convpool_supported(const ConvGeom& g, const PoolGeom& pg) {
   return g.algo == CO_ALGO_DEPTHWISE && taps && g.dtype == pg.dtype && g.B == pg.B &&
          g.Cout == pg.C && pg.H == g.Ho && pg.W == g.Wo && g.So() <= 64 && pg.kH == g.Ho &&
          pg.kW == g.Wo && pg.pH == 0 && pg.pW == 0 && pg.dH == 1 && pg.dW == 1 &&
-         pg.Ho == 1 && pg.Wo == 1 && pg.kT <= 64 &&
-         g.S() > 0;
+         pg.Ho == 1 && pg.Wo == 1 && pg.kT <= 64 && g.S() > 0 &&
+         // the step kernel addresses a frame with 32-bit buffer offsets
+         int64_t(g.B) * g.Cin * g.S() * (g.dtype == CO_BF16 ? 2 : 4) < (int64_t(1) << 31);
 }
 
 bool convpool_steps_supported(const ConvGeom& g, const PoolGeom& pg, int64_t T) {

@@ -162,12 +162,13 @@ int gemm_pick(const ConvGeom& g) {
   for (int id = 0; id < kGemmConfigs; ++id) {
     GemmConfig c;
     if (!gemm_config(g, id, &c)) continue;
-    // cycles of one wave: MFMA issue (bf16 16x16x32: 16 clk per fragment pair
+    // Cycles of one wave: MFMA issue (bf16 16x16x32: 16 clk per fragment pair
     // per 32 channels; f32 16x16x4: 4 x 32 clk per 16 channels), plus staging
-    // per chunk and the epilogue; waves beyond one per SIMD run in rounds
-    // Workgroups resident per CU (LDS, 2048 threads) and waves per SIMD; one
-    // wave per SIMD issues MFMAs at about 30 cycles each on MI355X, two or
-    // more at about 21 (bf16 16x16x32, measured).
+    // per chunk and the epilogue.  Workgroups resident per CU (LDS, 2048
+    // threads) give the waves per SIMD; the SIMD's matrix unit completes one
+    // instruction about every 30 cycles with one wave on it and every 21 with
+    // two or more (bf16 16x16x32, measured), so the resident waves of a SIMD
+    // take their turns: a round of workgroups lasts wps waves' worth.
     const int threads = 64 * c.NWM * c.NWN;
     const int64_t wg_cu = std::max<int64_t>(
         1, std::min<int64_t>(kLdsBytes / std::max<int64_t>(c.lds_bytes, 1), 2048 / threads));
@@ -177,7 +178,7 @@ int gemm_pick(const ConvGeom& g) {
                         300.0 * c.n_chunks + 100.0 * c.WM * c.WN;
     const double wgs = double(c.m_tiles) * c.n_tiles;
     const double rounds = std::ceil(wgs / (256.0 * double(wg_cu)));
-    const double cost = rounds * wave * std::max(1.0, wps) / std::max(1.0, wps);
+    const double cost = rounds * wave * std::max(1.0, wps);
     if (best < 0 || cost < best_cost) {
       best = id;
       best_cost = cost;
@@ -532,6 +533,8 @@ co_status pool_geom(const co_pool_desc* desc, PoolGeom* g) {
   if (Ho < 1 || Wo < 1) return CO_EINVAL;
   const int64_t in_frame = int64_t(d.batch) * d.channels * d.in_size[0] * d.in_size[1];
   if (in_frame > kMaxI32) return CO_EINVAL;
+  // the step kernels address a frame with 32-bit buffer offsets
+  if (in_frame * (d.dtype == CO_BF16 ? 2 : 4) >= (int64_t(1) << 31)) return CO_EINVAL;
 
   PoolGeom r{};
   r.kind = d.kind;

@@ -131,6 +131,9 @@ constexpr int kGemmConfigs = 4;
 constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)
 constexpr int kGemmStageItems = 1024;  // staging items per workgroup and chunk
 constexpr int64_t kLdsBytes = 160 * 1024;
+// Largest step counter a handle accepts: the schedule's virtual time n + pT
+// and the end n + count of a forward_steps call stay far from overflow.
+constexpr int64_t kMaxSteps = int64_t(1) << 62;
 
 // Persistent forward_steps of the LDS-tiled GEMM (bf16, temporal stride and
 // dilation 1, kT <= kStepsKT): a workgroup of kStepsNWM x kStepsNWN waves

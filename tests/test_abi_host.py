@@ -376,3 +376,119 @@ def test_delay_query_and_validation():
     assert C.co_add_frames(None, None, None, 4, 3, 0, 5, 0, C.CO_F32, None) == C.CO_OK
     assert C.co_add_frames(None, None, None, 4, 3, 4, 5, 2, C.CO_F32, None) == C.CO_EINVAL
     assert C.co_add_frames(None, None, None, 4, 0, 1, 5, 0, C.CO_F32, None) == C.CO_EINVAL
+
+
+def _oracle_count(mod, n0, T, pad_end):
+    """Outputs the oracle's sliding-window driver emits over T frames (plus
+    its end padding) after n0 earlier frames: the count is counted, not
+    computed."""
+    x = np.zeros((1, 1, n0 + T))
+    for t in range(n0):
+        mod.forward_step(x[:, :, t])
+    y = mod.forward_steps(x[:, :, n0:], pad_end=pad_end)
+    return 0 if y is None else y.shape[2]
+
+
+@pytest.mark.parametrize("k,s,p,dil", [(k, s, p, dil) for k, s, p, dil in
+                                       itertools.product((1, 2, 3, 5), (1, 2, 3), (0, 1, 2, 4),
+                                                         (1, 2))
+                                       if p <= dil * (k - 1)])
+def test_out_frames_calls_match_oracle_driver(k, s, p, dil):
+    """co_conv_out_frames / co_pool_out_frames (Principles 4-5, the capacity a
+    forward_steps call needs) against the number of outputs the oracle's
+    driver emits for the same call, from several step counters."""
+    d = desc1d(k=k, s=s, p=p, d=dil, cin=1, cout=1)
+    w = np.ones((1, 1, k))
+    for n0, T, pad_end in itertools.product((0, 1, 2, 5, 9), (0, 1, 3, 7, 12), (False, True)):
+        if n0 + T == 0:
+            continue  # no real frame at all: the oracle defines no output over padding only
+        got = C.conv_out_frames(d, n0, T, pad_end)
+        ref = _oracle_count(oracle.ContinualConv(w, None, stride=s, padding=p, dilation=dil),
+                            n0, T, pad_end)
+        assert got == ref, (k, s, p, dil, n0, T, pad_end)
+        if 2 * p <= k and dil == 1:  # PyTorch's pool padding rule
+            pd = C.pool_desc("max", 1, 1, (k,), (), (s,), (p,))
+            got = C.pool_out_frames(pd, n0, T, pad_end)
+            ref = _oracle_count(oracle.ContinualPool("max", (k,), (s,), (p,), spatial_dims=0),
+                                n0, T, pad_end)
+            assert got == ref, ("pool", k, s, p, n0, T, pad_end)
+
+
+def test_out_frames_rejects_bad_arguments():
+    d = desc1d()
+    n = C.i32()
+    assert C.co_conv_out_frames(ctypes.byref(d), -1, 4, 0, ctypes.byref(n)) == C.CO_EINVAL
+    assert C.co_conv_out_frames(ctypes.byref(d), 0, -1, 0, ctypes.byref(n)) == C.CO_EINVAL
+    assert C.co_conv_out_frames(ctypes.byref(d), (1 << 62) - 2, 4, 0,
+                                ctypes.byref(n)) == C.CO_EINVAL   # past the step limit
+    assert C.co_conv_out_frames(ctypes.byref(desc1d(p=3)), 0, 4, 0,
+                                ctypes.byref(n)) == C.CO_EINVAL   # invalid descriptor
+
+
+@pytest.mark.parametrize("k,p,dil", [(k, p, dil) for k, p, dil in
+                                     itertools.product((1, 2, 3, 4, 5, 7), range(0, 4), (1, 2))
+                                     if p <= dil * (k - 1)])
+def test_residual_align_matches_oracle_residual(k, p, dil):
+    """co_residual_align (section 3.1.1, Principle 7) against the oracle's
+    residual connection: its delay line, its clip-mode shrink, and the step
+    of its first non-empty output, counted by stepping it."""
+    f = dil * (k - 1) + 1
+    mod = oracle.ContinualConv(np.ones((1, 1, k)), None, padding=p, dilation=dil)
+    al = C.residual_align(f, 1, p, mod.delay)
+    if 2 * p > f - 1:
+        assert al is None
+        with pytest.raises(ValueError):
+            oracle.ContinualResidual(mod)
+        return
+    d_res, shrink, delay = al
+    res = oracle.ContinualResidual(mod)
+    assert res.b.d == d_res and res.shrink == shrink
+    x = np.ones((1, 1, 3 * f + 4))
+    first = next(t for t in range(x.shape[2]) if res.forward_step(x[:, :, t]) is not None)
+    assert first == delay
+    # clip mode: the module's output is the input less `shrink` frames at the
+    # start and at the end (one more at the end for an even receptive field,
+    # whose centre falls between two frames)
+    y = res.forward(x)
+    assert x.shape[2] - 2 * shrink - y.shape[2] == (1 - f % 2)
+    assert C.residual_align(f, 2, p, mod.delay) is None  # strided modules have no residual
+
+
+def test_stale_and_foreign_handles_rejected_without_device():
+    """A pointer the library never made (or one already destroyed) is not
+    dereferenced: every call returns CO_EINVAL."""
+    bogus = ctypes.c_void_p(0x1234)
+    n = C.i64()
+    assert C.co_conv_forward_step(bogus, bogus, bogus, 1, None) == C.CO_EINVAL
+    assert C.co_conv_get_steps(bogus, ctypes.byref(n)) == C.CO_EINVAL
+    assert C.co_conv_destroy(bogus) == C.CO_EINVAL
+    assert C.co_pool_destroy(bogus) == C.CO_EINVAL
+    assert C.co_delay_destroy(bogus) == C.CO_EINVAL
+    assert C.co_convpool_destroy(bogus) == C.CO_EINVAL
+    assert C.co_conv_algo_name(bogus) == b"none"
+
+
+def test_step_counter_limit_without_device():
+    """Step counters stay below 2^62 (the schedule's n + pT and n + count
+    cannot overflow): plans and attaches past it are rejected on the host."""
+    d = desc1d(p=2)
+    plan = C.StepPlan()
+    assert C.co_conv_plan_step(ctypes.byref(d), 1 << 62, 1, ctypes.byref(plan)) == C.CO_EINVAL
+    assert C.co_conv_plan_step(ctypes.byref(d), (1 << 62) - 1, 1, ctypes.byref(plan)) == C.CO_OK
+    assert plan.emit == 1 and plan.out_index == (1 << 62) - 1
+    h = ctypes.c_void_p()
+    assert C.co_conv_attach_state(ctypes.byref(d), ctypes.c_void_p(0x1000), 1 << 20,
+                                  (1 << 62) + 1, None, ctypes.byref(h)) == C.CO_EINVAL
+    pd = C.pool_desc("avg", 1, 1, (3,), (), (1,), (1,))
+    pplan = C.PoolPlan()
+    assert C.co_pool_plan_step(ctypes.byref(pd), 1 << 62, ctypes.byref(pplan)) == C.CO_EINVAL
+
+
+def test_pool_frames_of_2GiB_are_rejected():
+    """The pool step kernels address a frame with 32-bit buffer offsets: a
+    frame of 2^31 bytes or more is rejected when the descriptor is queried."""
+    info = C.PoolInfo()
+    big = C.pool_desc("avg", 1, 1, (2, 1, 1), (32768, 16384), (1, 1, 1), dtype=C.CO_F32)
+    assert C.co_pool_query(ctypes.byref(big), ctypes.byref(info)) == C.CO_EINVAL
+    half = C.pool_desc("avg", 1, 1, (2, 1, 1), (32768, 16384), (1, 1, 1), dtype=C.CO_BF16)
+    assert C.co_pool_query(ctypes.byref(half), ctypes.byref(info)) == C.CO_OK
