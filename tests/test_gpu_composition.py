@@ -10,7 +10,7 @@ import torch
 
 import oracle
 from paper_2204_03418_amd import synth
-from parity_util import assert_close, np64, oracle_conv, say
+from parity_util import assert_close, chain_atol, conv_terms, np64, oracle_conv, say, window_terms
 
 pytestmark = pytest.mark.gpu
 
@@ -60,11 +60,12 @@ def test_delay_line(d, dt, size):
         if r is None:
             assert y is None
         else:
-            assert_close(np64(y), np64(a[:, :, t]) + r, tdt, "delay add_step")
+            assert_close(np64(y), np64(a[:, :, t]) + r, tdt, "delay add_step", terms=2)
     # merge over a clip: the module's outputs are the last T - d steps
     dl4 = make()
     yc = dl4.add_steps(xd, ad[:, :, d:].contiguous())
-    assert_close(np64(yc), np64(a[:, :, d:]) + np64(x[:, :, :T - d]), tdt, "delay add_steps")
+    assert_close(np64(yc), np64(a[:, :, d:]) + np64(x[:, :, :T - d]), tdt, "delay add_steps",
+                 terms=2)
 
 
 @pytest.mark.parametrize("dt,k,p,shrink", [("f32", 3, 1, False), ("bf16", 3, 1, False),
@@ -87,13 +88,18 @@ def test_residual(dt, k, p, shrink):
     assert res.delay == ref.delay == k - 1 - p
     r = ref.forward_steps(np64(x))
     ys = res.forward_steps(xd)
-    assert_close(np64(ys), r, tdt, "residual forward_steps")
+    # the module's output is rounded to the io dtype before the residual sum
+    a_ref = oracle_conv(w, b, (1, 1, 1), (p, 1, 1), (1, 1, 1), 1).forward_steps(np64(x))
+    extra = chain_atol(a_ref, conv_terms(w), tdt)
+    assert_close(np64(ys), r, tdt, "residual forward_steps", terms=2, extra_atol=extra)
     res2 = make()
     outs = [res2.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
     assert all(o is None for o in outs[:res.delay])
     got = torch.stack([o for o in outs if o is not None], dim=2)
     assert torch.equal(got, ys)
-    assert_close(np64(res.forward(xd)), ref.forward(np64(x)), tdt, "residual forward")
+    a_clip = oracle.conv_forward(np64(x), np64(w), np64(b), 1, (p, 1, 1))
+    assert_close(np64(res.forward(xd)), ref.forward(np64(x)), tdt, "residual forward", terms=2,
+                 extra_atol=chain_atol(a_clip, conv_terms(w), tdt))
 
 
 def test_x3d_bottleneck_sequential():
@@ -128,8 +134,16 @@ def test_x3d_bottleneck_sequential():
     first = next(i for i, o in enumerate(outs) if o is not None)
     assert first == seq.delay
     got = torch.stack([o for o in outs if o is not None], dim=2)
-    # the oracle chains float64 stages; the GPU rounds each stage to bf16
-    assert_close(np64(got), r, tdt, "bottleneck steps")
+    # the oracle chains float64 stages; the GPU rounds each stage to bf16: the
+    # pointwise output's rounding passes through the depthwise weights, the
+    # depthwise output's through the average
+    o1 = oracle.ContinualConv(np64(w1), None).forward_steps(np64(x))
+    o2 = oracle.ContinualConv(np64(w2), np64(b2), padding=(1, 1, 1), groups=C).forward_steps(o1)
+    gain2 = float(np.abs(np64(w2)).reshape(C, -1).sum(axis=1).max())
+    extra = chain_atol(o2, conv_terms(w2), tdt) + chain_atol(o1, conv_terms(w1, False), tdt,
+                                                              gain=gain2)
+    assert_close(np64(got), r, tdt, "bottleneck steps", terms=window_terms((4, 7, 7)),
+                 extra_atol=extra)
     ys = make().forward_steps(xd)
     assert torch.equal(ys, got)
     # the unfused chain gives the same bits
@@ -210,7 +224,9 @@ def test_fused_depthwise_pool_step(case):
     ch = oracle.ContinualChain(
         oracle.ContinualConv(np64(w), np64(b), padding=pad, groups=C),
         oracle.ContinualPool(kind, (pk, ho, wo), stride=(1, ho, wo), count_include_pad=cip))
-    assert_close(np64(zc), ch.forward_steps(np64(x)), tdt, "convpool vs oracle")
+    yc = oracle.ContinualConv(np64(w), np64(b), padding=pad, groups=C).forward_steps(np64(x))
+    assert_close(np64(zc), ch.forward_steps(np64(x)), tdt, "convpool vs oracle",
+                 terms=window_terms((pk, ho, wo)), extra_atol=chain_atol(yc, conv_terms(w), tdt))
 
 
 def test_fused_depthwise_pool_workload():
@@ -245,7 +261,11 @@ def test_fused_depthwise_pool_workload():
     ch = oracle.ContinualChain(
         oracle.ContinualConv(np64(w), np64(b), padding=c.padding, groups=c.groups),
         oracle.ContinualPool("avg", pl.kernel, stride=pl.stride))
-    assert_close(np64(z[sel]), ch.forward_steps(np64(x[sel])), torch.bfloat16, "workload")
+    yc = oracle.ContinualConv(np64(w), np64(b), padding=c.padding,
+                              groups=c.groups).forward_steps(np64(x[sel]))
+    assert_close(np64(z[sel]), ch.forward_steps(np64(x[sel])), torch.bfloat16, "workload",
+                 terms=window_terms(pl.kernel),
+                 extra_atol=chain_atol(yc, conv_terms(w), torch.bfloat16))
 
 
 def test_expanded_temporal_average_pool():
@@ -267,7 +287,7 @@ def test_expanded_temporal_average_pool():
     ys = po.forward_steps(xd)
     assert ys.shape == (B, C, T - 63, 1, 1)
     ref = oracle.ContinualPool("avg", (64, H, W), stride=(1, H, W)).forward_steps(np64(x))
-    assert_close(np64(ys), ref, torch.bfloat16, "expanded pool")
+    assert_close(np64(ys), ref, torch.bfloat16, "expanded pool", terms=window_terms((64, H, W)))
     po2 = make()
     outs = [po2.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
     assert all(o is None for o in outs[:63])

@@ -15,7 +15,8 @@ import torch
 
 import oracle
 from paper_2204_03418_amd import synth
-from parity_util import TOL, assert_close, np64, oracle_conv, relerr, say
+from parity_util import (TOL, assert_close, chain_atol, conv_terms, np64, oracle_conv, relerr,
+                         say, window_terms)
 
 pytestmark = pytest.mark.gpu
 
@@ -63,12 +64,12 @@ def test_fuzz_conv_steps_and_clip(case):
         if r is None:
             assert ys is None
         else:
-            assert_close(np64(ys), r, tdt, f"steps {algo}")
+            assert_close(np64(ys), r, tdt, f"steps {algo}", terms=conv_terms(w))
         clip = co.forward(x.to(DEV))
         rc = oracle.conv_forward(np64(x), np64(w), np64(b), s, p, dil, G)
         assert tuple(clip.shape) == rc.shape
         if rc.size:
-            assert_close(np64(clip), rc, tdt, f"clip {algo}")
+            assert_close(np64(clip), rc, tdt, f"clip {algo}", terms=conv_terms(w))
 
 
 def _run_steps(co, x):
@@ -94,7 +95,7 @@ def test_workload_full_clip(name):
     torch.cuda.synchronize()
     ref = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x))
     got = np.stack([np64(o) for o in outs], axis=2)
-    assert_close(got, ref, synth.torch_dtype(c.dtype), name)
+    assert_close(got, ref, synth.torch_dtype(c.dtype), name, terms=conv_terms(w))
 
 
 @pytest.mark.parametrize("name,streams,frames", [
@@ -117,7 +118,7 @@ def test_workload_sampled_streams(name, streams, frames):
     sel = list(streams)
     got = np.stack([np64(o[sel]) for o in outs], axis=2)
     ref = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x[sel]))
-    assert_close(got, ref, synth.torch_dtype(c.dtype), name)
+    assert_close(got, ref, synth.torch_dtype(c.dtype), name, terms=conv_terms(w))
 
 
 def test_workload_depthwise_then_pool():
@@ -145,13 +146,14 @@ def test_workload_depthwise_then_pool():
     torch.cuda.synchronize()
     ref_c = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x))
     got_c = np.stack([np64(o) for o in conv_outs], axis=2)
-    assert_close(got_c, ref_c, torch.bfloat16, "depthwise conv")
+    assert_close(got_c, ref_c, torch.bfloat16, "depthwise conv", terms=conv_terms(w))
     # the pool oracle chains on the oracle's own (float64) conv outputs; the
     # GPU pool sees the bf16-rounded conv outputs, within the bf16 bound
     rp = oracle.ContinualPool("avg", pl.kernel, pl.stride).forward_steps(ref_c)
     got_p = np.stack([np64(o) for o in pool_outs], axis=2)
     assert got_p.shape == rp.shape
-    assert_close(got_p, rp, torch.bfloat16, "avg pool")
+    assert_close(got_p, rp, torch.bfloat16, "avg pool", terms=window_terms(pl.kernel),
+                 extra_atol=chain_atol(ref_c, conv_terms(w), torch.bfloat16))
     # the chain's output count: T - 5 frames after a delay of 5
     assert got_p.shape[2] == x.shape[2] - 5
 
@@ -186,10 +188,10 @@ def test_pool_fuzz(case):
     ys = po.forward_steps(x.to(DEV), pad_end=True)
     r = oracle.ContinualPool(kind, ks, ss, ps, ds, cip, spatial_dims=sd).forward_steps(
         np64(x), pad_end=True)
-    assert_close(np64(ys), r, dt, "pool steps")
+    assert_close(np64(ys), r, dt, "pool steps", terms=window_terms(ks))
     clip = po.forward(x.to(DEV))
     rc = oracle.pool_forward(kind, np64(x), ks, ss, ps, ds, cip)
-    assert_close(np64(clip), rc, dt, "pool clip")
+    assert_close(np64(clip), rc, dt, "pool clip", terms=window_terms(ks))
 
 
 def _small_conv(algo="auto", dtype="f32", **kw):
@@ -277,7 +279,7 @@ def test_temporal_edge_cases(k, p, s, dil):
         ref.clean_state()
         r = ref.forward_steps(np64(x), pad_end=True)
         ys = co.forward_steps(x.to(DEV), pad_end=True)
-        assert_close(np64(ys), r, torch.float32, f"edge {algo}")
+        assert_close(np64(ys), r, torch.float32, f"edge {algo}", terms=conv_terms(w))
 
 
 def test_all_empty_and_zero_length():
@@ -338,7 +340,7 @@ def test_gemm_forced(case):
         assert not outs
         return
     got = np.stack([np64(o) for o in outs], axis=2)
-    assert_close(got, r, tdt, "gemm steps")
+    assert_close(got, r, tdt, "gemm steps", terms=conv_terms(w))
     assert len(peeks) == len(outs)
     for a, bb in zip(peeks, outs):
         assert torch.equal(a, bb)
@@ -346,7 +348,8 @@ def test_gemm_forced(case):
     co.clean_state()
     ref.clean_state()
     ys = co.forward_steps(xd, pad_end=True)
-    assert_close(np64(ys), ref.forward_steps(np64(x), pad_end=True), tdt, "gemm steps pad_end")
+    assert_close(np64(ys), ref.forward_steps(np64(x), pad_end=True), tdt, "gemm steps pad_end",
+                 terms=conv_terms(w))
 
 
 REG_CASES = [
@@ -394,7 +397,7 @@ def test_gemm_reg_forced(case):
         assert not outs
     else:
         got = np.stack([np64(o) for o in outs], axis=2)
-        assert_close(got, r, tdt, "gemm_reg steps")
+        assert_close(got, r, tdt, "gemm_reg steps", terms=conv_terms(w))
         assert len(peeks) == len(outs)
         for a, bb in zip(peeks, outs):
             assert torch.equal(a, bb)
@@ -405,7 +408,7 @@ def test_gemm_reg_forced(case):
     if rp is None:
         assert ys is None
     else:
-        assert_close(np64(ys), rp, tdt, "gemm_reg steps pad_end")
+        assert_close(np64(ys), rp, tdt, "gemm_reg steps pad_end", terms=conv_terms(w))
 
 
 IMG_CASES = [
@@ -452,7 +455,7 @@ def test_gemm_img_forced(case):
         assert not outs
     else:
         got = np.stack([np64(o) for o in outs], axis=2)
-        assert_close(got, r, torch.bfloat16, "gemm_img steps")
+        assert_close(got, r, torch.bfloat16, "gemm_img steps", terms=conv_terms(w))
         assert len(peeks) == len(outs)
         for a, bb in zip(peeks, outs):
             assert torch.equal(a, bb)
@@ -463,7 +466,7 @@ def test_gemm_img_forced(case):
     if rp is None:
         assert ys is None
     else:
-        assert_close(np64(ys), rp, torch.bfloat16, "gemm_img steps pad_end")
+        assert_close(np64(ys), rp, torch.bfloat16, "gemm_img steps pad_end", terms=conv_terms(w))
 
 
 DW_STEPS_CASES = [
@@ -501,7 +504,7 @@ def test_depthwise_forward_steps_persistent(case):
     ref = oracle_conv(w, b, (1, 1, 1), p, (1, 1, 1), C)
     ys = co.forward_steps(xd, pad_end=True)
     rp = ref.forward_steps(np64(x), pad_end=True)
-    assert_close(np64(ys), rp, tdt, "persistent depthwise steps")
+    assert_close(np64(ys), rp, tdt, "persistent depthwise steps", terms=conv_terms(w))
     # bitwise against single steps
     co2 = make()
     outs = [co2.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
@@ -546,7 +549,7 @@ def _check_fused_steps(make, x, ref, tdt, what):
     assert co.steps_fused(T, pad_end=True), (what, co.algo)
     ys = co.forward_steps(xd, pad_end=True)
     rp = ref.forward_steps(np64(x), pad_end=True)
-    assert_close(np64(ys), rp, tdt, what)
+    assert_close(np64(ys), rp, tdt, what, terms=conv_terms(co.weight, co.bias is not None))
     co2 = make()
     outs = [co2.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
     outs = [o.clone() for o in outs if o is not None]
@@ -696,7 +699,7 @@ def test_workload_forward_steps_fused(name, streams):
     assert torch.equal(ys, torch.stack(outs, dim=2))
     sel = list(streams) if streams else list(range(c.batch))
     ref = oracle_conv(w, b, c.stride, c.padding, c.dilation, c.groups).forward_steps(np64(x[sel]))
-    assert_close(np64(ys[sel]), ref, synth.torch_dtype(c.dtype), name)
+    assert_close(np64(ys[sel]), ref, synth.torch_dtype(c.dtype), name, terms=conv_terms(w))
 
 
 POOL_STEPS_CASES = [
@@ -727,7 +730,7 @@ def test_pool_forward_steps_persistent(case):
     ys = po.forward_steps(xd, pad_end=True)
     r = oracle.ContinualPool(kind, ks, ss, ps, (1, 1, 1), cip, spatial_dims=2).forward_steps(
         np64(x), pad_end=True)
-    assert_close(np64(ys), r, tdt, "persistent pool steps")
+    assert_close(np64(ys), r, tdt, "persistent pool steps", terms=window_terms(ks))
     po2, po3 = make(), make()
     seq = [po2.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
     seq = [s_.clone() for s_ in seq if s_ is not None]
@@ -800,7 +803,8 @@ def test_forward_steps_clip_beyond_32bit_offsets(case):
         else:
             ref = oracle.conv_window(win, np.ones(3, np.uint8), np64(w), np64(b), groups, 1,
                                      (1, 1), (1, 1), (1, 1, 1))
-        assert_close(np64(y[:, :, k:k + 1]), ref, tdt, f"{what} frame {k}")
+        assert_close(np64(y[:, :, k:k + 1]), ref, tdt, f"{what} frame {k}",
+                     terms=27 if what == "avgpool" else conv_terms(w))
 
 
 @pytest.mark.parametrize("algo,dt", [("gemm", "bf16"), ("gemm", "f32"), ("gemm_img", "bf16")])
@@ -827,4 +831,4 @@ def test_misaligned_frame_is_staged(algo, dt):
     torch.cuda.synchronize()
     got = np.stack([np64(o) for o in outs], axis=2)
     ref = oracle_conv(w, b, spec.stride, spec.padding, spec.dilation, 1).forward_steps(np64(x))
-    assert_close(got, ref, synth.torch_dtype(dt), f"{algo} misaligned")
+    assert_close(got, ref, synth.torch_dtype(dt), f"{algo} misaligned", terms=conv_terms(w))

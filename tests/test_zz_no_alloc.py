@@ -14,7 +14,7 @@ import pytest
 import torch
 
 from paper_2204_03418_amd import coinf, synth
-from parity_util import assert_close, np64, oracle_conv, say
+from parity_util import assert_close, conv_terms, np64, oracle_conv, say
 
 pytestmark = pytest.mark.gpu
 
@@ -110,7 +110,7 @@ def test_noalloc_matches_allocating_entry_point(name, spec, algo, misaligned, up
             if ref is None:
                 assert y_b.shape[2] == 0
             else:
-                assert_close(np64(y_b), ref, co_b.torch_dtype, f"{name} T={T}")
+                assert_close(np64(y_b), ref, co_b.torch_dtype, f"{name} T={T}", terms=conv_terms(w))
 
 
 def test_noalloc_rejects_calls_beyond_the_scratch():
