@@ -88,6 +88,12 @@ typedef int32_t co_status;
 #define CO_ALGO_GEMM_IMG   5   /* implicit GEMM on MFMA with each stream's whole
                                   frame resident in LDS (bf16, groups = 1,
                                   small frames, C_in a multiple of 8) */
+#define CO_ALGO_GEMM_WS    6   /* implicit GEMM on MFMA, warp-specialized: producer
+                                  waves stage the input, consumer waves stream the
+                                  weights from L2 (bf16, groups = 1, 3x3 spatial
+                                  taps, stride and dilation 1, spatial padding <= 1,
+                                  Ho*Wo a multiple of 4); AUTO picks it for layers
+                                  with at least 128 of its 448 x 64 tiles */
 
 #define CO_POOL_AVG  0
 #define CO_POOL_MAX  1

@@ -1379,6 +1379,7 @@ hipError_t launch_conv_step_gemm(const ConvGeom& g, const ConvLayout& L, char* s
   // A frame pointer or plane stride that breaks the pixel-pair alignment, or
   // a frame past 32-bit reach, is copied into a contiguous buffer first.
   if (gemm_step_needs_staging(g, io)) return launch_conv_step_staged(g, L, state, io, plan, s);
+  if (c.ws) return launch_conv_step_gemm_ws(g, c, L, state, io, plan, s);
   if (g.kH == 3 && g.kW == 3) return gemm_dispatch_taps<3, 3>(g, c, L, state, io, plan, s);
   if (g.kH == 1 && g.kW == 1) return gemm_dispatch_taps<1, 1>(g, c, L, state, io, plan, s);
   return hipErrorInvalidValue;
@@ -1428,6 +1429,7 @@ hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, hipStream_t s) {
   GemmConfig c;
   if (!gemm_config(g, g.cfg, &c)) return hipErrorInvalidValue;
+  if (c.ws) return launch_pack_gemm_ws(g, c, L, state, weight, s);
   const int64_t total = int64_t(c.n_tiles) * c.n_chunks * g.kH * g.kW * c.N_WG * 4;
   uint4* out = reinterpret_cast<uint4*>(state + L.weight);
   if (g.dtype == CO_BF16)

@@ -131,6 +131,13 @@ hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* 
                                   const void* weight, hipStream_t stream);
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, hipStream_t stream);
+// The warp-specialized configuration of the GEMM step (conv_gemm_ws.hip):
+// bf16, 3x3 taps; its weights packed in the order its consumer waves load.
+hipError_t launch_conv_step_gemm_ws(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
+                                    char* state, const StepIO& io, const co_step_plan& plan,
+                                    hipStream_t stream);
+hipError_t launch_pack_gemm_ws(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
+                               char* state, const void* weight, hipStream_t stream);
 
 // Fused depthwise convolution step + global spatial pool step (convpool.hip):
 // one launch per step; pplan is null when the convolution does not emit

@@ -51,6 +51,7 @@ constexpr GemmShape kGemmShapes[kGemmConfigs] = {
     {CO_BF16, 2, 2, 1, 4, 8},  // 32 x 128: small K, wide N
     {CO_F32, 2, 2, 1, 4, 4},   // 32 x 128
     {CO_F32, 1, 1, 4, 1, 4},   // 64 x 16: small N, fills the chip with waves
+    {CO_BF16, kWsWM, kWsWN, kWsWaves, 1, 8},  // 448 x 64, warp-specialized (3x3 only)
 };
 
 // Input rows a tile of output pixels [m0, m1) needs, over all of its images.
@@ -86,8 +87,24 @@ bool gemm_geometry_ok(const ConvGeom& g) {
          g.W + 2 * g.pW <= 256 && frame_offsets_fit(g);
 }
 
+// Staged rows of a warp-specialized tile [m0, m1): the images' rows with
+// pH zero rows between consecutive images (one image's bottom halo is the
+// next one's top halo), from the first row the tile's taps reach to the last.
+int64_t ws_tile_rows(const ConvGeom& g, int64_t m0, int64_t m1) {
+  const int64_t r0 = m0 / g.Wo, r1 = (m1 - 1) / g.Wo;
+  const int64_t b0 = r0 / g.Ho, i0 = r0 % g.Ho;
+  const int64_t b1 = r1 / g.Ho, i1 = r1 % g.Ho;
+  return (b1 - b0) * (g.H + g.pH) + i1 - i0 + g.kH;
+}
+
 bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
   if (id < 0 || id >= kGemmConfigs || !gemm_geometry_ok(g)) return false;
+  // warp-specialized: 3x3 taps, at most one zero halo row between images
+  // and frames of a multiple of 4 pixels (a lane's four outputs are one
+  // 16-byte unit of a ring plane and one 8-byte unit of a y plane)
+  if (id == kGemmWs && !(g.kH == 3 && g.kW == 3 && g.pH <= 1 && g.Ho == g.H + 2 * g.pH - 2 &&
+                         g.So() % 4 == 0))
+    return false;
   const GemmShape& s = kGemmShapes[id];
   if (s.dtype != g.dtype) return false;
   GemmConfig r{};
@@ -118,6 +135,19 @@ bool gemm_config(const ConvGeom& g, int id, GemmConfig* c) {
   r.a_units = ((slots + 2) * r.cols + 2) * kGemmPixUnits;
   r.b_units = int64_t(g.kH) * g.kW * r.N_WG * 4;
   r.lds_bytes = 2 * (r.a_units + r.b_units) * 16;
+  r.ws = id == kGemmWs ? 1 : 0;
+  r.real_rows = int32_t(slots);
+  if (r.ws) {
+    // A stages only: every staged row (zero halo rows included), the first
+    // pixel of one more row (the last row's right halo) and two trash pixels
+    int64_t rows = 1;
+    for (int64_t t = 0; t < r.m_tiles; ++t)
+      rows = std::max(rows, ws_tile_rows(g, t * r.M_WG, std::min<int64_t>(M, (t + 1) * r.M_WG)));
+    r.max_slots = int32_t(rows);
+    r.a_units = (rows * r.cols + r.cols + 2) * kGemmPixUnits;
+    r.b_units = 0;
+    r.lds_bytes = 2 * r.a_units * 16;
+  }
   if (r.lds_bytes > kLdsBytes) return false;
   // staging items (row, channel group, pixel pair) must fit the per-thread
   // register budget of the kernel
@@ -157,9 +187,14 @@ bool gemm_steps_config(const ConvGeom& g, GemmStepsConfig* c) {
 }
 
 int gemm_pick(const ConvGeom& g) {
+  // the warp-specialized kernel when its tiles cover the chip
+  GemmConfig w;
+  if (gemm_config(g, kGemmWs, &w) && int64_t(w.m_tiles) * w.n_tiles >= kWsMinTiles)
+    return kGemmWs;
   int best = -1;
   double best_cost = 0;
   for (int id = 0; id < kGemmConfigs; ++id) {
+    if (id == kGemmWs) continue;
     GemmConfig c;
     if (!gemm_config(g, id, &c)) continue;
     // Cycles of one wave: MFMA issue (bf16 16x16x32: 16 clk per fragment pair
@@ -356,7 +391,7 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
   if (d.in_channels % d.groups || d.out_channels % d.groups) return CO_EINVAL;
   if (d.dtype != CO_F32 && d.dtype != CO_BF16) return CO_EINVAL;
   if (d.has_bias != 0 && d.has_bias != 1) return CO_EINVAL;
-  if (d.algo < CO_ALGO_AUTO || d.algo > CO_ALGO_GEMM_IMG) return CO_EINVAL;
+  if (d.algo < CO_ALGO_AUTO || d.algo > CO_ALGO_GEMM_WS) return CO_EINVAL;
   for (int a = 0; a < 3; ++a) {
     if (d.kernel[a] < 1 || d.stride[a] < 1 || d.dilation[a] < 1 || d.padding[a] < 0)
       return CO_EINVAL;
@@ -438,7 +473,14 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
     ImgConfig ic;
     if (!img_config(r, &ic)) return CO_ENOTSUP;
   }
-  if (algo == CO_ALGO_GEMM) r.cfg = gemm_pick(r);
+  if (algo == CO_ALGO_GEMM_WS) {
+    GemmConfig wc;
+    if (!gemm_config(r, kGemmWs, &wc)) return CO_ENOTSUP;
+    algo = CO_ALGO_GEMM;  // the GEMM family with its warp-specialized configuration
+    r.cfg = kGemmWs;
+  } else if (algo == CO_ALGO_GEMM) {
+    r.cfg = gemm_pick(r);
+  }
   if (algo == CO_ALGO_GEMM_REG) r.cfg = reg_pick(r);
   r.algo = algo;
   *g = r;

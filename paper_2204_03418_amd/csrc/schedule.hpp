@@ -73,6 +73,9 @@ struct GemmConfig {
   int64_t a_units;     // 16-byte units of one A stage in LDS
   int64_t b_units;     // 16-byte units of one B stage in LDS
   int64_t lds_bytes;   // 2 * (a_units + b_units) * 16
+  int32_t ws;          // warp-specialized kernel (conv_gemm_ws.hip): producer waves
+                       // stage A, consumer waves stream B from L2 (b_units = 0)
+  int32_t real_rows;   // ws: most input rows a tile stages (the rest are zero halo rows)
 };
 
 // Register-operand implicit GEMM (small K): one wave per 16-pixel x
@@ -127,7 +130,12 @@ constexpr int kImgThreadsHost = 512;
 
 constexpr int kRegConfigs = 10;
 
-constexpr int kGemmConfigs = 4;
+constexpr int kGemmConfigs = 5;
+constexpr int kGemmWs = 4;             // the warp-specialized bf16 3x3 configuration
+constexpr int kWsWM = 7;               // consumer wave: 7 pixel fragments ...
+constexpr int kWsWN = 4;               // ... x 4 column fragments of 16x16
+constexpr int kWsWaves = 4;            // consumer waves (and as many producer waves)
+constexpr int kWsMinTiles = 128;       // tiles below which the ws kernel leaves CUs idle
 constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)
 constexpr int kGemmStageItems = 1024;  // staging items per workgroup and chunk
 constexpr int64_t kLdsBytes = 160 * 1024;

@@ -492,3 +492,24 @@ def test_pool_frames_of_2GiB_are_rejected():
     assert C.co_pool_query(ctypes.byref(big), ctypes.byref(info)) == C.CO_EINVAL
     half = C.pool_desc("avg", 1, 1, (2, 1, 1), (32768, 16384), (1, 1, 1), dtype=C.CO_BF16)
     assert C.co_pool_query(ctypes.byref(half), ctypes.byref(info)) == C.CO_OK
+
+
+def test_warp_specialized_gemm_selection():
+    """CO_ALGO_GEMM_WS: granted for bf16 3x3 layers with Ho*Wo % 4 == 0 and
+    spatial padding <= 1, refused otherwise; AUTO picks it for the 64-stream
+    layer (252 tiles of 448 x 64) and not for a small one."""
+    def q(B, cin, cout, size, pad=(0, 1, 1), dtype=C.CO_BF16, algo=C.CO_ALGO_GEMM_WS, k=(3, 3, 3)):
+        d = C.conv_desc(B, cin, cout, k, size, (1, 1, 1), pad, (1, 1, 1), 1, True, dtype,
+                        algo=algo)
+        info = C.ConvInfo()
+        return C.co_conv_query(ctypes.byref(d), ctypes.byref(info)), info
+    st, info = q(3, 40, 24, (8, 10))
+    assert st == C.CO_OK and info.algo == C.CO_ALGO_GEMM
+    assert q(3, 40, 24, (9, 11))[0] == C.CO_ENOTSUP                    # Ho*Wo = 99
+    assert q(3, 40, 24, (8, 10), dtype=C.CO_F32)[0] == C.CO_ENOTSUP    # fp32
+    assert q(3, 40, 24, (8, 10), pad=(0, 2, 2))[0] == C.CO_ENOTSUP     # spatial padding 2
+    assert q(3, 40, 24, (8, 10), k=(3, 1, 1))[0] == C.CO_ENOTSUP       # 1x1 taps
+    # the 64-stream layer's state holds the ws kernel's packed weights
+    st, big = q(64, 192, 192, (14, 14), algo=C.CO_ALGO_AUTO)
+    st2, forced = q(64, 192, 192, (14, 14))
+    assert st == st2 == C.CO_OK and big.state_bytes == forced.state_bytes

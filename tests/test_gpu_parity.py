@@ -311,6 +311,64 @@ GEMM_CASES = [
 ]
 
 
+GEMM_WS_CASES = [
+    # B, Cin, Cout, kT, (kH, kW), in_size, (pH, pW), sT, pT, dT, dtype -- the
+    # warp-specialized configuration: bf16, 3x3, Ho*Wo a multiple of 4
+    (3, 40, 24, 3, (3, 3), (8, 10), (1, 1), 1, 0, 1, "bf16"),    # ragged chunk and column tile
+    (2, 32, 64, 2, (3, 3), (12, 9), (1, 1), 1, 1, 1, "bf16"),    # odd width: single-pixel loads
+    (4, 64, 32, 3, (3, 3), (10, 10), (0, 0), 1, 0, 1, "bf16"),   # valid convolution, pH = 0
+    (20, 16, 48, 3, (3, 3), (6, 6), (1, 1), 1, 2, 1, "bf16"),    # many images per tile, ragged tile
+    (2, 33, 40, 3, (3, 3), (10, 8), (1, 1), 2, 1, 2, "bf16"),    # temporal stride and dilation
+    (3, 24, 16, 1, (3, 3), (8, 8), (1, 1), 1, 0, 1, "bf16"),     # kT = 1: no ring
+    (64, 96, 96, 3, (3, 3), (14, 14), (1, 1), 1, 0, 1, "bf16"),  # the 64-stream shape, fewer channels
+]
+
+
+@pytest.mark.parametrize("case", GEMM_WS_CASES, ids=lambda c: "ws_" + "_".join(map(str, c[:4])))
+def test_gemm_ws_forced(case):
+    """The warp-specialized GEMM step (producer waves stage the input,
+    consumer waves stream the weights) against the oracle, stepping with
+    update_state=False peeks, and forward_steps with end padding."""
+    B, cin, cout, kT, ks, size, ps, sT, pT, dT, dt = case
+    say("gemm ws", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=(kT,) + ks,
+                          in_size=size, stride=(sT,) + (1,) * len(size),
+                          padding=(pT,) + ps, dilation=(dT,) + (1,) * len(size), dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 9, 63000 + cin * 7 + cout, "kaiming")
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=spec.stride,
+                      padding=spec.padding, dilation=spec.dilation, algo="gemm_ws")
+    assert co.algo == "gemm_ws_bf16"
+    ref = oracle_conv(w, b, spec.stride, spec.padding, spec.dilation, 1)
+    xd = x.to(DEV)
+    tdt = synth.torch_dtype(dt)
+    outs, peeks = [], []
+    for t in range(x.shape[2]):
+        fr = xd[:, :, t].contiguous()
+        pk = co.forward_step(fr, update_state=False)
+        if pk is not None:
+            peeks.append(pk.clone())
+        y = co.forward_step(fr)
+        if y is not None:
+            outs.append(y.clone())
+    r = ref.forward_steps(np64(x))
+    if r is None:
+        assert not outs
+    else:
+        got = np.stack([np64(o) for o in outs], axis=2)
+        assert_close(got, r, tdt, "gemm_ws steps", terms=conv_terms(w))
+        assert len(peeks) == len(outs)
+        for a, bb in zip(peeks, outs):
+            assert torch.equal(a, bb)
+    co.clean_state()
+    ref.clean_state()
+    ys = co.forward_steps(xd, pad_end=True)
+    rp = ref.forward_steps(np64(x), pad_end=True)
+    if rp is None:
+        assert ys is None
+    else:
+        assert_close(np64(ys), rp, tdt, "gemm_ws steps pad_end", terms=conv_terms(w))
+
+
 @pytest.mark.parametrize("case", GEMM_CASES, ids=lambda c: "gemm_" + "_".join(map(str, c[:4])) + c[-1])
 def test_gemm_forced(case):
     B, cin, cout, kT, ks, size, ps, sT, pT, dT, dt = case
