@@ -458,6 +458,57 @@ class ContinualDelay:
         return np.asarray(x, dtype=np.float64)
 
 
+class BatchNormEval:
+    """Batch normalisation in evaluation mode over channel axis 1 (the
+    nn.BatchNorm1d/2d/3d modules a continual network composes with, section
+    3.2): a per-channel affine map with the running statistics,
+
+        y[:, c, ...] = (x[:, c, ...] - mean[c]) / sqrt(var[c] + eps) * gamma[c] + beta[c].
+
+    It holds no state across time, so forward_step and forward apply the same
+    map to a frame or a clip, and the delay is 0."""
+
+    def __init__(self, gamma, beta, mean, var, eps=1e-5):
+        self.gamma = np.asarray(gamma, dtype=np.float64)
+        self.beta = np.asarray(beta, dtype=np.float64)
+        self.mean = np.asarray(mean, dtype=np.float64)
+        self.var = np.asarray(var, dtype=np.float64)
+        self.eps = float(eps)
+
+    delay = property(lambda self: 0)
+    receptive_field = property(lambda self: 1)
+
+    def clean_state(self):
+        pass
+
+    def forward(self, x):
+        x = np.asarray(x, dtype=np.float64)
+        shape = (1, -1) + (1,) * (x.ndim - 2)
+        inv = 1.0 / np.sqrt(self.var + self.eps)
+        return ((x - self.mean.reshape(shape)) * inv.reshape(shape) * self.gamma.reshape(shape)
+                + self.beta.reshape(shape))
+
+    def forward_step(self, x_t, update_state=True):
+        return self.forward(x_t)
+
+
+class ReLU:
+    """The rectifier max(x, 0), elementwise (nn.ReLU in a continual network,
+    section 3.2): stateless, delay 0."""
+
+    delay = property(lambda self: 0)
+    receptive_field = property(lambda self: 1)
+
+    def clean_state(self):
+        pass
+
+    def forward(self, x):
+        return np.maximum(np.asarray(x, dtype=np.float64), 0.0)
+
+    def forward_step(self, x_t, update_state=True):
+        return self.forward(x_t)
+
+
 def _steps(mod, x):
     """forward_step over the T axis; non-empty outputs stacked (None if none)."""
     outs = [mod.forward_step(x[:, :, t]) for t in range(x.shape[2])]
