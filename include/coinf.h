@@ -98,6 +98,11 @@ typedef int32_t co_status;
 #define CO_POOL_AVG  0
 #define CO_POOL_MAX  1
 
+/* Elementwise activations (section 3.2: activation functions compose with
+ * continual modules as stateless per-frame maps). */
+#define CO_ACT_NONE  0
+#define CO_ACT_RELU  1         /* max(x, 0) */
+
 #define CO_MAX_TAPS  64        /* largest temporal kernel size kT */
 
 /* Per-tap actions of one convolution step (see co_conv_plan_step). */
@@ -187,6 +192,37 @@ co_status co_conv_plan_step(const co_conv_desc* desc, int64_t n, int32_t update_
 co_status co_conv_init_state(const co_conv_desc* desc, const void* weight, const void* bias,
                              void* state, int64_t state_bytes, void* stream,
                              co_conv_handle** out);
+
+/*
+ * co_conv_init_state with an evaluation-mode batch normalisation of the
+ * convolution's output folded in (section 3.2: the library's continual
+ * convolutions compose with nn.BatchNorm layers; the paper's Inception listing
+ * wraps each one as conv -> BatchNorm3d -> ReLU).  Per output channel o,
+ * scale = gamma[o] / sqrt(var[o] + eps) multiplies the weights of o before
+ * they are rounded to the packed dtype (bf16 for the matrix-core kernels,
+ * float32 for the direct and depthwise kernels) and the bias becomes
+ * bias[o] * scale + beta[o] - mean[o] * scale (bias taken as 0 when
+ * has_bias = 0); every step then emits BN(conv(x)).  gamma, beta, mean and
+ * var are float32 device arrays of C_out; eps >= 0.  Otherwise as
+ * co_conv_init_state.
+ */
+co_status co_conv_init_state_bn(const co_conv_desc* desc, const void* weight, const void* bias,
+                                const float* gamma, const float* beta, const float* mean,
+                                const float* var, float eps, void* state, int64_t state_bytes,
+                                void* stream, co_conv_handle** out);
+
+/*
+ * The folded layer itself, for clip mode (co_conv_forward) over the same
+ * layer: w_out (C_out, C_in/groups, kT, kH, kW) and b_out (C_out) in the io
+ * dtype, caller-allocated device arrays.  Each weight is scaled and rounded
+ * to the io dtype exactly as the matrix-core packing of
+ * co_conv_init_state_bn rounds it; the bias is the float32 folded bias
+ * rounded to the io dtype (so a bf16 clip carries a bf16 bias where the
+ * steps add the float32 one).
+ */
+co_status co_conv_fold_bn(const co_conv_desc* desc, const void* weight, const void* bias,
+                          const float* gamma, const float* beta, const float* mean,
+                          const float* var, float eps, void* w_out, void* b_out, void* stream);
 
 /*
  * forward_step (Principle 2): consume one frame x_t (B, C_in, S1, S2) and,
@@ -437,6 +473,46 @@ co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_
 co_status co_convpool_destroy(co_convpool_handle* h);
 
 /*
+ * Fused step of an X3D-style bottleneck (sections 3.2-3.3; Table 2's CoX3D
+ * networks are built from such blocks): a pointwise convolution (1x1x1,
+ * stride 1, no padding, groups 1, made with CO_ALGO_DIRECT: delay 0) and its
+ * activation act1, a depthwise continual convolution and its activation
+ * act2, and the pool over the depthwise output's whole plane (the pair
+ * co_convpool_bind accepts), with batch normalisations folded into the
+ * convolutions by co_conv_init_state_bn.  One launch per step: the input
+ * frame of each stream is staged on chip once, and neither intermediate
+ * frame is written anywhere.  The handle borrows the three handles and
+ * advances their step counters and states exactly as the separate steps
+ * (co_conv_forward_step, co_act_forward, co_conv_forward_step,
+ * co_act_forward, co_pool_forward_step) would: the results are identical
+ * bit for bit, and fused and separate calls can be mixed.  The chain's
+ * delay is the depthwise convolution's plus the pool's (Principle 6; the
+ * pointwise convolution adds none).  Input planes of at most 64 pixels and
+ * C_in x H x W <= 12288.  CO_ENOTSUP when the layers do not fit, CO_EINVAL
+ * for an unknown activation.
+ */
+typedef struct co_bneck_handle co_bneck_handle;
+
+co_status co_bneck_bind(co_conv_handle* pw, int32_t act1, co_conv_handle* dw, int32_t act2,
+                        co_pool_handle* pool, co_bneck_handle** out);
+
+/* One step: x_t (B, C_in, S1, S2) in; the pool's output z_t (B, C, 1, 1) when
+ * the depthwise convolution and the pool both emit (CO_OK), else CO_EMPTY
+ * with z_t untouched. */
+co_status co_bneck_forward_step(co_bneck_handle* h, const void* x_t, void* z_t,
+                                int32_t update_state, void* stream);
+
+/* T steps over x (B, C_in, T, S1, S2), one fused launch per frame; the
+ * non-empty outputs, in order, into z (B, C, z_cap_frames, 1, 1); *n_out =
+ * their count.  With update_state = 0 the states are restored afterwards
+ * (a stream-ordered copy, as co_conv_forward_steps). */
+co_status co_bneck_forward_steps(co_bneck_handle* h, const void* x, int32_t T, void* z,
+                                 int32_t z_cap_frames, int32_t update_state, void* stream,
+                                 int32_t* n_out);
+
+co_status co_bneck_destroy(co_bneck_handle* h);
+
+/*
  * Delay (section 3.2, co.Delay): shifts a stream by `delay` steps, so that
  * parallel branches with different delays meet on the same frame
  * (Principle 7; residual connections, section 3.1.1).  Step n outputs input
@@ -509,6 +585,14 @@ co_status co_delay_add_steps(co_delay_handle* h, const void* x, int32_t T, const
 co_status co_add_frames(const void* a, const void* x, void* y, int32_t rows, int32_t frame_elems,
                         int32_t a_frames, int32_t x_frames, int32_t x_offset, int32_t dtype,
                         void* stream);
+
+/*
+ * Elementwise activation of n contiguous elements of dtype (a frame or a
+ * clip): y = act(x); y may equal x.  Stateless, delay 0.  ReLU maps NaN to 0.
+ * CO_EINVAL for an unknown act or dtype.
+ */
+co_status co_act_forward(const void* x, void* y, int64_t n, int32_t dtype, int32_t act,
+                         void* stream);
 
 co_status co_delay_clean_state(co_delay_handle* h, void* stream);
 co_status co_delay_get_steps(const co_delay_handle* h, int64_t* n);

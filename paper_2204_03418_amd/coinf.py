@@ -27,6 +27,7 @@ CO_F32, CO_BF16 = 0, 1
 CO_ALGO_AUTO, CO_ALGO_DIRECT, CO_ALGO_GEMM, CO_ALGO_DEPTHWISE, CO_ALGO_GEMM_REG = 0, 1, 2, 3, 4
 CO_ALGO_GEMM_IMG = 5
 CO_ALGO_GEMM_WS = 6
+CO_ACT_NONE, CO_ACT_RELU = 0, 1
 CO_POOL_AVG, CO_POOL_MAX = 0, 1
 CO_MAX_TAPS = 64
 CO_TAP_NONE, CO_TAP_START, CO_TAP_ACC, CO_TAP_EMIT, CO_TAP_EMIT_FRESH = 0, 1, 2, 3, 4
@@ -141,6 +142,16 @@ co_convpool_forward_step = _sig("co_convpool_forward_step", i32, [vp, vp, vp, i3
 co_convpool_forward_steps = _sig("co_convpool_forward_steps", i32,
                                  [vp, vp, i32, vp, i32, i32, vp, pi32])
 co_convpool_destroy = _sig("co_convpool_destroy", i32, [vp])
+pf32, f32 = ctypes.POINTER(ctypes.c_float), ctypes.c_float
+co_conv_init_state_bn = _sig("co_conv_init_state_bn", i32,
+                             [CD, vp, vp, vp, vp, vp, vp, f32, vp, i64, vp, pvp])
+co_conv_fold_bn = _sig("co_conv_fold_bn", i32, [CD, vp, vp, vp, vp, vp, vp, f32, vp, vp, vp])
+co_act_forward = _sig("co_act_forward", i32, [vp, vp, i64, i32, i32, vp])
+co_bneck_bind = _sig("co_bneck_bind", i32, [vp, i32, vp, i32, vp, pvp])
+co_bneck_forward_step = _sig("co_bneck_forward_step", i32, [vp, vp, vp, i32, vp])
+co_bneck_forward_steps = _sig("co_bneck_forward_steps", i32,
+                              [vp, vp, i32, vp, i32, i32, vp, pi32])
+co_bneck_destroy = _sig("co_bneck_destroy", i32, [vp])
 co_residual_align = _sig("co_residual_align", i32, [i64, i64, i64, i64, pi64, pi64, pi64])
 
 
@@ -250,11 +261,15 @@ class CoConv:
 
     weight (C_out, C_in/groups, kT, *kS) and bias (C_out,) are device tensors
     of one dtype (float32 or bfloat16); batch and in_size fix the frame shape
-    (B, C_in, *in_size).  kernel geometry comes from weight.shape.
+    (B, C_in, *in_size).  kernel geometry comes from weight.shape.  bn =
+    (gamma, beta, running_mean, running_var, eps), float32 device tensors of
+    C_out and a float, folds an evaluation-mode batch normalisation of the
+    output into the layer (co_conv_init_state_bn): every step emits
+    BN(conv(x)).
     """
 
     def __init__(self, weight, bias=None, *, batch, in_size=(), stride=1, padding=0,
-                 dilation=1, groups=1, algo="auto", state=None, attach_steps=None):
+                 dilation=1, groups=1, algo="auto", state=None, attach_steps=None, bn=None):
         dt = DTYPES[weight.dtype]
         self.torch_dtype = weight.dtype
         self.desc = conv_desc(batch, weight.shape[1] * groups, weight.shape[0],
@@ -264,7 +279,7 @@ class CoConv:
         self.batch, self.in_size = batch, tuple(in_size)
         self.in_channels, self.out_channels = weight.shape[1] * groups, weight.shape[0]
         self.out_size = tuple(self.info.out_size[:len(in_size)])
-        self.weight, self.bias = weight, bias
+        self.weight, self.bias, self.bn = weight, bias, bn
         dev = weight.device
         if state is None:
             state = torch.empty(self.info.state_bytes, dtype=torch.uint8, device=dev)
@@ -274,14 +289,27 @@ class CoConv:
             _need(weight, weight.dtype, weight.shape, "weight")
             if bias is not None:
                 _need(bias, weight.dtype, (weight.shape[0],), "bias")
-            check(co_conv_init_state(ctypes.byref(self.desc), _ptr(weight), _ptr(bias),
-                                     _ptr(state), state.numel(), _stream(), ctypes.byref(h)),
-                  "co_conv_init_state")
+            if bn is None:
+                check(co_conv_init_state(ctypes.byref(self.desc), _ptr(weight), _ptr(bias),
+                                         _ptr(state), state.numel(), _stream(),
+                                         ctypes.byref(h)), "co_conv_init_state")
+            else:
+                check(co_conv_init_state_bn(ctypes.byref(self.desc), _ptr(weight), _ptr(bias),
+                                            *self._bn_args(), _ptr(state), state.numel(),
+                                            _stream(), ctypes.byref(h)),
+                      "co_conv_init_state_bn")
         else:
             check(co_conv_attach_state(ctypes.byref(self.desc), _ptr(state), state.numel(),
                                        int(attach_steps), _stream(), ctypes.byref(h)),
                   "co_conv_attach_state")
         self.handle = h
+
+    def _bn_args(self):
+        gamma, beta, mean, var, eps = self.bn
+        for t, what in ((gamma, "gamma"), (beta, "beta"), (mean, "running_mean"),
+                        (var, "running_var")):
+            _need(t, torch.float32, (self.out_channels,), what)
+        return _ptr(gamma), _ptr(beta), _ptr(mean), _ptr(var), float(eps)
 
     # the destroy function is bound as a default so that objects collected
     # during interpreter shutdown, after the module globals are cleared, still
@@ -369,9 +397,25 @@ class CoConv:
               "co_conv_steps_fused")
         return bool(f.value)
 
+    def folded(self):
+        """(weight, bias) with the batch normalisation folded in, in the io
+        dtype (co_conv_fold_bn); the layer's own when it has none."""
+        if self.bn is None:
+            return self.weight, self.bias
+        w = torch.empty_like(self.weight)
+        b = torch.empty(self.out_channels, dtype=self.torch_dtype, device=self.weight.device)
+        check(co_conv_fold_bn(ctypes.byref(self.desc), _ptr(self.weight), _ptr(self.bias),
+                              *self._bn_args(), _ptr(w), _ptr(b), _stream()), "co_conv_fold_bn")
+        return w, b
+
     def forward(self, x):
         """Principle 2 forward (clip mode), stateless."""
-        return conv_forward(self.desc, self.weight, self.bias, x)
+        if self.bn is None:
+            return conv_forward(self.desc, self.weight, self.bias, x)
+        w, b = self.folded()
+        d = ConvDesc.from_buffer_copy(self.desc)
+        d.has_bias = 1
+        return conv_forward(d, w, b, x)
 
     def clean_state(self):
         check(co_conv_clean_state(self.handle, _stream()), "co_conv_clean_state")
@@ -656,6 +700,120 @@ def add_frames(a, x, x_offset=0):
     return y
 
 
+ACTS = {"none": CO_ACT_NONE, "relu": CO_ACT_RELU}
+
+
+def act_forward(x, act="relu", out=None):
+    """Elementwise activation of any contiguous tensor (co_act_forward)."""
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    y = torch.empty_like(x) if out is None else out
+    _need(y, x.dtype, x.shape, "out")
+    check(co_act_forward(_ptr(x), _ptr(y), x.numel(), DTYPES[x.dtype], ACTS[act], _stream()),
+          "co_act_forward")
+    return y
+
+
+class CoReLU:
+    """ReLU as a continual module: stateless and elementwise, so it has delay
+    0 and receptive field 1 (section 3.2's composition of per-frame
+    layers); every step emits."""
+
+    delay, receptive_field, t_stride, t_padding = 0, 1, 1, 0
+    act = "relu"
+
+    def forward_step(self, x_t, update_state=True):
+        return act_forward(x_t)
+
+    def forward_steps(self, x, update_state=True):
+        return act_forward(x.contiguous())
+
+    def forward(self, x):
+        return act_forward(x.contiguous())
+
+    def clean_state(self):
+        pass
+
+
+class Bottleneck:
+    """The X3D bottleneck front (pointwise CoConv -> optional ReLU ->
+    depthwise CoConv -> optional ReLU -> CoPool over its whole output plane,
+    batch normalisations folded into the convolutions) stepped as one launch
+    per frame (co_bneck_*).  The three modules keep their states and step
+    counters, and the outputs equal stepping them separately bit for bit.
+    The pointwise layer must be a 1x1x1 CoConv made with algo="direct"."""
+
+    def __init__(self, pw, relu1, dw, relu2, pool):
+        h = ctypes.c_void_p()
+        check(co_bneck_bind(pw.handle, CO_ACT_RELU if relu1 else CO_ACT_NONE, dw.handle,
+                            CO_ACT_RELU if relu2 else CO_ACT_NONE, pool.handle,
+                            ctypes.byref(h)), "co_bneck_bind")
+        self.pw, self.relu1, self.dw, self.relu2, self.pool = pw, relu1, dw, relu2, pool
+        self.handle = h
+
+    @staticmethod
+    def fits(pw, dw, pool):
+        h = ctypes.c_void_p()
+        if co_bneck_bind(pw.handle, CO_ACT_NONE, dw.handle, CO_ACT_NONE, pool.handle,
+                         ctypes.byref(h)) != CO_OK:
+            return False
+        co_bneck_destroy(h)
+        return True
+
+    # the destroy function is bound as a default so that objects collected
+    # during interpreter shutdown, after the module globals are cleared, still
+    # release their handles
+    def __del__(self, _destroy=co_bneck_destroy):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            _destroy(h)
+            self.handle = None
+
+    def _chain(self):
+        return [self.pw, self.dw, self.pool]
+
+    delay = property(lambda self: chain_delay(self._chain())[3])
+    receptive_field = property(lambda self: chain_delay(self._chain())[0])
+    t_stride = property(lambda self: chain_delay(self._chain())[2])
+    t_padding = property(lambda self: chain_delay(self._chain())[1])
+
+    def forward_step(self, x_t, update_state=True):
+        _need(x_t, self.pw.torch_dtype, self.pw.frame_shape(), "x_t")
+        z = torch.empty(self.pool.out_frame_shape(), dtype=self.pool.torch_dtype,
+                        device=x_t.device)
+        st = check(co_bneck_forward_step(self.handle, _ptr(x_t), _ptr(z),
+                                         1 if update_state else 0, _stream()),
+                   "co_bneck_forward_step")
+        return z if st == CO_OK else None
+
+    def forward_steps(self, x, update_state=True):
+        T = x.shape[2]
+        w, c, p = self.pw, self.dw, self.pool
+        _need(x, w.torch_dtype, (w.batch, w.in_channels, T) + w.in_size, "x")
+        # the pointwise layer emits every frame; the pool once per depthwise frame
+        cap = pool_out_frames(p.desc, p.steps, conv_out_frames(c.desc, c.steps, T))
+        z = torch.empty((p.batch, p.channels, cap) + p.out_size, dtype=p.torch_dtype,
+                        device=x.device)
+        n = i32()
+        check(co_bneck_forward_steps(self.handle, _ptr(x), T, _ptr(z), cap,
+                                     1 if update_state else 0, _stream(), ctypes.byref(n)),
+              "co_bneck_forward_steps")
+        return z if n.value else None
+
+    def forward(self, x):
+        y = self.pw.forward(x)
+        if self.relu1:
+            y = act_forward(y)
+        y = self.dw.forward(y)
+        if self.relu2:
+            y = act_forward(y)
+        return self.pool.forward(y)
+
+    def clean_state(self):
+        for m in self._chain():
+            m.clean_state()
+
+
 class ConvPool:
     """A depthwise CoConv followed by a CoPool over its whole output plane,
     stepped as one launch (co_convpool_*).  Both modules keep their states and
@@ -725,25 +883,55 @@ class ConvPool:
 class Sequential:
     """Section 3.3's Sequential: modules in a chain; an empty step output
     ends the step (downstream modules do not advance), and the chain's delay
-    follows Principle 6.  With fuse (the default) a depthwise CoConv directly
-    followed by a CoPool over its whole output plane runs as one ConvPool
-    launch per step, with identical results."""
+    follows Principle 6.  With fuse (the default) a pointwise CoConv, an
+    optional CoReLU, a depthwise CoConv, an optional CoReLU and a CoPool
+    over its whole output plane run as one Bottleneck launch per step, and
+    a depthwise CoConv directly followed by such a CoPool as one ConvPool
+    launch, with identical results."""
 
     def __init__(self, *modules, fuse=True):
         mods = list(modules)
         if fuse:
-            out, i = [], 0
-            while i < len(mods):
-                a = mods[i]
-                b = mods[i + 1] if i + 1 < len(mods) else None
-                if isinstance(a, CoConv) and isinstance(b, CoPool) and ConvPool.fits(a, b):
-                    out.append(ConvPool(a, b))
-                    i += 2
-                else:
-                    out.append(a)
-                    i += 1
-            mods = out
+            mods = self._fuse(mods)
         self.modules = mods
+
+    @staticmethod
+    def _bottleneck_at(mods, i):
+        """(Bottleneck, modules consumed) starting at mods[i], or None."""
+        j = i
+        parts = []
+        for kind in ("conv", "relu", "conv", "relu", "pool"):
+            m = mods[j] if j < len(mods) else None
+            if kind == "relu":
+                parts.append(isinstance(m, CoReLU))
+                j += 1 if isinstance(m, CoReLU) else 0
+                continue
+            want = CoConv if kind == "conv" else CoPool
+            if not isinstance(m, want):
+                return None
+            parts.append(m)
+            j += 1
+        pw, r1, dw, r2, pool = parts
+        if not Bottleneck.fits(pw, dw, pool):
+            return None
+        return Bottleneck(pw, r1, dw, r2, pool), j - i
+
+    def _fuse(self, mods):
+        out, i = [], 0
+        while i < len(mods):
+            a = mods[i]
+            b = mods[i + 1] if i + 1 < len(mods) else None
+            bn = self._bottleneck_at(mods, i)
+            if bn is not None:
+                out.append(bn[0])
+                i += bn[1]
+            elif isinstance(a, CoConv) and isinstance(b, CoPool) and ConvPool.fits(a, b):
+                out.append(ConvPool(a, b))
+                i += 2
+            else:
+                out.append(a)
+                i += 1
+        return out
 
     @property
     def delay(self):

@@ -2,6 +2,7 @@
 // Every entry point validates on the host before it enqueues anything, so a
 // negative status means nothing ran and the handle is unchanged.
 #include <algorithm>
+#include <cmath>
 #include <mutex>
 #include <new>
 #include <unordered_map>
@@ -37,6 +38,14 @@ struct co_convpool_handle {
   co_pool_handle* pool;
 };
 
+struct co_bneck_handle {
+  co_conv_handle* pw;   // pointwise convolution (1x1x1, delay 0)
+  int32_t act1;
+  co_conv_handle* dw;   // depthwise convolution
+  int32_t act2;
+  co_pool_handle* pool;
+};
+
 struct co_delay_handle {
   DelayGeom g;
   char* state;
@@ -44,6 +53,8 @@ struct co_delay_handle {
 };
 
 namespace {
+
+constexpr int64_t kMaxLaunchElems = int64_t(1) << 38;  // grid limit at 256 threads
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
@@ -54,7 +65,7 @@ co_status hip_status(hipError_t e) { return e == hipSuccess ? CO_OK : CO_EHIP; }
 // Live handles, by kind.  Every entry point checks its handle here, so a
 // destroyed handle, a second destroy, or a handle of another kind returns
 // CO_EINVAL without touching freed memory.
-enum class HKind : uint8_t { Conv, Pool, ConvPool, Delay };
+enum class HKind : uint8_t { Conv, Pool, ConvPool, Delay, Bneck };
 std::mutex g_live_mu;
 std::unordered_map<const void*, HKind>& live_map() {
   static auto* m = new std::unordered_map<const void*, HKind>();  // kept past exit
@@ -318,6 +329,44 @@ co_status co_conv_init_state(const co_conv_desc* desc, const void* weight, const
     return st;
   }
   return publish(h, HKind::Conv, out);
+}
+
+co_status co_conv_init_state_bn(const co_conv_desc* desc, const void* weight, const void* bias,
+                                const float* gamma, const float* beta, const float* mean,
+                                const float* var, float eps, void* state, int64_t state_bytes,
+                                void* stream, co_conv_handle** out) {
+  if (!out || !state || !weight || !gamma || !beta || !mean || !var) return CO_EINVAL;
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return CO_EINVAL;
+  ConvGeom g;
+  co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (g.has_bias && !bias) return CO_EINVAL;
+  const ConvLayout L = conv_layout(g);
+  if (state_bytes < L.total) return CO_ESTATE;
+  StateHeader hdr{kConvMagic, kStateVersion, conv_hash(g), L.total, g.algo, g.R};
+  co_conv_handle* h = new (std::nothrow) co_conv_handle{g, L, static_cast<char*>(state), 0};
+  if (!h) return CO_EINVAL;
+  st = hip_status(launch_conv_init_bn(g, L, h->state, weight, bias, gamma, beta, mean, var, eps,
+                                      hdr, as_stream(stream)));
+  if (st != CO_OK) {
+    delete h;
+    return st;
+  }
+  return publish(h, HKind::Conv, out);
+}
+
+co_status co_conv_fold_bn(const co_conv_desc* desc, const void* weight, const void* bias,
+                          const float* gamma, const float* beta, const float* mean,
+                          const float* var, float eps, void* w_out, void* b_out, void* stream) {
+  if (!weight || !gamma || !beta || !mean || !var || !w_out || !b_out) return CO_EINVAL;
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return CO_EINVAL;
+  ConvGeom g;
+  const co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (g.has_bias && !bias) return CO_EINVAL;
+  if (int64_t(g.Cg) * g.kT * g.kH * g.kW * g.Cout > kMaxLaunchElems) return CO_EINVAL;
+  return hip_status(launch_bn_fold(g, weight, bias, gamma, beta, mean, var, eps, w_out, b_out,
+                                   as_stream(stream)));
 }
 
 co_status co_conv_forward_step(co_conv_handle* h, const void* x_t, void* y_t,
@@ -684,10 +733,6 @@ co_status co_pool_destroy(co_pool_handle* h) {
 
 // ------------------------------------------------------------ delay, merges
 
-namespace {
-constexpr int64_t kMaxLaunchElems = int64_t(1) << 38;  // grid limit at 256 threads
-}
-
 co_status co_delay_query(const co_delay_desc* desc, int64_t* state_bytes) {
   if (!state_bytes) return CO_EINVAL;
   DelayGeom g;
@@ -797,6 +842,15 @@ co_status co_add_frames(const void* a, const void* x, void* y, int32_t rows, int
                                       dtype, as_stream(stream)));
 }
 
+co_status co_act_forward(const void* x, void* y, int64_t n, int32_t dtype, int32_t act,
+                         void* stream) {
+  if (n < 0 || (dtype != CO_F32 && dtype != CO_BF16)) return CO_EINVAL;
+  if (act != CO_ACT_NONE && act != CO_ACT_RELU) return CO_EINVAL;
+  if (n == 0) return CO_OK;
+  if (!x || !y || n > kMaxLaunchElems) return CO_EINVAL;
+  return hip_status(launch_act(x, y, n, dtype, act, as_stream(stream)));
+}
+
 co_status co_delay_clean_state(co_delay_handle* h, void* stream) {
   (void)stream;
   if (!live(h, HKind::Delay)) return CO_EINVAL;
@@ -873,14 +927,14 @@ co_status co_convpool_bind(co_conv_handle* conv, co_pool_handle* pool, co_convpo
 namespace {
 
 // A fused pair whose two handles are both still live.
-bool live_pair(const co_convpool_handle* h) {
+static bool live_pair(const co_convpool_handle* h) {
   return live(h, HKind::ConvPool) && live(h->conv, HKind::Conv) && live(h->pool, HKind::Pool);
 }
 
 // One fused step at the handles' counters, reading frame planes x_bc
 // elements apart; *emitted says whether z was written.
-co_status convpool_step(co_convpool_handle* h, const void* x_t, int64_t x_bc, void* z,
-                        int64_t z_bc, bool update, hipStream_t s, bool* emitted) {
+static co_status convpool_step(co_convpool_handle* h, const void* x_t, int64_t x_bc, void* z,
+                               int64_t z_bc, bool update, hipStream_t s, bool* emitted) {
   co_conv_handle* c = h->conv;
   co_pool_handle* p = h->pool;
   co_step_plan cplan;
@@ -970,6 +1024,119 @@ co_status co_convpool_forward_steps(co_convpool_handle* h, const void* x, int32_
   }
   *n_out = int32_t(k);
   return st;
+}
+
+// ------------------------------------------------------- fused bottleneck
+
+co_status co_bneck_bind(co_conv_handle* pw, int32_t act1, co_conv_handle* dw, int32_t act2,
+                        co_pool_handle* pool, co_bneck_handle** out) {
+  if (!live(pw, HKind::Conv) || !live(dw, HKind::Conv) || !live(pool, HKind::Pool) || !out)
+    return CO_EINVAL;
+  for (const int32_t a : {act1, act2})
+    if (a != CO_ACT_NONE && a != CO_ACT_RELU) return CO_EINVAL;
+  if (!bneck_supported(pw->g, dw->g, pool->g)) return CO_ENOTSUP;
+  co_bneck_handle* h = new (std::nothrow) co_bneck_handle{pw, act1, dw, act2, pool};
+  if (!h) return CO_EINVAL;
+  return publish(h, HKind::Bneck, out);
+}
+
+namespace {
+
+static bool live_bneck(const co_bneck_handle* h) {
+  return live(h, HKind::Bneck) && live(h->pw, HKind::Conv) && live(h->dw, HKind::Conv) &&
+         live(h->pool, HKind::Pool);
+}
+
+// One fused bottleneck step at the handles' counters, reading input planes
+// x_bc elements apart; *emitted says whether z was written.
+static co_status bneck_step(co_bneck_handle* h, const void* x_t, int64_t x_bc, void* z,
+                            int64_t z_bc, bool update, hipStream_t s, bool* emitted) {
+  co_conv_handle* pw = h->pw;
+  co_conv_handle* c = h->dw;
+  co_pool_handle* p = h->pool;
+  co_step_plan cplan;
+  conv_plan(c->g, c->n, update, &cplan);
+  co_pool_plan pplan;
+  if (cplan.emit) pool_plan(p->g, p->n, &pplan);
+  const bool pemit = cplan.emit && pplan.emit;
+  if (pemit && !z) return CO_EINVAL;
+  if (any_tap(cplan) || cplan.emit) {
+    const co_status st = hip_status(launch_bneck_step(
+        pw->g, pw->L, pw->state, h->act1, c->g, c->L, c->state, h->act2, p->g, p->L, p->state,
+        x_t, x_bc, z, z_bc, cplan, cplan.emit ? &pplan : nullptr, update, s));
+    if (st != CO_OK) return st;
+  }
+  if (update) {
+    ++pw->n;  // the pointwise convolution emits every frame (delay 0)
+    ++c->n;
+    if (cplan.emit) ++p->n;
+  }
+  *emitted = pemit;
+  return CO_OK;
+}
+
+}  // namespace
+
+co_status co_bneck_forward_step(co_bneck_handle* h, const void* x_t, void* z_t,
+                                int32_t update_state, void* stream) {
+  if (!live_bneck(h) || !x_t) return CO_EINVAL;
+  if (h->pw->n >= kMaxSteps || h->dw->n >= kMaxSteps) return CO_EINVAL;
+  bool emitted = false;
+  const co_status st = bneck_step(h, x_t, h->pw->g.S(), z_t, 1, update_state != 0,
+                                  as_stream(stream), &emitted);
+  if (st != CO_OK) return st;
+  return emitted ? CO_OK : CO_EMPTY;
+}
+
+co_status co_bneck_forward_steps(co_bneck_handle* h, const void* x, int32_t T, void* z,
+                                 int32_t z_cap_frames, int32_t update_state, void* stream,
+                                 int32_t* n_out) {
+  if (!live_bneck(h) || T < 0 || z_cap_frames < 0 || !n_out) return CO_EINVAL;
+  if (T > 0 && !x) return CO_EINVAL;
+  co_conv_handle* pw = h->pw;
+  co_conv_handle* c = h->dw;
+  co_pool_handle* p = h->pool;
+  if (T > kMaxSteps - pw->n || T > kMaxSteps - c->n) return CO_EINVAL;
+  // the pool steps once per emitted depthwise frame
+  const int64_t conv_out = conv_emissions(c->g, c->n, T);
+  const int64_t n_emit = pool_emissions(p->g, p->n, conv_out);
+  if (n_emit > z_cap_frames || (n_emit > 0 && !z)) return CO_EINVAL;
+  const int64_t S = pw->g.S();
+  const size_t esz = pw->g.dtype == CO_BF16 ? 2 : 4;
+  hipStream_t s = as_stream(stream);
+  const int64_t n0w = pw->n, n0c = c->n, n0p = p->n;
+  Backup bk_ring, bk_fifo;
+  if (!update_state) {
+    co_status st = backup_range(c->state + c->L.ring, int64_t(c->g.R) * c->L.ring_slot_elems * 4,
+                                s, &bk_ring);
+    if (st == CO_OK)
+      st = backup_range(p->state + p->L.valid, p->L.total - p->L.valid, s, &bk_fifo);
+    if (st != CO_OK) return st;
+  }
+  co_status st = CO_OK;
+  int64_t k = 0;
+  for (int32_t t = 0; t < T && st == CO_OK; ++t) {
+    bool emitted = false;
+    st = bneck_step(h, static_cast<const char*>(x) + size_t(t) * S * esz, int64_t(T) * S,
+                    static_cast<char*>(z) + size_t(k) * esz, z_cap_frames, true, s, &emitted);
+    if (emitted) ++k;
+  }
+  if (!update_state) {
+    const co_status r1 = restore_range(c->state + c->L.ring, s, &bk_ring);
+    const co_status r2 = restore_range(p->state + p->L.valid, s, &bk_fifo);
+    if (st == CO_OK) st = r1 != CO_OK ? r1 : r2;
+    pw->n = n0w;
+    c->n = n0c;
+    p->n = n0p;
+  }
+  *n_out = int32_t(k);
+  return st;
+}
+
+co_status co_bneck_destroy(co_bneck_handle* h) {
+  if (!retire(h, HKind::Bneck)) return CO_EINVAL;
+  delete h;
+  return CO_OK;
 }
 
 co_status co_convpool_destroy(co_convpool_handle* h) {

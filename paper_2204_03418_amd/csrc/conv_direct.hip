@@ -136,11 +136,57 @@ __global__ __launch_bounds__(kBlock) void pack_bias_kernel(int32_t n, int32_t ha
   if (i < n) dst[i] = has_bias ? to_f32<T>(src[i]) : 0.f;
 }
 
+// Weights as float32 in PyTorch order; each output channel's (per_out
+// consecutive values) times its scale when one is given.
 template <typename T>
-__global__ __launch_bounds__(kBlock) void pack_f32_kernel(int64_t n, const T* __restrict__ src,
+__global__ __launch_bounds__(kBlock) void pack_f32_kernel(int64_t n, int64_t per_out,
+                                                          const T* __restrict__ src,
+                                                          const float* __restrict__ wscale,
                                                           float* __restrict__ dst) {
   const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-  if (i < n) dst[i] = to_f32<T>(src[i]);
+  if (i < n) dst[i] = wscale ? to_f32<T>(src[i]) * wscale[i / per_out] : to_f32<T>(src[i]);
+}
+
+// Batch normalisation folded into a convolution (evaluation mode): the
+// per-channel scale gamma / sqrt(var + eps), written where the weight
+// packing reads it, and the folded bias bias * scale + beta - mean * scale.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void bn_fold_kernel(int32_t n, int32_t has_bias,
+                                                         const T* __restrict__ bias,
+                                                         const float* __restrict__ gamma,
+                                                         const float* __restrict__ beta,
+                                                         const float* __restrict__ mean,
+                                                         const float* __restrict__ var, float eps,
+                                                         float* __restrict__ scale,
+                                                         float* __restrict__ bdst) {
+  const int32_t o = int32_t(blockIdx.x) * kBlock + int32_t(threadIdx.x);
+  if (o >= n) return;
+  const float sc = gamma[o] / sqrtf(var[o] + eps);
+  const float b = has_bias ? to_f32<T>(bias[o]) : 0.f;
+  scale[o] = sc;
+  bdst[o] = fmaf(b, sc, beta[o] - mean[o] * sc);
+}
+
+// The folded weights and bias themselves, in the io dtype: each weight
+// scaled and rounded as the matrix-core packing does, the bias rounded from
+// the same float32 value the state holds.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void bn_fold_out_kernel(
+    int64_t n, int64_t per_out, int32_t cout, int32_t has_bias, const T* __restrict__ w,
+    const T* __restrict__ bias, const float* __restrict__ gamma, const float* __restrict__ beta,
+    const float* __restrict__ mean, const float* __restrict__ var, float eps,
+    T* __restrict__ w_out, T* __restrict__ b_out) {
+  const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (i < n) {
+    const int32_t o = int32_t(i / per_out);
+    w_out[i] = from_f32<T>(to_f32<T>(w[i]) * (gamma[o] / sqrtf(var[o] + eps)));
+  }
+  if (i < cout) {
+    const int32_t o = int32_t(i);
+    const float sc = gamma[o] / sqrtf(var[o] + eps);
+    const float b = has_bias ? to_f32<T>(bias[o]) : 0.f;
+    b_out[o] = from_f32<T>(fmaf(b, sc, beta[o] - mean[o] * sc));
+  }
 }
 
 __global__ void write_header_kernel(StateHeader h, StateHeader* dst) {
@@ -455,6 +501,42 @@ hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,
   }
 }
 
+namespace {
+
+// Weight packing of the handle's algorithm and the state header, after the
+// bias went in; wscale as launch_pack_gemm.
+hipError_t pack_weights_and_header(const ConvGeom& g, const ConvLayout& L, char* state,
+                                   const void* weight, const float* wscale,
+                                   const StateHeader& hdr, hipStream_t s) {
+  hipError_t e = hipSuccess;
+  if (g.algo == CO_ALGO_GEMM) {
+    e = launch_pack_gemm(g, L, state, weight, wscale, s);
+    if (e == hipSuccess && L.steps_weight_bytes > 0)
+      e = launch_pack_gemm_steps(g, L, state, weight, wscale, s);
+  } else if (g.algo == CO_ALGO_GEMM_REG) {
+    e = launch_pack_reg(g, L, state, weight, wscale, s);
+  } else if (g.algo == CO_ALGO_GEMM_IMG) {
+    e = launch_pack_img(g, L, state, weight, wscale, s);
+  } else {
+    const int64_t per_out = int64_t(g.Cg) * g.kT * g.kH * g.kW;
+    const int64_t n = int64_t(g.Cout) * per_out;
+    float* wdst = reinterpret_cast<float*>(state + L.weight);
+    if (g.dtype == CO_BF16)
+      hipLaunchKernelGGL(pack_f32_kernel<bf16_t>, dim3(grid_for(n)), dim3(kBlock), 0, s, n,
+                         per_out, static_cast<const bf16_t*>(weight), wscale, wdst);
+    else
+      hipLaunchKernelGGL(pack_f32_kernel<float>, dim3(grid_for(n)), dim3(kBlock), 0, s, n,
+                         per_out, static_cast<const float*>(weight), wscale, wdst);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, s, hdr,
+                     reinterpret_cast<StateHeader*>(state + L.header));
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, const void* bias, const StateHeader& hdr,
                             hipStream_t s) {
@@ -465,29 +547,49 @@ hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
   else
     hipLaunchKernelGGL(pack_bias_kernel<float>, dim3(grid_for(g.Cout)), dim3(kBlock), 0, s,
                        g.Cout, g.has_bias, static_cast<const float*>(bias), bdst);
-  hipError_t e = hipGetLastError();
+  const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (g.algo == CO_ALGO_GEMM) {
-    e = launch_pack_gemm(g, L, state, weight, s);
-    if (e == hipSuccess && L.steps_weight_bytes > 0) e = launch_pack_gemm_steps(g, L, state, weight, s);
-  } else if (g.algo == CO_ALGO_GEMM_REG) {
-    e = launch_pack_reg(g, L, state, weight, s);
-  } else if (g.algo == CO_ALGO_GEMM_IMG) {
-    e = launch_pack_img(g, L, state, weight, s);
-  } else {
-    const int64_t n = int64_t(g.Cout) * g.Cg * g.kT * g.kH * g.kW;
-    float* wdst = reinterpret_cast<float*>(state + L.weight);
-    if (g.dtype == CO_BF16)
-      hipLaunchKernelGGL(pack_f32_kernel<bf16_t>, dim3(grid_for(n)), dim3(kBlock), 0, s, n,
-                         static_cast<const bf16_t*>(weight), wdst);
-    else
-      hipLaunchKernelGGL(pack_f32_kernel<float>, dim3(grid_for(n)), dim3(kBlock), 0, s, n,
-                         static_cast<const float*>(weight), wdst);
-    e = hipGetLastError();
-  }
+  return pack_weights_and_header(g, L, state, weight, nullptr, hdr, s);
+}
+
+hipError_t launch_conv_init_bn(const ConvGeom& g, const ConvLayout& L, char* state,
+                               const void* weight, const void* bias, const float* gamma,
+                               const float* beta, const float* mean, const float* var, float eps,
+                               const StateHeader& hdr, hipStream_t s) {
+  // The scales go to the start of the ring (at least C_out floats, and not
+  // read before the first step writes it), where the weight packing reads
+  // them; the folded bias goes to the state's bias.
+  float* bdst = reinterpret_cast<float*>(state + L.bias);
+  float* scale = reinterpret_cast<float*>(state + L.ring);
+  if (g.dtype == CO_BF16)
+    hipLaunchKernelGGL(bn_fold_kernel<bf16_t>, dim3(grid_for(g.Cout)), dim3(kBlock), 0, s,
+                       g.Cout, g.has_bias, static_cast<const bf16_t*>(bias), gamma, beta, mean,
+                       var, eps, scale, bdst);
+  else
+    hipLaunchKernelGGL(bn_fold_kernel<float>, dim3(grid_for(g.Cout)), dim3(kBlock), 0, s,
+                       g.Cout, g.has_bias, static_cast<const float*>(bias), gamma, beta, mean,
+                       var, eps, scale, bdst);
+  const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, s, hdr,
-                     reinterpret_cast<StateHeader*>(state + L.header));
+  return pack_weights_and_header(g, L, state, weight, scale, hdr, s);
+}
+
+hipError_t launch_bn_fold(const ConvGeom& g, const void* weight, const void* bias,
+                          const float* gamma, const float* beta, const float* mean,
+                          const float* var, float eps, void* w_out, void* b_out, hipStream_t s) {
+  const int64_t per_out = int64_t(g.Cg) * g.kT * g.kH * g.kW;
+  const int64_t n = per_out * g.Cout;
+  const unsigned grid = grid_for(std::max<int64_t>(n, g.Cout));
+  if (g.dtype == CO_BF16)
+    hipLaunchKernelGGL(bn_fold_out_kernel<bf16_t>, dim3(grid), dim3(kBlock), 0, s, n, per_out,
+                       g.Cout, g.has_bias, static_cast<const bf16_t*>(weight),
+                       static_cast<const bf16_t*>(bias), gamma, beta, mean, var, eps,
+                       static_cast<bf16_t*>(w_out), static_cast<bf16_t*>(b_out));
+  else
+    hipLaunchKernelGGL(bn_fold_out_kernel<float>, dim3(grid), dim3(kBlock), 0, s, n, per_out,
+                       g.Cout, g.has_bias, static_cast<const float*>(weight),
+                       static_cast<const float*>(bias), gamma, beta, mean, var, eps,
+                       static_cast<float*>(w_out), static_cast<float*>(b_out));
   return hipGetLastError();
 }
 

@@ -478,6 +478,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void conv_step_gemm_kernel(
 template <typename T>
 __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfig c,
                                                            const T* __restrict__ w,
+                                                           const float* __restrict__ wscale,
                                                            uint4* __restrict__ out) {
   constexpr int KL = 16 / int(sizeof(T));
   const int64_t khw = int64_t(g.kH) * g.kW;
@@ -505,7 +506,8 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_kernel(ConvGeom g, GemmConfi
     const int cc = ch * c.CK + grp * KL + e;
     T val = T(0);
     if (n < g.kT * g.Cout && cc < g.Cin)
-      val = w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * g.kH + u) * g.kW) + v];
+      val = scaled_weight<T>(w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * g.kH + u) * g.kW) + v],
+                             wscale, o);
     pk.v[e] = val;
   }
   out[U] = pk.q;
@@ -1191,6 +1193,7 @@ __global__ __launch_bounds__(kWregThreads) void conv_steps_gemm_wreg_kernel(
 // persistent kernel reads them.
 __global__ __launch_bounds__(kBlock) void pack_gemm_steps_kernel(ConvGeom g, GemmStepsConfig c,
                                                                  const bf16_t* __restrict__ w,
+                                                                 const float* __restrict__ wscale,
                                                                  uint4* __restrict__ out) {
   const int64_t total = c.weight_bytes / 16;
   const int64_t U = int64_t(blockIdx.x) * kBlock + threadIdx.x;
@@ -1216,7 +1219,8 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_steps_kernel(ConvGeom g, Gem
     const int cc = ch * 32 + grp * 8 + e;
     bf16_t val = 0;
     if (t < g.kT && o < g.Cout && cc < g.Cin)
-      val = w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * g.kH + u) * g.kW) + v];
+      val = scaled_weight<bf16_t>(
+          w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * g.kH + u) * g.kW) + v], wscale, o);
     pk.v[e] = val;
   }
   out[U] = pk.q;
@@ -1415,29 +1419,29 @@ hipError_t launch_conv_steps_gemm(const ConvGeom& g, const ConvLayout& L, char* 
 }
 
 hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* state,
-                                  const void* weight, hipStream_t s) {
+                                  const void* weight, const float* wscale, hipStream_t s) {
   GemmStepsConfig c;
   if (!gemm_steps_config(g, &c)) return hipSuccess;
   const int64_t total = c.weight_bytes / 16;
   hipLaunchKernelGGL(pack_gemm_steps_kernel, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
-                     static_cast<const bf16_t*>(weight),
+                     static_cast<const bf16_t*>(weight), wscale,
                      reinterpret_cast<uint4*>(state + L.steps_weight));
   return hipGetLastError();
 }
 
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
-                            const void* weight, hipStream_t s) {
+                            const void* weight, const float* wscale, hipStream_t s) {
   GemmConfig c;
   if (!gemm_config(g, g.cfg, &c)) return hipErrorInvalidValue;
-  if (c.ws) return launch_pack_gemm_ws(g, c, L, state, weight, s);
+  if (c.ws) return launch_pack_gemm_ws(g, c, L, state, weight, wscale, s);
   const int64_t total = int64_t(c.n_tiles) * c.n_chunks * g.kH * g.kW * c.N_WG * 4;
   uint4* out = reinterpret_cast<uint4*>(state + L.weight);
   if (g.dtype == CO_BF16)
     hipLaunchKernelGGL(pack_gemm_kernel<bf16_t>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
-                       static_cast<const bf16_t*>(weight), out);
+                       static_cast<const bf16_t*>(weight), wscale, out);
   else
     hipLaunchKernelGGL(pack_gemm_kernel<float>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
-                       static_cast<const float*>(weight), out);
+                       static_cast<const float*>(weight), wscale, out);
   return hipGetLastError();
 }
 

@@ -347,6 +347,7 @@ __global__ __launch_bounds__(kThreads) void conv_step_gemm_ws_kernel(
 // order), zero past C_in and past kT * C_out.
 __global__ __launch_bounds__(kBlock) void pack_gemm_ws_kernel(ConvGeom g, GemmConfig c,
                                                               const bf16_t* __restrict__ w,
+                                                              const float* __restrict__ wscale,
                                                               uint4* __restrict__ out) {
   const int64_t total = int64_t(c.n_tiles) * c.n_chunks * kKHW * kWN * 64;
   const int64_t U = int64_t(blockIdx.x) * kBlock + threadIdx.x;
@@ -371,7 +372,8 @@ __global__ __launch_bounds__(kBlock) void pack_gemm_ws_kernel(ConvGeom g, GemmCo
     const int cc = ch * 32 + (lane >> 4) * 8 + e;
     bf16_t val = 0;
     if (n < g.kT * g.Cout && cc < g.Cin)
-      val = w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * 3 + u) * 3) + v];
+      val = scaled_weight<bf16_t>(w[((((int64_t(o) * g.Cin + cc) * g.kT + t) * 3 + u) * 3) + v],
+                                  wscale, o);
     pk.e[e] = val;
   }
   out[U] = pk.q;
@@ -451,11 +453,12 @@ hipError_t launch_conv_step_gemm_ws(const ConvGeom& g, const GemmConfig& c, cons
 }
 
 hipError_t launch_pack_gemm_ws(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
-                               char* state, const void* weight, hipStream_t s) {
+                               char* state, const void* weight, const float* wscale,
+                               hipStream_t s) {
   const int64_t total = int64_t(c.n_tiles) * c.n_chunks * kKHW * kWN * 64;
   if (total * 16 != L.weight_bytes) return hipErrorInvalidValue;
   hipLaunchKernelGGL(pack_gemm_ws_kernel, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
-                     static_cast<const bf16_t*>(weight),
+                     static_cast<const bf16_t*>(weight), wscale,
                      reinterpret_cast<uint4*>(state + L.weight));
   return hipGetLastError();
 }

@@ -370,6 +370,7 @@ conv_step_img_kernel(ConvGeom g, ImgArgs ia, const bf16_t* __restrict__ x, int64
 // and unit p of column n holds channel group p ^ ((n >> 2) & 3).
 __global__ __launch_bounds__(kBlock) void pack_img_kernel(ConvGeom g, ImgConfig c,
                                                           const bf16_t* __restrict__ w,
+                                                          const float* __restrict__ wscale,
                                                           uint4* __restrict__ out) {
   const int64_t idx = int64_t(blockIdx.x) * kBlock + threadIdx.x;
   if (idx >= c.weight_units) return;
@@ -396,7 +397,8 @@ __global__ __launch_bounds__(kBlock) void pack_img_kernel(ConvGeom g, ImgConfig 
       const int ch = cb * 32 + grp * 8 + 2 * e + h;
       uint32_t val = 0;
       if (col && ch < g.Cin)
-        val = w[((((int64_t(o) * g.Cin + ch) * g.kT + t) * g.kH + u) * g.kW) + v];
+        val = scaled_weight<bf16_t>(
+            w[((((int64_t(o) * g.Cin + ch) * g.kT + t) * g.kH + u) * g.kW) + v], wscale, o);
       pr |= val << (16 * h);
     }
     word[e] = pr;
@@ -504,11 +506,11 @@ hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* st
 }
 
 hipError_t launch_pack_img(const ConvGeom& g, const ConvLayout& L, char* state,
-                           const void* weight, hipStream_t s) {
+                           const void* weight, const float* wscale, hipStream_t s) {
   ImgConfig c;
   if (!img_config(g, &c)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(pack_img_kernel, dim3(grid_for(c.weight_units)), dim3(kBlock), 0, s, g, c,
-                     static_cast<const bf16_t*>(weight),
+                     static_cast<const bf16_t*>(weight), wscale,
                      reinterpret_cast<uint4*>(state + L.weight));
   return hipGetLastError();
 }

@@ -341,6 +341,7 @@ __global__ __launch_bounds__(64 * KSPLIT * kRegTiles) void conv_step_reg_kernel(
 template <typename T>
 __global__ __launch_bounds__(kBlock) void pack_reg_kernel(ConvGeom g, RegConfig c,
                                                           const T* __restrict__ w,
+                                                          const float* __restrict__ wscale,
                                                           uint4* __restrict__ out) {
   constexpr bool kBF = sizeof(T) == 2;
   const int ntaps = g.kH * g.kW;
@@ -359,7 +360,8 @@ __global__ __launch_bounds__(kBlock) void pack_reg_kernel(ConvGeom g, RegConfig 
   const bool ncol = n < g.kT * g.Cout;
   auto weight = [&](int cb, int c_in) -> T {
     if (!ncol || cb >= c.CS || c_in >= g.Cin) return T(0);
-    return w[(((int64_t(o) * g.Cin + c_in) * g.kT + t) * g.kH + u) * g.kW + v];
+    return scaled_weight<T>(w[(((int64_t(o) * g.Cin + c_in) * g.kT + t) * g.kH + u) * g.kW + v],
+                            wscale, o);
   };
   uint32_t word[4] = {0u, 0u, 0u, 0u};
   if constexpr (kBF) {
@@ -868,17 +870,17 @@ hipError_t launch_conv_steps_reg(const ConvGeom& g, const ConvLayout& L, char* s
 }
 
 hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,
-                           const void* weight, hipStream_t s) {
+                           const void* weight, const float* wscale, hipStream_t s) {
   RegConfig c;
   if (!reg_config(g, g.cfg, &c)) return hipErrorInvalidValue;
   const int64_t total = int64_t(c.n_frags) * c.U * 64;
   uint4* out = reinterpret_cast<uint4*>(state + L.weight);
   if (g.dtype == CO_BF16)
     hipLaunchKernelGGL(pack_reg_kernel<bf16_t>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
-                       static_cast<const bf16_t*>(weight), out);
+                       static_cast<const bf16_t*>(weight), wscale, out);
   else
     hipLaunchKernelGGL(pack_reg_kernel<float>, dim3(grid_for(total)), dim3(kBlock), 0, s, g, c,
-                       static_cast<const float*>(weight), out);
+                       static_cast<const float*>(weight), wscale, out);
   return hipGetLastError();
 }
 

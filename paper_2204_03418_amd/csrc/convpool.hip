@@ -53,41 +53,17 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// The depthwise step of one lane (output pixel p of plane (stream, channel
+// c), flat plane index bc, ring index ridx) from its stencil values xv, then
+// the pool step on the completed frame (see the kernels below): shared by
+// the fused kernels so that they give the separate steps' bits.
 template <typename T, int KH, int KW>
-__global__ __launch_bounds__(64 * kCpWaves) void convpool_step_kernel(
-    ConvGeom g, const T* __restrict__ x, int64_t x_bc, const float* __restrict__ w,
-    const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot, CpTaps at,
-    PoolGeom pg, T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo, int64_t fifo_slot,
-    float* __restrict__ valid, CpPool pp, FastDiv fd_Cout, FastDiv fd_Wo) {
-  const int lane = int(threadIdx.x) & 63;
-  const int wave = int(threadIdx.x) >> 6;
-  const int BC = g.B * g.Cout;
-  const int bc = int(blockIdx.x) * kCpWaves + wave;
-  if (bc >= BC) return;  // whole waves; no barrier follows
-  const int So = g.Ho * g.Wo;
-  const bool pl = lane < So;
-  const int p = pl ? lane : 0;
-  const int bq = fdiv(bc, fd_Cout), c = bc - bq * g.Cout;
-  const int i = fdiv(p, fd_Wo), jo = p - i * g.Wo;
-  const int ridx = (c * g.B + bq) * So + p;
-
-  // the depthwise step (see conv_step_dw_kernel)
-  // frame planes are x_bc elements apart (S for a single frame, T * S when
-  // the frame is read in place from a clip)
-  const int x_extent = int(((int64_t(g.B) * g.Cin - 1) * x_bc + g.H * g.W) * int64_t(sizeof(T)));
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, x_extent);
-  const int plane = int(int64_t(bc) * x_bc);
-  float xv[KH * KW];
-#pragma unroll
-  for (int u = 0; u < KH; ++u) {
-    const int hi = i * g.sH + u * g.dH - g.pH;
-#pragma unroll
-    for (int v = 0; v < KW; ++v) {
-      const int wi = jo * g.sW + v * g.dW - g.pW;
-      const bool in = pl && hi >= 0 && hi < g.H && wi >= 0 && wi < g.W;
-      xv[u * KW + v] = load_or_zero<T>(xr, plane + hi * g.W + wi, in);
-    }
-  }
+__device__ __forceinline__ void dw_pool_tail(
+    const float (&xv)[KH * KW], bool pl, int lane, int c, int bc, int ridx, const ConvGeom& g,
+    const float* __restrict__ w, const float* __restrict__ bias, float* __restrict__ ring,
+    int64_t ring_slot, const CpTaps& at, int act2, const PoolGeom& pg, T* __restrict__ z,
+    int64_t z_bc, float* __restrict__ fifo, int64_t fifo_slot, float* __restrict__ valid,
+    const CpPool& pp) {
   const float* wc = w + int64_t(c) * g.kT * (KH * KW);
   const float bo = bias[c];
   T yv = from_f32<T>(0.f);
@@ -105,6 +81,9 @@ __global__ __launch_bounds__(64 * kCpWaves) void convpool_step_kernel(
       yv = from_f32<T>(acc + bo);
     }
   }
+  // an activation between the convolution and the pool applies to the
+  // emitted (rounded) frame, as a separate elementwise step would
+  if (act2 == CO_ACT_RELU) yv = from_f32<T>(fmaxf(to_f32<T>(yv), 0.f));
   if (!pp.step) return;
 
   // the pool step on the frame just completed (see pool_step_kernel): lane p
@@ -151,6 +130,115 @@ __global__ __launch_bounds__(64 * kCpWaves) void convpool_step_kernel(
     out = div > 0.f ? acc / div : 0.f;
   }
   z[int64_t(bc) * z_bc] = from_f32<T>(out);
+}
+
+template <typename T, int KH, int KW>
+__global__ __launch_bounds__(64 * kCpWaves) void convpool_step_kernel(
+    ConvGeom g, const T* __restrict__ x, int64_t x_bc, const float* __restrict__ w,
+    const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot, CpTaps at,
+    PoolGeom pg, T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo, int64_t fifo_slot,
+    float* __restrict__ valid, CpPool pp, FastDiv fd_Cout, FastDiv fd_Wo) {
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = int(threadIdx.x) >> 6;
+  const int BC = g.B * g.Cout;
+  const int bc = int(blockIdx.x) * kCpWaves + wave;
+  if (bc >= BC) return;  // whole waves; no barrier follows
+  const int So = g.Ho * g.Wo;
+  const bool pl = lane < So;
+  const int p = pl ? lane : 0;
+  const int bq = fdiv(bc, fd_Cout), c = bc - bq * g.Cout;
+  const int i = fdiv(p, fd_Wo), jo = p - i * g.Wo;
+  const int ridx = (c * g.B + bq) * So + p;
+
+  // the depthwise step (see conv_step_dw_kernel)
+  // frame planes are x_bc elements apart (S for a single frame, T * S when
+  // the frame is read in place from a clip)
+  const int x_extent = int(((int64_t(g.B) * g.Cin - 1) * x_bc + g.H * g.W) * int64_t(sizeof(T)));
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, x_extent);
+  const int plane = int(int64_t(bc) * x_bc);
+  float xv[KH * KW];
+#pragma unroll
+  for (int u = 0; u < KH; ++u) {
+    const int hi = i * g.sH + u * g.dH - g.pH;
+#pragma unroll
+    for (int v = 0; v < KW; ++v) {
+      const int wi = jo * g.sW + v * g.dW - g.pW;
+      const bool in = pl && hi >= 0 && hi < g.H && wi >= 0 && wi < g.W;
+      xv[u * KW + v] = load_or_zero<T>(xr, plane + hi * g.W + wi, in);
+    }
+  }
+  dw_pool_tail<T, KH, KW>(xv, pl, lane, c, bc, ridx, g, w, bias, ring, ring_slot, at, CO_ACT_NONE,
+                          pg, z, z_bc, fifo, fifo_slot, valid, pp);
+}
+
+// Fused step of an X3D-style bottleneck (sections 3.2-3.3: a pointwise
+// convolution, batch normalisation and activation, a depthwise continual
+// convolution, batch normalisation and activation, and the pool over the
+// plane; the normalisations are folded into the convolutions' weights at
+// init).  A workgroup owns kBnWaves channel planes of one stream.  The
+// stream's input frame (C_in x H x W, at most 64 pixels per plane) is staged
+// into LDS once; each wave computes its channel's pointwise output at every
+// pixel (lane = pixel) exactly as the pointwise (1x1x1) direct step kernel
+// does -- products accumulated over the input channels in order with fmaf
+// from zero, the bias added, the result rounded to the io dtype and the
+// activation applied -- and writes it into its own zero-haloed plane in LDS.
+// The depthwise stencil then reads that plane instead of memory, and the
+// depthwise and pool steps follow as in convpool_step_kernel.  The
+// intermediate frames never leave the CU; the results equal the separate
+// steps bit for bit.
+constexpr int kBnWaves = 4;
+
+template <typename T, int KH, int KW>
+__global__ __launch_bounds__(64 * kBnWaves) void bneck_step_kernel(
+    int32_t Ci, const T* __restrict__ x, int64_t x_bc, const float* __restrict__ w1,
+    const float* __restrict__ b1, int32_t act1, ConvGeom g, const float* __restrict__ w,
+    const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot, CpTaps at,
+    int32_t act2, PoolGeom pg, T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo,
+    int64_t fifo_slot, float* __restrict__ valid, CpPool pp, int32_t cblocks, FastDiv fd_S,
+    FastDiv fd_W, FastDiv fd_Wo) {
+  extern __shared__ float lds[];
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int S = g.H * g.W;
+  const int Hp = g.H + 2 * g.pH, Wp = g.W + 2 * g.pW;
+  const int bq = int(blockIdx.x) / cblocks;
+  const int cb = int(blockIdx.x) - bq * cblocks;
+  float* xs = lds;                 // the stream's input frame, [C_in][S]
+  float* zs = lds + Ci * S;        // kBnWaves zero-haloed planes of Hp x Wp
+  float* zw = zs + wave * Hp * Wp;
+  for (int e = tid; e < kBnWaves * Hp * Wp; e += 64 * kBnWaves) zs[e] = 0.f;
+  for (int e = tid; e < Ci * S; e += 64 * kBnWaves) {
+    const int ci = fdiv(e, fd_S), q = e - ci * S;
+    xs[e] = to_f32<T>(x[(int64_t(bq) * Ci + ci) * x_bc + q]);
+  }
+  __syncthreads();
+  const int c = cb * kBnWaves + wave;
+  const bool cvalid = c < g.Cout;
+  if (cvalid && lane < S) {
+    const float* wr = w1 + int64_t(c) * Ci;
+    float acc = 0.f;
+    for (int ci = 0; ci < Ci; ++ci) acc = fmaf(wr[ci], xs[ci * S + lane], acc);
+    T z1 = from_f32<T>(acc + b1[c]);
+    if (act1 == CO_ACT_RELU) z1 = from_f32<T>(fmaxf(to_f32<T>(z1), 0.f));
+    const int qi = fdiv(lane, fd_W), qj = lane - qi * g.W;
+    zw[(qi + g.pH) * Wp + qj + g.pW] = to_f32<T>(z1);
+  }
+  __syncthreads();
+  if (!cvalid) return;  // after the last barrier
+  const int So = g.Ho * g.Wo;
+  const bool pl = lane < So;
+  const int p = pl ? lane : 0;
+  const int i = fdiv(p, fd_Wo), jo = p - i * g.Wo;
+  float xv[KH * KW];
+#pragma unroll
+  for (int u = 0; u < KH; ++u)
+#pragma unroll
+    for (int v = 0; v < KW; ++v)
+      xv[u * KW + v] = pl ? zw[(i * g.sH + u * g.dH) * Wp + jo * g.sW + v * g.dW] : 0.f;
+  const int bc = bq * g.Cout + c;
+  const int ridx = (c * g.B + bq) * So + p;
+  dw_pool_tail<T, KH, KW>(xv, pl, lane, c, bc, ridx, g, w, bias, ring, ring_slot, at, act2, pg,
+                          z, z_bc, fifo, fifo_slot, valid, pp);
 }
 
 template <typename T, int KH, int KW>
@@ -523,6 +611,91 @@ hipError_t cps_dispatch(const ConvGeom& g, const ConvLayout& L, char* cstate, co
 }
 
 }  // namespace
+
+namespace {
+
+// The plans of one fused step, as cp_launch builds them.
+void cp_plans(const ConvGeom& g, const co_step_plan& cplan, const co_pool_plan* pplan,
+              bool update, CpTaps* at, CpPool* pp) {
+  at->n = 0;
+  for (int j = 0; j < g.kT; ++j) {
+    if (cplan.action[j] == CO_TAP_NONE) continue;
+    at->tap[at->n] = j;
+    at->act[at->n] = cplan.action[j];
+    at->slot[at->n] = cplan.slot[j] < 0 ? 0 : cplan.slot[j];
+    ++at->n;
+  }
+  *pp = CpPool{};
+  pp->step = pplan ? 1 : 0;
+  if (pplan) {
+    pp->update = update ? 1 : 0;
+    pp->emit = pplan->emit;
+    pp->write_slot = pplan->write_slot;
+    for (int t = 0; t < CO_MAX_TAPS; ++t) pp->src[t] = pplan->src[t];
+  }
+}
+
+template <typename T, int KH, int KW>
+hipError_t bn_launch(const ConvGeom& pw, const ConvLayout& PWL, char* pwstate, int32_t act1,
+                     const ConvGeom& g, const ConvLayout& L, char* cstate, int32_t act2,
+                     const PoolGeom& pg, const PoolLayout& PL, char* pstate, const void* x,
+                     int64_t x_bc, void* z, int64_t z_bc, const co_step_plan& cplan,
+                     const co_pool_plan* pplan, bool update, hipStream_t s) {
+  CpTaps at;
+  CpPool pp;
+  cp_plans(g, cplan, pplan, update, &at, &pp);
+  if (at.n == 0 && !pp.step) return hipSuccess;
+  const int32_t cblocks = int32_t((g.Cout + kBnWaves - 1) / kBnWaves);
+  const int S = g.H * g.W;
+  const size_t lds = size_t(pw.Cin * S + kBnWaves * (g.H + 2 * g.pH) * (g.W + 2 * g.pW)) * 4;
+  hipLaunchKernelGGL((bneck_step_kernel<T, KH, KW>), dim3(unsigned(g.B * cblocks)),
+                     dim3(64 * kBnWaves), lds, s, pw.Cin, static_cast<const T*>(x), x_bc,
+                     reinterpret_cast<const float*>(pwstate + PWL.weight),
+                     reinterpret_cast<const float*>(pwstate + PWL.bias), act1, g,
+                     reinterpret_cast<const float*>(cstate + L.weight),
+                     reinterpret_cast<const float*>(cstate + L.bias),
+                     reinterpret_cast<float*>(cstate + L.ring), L.ring_slot_elems, at, act2, pg,
+                     static_cast<T*>(z), z_bc, reinterpret_cast<float*>(pstate + PL.fifo),
+                     PL.fifo_slot_elems, reinterpret_cast<float*>(pstate + PL.valid), pp, cblocks,
+                     make_fastdiv(uint32_t(S)), make_fastdiv(uint32_t(g.W)),
+                     make_fastdiv(uint32_t(g.Wo)));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool bneck_supported(const ConvGeom& pw, const ConvGeom& g, const PoolGeom& pg) {
+  const int64_t S = int64_t(g.H) * g.W;
+  return convpool_supported(g, pg) && pw.algo == CO_ALGO_DIRECT && pw.G == 1 && pw.kT == 1 &&
+         pw.kH == 1 && pw.kW == 1 && pw.sT == 1 && pw.sH == 1 && pw.sW == 1 && pw.pT == 0 &&
+         pw.pH == 0 && pw.pW == 0 && pw.dtype == g.dtype && pw.B == g.B && pw.Cout == g.Cin &&
+         pw.H == g.H && pw.W == g.W && S <= 64 && int64_t(pw.Cin) * S <= kBnMaxStage &&
+         int64_t(pw.B) * pw.Cin * S * (pw.dtype == CO_BF16 ? 2 : 4) < (int64_t(1) << 31);
+}
+
+hipError_t launch_bneck_step(const ConvGeom& pw, const ConvLayout& PWL, char* pwstate,
+                             int32_t act1, const ConvGeom& g, const ConvLayout& L, char* cstate,
+                             int32_t act2, const PoolGeom& pg, const PoolLayout& PL, char* pstate,
+                             const void* x, int64_t x_bc, void* z, int64_t z_bc,
+                             const co_step_plan& cplan, const co_pool_plan* pplan, bool update,
+                             hipStream_t s) {
+  if (g.dtype == CO_BF16) {
+    if (g.kH == 3 && g.kW == 3)
+      return bn_launch<bf16_t, 3, 3>(pw, PWL, pwstate, act1, g, L, cstate, act2, pg, PL, pstate,
+                                     x, x_bc, z, z_bc, cplan, pplan, update, s);
+    if (g.kH == 1 && g.kW == 1)
+      return bn_launch<bf16_t, 1, 1>(pw, PWL, pwstate, act1, g, L, cstate, act2, pg, PL, pstate,
+                                     x, x_bc, z, z_bc, cplan, pplan, update, s);
+  } else {
+    if (g.kH == 3 && g.kW == 3)
+      return bn_launch<float, 3, 3>(pw, PWL, pwstate, act1, g, L, cstate, act2, pg, PL, pstate, x,
+                                    x_bc, z, z_bc, cplan, pplan, update, s);
+    if (g.kH == 1 && g.kW == 1)
+      return bn_launch<float, 1, 1>(pw, PWL, pwstate, act1, g, L, cstate, act2, pg, PL, pstate, x,
+                                    x_bc, z, z_bc, cplan, pplan, update, s);
+  }
+  return hipErrorInvalidValue;
+}
 
 bool convpool_supported(const ConvGeom& g, const PoolGeom& pg) {
   const bool taps = (g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1);

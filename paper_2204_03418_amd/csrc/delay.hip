@@ -161,6 +161,32 @@ hipError_t launch_delay_steps(const DelayGeom& g, char* state, const void* x, in
   return steps_t<float>(g, state, x, T, a, y, y_frames, n0, t_first, nout, update, s);
 }
 
+namespace {
+
+// Elementwise activation: the stateless maps (nn.ReLU and the like) a
+// continual network applies to each frame as it applies them to a clip.
+// ReLU is exact in either dtype: max(v, 0) of a representable value.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void act_kernel(const T* __restrict__ x, T* __restrict__ y,
+                                                     int64_t n, int32_t act) {
+  const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n) return;
+  y[i] = act == CO_ACT_RELU ? from_f32<T>(fmaxf(to_f32<T>(x[i]), 0.f)) : x[i];
+}
+
+}  // namespace
+
+hipError_t launch_act(const void* x, void* y, int64_t n, int32_t dtype, int32_t act,
+                      hipStream_t s) {
+  if (dtype == CO_BF16)
+    hipLaunchKernelGGL(act_kernel<bf16_t>, dim3(grid_for(n)), dim3(kBlock), 0, s,
+                       static_cast<const bf16_t*>(x), static_cast<bf16_t*>(y), n, act);
+  else
+    hipLaunchKernelGGL(act_kernel<float>, dim3(grid_for(n)), dim3(kBlock), 0, s,
+                       static_cast<const float*>(x), static_cast<float*>(y), n, act);
+  return hipGetLastError();
+}
+
 hipError_t launch_add_frames(const void* a, const void* x, void* y, int64_t rows, int32_t E,
                              int32_t a_frames, int32_t x_frames, int32_t x_offset, int32_t dtype,
                              hipStream_t s) {

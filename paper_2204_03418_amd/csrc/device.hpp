@@ -37,6 +37,15 @@ __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <>
 __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
+// Weight w of output channel o times that channel's scale (batch
+// normalisation folded into the weights at init), rounded once to T; with no
+// scale, w unchanged.
+template <typename T>
+__device__ __forceinline__ T scaled_weight(T w, const float* scale, int o) {
+  if (!scale) return w;
+  return from_f32<T>(to_f32<T>(w) * scale[o]);
+}
+
 // n / f.d for 0 <= n < 2^31 (see FastDiv).
 __device__ __forceinline__ int fdiv(int n, const FastDiv& f) {
   return int((uint64_t(uint32_t(n)) * f.m) >> f.s);

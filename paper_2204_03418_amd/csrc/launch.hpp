@@ -32,6 +32,18 @@ hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,
 hipError_t launch_conv_init(const ConvGeom& g, const ConvLayout& L, char* state,
                             const void* weight, const void* bias, const StateHeader& hdr,
                             hipStream_t stream);
+// The same with an evaluation-mode batch normalisation folded in: per output
+// channel o, scale = gamma / sqrt(var + eps) multiplies the weights and the
+// bias becomes bias * scale + beta - mean * scale (gamma, beta, mean, var:
+// float32, C_out each).
+hipError_t launch_conv_init_bn(const ConvGeom& g, const ConvLayout& L, char* state,
+                               const void* weight, const void* bias, const float* gamma,
+                               const float* beta, const float* mean, const float* var, float eps,
+                               const StateHeader& hdr, hipStream_t stream);
+// Folded weights (C_out, C_in/G, kT, kH, kW) and bias (C_out) in the io dtype.
+hipError_t launch_bn_fold(const ConvGeom& g, const void* weight, const void* bias,
+                          const float* gamma, const float* beta, const float* mean,
+                          const float* var, float eps, void* w_out, void* b_out, hipStream_t s);
 
 // Clip-mode regular convolution (symmetric temporal padding).
 hipError_t launch_conv_clip(const ConvGeom& g, int32_t T, int32_t T_out, const void* weight,
@@ -114,11 +126,11 @@ hipError_t launch_conv_steps_reg(const ConvGeom& g, const ConvLayout& L, char* s
                                  const void* x, int64_t x_bc, int32_t T, int32_t count, void* y,
                                  int64_t y_bc, int64_t n0, bool update, hipStream_t stream);
 hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,
-                           const void* weight, hipStream_t stream);
+                           const void* weight, const float* wscale, hipStream_t stream);
 hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* state,
                                 const StepIO& io, const co_step_plan& plan, hipStream_t stream);
 hipError_t launch_pack_img(const ConvGeom& g, const ConvLayout& L, char* state,
-                           const void* weight, hipStream_t stream);
+                           const void* weight, const float* wscale, hipStream_t stream);
 // Persistent forward_steps of the LDS-tiled GEMM (bf16; same conventions as
 // the depthwise one): temporal stride 1 and dilation 1, kT <= 3, 3x3 or 1x1
 // taps, tiles within the LDS and staging budgets.  x is the clip pointer
@@ -128,16 +140,20 @@ hipError_t launch_conv_steps_gemm(const ConvGeom& g, const ConvLayout& L, char* 
                                   const void* x, int64_t x_bc, int32_t T, int32_t count, void* y,
                                   int64_t y_bc, int64_t n0, bool update, hipStream_t stream);
 hipError_t launch_pack_gemm_steps(const ConvGeom& g, const ConvLayout& L, char* state,
-                                  const void* weight, hipStream_t stream);
+                                  const void* weight, const float* wscale, hipStream_t stream);
+// Weight packing: wscale (float32, C_out) multiplies each output channel's
+// weights before they are rounded to the packed dtype (batch normalisation
+// folded at init); null leaves them as given.
 hipError_t launch_pack_gemm(const ConvGeom& g, const ConvLayout& L, char* state,
-                            const void* weight, hipStream_t stream);
+                            const void* weight, const float* wscale, hipStream_t stream);
 // The warp-specialized configuration of the GEMM step (conv_gemm_ws.hip):
 // bf16, 3x3 taps; its weights packed in the order its consumer waves load.
 hipError_t launch_conv_step_gemm_ws(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
                                     char* state, const StepIO& io, const co_step_plan& plan,
                                     hipStream_t stream);
 hipError_t launch_pack_gemm_ws(const ConvGeom& g, const GemmConfig& c, const ConvLayout& L,
-                               char* state, const void* weight, hipStream_t stream);
+                               char* state, const void* weight, const float* wscale,
+                               hipStream_t stream);
 
 // Fused depthwise convolution step + global spatial pool step (convpool.hip):
 // one launch per step; pplan is null when the convolution does not emit
@@ -160,6 +176,20 @@ hipError_t launch_convpool_steps(const ConvGeom& g, const ConvLayout& L, char* c
                                  const void* x, int32_t T, void* z, int64_t z_cap, int64_t n0c,
                                  int64_t n0p, bool update, hipStream_t stream);
 
+// Fused X3D-style bottleneck step (convpool.hip): a pointwise (1x1x1,
+// direct-packed, delay 0) convolution with activation act1, a depthwise
+// convolution with activation act2 and the pool over its plane, in one
+// launch; the three handles' plans as for the separate steps (the pointwise
+// one always emits).  Input planes x_bc elements apart.
+constexpr int64_t kBnMaxStage = 12288;  // input channels x plane pixels staged in LDS
+bool bneck_supported(const ConvGeom& pw, const ConvGeom& g, const PoolGeom& pg);
+hipError_t launch_bneck_step(const ConvGeom& pw, const ConvLayout& PWL, char* pwstate,
+                             int32_t act1, const ConvGeom& g, const ConvLayout& L, char* cstate,
+                             int32_t act2, const PoolGeom& pg, const PoolLayout& PL, char* pstate,
+                             const void* x, int64_t x_bc, void* z, int64_t z_bc,
+                             const co_step_plan& cplan, const co_pool_plan* pplan, bool update,
+                             hipStream_t stream);
+
 // Delay line and residual merges (delay.hip).
 hipError_t launch_delay_init(const DelayGeom& g, char* state, const StateHeader& hdr,
                              hipStream_t stream);
@@ -168,6 +198,9 @@ hipError_t launch_delay_step(const DelayGeom& g, char* state, const void* x, con
 hipError_t launch_delay_steps(const DelayGeom& g, char* state, const void* x, int32_t T,
                               const void* a, void* y, int32_t y_frames, int64_t n0,
                               int32_t t_first, int32_t nout, bool update, hipStream_t stream);
+// Elementwise activation of n contiguous elements (y may alias x).
+hipError_t launch_act(const void* x, void* y, int64_t n, int32_t dtype, int32_t act,
+                      hipStream_t stream);
 hipError_t launch_add_frames(const void* a, const void* x, void* y, int64_t rows, int32_t E,
                              int32_t a_frames, int32_t x_frames, int32_t x_offset, int32_t dtype,
                              hipStream_t stream);

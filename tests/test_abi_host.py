@@ -465,6 +465,13 @@ def test_stale_and_foreign_handles_rejected_without_device():
     assert C.co_pool_destroy(bogus) == C.CO_EINVAL
     assert C.co_delay_destroy(bogus) == C.CO_EINVAL
     assert C.co_convpool_destroy(bogus) == C.CO_EINVAL
+    assert C.co_bneck_destroy(bogus) == C.CO_EINVAL
+    out = ctypes.c_void_p()
+    assert C.co_bneck_bind(bogus, 0, bogus, 0, bogus, ctypes.byref(out)) == C.CO_EINVAL
+    assert C.co_bneck_forward_step(bogus, bogus, bogus, 1, None) == C.CO_EINVAL
+    n32 = C.i32()
+    assert C.co_bneck_forward_steps(bogus, bogus, 1, bogus, 1, 1, None,
+                                    ctypes.byref(n32)) == C.CO_EINVAL
     assert C.co_conv_algo_name(bogus) == b"none"
 
 
@@ -513,3 +520,28 @@ def test_warp_specialized_gemm_selection():
     st, big = q(64, 192, 192, (14, 14), algo=C.CO_ALGO_AUTO)
     st2, forced = q(64, 192, 192, (14, 14))
     assert st == st2 == C.CO_OK and big.state_bytes == forced.state_bytes
+
+
+def test_batch_norm_and_activation_validation_without_device():
+    """co_conv_init_state_bn / co_conv_fold_bn reject missing statistics and
+    a negative or non-finite eps, and co_act_forward an unknown activation or
+    dtype, all before anything is launched; zero elements is a no-op."""
+    d = desc1d(p=2)
+    dev = ctypes.c_void_p(0x1000)
+    h = ctypes.c_void_p()
+    for eps in (-1e-5, float("nan"), float("inf")):
+        assert C.co_conv_init_state_bn(ctypes.byref(d), dev, dev, dev, dev, dev, dev, eps, dev,
+                                       1 << 20, None, ctypes.byref(h)) == C.CO_EINVAL
+        assert C.co_conv_fold_bn(ctypes.byref(d), dev, dev, dev, dev, dev, dev, eps, dev, dev,
+                                 None) == C.CO_EINVAL
+    assert C.co_conv_init_state_bn(ctypes.byref(d), dev, dev, None, dev, dev, dev, 1e-5, dev,
+                                   1 << 20, None, ctypes.byref(h)) == C.CO_EINVAL
+    assert C.co_conv_fold_bn(ctypes.byref(d), dev, dev, dev, dev, dev, None, 1e-5, dev, dev,
+                             None) == C.CO_EINVAL
+    assert C.co_conv_init_state_bn(ctypes.byref(d), dev, dev, dev, dev, dev, dev, 1e-5, dev,
+                                   16, None, ctypes.byref(h)) == C.CO_ESTATE
+    assert C.co_act_forward(dev, dev, 4, C.CO_F32, 7, None) == C.CO_EINVAL
+    assert C.co_act_forward(dev, dev, 4, 9, C.CO_ACT_RELU, None) == C.CO_EINVAL
+    assert C.co_act_forward(dev, dev, -1, C.CO_F32, C.CO_ACT_RELU, None) == C.CO_EINVAL
+    assert C.co_act_forward(None, None, 0, C.CO_BF16, C.CO_ACT_RELU, None) == C.CO_OK
+    assert C.co_act_forward(None, dev, 4, C.CO_F32, C.CO_ACT_RELU, None) == C.CO_EINVAL

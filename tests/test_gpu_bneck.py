@@ -1,0 +1,350 @@
+"""GPU parity of batch normalisation folded into the continual convolutions
+(co_conv_init_state_bn, co_conv_fold_bn), the activation call
+(co_act_forward) and the fused X3D bottleneck step (co_bneck_*), through the
+C ABI, against the oracle chains conv -> BatchNormEval [-> ReLU] (section
+3.2: continual convolutions compose with per-frame layers; section 3.3:
+Sequential; Principle 6 for the chain's delay)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2204_03418_amd import synth
+from parity_util import (UNIT_ROUNDOFF, U32, assert_close, chain_atol, conv_terms, np64, say,
+                         window_terms)
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2204_03418_amd import coinf
+DEV = "cuda"
+EPS = 1e-5
+
+
+def bn_params(C, seed):
+    """Evaluation-mode statistics: gamma near 1, small beta and mean, a
+    positive variance (float32, as nn.BatchNorm keeps them)."""
+    gamma = 1.0 + 0.3 * synth.normal((C,), seed)
+    beta = 0.1 * synth.normal((C,), seed + 1)
+    mean = 0.2 * synth.normal((C,), seed + 2)
+    var = 0.5 + synth.normal((C,), seed + 3).abs()
+    return gamma, beta, mean, var
+
+
+def dev_bn(p):
+    return tuple(t.to(DEV) for t in p) + (EPS,)
+
+
+def oracle_bn(p):
+    return oracle.BatchNormEval(*(np64(t) for t in p), EPS)
+
+
+def fold_atol(x, w, p, groups, stride, padding, dilation, b, dtype):
+    """Extra error of the folded layer against conv -> BN in float64: each
+    folded weight w * s is rounded once to the packed dtype (at most 2^-8 of
+    itself for bfloat16 packs, a few float32 ulps otherwise), so an output is
+    off by at most that times its sum of |w s| |x| -- computed by the oracle's
+    convolution of |x| with |w s| -- plus the float32 rounding of the folded
+    bias b s + beta - mean s."""
+    gamma, beta, mean, var = (np64(t) for t in p)
+    s = gamma / np.sqrt(var + EPS)
+    ws = np.abs(np64(w)) * s.reshape((-1,) + (1,) * (w.dim() - 1))
+    mag = oracle.conv_forward(np.abs(np64(x)), ws, None, stride, padding, dilation, groups)
+    u = UNIT_ROUNDOFF[torch.bfloat16] if dtype == torch.bfloat16 else 4 * U32
+    bias_mag = np.abs(beta) + np.abs(mean * s) + (0 if b is None else np.abs(np64(b) * s))
+    return u * float(mag.max()) + 4 * U32 * float(bias_mag.max())
+
+
+ALGO_CASES = [
+    # algo, B, Cin, Cout, kernel, in_size, padding, groups, dtype
+    ("direct", 2, 5, 7, (3, 3, 3), (6, 5), (1, 1, 1), 1, "f32"),
+    ("direct", 2, 6, 4, (2, 3, 3), (5, 5), (0, 1, 1), 1, "bf16"),
+    ("gemm", 3, 40, 24, (3, 3, 3), (9, 11), (0, 1, 1), 1, "bf16"),
+    ("gemm", 2, 20, 36, (2, 3, 3), (7, 6), (1, 0, 1), 1, "f32"),
+    ("gemm_reg", 3, 12, 40, (3, 3, 3), (7, 9), (1, 1, 1), 1, "bf16"),
+    ("gemm_reg", 4, 16, 16, (1, 3, 3), (8, 8), (0, 1, 1), 1, "f32"),
+    ("gemm_ws", 3, 40, 24, (3, 3, 3), (8, 10), (0, 1, 1), 1, "bf16"),
+    ("gemm_img", 2, 48, 64, (3, 3, 3), (12, 12), (1, 1, 1), 1, "bf16"),
+    ("depthwise", 3, 10, 10, (3, 3, 3), (7, 7), (1, 1, 1), 10, "bf16"),
+    ("depthwise", 2, 6, 6, (2, 3, 3), (5, 6), (0, 1, 1), 6, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", ALGO_CASES, ids=lambda c: f"bn_{c[0]}_{c[-1]}_{c[2]}")
+def test_conv_bn_folded_init(case):
+    """co_conv_init_state_bn for every kernel family: steps (single and
+    forward_steps, whichever kernels they run) emit BN(conv(x)) of the
+    oracle within the folding bound; the clip forward through
+    co_conv_fold_bn too."""
+    algo, B, ci, co_, k, size, pad, G, dt = case
+    say("conv+bn", case)
+    tdt = synth.torch_dtype(dt)
+    T = 9
+    x = synth.normal((B, ci, T) + size, 5100 + ci, dtype=dt)
+    w = synth.normal((co_, ci // G) + k, 5101 + co_, std=0.3, dtype=dt)
+    b = synth.normal((co_,), 5102, std=0.1, dtype=dt)
+    p = bn_params(co_, 5110 + co_)
+    xd = x.to(DEV)
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=pad, groups=G,
+                            algo=algo, bn=dev_bn(p))
+
+    conv = make()
+    assert conv.algo.startswith(algo), conv.algo
+    ref = oracle.ContinualChain(oracle.ContinualConv(np64(w), np64(b), padding=pad, groups=G),
+                                oracle_bn(p))
+    r = ref.forward_steps(np64(x))
+    extra = fold_atol(x, w, p, G, 1, pad, 1, b, tdt)
+    terms = conv_terms(w) + 1
+    outs = [conv.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    assert sum(o is None for o in outs) == conv.delay
+    got = torch.stack([o for o in outs if o is not None], dim=2)
+    assert_close(np64(got), r, tdt, f"{algo} bn steps", terms=terms, extra_atol=extra)
+    ys = make().forward_steps(xd)
+    assert_close(np64(ys), r, tdt, f"{algo} bn forward_steps", terms=terms, extra_atol=extra)
+    # clip mode with the folded weights and the io-dtype folded bias
+    clip = conv.forward(xd)
+    rc = oracle_bn(p).forward(oracle.conv_forward(np64(x), np64(w), np64(b), 1, pad, 1, G))
+    bias_round = UNIT_ROUNDOFF[tdt] * float(np.abs(np64(conv.folded()[1])).max())
+    assert_close(np64(clip), rc, tdt, f"{algo} bn clip", terms=terms,
+                 extra_atol=extra + bias_round)
+
+
+def test_fold_bn_matches_state_packing():
+    """co_conv_fold_bn's weights are the matrix-core packing's rounding of
+    w * s: a bf16 layer built from the folded weights without BN steps to
+    the same bits as the BN-initialised layer (same kernel, same packed
+    operands, the bias only differs by its bf16 rounding, so it is set to
+    zero here by a beta that cancels it)."""
+    say("fold == pack")
+    B, ci, co_, size = 3, 40, 24, (8, 10)
+    x = synth.normal((B, ci, 6) + size, 5200, dtype="bf16").to(DEV)
+    w = synth.normal((co_, ci, 3, 3, 3), 5201, std=0.3, dtype="bf16")
+    gamma, _, mean, var = bn_params(co_, 5210)
+    beta = mean * gamma / torch.sqrt(var + EPS)  # folded bias ~ 0 (no conv bias)
+    p = (gamma, beta, mean, var)
+    a = coinf.CoConv(w.to(DEV), None, batch=B, in_size=size, padding=(0, 1, 1), algo="gemm",
+                     bn=dev_bn(p))
+    wf, bf = a.folded()
+    # the folded weights are w * s rounded once to bf16
+    s_ = gamma / torch.sqrt(var + EPS)
+    want = (w.float() * s_.reshape(-1, 1, 1, 1, 1)).to(torch.bfloat16)
+    assert torch.allclose(wf.cpu().float(), want.float(), rtol=2.0 ** -8, atol=0)
+    c = coinf.CoConv(wf, bf, batch=B, in_size=size, padding=(0, 1, 1), algo="gemm")
+    assert a.algo == c.algo
+    ya, yc = a.forward_steps(x), c.forward_steps(x)
+    # identical products; the biases differ by at most the bf16 rounding of
+    # a value near zero
+    diff = (ya.float() - yc.float()).abs().max().item()
+    bmax = float(np.abs(np64(bf)).max())
+    assert diff <= 2 * (bmax + UNIT_ROUNDOFF[torch.bfloat16] * float(ya.float().abs().max())), diff
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_act_forward_relu(dt):
+    """co_act_forward(RELU) equals max(x, 0) bit for bit; NONE copies."""
+    say("act", dt)
+    x = synth.normal((3, 5, 7, 11), 5300, dtype=dt)
+    xd = x.to(DEV)
+    y = coinf.act_forward(xd, "relu")
+    assert torch.equal(y.cpu(), torch.clamp(x, min=0))
+    assert torch.equal(coinf.act_forward(xd, "none").cpu(), x)
+    e = torch.empty(0, dtype=x.dtype, device=DEV)
+    assert coinf.act_forward(e).numel() == 0
+
+
+BNECK_CASES = [
+    # B, C_in, C (depthwise channels), in_size, dw kernel, dw padding, pool kind, pool kT,
+    # relu1, relu2, dtype
+    (4, 8, 16, (7, 7), (3, 3, 3), (1, 1, 1), "avg", 4, True, True, "bf16"),   # the X3D block
+    (3, 6, 10, (5, 6), (2, 3, 3), (0, 1, 1), "max", 3, True, False, "f32"),
+    (2, 5, 7, (4, 4), (3, 1, 1), (2, 0, 0), "avg", 2, False, True, "f32"),
+    (5, 12, 9, (8, 8), (3, 3, 3), (1, 1, 1), "avg", 3, True, True, "bf16"),  # 64-pixel planes
+]
+
+
+def _bneck_parts(case, seed):
+    B, ci, C, size, k, pad, kind, pk, r1, r2, dt = case
+    tdt = synth.torch_dtype(dt)
+    w1 = synth.normal((C, ci, 1, 1, 1), seed, std=0.4, dtype=dt)
+    b1 = synth.normal((C,), seed + 1, std=0.1, dtype=dt)
+    w2 = synth.normal((C, 1) + k, seed + 2, std=0.3, dtype=dt)
+    p1, p2 = bn_params(C, seed + 10), bn_params(C, seed + 20)
+    ho, wo = size[0] - k[1] + 1 + 2 * pad[1], size[1] - k[2] + 1 + 2 * pad[2]
+
+    def modules():
+        pw = coinf.CoConv(w1.to(DEV), b1.to(DEV), batch=B, in_size=size, algo="direct",
+                          bn=dev_bn(p1))
+        dw = coinf.CoConv(w2.to(DEV), None, batch=B, in_size=size, padding=pad, groups=C,
+                          bn=dev_bn(p2))
+        pool = coinf.CoPool(kind, batch=B, channels=C, kernel=(pk, ho, wo), in_size=(ho, wo),
+                            stride=(1, ho, wo), dtype=tdt)
+        return pw, dw, pool
+
+    def seq(fuse=True):
+        pw, dw, pool = modules()
+        mods = [pw] + ([coinf.CoReLU()] if r1 else []) + [dw] + ([coinf.CoReLU()] if r2 else [])
+        return coinf.Sequential(*mods, pool, fuse=fuse)
+
+    def oracle_chain():
+        mods = [oracle.ContinualConv(np64(w1), np64(b1)), oracle_bn(p1)]
+        mods += [oracle.ReLU()] if r1 else []
+        mods += [oracle.ContinualConv(np64(w2), None, padding=pad, groups=C), oracle_bn(p2)]
+        mods += [oracle.ReLU()] if r2 else []
+        mods += [oracle.ContinualPool(kind, (pk, ho, wo), stride=(1, ho, wo))]
+        return oracle.ContinualChain(*mods)
+
+    return (w1, b1, w2, p1, p2, ho, wo), modules, seq, oracle_chain
+
+
+def _bneck_atol(case, parts, x):
+    """Extra error of the fused chain against the float64 oracle chain: the
+    pointwise output (folded weights, rounded to the io dtype) passes its
+    error through the rectifier (1-Lipschitz) and the folded depthwise
+    weights (gain: their largest absolute row sum); the depthwise output's
+    own error passes through the pool (gain 1)."""
+    B, ci, C, size, k, pad, kind, pk, r1, r2, dt = case
+    tdt = synth.torch_dtype(dt)
+    w1, b1, w2, p1, p2, ho, wo = parts
+    xx = np64(x)
+    o1 = oracle_bn(p1).forward(oracle.conv_forward(xx, np64(w1), np64(b1)))
+    if r1:
+        o1 = np.maximum(o1, 0)
+    o2 = oracle_bn(p2).forward(oracle.conv_forward(o1, np64(w2), None, 1, pad, 1, C))
+    s2 = np64(p2[0]) / np.sqrt(np64(p2[3]) + EPS)
+    gain2 = float((np.abs(np64(w2)).reshape(C, -1).sum(axis=1) * np.abs(s2)).max())
+    e1 = chain_atol(o1, conv_terms(w1) + 1, tdt) + fold_atol(x, w1, p1, 1, 1, 0, 1, b1, tdt)
+    e2 = chain_atol(o2, conv_terms(w2, False) + 1, tdt)
+    e2 += fold_atol(torch.from_numpy(o1), w2, p2, C, 1, pad, 1, None, tdt)
+    return gain2 * e1 * (1 + UNIT_ROUNDOFF[tdt]) + e2, gain2
+
+
+@pytest.mark.parametrize("case", BNECK_CASES, ids=lambda c: f"bneck_{c[6]}_{c[-1]}_{c[1]}")
+def test_fused_bottleneck(case):
+    """co_bneck: one launch per step equals the separate steps (pointwise
+    conv+BN, ReLU, depthwise conv+BN, ReLU, pool) bit for bit -- steps,
+    clips in one and two calls, fused and separate calls mixed,
+    update_state=False -- the chain's delay is Principle 6's, and the output
+    matches the oracle chain."""
+    B, ci, C, size, k, pad, kind, pk, r1, r2, dt = case
+    say("bneck", case)
+    tdt = synth.torch_dtype(dt)
+    T = 13
+    x = synth.normal((B, ci, T) + size, 5400 + ci, dtype=dt)
+    xd = x.to(DEV)
+    parts, modules, seq, oracle_chain = _bneck_parts(case, 5410 + C)
+    fused = seq()
+    assert len(fused.modules) == 1 and isinstance(fused.modules[0], coinf.Bottleneck)
+    separate = seq(fuse=False)
+    assert not any(isinstance(m, (coinf.Bottleneck, coinf.ConvPool)) for m in separate.modules)
+    # Principle 6: the pointwise layer and the rectifiers add no delay
+    dw_delay = k[0] - pad[0] - 1
+    assert fused.delay == separate.delay == dw_delay + pk - 1
+    got = [fused.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    ref = [separate.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
+    assert [g is None for g in got] == [r is None for r in ref]
+    assert next(i for i, g in enumerate(got) if g is not None) == fused.delay
+    for g_, r_ in zip(got, ref):
+        if r_ is not None:
+            assert torch.equal(g_, r_)
+    steps = torch.stack([r_ for r_ in ref if r_ is not None], dim=2)
+    # a clip in one call, and in two calls continuing the state
+    assert torch.equal(seq().forward_steps(xd), steps)
+    s2 = seq()
+    za, zb = s2.forward_steps(xd[:, :, :6].contiguous()), s2.forward_steps(xd[:, :, 6:].contiguous())
+    assert torch.equal(torch.cat([z_ for z_ in (za, zb) if z_ is not None], dim=2), steps)
+    # fused and separate calls on the same modules, mixed
+    pw, dw, pool = modules()
+    bn = coinf.Bottleneck(pw, r1, dw, r2, pool)
+
+    def sep_step(t):
+        y = pw.forward_step(xd[:, :, t].contiguous())
+        y = coinf.act_forward(y) if r1 else y
+        y = dw.forward_step(y)
+        if y is None:
+            return None
+        y = coinf.act_forward(y) if r2 else y
+        return pool.forward_step(y)
+
+    mix = [sep_step(t) for t in range(4)] + [bn.forward_step(xd[:, :, t].contiguous())
+                                             for t in range(4, 9)]
+    mix += [sep_step(t) for t in range(9, T)]
+    for g_, r_ in zip(mix, ref):
+        assert (g_ is None and r_ is None) or torch.equal(g_, r_)
+    # update_state=False leaves every state and counter as it was
+    torch.cuda.synchronize()
+    st = [m.state.clone() for m in (pw, dw, pool)]
+    n = (pw.steps, dw.steps, pool.steps)
+    bn.forward_steps(xd[:, :, :5].contiguous(), update_state=False)
+    bn.forward_step(xd[:, :, 0].contiguous(), update_state=False)
+    torch.cuda.synchronize()
+    assert all(torch.equal(m.state, s_) for m, s_ in zip((pw, dw, pool), st))
+    assert (pw.steps, dw.steps, pool.steps) == n
+    # the oracle chain
+    r = oracle_chain().forward_steps(np64(x))
+    extra, gain2 = _bneck_atol(case, parts, x)
+    terms = window_terms((pk, parts[5], parts[6]))
+    assert_close(np64(steps), r, tdt, "bneck vs oracle", terms=terms, extra_atol=extra)
+    # clip mode through the folded layers, whose biases are rounded to the io
+    # dtype: the pointwise one's error passes through the depthwise weights
+    clip = fused.forward(xd)
+    rc = oracle_chain().forward(np64(x))
+    fb = fused.modules[0]
+    b1f, b2f = (float(np.abs(np64(m.folded()[1])).max()) for m in (fb.pw, fb.dw))
+    b_round = UNIT_ROUNDOFF[tdt] * (gain2 * b1f + b2f)
+    assert_close(np64(clip), rc, tdt, "bneck clip", terms=terms, extra_atol=extra + b_round)
+
+
+def test_bottleneck_refused_shapes():
+    """co_bneck_bind refuses layers it cannot fuse (CO_ENOTSUP): a pointwise
+    layer not built on the direct kernel, a plane over 64 pixels, channels
+    that do not chain."""
+    say("bneck refusals")
+    B, ci, C = 2, 4, 6
+    w1 = synth.normal((C, ci, 1, 1, 1), 5500, dtype="f32").to(DEV)
+    w2 = synth.normal((C, 1, 3, 3, 3), 5501, dtype="f32").to(DEV)
+
+    def dw(size):
+        return coinf.CoConv(w2, None, batch=B, in_size=size, padding=(1, 1, 1), groups=C)
+
+    def pool(size):
+        return coinf.CoPool("avg", batch=B, channels=C, kernel=(2,) + size, in_size=size,
+                            stride=(1,) + size)
+
+    pw_gemm = coinf.CoConv(w1, None, batch=B, in_size=(5, 5), algo="gemm")
+    assert not coinf.Bottleneck.fits(pw_gemm, dw((5, 5)), pool((5, 5)))
+    pw_big = coinf.CoConv(w1, None, batch=B, in_size=(9, 9), algo="direct")
+    assert not coinf.Bottleneck.fits(pw_big, dw((9, 9)), pool((9, 9)))
+    pw = coinf.CoConv(w1, None, batch=B, in_size=(5, 5), algo="direct")
+    assert coinf.Bottleneck.fits(pw, dw((5, 5)), pool((5, 5)))
+    w3 = synth.normal((C + 1, ci, 1, 1, 1), 5502, dtype="f32").to(DEV)
+    pw3 = coinf.CoConv(w3, None, batch=B, in_size=(5, 5), algo="direct")
+    assert not coinf.Bottleneck.fits(pw3, dw((5, 5)), pool((5, 5)))
+    h = coinf.ctypes.c_void_p()
+    d5, p5 = dw((5, 5)), pool((5, 5))
+    assert coinf.co_bneck_bind(pw.handle, 3, d5.handle, 0, p5.handle,
+                               coinf.ctypes.byref(h)) == coinf.CO_EINVAL
+
+
+def test_bottleneck_workload():
+    """The X3D-M stage-5 bottleneck front at full size (16 streams, 192 ->
+    432 channels, 7x7, bf16): fused against separate steps bit for bit over
+    10 frames, and against the oracle chain on sampled streams."""
+    say("bneck workload")
+    case = (16, 192, 432, (7, 7), (3, 3, 3), (1, 1, 1), "avg", 4, True, True, "bf16")
+    B, ci, C = case[:3]
+    T = 10
+    x = synth.normal((B, ci, T, 7, 7), 5600, dtype="bf16")
+    xd = x.to(DEV)
+    parts, modules, seq, oracle_chain = _bneck_parts(case, 5610)
+    fused = seq()
+    assert isinstance(fused.modules[0], coinf.Bottleneck)
+    z = fused.forward_steps(xd)
+    ref = seq(fuse=False).forward_steps(xd)
+    assert torch.equal(z, ref)
+    sel = [0, 9, 15]
+    xs = x[sel]
+    r = oracle_chain().forward_steps(np64(xs))
+    assert_close(np64(z[sel]), r, torch.bfloat16, "bneck workload",
+                 terms=window_terms((4, 7, 7)), extra_atol=_bneck_atol(case, parts, xs)[0])
