@@ -22,6 +22,8 @@ steps and is repeated (at least 5 times, and until the repetitions cover
   over the resident clip, and (depthwise) through the fused conv+pool step;
 * workloads: the eager step, its kernel and forward_steps, with rooflines,
   for every named workload;
+* bottleneck: the fused X3D bottleneck front against its layers stepped
+  separately;
 * cpu_baseline: the oracle timed on a bounded sample of the same workload on
   the host cores, at the host's thread count and at one thread.
 """
@@ -379,6 +381,116 @@ class Workload:
         return self.c.batch / (us * 1e-6), out
 
 
+def bottleneck_entry(dev, K):
+    """The fused X3D bottleneck front (pointwise conv+BN+ReLU, depthwise
+    conv+BN+ReLU, average pool; one co_bneck launch per step) against the
+    same modules stepped separately (pointwise layer on the kernel AUTO
+    picks, then the activation, depthwise and pool launches), and the fused
+    forward_steps over the resident clip.  Priced on the block's algorithmic
+    FLOPs (pointwise + depthwise) and bytes (input frame, the depthwise
+    ring's kT-1 slots read and written, the pool's reduced frames, output,
+    weights once)."""
+    import torch
+
+    from paper_2204_03418_amd import coinf, synth
+
+    sp = synth.BOTTLENECK
+    x, w1, b1, w2, st1, st2 = synth.bottleneck_inputs(sp)
+    B, Ci, C, (H, W) = sp.batch, sp.in_channels, sp.channels, sp.in_size
+    T = x.shape[2]
+    tdt = synth.torch_dtype(sp.dtype)
+    xd = x.to(dev)
+    frames = [x[:, :, t].contiguous().to(dev) for t in range(T)]
+    fptr = [ctypes.c_void_p(f.data_ptr()) for f in frames]
+    bn1 = tuple(t.to(dev) for t in st1) + (1e-5,)
+    bn2 = tuple(t.to(dev) for t in st2) + (1e-5,)
+    kT = sp.kernel[0]
+    Ho, Wo = H + 2 * sp.padding[1] - sp.kernel[1] + 1, W + 2 * sp.padding[2] - sp.kernel[2] + 1
+
+    def modules(pw_algo):
+        pw = coinf.CoConv(w1.to(dev), b1.to(dev), batch=B, in_size=sp.in_size, algo=pw_algo,
+                          bn=bn1)
+        dw = coinf.CoConv(w2.to(dev), None, batch=B, in_size=sp.in_size, padding=sp.padding,
+                          groups=C, bn=bn2)
+        pool = coinf.CoPool("avg", batch=B, channels=C, kernel=sp.pool_kernel,
+                            in_size=(Ho, Wo), stride=(1, Ho, Wo), dtype=tdt, device=dev)
+        return pw, dw, pool
+
+    stream = torch.cuda.current_stream()
+    spp = ctypes.c_void_p(stream.cuda_stream)
+    z = torch.empty((B, C, 1, 1), dtype=tdt, device=dev)
+    zp = ctypes.c_void_p(z.data_ptr())
+    fused_mods = modules("auto")
+    bn = coinf.Bottleneck(fused_mods[0], True, fused_mods[1], True, fused_mods[2])
+    step = coinf.co_bneck_forward_step
+    state = {"n": 0}
+
+    def run_fused(count):
+        for i in range(state["n"], state["n"] + count):
+            step(bn.handle, fptr[i % T], zp, 1, spp)
+        state["n"] += count
+
+    run_fused(2 * T)
+    ms, _ = timed(lambda: run_fused(K), stream)
+    fused_us = ms * 1e3 / K
+
+    pw, dw, pool = modules("auto")
+    y1 = torch.empty((B, C) + tuple(sp.in_size), dtype=tdt, device=dev)
+    y2 = torch.empty((B, C, Ho, Wo), dtype=tdt, device=dev)
+    y1p, y2p = ctypes.c_void_p(y1.data_ptr()), ctypes.c_void_p(y2.data_ptr())
+    act = coinf.co_act_forward
+    dt_code = coinf.DTYPES[tdt]
+    cstep, pstep = coinf.co_conv_forward_step, coinf.co_pool_forward_step
+    sep = {"n": 0}
+
+    def run_separate(count):
+        for i in range(sep["n"], sep["n"] + count):
+            cstep(pw.handle, fptr[i % T], y1p, 1, spp)
+            act(y1p, y1p, y1.numel(), dt_code, coinf.CO_ACT_RELU, spp)
+            if cstep(dw.handle, y1p, y2p, 1, spp) == coinf.CO_OK:
+                act(y2p, y2p, y2.numel(), dt_code, coinf.CO_ACT_RELU, spp)
+                pstep(pool.handle, y2p, zp, 1, spp)
+        sep["n"] += count
+
+    run_separate(2 * T)
+    ms, _ = timed(lambda: run_separate(K), stream)
+    sep_us = ms * 1e3 / K
+
+    calls = max(1, -(-K // T))
+
+    def clip():
+        for _ in range(calls):
+            bn.forward_steps(xd)
+
+    clip()
+    ms, _ = timed(clip, stream)
+    fs_us = ms * 1e3 / (calls * T)
+
+    esz = 2 if sp.dtype == "bf16" else 4
+    flops = 2 * B * H * W * C * Ci + 2 * B * C * Ho * Wo * kT * sp.kernel[1] * sp.kernel[2]
+    pk = sp.pool_kernel[0]
+    nbytes = (B * Ci * H * W * esz + 2 * (kT - 1) * B * C * Ho * Wo * 4
+              + (pk + 1) * B * C * 4 + B * C * esz + C * Ci * 4 + C * kT * 9 * 4)
+    ridge = PEAK_VALU_F32_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+    def roof(us):
+        if flops / nbytes >= ridge:
+            a = flops / (us * 1e-6) / 1e12
+            return {"bound": "alu", "achieved": round(a, 3), "peak": PEAK_VALU_F32_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(a / PEAK_VALU_F32_TFLOPS, 5)}
+        a = nbytes / (us * 1e-6) / 1e9
+        return {"bound": "hbm", "achieved": round(a, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(a / PEAK_HBM_GBS, 5)}
+
+    return {"workload": sp.name, "batch": B, "dtype": sp.dtype,
+            "fused_step": round(B / (fused_us * 1e-6), 1), "fused_us_per_step": round(fused_us, 3),
+            "separate_step": round(B / (sep_us * 1e-6), 1),
+            "separate_us_per_step": round(sep_us, 3), "separate_pointwise_algo": pw.algo,
+            "fused_forward_steps": round(B / (fs_us * 1e-6), 1),
+            "fused_forward_steps_us_per_frame": round(fs_us, 3),
+            "flops_per_step": flops, "bytes_per_step": nbytes, "roofline": roof(fused_us)}
+
+
 def main():
     args = parse()
     if args.copy_mib > 0:
@@ -439,10 +551,12 @@ def main():
             modes_roof["cold_conv_step"] = cr
 
     table = {}
+    bneck = None
     if not args.no_workloads:
         for name in synth.WORKLOADS:
             table[name] = workload_entry(wk if name == args.workload else None, name, dev, K,
                                          args.algo, args.warmup)
+        bneck = bottleneck_entry(dev, K)
 
     cpu = None
     if not args.no_cpu:
@@ -475,6 +589,7 @@ def main():
         "modes": modes,
         "modes_roofline": modes_roof,
         "workloads": table,
+        "bottleneck": bneck,
     }
     print(json.dumps(out))
 

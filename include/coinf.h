@@ -444,7 +444,8 @@ co_status co_pool_destroy(co_pool_handle* h);
  * (sections 3.2-3.3; the X3D bottleneck closes with such a pair), when the
  * pool's spatial window is the whole output plane (kernel = stride = the
  * plane, no spatial padding: a 1x1 pooled frame), the plane has at most 64
- * pixels and the kernels are 3x3 or 1x1.  The fused handle borrows the two
+ * pixels, the kernels are 3x3 or 1x1 with at most 8 temporal taps.  The
+ * fused handle borrows the two
  * handles (it neither owns nor frees them) and advances their states and
  * step counters exactly as co_conv_forward_step followed, when the
  * convolution emits, by co_pool_forward_step would: the results are
@@ -475,21 +476,23 @@ co_status co_convpool_destroy(co_convpool_handle* h);
 /*
  * Fused step of an X3D-style bottleneck (sections 3.2-3.3; Table 2's CoX3D
  * networks are built from such blocks): a pointwise convolution (1x1x1,
- * stride 1, no padding, groups 1, made with CO_ALGO_DIRECT: delay 0) and its
- * activation act1, a depthwise continual convolution and its activation
- * act2, and the pool over the depthwise output's whole plane (the pair
- * co_convpool_bind accepts), with batch normalisations folded into the
- * convolutions by co_conv_init_state_bn.  One launch per step: the input
- * frame of each stream is staged on chip once, and neither intermediate
+ * stride 1, no padding, groups 1: delay 0) on the register-GEMM kernel
+ * (CO_ALGO_GEMM_REG, which AUTO picks for such layers) and its activation
+ * act1, a depthwise continual convolution and its activation act2, and the
+ * pool over the depthwise output's whole plane (the pair co_convpool_bind
+ * accepts), with batch normalisations folded into the convolutions by
+ * co_conv_init_state_bn.  One launch per step: each workgroup computes a
+ * 16-channel slice of the pointwise output on the matrix cores into LDS and
+ * runs the depthwise and pool steps from there, so neither intermediate
  * frame is written anywhere.  The handle borrows the three handles and
  * advances their step counters and states exactly as the separate steps
  * (co_conv_forward_step, co_act_forward, co_conv_forward_step,
  * co_act_forward, co_pool_forward_step) would: the results are identical
- * bit for bit, and fused and separate calls can be mixed.  The chain's
- * delay is the depthwise convolution's plus the pool's (Principle 6; the
- * pointwise convolution adds none).  Input planes of at most 64 pixels and
- * C_in x H x W <= 12288.  CO_ENOTSUP when the layers do not fit, CO_EINVAL
- * for an unknown activation.
+ * bit for bit, and fused and separate calls can be mixed.  The chain's delay
+ * is the depthwise convolution's plus the pool's (Principle 6; the pointwise
+ * convolution adds none).  Planes of at most 64 pixels (128 with the
+ * depthwise padding).  CO_ENOTSUP when the layers do not fit, CO_EINVAL for
+ * an unknown activation.
  */
 typedef struct co_bneck_handle co_bneck_handle;
 

@@ -741,7 +741,8 @@ class Bottleneck:
     batch normalisations folded into the convolutions) stepped as one launch
     per frame (co_bneck_*).  The three modules keep their states and step
     counters, and the outputs equal stepping them separately bit for bit.
-    The pointwise layer must be a 1x1x1 CoConv made with algo="direct"."""
+    The pointwise layer must be a 1x1x1 CoConv on the register-GEMM kernel
+    (algo "gemm_reg", AUTO's choice for such layers)."""
 
     def __init__(self, pw, relu1, dw, relu2, pool):
         h = ctypes.c_void_p()

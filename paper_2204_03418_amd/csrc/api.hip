@@ -1097,12 +1097,14 @@ co_status co_bneck_forward_steps(co_bneck_handle* h, const void* x, int32_t T, v
   co_conv_handle* c = h->dw;
   co_pool_handle* p = h->pool;
   if (T > kMaxSteps - pw->n || T > kMaxSteps - c->n) return CO_EINVAL;
+  const int64_t S = pw->g.S();
+  const int64_t esz = pw->g.dtype == CO_BF16 ? 2 : 4;
+  // frames are read in place from the clip with 32-bit buffer offsets
+  if (int64_t(pw->g.B) * pw->g.Cin * int64_t(T) * S * esz >= (int64_t(1) << 31)) return CO_EINVAL;
   // the pool steps once per emitted depthwise frame
   const int64_t conv_out = conv_emissions(c->g, c->n, T);
   const int64_t n_emit = pool_emissions(p->g, p->n, conv_out);
   if (n_emit > z_cap_frames || (n_emit > 0 && !z)) return CO_EINVAL;
-  const int64_t S = pw->g.S();
-  const size_t esz = pw->g.dtype == CO_BF16 ? 2 : 4;
   hipStream_t s = as_stream(stream);
   const int64_t n0w = pw->n, n0c = c->n, n0p = p->n;
   Backup bk_ring, bk_fifo;

@@ -29,9 +29,10 @@ constexpr int kCpWaves = 1;
 
 struct CpTaps {  // the convolution step's active taps, compacted
   int32_t n;
-  int32_t tap[CO_MAX_TAPS];
-  int32_t act[CO_MAX_TAPS];
-  int32_t slot[CO_MAX_TAPS];
+  int32_t pk[CO_MAX_TAPS];  // tap | action << 8 | ring slot << 16
+  __host__ __device__ int tap(int a) const { return pk[a] & 0xff; }
+  __host__ __device__ int act(int a) const { return (pk[a] >> 8) & 0xff; }
+  __host__ __device__ int slot(int a) const { return pk[a] >> 16; }
 };
 
 struct CpPool {  // the pool step's plan
@@ -53,30 +54,70 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// The depthwise step of one lane (output pixel p of plane (stream, channel
-// c), flat plane index bc, ring index ridx) from its stencil values xv, then
-// the pool step on the completed frame (see the kernels below): shared by
-// the fused kernels so that they give the separate steps' bits.
+constexpr int kCpMaxTaps = 8;  // temporal taps of a fused depthwise convolution
+
+// What one lane of a fused step reads from the states, all of it known
+// before the step's arithmetic: the ring partial sums of the taps that
+// continue one (ACC, EMIT) and, when the pool emits, the pooled frame and
+// valid flag of window element `lane` from the FIFO.  Loading them at the
+// start of the kernel overlaps their round trips with the rest.
+struct CpPrefetch {
+  float prev[kCpMaxTaps];
+  float fev, fok;
+};
+
+__device__ __forceinline__ void dw_pool_prefetch(bool pl, int lane, int bc, int ridx,
+                                                 const float* __restrict__ ring,
+                                                 int64_t ring_slot, const CpTaps& at,
+                                                 const PoolGeom& pg,
+                                                 const float* __restrict__ fifo,
+                                                 int64_t fifo_slot,
+                                                 const float* __restrict__ valid,
+                                                 const CpPool& pp, CpPrefetch* f) {
+#pragma unroll
+  for (int a = 0; a < kCpMaxTaps; ++a) {
+    f->prev[a] = 0.f;
+    if (a < at.n) {
+      const int act = at.act(a);
+      if (pl && (act == CO_TAP_ACC || act == CO_TAP_EMIT))
+        f->prev[a] = ring[int64_t(at.slot(a)) * ring_slot + ridx];
+    }
+  }
+  f->fev = 0.f;
+  f->fok = 0.f;
+  // the FIFO slots read here are never the one this step writes (the
+  // window's other frames are older than the arriving one)
+  if (pp.step && pp.emit && lane < pg.kT) {
+    const int s = pp.src[lane];
+    if (s >= 0) {
+      f->fev = fifo[int64_t(s) * fifo_slot + bc];
+      f->fok = valid[s];
+    }
+  }
+}
+
+// The depthwise step of one lane (output pixel p of a plane with flat index
+// bc, ring index ridx, the channel's weights wc (kT x KH x KW) and bias bo)
+// from its stencil values xv and the prefetched state values, then the pool
+// step on the completed frame (see the kernels below): shared by the fused
+// kernels so that they give the separate steps' bits.
 template <typename T, int KH, int KW>
 __device__ __forceinline__ void dw_pool_tail(
-    const float (&xv)[KH * KW], bool pl, int lane, int c, int bc, int ridx, const ConvGeom& g,
-    const float* __restrict__ w, const float* __restrict__ bias, float* __restrict__ ring,
-    int64_t ring_slot, const CpTaps& at, int act2, const PoolGeom& pg, T* __restrict__ z,
-    int64_t z_bc, float* __restrict__ fifo, int64_t fifo_slot, float* __restrict__ valid,
-    const CpPool& pp) {
-  const float* wc = w + int64_t(c) * g.kT * (KH * KW);
-  const float bo = bias[c];
+    const float (&xv)[KH * KW], const CpPrefetch& f, bool pl, int lane, int bc, int ridx,
+    const float* wc, float bo, float* __restrict__ ring, int64_t ring_slot, const CpTaps& at,
+    int act2, const PoolGeom& pg, T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo,
+    int64_t fifo_slot, float* __restrict__ valid, const CpPool& pp) {
   T yv = from_f32<T>(0.f);
-  for (int a = 0; a < at.n; ++a) {
-    const int act = at.act[a];
-    float acc = 0.f;
-    if (pl && (act == CO_TAP_ACC || act == CO_TAP_EMIT))
-      acc = ring[int64_t(at.slot[a]) * ring_slot + ridx];
-    const float* wj = wc + at.tap[a] * (KH * KW);
+#pragma unroll
+  for (int a = 0; a < kCpMaxTaps; ++a) {
+    if (a >= at.n) break;
+    const int act = at.act(a);
+    float acc = f.prev[a];
+    const float* wj = wc + at.tap(a) * (KH * KW);
 #pragma unroll
     for (int e = 0; e < KH * KW; ++e) acc = fmaf(wj[e], xv[e], acc);
     if (act == CO_TAP_START || act == CO_TAP_ACC) {
-      if (pl) ring[int64_t(at.slot[a]) * ring_slot + ridx] = acc;
+      if (pl) ring[int64_t(at.slot(a)) * ring_slot + ridx] = acc;
     } else {
       yv = from_f32<T>(acc + bo);
     }
@@ -102,16 +143,9 @@ __device__ __forceinline__ void dw_pool_tail(
   if (lane < pg.kT) {
     const int s = pp.src[lane];
     if (s != -1) {
-      float ev, ok;
-      if (s == -2) {
-        ev = val;
-        ok = 1.f;
-      } else {
-        ev = fifo[int64_t(s) * fifo_slot + bc];
-        ok = valid[s];
-      }
+      const float ev = s == -2 ? val : f.fev;
       acc = is_max ? fmaxf(acc, ev) : acc + ev;
-      tcount += ok;
+      tcount += s == -2 ? 1.f : f.fok;
     }
   }
   if (is_max) {
@@ -153,6 +187,8 @@ __global__ __launch_bounds__(64 * kCpWaves) void convpool_step_kernel(
   // the depthwise step (see conv_step_dw_kernel)
   // frame planes are x_bc elements apart (S for a single frame, T * S when
   // the frame is read in place from a clip)
+  CpPrefetch pf;
+  dw_pool_prefetch(pl, lane, bc, ridx, ring, ring_slot, at, pg, fifo, fifo_slot, valid, pp, &pf);
   const int x_extent = int(((int64_t(g.B) * g.Cin - 1) * x_bc + g.H * g.W) * int64_t(sizeof(T)));
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, x_extent);
   const int plane = int(int64_t(bc) * x_bc);
@@ -167,78 +203,212 @@ __global__ __launch_bounds__(64 * kCpWaves) void convpool_step_kernel(
       xv[u * KW + v] = load_or_zero<T>(xr, plane + hi * g.W + wi, in);
     }
   }
-  dw_pool_tail<T, KH, KW>(xv, pl, lane, c, bc, ridx, g, w, bias, ring, ring_slot, at, CO_ACT_NONE,
-                          pg, z, z_bc, fifo, fifo_slot, valid, pp);
+  dw_pool_tail<T, KH, KW>(xv, pf, pl, lane, bc, ridx, w + int64_t(c) * g.kT * (KH * KW), bias[c],
+                          ring, ring_slot, at, CO_ACT_NONE, pg, z, z_bc, fifo, fifo_slot, valid,
+                          pp);
 }
 
 // Fused step of an X3D-style bottleneck (sections 3.2-3.3: a pointwise
 // convolution, batch normalisation and activation, a depthwise continual
 // convolution, batch normalisation and activation, and the pool over the
 // plane; the normalisations are folded into the convolutions' weights at
-// init).  A workgroup owns kBnWaves channel planes of one stream.  The
-// stream's input frame (C_in x H x W, at most 64 pixels per plane) is staged
-// into LDS once; each wave computes its channel's pointwise output at every
-// pixel (lane = pixel) exactly as the pointwise (1x1x1) direct step kernel
-// does -- products accumulated over the input channels in order with fmaf
-// from zero, the bias added, the result rounded to the io dtype and the
-// activation applied -- and writes it into its own zero-haloed plane in LDS.
-// The depthwise stencil then reads that plane instead of memory, and the
-// depthwise and pool steps follow as in convpool_step_kernel.  The
-// intermediate frames never leave the CU; the results equal the separate
-// steps bit for bit.
-constexpr int kBnWaves = 4;
+// init).  A workgroup owns one 16-channel fragment of the pointwise output
+// for one stream (at most 64 pixels per plane).  Wave w computes pixels
+// 16w..16w+15 of the fragment on the matrix cores exactly as the register
+// GEMM step kernel computes a pointwise layer: the same packed weights, the
+// same operand lanes (eight channels per lane and k-step for bf16, one for
+// fp32), the k-steps in the same order from zero, the same epilogue (the zero
+// partial sum and the bias added, rounded to the io dtype), then the
+// activation as the elementwise step applies it.  The results go into 16
+// zero-haloed planes in LDS; after one barrier each of the 8 waves runs the
+// depthwise and pool steps of two channels from there, as in
+// convpool_step_kernel, with every state read issued at the kernel's start.  The intermediate frames never leave the CU, and the
+// results equal the separate steps bit for bit.
+constexpr int kBnWaves = 4;  // pixel fragments of the plane (64 pixels)
+constexpr int kBnCh = 16;    // channels per workgroup: one 16-column fragment
+constexpr int kBnTail = 16;  // waves per workgroup; each steps kBnCh / kBnTail channels
+constexpr int kBnPer = kBnCh / kBnTail;
+// k-steps whose operand loads issue together (bf16: eight 2-byte loads per
+// lane and k-step; fp32: one)
+constexpr int kBnKB = 2;
+constexpr int kBnKF = 8;
+
+typedef float bn_v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 bn_v8bf __attribute__((ext_vector_type(8)));
 
 template <typename T, int KH, int KW>
-__global__ __launch_bounds__(64 * kBnWaves) void bneck_step_kernel(
-    int32_t Ci, const T* __restrict__ x, int64_t x_bc, const float* __restrict__ w1,
-    const float* __restrict__ b1, int32_t act1, ConvGeom g, const float* __restrict__ w,
-    const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot, CpTaps at,
-    int32_t act2, PoolGeom pg, T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo,
-    int64_t fifo_slot, float* __restrict__ valid, CpPool pp, int32_t cblocks, FastDiv fd_S,
-    FastDiv fd_W, FastDiv fd_Wo) {
+__global__ __launch_bounds__(64 * kBnTail, 8) void bneck_step_kernel(
+    int32_t Ci, int32_t CS, int32_t CSU, const T* __restrict__ x, int64_t x_bc, int32_t x_bytes,
+    const uint4* __restrict__ w1, int32_t w1_bytes, const float* __restrict__ b1, int32_t act1,
+    ConvGeom g, const float* __restrict__ w, const float* __restrict__ bias,
+    float* __restrict__ ring, int64_t ring_slot, CpTaps at, int32_t act2, PoolGeom pg,
+    T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo, int64_t fifo_slot,
+    float* __restrict__ valid, CpPool pp, int32_t cblocks, FastDiv fd_W, FastDiv fd_Wo) {
+  // LDS: the workgroup's depthwise weights (kBnCh x kT x KH x KW) and biases
+  // (kBnCh), then kBnCh zero-haloed planes of Hp x Wp
   extern __shared__ float lds[];
+  constexpr bool kBF = sizeof(T) == 2;
   const int tid = int(threadIdx.x);
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lrow = lane & 15, lgrp = lane >> 4;
   const int S = g.H * g.W;
-  const int Hp = g.H + 2 * g.pH, Wp = g.W + 2 * g.pW;
+  const int Hp = g.H + 2 * g.pH, Wp = g.W + 2 * g.pW, HWp = Hp * Wp;
   const int bq = int(blockIdx.x) / cblocks;
-  const int cb = int(blockIdx.x) - bq * cblocks;
-  float* xs = lds;                 // the stream's input frame, [C_in][S]
-  float* zs = lds + Ci * S;        // kBnWaves zero-haloed planes of Hp x Wp
-  float* zw = zs + wave * Hp * Wp;
-  for (int e = tid; e < kBnWaves * Hp * Wp; e += 64 * kBnWaves) zs[e] = 0.f;
-  for (int e = tid; e < Ci * S; e += 64 * kBnWaves) {
-    const int ci = fdiv(e, fd_S), q = e - ci * S;
-    xs[e] = to_f32<T>(x[(int64_t(bq) * Ci + ci) * x_bc + q]);
+  const int nf = int(blockIdx.x) - bq * cblocks;  // channel fragment
+  const int kTW = g.kT * KH * KW;
+  float* ws = lds;
+  float* zs = lds + kBnCh * (kTW + 1);
+  // the fragment's channels are consecutive, so their weights are one run
+  {
+    const int nch = min(kBnCh, g.Cout - nf * kBnCh);
+    for (int e = tid; e < nch * kTW; e += 64 * kBnTail) ws[e] = w[int64_t(nf) * kBnCh * kTW + e];
+    if (tid < nch) ws[kBnCh * kTW + tid] = bias[nf * kBnCh + tid];
   }
-  __syncthreads();
-  const int c = cb * kBnWaves + wave;
-  const bool cvalid = c < g.Cout;
-  if (cvalid && lane < S) {
-    const float* wr = w1 + int64_t(c) * Ci;
-    float acc = 0.f;
-    for (int ci = 0; ci < Ci; ++ci) acc = fmaf(wr[ci], xs[ci * S + lane], acc);
-    T z1 = from_f32<T>(acc + b1[c]);
-    if (act1 == CO_ACT_RELU) z1 = from_f32<T>(fmaxf(to_f32<T>(z1), 0.f));
-    const int qi = fdiv(lane, fd_W), qj = lane - qi * g.W;
-    zw[(qi + g.pH) * Wp + qj + g.pW] = to_f32<T>(z1);
-  }
-  __syncthreads();
-  if (!cvalid) return;  // after the last barrier
+  // this wave's depthwise channels (wave + kBnTail k of the fragment) and
+  // output pixel: their state reads first
   const int So = g.Ho * g.Wo;
   const bool pl = lane < So;
   const int p = pl ? lane : 0;
+  int cl[kBnPer], bc[kBnPer], ridx[kBnPer];
+  bool cv[kBnPer];
+#pragma unroll
+  for (int k = 0; k < kBnPer; ++k) {
+    cl[k] = wave + kBnTail * k;
+    const int c = nf * kBnCh + cl[k];
+    cv[k] = c < g.Cout;
+    bc[k] = bq * g.Cout + c;
+    ridx[k] = (c * g.B + bq) * So + p;
+  }
+  CpPrefetch pf[kBnPer];
+  const bool pw_wave = wave < kBnWaves;
+#pragma unroll
+  for (int k = 0; k < kBnPer; ++k)
+    dw_pool_prefetch(pl & cv[k], cv[k] ? lane : 64, bc[k], ridx[k], ring, ring_slot, at, pg, fifo,
+                     fifo_slot, valid, pp, &pf[k]);
+  // zero the planes' halo; the interior is written by the pointwise phase
+  // below (every pixel of every plane in use), so the two never touch the
+  // same element before the barrier
+  for (int e = tid; e < kBnCh * HWp; e += 64 * kBnTail) {
+    const int q = e % HWp;
+    const int r = q / Wp, col = q - r * Wp;
+    if (r < g.pH || r >= g.pH + g.H || col < g.pW || col >= g.pW + g.W) zs[e] = 0.f;
+  }
+
+  // ---- pointwise convolution on the matrix cores (waves 0-3) -------------
+  // lane (lrow, lgrp) supplies pixel P = 16 * wave + lrow; pixels past the
+  // plane and channels past C_in read an out-of-range offset (zero)
+  if (pw_wave) {
+    const int oc = nf * 16 + lrow;  // the output channel this lane holds
+    const bool ov = oc < g.Cin;
+    const float bo = ov ? b1[oc] : 0.f;
+    const int P = wave * 16 + lrow;
+    const bool pv = P < S;
+    constexpr uint32_t esz = sizeof(T);
+    const uint32_t plane_b = uint32_t(x_bc) * esz;
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, x_bytes);
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(w1, w1_bytes);
+    // k-steps in groups of kBnKB whose loads issue together; k-steps past the
+    // layer's read zeros (as the step kernel's k-steps past C_in do)
+    bn_v4f acc = bn_v4f{0.f, 0.f, 0.f, 0.f};
+    if constexpr (kBF) {
+      const int lane_c = lgrp * 8;
+      const uint32_t base = (uint32_t(bq) * uint32_t(Ci) + uint32_t(lane_c)) * plane_b +
+                            uint32_t(pv ? P : 0) * esz;
+      for (int c0 = 0; c0 < CS; c0 += kBnKB) {
+        uint4 a[kBnKB], b[kBnKB];
+#pragma unroll
+        for (int k = 0; k < kBnKB; ++k) {
+          const int cb = c0 + k;
+          const bool live = cb < CS;
+          uint32_t r[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bool ok = live & pv & (cb * 32 + lane_c + e < Ci);
+            r[e] = __builtin_amdgcn_raw_buffer_load_b16(
+                xr, ok ? int(base + uint32_t(cb * 32 + e) * plane_b) : kOutOfRange, 0, 0);
+          }
+          a[k] = make_uint4(r[0] | (r[1] << 16), r[2] | (r[3] << 16), r[4] | (r[5] << 16),
+                            r[6] | (r[7] << 16));
+          const auto b4 = __builtin_amdgcn_raw_buffer_load_b128(
+              wr, live ? ((nf * CSU + cb) << 10) + lane * 16 : kOutOfRange, 0, 0);
+          b[k] = make_uint4(b4[0], b4[1], b4[2], b4[3]);
+        }
+        // keep the group's loads one batch ahead of its matrix work
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < kBnKB; ++k)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bn_v8bf, a[k]),
+                                                        __builtin_bit_cast(bn_v8bf, b[k]), acc, 0,
+                                                        0, 0);
+      }
+    } else {
+      // one channel per lane and k-step; a weight unit holds four k-steps
+      const uint32_t base = (uint32_t(bq) * uint32_t(Ci) + uint32_t(lgrp)) * plane_b +
+                            uint32_t(pv ? P : 0) * esz;
+      for (int c0 = 0; c0 < CS; c0 += kBnKF) {
+        float a[kBnKF];
+        uint4 b[kBnKF / 4];
+#pragma unroll
+        for (int k = 0; k < kBnKF; ++k) {
+          const int cb = c0 + k;
+          const bool ok = (cb < CS) & pv & (cb * 4 + lgrp < Ci);
+          a[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+              xr, ok ? int(base + uint32_t(cb * 4) * plane_b) : kOutOfRange, 0, 0));
+        }
+#pragma unroll
+        for (int q = 0; q < kBnKF / 4; ++q) {
+          const int cq = c0 / 4 + q;
+          const auto b4 = __builtin_amdgcn_raw_buffer_load_b128(
+              wr, cq < CSU ? ((nf * CSU + cq) << 10) + lane * 16 : kOutOfRange, 0, 0);
+          b[q] = make_uint4(b4[0], b4[1], b4[2], b4[3]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < kBnKF; ++k) {
+          const uint4 u = b[k / 4];
+          const uint32_t bw = (k & 3) == 0 ? u.x : (k & 3) == 1 ? u.y : (k & 3) == 2 ? u.z : u.w;
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[k], __uint_as_float(bw), acc, 0, 0, 0);
+        }
+      }
+    }
+    // lane (lrow, lgrp) holds channel oc at pixels 16*wave + 4*lgrp + r
+    float* zc = zs + lrow * HWp;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int p = wave * 16 + 4 * lgrp + r;
+      const float v = acc[r] + 0.f;  // the step kernel adds its (zero) partial sum
+      const float val = v + bo;
+      T z1;
+      if constexpr (kBF)
+        z1 = __builtin_bit_cast(uint16_t, __bf16(val));
+      else
+        z1 = val;
+      if (act1 == CO_ACT_RELU) z1 = from_f32<T>(fmaxf(to_f32<T>(z1), 0.f));
+      if (ov & (p < S)) {
+        const int qi = fdiv(p, fd_W), qj = p - qi * g.W;
+        zc[(qi + g.pH) * Wp + qj + g.pW] = to_f32<T>(z1);
+      }
+    }
+  }  // pointwise waves
+  __syncthreads();
+
+  // ---- depthwise convolution and pool, kBnPer channels per wave -----------
   const int i = fdiv(p, fd_Wo), jo = p - i * g.Wo;
-  float xv[KH * KW];
 #pragma unroll
-  for (int u = 0; u < KH; ++u)
+  for (int k = 0; k < kBnPer; ++k) {
+    if (!cv[k]) return;  // wave-uniform, after the last barrier
+    const float* zw = zs + cl[k] * HWp;
+    float xv[KH * KW];
 #pragma unroll
-    for (int v = 0; v < KW; ++v)
-      xv[u * KW + v] = pl ? zw[(i * g.sH + u * g.dH) * Wp + jo * g.sW + v * g.dW] : 0.f;
-  const int bc = bq * g.Cout + c;
-  const int ridx = (c * g.B + bq) * So + p;
-  dw_pool_tail<T, KH, KW>(xv, pl, lane, c, bc, ridx, g, w, bias, ring, ring_slot, at, act2, pg,
-                          z, z_bc, fifo, fifo_slot, valid, pp);
+    for (int u = 0; u < KH; ++u)
+#pragma unroll
+      for (int v = 0; v < KW; ++v)
+        xv[u * KW + v] = pl ? zw[(i * g.sH + u * g.dH) * Wp + jo * g.sW + v * g.dW] : 0.f;
+    dw_pool_tail<T, KH, KW>(xv, pf[k], pl, lane, bc[k], ridx[k], ws + cl[k] * kTW,
+                            ws[kBnCh * kTW + cl[k]], ring, ring_slot, at, act2, pg, z, z_bc,
+                            fifo, fifo_slot, valid, pp);
+  }
 }
 
 template <typename T, int KH, int KW>
@@ -250,9 +420,8 @@ hipError_t cp_launch(const ConvGeom& g, const ConvLayout& L, char* cstate, const
   at.n = 0;
   for (int j = 0; j < g.kT; ++j) {
     if (cplan.action[j] == CO_TAP_NONE) continue;
-    at.tap[at.n] = j;
-    at.act[at.n] = cplan.action[j];
-    at.slot[at.n] = cplan.slot[j] < 0 ? 0 : cplan.slot[j];
+    at.pk[at.n] =
+        j | (int32_t(cplan.action[j]) << 8) | ((cplan.slot[j] < 0 ? 0 : cplan.slot[j]) << 16);
     ++at.n;
   }
   CpPool pp{};
@@ -620,9 +789,8 @@ void cp_plans(const ConvGeom& g, const co_step_plan& cplan, const co_pool_plan* 
   at->n = 0;
   for (int j = 0; j < g.kT; ++j) {
     if (cplan.action[j] == CO_TAP_NONE) continue;
-    at->tap[at->n] = j;
-    at->act[at->n] = cplan.action[j];
-    at->slot[at->n] = cplan.slot[j] < 0 ? 0 : cplan.slot[j];
+    at->pk[at->n] =
+        j | (int32_t(cplan.action[j]) << 8) | ((cplan.slot[j] < 0 ? 0 : cplan.slot[j]) << 16);
     ++at->n;
   }
   *pp = CpPool{};
@@ -645,20 +813,27 @@ hipError_t bn_launch(const ConvGeom& pw, const ConvLayout& PWL, char* pwstate, i
   CpPool pp;
   cp_plans(g, cplan, pplan, update, &at, &pp);
   if (at.n == 0 && !pp.step) return hipSuccess;
-  const int32_t cblocks = int32_t((g.Cout + kBnWaves - 1) / kBnWaves);
-  const int S = g.H * g.W;
-  const size_t lds = size_t(pw.Cin * S + kBnWaves * (g.H + 2 * g.pH) * (g.W + 2 * g.pW)) * 4;
+  RegConfig rc;
+  if (!reg_config(pw, pw.cfg, &rc)) return hipErrorInvalidValue;
+  const int32_t cblocks = int32_t((g.Cin + kBnCh - 1) / kBnCh);
+  const int64_t S = int64_t(g.H) * g.W;
+  const int64_t x_bytes = ((int64_t(pw.B) * pw.Cin - 1) * x_bc + S) * int64_t(sizeof(T));
+  const int64_t w_bytes = int64_t(rc.n_frags) * rc.U * 64 * 16;
+  if (x_bytes >= (int64_t(1) << 31) || w_bytes >= (int64_t(1) << 31))
+    return hipErrorInvalidValue;
+  const size_t lds =
+      size_t(kBnCh) * ((g.H + 2 * g.pH) * (g.W + 2 * g.pW) + g.kT * KH * KW + 1) * 4;
   hipLaunchKernelGGL((bneck_step_kernel<T, KH, KW>), dim3(unsigned(g.B * cblocks)),
-                     dim3(64 * kBnWaves), lds, s, pw.Cin, static_cast<const T*>(x), x_bc,
-                     reinterpret_cast<const float*>(pwstate + PWL.weight),
+                     dim3(64 * kBnTail), lds, s, pw.Cin, rc.CS, rc.CSU,
+                     static_cast<const T*>(x), x_bc, int32_t(x_bytes),
+                     reinterpret_cast<const uint4*>(pwstate + PWL.weight), int32_t(w_bytes),
                      reinterpret_cast<const float*>(pwstate + PWL.bias), act1, g,
                      reinterpret_cast<const float*>(cstate + L.weight),
                      reinterpret_cast<const float*>(cstate + L.bias),
                      reinterpret_cast<float*>(cstate + L.ring), L.ring_slot_elems, at, act2, pg,
                      static_cast<T*>(z), z_bc, reinterpret_cast<float*>(pstate + PL.fifo),
                      PL.fifo_slot_elems, reinterpret_cast<float*>(pstate + PL.valid), pp, cblocks,
-                     make_fastdiv(uint32_t(S)), make_fastdiv(uint32_t(g.W)),
-                     make_fastdiv(uint32_t(g.Wo)));
+                     make_fastdiv(uint32_t(g.W)), make_fastdiv(uint32_t(g.Wo)));
   return hipGetLastError();
 }
 
@@ -666,10 +841,13 @@ hipError_t bn_launch(const ConvGeom& pw, const ConvLayout& PWL, char* pwstate, i
 
 bool bneck_supported(const ConvGeom& pw, const ConvGeom& g, const PoolGeom& pg) {
   const int64_t S = int64_t(g.H) * g.W;
-  return convpool_supported(g, pg) && pw.algo == CO_ALGO_DIRECT && pw.G == 1 && pw.kT == 1 &&
-         pw.kH == 1 && pw.kW == 1 && pw.sT == 1 && pw.sH == 1 && pw.sW == 1 && pw.pT == 0 &&
-         pw.pH == 0 && pw.pW == 0 && pw.dtype == g.dtype && pw.B == g.B && pw.Cout == g.Cin &&
-         pw.H == g.H && pw.W == g.W && S <= 64 && int64_t(pw.Cin) * S <= kBnMaxStage &&
+  const int64_t Hp = g.H + 2 * g.pH, Wp = g.W + 2 * g.pW;
+  RegConfig rc;
+  return convpool_supported(g, pg) && pw.algo == CO_ALGO_GEMM_REG &&
+         reg_config(pw, pw.cfg, &rc) && pw.G == 1 && pw.kT == 1 && pw.kH == 1 && pw.kW == 1 &&
+         pw.sT == 1 && pw.sH == 1 && pw.sW == 1 && pw.pT == 0 && pw.pH == 0 && pw.pW == 0 &&
+         pw.dtype == g.dtype && pw.B == g.B && pw.Cout == g.Cin && pw.H == g.H && pw.W == g.W &&
+         S <= 16 * kBnWaves && Hp * Wp <= kCpsMaxPadded &&
          int64_t(pw.B) * pw.Cin * S * (pw.dtype == CO_BF16 ? 2 : 4) < (int64_t(1) << 31);
 }
 
@@ -699,7 +877,9 @@ hipError_t launch_bneck_step(const ConvGeom& pw, const ConvLayout& PWL, char* pw
 
 bool convpool_supported(const ConvGeom& g, const PoolGeom& pg) {
   const bool taps = (g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1);
-  return g.algo == CO_ALGO_DEPTHWISE && taps && g.dtype == pg.dtype && g.B == pg.B &&
+  return g.algo == CO_ALGO_DEPTHWISE && taps && g.kT <= kCpMaxTaps && g.R < 32768 &&
+         g.dtype == pg.dtype &&
+         g.B == pg.B &&
          g.Cout == pg.C && pg.H == g.Ho && pg.W == g.Wo && g.So() <= 64 && pg.kH == g.Ho &&
          pg.kW == g.Wo && pg.pH == 0 && pg.pW == 0 && pg.dH == 1 && pg.dW == 1 &&
          pg.Ho == 1 && pg.Wo == 1 && pg.kT <= 64 && g.S() > 0 &&

@@ -181,7 +181,6 @@ hipError_t launch_convpool_steps(const ConvGeom& g, const ConvLayout& L, char* c
 // convolution with activation act2 and the pool over its plane, in one
 // launch; the three handles' plans as for the separate steps (the pointwise
 // one always emits).  Input planes x_bc elements apart.
-constexpr int64_t kBnMaxStage = 12288;  // input channels x plane pixels staged in LDS
 bool bneck_supported(const ConvGeom& pw, const ConvGeom& g, const PoolGeom& pg);
 hipError_t launch_bneck_step(const ConvGeom& pw, const ConvLayout& PWL, char* pwstate,
                              int32_t act1, const ConvGeom& g, const ConvLayout& L, char* cstate,

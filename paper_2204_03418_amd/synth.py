@@ -172,3 +172,47 @@ def workload_inputs(name: str):
     """Inputs of a named workload (seeds 1000*index + {0, 1, 2})."""
     w = WORKLOADS[name]
     return conv_inputs(w.conv, w.frames, 1000 * w.index, w.weight_init)
+
+
+@dataclass(frozen=True)
+class BottleneckSpec:
+    """The front of an X3D bottleneck block: pointwise conv + BN + ReLU,
+    depthwise CoConv3d + BN + ReLU, continual average pool over the plane."""
+    name: str
+    batch: int
+    in_channels: int
+    channels: int
+    in_size: tuple
+    kernel: tuple        # depthwise kernel, time first
+    padding: tuple       # depthwise padding, time first
+    pool_kernel: tuple   # (kT, H, W) over the depthwise output plane
+    frames: int
+    seed: int
+    dtype: str = "bf16"
+
+
+# X3D-M's last stage at 7x7 (192 channels in, expanded to 432), the same
+# depthwise and pool shapes as the depthwise workload, 16 streams.
+BOTTLENECK = BottleneckSpec(name="bneck_b16_c192to432_k3_7x7_avgpool_bf16", batch=16,
+                            in_channels=192, channels=432, in_size=(7, 7), kernel=(3, 3, 3),
+                            padding=(0, 1, 1), pool_kernel=(4, 7, 7), frames=16, seed=6000)
+
+
+def bottleneck_inputs(spec: BottleneckSpec = BOTTLENECK):
+    """CPU tensors: x (B, C_in, T, H, W); pointwise weight (C, C_in, 1, 1, 1)
+    and bias; depthwise weight (C, 1, kT, kH, kW); two sets of evaluation
+    statistics (gamma, beta, mean, var) as float32.  Seeds spec.seed + i."""
+    s0, dt = spec.seed, spec.dtype
+    C = spec.channels
+    x = normal((spec.batch, spec.in_channels, spec.frames) + tuple(spec.in_size), s0, dtype=dt)
+    w1_shape = (C, spec.in_channels, 1, 1, 1)
+    w1 = normal(w1_shape, s0 + 1, std=kaiming_std(w1_shape), dtype=dt)
+    b1 = normal((C,), s0 + 2, std=0.1, dtype=dt)
+    w2_shape = (C, 1) + tuple(spec.kernel)
+    w2 = normal(w2_shape, s0 + 3, std=kaiming_std(w2_shape), dtype=dt)
+
+    def stats(k):
+        return (1.0 + 0.1 * normal((C,), k), 0.1 * normal((C,), k + 1),
+                0.1 * normal((C,), k + 2), 0.5 + normal((C,), k + 3).abs())
+
+    return x, w1, b1, w2, stats(s0 + 10), stats(s0 + 20)

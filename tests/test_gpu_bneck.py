@@ -158,9 +158,10 @@ BNECK_CASES = [
     # B, C_in, C (depthwise channels), in_size, dw kernel, dw padding, pool kind, pool kT,
     # relu1, relu2, dtype
     (4, 8, 16, (7, 7), (3, 3, 3), (1, 1, 1), "avg", 4, True, True, "bf16"),   # the X3D block
-    (3, 6, 10, (5, 6), (2, 3, 3), (0, 1, 1), "max", 3, True, False, "f32"),
-    (2, 5, 7, (4, 4), (3, 1, 1), (2, 0, 0), "avg", 2, False, True, "f32"),
-    (5, 12, 9, (8, 8), (3, 3, 3), (1, 1, 1), "avg", 3, True, True, "bf16"),  # 64-pixel planes
+    (3, 6, 20, (5, 6), (2, 3, 3), (0, 1, 1), "max", 3, True, False, "f32"),   # ragged fragment
+    (2, 5, 17, (4, 4), (3, 1, 1), (2, 0, 0), "avg", 2, False, True, "f32"),
+    (5, 40, 24, (8, 8), (3, 3, 3), (1, 1, 1), "avg", 3, True, True, "bf16"),  # 64-pixel planes
+    (3, 300, 32, (6, 6), (3, 3, 3), (0, 1, 1), "avg", 2, True, True, "bf16"),  # 10 k-steps
 ]
 
 
@@ -174,7 +175,7 @@ def _bneck_parts(case, seed):
     ho, wo = size[0] - k[1] + 1 + 2 * pad[1], size[1] - k[2] + 1 + 2 * pad[2]
 
     def modules():
-        pw = coinf.CoConv(w1.to(DEV), b1.to(DEV), batch=B, in_size=size, algo="direct",
+        pw = coinf.CoConv(w1.to(DEV), b1.to(DEV), batch=B, in_size=size, algo="gemm_reg",
                           bn=dev_bn(p1))
         dw = coinf.CoConv(w2.to(DEV), None, batch=B, in_size=size, padding=pad, groups=C,
                           bn=dev_bn(p2))
@@ -298,10 +299,10 @@ def test_fused_bottleneck(case):
 
 def test_bottleneck_refused_shapes():
     """co_bneck_bind refuses layers it cannot fuse (CO_ENOTSUP): a pointwise
-    layer not built on the direct kernel, a plane over 64 pixels, channels
-    that do not chain."""
+    layer not built on the register-GEMM kernel, a plane over 64 pixels,
+    channels that do not chain."""
     say("bneck refusals")
-    B, ci, C = 2, 4, 6
+    B, ci, C = 2, 4, 16
     w1 = synth.normal((C, ci, 1, 1, 1), 5500, dtype="f32").to(DEV)
     w2 = synth.normal((C, 1, 3, 3, 3), 5501, dtype="f32").to(DEV)
 
@@ -314,12 +315,14 @@ def test_bottleneck_refused_shapes():
 
     pw_gemm = coinf.CoConv(w1, None, batch=B, in_size=(5, 5), algo="gemm")
     assert not coinf.Bottleneck.fits(pw_gemm, dw((5, 5)), pool((5, 5)))
-    pw_big = coinf.CoConv(w1, None, batch=B, in_size=(9, 9), algo="direct")
+    pw_dir = coinf.CoConv(w1, None, batch=B, in_size=(5, 5), algo="direct")
+    assert not coinf.Bottleneck.fits(pw_dir, dw((5, 5)), pool((5, 5)))
+    pw_big = coinf.CoConv(w1, None, batch=B, in_size=(9, 9), algo="gemm_reg")
     assert not coinf.Bottleneck.fits(pw_big, dw((9, 9)), pool((9, 9)))
-    pw = coinf.CoConv(w1, None, batch=B, in_size=(5, 5), algo="direct")
+    pw = coinf.CoConv(w1, None, batch=B, in_size=(5, 5), algo="gemm_reg")
     assert coinf.Bottleneck.fits(pw, dw((5, 5)), pool((5, 5)))
     w3 = synth.normal((C + 1, ci, 1, 1, 1), 5502, dtype="f32").to(DEV)
-    pw3 = coinf.CoConv(w3, None, batch=B, in_size=(5, 5), algo="direct")
+    pw3 = coinf.CoConv(w3, None, batch=B, in_size=(5, 5), algo="gemm_reg")
     assert not coinf.Bottleneck.fits(pw3, dw((5, 5)), pool((5, 5)))
     h = coinf.ctypes.c_void_p()
     d5, p5 = dw((5, 5)), pool((5, 5))
