@@ -206,6 +206,7 @@ __global__ __launch_bounds__(kThreads) void conv_step_gemm_ws_kernel(
   // four pixels are one 16-byte unit of the plane).
   const __amdgpu_buffer_rsrc_t rr = make_rsrc(ring, wa.ring_bytes);
   int e_act[kWN], e_o[kWN], e_ring[kWN];
+  float e_bias[kWN];  // requested here, used only by the epilogue
 #pragma unroll
   for (int nf = 0; nf < kWN; ++nf) {
     const int ncol = n_tile * kNWG + nf * 16 + lrow;
@@ -215,6 +216,7 @@ __global__ __launch_bounds__(kThreads) void conv_step_gemm_ws_kernel(
     e_o[nf] = o;
     const int sl = tt.slot[t] < 0 ? 0 : tt.slot[t];
     e_ring[nf] = int((int64_t(sl) * ring_slot + int64_t(o) * wa.M) * 4);
+    e_bias[nf] = bias[o];
   }
 
   // Accumulators start from the partial sum the ring holds for the taps
@@ -306,9 +308,6 @@ __global__ __launch_bounds__(kThreads) void conv_step_gemm_ws_kernel(
   // and write y; every other store goes to the out-of-range offset, which
   // drops it.
   const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, wa.y_bytes);
-  float e_bias[kWN];
-#pragma unroll
-  for (int nf = 0; nf < kWN; ++nf) e_bias[nf] = bias[e_o[nf]];
 #pragma unroll
   for (int mf = 0; mf < kWM; ++mf) {
     const int P0 = m0 + (w * kWM + mf) * 16 + lgrp * 4;

@@ -590,30 +590,26 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   }
   // Raw loaded bits (eight bf16 channels or one fp32 per lane and k-step),
   // packed into operands only when the frame is multiplied: packing right
-  // after the loads would make the wave wait for them there.
+  // after the loads would make the wave wait for them there.  Frames past
+  // the clip (end padding, or past the call) issue the same loads at the
+  // out-of-range offset, which return zero: every frame issues the same
+  // memory operations, so the compiler's count of those in flight stays
+  // exact around the frame loop and no wait covers more than its own frame.
   auto load_frame = [&](int t, uint32_t (&a)[TH][CSMAX][CL]) {
-    if (t < rs.T) {  // uniform; end-padding frames are zero
-      const int fo = t * rs.fstride;
+    const bool real = t < rs.T;  // uniform
+    const int fo = real ? t * rs.fstride : 0;
 #pragma unroll
-      for (int i2 = 0; i2 < TH; ++i2)
+    for (int i2 = 0; i2 < TH; ++i2)
 #pragma unroll
-        for (int cb = 0; cb < CSMAX; ++cb) {
-          const bool lv = cb < rs.CS, last = cb == rs.CS - 1;  // uniform
-          const int sb = int(uint32_t(cb * CKS) * plane_b) + fo;
+      for (int cb = 0; cb < CSMAX; ++cb) {
+        const bool lv = real & (cb < rs.CS), last = cb == rs.CS - 1;  // uniform
+        const int sb = int(uint32_t(cb * CKS) * plane_b) + fo;
 #pragma unroll
-          for (int e = 0; e < CL; ++e) {
-            const int v = (lv & (!last | (e < nv_last))) ? vt[i2] : kOutOfRange;
-            a[i2][cb][e] = load_raw_at<T>(xr, v, sb + int(uint32_t(e) * plane_b));
-          }
+        for (int e = 0; e < CL; ++e) {
+          const int v = (lv & (!last | (e < nv_last))) ? vt[i2] : kOutOfRange;
+          a[i2][cb][e] = load_raw_at<T>(xr, v, sb + int(uint32_t(e) * plane_b));
         }
-    } else {
-#pragma unroll
-      for (int i2 = 0; i2 < TH; ++i2)
-#pragma unroll
-        for (int cb = 0; cb < CSMAX; ++cb)
-#pragma unroll
-          for (int e = 0; e < CL; ++e) a[i2][cb][e] = 0u;
-    }
+      }
   };
   auto operand = [&](const uint32_t (&r)[CL]) -> AReg {
     if constexpr (kBF)
@@ -626,14 +622,22 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   uint32_t araw[PF][TH][CSMAX][CL];
   // products handed from chain 1 to chain 0: [tile][frame parity][tap j][lane]
   __shared__ v4f red[KSPLIT == 2 ? TPW : 1][2][KSPLIT == 2 ? KTM : 1][64];
+  // in frame order (the loop below waits for frame u's loads with the later
+  // frames' still in flight)
 #pragma unroll
-  for (int u = 0; u < PF; ++u) load_frame(u, araw[u]);
+  for (int u = 0; u < PF; ++u) {
+    load_frame(u, araw[u]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 
+  // Whole groups of PF frames, with no exit inside a group: frames past the
+  // call (the last group's tail) run with their stores dropped and the
+  // partial sums left as they are.
   for (int t0 = 0; t0 < rs.count; t0 += PF) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
       const int t = t0 + u;
-      if (t >= rs.count) break;
+      const bool dead = t >= rs.count;  // uniform
       const int v = rs.v0 + t;
       // products of every temporal tap over this wave's chain of k-steps
       v4f c[KTM];
@@ -684,7 +688,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
         // output v - j exists once tau >= 0 (a uniform select, no branch:
         // the stores of a missing output carry the out-of-range offset)
         const int tau = v - j;
-        const bool exists = tau >= 0;
+        const bool exists = (tau >= 0) & !dead;
         const int first = tau >= g.pT ? 0 : g.pT - tau;
         v4f sum = c[j];
         if constexpr (KSPLIT == 2) sum = sum + c1[j];
@@ -707,7 +711,11 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       }
       // output v - j continues as v + 1 - (j + 1)
 #pragma unroll
-      for (int j = KTM - 1; j >= 1; --j) part[j] = nxt[j - 1];
+      for (int j = KTM - 1; j >= 1; --j) part[j] = dead ? part[j] : nxt[j - 1];
+      // keep the frames in order: hoisting the next frame's matrix work
+      // above this frame's loads would make it wait for operands requested
+      // only just before, instead of PF frames earlier
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 

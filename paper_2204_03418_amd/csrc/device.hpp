@@ -15,12 +15,10 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(uint32_t(b) << 16);
 }
 
-// float32 -> bfloat16, round to nearest even; NaN stays a quiet NaN.
+// float32 -> bfloat16, round to nearest even (the hardware conversion: one
+// instruction, no branch; NaN stays a quiet NaN).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t((u >> 16) | 0x0040u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return bf16_t(u >> 16);
+  return __builtin_bit_cast(bf16_t, __bf16(f));
 }
 
 template <typename T>
