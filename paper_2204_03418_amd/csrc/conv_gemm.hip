@@ -1103,31 +1103,35 @@ __global__ __launch_bounds__(kWregThreads) void conv_steps_gemm_wreg_kernel(
       const int nch = lastc ? 0 : ch + 1;
       const int ntf = lastc ? t + 1 : t;
       const int ks0 = ch * KHW;
-      Frag af[2][WM];
-      auto load_a = [&](int uv, int k) {
-        const int u = uv / KW, vv = uv % KW;
-#pragma unroll
-        for (int mf = 0; mf < WM; ++mf)
-          af[k][mf] = __builtin_bit_cast(Frag, As[(pixbase[mf][u] + vv) * kPixUnits + lgrp]);
+      // input fragments of the current tap, refilled one by one: each feeds
+      // its KTM matrix instructions, then takes the next tap's fragment,
+      // which has the rest of this tap's instructions to arrive (one set of
+      // registers instead of two)
+      Frag af[WM];
+      auto a_at = [&](int uv, int mf) {
+        return __builtin_bit_cast(
+            Frag, As[(pixbase[mf][uv / KW] + uv % KW) * kPixUnits + lgrp]);
       };
-      load_a(0, 0);
+#pragma unroll
+      for (int mf = 0; mf < WM; ++mf) af[mf] = a_at(0, mf);
 #pragma unroll
       for (int uv = 0; uv < KHW; ++uv) {
         // weights DB k-steps ahead (wrapping into the next frame's first
-        // chunk), the next chunk's input share, then the next tap's pixels
+        // chunk), then the next chunk's input share
         int ks = ks0 + uv + DB;
         if (ks >= steps_per_frame) ks -= steps_per_frame;
         load_b(ks, (uv + DB) % NB);
 #pragma unroll
         for (int e = uv * LPS; e < uv * LPS + LPS; ++e)
           if (e < AI * KL) prefetch_one(ntf, nch, e);
-        if (uv + 1 < KHW) load_a(uv + 1, (uv + 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < KTM; ++j)
+        for (int mf = 0; mf < WM; ++mf) {
 #pragma unroll
-          for (int mf = 0; mf < WM; ++mf) mma(c[mf][j], af[uv & 1][mf], bq[uv % NB][j]);
-        __builtin_amdgcn_sched_barrier(0);
+          for (int j = 0; j < KTM; ++j) mma(c[mf][j], af[mf], bq[uv % NB][j]);
+          if (uv + 1 < KHW) af[mf] = a_at(uv + 1, mf);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
       // unconditional, also after the call's last chunk (into a buffer no
       // one reads again): a store under a branch lets the compiler sink the
