@@ -465,14 +465,28 @@ struct RegSteps {
   int32_t v0;       // virtual time of the first frame, capped at 2^29
   int32_t slot_v0;  // v0 mod R (uncapped)
   int32_t count, T, k0, update;
-  FastDiv fd_So, fd_Wo, fd_ofr;
+  int32_t o_groups;  // STG: workgroups per pixel fragment, ceil(o_frags / kRegStgWaves)
+  FastDiv fd_So, fd_Wo, fd_ofr, fd_og;
 };
 
-template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL>
-__global__ __launch_bounds__(64 * KSPLIT * kRegTiles) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// STG (1x1 spatial taps, one chain per tile): the kRegStgWaves waves of a
+// workgroup share one 16-pixel fragment and take consecutive 16-channel
+// output fragments.  Each frame's input tile (16 pixels x every input
+// channel) is gathered once per workgroup -- four consecutive channels of one
+// pixel per thread -- and staged channels-last in LDS (double buffered, one
+// barrier per frame); each wave reads its operands from there with one
+// 16-byte (bf16) or 4-byte (fp32) read per k-step.  Without staging every
+// wave gathered the same tile in 2-byte pieces, and the vector L1 stalled on
+// the requests.  The operands, and so the results, are the same.
+constexpr int kRegStgWaves = 4;
+
+template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL, bool STG>
+__global__ __launch_bounds__(64 * (STG ? kRegStgWaves : KSPLIT * kRegTiles))
+__attribute__((amdgpu_waves_per_eu(1, 1)))
 void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
                            T* __restrict__ y, const uint4* __restrict__ wp,
                            const float* __restrict__ bias, float* __restrict__ ring) {
+  static_assert(!STG || (TAPS == 1 && KSPLIT == 1), "staging: 1x1 taps, one chain");
   constexpr bool kBF = sizeof(T) == 2;
   constexpr int CL = kBF ? 8 : 1;
   constexpr int CKS = 4 * CL;
@@ -492,16 +506,28 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   // wave adds its two chains.  Waves past the last tile keep to the per-frame
   // barrier: they redo tile 0 with every store masked.
   constexpr int TPW = kRegTiles;  // tiles per workgroup
-  const int h = wave % KSPLIT, wslot = wave / KSPLIT;
-  const int tile_raw = lb * TPW + wslot;
-  const bool live = tile_raw < rs.m_frags * rs.o_frags;
-  if constexpr (KSPLIT == 1) {
-    if (!live) return;  // whole waves; no barrier follows
+  const int h = STG ? 0 : wave % KSPLIT, wslot = STG ? 0 : wave / KSPLIT;
+  int mf, of;
+  bool owner;  // the wave that keeps the sums and stores
+  if constexpr (STG) {
+    // workgroup lb: pixel fragment mf, output fragments kRegStgWaves * group
+    // + wave; waves past the last fragment stage and meet the barriers with
+    // every store masked (their channels are past C_out)
+    if (lb >= rs.m_frags * rs.o_groups) return;  // whole workgroups
+    mf = fdiv(lb, rs.fd_og);
+    of = (lb - mf * rs.o_groups) * kRegStgWaves + wave;
+    owner = true;
+  } else {
+    const int tile_raw = lb * TPW + wslot;
+    const bool live = tile_raw < rs.m_frags * rs.o_frags;
+    if constexpr (KSPLIT == 1) {
+      if (!live) return;  // whole waves; no barrier follows
+    }
+    const int tile = live ? tile_raw : 0;
+    owner = live & (h == 0);
+    mf = fdiv(tile, rs.fd_ofr);
+    of = tile - mf * rs.o_frags;
   }
-  const int tile = live ? tile_raw : 0;
-  const bool owner = live & (h == 0);  // the wave that keeps the sums and stores
-  const int mf = fdiv(tile, rs.fd_ofr);
-  const int of = tile - mf * rs.o_frags;
   // FULL: the layer uses every temporal tap of the instantiation (kT == KTM),
   // so the per-tap tests below are compile-time and the frame loop is
   // straight-line matrix work with no branch between the instructions
@@ -619,104 +645,194 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       return __uint_as_float(r[0]);
   };
 
-  uint32_t araw[PF][TH][CSMAX][CL];
+  // ---- staging (STG): thread (px, quad) gathers channels 4 (quad + 16 k)
+  // .. + 3 of pixel mf * 16 + px; out-of-range reads (pixels past M,
+  // channels past C_in, frames past the clip) return zero
+  constexpr int SCH = CSMAX * CKS;            // staged channels (upper bound)
+  constexpr int SQ = (SCH / 4 + 15) / 16;     // channel quads per thread
+  constexpr int PU = SCH * int(esz) / 16 + 1;  // LDS row pitch, 16-byte units
+  constexpr int SPF = STG ? (SQ <= 2 ? 4 : 2) : 1;  // frames in flight
+  __shared__ uint4 stg[STG ? 2 : 1][STG ? 16 * PU : 1];
+  uint32_t sraw[SPF][STG ? SQ : 1][4];
+  const int tid = int(threadIdx.x);
+  const int spx = tid & 15, sq0 = tid >> 4;
+  const int Ps = mf * 16 + spx;
+  const bool ps_ok = Ps < rs.M;
+  const int sb = fdiv(ps_ok ? Ps : 0, rs.fd_So), sp = (ps_ok ? Ps : 0) - sb * rs.So;
+  const uint32_t s_base = uint32_t(sb) * uint32_t(g.Cin) * plane_b + uint32_t(sp) * esz;
+  auto load_stage = [&](int t, uint32_t (&a)[STG ? SQ : 1][4]) {
+    const bool real = t < rs.T;  // uniform
+    const int fo = real ? t * rs.fstride : 0;
+#pragma unroll
+    for (int k = 0; k < SQ; ++k) {
+      const int qd = sq0 + 16 * k;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * qd + e;
+        const bool ok = real & ps_ok & (c < g.Cin);
+        a[k][e] = load_raw_at<T>(xr, ok ? int(s_base + uint32_t(c) * plane_b) : kOutOfRange, fo);
+      }
+    }
+  };
+  auto write_stage = [&](int buf, const uint32_t (&a)[STG ? SQ : 1][4]) {
+    // every quad of the row, also those past C_in (the k-steps past the
+    // layer's multiply them, as zeros, by zero weights)
+    uint4* row = &stg[buf][spx * PU];
+#pragma unroll
+    for (int k = 0; k < SQ; ++k) {
+      const int qd = sq0 + 16 * k;
+      if (qd < SCH / 4) {
+        if constexpr (kBF)
+          reinterpret_cast<uint2*>(row)[qd] =
+              make_uint2(a[k][0] | (a[k][1] << 16), a[k][2] | (a[k][3] << 16));
+        else
+          row[qd] = make_uint4(a[k][0], a[k][1], a[k][2], a[k][3]);
+      }
+    }
+  };
+  auto staged_operand = [&](int buf, int cb) -> AReg {
+    const uint4* row = &stg[buf][lrow * PU];
+    if constexpr (kBF)
+      return row[cb * 4 + lgrp];
+    else
+      return reinterpret_cast<const float*>(row)[cb * 4 + lgrp];
+  };
+
+  uint32_t araw[STG ? 1 : PF][TH][CSMAX][CL];
   // products handed from chain 1 to chain 0: [tile][frame parity][tap j][lane]
   __shared__ v4f red[KSPLIT == 2 ? TPW : 1][2][KSPLIT == 2 ? KTM : 1][64];
   // in frame order (the loop below waits for frame u's loads with the later
   // frames' still in flight)
+  if constexpr (STG) {
 #pragma unroll
-  for (int u = 0; u < PF; ++u) {
-    load_frame(u, araw[u]);
-    __builtin_amdgcn_sched_barrier(0);
+    for (int u = 0; u < SPF; ++u) {
+      load_stage(u, sraw[u]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      load_frame(u, araw[u]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
+  constexpr int FPG = STG ? SPF : PF;  // frames per group
 
   // Whole groups of PF frames, with no exit inside a group: frames past the
   // call (the last group's tail) run with their stores dropped and the
   // partial sums left as they are.
-  for (int t0 = 0; t0 < rs.count; t0 += PF) {
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int t = t0 + u;
-      const bool dead = t >= rs.count;  // uniform
-      const int v = rs.v0 + t;
-      // products of every temporal tap over this wave's chain of k-steps
-      v4f c[KTM];
-#pragma unroll
-      for (int j = 0; j < KTM; ++j) c[j] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i2 = 0; i2 < TH; ++i2)
-#pragma unroll
-        for (int cb = 0; cb < CSMAX; ++cb)
-#pragma unroll
-          for (int j = 0; j < KTM; ++j) {
-            if (!FULL && j >= kT) continue;  // uniform
-            const AReg av = operand(araw[u][i2][cb]);
-            if constexpr (kBF) {
-              c[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  __builtin_bit_cast(v8bf, av), __builtin_bit_cast(v8bf, wreg[j][i2][cb]), c[j],
-                  0, 0, 0);
-            } else {
-              const uint4 u4 = wreg[j][i2][cb / 4];
-              const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
-              c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, __uint_as_float(bw), c[j], 0, 0, 0);
-            }
-          }
-      // the next frames' operands are requested before this frame's epilogue
-      load_frame(t + PF, araw[u]);
-      v4f c1[KTM];  // chain 1's products (KSPLIT = 2), as chain 0 adds them
-      if constexpr (KSPLIT == 2) {
-        if (h == 1) {
-#pragma unroll
-          for (int j = 0; j < KTM; ++j) red[wslot][t & 1][j][lane] = c[j];
-        }
-        __syncthreads();  // (a slot is rewritten two frames later, after another barrier)
-        // Both waves run the fold below: the helper's stores carry the
-        // out-of-range offset and are dropped.  A branch around it would
-        // give the two paths different counts of outstanding memory
-        // operations, and the compiler would then wait for all of them
-        // (the frames in flight included) before each frame's products.
-#pragma unroll
-        for (int j = 0; j < KTM; ++j) c1[j] = red[wslot][t & 1][j][lane];
-      }
-      // fold each product into its output: tap j completes v - (kT - 1),
-      // starts at the first tap on a real frame, continues otherwise
-      v4f nxt[KTM];
-#pragma unroll
-      for (int j = 0; j < KTM; ++j) {
-        nxt[j] = v4f{0.f, 0.f, 0.f, 0.f};
-        if (!FULL && j >= kT) continue;
-        // output v - j exists once tau >= 0 (a uniform select, no branch:
-        // the stores of a missing output carry the out-of-range offset)
-        const int tau = v - j;
-        const bool exists = (tau >= 0) & !dead;
-        const int first = tau >= g.pT ? 0 : g.pT - tau;
-        v4f sum = c[j];
-        if constexpr (KSPLIT == 2) sum = sum + c1[j];
-        const v4f a = (j == first) ? sum : sum + part[j];
-        if (j == kT - 1) {
-          const int fo = exists ? (rs.k0 + t) * rs.So * int(esz) : 0;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float val = a[r] + bo;
-            const int yo = exists ? yoff[r] : kOutOfRange;
-            if constexpr (kBF)
-              __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)),
-                                                    yr, yo, fo, 0);
-            else
-              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, yo, fo, 0);
-          }
-        } else {
-          nxt[j] = exists ? a : v4f{0.f, 0.f, 0.f, 0.f};
-        }
-      }
-      // output v - j continues as v + 1 - (j + 1)
-#pragma unroll
-      for (int j = KTM - 1; j >= 1; --j) part[j] = dead ? part[j] : nxt[j - 1];
-      // keep the frames in order: hoisting the next frame's matrix work
-      // above this frame's loads would make it wait for operands requested
-      // only just before, instead of PF frames earlier
-      __builtin_amdgcn_sched_barrier(0);
+  // One frame.  In a steady group (STG only: every frame inside the call,
+  // every temporal tap continuing an output that started on a real frame)
+  // the fold needs no selects; the general form handles the stream's first
+  // frames, end padding and the call's last group.  Both issue the same
+  // memory operations in the same order.
+  auto frame = [&](int t0, int u, auto steady_tag) {
+    constexpr bool STEADY = decltype(steady_tag)::value;
+    const int t = t0 + u;
+    const bool dead = STEADY ? false : t >= rs.count;  // uniform
+    const int v = rs.v0 + t;
+    if constexpr (STG) {
+      // frame t into LDS buffer t & 1 (every wave left it at the previous
+      // frame's barrier), then frame t + SPF's gathers
+      write_stage(t & 1, sraw[u]);
+      load_stage(t + SPF, sraw[u]);
+      __syncthreads();
     }
+    // products of every temporal tap over this wave's chain of k-steps
+    v4f c[KTM];
+#pragma unroll
+    for (int j = 0; j < KTM; ++j) c[j] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i2 = 0; i2 < TH; ++i2)
+#pragma unroll
+      for (int cb = 0; cb < CSMAX; ++cb)
+#pragma unroll
+        for (int j = 0; j < KTM; ++j) {
+          if (!FULL && j >= kT) continue;  // uniform
+          AReg av;
+          if constexpr (STG)
+            av = staged_operand(t & 1, cb);
+          else
+            av = operand(araw[u][i2][cb]);
+          if constexpr (kBF) {
+            c[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(v8bf, av), __builtin_bit_cast(v8bf, wreg[j][i2][cb]), c[j],
+                0, 0, 0);
+          } else {
+            const uint4 u4 = wreg[j][i2][cb / 4];
+            const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
+            c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, __uint_as_float(bw), c[j], 0, 0, 0);
+          }
+        }
+    // the next frames' operands are requested before this frame's epilogue
+    if constexpr (!STG) load_frame(t + PF, araw[u]);
+    v4f c1[KTM];  // chain 1's products (KSPLIT = 2), as chain 0 adds them
+    if constexpr (KSPLIT == 2) {
+      if (h == 1) {
+#pragma unroll
+        for (int j = 0; j < KTM; ++j) red[wslot][t & 1][j][lane] = c[j];
+      }
+      __syncthreads();  // (a slot is rewritten two frames later, after another barrier)
+      // Both waves run the fold below: the helper's stores carry the
+      // out-of-range offset and are dropped.  A branch around it would
+      // give the two paths different counts of outstanding memory
+      // operations, and the compiler would then wait for all of them
+      // (the frames in flight included) before each frame's products.
+#pragma unroll
+      for (int j = 0; j < KTM; ++j) c1[j] = red[wslot][t & 1][j][lane];
+    }
+    // fold each product into its output: tap j completes v - (kT - 1),
+    // starts at the first tap on a real frame, continues otherwise
+    v4f nxt[KTM];
+#pragma unroll
+    for (int j = 0; j < KTM; ++j) {
+      nxt[j] = v4f{0.f, 0.f, 0.f, 0.f};
+      if (!FULL && j >= kT) continue;
+      // output v - j exists once tau >= 0 (a uniform select, no branch:
+      // the stores of a missing output carry the out-of-range offset)
+      const int tau = v - j;
+      const bool exists = STEADY ? true : (tau >= 0) & !dead;
+      const int first = STEADY ? 0 : tau >= g.pT ? 0 : g.pT - tau;
+      v4f sum = c[j];
+      if constexpr (KSPLIT == 2) sum = sum + c1[j];
+      const v4f a = (j == first) ? sum : sum + part[j];
+      if (j == kT - 1) {
+        const int fo = exists ? (rs.k0 + t) * rs.So * int(esz) : 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float val = a[r] + bo;
+          const int yo = exists ? yoff[r] : kOutOfRange;
+          if constexpr (kBF)
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)),
+                                                  yr, yo, fo, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, yo, fo, 0);
+        }
+      } else {
+        nxt[j] = exists ? a : v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    // output v - j continues as v + 1 - (j + 1)
+#pragma unroll
+    for (int j = KTM - 1; j >= 1; --j) part[j] = dead ? part[j] : nxt[j - 1];
+    // keep the frames in order: hoisting the next frame's matrix work
+    // above this frame's loads would make it wait for operands requested
+    // only just before, instead of PF frames earlier
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int t0 = 0; t0 < rs.count; t0 += FPG) {
+    // uniform: the outputs v - j of every frame of the group started at or
+    // after the first real frame
+    const bool steady = (rs.v0 + t0 >= g.pT + kT - 1) & (t0 + FPG <= rs.count);
+    if constexpr (STG) {
+      if (steady) {
+#pragma unroll
+        for (int u = 0; u < FPG; ++u) frame(t0, u, std::true_type{});
+        continue;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < FPG; ++u) frame(t0, u, std::false_type{});
   }
 
   if (rs.update && h == 0) {
@@ -795,9 +911,17 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.fd_So = make_fastdiv(uint32_t(rs.So));
   rs.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   rs.fd_ofr = make_fastdiv(uint32_t(rs.o_frags));
-  auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true>
-                          : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false>;
-  hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * KSPLIT * kRegTiles),
+  constexpr bool STG = TAPS == 1 && KSPLIT == 1;
+  rs.o_groups = int32_t(ceil_div(rs.o_frags, kRegStgWaves));
+  rs.fd_og = make_fastdiv(uint32_t(rs.o_groups));
+  if (STG) {
+    const int64_t wgs = int64_t(rs.m_frags) * rs.o_groups;
+    rs.blocks_per_xcd = int32_t(ceil_div(wgs, 8));
+  }
+  auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true, STG>
+                          : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false, STG>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)),
+                     dim3(64 * (STG ? kRegStgWaves : KSPLIT * kRegTiles)),
                      0, s, g, rs, static_cast<const T*>(x), x_bc, static_cast<T*>(y),
                      reinterpret_cast<const uint4*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
