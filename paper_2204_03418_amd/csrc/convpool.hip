@@ -496,7 +496,7 @@ struct CpSteps {
   FastDiv fd_Cout, fd_Wo, fd_W;
 };
 
-template <typename T, int KH, int KW, int KT, int PKT>
+template <typename T, int KH, int KW, int KT, int PKT, bool IS_MAX>
 __global__ __launch_bounds__(64 * kCpsWaves) void convpool_steps_kernel(
     ConvGeom g, CpSteps cs, const T* __restrict__ x, int64_t x_bc, const float* __restrict__ w,
     const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot, PoolGeom pg,
@@ -545,7 +545,7 @@ __global__ __launch_bounds__(64 * kCpsWaves) void convpool_steps_kernel(
 
   // pool: reduced value and validity of pool frame m - (PKT - 1) + q before
   // the pool's step m; frames before the stream began are start padding
-  const bool is_max = pg.kind == CO_POOL_MAX;
+  constexpr bool is_max = IS_MAX;  // (compile-time: no select per operation)
   const float neutral = is_max ? -INFINITY : 0.f;
   const int kHW = pg.kH * pg.kW;
   float fv[PKT], fok[PKT];
@@ -629,32 +629,45 @@ __global__ __launch_bounds__(64 * kCpsWaves) void convpool_steps_kernel(
           fok[PKT - 1] = 1.f;
           const int64_t m = cs.n0p + (t - cs.tfirst);
           if (m >= pg.d) {
-            float tv[8], tc[8];
+            float tv[8];
 #pragma unroll
             for (int l = 0; l < 8; ++l) {
               const bool in = l < PKT && m - (PKT - 1) + l >= 0;
               tv[l] = in ? fv[l < PKT ? l : 0] : neutral;
-              tc[l] = in ? fok[l < PKT ? l : 0] : 0.f;
             }
 #pragma unroll
             for (int mm = 4; mm > 0; mm >>= 1) {
-              float nv[8], nc[8];
+              float nv[8];
 #pragma unroll
-              for (int l = 0; l < 8; ++l) {
+              for (int l = 0; l < 8; ++l)
                 nv[l] = is_max ? fmaxf(tv[l], tv[l ^ mm]) : tv[l] + tv[l ^ mm];
-                nc[l] = tc[l] + tc[l ^ mm];
-              }
 #pragma unroll
-              for (int l = 0; l < 8; ++l) {
-                tv[l] = nv[l];
-                tc[l] = nc[l];
-              }
+              for (int l = 0; l < 8; ++l) tv[l] = nv[l];
             }
             float out;
             if (is_max) {
               out = tv[0];
             } else {
-              const float div = pg.count_include_pad ? float(PKT * kHW) : tc[0] * float(kHW);
+              // the count of real frames only for an average without the pads
+              float tcount = 0.f;
+              if (!pg.count_include_pad) {
+                float tc[8];
+#pragma unroll
+                for (int l = 0; l < 8; ++l) {
+                  const bool in = l < PKT && m - (PKT - 1) + l >= 0;
+                  tc[l] = in ? fok[l < PKT ? l : 0] : 0.f;
+                }
+#pragma unroll
+                for (int mm = 4; mm > 0; mm >>= 1) {
+                  float nc[8];
+#pragma unroll
+                  for (int l = 0; l < 8; ++l) nc[l] = tc[l] + tc[l ^ mm];
+#pragma unroll
+                  for (int l = 0; l < 8; ++l) tc[l] = nc[l];
+                }
+                tcount = tc[0];
+              }
+              const float div = pg.count_include_pad ? float(PKT * kHW) : tcount * float(kHW);
               out = div > 0.f ? tv[0] / div : 0.f;
             }
             if (wlive && lane == 0) z[int64_t(bc) * z_bc + (m - cs.emit0p)] = from_f32<T>(out);
@@ -724,9 +737,10 @@ hipError_t cps_launch(const ConvGeom& g, const ConvLayout& L, char* cstate, cons
   const int64_t planes = int64_t(g.B) * g.Cout;
   const size_t lds = size_t(kCpsWaves) * 2 * cs.Hp * cs.Wp * kCpsF * sizeof(float);
   float* valid = reinterpret_cast<float*>(pstate + PL.valid);
-  hipLaunchKernelGGL((convpool_steps_kernel<T, KH, KW, KT, PKT>),
-                     dim3(unsigned((planes + kCpsWaves - 1) / kCpsWaves)), dim3(64 * kCpsWaves),
-                     lds, s, g, cs, static_cast<const T*>(x), x_bc,
+  auto kern = pg.kind == CO_POOL_MAX ? convpool_steps_kernel<T, KH, KW, KT, PKT, true>
+                                      : convpool_steps_kernel<T, KH, KW, KT, PKT, false>;
+  hipLaunchKernelGGL(kern, dim3(unsigned((planes + kCpsWaves - 1) / kCpsWaves)),
+                     dim3(64 * kCpsWaves), lds, s, g, cs, static_cast<const T*>(x), x_bc,
                      reinterpret_cast<const float*>(cstate + L.weight),
                      reinterpret_cast<const float*>(cstate + L.bias),
                      reinterpret_cast<float*>(cstate + L.ring), L.ring_slot_elems, pg,

@@ -193,7 +193,7 @@ struct PoolSteps {
   FastDiv fd_So, fd_Wo, fd_kW;
 };
 
-template <typename T, int G, int KT>
+template <typename T, int G, int KT, bool IS_MAX>
 __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
     PoolGeom g, PoolSteps ps, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
     int64_t y_bc, float* __restrict__ fifo, int64_t fifo_slot, const float* __restrict__ valid) {
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
   const int32_t bc = fdiv(idx, ps.fd_So);
   const int32_t p = idx - bc * So;
   const int32_t i = fdiv(p, ps.fd_Wo), jo = p - i * g.Wo;
-  const bool is_max = g.kind == CO_POOL_MAX;
+  constexpr bool is_max = IS_MAX;  // (compile-time: no select per operation)
   const float neutral = is_max ? -INFINITY : 0.f;
   const int32_t kHW = g.kH * g.kW;
 
@@ -252,8 +252,12 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ps.x_bytes);
   const int loff = soff >= 0 ? int((uint32_t(bc) * uint32_t(x_bc) + uint32_t(soff)) * sizeof(T))
                              : kOutOfRange;
+  // every frame issues its load (frames past the clip at the out-of-range
+  // offset), so the compiler's count of loads in flight stays exact around
+  // the frame loop
   auto load = [&](int t) -> uint32_t {
-    return t < ps.T ? load_raw_at<T>(xr, loff, t * ps.fstride) : 0u;
+    const bool real = t < ps.T;  // uniform
+    return load_raw_at<T>(xr, real ? loff : kOutOfRange, real ? t * ps.fstride : 0);
   };
   auto value = [&](int t, uint32_t raw) {
     return (t < ps.T && soff >= 0) ? raw_to_f32<T>(raw) : neutral;
@@ -264,12 +268,17 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
   constexpr int PF = 16;
   uint32_t xq[PF];
 #pragma unroll
-  for (int u = 0; u < PF; ++u) xq[u] = load(u);
+  for (int u = 0; u < PF; ++u) {
+    xq[u] = load(u);
+    __builtin_amdgcn_sched_barrier(0);  // in frame order
+  }
+  // whole groups of PF frames with no exit inside: frames past the call
+  // (the last group's tail) store nothing and leave the window as it is
   for (int t0 = 0; t0 < ps.count; t0 += PF) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
       const int t = t0 + u;
-      if (t >= ps.count) break;
+      const bool dead = t >= ps.count;  // uniform
       const float xv = value(t, xq[u]);
       const float val = is_max ? group_max<G>(xv) : group_sum<G>(xv);
       xq[u] = load(t + PF);
@@ -280,28 +289,41 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
         // the window's frames as the per-step kernel combines them (tap q in
         // lane q of a lane group, then an xor-shuffle tree), so both paths
         // give the same bits; start padding contributes nothing
-        float tv[8], tc[8];
+        float tv[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           const bool in = q < KT && n - (KT - 1) + q >= 0;
           tv[q] = in ? fv[q < KT ? q : 0] : neutral;
-          tc[q] = in ? fok[q < KT ? q : 0] : 0.f;
         }
 #pragma unroll
         for (int m = 4; m > 0; m >>= 1) {
-          float nv[8], nc[8];
+          float nv[8];
 #pragma unroll
-          for (int l = 0; l < 8; ++l) {
-            nv[l] = is_max ? fmaxf(tv[l], tv[l ^ m]) : tv[l] + tv[l ^ m];
-            nc[l] = tc[l] + tc[l ^ m];
-          }
+          for (int l = 0; l < 8; ++l) nv[l] = is_max ? fmaxf(tv[l], tv[l ^ m]) : tv[l] + tv[l ^ m];
 #pragma unroll
-          for (int l = 0; l < 8; ++l) {
-            tv[l] = nv[l];
-            tc[l] = nc[l];
-          }
+          for (int l = 0; l < 8; ++l) tv[l] = nv[l];
         }
-        const float acc = tv[0], tcount = tc[0];
+        const float acc = tv[0];
+        // the count of real frames, only for an average without the pads
+        // (uniform branch, no memory operation inside)
+        float tcount = 0.f;
+        if (!is_max && !g.count_include_pad) {
+          float tc[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const bool in = q < KT && n - (KT - 1) + q >= 0;
+            tc[q] = in ? fok[q < KT ? q : 0] : 0.f;
+          }
+#pragma unroll
+          for (int m = 4; m > 0; m >>= 1) {
+            float nc[8];
+#pragma unroll
+            for (int l = 0; l < 8; ++l) nc[l] = tc[l] + tc[l ^ m];
+#pragma unroll
+            for (int l = 0; l < 8; ++l) tc[l] = nc[l];
+          }
+          tcount = tc[0];
+        }
         float out;
         if (is_max) {
           out = acc;
@@ -309,15 +331,18 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
           const float div = g.count_include_pad ? float(KT * kHW) : tcount * float(vh * vw);
           out = div > 0.f ? acc / div : 0.f;
         }
-        const bool emits = n >= g.d;  // uniform
+        const bool emits = (n >= g.d) & !dead;  // uniform
         store_at(yr, (emits && r == 0) ? yoff : kOutOfRange,
                  emits ? int((n - ps.emit0) * So * int64_t(sizeof(T))) : 0, from_f32<T>(out));
       }
+      // (a dead frame's value went into the last place only, which the next
+      // frame overwrites; the call ends after the group anyway)
 #pragma unroll
       for (int q = 0; q + 1 < KT; ++q) {
-        fv[q] = fv[q + 1];
-        fok[q] = fok[q + 1];
+        fv[q] = dead ? fv[q] : fv[q + 1];
+        fok[q] = dead ? fok[q] : fok[q + 1];
       }
+      __builtin_amdgcn_sched_barrier(0);  // frames in order
     }
   }
   if (ps.update && r == 0) {
@@ -418,9 +443,11 @@ hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state
   ps.fd_kW = make_fastdiv(uint32_t(g.kW));
   float* fifo = reinterpret_cast<float*>(state + L.fifo);
   float* valid = reinterpret_cast<float*>(state + L.valid);
-  hipLaunchKernelGGL((pool_steps_kernel<T, G, KT>), dim3(grid_for(g.out_frame_elems() * G)),
-                     dim3(kBlock), 0, s, g, ps, static_cast<const T*>(x), x_bc,
-                     static_cast<T*>(y), y_bc, fifo, L.fifo_slot_elems, valid);
+  auto kern = g.kind == CO_POOL_MAX ? pool_steps_kernel<T, G, KT, true>
+                                     : pool_steps_kernel<T, G, KT, false>;
+  hipLaunchKernelGGL(kern, dim3(grid_for(g.out_frame_elems() * G)), dim3(kBlock), 0, s, g, ps,
+                     static_cast<const T*>(x), x_bc, static_cast<T*>(y), y_bc, fifo,
+                     L.fifo_slot_elems, valid);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !update) return e;
   hipLaunchKernelGGL(pool_valid_kernel, dim3(1), dim3(64), 0, s, valid, g.R, n0, count, nreal);
