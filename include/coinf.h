@@ -298,6 +298,36 @@ co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_
 co_status co_conv_forward(const co_conv_desc* desc, const void* weight, const void* bias,
                           const void* x, int32_t T, void* y, void* stream);
 
+/* Evaluation-mode batch normalisation of a convolution's output, as
+ * co_conv_init_state_bn takes it: float32 device arrays of C_out. */
+typedef struct {
+  const float* gamma;
+  const float* beta;
+  const float* mean;
+  const float* var;
+  float eps;
+} co_bn_params;
+
+/*
+ * forward (clip mode) on the step kernels: the same result as
+ * co_conv_forward (Principle 2: a clip processed by the continual layer from
+ * a clean state, with padding[0] end-padding frames, emits exactly the
+ * regular convolution's T_out frames; Example 1, Principle 4) up to
+ * summation order, computed by building a clean state in the caller's
+ * workspace (workspace_bytes >= state_bytes of co_conv_query; CO_ESTATE
+ * otherwise) and running co_conv_forward_steps with end padding over x read
+ * in place -- on the matrix-core kernels AUTO (or desc->algo) picks, one
+ * persistent launch where co_conv_steps_fused says so.  bn, when not NULL,
+ * folds a batch normalisation in as co_conv_init_state_bn does, so a folded
+ * layer's clip equals its steps bit for bit.  The workspace is scratch: its
+ * contents are undefined afterwards.  Nothing is allocated, except the
+ * stream-ordered staging copy co_conv_forward_steps makes for a clip whose
+ * reach passes 2^31 bytes on a kernel that loops over steps.
+ */
+co_status co_conv_forward_ws(const co_conv_desc* desc, const void* weight, const void* bias,
+                             const co_bn_params* bn, const void* x, int32_t T, void* y,
+                             void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Number of T_out frames co_conv_forward produces for a clip of T frames. */
 co_status co_conv_clip_frames(const co_conv_desc* desc, int32_t T, int32_t* t_out);
 

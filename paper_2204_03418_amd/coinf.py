@@ -147,6 +147,14 @@ co_conv_init_state_bn = _sig("co_conv_init_state_bn", i32,
                              [CD, vp, vp, vp, vp, vp, vp, f32, vp, i64, vp, pvp])
 co_conv_fold_bn = _sig("co_conv_fold_bn", i32, [CD, vp, vp, vp, vp, vp, vp, f32, vp, vp, vp])
 co_act_forward = _sig("co_act_forward", i32, [vp, vp, i64, i32, i32, vp])
+
+
+class BnParams(ctypes.Structure):
+    _fields_ = [("gamma", vp), ("beta", vp), ("mean", vp), ("var", vp), ("eps", ctypes.c_float)]
+
+
+co_conv_forward_ws = _sig("co_conv_forward_ws", i32,
+                          [CD, vp, vp, ctypes.POINTER(BnParams), vp, i32, vp, vp, i64, vp])
 co_bneck_bind = _sig("co_bneck_bind", i32, [vp, i32, vp, i32, vp, pvp])
 co_bneck_forward_step = _sig("co_bneck_forward_step", i32, [vp, vp, vp, i32, vp])
 co_bneck_forward_steps = _sig("co_bneck_forward_steps", i32,
@@ -409,13 +417,14 @@ class CoConv:
         return w, b
 
     def forward(self, x):
-        """Principle 2 forward (clip mode), stateless."""
-        if self.bn is None:
-            return conv_forward(self.desc, self.weight, self.bias, x)
-        w, b = self.folded()
-        d = ConvDesc.from_buffer_copy(self.desc)
-        d.has_bias = 1
-        return conv_forward(d, w, b, x)
+        """Principle 2 forward (clip mode), stateless: on the step kernels
+        from a clean state in a scratch workspace (co_conv_forward_ws), with
+        the batch normalisation folded in as the steps have it."""
+        bn = None
+        if self.bn is not None:
+            gamma, beta, mean, var, eps = self._bn_args()
+            bn = BnParams(gamma, beta, mean, var, eps)
+        return conv_forward(self.desc, self.weight, self.bias, x, bn=bn)
 
     def clean_state(self):
         check(co_conv_clean_state(self.handle, _stream()), "co_conv_clean_state")
@@ -450,7 +459,10 @@ def residual_align(f, s, p, module_delay):
     return d_res.value, shrink.value, delay.value
 
 
-def conv_forward(desc, weight, bias, x):
+def conv_forward(desc, weight, bias, x, bn=None, direct=False):
+    """Clip-mode forward: on the step kernels AUTO picks, from a clean state
+    in a scratch workspace (co_conv_forward_ws), or with direct=True on the
+    direct clip kernel (co_conv_forward)."""
     T = x.shape[2]
     t_out = i32()
     check(co_conv_clip_frames(ctypes.byref(desc), T, ctypes.byref(t_out)), "co_conv_clip_frames")
@@ -458,8 +470,16 @@ def conv_forward(desc, weight, bias, x):
     info = conv_query(desc)
     y = torch.empty((desc.batch, desc.out_channels, t_out.value) + tuple(info.out_size[:sd]),
                     dtype=x.dtype, device=x.device)
-    check(co_conv_forward(ctypes.byref(desc), _ptr(weight), _ptr(bias), _ptr(x), T, _ptr(y),
-                          _stream()), "co_conv_forward")
+    if direct:
+        if bn is not None:
+            raise ValueError("the direct clip kernel takes no batch normalisation")
+        check(co_conv_forward(ctypes.byref(desc), _ptr(weight), _ptr(bias), _ptr(x), T, _ptr(y),
+                              _stream()), "co_conv_forward")
+        return y
+    ws = torch.empty(info.state_bytes, dtype=torch.uint8, device=x.device)
+    check(co_conv_forward_ws(ctypes.byref(desc), _ptr(weight), _ptr(bias),
+                             ctypes.byref(bn) if bn is not None else None, _ptr(x), T, _ptr(y),
+                             _ptr(ws), ws.numel(), _stream()), "co_conv_forward_ws")
     return y
 
 

@@ -448,6 +448,30 @@ co_status co_conv_forward(const co_conv_desc* desc, const void* weight, const vo
   return hip_status(launch_conv_clip(g, T, int32_t(T_out), weight, bias, x, y, as_stream(stream)));
 }
 
+co_status co_conv_forward_ws(const co_conv_desc* desc, const void* weight, const void* bias,
+                             const co_bn_params* bn, const void* x, int32_t T, void* y,
+                             void* workspace, int64_t workspace_bytes, void* stream) {
+  ConvGeom g;
+  co_status st = conv_geom(desc, &g);
+  if (st != CO_OK) return st;
+  if (T < 0 || !weight || (g.has_bias && !bias)) return CO_EINVAL;
+  const int64_t T_out = axis_out_len(T, g.kT, g.sT, g.pT, g.dT);
+  if (T_out == 0) return CO_OK;
+  if (!x || !y || !workspace || T_out > INT32_MAX) return CO_EINVAL;
+  // a clean state in the workspace, then the clip with its end padding: the
+  // steps emit exactly the clip's T_out frames, written in place into y
+  co_conv_handle* h = nullptr;
+  st = bn ? co_conv_init_state_bn(desc, weight, bias, bn->gamma, bn->beta, bn->mean, bn->var,
+                                  bn->eps, workspace, workspace_bytes, stream, &h)
+          : co_conv_init_state(desc, weight, bias, workspace, workspace_bytes, stream, &h);
+  if (st != CO_OK) return st;
+  int32_t n = 0;
+  st = conv_forward_steps(h, x, T, y, int32_t(T_out), 1, 1, as_stream(stream), &n, nullptr);
+  co_conv_destroy(h);
+  if (st == CO_OK && n != T_out) return CO_EINVAL;  // (Principle 4: cannot happen)
+  return st;
+}
+
 co_status co_conv_clean_state(co_conv_handle* h, void* stream) {
   (void)stream;
   if (!live(h, HKind::Conv)) return CO_EINVAL;

@@ -545,3 +545,22 @@ def test_batch_norm_and_activation_validation_without_device():
     assert C.co_act_forward(dev, dev, -1, C.CO_F32, C.CO_ACT_RELU, None) == C.CO_EINVAL
     assert C.co_act_forward(None, None, 0, C.CO_BF16, C.CO_ACT_RELU, None) == C.CO_OK
     assert C.co_act_forward(None, dev, 4, C.CO_F32, C.CO_ACT_RELU, None) == C.CO_EINVAL
+
+
+def test_clip_forward_ws_validation_without_device():
+    """co_conv_forward_ws: a missing workspace or buffer is CO_EINVAL, a
+    workspace below state_bytes CO_ESTATE, a clip too short to emit is a
+    no-op; nothing is launched in these cases."""
+    d = desc1d(k=3, p=0, cin=2, cout=3)
+    info = C.conv_query(d)
+    dev = ctypes.c_void_p(0x1000)
+    assert C.co_conv_forward_ws(ctypes.byref(d), dev, dev, None, dev, 2, dev, dev,
+                                info.state_bytes, None) == C.CO_OK  # T_out = 0
+    assert C.co_conv_forward_ws(ctypes.byref(d), dev, dev, None, dev, 5, dev, None,
+                                info.state_bytes, None) == C.CO_EINVAL
+    assert C.co_conv_forward_ws(ctypes.byref(d), dev, dev, None, None, 5, dev, dev,
+                                info.state_bytes, None) == C.CO_EINVAL
+    assert C.co_conv_forward_ws(ctypes.byref(d), dev, dev, None, dev, 5, dev, dev,
+                                info.state_bytes - 1, None) == C.CO_ESTATE
+    assert C.co_conv_forward_ws(ctypes.byref(d), None, dev, None, dev, 5, dev, dev,
+                                info.state_bytes, None) == C.CO_EINVAL

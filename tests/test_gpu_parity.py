@@ -890,3 +890,65 @@ def test_misaligned_frame_is_staged(algo, dt):
     got = np.stack([np64(o) for o in outs], axis=2)
     ref = oracle_conv(w, b, spec.stride, spec.padding, spec.dilation, 1).forward_steps(np64(x))
     assert_close(got, ref, synth.torch_dtype(dt), f"{algo} misaligned", terms=conv_terms(w))
+
+
+CLIP_WS_CASES = [
+    # algo, B, Cin, Cout, kernel (time first), in_size, stride, padding, dilation, dtype
+    ("gemm_ws", 3, 40, 24, (3, 3, 3), (8, 10), (1, 1, 1), (1, 1, 1), (1, 1, 1), "bf16"),
+    ("gemm", 2, 20, 36, (2, 3, 3), (7, 6), (1, 1, 1), (1, 0, 1), (1, 1, 1), "f32"),
+    ("gemm_reg", 4, 64, 48, (4, 1), (25,), (1, 1), (2, 0), (1, 1), "bf16"),
+    ("gemm_reg", 3, 12, 40, (5, 3, 3), (7, 9), (2, 2, 2), (3, 1, 1), (1, 2, 1), "bf16"),
+    ("depthwise", 3, 10, 10, (3, 3, 3), (7, 7), (1, 1, 1), (1, 1, 1), (1, 1, 1), "bf16"),
+    ("direct", 1, 4, 8, (3,), (), (2,), (1,), (2,), "f32"),
+]
+
+
+@pytest.mark.parametrize("case", CLIP_WS_CASES, ids=lambda c: "clipws_" + c[0] + "_" + c[-1])
+def test_clip_forward_on_step_kernels(case):
+    """co_conv_forward_ws (clip mode on the step kernels, from a clean state
+    in a scratch workspace): the regular convolution of the oracle, the
+    direct clip kernel within the same bound, and forward_steps with end
+    padding from a clean state bit for bit (Principles 2 and 4: a clip
+    processed step by step with its end padding emits the regular output)."""
+    algo, B, ci, co_, k, size, s, p, dil, dt = case
+    say("clip ws", case)
+    tdt = synth.torch_dtype(dt)
+    spec = synth.ConvSpec(batch=B, in_channels=ci, out_channels=co_, kernel=k, in_size=size,
+                          stride=s, padding=p, dilation=dil,
+                          groups=ci if algo == "depthwise" else 1, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, 11, 99000 + ci * 3 + co_, "kaiming")
+    xd = x.to(DEV)
+    G = ci if algo == "depthwise" else 1
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=s, padding=p,
+                            dilation=dil, groups=G, algo=algo)
+
+    co = make()
+    assert co.algo.startswith(algo)
+    clip = co.forward(xd)
+    ref = oracle.conv_forward(np64(x), np64(w), np64(b), s, p, dil, G)
+    assert_close(np64(clip), ref, tdt, f"clip ws {algo}", terms=conv_terms(w))
+    direct = coinf.conv_forward(co.desc, co.weight, co.bias, xd, direct=True)
+    assert_close(np64(direct), ref, tdt, f"clip direct {algo}", terms=conv_terms(w))
+    steps = make().forward_steps(xd, pad_end=True)
+    assert torch.equal(clip, steps)
+
+
+def test_clip_forward_on_step_kernels_64_streams():
+    """The 64-stream layer's clip through co_conv_forward_ws (its steps run
+    on the warp-specialized and persistent GEMM kernels): sampled streams
+    against the oracle's regular convolution."""
+    name = "conv3d_b64_c192_k3_14x14_bf16"
+    wl = synth.WORKLOADS[name]
+    c = wl.conv
+    say("clip ws", name)
+    x, w, b = synth.workload_inputs(name)
+    x = x[:, :, :6].contiguous()
+    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=c.batch, in_size=c.in_size, stride=c.stride,
+                      padding=c.padding, dilation=c.dilation, groups=c.groups)
+    clip = co.forward(x.to(DEV))
+    sel = [0, 31, 63]
+    ref = oracle.conv_forward(np64(x[sel]), np64(w), np64(b), c.stride, c.padding, c.dilation,
+                              c.groups)
+    assert_close(np64(clip[sel]), ref, torch.bfloat16, "64-stream clip", terms=conv_terms(w))
