@@ -79,9 +79,15 @@ typedef int32_t co_status;
 #define CO_BF16  1
 
 /* Algorithm choice for a convolution (all compute the same result). */
-#define CO_ALGO_AUTO       0   /* library heuristic */
+#define CO_ALGO_AUTO       0   /* library heuristic: depthwise where it applies;
+                                  else the register GEMM below 3e8
+                                  multiply-accumulates per step, the
+                                  warp-specialized GEMM, the LDS-tiled GEMM,
+                                  the register GEMM, the direct kernel: the
+                                  first that applies (tiny layers direct) */
 #define CO_ALGO_DIRECT     1   /* generic direct kernel, any shape */
-#define CO_ALGO_GEMM       2   /* implicit GEMM on MFMA (groups = 1) */
+#define CO_ALGO_GEMM       2   /* implicit GEMM on MFMA, operand tiles staged
+                                  through LDS (groups = 1) */
 #define CO_ALGO_DEPTHWISE  3   /* depthwise stencil (groups = C_in = C_out) */
 #define CO_ALGO_GEMM_REG   4   /* implicit GEMM on MFMA with register operands
                                   (groups = 1, small kH*kW*C_in) */
@@ -92,8 +98,7 @@ typedef int32_t co_status;
                                   waves stage the input, consumer waves stream the
                                   weights from L2 (bf16, groups = 1, 3x3 spatial
                                   taps, stride and dilation 1, spatial padding <= 1,
-                                  Ho*Wo a multiple of 4); AUTO picks it for layers
-                                  with at least 128 of its 448 x 64 tiles */
+                                  Ho*Wo a multiple of 4) */
 
 #define CO_POOL_AVG  0
 #define CO_POOL_MAX  1

@@ -187,10 +187,8 @@ bool gemm_steps_config(const ConvGeom& g, GemmStepsConfig* c) {
 }
 
 int gemm_pick(const ConvGeom& g) {
-  // the warp-specialized kernel when its tiles cover the chip
-  GemmConfig w;
-  if (gemm_config(g, kGemmWs, &w) && int64_t(w.m_tiles) * w.n_tiles >= kWsMinTiles)
-    return kGemmWs;
+  // LDS-tiled configurations only: the warp-specialized one is its own
+  // algorithm (CO_ALGO_GEMM_WS)
   int best = -1;
   double best_cost = 0;
   for (int id = 0; id < kGemmConfigs; ++id) {
@@ -452,17 +450,27 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
   // whose single pass costs less than staging tiles through LDS
   const double macs = double(r.B) * r.So() * r.Cout * r.kT * r.Cg * r.kH * r.kW;
   if (algo == CO_ALGO_AUTO) {
-    // depthwise stencil; else matrix cores, with operands in registers when
-    // the reduction is shallow enough (one memory round trip per step) and
-    // staged through LDS otherwise; tiny layers on the direct kernel
-    // (the frame-resident GEMM is chosen only on request: on the 64-stream
-    // 14x14 layer it measures slower than the LDS-tiled kernel)
+    // Depthwise stencil; else matrix cores: operands in registers below
+    // kRegMaxAutoMacs multiply-accumulates per step (one memory round trip
+    // per step, which the LDS-staged kernels cannot amortize on small layers;
+    // measured on bf16 3x3 and 3x1x1 layers from 14 to 1400 M), above it the
+    // warp-specialized GEMM where it applies (faster than the LDS-tiled
+    // configurations from 14 to 252 of its tiles), else the LDS-tiled GEMM;
+    // tiny layers on the direct kernel.  The frame-resident GEMM is chosen
+    // only on request: it never measured faster than these.
+    GemmConfig wc;
     if (depthwise_supported(r))
       algo = CO_ALGO_DEPTHWISE;
+    else if (reg_supported(r) && macs < kRegMaxAutoMacs)
+      algo = CO_ALGO_GEMM_REG;
+    else if (macs >= 1.0e5 && gemm_config(r, kGemmWs, &wc))
+      algo = CO_ALGO_GEMM_WS;
+    else if (macs >= 1.0e5 && gemm_supported(r))
+      algo = CO_ALGO_GEMM;
     else if (reg_supported(r))
       algo = CO_ALGO_GEMM_REG;
     else
-      algo = (macs >= 1.0e5 && gemm_supported(r)) ? CO_ALGO_GEMM : CO_ALGO_DIRECT;
+      algo = CO_ALGO_DIRECT;
   } else if (algo == CO_ALGO_DEPTHWISE) {
     if (!depthwise_supported(r)) return CO_ENOTSUP;
   } else if (algo == CO_ALGO_GEMM) {

@@ -135,7 +135,9 @@ constexpr int kGemmWs = 4;             // the warp-specialized bf16 3x3 configur
 constexpr int kWsWM = 7;               // consumer wave: 7 pixel fragments ...
 constexpr int kWsWN = 4;               // ... x 4 column fragments of 16x16
 constexpr int kWsWaves = 4;            // consumer waves (and as many producer waves)
-constexpr int kWsMinTiles = 128;       // tiles below which the ws kernel leaves CUs idle
+// Multiply-accumulates per step above which AUTO takes the LDS-staged GEMM
+// family over the register GEMM.
+constexpr double kRegMaxAutoMacs = 3.0e8;
 constexpr int kGemmPixUnits = 5;  // 16-byte units per staged pixel (4 + 1 pad)
 constexpr int kGemmStageItems = 1024;  // staging items per workgroup and chunk
 constexpr int64_t kLdsBytes = 160 * 1024;

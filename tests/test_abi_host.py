@@ -503,8 +503,10 @@ def test_pool_frames_of_2GiB_are_rejected():
 
 def test_warp_specialized_gemm_selection():
     """CO_ALGO_GEMM_WS: granted for bf16 3x3 layers with Ho*Wo % 4 == 0 and
-    spatial padding <= 1, refused otherwise; AUTO picks it for the 64-stream
-    layer (252 tiles of 448 x 64) and not for a small one."""
+    spatial padding <= 1, refused otherwise.  AUTO takes the register GEMM
+    below 3e8 multiply-accumulates per step and the warp-specialized GEMM
+    above it where it applies (the 64-stream layer, a 16-stream 128-channel
+    layer), else the LDS-tiled GEMM."""
     def q(B, cin, cout, size, pad=(0, 1, 1), dtype=C.CO_BF16, algo=C.CO_ALGO_GEMM_WS, k=(3, 3, 3)):
         d = C.conv_desc(B, cin, cout, k, size, (1, 1, 1), pad, (1, 1, 1), 1, True, dtype,
                         algo=algo)
@@ -520,6 +522,12 @@ def test_warp_specialized_gemm_selection():
     st, big = q(64, 192, 192, (14, 14), algo=C.CO_ALGO_AUTO)
     st2, forced = q(64, 192, 192, (14, 14))
     assert st == st2 == C.CO_OK and big.state_bytes == forced.state_bytes
+    # AUTO by the work of a step
+    assert q(3, 40, 24, (8, 10), algo=C.CO_ALGO_AUTO)[1].algo == C.CO_ALGO_GEMM_REG
+    st, mid = q(16, 128, 128, (14, 14), algo=C.CO_ALGO_AUTO)
+    assert st == C.CO_OK and mid.state_bytes == q(16, 128, 128, (14, 14))[1].state_bytes
+    st, wide = q(4, 256, 256, (28, 28), pad=(0, 0, 0), k=(3, 1, 1), algo=C.CO_ALGO_AUTO)
+    assert st == C.CO_OK and wide.algo == C.CO_ALGO_GEMM                # 617 M: LDS-tiled
 
 
 def test_batch_norm_and_activation_validation_without_device():
