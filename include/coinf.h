@@ -91,10 +91,7 @@ typedef int32_t co_status;
 #define CO_ALGO_DEPTHWISE  3   /* depthwise stencil (groups = C_in = C_out) */
 #define CO_ALGO_GEMM_REG   4   /* implicit GEMM on MFMA with register operands
                                   (groups = 1, small kH*kW*C_in) */
-#define CO_ALGO_GEMM_IMG   5   /* implicit GEMM on MFMA with each stream's whole
-                                  frame resident in LDS (bf16, groups = 1,
-                                  small frames, C_in a multiple of 8) */
-#define CO_ALGO_GEMM_WS    6   /* implicit GEMM on MFMA, warp-specialized: producer
+#define CO_ALGO_GEMM_WS    5   /* implicit GEMM on MFMA, warp-specialized: producer
                                   waves stage the input, consumer waves stream the
                                   weights from L2 (bf16, groups = 1, 3x3 spatial
                                   taps, stride and dilation 1, spatial padding <= 1,

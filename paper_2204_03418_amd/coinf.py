@@ -25,8 +25,7 @@ CO_OK, CO_EMPTY, CO_EINVAL, CO_ENOTSUP, CO_ESTATE, CO_EHIP = 0, 1, -1, -2, -3, -
 CO_ESCRATCH = -5
 CO_F32, CO_BF16 = 0, 1
 CO_ALGO_AUTO, CO_ALGO_DIRECT, CO_ALGO_GEMM, CO_ALGO_DEPTHWISE, CO_ALGO_GEMM_REG = 0, 1, 2, 3, 4
-CO_ALGO_GEMM_IMG = 5
-CO_ALGO_GEMM_WS = 6
+CO_ALGO_GEMM_WS = 5
 CO_ACT_NONE, CO_ACT_RELU = 0, 1
 CO_POOL_AVG, CO_POOL_MAX = 0, 1
 CO_MAX_TAPS = 64
@@ -34,7 +33,7 @@ CO_TAP_NONE, CO_TAP_START, CO_TAP_ACC, CO_TAP_EMIT, CO_TAP_EMIT_FRESH = 0, 1, 2,
 
 ALGOS = {"auto": CO_ALGO_AUTO, "direct": CO_ALGO_DIRECT, "gemm": CO_ALGO_GEMM,
          "depthwise": CO_ALGO_DEPTHWISE, "gemm_reg": CO_ALGO_GEMM_REG,
-         "gemm_img": CO_ALGO_GEMM_IMG, "gemm_ws": CO_ALGO_GEMM_WS}
+         "gemm_ws": CO_ALGO_GEMM_WS}
 DTYPES = {torch.float32: CO_F32, torch.bfloat16: CO_BF16}
 
 i32, i64, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p

@@ -532,7 +532,6 @@ const char* co_conv_algo_name(const co_conv_handle* h) {
       if (h->g.cfg == kGemmWs) return "gemm_ws_bf16";
       return h->g.dtype == CO_BF16 ? "gemm_bf16" : "gemm_f32";
     case CO_ALGO_GEMM_REG: return h->g.dtype == CO_BF16 ? "gemm_reg_bf16" : "gemm_reg_f32";
-    case CO_ALGO_GEMM_IMG: return "gemm_img_bf16";
     default: return "direct";
   }
 }

@@ -415,7 +415,6 @@ int64_t conv_step_staging_bytes(const ConvGeom& g, const StepIO& io) {
   switch (g.algo) {
     case CO_ALGO_GEMM: staged = gemm_step_needs_staging(g, io); break;
     case CO_ALGO_GEMM_REG: staged = reg_step_needs_staging(g, io); break;
-    case CO_ALGO_GEMM_IMG: staged = img_step_needs_staging(g, io); break;
     default: return 0;  // the direct and depthwise kernels use 64-bit offsets
   }
   if (!staged) return 0;
@@ -496,7 +495,6 @@ hipError_t launch_conv_step(const ConvGeom& g, const ConvLayout& L, char* state,
     case CO_ALGO_DEPTHWISE: return launch_conv_step_depthwise(g, L, state, io, plan, s);
     case CO_ALGO_GEMM: return launch_conv_step_gemm(g, L, state, io, plan, s);
     case CO_ALGO_GEMM_REG: return launch_conv_step_reg(g, L, state, io, plan, s);
-    case CO_ALGO_GEMM_IMG: return launch_conv_step_img(g, L, state, io, plan, s);
     default: return launch_conv_step_direct(g, L, state, io, plan, false, s);
   }
 }
@@ -515,8 +513,6 @@ hipError_t pack_weights_and_header(const ConvGeom& g, const ConvLayout& L, char*
       e = launch_pack_gemm_steps(g, L, state, weight, wscale, s);
   } else if (g.algo == CO_ALGO_GEMM_REG) {
     e = launch_pack_reg(g, L, state, weight, wscale, s);
-  } else if (g.algo == CO_ALGO_GEMM_IMG) {
-    e = launch_pack_img(g, L, state, weight, wscale, s);
   } else {
     const int64_t per_out = int64_t(g.Cg) * g.kT * g.kH * g.kW;
     const int64_t n = int64_t(g.Cout) * per_out;

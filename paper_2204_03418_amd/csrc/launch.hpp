@@ -92,7 +92,6 @@ int64_t conv_step_staging_bytes(const ConvGeom& g, const StepIO& io);
 // have it staged (true).
 bool gemm_step_needs_staging(const ConvGeom& g, const StepIO& io);
 bool reg_step_needs_staging(const ConvGeom& g, const StepIO& io);
-bool img_step_needs_staging(const ConvGeom& g, const StepIO& io);
 // Persistent forward_steps of small direct layers (same conventions as the
 // depthwise one): temporal stride 1 and dilation 1, kT <= 4 and
 // C_in/G * kH * kW <= 16.
@@ -126,10 +125,6 @@ hipError_t launch_conv_steps_reg(const ConvGeom& g, const ConvLayout& L, char* s
                                  const void* x, int64_t x_bc, int32_t T, int32_t count, void* y,
                                  int64_t y_bc, int64_t n0, bool update, hipStream_t stream);
 hipError_t launch_pack_reg(const ConvGeom& g, const ConvLayout& L, char* state,
-                           const void* weight, const float* wscale, hipStream_t stream);
-hipError_t launch_conv_step_img(const ConvGeom& g, const ConvLayout& L, char* state,
-                                const StepIO& io, const co_step_plan& plan, hipStream_t stream);
-hipError_t launch_pack_img(const ConvGeom& g, const ConvLayout& L, char* state,
                            const void* weight, const float* wscale, hipStream_t stream);
 // Persistent forward_steps of the LDS-tiled GEMM (bf16; same conventions as
 // the depthwise one): temporal stride 1 and dilation 1, kT <= 3, 3x3 or 1x1

@@ -317,46 +317,6 @@ int reg_pick(const ConvGeom& g) {
 
 bool reg_supported(const ConvGeom& g) { return reg_pick(g) >= 0; }
 
-bool img_config(const ConvGeom& g, ImgConfig* c) {
-  const bool taps = (g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1);
-  if (g.dtype != CO_BF16 || g.G != 1 || !taps || g.sH != 1 || g.sW != 1 || g.dH != 1 ||
-      g.dW != 1 || g.Cin % 8 != 0 || !frame_offsets_fit(g))
-    return false;
-  ImgConfig r{};
-  const int64_t mf = ceil_div(g.So(), 16);
-  r.mo = int32_t(mf / 4);
-  r.mr = int32_t(mf % 4);
-  // instantiated (own, shared) fragment rows per wave
-  const int key = r.mo * 4 + r.mr;
-  if (key != 4 && key != 9 && key != 13 && key != 16) return false;
-  r.MT = r.mo + r.mr;
-  r.NF = kImgNF;
-  r.slabs = int32_t(ceil_div(int64_t(g.kT) * g.Cout, 16 * r.NF));
-  // channel blocks, padded so the k-steps fill whole weight stages (the
-  // padding blocks are zero in the frame and in the weights)
-  const int khw = g.kH * g.kW;
-  r.cbs = int32_t(ceil_div(g.Cin, 32));
-  while ((r.cbs * khw) % kImgKC) ++r.cbs;
-  r.pix_units = 4 * r.cbs + 1;  // odd: 16 consecutive pixels hit 16 bank groups
-  r.cols = g.W + g.pW;
-  const int64_t a_pixels = int64_t(g.H + 2 * g.pH) * r.cols + g.pW;
-  r.a_units = int32_t(a_pixels * r.pix_units);
-  r.nsteps = r.cbs * khw;
-  r.nchunks = r.nsteps / kImgKC;
-  r.pair = g.W % 2 == 0 ? 1 : 0;
-  r.pairs = g.H * (r.pair ? g.W / 2 : g.W);
-  r.items = r.pairs * (g.Cin / 8);
-  if (r.items > kImgItems * kImgThreadsHost) return false;
-  const int64_t b_bytes = 2 * int64_t(kImgKC) * r.NF * 1024;
-  // (after the main loop the same LDS holds the pairs' partial sums)
-  const int64_t nacc = int64_t(r.mo) * r.NF + r.mr * ((r.NF + 3) / 4);
-  r.lds_bytes = std::max<int64_t>(int64_t(r.a_units) * 16 + b_bytes, 4 * nacc * 1024);
-  if (r.lds_bytes > kLdsBytes) return false;
-  r.weight_units = int64_t(r.slabs) * r.nchunks * kImgKC * r.NF * 64;
-  *c = r;
-  return true;
-}
-
 int64_t packed_weight_bytes(const ConvGeom& g) {
   const int64_t n = int64_t(g.Cout) * g.Cg * g.kT * g.kH * g.kW;
   if (g.algo == CO_ALGO_GEMM) {
@@ -365,12 +325,6 @@ int64_t packed_weight_bytes(const ConvGeom& g) {
     if (!gemm_config(g, g.cfg, &c)) return 0;
     return int64_t(c.n_tiles) * c.n_chunks * g.kH * g.kW * c.N_WG * c.CK *
            (g.dtype == CO_BF16 ? 2 : 4);
-  }
-  if (g.algo == CO_ALGO_GEMM_IMG) {
-    // [slab][weight stage][k-step][column][4 units of 8 channels], 16 bytes each
-    ImgConfig c;
-    if (!img_config(g, &c)) return 0;
-    return c.weight_units * 16;
   }
   if (g.algo == CO_ALGO_GEMM_REG) {
     // [fragment][unit][lane] of 16 bytes, in the matrix instruction's order
@@ -456,8 +410,7 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
     // measured on bf16 3x3 and 3x1x1 layers from 14 to 1400 M), above it the
     // warp-specialized GEMM where it applies (faster than the LDS-tiled
     // configurations from 14 to 252 of its tiles), else the LDS-tiled GEMM;
-    // tiny layers on the direct kernel.  The frame-resident GEMM is chosen
-    // only on request: it never measured faster than these.
+    // tiny layers on the direct kernel.
     GemmConfig wc;
     if (depthwise_supported(r))
       algo = CO_ALGO_DEPTHWISE;
@@ -477,9 +430,6 @@ co_status conv_geom(const co_conv_desc* desc, ConvGeom* g) {
     if (!gemm_supported(r)) return CO_ENOTSUP;
   } else if (algo == CO_ALGO_GEMM_REG) {
     if (!reg_supported(r)) return CO_ENOTSUP;
-  } else if (algo == CO_ALGO_GEMM_IMG) {
-    ImgConfig ic;
-    if (!img_config(r, &ic)) return CO_ENOTSUP;
   }
   if (algo == CO_ALGO_GEMM_WS) {
     GemmConfig wc;

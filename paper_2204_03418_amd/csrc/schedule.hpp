@@ -99,35 +99,6 @@ struct RegConfig {
   int32_t n_frags;  // 16-column fragments, ceil(kT*C_out / 16)
 };
 
-// Frame-resident implicit GEMM (bf16): a workgroup of four waves owns one
-// stream's whole frame, staged once into LDS with every input channel, and a
-// slab of 16*NF output columns (temporal tap, output channel) whose weights
-// stream through LDS in stages of kImgKC k-steps.  The frame's 16-pixel
-// fragments are dealt to the waves: `mo` each, and a single remaining one
-// (mr = 1) is shared out among them by column fragments.
-struct ImgConfig {
-  int32_t NF;          // 16-column fragments per slab
-  int32_t MT;          // accumulator fragment rows per wave: mo + mr
-  int32_t mo, mr;      // own and shared pixel fragments per wave
-  int32_t slabs;       // column slabs: ceil(kT*C_out / (16*NF))
-  int32_t cbs;         // channel blocks of 32, padded so kH*kW*cbs % kImgKC == 0
-  int32_t pix_units;   // 16-byte LDS units per staged pixel: 4*cbs + 1
-  int32_t cols;        // staged row pitch in pixels: W + pW (rows share their halo)
-  int32_t a_units;     // 16-byte units of the staged frame
-  int32_t nsteps;      // k-steps: cbs * kH * kW
-  int32_t nchunks;     // weight stages: nsteps / kImgKC
-  int32_t items;       // staging items: pixel pairs (or pixels) x channel octets
-  int32_t pairs;       // staging items per channel octet
-  int32_t pair;        // even width: two pixels per staging load
-  int64_t lds_bytes;   // a_units*16 + two weight stages
-  int64_t weight_units;  // packed weights, 16-byte units
-};
-
-constexpr int kImgKC = 3;          // k-steps per weight stage
-constexpr int kImgNF = 9;          // 16-column fragments per slab (144 columns)
-constexpr int kImgItems = 5;       // staging items per thread (512 threads)
-constexpr int kImgThreadsHost = 512;
-
 constexpr int kRegConfigs = 10;
 
 constexpr int kGemmConfigs = 5;
@@ -257,7 +228,6 @@ int gemm_pick(const ConvGeom& g);
 // Register-operand GEMM: derived sizes of instantiation `id` (false when it
 // does not apply) and the one the library picks (-1: none holds K).
 bool reg_config(const ConvGeom& g, int id, RegConfig* c);
-bool img_config(const ConvGeom& g, ImgConfig* c);
 int reg_pick(const ConvGeom& g);
 bool reg_supported(const ConvGeom& g);
 

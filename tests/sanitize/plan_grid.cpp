@@ -73,8 +73,6 @@ static void check_conv_plans(const ConvGeom& g) {
   }
   GemmStepsConfig sc;
   (void)gemm_steps_config(g, &sc);
-  ImgConfig ic;
-  (void)img_config(g, &ic);
   (void)reg_pick(g);
   (void)packed_weight_bytes(g);
 }

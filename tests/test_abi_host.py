@@ -312,28 +312,6 @@ def test_register_gemm_shapes():
     assert _status(grouped) == C.CO_ENOTSUP
 
 
-def test_frame_resident_gemm_shapes():
-    """The frame-resident GEMM keeps one stream's frame, every channel of it,
-    in LDS: bf16, groups 1, 3x3 or 1x1 spatial taps at stride 1, C_in a
-    multiple of 8, frames of at most 16 x 16-pixel fragments per wave set."""
-    auto = C.conv_desc(64, 192, 192, (3, 3, 3), (14, 14), padding=(0, 1, 1), dtype=C.CO_BF16)
-    assert C.conv_query(auto).algo == C.CO_ALGO_GEMM        # only on request
-    forced = C.conv_desc(2, 192, 192, (3, 3, 3), (14, 14), padding=(0, 1, 1), dtype=C.CO_BF16,
-                         algo="gemm_img")
-    assert C.conv_query(forced).algo == C.CO_ALGO_GEMM_IMG
-    for bad in (C.conv_desc(2, 192, 192, (3, 3, 3), (14, 14), padding=(0, 1, 1),
-                            algo="gemm_img"),                                  # float32
-                C.conv_desc(2, 20, 32, (3, 3, 3), (14, 14), padding=(0, 1, 1),
-                            dtype=C.CO_BF16, algo="gemm_img"),                 # C_in % 8
-                C.conv_desc(2, 32, 32, (3, 3, 3), (28, 28), padding=(0, 1, 1),
-                            dtype=C.CO_BF16, algo="gemm_img"),                 # 49 fragments
-                C.conv_desc(2, 32, 32, (3, 5, 5), (14, 14), padding=(0, 2, 2),
-                            dtype=C.CO_BF16, algo="gemm_img"),                 # 5x5 taps
-                C.conv_desc(2, 512, 32, (3, 3, 3), (14, 14), padding=(0, 1, 1),
-                            dtype=C.CO_BF16, algo="gemm_img")):                # LDS
-        assert _status(bad) == C.CO_ENOTSUP
-
-
 def _chain(f, s, p):
     n = len(f)
     arr = ctypes.c_int32 * n

@@ -64,7 +64,6 @@ ALGO_CASES = [
     ("gemm_reg", 3, 12, 40, (3, 3, 3), (7, 9), (1, 1, 1), 1, "bf16"),
     ("gemm_reg", 4, 16, 16, (1, 3, 3), (8, 8), (0, 1, 1), 1, "f32"),
     ("gemm_ws", 3, 40, 24, (3, 3, 3), (8, 10), (0, 1, 1), 1, "bf16"),
-    ("gemm_img", 2, 48, 64, (3, 3, 3), (12, 12), (1, 1, 1), 1, "bf16"),
     ("depthwise", 3, 10, 10, (3, 3, 3), (7, 7), (1, 1, 1), 10, "bf16"),
     ("depthwise", 2, 6, 6, (2, 3, 3), (5, 6), (0, 1, 1), 6, "f32"),
 ]

@@ -469,64 +469,6 @@ def test_gemm_reg_forced(case):
         assert_close(np64(ys), rp, tdt, "gemm_reg steps pad_end", terms=conv_terms(w))
 
 
-IMG_CASES = [
-    # B, Cin, Cout, kernel (time first), in_size, stride, padding, dilation
-    (2, 192, 192, (3, 3, 3), (14, 14), (1, 1, 1), (0, 1, 1), (1, 1, 1)),   # the 64-stream layer
-    (3, 40, 24, (3, 3, 3), (11, 13), (1, 1, 1), (1, 1, 1), (1, 1, 1)),     # odd width, 1 shared
-    (2, 64, 80, (2, 1, 1), (7, 9), (1, 1, 1), (1, 0, 0), (1, 1, 1)),       # 1x1, ragged frame
-    (5, 16, 48, (4, 3, 3), (10, 10), (1, 1, 1), (0, 0, 0), (1, 1, 1)),     # valid rows, 2 slabs
-    (2, 48, 64, (3, 3, 3), (12, 12), (1, 1, 1), (1, 1, 1), (1, 1, 1)),     # 2 own + 1 shared
-    (3, 24, 100, (3, 3, 3), (7, 7), (1, 1, 1), (2, 1, 1), (1, 1, 1)),      # delay 0, 3 slabs
-    (2, 32, 40, (3, 3, 3), (8, 8), (2, 1, 1), (1, 1, 1), (2, 1, 1)),       # temporal stride, dil
-    (4, 96, 80, (5, 3, 3), (14, 14), (1, 1, 1), (2, 1, 1), (1, 1, 1)),     # 3 channel blocks
-    (3, 16, 16, (1, 3, 3), (8, 8), (1, 1, 1), (0, 1, 1), (1, 1, 1)),       # kT = 1: no ring
-    (2, 32, 32, (3, 3, 3), (16, 16), (1, 1, 1), (0, 1, 1), (1, 1, 1)),     # 16 fragments, none shared
-]
-
-
-@pytest.mark.parametrize("case", IMG_CASES, ids=lambda c: "img_" + "_".join(map(str, c[:3])))
-def test_gemm_img_forced(case):
-    """Frame-resident GEMM step (forced, bf16) against the oracle: forward_step
-    with update_state=False peeks, then forward_steps with end padding (frames
-    read in place from the clip)."""
-    B, cin, cout, k, size, s, p, dil = case
-    say("gemm_img", case)
-    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
-                          stride=s, padding=p, dilation=dil, dtype="bf16")
-    x, w, b = synth.conv_inputs(spec, 12, 81000 + cin * 7 + cout, "kaiming")
-    co = coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=s, padding=p,
-                      dilation=dil, algo="gemm_img")
-    assert co.algo == "gemm_img_bf16"
-    ref = oracle_conv(w, b, s, p, dil, 1)
-    xd = x.to(DEV)
-    outs, peeks = [], []
-    for t in range(x.shape[2]):
-        fr = xd[:, :, t].contiguous()
-        pk = co.forward_step(fr, update_state=False)
-        if pk is not None:
-            peeks.append(pk.clone())
-        y = co.forward_step(fr)
-        if y is not None:
-            outs.append(y.clone())
-    r = ref.forward_steps(np64(x))
-    if r is None:
-        assert not outs
-    else:
-        got = np.stack([np64(o) for o in outs], axis=2)
-        assert_close(got, r, torch.bfloat16, "gemm_img steps", terms=conv_terms(w))
-        assert len(peeks) == len(outs)
-        for a, bb in zip(peeks, outs):
-            assert torch.equal(a, bb)
-    co.clean_state()
-    ref.clean_state()
-    ys = co.forward_steps(xd, pad_end=True)
-    rp = ref.forward_steps(np64(x), pad_end=True)
-    if rp is None:
-        assert ys is None
-    else:
-        assert_close(np64(ys), rp, torch.bfloat16, "gemm_img steps pad_end", terms=conv_terms(w))
-
-
 DW_STEPS_CASES = [
     # B, C, kT, (kH, kW), in_size, (pT, pH, pW), dtype
     (3, 20, 3, (3, 3), (7, 7), (0, 1, 1), "bf16"),    # the X3D-style block, small
@@ -817,7 +759,7 @@ LARGE_CLIP_CASES = [
     ("avgpool", 2, 32, (64, 64), "f32", 2100),
     ("gemm", 2, 32, (64, 64), "f32", 2100),
     ("gemm_reg", 2, 24, (64, 64), "f32", 2800),
-    ("gemm_img", 8, 32, (14, 14), "bf16", 21504),
+    ("gemm_ws", 8, 32, (14, 14), "bf16", 21504),
 ]
 
 
@@ -865,7 +807,7 @@ def test_forward_steps_clip_beyond_32bit_offsets(case):
                      terms=27 if what == "avgpool" else conv_terms(w))
 
 
-@pytest.mark.parametrize("algo,dt", [("gemm", "bf16"), ("gemm", "f32"), ("gemm_img", "bf16")])
+@pytest.mark.parametrize("algo,dt", [("gemm", "bf16"), ("gemm", "f32"), ("gemm_ws", "bf16")])
 def test_misaligned_frame_is_staged(algo, dt):
     """A frame that starts one element past an aligned address: the GEMM-family
     step stages it into an aligned copy and still matches the oracle."""
