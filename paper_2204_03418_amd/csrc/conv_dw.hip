@@ -159,7 +159,7 @@ struct DwSteps {
   int32_t k0;       // output frame index of the call's first frame: n0 - max(n0, d)
   int32_t update;   // write the live partial sums back
   int32_t x_bytes, y_bytes;  // buffer extents from the clip pointers
-  FastDiv fd_So, fd_Cout, fd_Wo;
+  FastDiv fd_So, fd_Cout, fd_Wo, fd_W;
 };
 
 constexpr int PF = 4;  // frames in flight per thread
@@ -277,24 +277,29 @@ __global__ __launch_bounds__(kBlock) void conv_steps_dw_kernel(
   }
 }
 
-// Small planes (Ho * Wo <= 64): one wave per (stream, channel) plane and one
-// lane per output pixel.  A plane's frames lie contiguously in the clip, so
-// the wave moves a block of F frames with a couple of 16-byte loads per lane
-// (aligned down to 16 bytes; the buffer returns zero past its end) into its
-// own LDS region, and each lane reads its stencil from there.  The
-// thread-per-output kernel above issues one 2-byte gather per tap, output
-// and frame instead.  Double buffered: block k + 1 sits in registers while
-// block k is evaluated.  The taps, partial sums and summation order are those
-// of the thread-per-output kernel.
-constexpr int kDwpWaves = 4;   // planes per workgroup
-constexpr int kDwpLoads = 2;   // 16-byte loads per lane and block
-constexpr int kDwpUnits = 64 * kDwpLoads;  // 16-byte LDS units per wave and buffer
+// Small planes (H * W <= 64 and Ho * Wo <= 64): one wave per (stream,
+// channel) plane, one lane per input pixel and per output pixel.  Each frame
+// is written, as float, into a zero-haloed tile of LDS, so every stencil tap
+// is one LDS read at a lane address fixed for the whole clip plus a
+// compile-time slot offset: no bounds test per tap, no address arithmetic per
+// frame.  The channel's weights are wave-uniform (scalar registers).  Frames
+// go in groups of U: while a group is evaluated from its U slots, the next
+// group's pixels are in flight in registers.  Groups whose frames all take
+// every tap on a real output (past a stream's start) skip the start and
+// existence tests.  Each
+// wave owns its slots, and LDS operations of a wave complete in program
+// order, so only the compiler is kept from reordering them (no barrier).
+// Taps, partial sums and summation order are those of the thread-per-output
+// kernel above.
+constexpr int kDwpWaves = 4;    // planes per workgroup (independent waves)
+constexpr int kDwpSlot = 128;   // floats per frame slot: padded tile + one sink cell
 
 struct DwpArgs {
-  int32_t F;        // frames per block: (F * S * esz + 31) <= 16 * kDwpUnits
-  int32_t nblk;     // blocks: ceil(count / F)
-  int32_t frame_bytes;
+  int32_t PW;         // padded tile width: W + 2 pW
+  int32_t frame_bytes;  // input frame, bytes (frames of a plane are contiguous)
 };
+
+__device__ __forceinline__ void lds_order() { __asm__ volatile("" ::: "memory"); }
 
 template <typename T, int KH, int KW, int KT>
 __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
@@ -302,19 +307,42 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
     T* __restrict__ y, int64_t y_bc, const float* __restrict__ w,
     const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot) {
   constexpr int NS = KH * KW;
+  constexpr int U = KT * ((4 + KT - 1) / KT);  // frames per group (acc names cycle)
   constexpr uint32_t esz = sizeof(T);
-  __shared__ uint4 lds[kDwpWaves][2][kDwpUnits];
+  __shared__ float lds[kDwpWaves][U][kDwpSlot];
   const int lane = int(threadIdx.x) & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
-  const int BC = g.B * g.Cout;
-  const int bc_raw = int(blockIdx.x) * kDwpWaves + wave;
-  const bool wlive = bc_raw < BC;  // whole waves; idle ones still meet the barriers
-  const int bc = wlive ? bc_raw : 0;
-  const int So = g.Ho * g.Wo;
-  const bool pl = wlive && lane < So;
-  const int p = lane < So ? lane : 0;
+  const int bc = int(blockIdx.x) * kDwpWaves + wave;
+  if (bc >= g.B * g.Cout) return;  // whole waves; no workgroup barrier below
+  const int S = g.H * g.W, So = g.Ho * g.Wo;
   const int bq = fdiv(bc, ds.fd_Cout), c = bc - bq * g.Cout;
+  float(*sl)[kDwpSlot] = lds[wave];
+
+  // zero the tiles once: halo cells are never written again
+  for (int e = lane; e < U * kDwpSlot; e += 64) (&sl[0][0])[e] = 0.f;
+
+  // input lane: pixel `lane` of the frame into its padded cell (lanes past
+  // the frame load zero into the sink cell after the tile)
+  const bool in_px = lane < S;
+  int wpos = kDwpSlot - 1;
+  if (in_px) {
+    const int hp = fdiv(lane, ds.fd_W);
+    wpos = (hp + g.pH) * pa.PW + (lane - hp * g.W) + g.pW;
+  }
+  float* const wp = &sl[0][wpos];  // + u * kDwpSlot: slot u
+  const int plane = int(uint32_t(bc) * uint32_t(x_bc) * esz);
+  const int xin = in_px ? plane + lane * int(esz) : kOutOfRange;
+  // output lane: its stencil cells in the padded tile
+  const bool pl = lane < So;
+  const int p = pl ? lane : 0;
   const int i = fdiv(p, ds.fd_Wo), jo = p - i * g.Wo;
+  const float* rp[NS];  // + u * kDwpSlot: slot u
+#pragma unroll
+  for (int u = 0; u < KH; ++u)
+#pragma unroll
+    for (int v = 0; v < KW; ++v)
+      rp[u * KW + v] = &sl[0][(i * g.sH + u * g.dH) * pa.PW + jo * g.sW + v * g.dW];
+  const int yo = pl ? int((uint32_t(bc) * uint32_t(y_bc) + uint32_t(p)) * esz) : kOutOfRange;
   const int ridx = (c * g.B + bq) * So + p;
 
   float wr[KT][NS];
@@ -327,115 +355,92 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
 #pragma unroll
   for (int q = 0; q < KT; ++q) {
     const int tau = ds.v0 - (KT - 1) + q;
-    const int sl = (ds.slot0 + q) % KT;
-    acc[q] = (pl && q < KT - 1 && tau >= 0) ? ring[sl * ring_slot + ridx] : 0.f;
-  }
-  // stencil: element offset inside a frame, or -1 outside it
-  int soff[NS];
-#pragma unroll
-  for (int u = 0; u < KH; ++u) {
-    const int hi = i * g.sH + u * g.dH - g.pH;
-#pragma unroll
-    for (int v = 0; v < KW; ++v) {
-      const int wi = jo * g.sW + v * g.dW - g.pW;
-      const bool in = hi >= 0 && hi < g.H && wi >= 0 && wi < g.W;
-      soff[u * KW + v] = in ? hi * g.W + wi : -1;
-    }
+    const int slq = (ds.slot0 + q) % KT;
+    acc[q] = (pl && q < KT - 1 && tau >= 0) ? ring[slq * ring_slot + ridx] : 0.f;
   }
 
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ds.x_bytes);
-  const int plane0 = int(uint32_t(bc) * uint32_t(x_bc) * esz);  // byte offset of the plane's clip
-  // block k: real frames [k F, min(k F + F, T)) of the plane, from the
-  // 16-byte boundary at or below their first byte
-  auto fetch = [&](int k, uint4 (&rb)[kDwpLoads]) {
-    const int t0 = k * pa.F;
-    const int nr = min(max(ds.T - t0, 0), pa.F);
-    const int s0 = plane0 + t0 * pa.frame_bytes;
-    const int a0 = s0 & ~15;
-    const int nunits = nr > 0 ? (s0 + nr * pa.frame_bytes - a0 + 15) >> 4 : 0;
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ds.y_bytes);
+  // raw bits of this lane's pixel of frame t (zero past the clip's real frames)
+  auto load = [&](int t) {
+    const bool real = t < ds.T;
+    return load_raw_at<T>(xr, real ? xin : kOutOfRange, real ? t * pa.frame_bytes : 0);
+  };
+  // evaluate the frame held in slot u: every live output takes its tap, the
+  // oldest completes (STEADY: all KT outputs exist and have started)
+  auto eval = [&](int t, int u, bool steady) {
+    float xv[NS];
 #pragma unroll
-    for (int l = 0; l < kDwpLoads; ++l) {
-      const int u = l * 64 + lane;
-      const int off = a0 + u * 16;
-      if (!wlive || u >= nunits) {
-        rb[l] = make_uint4(0u, 0u, 0u, 0u);
-      } else if (off + 16 <= ds.x_bytes) {
-        const auto v4 = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
-        rb[l] = make_uint4(v4[0], v4[1], v4[2], v4[3]);
+    for (int e = 0; e < NS; ++e) xv[e] = rp[e][u * kDwpSlot];
+    const int v = ds.v0 + t;
+#pragma unroll
+    for (int j = KT - 1; j >= 0; --j) {
+      const int q = KT - 1 - j;
+      const int tau = v - j;
+      const int first = steady ? 0 : (tau >= g.pT ? 0 : g.pT - tau);
+      float a = (j == first) ? 0.f : acc[q];
+#pragma unroll
+      for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
+      if (j == KT - 1) {
+        const bool exists = steady || tau >= 0;
+        store_at(yr, exists ? yo : kOutOfRange, exists ? (ds.k0 + t) * So * int(esz) : 0,
+                 from_f32<T>(a + bo));
       } else {
-        // the unit that runs past the end of the clip: 2-byte reads, each
-        // inside the buffer or at the out-of-range offset
-        uint32_t h[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          h[e] = __builtin_amdgcn_raw_buffer_load_b16(
-              xr, off + 2 * e + 2 <= ds.x_bytes ? off + 2 * e : kOutOfRange, 0, 0);
-        rb[l] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                           h[6] | (h[7] << 16));
+        acc[q] = a;
       }
     }
+#pragma unroll
+    for (int q = 0; q + 1 < KT; ++q) acc[q] = acc[q + 1];
   };
-  auto stash = [&](int buf, const uint4 (&rb)[kDwpLoads]) {
+  // groups of U frames: the group's pixels go to slots 0..U-1, the next
+  // group's loads are issued, then the group is evaluated; a group is steady
+  // once its first frame is (then so are the rest)
+  uint32_t xa[U];
 #pragma unroll
-    for (int l = 0; l < kDwpLoads; ++l) lds[wave][buf][l * 64 + lane] = rb[l];
-  };
-
-  T* yb = y + int64_t(bc) * y_bc + p;
-  uint4 rb[kDwpLoads];
-  fetch(0, rb);
-  stash(0, rb);
-  if (pa.nblk > 1) fetch(1, rb);
-  __syncthreads();
-  for (int k = 0; k < pa.nblk; ++k) {
-    const int buf = k & 1;
-    const int t0 = k * pa.F;
-    const int shift = ((plane0 + t0 * pa.frame_bytes) & 15) / int(esz);  // elements
-    const T* fr = reinterpret_cast<const T*>(&lds[wave][buf][0]) + shift;
-    for (int f = 0; f < pa.F; ++f) {
-      const int t = t0 + f;
-      if (t >= ds.count) break;  // uniform
-      const bool real = t < ds.T;
-      float xv[NS];
+  for (int u = 0; u < U; ++u) xa[u] = load(u);
+  int t = 0;
+  for (; t + U <= ds.count; t += U) {
+    lds_order();
 #pragma unroll
-      for (int e = 0; e < NS; ++e)
-        xv[e] = (real && soff[e] >= 0) ? to_f32<T>(fr[f * (pa.frame_bytes / int(esz)) + soff[e]])
-                                       : 0.f;
-      const int v = ds.v0 + t;
+    for (int u = 0; u < U; ++u) wp[u * kDwpSlot] = raw_to_f32<T>(xa[u]);
+    lds_order();
 #pragma unroll
-      for (int j = KT - 1; j >= 0; --j) {
-        const int q = KT - 1 - j;
-        const int tau = v - j;
-        const bool exists = tau >= 0;  // as above: only the store is guarded
-        const int first = tau >= g.pT ? 0 : g.pT - tau;
-        float a = (j == first) ? 0.f : acc[q];
+    for (int u = 0; u < U; ++u) xa[u] = load(t + U + u);
+    if (ds.v0 + t - (KT - 1) >= g.pT) {
 #pragma unroll
-        for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
-        if (j == KT - 1) {
-          if (pl && exists) yb[int64_t(ds.k0 + t) * So] = from_f32<T>(a + bo);
-        } else {
-          acc[q] = a;
-        }
-      }
+      for (int u = 0; u < U; ++u) eval(t + u, u, true);
+    } else {
 #pragma unroll
-      for (int q = 0; q + 1 < KT; ++q) acc[q] = acc[q + 1];
+      for (int u = 0; u < U; ++u) eval(t + u, u, false);
     }
-    if (k + 1 < pa.nblk) {
-      // block k + 1 into the buffer block k - 1 used (every wave left it at
-      // the last barrier), then block k + 2 into registers
-      stash(buf ^ 1, rb);
-      if (k + 2 < pa.nblk) fetch(k + 2, rb);
-    }
-    __syncthreads();
   }
+  // ragged tail: its frames are already in registers
+  lds_order();
+#pragma unroll
+  for (int u = 0; u < U; ++u) wp[u * kDwpSlot] = raw_to_f32<T>(xa[u]);
+  lds_order();
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    if (t + u >= ds.count) break;
+    eval(t + u, u, false);
+  }
+
   if (ds.update && pl) {
     const int v1 = ds.v0 + ds.count;
 #pragma unroll
     for (int q = 0; q + 1 < KT; ++q) {
       const int tau = v1 - (KT - 1) + q;
-      const int sl = (ds.slot0 + ds.count + q) % KT;
-      if (tau >= 0) ring[sl * ring_slot + ridx] = acc[q];
+      const int slq = (ds.slot0 + ds.count + q) % KT;
+      if (tau >= 0) ring[slq * ring_slot + ridx] = acc[q];
     }
   }
+}
+
+// The small-plane kernel's conditions: one lane per input and per output
+// pixel, the padded tile and its sink cell within a slot.
+bool dwp_fits(const ConvGeom& g) {
+  return g.S() <= 64 && g.So() <= 64 &&
+         int64_t(g.H + 2 * g.pH) * (g.W + 2 * g.pW) + 1 <= kDwpSlot;
 }
 
 template <typename T, int KH, int KW, int KT>
@@ -457,11 +462,11 @@ hipError_t dw_steps_launch(const ConvGeom& g, const ConvLayout& L, char* state, 
   ds.fd_So = make_fastdiv(uint32_t(g.So()));
   ds.fd_Cout = make_fastdiv(uint32_t(g.Cout));
   ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
+  ds.fd_W = make_fastdiv(uint32_t(g.W));
   const int64_t fbytes = g.S() * esz;
-  if (g.So() <= 64 && fbytes + 31 <= 16 * kDwpUnits) {
+  if (dwp_fits(g)) {
     DwpArgs pa;
-    pa.F = int32_t(std::min<int64_t>(16, (16 * kDwpUnits - 31) / fbytes));
-    pa.nblk = int32_t((int64_t(count) + pa.F - 1) / pa.F);
+    pa.PW = g.W + 2 * g.pW;
     pa.frame_bytes = int32_t(fbytes);
     const int64_t planes = int64_t(g.B) * g.Cout;
     hipLaunchKernelGGL((conv_steps_dwp_kernel<T, KH, KW, KT>),

@@ -355,6 +355,216 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
   }
 }
 
+// Global spatial pooling (the window covers the whole frame: kH = H, kW = W,
+// no spatial padding or dilation, one output per plane and frame), as in a
+// network head.  Lanes hold frames instead of window positions: one wave per
+// (stream, channel) plane stages a block of kPgFrames of its frames -- they
+// lie contiguously in the clip -- into LDS with 16-byte loads (the next
+// block's loads in flight while a block is reduced), and lane t reduces
+// frame t of the block alone, in the order of the per-step kernel's shuffle
+// tree over 64 window lanes (element r in leaf r, the rest neutral), so both
+// paths give the same bits.  The window's frames then come from the lanes
+// below (from the previous block, or the FIFO, across the block's start) and
+// combine in that kernel's temporal tree.  The per-step kernel spends a
+// shuffle tree, a temporal tree and a division on each frame for one value;
+// here each costs one lane.
+constexpr int kPgFrames = 32;  // frames per block, lanes 0..31
+
+struct PoolGlobalArgs {
+  int32_t nblk;       // blocks of the call: ceil(count / kPgFrames)
+  int32_t lds_bytes;  // per wave: a block, its alignment and 64 elements of over-read
+};
+
+// Value of `cur` in lane (lane - k) of this block, or of `prev` in the
+// previous block's lane kPgFrames + lane - k.
+__device__ __forceinline__ float lane_back(float cur, float prev, int lane, int k) {
+  const float a = __int_as_float(__builtin_amdgcn_ds_bpermute(((lane - k) & 63) << 2,
+                                                              __float_as_int(cur)));
+  const float b = __int_as_float(__builtin_amdgcn_ds_bpermute(
+      ((kPgFrames + lane - k) & 63) << 2, __float_as_int(prev)));
+  return lane >= k ? a : b;
+}
+
+template <typename T, int KT, bool IS_MAX>
+__global__ __launch_bounds__(64) void pool_steps_global_kernel(
+    PoolGeom g, PoolSteps ps, PoolGlobalArgs pa, const T* __restrict__ x, int64_t x_bc,
+    T* __restrict__ y, int64_t y_bc, float* __restrict__ fifo, int64_t fifo_slot,
+    const float* __restrict__ valid) {
+  extern __shared__ uint4 pg_lds[];
+  constexpr uint32_t esz = sizeof(T);
+  constexpr int NU = esz == 2 ? 5 : 9;  // 16-byte units per lane and block
+  constexpr bool is_max = IS_MAX;
+  const float neutral = is_max ? -INFINITY : 0.f;
+  const int lane = int(threadIdx.x);
+  const int bc = int(blockIdx.x);  // one wave per plane
+  const int S = g.H * g.W;
+  const int plane = int(uint32_t(bc) * uint32_t(x_bc) * esz);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ps.x_bytes);
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ps.y_bytes);
+  const int yplane = int(uint32_t(bc) * uint32_t(y_bc) * esz);
+
+  // the previous block's reduced frames and validity by lane; before the
+  // first block, lanes kPgFrames - (KT - 1) + q hold the FIFO's frame
+  // n0 - (KT - 1) + q
+  float prev = neutral, prevok = 0.f;
+  {
+    const int q = lane - (kPgFrames - (KT - 1));
+    const int64_t rf = ps.n0 - (KT - 1) + q;
+    if (q >= 0 && lane < kPgFrames && rf >= 0) {
+      prev = fifo[(rf % KT) * fifo_slot + bc];
+      prevok = valid[rf % KT];
+    }
+  }
+
+  // block b's real frames from the 16-byte boundary at or below their first
+  // byte; units past them read the out-of-range offset, and the one unit
+  // that runs past the clip's end is read element by element
+  struct Block {
+    int s0, a0, units;
+  };
+  auto block = [&](int b) {
+    Block k;
+    const int t0 = b * kPgFrames;
+    const int nr = min(max(ps.T - t0, 0), kPgFrames);
+    k.s0 = plane + t0 * ps.fstride;
+    k.a0 = k.s0 & ~15;
+    k.units = nr > 0 ? (k.s0 + nr * ps.fstride - k.a0 + 15) >> 4 : 0;
+    return k;
+  };
+  auto fetch = [&](const Block& k, uint4 (&v)[NU]) {
+#pragma unroll
+    for (int j = 0; j < NU; ++j) {
+      const int u = j * 64 + lane;
+      const int off = k.a0 + u * 16;
+      const bool whole = u < k.units && off + 16 <= ps.x_bytes;
+      const auto v4 = __builtin_amdgcn_raw_buffer_load_b128(xr, whole ? off : kOutOfRange, 0, 0);
+      v[j] = make_uint4(v4[0], v4[1], v4[2], v4[3]);
+      if (u < k.units && off + 16 > ps.x_bytes) {
+        uint32_t h[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if constexpr (esz == 2) {
+            const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(
+                xr, off + 4 * e + 2 <= ps.x_bytes ? off + 4 * e : kOutOfRange, 0, 0);
+            const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(
+                xr, off + 4 * e + 4 <= ps.x_bytes ? off + 4 * e + 2 : kOutOfRange, 0, 0);
+            h[e] = lo | (hi << 16);
+          } else {
+            h[e] = __builtin_amdgcn_raw_buffer_load_b32(
+                xr, off + 4 * e + 4 <= ps.x_bytes ? off + 4 * e : kOutOfRange, 0, 0);
+          }
+        }
+        v[j] = make_uint4(h[0], h[1], h[2], h[3]);
+      }
+    }
+  };
+
+  uint4 v[NU];
+  Block cb = block(0);
+  fetch(cb, v);
+  for (int b = 0; b < pa.nblk; ++b) {
+#pragma unroll
+    for (int j = 0; j < NU; ++j)
+      if (j * 64 + lane < cb.units) pg_lds[j * 64 + lane] = v[j];
+    __syncthreads();  // (one wave: its LDS writes land before the reads)
+    const int shift = cb.s0 - cb.a0;
+    if (b + 1 < pa.nblk) {
+      cb = block(b + 1);
+      fetch(cb, v);
+    }
+
+    // lane t: frame t0 + t, its S elements in leaves 0..S-1.  The leaf
+    // masks are built from a vector copy of S made here, in the loop: as
+    // loop invariants the compiler would hoist all 64 of them, as scalar
+    // lane masks, out of the loop and spill them
+    int Sv;
+    __asm__ volatile("v_mov_b32 %0, %1" : "=v"(Sv) : "s"(S));
+    const uint32_t nb = __float_as_uint(neutral);
+    const int t = b * kPgFrames + lane;
+    const bool live = lane < kPgFrames;
+    const char* fb =
+        reinterpret_cast<const char*>(pg_lds) + shift + (live ? lane : 0) * ps.fstride;
+    auto leaf = [&](int r) {
+      float xv;
+      if constexpr (esz == 2)
+        xv = __uint_as_float(uint32_t(*reinterpret_cast<const uint16_t*>(fb + 2 * r)) << 16);
+      else
+        xv = *reinterpret_cast<const float*>(fb + 4 * r);
+      // as the per-step kernel: the neutral value, combined with the element
+      const float lv = is_max ? fmaxf(neutral, xv) : neutral + xv;
+      const uint32_t keep = uint32_t((r - Sv) >> 31);  // all ones when r < S
+      return __uint_as_float((__float_as_uint(lv) & keep) | (nb & ~keep));
+    };
+    auto comb = [&](float a, float c) { return is_max ? fmaxf(a, c) : a + c; };
+    float tr[32];
+#pragma unroll
+    for (int l = 0; l < 32; ++l) tr[l] = comb(leaf(l), leaf(l + 32));
+#pragma unroll
+    for (int m = 16; m > 0; m >>= 1)
+#pragma unroll
+      for (int l = 0; l < m; ++l) tr[l] = comb(tr[l], tr[l + m]);
+    const bool real = live && t < ps.T;
+    const float cur = real ? tr[0] : neutral;
+    const float curok = real ? 1.f : 0.f;
+    __syncthreads();  // the reads are done before the next block's writes
+
+    // the window of step n = n0 + t: frames n - (KT - 1) + q, q = 0..KT-1
+    const int64_t n = ps.n0 + t;
+    float fv[KT], fok[KT];
+    fv[KT - 1] = cur;
+    fok[KT - 1] = curok;
+#pragma unroll
+    for (int q = 0; q + 1 < KT; ++q) {
+      fv[q] = lane_back(cur, prev, lane, KT - 1 - q);
+      fok[q] = lane_back(curok, prevok, lane, KT - 1 - q);
+    }
+    float tv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const bool in = q < KT && n - (KT - 1) + q >= 0;
+      tv[q] = in ? fv[q < KT ? q : 0] : neutral;
+    }
+#pragma unroll
+    for (int m = 4; m > 0; m >>= 1) {
+      float nv[8];
+#pragma unroll
+      for (int l = 0; l < 8; ++l) nv[l] = is_max ? fmaxf(tv[l], tv[l ^ m]) : tv[l] + tv[l ^ m];
+#pragma unroll
+      for (int l = 0; l < 8; ++l) tv[l] = nv[l];
+    }
+    float out = tv[0];
+    if (!is_max) {
+      float div = float(KT * S);
+      if (!g.count_include_pad) {
+        float tc[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const bool in = q < KT && n - (KT - 1) + q >= 0;
+          tc[q] = in ? fok[q < KT ? q : 0] : 0.f;
+        }
+#pragma unroll
+        for (int m = 4; m > 0; m >>= 1) {
+          float nc[8];
+#pragma unroll
+          for (int l = 0; l < 8; ++l) nc[l] = tc[l] + tc[l ^ m];
+#pragma unroll
+          for (int l = 0; l < 8; ++l) tc[l] = nc[l];
+        }
+        div = tc[0] * float(S);
+      }
+      out = div > 0.f ? out / div : 0.f;
+    }
+    const bool emits = live && t < ps.count && n >= g.d;
+    store_at(yr, emits ? yplane : kOutOfRange, emits ? int((n - ps.emit0) * int64_t(esz)) : 0,
+             from_f32<T>(out));
+    // the call's last KT - 1 frames go to their FIFO slots
+    if (ps.update && live && t < ps.count && t >= ps.count - (KT - 1))
+      fifo[(n % KT) * fifo_slot + bc] = cur;
+    prev = cur;
+    prevok = curok;
+  }
+}
+
 // Validity flags of the FIFO slots the call's frames went to (one thread).
 __global__ void pool_valid_kernel(float* valid, int32_t R, int64_t n0, int32_t count, int32_t T) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
@@ -424,10 +634,18 @@ hipError_t launch_pool_clip(const PoolGeom& g, int32_t T, int32_t T_out, const v
 
 namespace {
 
+template <typename T, int KT>
+hipError_t pool_global_launch(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                              int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                              int64_t n0, bool update, hipStream_t s);
+bool pool_global_fits(const PoolGeom& g);
+
 template <typename T, int G, int KT>
 hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
                              int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
                              int64_t n0, bool update, hipStream_t s) {
+  if (pool_global_fits(g))
+    return pool_global_launch<T, KT>(g, L, state, x, x_bc, nreal, count, y, y_bc, n0, update, s);
   PoolSteps ps;
   ps.n0 = n0;
   ps.count = count;
@@ -447,6 +665,46 @@ hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state
                                      : pool_steps_kernel<T, G, KT, false>;
   hipLaunchKernelGGL(kern, dim3(grid_for(g.out_frame_elems() * G)), dim3(kBlock), 0, s, g, ps,
                      static_cast<const T*>(x), x_bc, static_cast<T*>(y), y_bc, fifo,
+                     L.fifo_slot_elems, valid);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !update) return e;
+  hipLaunchKernelGGL(pool_valid_kernel, dim3(1), dim3(64), 0, s, valid, g.R, n0, count, nreal);
+  return hipGetLastError();
+}
+
+// Global spatial pooling over small frames with the per-step kernel's
+// 64-lane window groups (16 < H*W <= 64): the frames-in-lanes kernel.
+bool pool_global_fits(const PoolGeom& g) {
+  const int kHW = g.kH * g.kW;
+  return g.kH == g.H && g.kW == g.W && g.pH == 0 && g.pW == 0 && g.dH == 1 && g.dW == 1 &&
+         g.Ho == 1 && g.Wo == 1 && kHW > 16 && kHW <= 64;
+}
+
+template <typename T, int KT>
+hipError_t pool_global_launch(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
+                              int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
+                              int64_t n0, bool update, hipStream_t s) {
+  PoolSteps ps;
+  ps.n0 = n0;
+  ps.count = count;
+  ps.T = nreal;
+  ps.emit0 = n0 > g.d ? n0 : g.d;
+  ps.update = update ? 1 : 0;
+  const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
+  ps.x_bytes = int32_t(((int64_t(g.B) * g.C - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
+  ps.y_bytes = int32_t(int64_t(g.B) * g.C * y_bc * esz);
+  ps.fstride = int32_t(g.S() * esz);
+  PoolGlobalArgs pa;
+  pa.nblk = int32_t((int64_t(count) + kPgFrames - 1) / kPgFrames);
+  // the block, its alignment shift and the 64-element over-read of the last lane
+  pa.lds_bytes = int32_t(((kPgFrames * g.S() + 64) * esz + 16 + 15) / 16 * 16);
+  if (pa.lds_bytes > 64 * 16 * (esz == 2 ? 5 : 9)) return hipErrorInvalidValue;  // NU units
+  float* fifo = reinterpret_cast<float*>(state + L.fifo);
+  float* valid = reinterpret_cast<float*>(state + L.valid);
+  auto kern = g.kind == CO_POOL_MAX ? pool_steps_global_kernel<T, KT, true>
+                                     : pool_steps_global_kernel<T, KT, false>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(int64_t(g.B) * g.C)), dim3(64), pa.lds_bytes, s, g, ps,
+                     pa, static_cast<const T*>(x), x_bc, static_cast<T*>(y), y_bc, fifo,
                      L.fifo_slot_elems, valid);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !update) return e;

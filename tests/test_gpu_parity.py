@@ -478,6 +478,10 @@ DW_STEPS_CASES = [
     (1, 33, 5, (3, 3), (9, 4), (2, 1, 1), "f32"),     # ragged, kT = 5
     (1, 3, 3, (3, 3), (5, 5), (1, 1, 1), "bf16"),     # clip bytes not a multiple of 16
     (2, 8, 3, (3, 3), (10, 9), (1, 1, 1), "bf16"),    # 90 output pixels: thread per output
+    (2, 10, 3, (3, 3), (8, 8), (1, 1, 1), "bf16", (2, 2), (1, 1)),  # spatial stride 2
+    (2, 7, 3, (3, 3), (7, 7), (0, 2, 2), "f32", (1, 1), (2, 2)),    # dilation 2: 11 x 11 tile
+    (2, 6, 2, (3, 3), (8, 8), (0, 2, 2), "bf16", (1, 1), (2, 2)),   # 12 x 12 tile: thread per output
+    (1, 5, 3, (3, 3), (6, 6), (2, 1, 1), "bf16", (1, 2), (1, 1)),   # stride in one axis only
 ]
 
 
@@ -488,20 +492,23 @@ def test_depthwise_forward_steps_persistent(case):
     bitwise against the per-frame step kernel (same arithmetic order), also
     when a clip continues a state left by single steps, after clean_state
     (stale ring contents) and with update_state=False."""
-    B, C, kT, ks, size, p, dt = case
+    B, C, kT, ks, size, p, dt = case[:7]
+    st = (1,) + (case[7] if len(case) > 7 else (1, 1))
+    dil = (1,) + (case[8] if len(case) > 8 else (1, 1))
     say("depthwise steps", case)
     spec = synth.ConvSpec(batch=B, in_channels=C, out_channels=C, kernel=(kT,) + ks, in_size=size,
-                          padding=p, groups=C, dtype=dt)
+                          stride=st, padding=p, dilation=dil, groups=C, dtype=dt)
     x, w, b = synth.conv_inputs(spec, 14, 91000 + 13 * C + kT, "kaiming")
     tdt = synth.torch_dtype(dt)
     xd = x.to(DEV)
 
     def make():
-        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=p, groups=C)
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=st, padding=p,
+                            dilation=dil, groups=C)
 
     co = make()
-    assert co.algo == "depthwise"
-    ref = oracle_conv(w, b, (1, 1, 1), p, (1, 1, 1), C)
+    assert co.algo == "depthwise" and co.steps_fused(x.shape[2])
+    ref = oracle_conv(w, b, st, p, dil, C)
     ys = co.forward_steps(xd, pad_end=True)
     rp = ref.forward_steps(np64(x), pad_end=True)
     assert_close(np64(ys), rp, tdt, "persistent depthwise steps", terms=conv_terms(w))
@@ -708,18 +715,26 @@ POOL_STEPS_CASES = [
     ("avg", (3, 3, 2), (7, 6), (1, 2, 1), (1, 1, 0), False, "f32"),
     ("max", (5, 3, 3), (6, 5), (1, 1, 1), (2, 1, 1), True, "f32"),
     ("max", (1, 2, 2), (4, 4), (1, 2, 2), (0, 0, 0), True, "bf16"),
+    # global spatial pools (frames in lanes), clips over several 32-frame blocks
+    ("avg", (4, 7, 7), (7, 7), (1, 7, 7), (0, 0, 0), False, "bf16", 75),
+    ("max", (3, 6, 6), (6, 6), (1, 1, 1), (1, 0, 0), True, "f32", 40),
+    ("avg", (2, 5, 5), (5, 5), (1, 5, 5), (0, 0, 0), True, "bf16", 33),
+    ("avg", (5, 8, 8), (8, 8), (1, 1, 1), (2, 0, 0), False, "f32", 70),
+    ("max", (4, 7, 7), (7, 7), (1, 7, 7), (0, 0, 0), True, "bf16", 64),
 ]
 
 
-@pytest.mark.parametrize("case", POOL_STEPS_CASES, ids=lambda c: "poolsteps_" + c[0] + str(c[1][0]))
+@pytest.mark.parametrize("case", POOL_STEPS_CASES, ids=lambda c: "poolsteps_" + c[0] + str(c[1][0]) + (
+    f"_T{c[7]}" if len(c) > 7 else ""))
 def test_pool_forward_steps_persistent(case):
     """Pool forward_steps as one persistent launch against the oracle (end
     padding), bitwise against per-frame steps, continuing a state left by
     single steps, and with update_state=False."""
-    kind, ks, size, ss, ps, cip, dt = case
+    kind, ks, size, ss, ps, cip, dt = case[:7]
+    T = case[7] if len(case) > 7 else 12
     say("pool steps", case)
     tdt = synth.torch_dtype(dt)
-    x = synth.normal((3, 6, 12) + size, 7700 + ks[0], dtype=dt)
+    x = synth.normal((3, 6, T) + size, 7700 + ks[0] + T, dtype=dt)
     xd = x.to(DEV)
 
     def make():
