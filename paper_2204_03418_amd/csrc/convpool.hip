@@ -461,25 +461,27 @@ hipError_t cp_dispatch(const ConvGeom& g, const ConvLayout& L, char* cstate, con
 }
 
 // A clip of `count` frames in one launch (temporal stride and dilation 1 in
-// both modules).  One wave per (stream, channel) plane, as in the step kernel
-// above, for the whole clip: the convolution's kT - 1 partial sums and the
-// pool's last kT reduced frames stay in registers, so only the clip, the
-// pooled outputs and the two states move through memory.
+// both modules).  One wave per (stream, channel) plane for the whole clip,
+// one lane per input and per output pixel: the convolution's kT - 1 partial
+// sums stay in registers, so only the clip, the pooled outputs and the two
+// states move through memory.
 //
-// The plane's frames are staged through LDS in blocks of kCpsF frames,
-// widened to fp32 once and laid out as a zero-haloed padded plane with the
-// block's frames of one position side by side: a stencil tap is then one
-// 8-byte LDS read per two frames at an address fixed for the lane, with no
-// bounds test and no conversion per use.  Block k + 1 is written to the
-// other buffer while block k is evaluated, and block k + 2 is already in
-// registers.  Arithmetic per frame is the step kernels': the same
-// multiply-add chain per tap, the same rounding of the output, the same lane
-// tree for the spatial window and the pool step's tap tree for the temporal
-// one, so a clip gives the bits of stepping frame by frame.
-constexpr int kCpsWaves = 1;  // planes per workgroup (as above)
-constexpr int kCpsF = 8;           // frames per staged block
-constexpr int kCpsG = 2;           // frames per LDS read of a tap
-constexpr int kCpsMaxPadded = 128;  // padded plane, elements
+// Convolution: each frame is written, as float, into a zero-haloed tile of
+// LDS, so a stencil tap is one LDS read at a lane address fixed for the clip
+// plus a compile-time slot offset; the channel's weights are wave-uniform;
+// frames go in groups of U, the next group's pixels in flight while a group
+// is evaluated (the depthwise forward_steps kernel's scheme).  Pool: lane p
+// turns its completed, rounded output into window leaf p as the pool step
+// kernel does (the neutral value combined with the element; lanes past the
+// plane hold the neutral value) and writes it to the frame's row of 64 leaves
+// in LDS.  Every NB frames the lanes switch to frames: lane r reduces row r
+// in the pool step kernel's shuffle-tree order, takes the window's frames
+// from the lanes below (the previous block's, or the FIFO's, across the
+// block's start) and combines them in that kernel's temporal tree.  So a clip
+// gives the bits of stepping frame by frame, and the spatial tree, temporal
+// tree and division cost one lane per frame, not a wave.
+constexpr int kCpsSlot = 128;       // floats per frame slot: padded tile + sink cell
+constexpr int kCpsMaxPadded = 128;  // padded plane, elements (the bottleneck kernel's bound)
 
 struct CpSteps {
   int32_t v0;       // virtual time of the first frame: n0 + pT (clamped)
@@ -488,39 +490,60 @@ struct CpSteps {
   int32_t update;
   int32_t x_bytes;  // bytes of the clip reachable from x
   int32_t fstride;  // bytes between consecutive frames of a plane
-  int32_t Hp, Wp;   // padded input plane
-  int32_t nblk;     // staged blocks: ceil(count / kCpsF)
+  int32_t PW;       // padded tile width: W + 2 pW
   int32_t tfirst;   // first frame of the call whose convolution step emits
   int64_t n0p;      // pool steps before the call
   int64_t emit0p;   // first pool step of the call that emits: max(n0p, pool delay)
   FastDiv fd_Cout, fd_Wo, fd_W;
 };
 
+__device__ __forceinline__ void cps_lds_order() { __asm__ volatile("" ::: "memory"); }
+
 template <typename T, int KH, int KW, int KT, int PKT, bool IS_MAX>
-__global__ __launch_bounds__(64 * kCpsWaves) void convpool_steps_kernel(
+__global__ __launch_bounds__(64) void convpool_steps_kernel(
     ConvGeom g, CpSteps cs, const T* __restrict__ x, int64_t x_bc, const float* __restrict__ w,
     const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot, PoolGeom pg,
     T* __restrict__ z, int64_t z_bc, float* __restrict__ fifo, int64_t fifo_slot,
     const float* __restrict__ valid) {
   constexpr int NS = KH * KW;
-  constexpr int F = kCpsF;
+  constexpr int U = KT * ((4 + KT - 1) / KT);  // frames per group (acc names cycle)
   constexpr uint32_t esz = sizeof(T);
-  extern __shared__ float cps_lds[];  // [wave][buffer][padded position][frame]
-  const int lane = int(threadIdx.x) & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
-  const int BC = g.B * g.Cout;
-  const int bc_raw = int(blockIdx.x) * kCpsWaves + wave;
-  const bool wlive = bc_raw < BC;  // whole waves; idle ones still meet the barriers
-  const int bc = wlive ? bc_raw : 0;
-  const int So = g.Ho * g.Wo;
-  const bool pl = wlive && lane < So;
-  const int p = lane < So ? lane : 0;
+  // frames per pool block: whole groups, about 2.3 KB of leaf rows
+  constexpr int NB = U * ((2304 / (64 * int(esz))) / U > 0 ? (2304 / (64 * int(esz))) / U : 1);
+  static_assert(NB <= 64, "one lane per row");
+  constexpr bool is_max = IS_MAX;
+  __shared__ float slot[U][kCpsSlot];
+  constexpr int RS = 64 + 16 / int(esz);  // row stride: rows 16 bytes apart in bank order
+  __shared__ T rows[NB][RS];
+  const float neutral = is_max ? -INFINITY : 0.f;
+  const int lane = int(threadIdx.x);
+  const int bc = int(blockIdx.x);  // one wave per plane
+  const int S = g.H * g.W, So = g.Ho * g.Wo;
   const int bq = fdiv(bc, cs.fd_Cout), c = bc - bq * g.Cout;
+
+  for (int e = lane; e < U * kCpsSlot; e += 64) (&slot[0][0])[e] = 0.f;  // halos stay zero
+
+  // input lane: pixel `lane` of the frame into its padded cell (lanes past
+  // the frame load zero into the sink cell after the tile)
+  int wpos = kCpsSlot - 1;
+  if (lane < S) {
+    const int hp = fdiv(lane, cs.fd_W);
+    wpos = (hp + g.pH) * cs.PW + (lane - hp * g.W) + g.pW;
+  }
+  float* const wp = &slot[0][wpos];  // + u * kCpsSlot: slot u
+  const int xin = lane < S ? int((uint32_t(bc) * uint32_t(x_bc) + uint32_t(lane)) * esz)
+                           : kOutOfRange;
+  // output lane: its stencil cells in the padded tile
+  const bool pl = lane < So;
+  const int p = pl ? lane : 0;
   const int i = fdiv(p, cs.fd_Wo), jo = p - i * g.Wo;
+  const float* rp[NS];  // + u * kCpsSlot: slot u
+#pragma unroll
+  for (int u = 0; u < KH; ++u)
+#pragma unroll
+    for (int v = 0; v < KW; ++v)
+      rp[u * KW + v] = &slot[0][(i * g.sH + u * g.dH) * cs.PW + jo * g.sW + v * g.dW];
   const int ridx = (c * g.B + bq) * So + p;
-  const int buf_elems = cs.Hp * cs.Wp * F;
-  float* wl = cps_lds + wave * 2 * buf_elems;
-  for (int e = lane; e < 2 * buf_elems; e += 64) wl[e] = 0.f;  // the halo stays zero
 
   float wr[KT][NS];
 #pragma unroll
@@ -532,180 +555,164 @@ __global__ __launch_bounds__(64 * kCpsWaves) void convpool_steps_kernel(
 #pragma unroll
   for (int q = 0; q < KT; ++q) {
     const int tau = cs.v0 - (KT - 1) + q;
-    const int sl = (cs.slot0 + q) % KT;
-    acc[q] = (pl && q < KT - 1 && tau >= 0) ? ring[sl * ring_slot + ridx] : 0.f;
+    const int slq = (cs.slot0 + q) % KT;
+    acc[q] = (pl && q < KT - 1 && tau >= 0) ? ring[slq * ring_slot + ridx] : 0.f;
   }
-  // stencil taps: padded positions of this lane's output pixel, times F
-  int toff[NS];
-#pragma unroll
-  for (int u = 0; u < KH; ++u)
-#pragma unroll
-    for (int v = 0; v < KW; ++v)
-      toff[u * KW + v] = ((i * g.sH + u * g.dH) * cs.Wp + (jo * g.sW + v * g.dW)) * F;
 
-  // pool: reduced value and validity of pool frame m - (PKT - 1) + q before
-  // the pool's step m; frames before the stream began are start padding
-  constexpr bool is_max = IS_MAX;  // (compile-time: no select per operation)
-  const float neutral = is_max ? -INFINITY : 0.f;
-  const int kHW = pg.kH * pg.kW;
-  float fv[PKT], fok[PKT];
-#pragma unroll
-  for (int q = 0; q + 1 < PKT; ++q) {
+  // pool: the previous block's reduced frames and validity by lane; before
+  // the first block, lanes NB - (PKT - 1) + q hold the FIFO's pool frame
+  // n0p - (PKT - 1) + q (frames before the stream began are start padding)
+  float prev = neutral, prevok = 0.f;
+  {
+    const int q = lane - (NB - (PKT - 1));
     const int64_t rf = cs.n0p - (PKT - 1) + q;
-    const bool have = wlive && rf >= 0;
-    fv[q] = have ? fifo[(rf % PKT) * fifo_slot + bc] : neutral;
-    fok[q] = have ? valid[rf % PKT] : 0.f;
+    if (q >= 0 && lane < NB && rf >= 0) {
+      prev = fifo[(rf % PKT) * fifo_slot + bc];
+      prevok = valid[rf % PKT];
+    }
   }
 
-  // staging: lane e holds input element e of the plane (H * W <= 64)
-  const int h_in = fdiv(lane, cs.fd_W), w_in = lane - h_in * g.W;
-  const int spos = (wlive && lane < g.H * g.W) ? ((h_in + g.pH) * cs.Wp + w_in + g.pW) * F : -1;
-  const int sbyte = int((uint32_t(bc) * uint32_t(x_bc) + uint32_t(lane)) * esz);
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, cs.x_bytes);
-  uint32_t raw[F];
-  auto fetch = [&](int blk) {
-#pragma unroll
-    for (int f = 0; f < F; ++f) {
-      const int t = blk * F + f;
-      raw[f] = 0u;
-      if (spos >= 0 && t < cs.count) raw[f] = load_raw_at<T>(xr, sbyte, t * cs.fstride);
-    }
+  auto load = [&](int t) {
+    const bool real = t < cs.count;
+    return load_raw_at<T>(xr, real ? xin : kOutOfRange, real ? t * cs.fstride : 0);
   };
-  auto stash = [&](int buf) {
-    if (spos < 0) return;
-    float4* dst = reinterpret_cast<float4*>(wl + buf * buf_elems + spos);
+  // evaluate the frame in slot u (row r of the pool block): every live
+  // output takes its tap, the oldest completes and becomes this lane's leaf
+  auto eval = [&](int t, int u, T* row, bool steady) {
+    float xv[NS];
 #pragma unroll
-    for (int f4 = 0; f4 < F / 4; ++f4)
-      dst[f4] = make_float4(raw_to_f32<T>(raw[4 * f4]), raw_to_f32<T>(raw[4 * f4 + 1]),
-                            raw_to_f32<T>(raw[4 * f4 + 2]), raw_to_f32<T>(raw[4 * f4 + 3]));
-  };
-
-  __syncthreads();  // the zero fill before the first block lands
-  fetch(0);
-  stash(0);
-  if (cs.nblk > 1) fetch(1);
-  __syncthreads();
-  for (int k = 0; k < cs.nblk; ++k) {
-    const float* fb = wl + (k & 1) * buf_elems;
+    for (int e = 0; e < NS; ++e) xv[e] = rp[e][u * kCpsSlot];
+    const int v = cs.v0 + t;
 #pragma unroll
-    for (int h2 = 0; h2 < F / kCpsG; ++h2) {
-      if (k * F + kCpsG * h2 >= cs.count) break;  // uniform
-      float2 xq[NS];
+    for (int j = KT - 1; j >= 0; --j) {
+      const int q = KT - 1 - j;
+      const int tau = v - j;
+      const int first = steady ? 0 : (tau >= g.pT ? 0 : g.pT - tau);
+      float a = (j == first) ? 0.f : acc[q];
 #pragma unroll
-      for (int e = 0; e < NS; ++e)
-        xq[e] = *reinterpret_cast<const float2*>(fb + toff[e] + kCpsG * h2);
-#pragma unroll
-      for (int ff = 0; ff < kCpsG; ++ff) {
-        const int t = k * F + kCpsG * h2 + ff;
-        if (t >= cs.count) break;  // uniform
-        float xv[NS];
-#pragma unroll
-        for (int e = 0; e < NS; ++e) xv[e] = ff == 0 ? xq[e].x : xq[e].y;
-        const int v = cs.v0 + t;
-#pragma unroll
-        for (int j = KT - 1; j >= 0; --j) {
-          const int q = KT - 1 - j;
-          const int tau = v - j;
-          if (tau < 0) continue;
-          const int first = tau >= g.pT ? 0 : g.pT - tau;
-          float a = (j == first) ? 0.f : acc[q];
-#pragma unroll
-          for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
-          if (j != KT - 1) {
-            acc[q] = a;
-            continue;
-          }
-          // the convolution emits: the pool steps on the rounded frame
-          const T yv = from_f32<T>(a + bo);
-          float val = neutral;
-          if (pl) val = is_max ? fmaxf(val, to_f32<T>(yv)) : val + to_f32<T>(yv);
-#pragma unroll
-          for (int m = 32; m > 0; m >>= 1) {
-            const float o = __shfl_xor(val, m, 64);
-            val = is_max ? fmaxf(val, o) : val + o;
-          }
-          val = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(val), 0));
-          fv[PKT - 1] = val;
-          fok[PKT - 1] = 1.f;
-          const int64_t m = cs.n0p + (t - cs.tfirst);
-          if (m >= pg.d) {
-            float tv[8];
-#pragma unroll
-            for (int l = 0; l < 8; ++l) {
-              const bool in = l < PKT && m - (PKT - 1) + l >= 0;
-              tv[l] = in ? fv[l < PKT ? l : 0] : neutral;
-            }
-#pragma unroll
-            for (int mm = 4; mm > 0; mm >>= 1) {
-              float nv[8];
-#pragma unroll
-              for (int l = 0; l < 8; ++l)
-                nv[l] = is_max ? fmaxf(tv[l], tv[l ^ mm]) : tv[l] + tv[l ^ mm];
-#pragma unroll
-              for (int l = 0; l < 8; ++l) tv[l] = nv[l];
-            }
-            float out;
-            if (is_max) {
-              out = tv[0];
-            } else {
-              // the count of real frames only for an average without the pads
-              float tcount = 0.f;
-              if (!pg.count_include_pad) {
-                float tc[8];
-#pragma unroll
-                for (int l = 0; l < 8; ++l) {
-                  const bool in = l < PKT && m - (PKT - 1) + l >= 0;
-                  tc[l] = in ? fok[l < PKT ? l : 0] : 0.f;
-                }
-#pragma unroll
-                for (int mm = 4; mm > 0; mm >>= 1) {
-                  float nc[8];
-#pragma unroll
-                  for (int l = 0; l < 8; ++l) nc[l] = tc[l] + tc[l ^ mm];
-#pragma unroll
-                  for (int l = 0; l < 8; ++l) tc[l] = nc[l];
-                }
-                tcount = tc[0];
-              }
-              const float div = pg.count_include_pad ? float(PKT * kHW) : tcount * float(kHW);
-              out = div > 0.f ? tv[0] / div : 0.f;
-            }
-            if (wlive && lane == 0) z[int64_t(bc) * z_bc + (m - cs.emit0p)] = from_f32<T>(out);
-          }
-#pragma unroll
-          for (int q2 = 0; q2 + 1 < PKT; ++q2) {
-            fv[q2] = fv[q2 + 1];
-            fok[q2] = fok[q2 + 1];
-          }
-        }
-#pragma unroll
-        for (int q = 0; q + 1 < KT; ++q) acc[q] = acc[q + 1];
+      for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
+      if (j == KT - 1) {
+        const float yv = to_f32<T>(from_f32<T>(a + bo));
+        const float lf = is_max ? fmaxf(neutral, yv) : neutral + yv;
+        row[lane] = from_f32<T>(pl ? lf : neutral);
+      } else {
+        acc[q] = a;
       }
     }
-    if (k + 1 < cs.nblk) {
-      // block k + 1 into the buffer block k - 1 used (every wave left it at
-      // the last barrier), then block k + 2 into registers
-      stash((k + 1) & 1);
-      if (k + 2 < cs.nblk) fetch(k + 2);
+#pragma unroll
+    for (int q = 0; q + 1 < KT; ++q) acc[q] = acc[q + 1];
+  };
+  auto comb = [&](float a, float b2) { return is_max ? fmaxf(a, b2) : a + b2; };
+
+  uint32_t xa[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) xa[u] = load(u);
+  for (int sb0 = 0; sb0 < cs.count; sb0 += NB) {
+    // the block's frames through the convolution, in groups of U
+    for (int gi = 0; gi < NB / U; ++gi) {
+      const int t = sb0 + gi * U;
+      if (t >= cs.count) break;  // uniform
+      cps_lds_order();
+#pragma unroll
+      for (int u = 0; u < U; ++u) wp[u * kCpsSlot] = raw_to_f32<T>(xa[u]);
+      cps_lds_order();
+#pragma unroll
+      for (int u = 0; u < U; ++u) xa[u] = load(t + U + u);
+      T* row0 = &rows[gi * U][0];
+      if (t + U <= cs.count && cs.v0 + t - (KT - 1) >= g.pT) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) eval(t + u, u, row0 + u * RS, true);
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (t + u >= cs.count) break;  // (the clip's last, ragged group)
+          eval(t + u, u, row0 + u * RS, false);
+        }
+      }
     }
-    __syncthreads();
+    cps_lds_order();
+
+    // lanes = frames: lane r reduces frame sb0 + r of the block
+    const int t = sb0 + lane;
+    const bool pooled = lane < NB && t < cs.count && t >= cs.tfirst;  // the pool steps
+    const T* row = &rows[lane < NB ? lane : 0][0];
+    float tr[32];
+#pragma unroll
+    for (int l = 0; l < 32; ++l) tr[l] = comb(to_f32<T>(row[l]), to_f32<T>(row[l + 32]));
+#pragma unroll
+    for (int m = 16; m > 0; m >>= 1)
+#pragma unroll
+      for (int l = 0; l < m; ++l) tr[l] = comb(tr[l], tr[l + m]);
+    cps_lds_order();
+    const float cur = pooled ? tr[0] : neutral;
+    const float curok = pooled ? 1.f : 0.f;
+    // the window of pool step m: pool frames m - (PKT - 1) + q, q = 0..PKT-1
+    const int64_t m = cs.n0p + (t - cs.tfirst);
+    float fv[PKT], fok[PKT];
+    fv[PKT - 1] = cur;
+    fok[PKT - 1] = curok;
+#pragma unroll
+    for (int q = 0; q + 1 < PKT; ++q) {
+      const int k = PKT - 1 - q;
+      const int src = ((lane - k) & 63) << 2, psrc = ((NB + lane - k) & 63) << 2;
+      const float a1 = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(cur)));
+      const float b1 = __int_as_float(__builtin_amdgcn_ds_bpermute(psrc, __float_as_int(prev)));
+      const float a2 = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(curok)));
+      const float b2 = __int_as_float(__builtin_amdgcn_ds_bpermute(psrc, __float_as_int(prevok)));
+      fv[q] = lane >= k ? a1 : b1;
+      fok[q] = lane >= k ? a2 : b2;
+    }
+    float tv[8];
+#pragma unroll
+    for (int l = 0; l < 8; ++l) {
+      const bool in = l < PKT && m - (PKT - 1) + l >= 0;
+      tv[l] = in ? fv[l < PKT ? l : 0] : neutral;
+    }
+#pragma unroll
+    for (int mm = 4; mm > 0; mm >>= 1) {
+      float nv[8];
+#pragma unroll
+      for (int l = 0; l < 8; ++l) nv[l] = comb(tv[l], tv[l ^ mm]);
+#pragma unroll
+      for (int l = 0; l < 8; ++l) tv[l] = nv[l];
+    }
+    float out = tv[0];
+    if (!is_max) {
+      float div = float(PKT * So);
+      if (!pg.count_include_pad) {
+        float tc[8];
+#pragma unroll
+        for (int l = 0; l < 8; ++l) {
+          const bool in = l < PKT && m - (PKT - 1) + l >= 0;
+          tc[l] = in ? fok[l < PKT ? l : 0] : 0.f;
+        }
+#pragma unroll
+        for (int mm = 4; mm > 0; mm >>= 1) {
+          float nc[8];
+#pragma unroll
+          for (int l = 0; l < 8; ++l) nc[l] = tc[l] + tc[l ^ mm];
+#pragma unroll
+          for (int l = 0; l < 8; ++l) tc[l] = nc[l];
+        }
+        div = tc[0] * float(So);
+      }
+      out = div > 0.f ? out / div : 0.f;
+    }
+    if (pooled && m >= pg.d) z[int64_t(bc) * z_bc + (m - cs.emit0p)] = from_f32<T>(out);
+    // the call's last PKT - 1 pool frames go to their FIFO slots
+    if (cs.update && pooled && t >= cs.count - (PKT - 1)) fifo[(m % PKT) * fifo_slot + bc] = cur;
+    prev = cur;
+    prevok = curok;
   }
-  if (!cs.update) return;
-  if (pl) {
+
+  if (cs.update && pl) {
     const int v1 = cs.v0 + cs.count;
 #pragma unroll
     for (int q = 0; q + 1 < KT; ++q) {
       const int tau = v1 - (KT - 1) + q;
-      const int sl = (cs.slot0 + cs.count + q) % KT;
-      if (tau >= 0) ring[sl * ring_slot + ridx] = acc[q];
-    }
-  }
-  if (wlive && lane == 0) {
-    const int64_t n1p = cs.n0p + (cs.count > cs.tfirst ? cs.count - cs.tfirst : 0);
-#pragma unroll
-    for (int q = 0; q + 1 < PKT; ++q) {
-      const int64_t rf = n1p - (PKT - 1) + q;
-      if (rf >= 0) fifo[(rf % PKT) * fifo_slot + bc] = fv[q];
+      const int slq = (cs.slot0 + cs.count + q) % KT;
+      if (tau >= 0) ring[slq * ring_slot + ridx] = acc[q];
     }
   }
 }
@@ -724,9 +731,7 @@ hipError_t cps_launch(const ConvGeom& g, const ConvLayout& L, char* cstate, cons
   const int64_t x_bc = int64_t(T_in) * g.S();
   cs.x_bytes = int32_t(int64_t(g.B) * g.Cin * x_bc * esz);
   cs.fstride = int32_t(g.S() * esz);
-  cs.Hp = g.H + 2 * g.pH;
-  cs.Wp = g.W + 2 * g.pW;
-  cs.nblk = (T_in + kCpsF - 1) / kCpsF;
+  cs.PW = g.W + 2 * g.pW;
   const int64_t tf = int64_t(g.kT - 1) - v0;
   cs.tfirst = int32_t(tf > 0 ? tf : 0);
   cs.n0p = n0p;
@@ -735,12 +740,11 @@ hipError_t cps_launch(const ConvGeom& g, const ConvLayout& L, char* cstate, cons
   cs.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   cs.fd_W = make_fastdiv(uint32_t(g.W));
   const int64_t planes = int64_t(g.B) * g.Cout;
-  const size_t lds = size_t(kCpsWaves) * 2 * cs.Hp * cs.Wp * kCpsF * sizeof(float);
   float* valid = reinterpret_cast<float*>(pstate + PL.valid);
   auto kern = pg.kind == CO_POOL_MAX ? convpool_steps_kernel<T, KH, KW, KT, PKT, true>
                                       : convpool_steps_kernel<T, KH, KW, KT, PKT, false>;
-  hipLaunchKernelGGL(kern, dim3(unsigned((planes + kCpsWaves - 1) / kCpsWaves)),
-                     dim3(64 * kCpsWaves), lds, s, g, cs, static_cast<const T*>(x), x_bc,
+  hipLaunchKernelGGL(kern, dim3(unsigned(planes)), dim3(64), 0, s, g, cs,
+                     static_cast<const T*>(x), x_bc,
                      reinterpret_cast<const float*>(cstate + L.weight),
                      reinterpret_cast<const float*>(cstate + L.bias),
                      reinterpret_cast<float*>(cstate + L.ring), L.ring_slot_elems, pg,
@@ -906,7 +910,7 @@ bool convpool_steps_supported(const ConvGeom& g, const PoolGeom& pg, int64_t T) 
   const int64_t Hp = g.H + 2 * g.pH, Wp = g.W + 2 * g.pW;
   return convpool_supported(g, pg) && g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 &&
          pg.sT == 1 && pg.dT == 1 && pg.kT >= 1 && pg.kT <= 5 && pg.R == pg.kT &&
-         g.R == g.kT && Hp * Wp <= kCpsMaxPadded && int64_t(g.H) * g.W <= 64 &&
+         g.R == g.kT && Hp * Wp + 1 <= kCpsSlot && int64_t(g.H) * g.W <= 64 &&
          int64_t(g.B) * g.Cin * T * g.S() * esz < (int64_t(1) << 31);
 }
 

@@ -159,12 +159,14 @@ CONVPOOL_CASES = [
     (4, 24, (3, 3, 3), (7, 7), (0, 1, 1), "avg", 4, True, "bf16"),   # the X3D block
     (3, 10, (2, 3, 3), (5, 6), (1, 1, 1), "max", 3, True, "f32"),
     (2, 7, (3, 1, 1), (4, 4), (2, 0, 0), "avg", 2, False, "f32"),
+    (2, 6, (5, 3, 3), (6, 6), (2, 1, 1), "max", 5, True, "bf16"),    # kT = 5 both
+    (3, 4, (4, 3, 3), (8, 7), (1, 1, 1), "avg", 5, False, "bf16"),   # groups of 4 frames
     # a padded plane too large for the one-launch clip: per-frame fused launches
     (2, 5, (3, 3, 3), (10, 10), (1, 0, 0), "avg", 3, False, "bf16"),
 ]
 
 
-@pytest.mark.parametrize("case", CONVPOOL_CASES, ids=lambda c: f"convpool_{c[5]}_{c[8]}")
+@pytest.mark.parametrize("case", CONVPOOL_CASES, ids=lambda c: f"convpool_{c[5]}_{c[8]}_k{c[2][0]}")
 def test_fused_depthwise_pool_step(case):
     """co_convpool: one launch per step equals the depthwise conv step
     followed by the pool step bit for bit (steps, clips, mixing fused and
@@ -172,7 +174,7 @@ def test_fused_depthwise_pool_step(case):
     B, C, k, size, pad, kind, pk, cip, dt = case
     say("convpool", case)
     tdt = synth.torch_dtype(dt)
-    T = 14
+    T = 45  # clips over several blocks of the one-launch kernel, with a ragged end
     x = synth.normal((B, C, T) + size, 4500 + C, dtype=dt)
     w = synth.normal((C, 1) + k, 4501 + C, std=0.3, dtype=dt)
     b = synth.normal((C,), 4502 + C, std=0.1, dtype=dt)
@@ -241,7 +243,7 @@ def test_fused_depthwise_pool_workload():
     c, pl = wl.conv, wl.pool
     say("convpool workload")
     x, w, b = synth.workload_inputs(name)
-    x = x[:, :, :20].contiguous()
+    x = x[:, :, :40].contiguous()
     xd = x.to(DEV)
 
     def pair():
