@@ -214,7 +214,10 @@ class Workload:
         Ho, Wo = (tuple(self.co.out_size) + (1, 1))[:2]
         self.flops, self.nbytes = per_step_work(c, Ho, Wo)
         self.io_bytes = self.nbytes - 2 * (kT_of(c) - 1) * c.batch * c.out_channels * Ho * Wo * 4
-        if c.dtype == "bf16" or self.co.algo.startswith("gemm"):
+        self.in_bytes = c.batch * c.in_channels * math.prod(c.in_size) * (2 if c.dtype == "bf16" else 4)
+        # the GEMM family runs on the matrix cores, the depthwise and direct
+        # kernels on the vector ALUs
+        if self.co.algo.startswith("gemm"):
             self.bound_compute, self.peak_c = "mfma", PEAK_MFMA_TFLOPS[c.dtype]
         else:
             self.bound_compute, self.peak_c = "alu", PEAK_VALU_F32_TFLOPS
@@ -627,6 +630,16 @@ def workload_entry(wk, name, dev, K, algo, warmup):
          "forward_steps_us_per_frame": round(us_frame, 3),
          "forward_steps_persistent": bool(wk.co.steps_fused(wk.T)),
          "forward_steps_roofline": wk.roofline(us_frame, nbytes=wk.io_bytes)}
+    fused = wk.fused_convpool(K)
+    if fused is not None:
+        # depthwise conv + global pool in one launch per step / per clip (the
+        # intermediate frame stays on chip); priced on the conv's FLOPs and
+        # the clip bytes read
+        us_fused = wk.c.batch / fused[1] * 1e6
+        e["fused_convpool_step"] = round(fused[0], 1)
+        e["fused_convpool_forward_steps"] = round(fused[1], 1)
+        e["fused_convpool_forward_steps_us_per_frame"] = round(us_fused, 3)
+        e["fused_convpool_forward_steps_roofline"] = wk.roofline(us_fused, nbytes=wk.in_bytes)
     traffic = measured_traffic(name)
     if traffic is not None:
         e["roofline"]["traffic"] = traffic
