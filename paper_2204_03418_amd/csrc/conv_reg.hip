@@ -24,6 +24,7 @@
 // stores the ring / output.  No LDS and no barrier: one round trip to memory
 // plus the matrix work.  Each lane computes its own input address, so any
 // stride, dilation and spatial padding is handled.
+#include <algorithm>
 #include <type_traits>
 
 #include "device.hpp"
@@ -146,8 +147,10 @@ __global__ __launch_bounds__(64 * KSPLIT * kRegTiles) void conv_step_reg_kernel(
 
   // ---- one batch of loads: ring partial sums, bias, then the operands ----
   // The ring holds a partial sum for taps that add to it (ACC, EMIT); other
-  // taps read an out-of-range offset (zero).  The values are added after the
-  // matrix work, so no instruction waits for them before the last MFMA.
+  // taps read an out-of-range offset (zero).  The matrix work accumulates
+  // onto them (the first chain of a split tile; the other starts from zero),
+  // so the persistent kernel, whose partial sums stay in the accumulators,
+  // folds each frame exactly as this step does.
   v4f prev[WN];
 #pragma unroll
   for (int f = 0; f < WN; ++f) {
@@ -253,7 +256,7 @@ __global__ __launch_bounds__(64 * KSPLIT * kRegTiles) void conv_step_reg_kernel(
   __builtin_amdgcn_sched_barrier(0);
   v4f acc[WN];
 #pragma unroll
-  for (int f = 0; f < WN; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
+  for (int f = 0; f < WN; ++f) acc[f] = h == 0 ? prev[f] : v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int tp = 0; tp < TAPS; ++tp) {
 #pragma unroll
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(64 * KSPLIT * kRegTiles) void conv_step_reg_kernel(
     const int act = e_act[f];
     const bool to_ring = ((act == CO_TAP_START) | (act == CO_TAP_ACC)) & owner;
     const bool to_y = ((act == CO_TAP_EMIT) | (act == CO_TAP_EMIT_FRESH)) & owner;
-    const v4f v = acc[f] + prev[f];
+    const v4f v = acc[f];
     if constexpr (VEC) {  // M % 4 == 0: a lane's four pixels are all valid or none
       __builtin_amdgcn_raw_buffer_store_b128(
           __builtin_bit_cast(v4u, v), rr, (to_ring & (P0 < ra.M)) ? (e_off[f] + P0) * 4 : kOutOfRange,
@@ -450,8 +453,9 @@ hipError_t reg_launch(const ConvGeom& g, const RegConfig& c, const ConvLayout& L
 // written back at the end), and only the frames and the emitted outputs move
 // through memory.  Weights stay in registers too.  Per frame and tap the
 // products are summed over the k-steps in the order of the step kernel of
-// the same instantiation (split halves added first half + second), then
-// added to the partial sum, so forward_steps reproduces forward_step.  A
+// the same instantiation, accumulated onto the partial sum (a split
+// instantiation's second half added after), so forward_steps reproduces
+// forward_step, and the matrix instructions do the fold.  A
 // split instantiation (KSPLIT = 2) runs its two halves on two waves, which
 // meet in LDS once per frame: twice the waves, half the serial matrix work
 // per wave.
@@ -466,8 +470,19 @@ struct RegSteps {
   int32_t slot_v0;  // v0 mod R (uncapped)
   int32_t count, T, k0, update;
   int32_t o_groups;  // STG: workgroups per pixel fragment, ceil(o_frags / kRegStgWaves)
+  int32_t nseg;      // time segments of the call
+  int32_t seg_len;   // frames per segment (the last may be shorter)
+  int32_t wgs;       // workgroups per segment
   FastDiv fd_So, fd_Wo, fd_ofr, fd_og;
 };
+
+// Waves per SIMD an instantiation is compiled for: two where its registers
+// allow it without spilling (the bf16 1x1 shape with two channel blocks),
+// so that time segments can put two waves on every SIMD.
+template <typename T, int CSMAX, bool STG>
+constexpr int reg_steps_wpe() {
+  return (STG && sizeof(T) == 2 && CSMAX == 2) ? 2 : 1;
+}
 
 // STG (1x1 spatial taps, one chain per tile): the kRegStgWaves waves of a
 // workgroup share one 16-pixel fragment and take consecutive 16-channel
@@ -482,7 +497,7 @@ constexpr int kRegStgWaves = 4;
 
 template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL, bool STG>
 __global__ __launch_bounds__(64 * (STG ? kRegStgWaves : KSPLIT * kRegTiles))
-__attribute__((amdgpu_waves_per_eu(1, 1)))
+__attribute__((amdgpu_waves_per_eu(reg_steps_wpe<T, CSMAX, STG>(), reg_steps_wpe<T, CSMAX, STG>())))
 void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
                            T* __restrict__ y, const uint4* __restrict__ wp,
                            const float* __restrict__ bias, float* __restrict__ ring) {
@@ -499,7 +514,18 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
   const int lrow = lane & 15, lgrp = lane >> 4;
   const int bid = int(blockIdx.x);
-  const int lb = (bid & 7) * rs.blocks_per_xcd + (bid >> 3);
+  int lb = (bid & 7) * rs.blocks_per_xcd + (bid >> 3);
+  // Time segment: the clip's frames are dealt to rs.nseg groups of waves.
+  // Segment s > 0 starts kT - 1 frames before its first frame s0, with zero
+  // partial sums, and stores nothing before s0: every output it stores then
+  // took all its taps here, starting from zero at its first tap and adding
+  // in frame order, as stepping does, so the bits are the same.  Only
+  // segment 0 reads the ring and only the last writes it back.
+  const int seg = lb / rs.wgs;  // (wave-uniform, once)
+  if (seg >= rs.nseg) return;   // whole workgroups
+  lb -= seg * rs.wgs;
+  const int s0 = seg * rs.seg_len, s1 = min(rs.count, s0 + rs.seg_len);
+  const int tw = seg == 0 ? 0 : s0 - (g.kT - 1);
   // With KSPLIT = 2 the two chains of a tile run on two waves (h = 0 takes
   // spatial taps 0 .. TH - 1, h = 1 the rest); h = 1 hands its products to
   // h = 0 through LDS every frame, and h = 0 adds them exactly as a single
@@ -555,23 +581,32 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
         wreg[j][i2][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
   }
-  const __amdgpu_buffer_rsrc_t br = make_rsrc(bias, g.Cout * 4);
-  const float bo = __uint_as_float(
-      __builtin_amdgcn_raw_buffer_load_b32(br, ocol ? o * 4 : kOutOfRange, 0, 0));
-
-  // ---- output rows of this lane: pixels P0 .. P0 + 3 of channel o
-  const int P0 = mf * 16 + lgrp * 4;
+  // ---- outputs of this lane.  The matrix instructions take the weights as
+  // their first operand and the frame as their second (the same registers as
+  // the step kernel's, which holds the product transposed), so a lane's
+  // results are output channels oc + r, r = 0..3, of pixel Po: an output
+  // store then covers 16 consecutive pixels of four channel rows, where the
+  // step kernel's layout scattered 2-byte stores over 16 channel rows.
+  const int oc = of * 16 + lgrp * 4;
+  const int Po = mf * 16 + lrow;
   constexpr uint32_t esz = sizeof(T);
-  int yoff[4];  // byte offset of (b, o, frame 0, p) in y, or out of range
-  int roff[4];  // float offset of (o, P) inside a ring slot, or -1
+  const __amdgpu_buffer_rsrc_t br = make_rsrc(bias, g.Cout * 4);
+  float bo[4];
+  int yoff[4];  // byte offset of (b, oc + r, frame 0, p) in y, or out of range
+  int roff[4];  // float offset of (oc + r, Po) inside a ring slot, or -1
+  {
+    const bool pok = (Po < rs.M) & owner;
+    const int b = fdiv(pok ? Po : 0, rs.fd_So), p = (pok ? Po : 0) - b * rs.So;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int P = P0 + r;
-    const bool ok = ocol & (P < rs.M) & owner;
-    const int b = fdiv(ok ? P : 0, rs.fd_So), p = (ok ? P : 0) - b * rs.So;
-    yoff[r] = ok ? int((uint32_t(b * g.Cout + o) * uint32_t(rs.y_bc) + uint32_t(p)) * esz)
-                 : kOutOfRange;
-    roff[r] = ok ? o * rs.M + P : -1;
+    for (int r = 0; r < 4; ++r) {
+      const int orow = oc + r;
+      const bool ok = pok & (orow < g.Cout);
+      bo[r] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(br, orow < g.Cout ? orow * 4 : kOutOfRange, 0, 0));
+      yoff[r] = ok ? int((uint32_t(b * g.Cout + orow) * uint32_t(rs.y_bc) + uint32_t(p)) * esz)
+                   : kOutOfRange;
+      roff[r] = ok ? orow * rs.M + Po : -1;
+    }
   }
   const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, rs.y_bytes);
   const __amdgpu_buffer_rsrc_t rr = make_rsrc(ring, rs.ring_bytes);
@@ -583,7 +618,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   for (int j = 1; j < KTM; ++j) {
     part[j] = v4f{0.f, 0.f, 0.f, 0.f};
     const int tau = rs.v0 - j;
-    if (j < kT && tau >= 0) {  // uniform
+    if (seg == 0 && j < kT && tau >= 0) {  // uniform
       const int sl = (rs.slot_v0 - j + R) % R;
 #pragma unroll
       for (int r = 0; r < 4; ++r)
@@ -651,7 +686,18 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   constexpr int SCH = CSMAX * CKS;            // staged channels (upper bound)
   constexpr int SQ = (SCH / 4 + 15) / 16;     // channel quads per thread
   constexpr int PU = SCH * int(esz) / 16 + 1;  // LDS row pitch, 16-byte units
-  constexpr int SPF = STG ? (SQ <= 2 ? 4 : 2) : 1;  // frames in flight
+  constexpr int SPF0 = SQ <= 2 ? 4 : 2;
+  // frames per group: whole periods of the partial sums' rotation, so a
+  // group ends with every sum back in the register it started in; frames in
+  // flight: the group, or where two waves share a SIMD (registers for two) a
+  // divisor of it, at most SPF0
+  constexpr int FPG_S = KTM * ((SPF0 + KTM - 1) / KTM);
+  constexpr int SPF = !STG                                  ? 1
+                      : reg_steps_wpe<T, CSMAX, STG>() == 1 ? FPG_S
+                      : FPG_S % 4 == 0                      ? 4
+                      : FPG_S % 3 == 0                      ? 3
+                      : FPG_S % 2 == 0                      ? 2
+                                                            : FPG_S;
   __shared__ uint4 stg[STG ? 2 : 1][STG ? 16 * PU : 1];
   uint32_t sraw[SPF][STG ? SQ : 1][4];
   const int tid = int(threadIdx.x);
@@ -681,7 +727,9 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
 #pragma unroll
     for (int k = 0; k < SQ; ++k) {
       const int qd = sq0 + 16 * k;
-      if (qd < SCH / 4) {
+      // (a compile-time test where the quads fill the threads: a divergent
+      // branch here would split the frame loop into blocks)
+      if ((SCH / 4) % 16 == 0 || qd < SCH / 4) {
         if constexpr (kBF)
           reinterpret_cast<uint2*>(row)[qd] =
               make_uint2(a[k][0] | (a[k][1] << 16), a[k][2] | (a[k][3] << 16));
@@ -703,20 +751,28 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   __shared__ v4f red[KSPLIT == 2 ? TPW : 1][2][KSPLIT == 2 ? KTM : 1][64];
   // in frame order (the loop below waits for frame u's loads with the later
   // frames' still in flight)
+  // STG: operands of the frame being multiplied, read from LDS after the
+  // previous frame's barrier
+  AReg aq[STG ? CSMAX : 1];
   if constexpr (STG) {
 #pragma unroll
     for (int u = 0; u < SPF; ++u) {
-      load_stage(u, sraw[u]);
+      load_stage(tw + u, sraw[u]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    write_stage(tw & 1, sraw[0]);
+    load_stage(tw + SPF, sraw[0]);
+    __syncthreads();
+#pragma unroll
+    for (int cb = 0; cb < CSMAX; ++cb) aq[cb] = staged_operand(tw & 1, cb);
   } else {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
-      load_frame(u, araw[u]);
+      load_frame(tw + u, araw[u]);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  constexpr int FPG = STG ? SPF : PF;  // frames per group
+  constexpr int FPG = STG ? FPG_S : PF;  // frames per group
 
   // Whole groups of PF frames, with no exit inside a group: frames past the
   // call (the last group's tail) run with their stores dropped and the
@@ -729,19 +785,17 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   auto frame = [&](int t0, int u, auto steady_tag) {
     constexpr bool STEADY = decltype(steady_tag)::value;
     const int t = t0 + u;
-    const bool dead = STEADY ? false : t >= rs.count;  // uniform
+    const bool dead = STEADY ? false : t >= s1;  // uniform
     const int v = rs.v0 + t;
-    if constexpr (STG) {
-      // frame t into LDS buffer t & 1 (every wave left it at the previous
-      // frame's barrier), then frame t + SPF's gathers
-      write_stage(t & 1, sraw[u]);
-      load_stage(t + SPF, sraw[u]);
-      __syncthreads();
-    }
-    // products of every temporal tap over this wave's chain of k-steps
+    // every temporal tap's chain of k-steps, accumulated onto the sum it
+    // continues (zero for an output that starts, and on a split tile's
+    // second chain)
     v4f c[KTM];
 #pragma unroll
-    for (int j = 0; j < KTM; ++j) c[j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < KTM; ++j) {
+      const int first = STEADY ? 0 : (v - j >= g.pT ? 0 : g.pT - (v - j));
+      c[j] = (h == 0 && j != 0 && j != first) ? part[j] : v4f{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
     for (int i2 = 0; i2 < TH; ++i2)
 #pragma unroll
@@ -751,21 +805,33 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
           if (!FULL && j >= kT) continue;  // uniform
           AReg av;
           if constexpr (STG)
-            av = staged_operand(t & 1, cb);
+            av = aq[cb];
           else
             av = operand(araw[u][i2][cb]);
           if constexpr (kBF) {
             c[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(v8bf, av), __builtin_bit_cast(v8bf, wreg[j][i2][cb]), c[j],
+                __builtin_bit_cast(v8bf, wreg[j][i2][cb]), __builtin_bit_cast(v8bf, av), c[j],
                 0, 0, 0);
           } else {
             const uint4 u4 = wreg[j][i2][cb / 4];
             const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
-            c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, __uint_as_float(bw), c[j], 0, 0, 0);
+            c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bw), av, c[j], 0, 0, 0);
           }
         }
     // the next frames' operands are requested before this frame's epilogue
     if constexpr (!STG) load_frame(t + PF, araw[u]);
+    if constexpr (STG) {
+      // frame t + 1 into LDS buffer (t + 1) & 1 (every wave read frame t - 1
+      // from it before the previous barrier), frame t + 1 + SPF's gathers,
+      // and after the barrier frame t + 1's operands: their LDS latency runs
+      // under this frame's matrix work and epilogue
+      const int un = (u + 1) % SPF;
+      write_stage((t + 1) & 1, sraw[un]);
+      load_stage(t + 1 + SPF, sraw[un]);
+      __syncthreads();
+#pragma unroll
+      for (int cb = 0; cb < CSMAX; ++cb) aq[cb] = staged_operand((t + 1) & 1, cb);
+    }
     v4f c1[KTM];  // chain 1's products (KSPLIT = 2), as chain 0 adds them
     if constexpr (KSPLIT == 2) {
       if (h == 1) {
@@ -781,8 +847,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
 #pragma unroll
       for (int j = 0; j < KTM; ++j) c1[j] = red[wslot][t & 1][j][lane];
     }
-    // fold each product into its output: tap j completes v - (kT - 1),
-    // starts at the first tap on a real frame, continues otherwise
+    // tap j completes output v - (kT - 1); the others carry on
     v4f nxt[KTM];
 #pragma unroll
     for (int j = 0; j < KTM; ++j) {
@@ -792,16 +857,16 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       // the stores of a missing output carry the out-of-range offset)
       const int tau = v - j;
       const bool exists = STEADY ? true : (tau >= 0) & !dead;
-      const int first = STEADY ? 0 : tau >= g.pT ? 0 : g.pT - tau;
-      v4f sum = c[j];
-      if constexpr (KSPLIT == 2) sum = sum + c1[j];
-      const v4f a = (j == first) ? sum : sum + part[j];
+      // (a segment's warm-up frames keep their sums but store nothing)
+      const bool stores = STEADY ? true : exists & (t >= s0);
+      v4f a = c[j];
+      if constexpr (KSPLIT == 2) a = a + c1[j];
       if (j == kT - 1) {
-        const int fo = exists ? (rs.k0 + t) * rs.So * int(esz) : 0;
+        const int fo = stores ? (rs.k0 + t) * rs.So * int(esz) : 0;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float val = a[r] + bo;
-          const int yo = exists ? yoff[r] : kOutOfRange;
+          const float val = a[r] + bo[r];
+          const int yo = stores ? yoff[r] : kOutOfRange;
           if constexpr (kBF)
             __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)),
                                                   yr, yo, fo, 0);
@@ -820,10 +885,10 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
     // only just before, instead of PF frames earlier
     __builtin_amdgcn_sched_barrier(0);
   };
-  for (int t0 = 0; t0 < rs.count; t0 += FPG) {
+  for (int t0 = tw; t0 < s1; t0 += FPG) {
     // uniform: the outputs v - j of every frame of the group started at or
     // after the first real frame
-    const bool steady = (rs.v0 + t0 >= g.pT + kT - 1) & (t0 + FPG <= rs.count);
+    const bool steady = (rs.v0 + t0 >= g.pT + kT - 1) & (t0 >= s0) & (t0 + FPG <= s1);
     if constexpr (STG) {
       if (steady) {
 #pragma unroll
@@ -835,14 +900,14 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
     for (int u = 0; u < FPG; ++u) frame(t0, u, std::false_type{});
   }
 
-  if (rs.update && h == 0) {
+  if (rs.update && h == 0 && s1 == rs.count) {
     const int v1 = rs.v0 + rs.count;
-    const int s1 = (rs.slot_v0 + rs.count) % R;
+    const int slot1 = (rs.slot_v0 + rs.count) % R;
 #pragma unroll
     for (int j = 1; j < KTM; ++j) {
       const int tau = v1 - j;
       if (j < kT && tau >= 0) {  // uniform
-        const int sl = (s1 - j + R) % R;
+        const int sl = (slot1 - j + R) % R;
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           __builtin_amdgcn_raw_buffer_store_b32(
@@ -914,10 +979,19 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   constexpr bool STG = TAPS == 1 && KSPLIT == 1;
   rs.o_groups = int32_t(ceil_div(rs.o_frags, kRegStgWaves));
   rs.fd_og = make_fastdiv(uint32_t(rs.o_groups));
-  if (STG) {
-    const int64_t wgs = int64_t(rs.m_frags) * rs.o_groups;
-    rs.blocks_per_xcd = int32_t(ceil_div(wgs, 8));
-  }
+  // time segments: as many as keep every wave resident at the waves per
+  // SIMD the instantiation is compiled for (1024 SIMDs), with each
+  // segment's warm-up (kT - 1 frames) at most a quarter of its frames
+  const int64_t wgs = STG ? int64_t(rs.m_frags) * rs.o_groups : blocks;
+  const int64_t waves = wgs * (STG ? kRegStgWaves : KSPLIT * kRegTiles);
+  constexpr int64_t kSimds = 1024;
+  int64_t nseg = (reg_steps_wpe<T, CSMAX, STG>() * kSimds) / std::max<int64_t>(waves, 1);
+  if (g.kT > 1) nseg = std::min<int64_t>(nseg, count / (4 * (g.kT - 1)));
+  nseg = std::max<int64_t>(1, std::min<int64_t>(nseg, 64));
+  rs.seg_len = int32_t(ceil_div(count, nseg));
+  rs.nseg = int32_t(ceil_div(count, rs.seg_len));
+  rs.wgs = int32_t(wgs);
+  rs.blocks_per_xcd = int32_t(ceil_div(wgs * rs.nseg, 8));
   auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true, STG>
                           : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false, STG>;
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)),

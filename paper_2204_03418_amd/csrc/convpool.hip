@@ -377,8 +377,7 @@ __global__ __launch_bounds__(64 * kBnTail, 8) void bneck_step_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int p = wave * 16 + 4 * lgrp + r;
-      const float v = acc[r] + 0.f;  // the step kernel adds its (zero) partial sum
-      const float val = v + bo;
+      const float val = acc[r] + bo;  // (the step kernel's chain starts from a zero partial sum)
       T z1;
       if constexpr (kBF)
         z1 = __builtin_bit_cast(uint16_t, __bf16(val));

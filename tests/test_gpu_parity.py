@@ -678,6 +678,63 @@ def test_gemm_forward_steps_persistent(case):
                        "gemm steps")
 
 
+REG_SEG_CASES = [
+    # B, C_in, C_out, kernel (time first), in_size, padding, frames, dtype, oracle streams
+    (32, 64, 256, (9, 1), (25,), (0, 0), 100, "bf16", (0, 31)),        # skeleton layer: 2 segments
+    (1, 24, 24, (3, 3, 3), (28, 28), (0, 1, 1), 40, "f32", (0,)),      # 3x3 taps: 5 segments
+    (2, 20, 36, (3, 3, 3), (14, 15), (2, 1, 1), 33, "f32", (1,)),      # start padding, ragged
+]
+
+
+@pytest.mark.parametrize("case", REG_SEG_CASES, ids=lambda c: f"regseg_{c[0]}_{c[1]}_{c[2]}_T{c[6]}")
+def test_reg_forward_steps_time_segments(case):
+    """The persistent register GEMM over a clip long enough to be split into
+    time segments (each after the first replays kT - 1 frames and stores
+    from its own first frame): against the oracle with end padding on
+    sampled streams, bitwise against stepping on all, as a clip that
+    continues single steps, and with update_state=False."""
+    B, cin, cout, k, size, p, T, dt, sel = case
+    say("reg segments", case)
+    tdt = synth.torch_dtype(dt)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          padding=p, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, T, 99000 + cin + cout + T, "kaiming")
+    xd = x.to(DEV)
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, padding=p,
+                            algo="gemm_reg")
+
+    co = make()
+    assert co.algo.startswith("gemm_reg") and co.steps_fused(T, pad_end=True)
+    ones = (1,) * len(k)
+    ys = co.forward_steps(xd, pad_end=True)
+    sl = list(sel)
+    rp = oracle_conv(w, b, ones, p, ones, 1).forward_steps(np64(x[sl]), pad_end=True)
+    assert_close(np64(ys[sl]), rp, tdt, "reg segments", terms=conv_terms(w))
+    # bitwise: the clip, stepping, and a clip between single steps
+    seq = _run_steps(make(), xd)
+    co.clean_state()
+    assert torch.equal(co.forward_steps(xd), torch.stack(seq, dim=2))
+    co3 = make()
+    for t in range(3):
+        co3.forward_step(xd[:, :, t].contiguous())
+    mid = co3.forward_steps(xd[:, :, 3:T - 5].contiguous())
+    tail = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(T - 5, T)]
+    got = [mid[:, :, i] for i in range(mid.shape[2])] + [t_ for t_ in tail if t_ is not None]
+    n_first = sum(1 for t in range(3) if t >= co3.delay)
+    assert len(got) == len(seq) - n_first
+    for g_, s_ in zip(got, seq[n_first:]):
+        assert torch.equal(g_, s_)
+    # update_state=False: same outputs, state unchanged
+    torch.cuda.synchronize()
+    before, n = co3.state.clone(), co3.steps
+    peek = co3.forward_steps(xd, update_state=False)
+    torch.cuda.synchronize()
+    assert co3.steps == n and torch.equal(co3.state, before)
+    assert torch.equal(peek, co3.forward_steps(xd))
+
+
 @pytest.mark.parametrize("name,streams", [
     ("conv3d_b64_c192_k3_14x14_bf16", (0, 37, 63)),
     ("dwconv3d_b16_c432_k3_7x7_avgpool_bf16", (0, 9, 15)),
