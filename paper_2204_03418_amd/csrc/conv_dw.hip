@@ -436,6 +436,143 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
   }
 }
 
+// Temporal stride or dilation above 1 (Principle 5): which output a tap
+// feeds, and whether it starts, continues or completes it, now depends on the
+// frame.  The kernel follows the host's step plans (the ones the per-frame
+// step launches take), packed per frame as 6 bits a tap: action (3 bits, the
+// CO_TAP_ codes) and ring slot (3 bits).  They are explicit for the call's
+// frames in a stream's first (kT - 1) dT steps, where start padding and
+// missing outputs matter, and periodic afterwards: from then on the plan of
+// step n + sT R equals that of step n (slots cycle with the output index
+// mod R).  Each lane keeps the R partial sums of its pixel in LDS, where a
+// slot chosen at run time costs no more than a fixed one; frames go through
+// zero-haloed LDS tiles as in the kernel above.  Per tap the arithmetic is
+// the step kernel's: from the ring value (ACC, EMIT) or zero, the 3x3 chain,
+// then back to the slot or out with the bias.
+constexpr int kDwgMaxR = 8;       // ring slots (3-bit slot field)
+constexpr int kDwgStart = 32;     // explicit plans: stream-start frames of a call
+constexpr int kDwgPeriod = 64;    // periodic plans: sT R steps
+constexpr int kDwgU = 4;          // frames per group
+
+struct DwgArgs {
+  int32_t n_start;  // frames of the call that take explicit plans
+  int32_t period;   // sT * R
+  int32_t ph0;      // phase of frame n_start in the periodic table
+  int32_t PW;       // padded tile width
+  int32_t frame_bytes;
+  int32_t code_start[kDwgStart];
+  int32_t code_period[kDwgPeriod];
+};
+
+template <typename T, int KH, int KW, int KT>
+__global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwg_kernel(
+    ConvGeom g, DwSteps ds, DwgArgs ga, const T* __restrict__ x, int64_t x_bc,
+    T* __restrict__ y, int64_t y_bc, const float* __restrict__ w,
+    const float* __restrict__ bias, float* __restrict__ ring, int64_t ring_slot) {
+  constexpr int NS = KH * KW;
+  constexpr int U = kDwgU;
+  constexpr uint32_t esz = sizeof(T);
+  __shared__ float lds[kDwpWaves][U][kDwpSlot];
+  __shared__ float parts[kDwpWaves][kDwgMaxR][64];
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  const int bc = int(blockIdx.x) * kDwpWaves + wave;
+  if (bc >= g.B * g.Cout) return;  // whole waves; no workgroup barrier below
+  const int S = g.H * g.W, So = g.Ho * g.Wo;
+  const int bq = fdiv(bc, ds.fd_Cout), c = bc - bq * g.Cout;
+  float(*sl)[kDwpSlot] = lds[wave];
+  float* const pp = &parts[wave][0][lane];  // + slot * 64
+
+  for (int e = lane; e < U * kDwpSlot; e += 64) (&sl[0][0])[e] = 0.f;  // halos stay zero
+
+  const bool in_px = lane < S;
+  int wpos = kDwpSlot - 1;
+  if (in_px) {
+    const int hp = fdiv(lane, ds.fd_W);
+    wpos = (hp + g.pH) * ga.PW + (lane - hp * g.W) + g.pW;
+  }
+  float* const wp = &sl[0][wpos];
+  const int plane = int(uint32_t(bc) * uint32_t(x_bc) * esz);
+  const int xin = in_px ? plane + lane * int(esz) : kOutOfRange;
+  const bool pl = lane < So;
+  const int p = pl ? lane : 0;
+  const int i = fdiv(p, ds.fd_Wo), jo = p - i * g.Wo;
+  const float* rp[NS];
+#pragma unroll
+  for (int u = 0; u < KH; ++u)
+#pragma unroll
+    for (int v = 0; v < KW; ++v)
+      rp[u * KW + v] = &sl[0][(i * g.sH + u * g.dH) * ga.PW + jo * g.sW + v * g.dW];
+  const int yo = pl ? int((uint32_t(bc) * uint32_t(y_bc) + uint32_t(p)) * esz) : kOutOfRange;
+  const int ridx = (c * g.B + bq) * So + p;
+
+  float wr[KT][NS];
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+#pragma unroll
+    for (int e = 0; e < NS; ++e) wr[j][e] = w[(c * KT + j) * NS + e];
+  const float bo = bias[c];
+  // the ring's R slots of this pixel, live or not (stale slots go back as read)
+  for (int q = 0; q < g.R; ++q) pp[q * 64] = pl ? ring[q * ring_slot + ridx] : 0.f;
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, ds.x_bytes);
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, ds.y_bytes);
+  auto load = [&](int t) {
+    const bool real = t < ds.T;
+    return load_raw_at<T>(xr, real ? xin : kOutOfRange, real ? t * ga.frame_bytes : 0);
+  };
+  int k = 0;          // outputs emitted so far in the call
+  int ph = ga.ph0;    // phase of the next periodic frame
+  auto eval = [&](int t, int u) {
+    int code;
+    if (t < ga.n_start) {
+      code = ga.code_start[t];
+    } else {
+      code = ga.code_period[ph];
+      ph = ph + 1 == ga.period ? 0 : ph + 1;
+    }
+    float xv[NS];
+#pragma unroll
+    for (int e = 0; e < NS; ++e) xv[e] = rp[e][u * kDwpSlot];
+    bool emitted = false;
+#pragma unroll
+    for (int j = KT - 1; j >= 0; --j) {
+      const int act = (code >> (6 * j)) & 7, slot = (code >> (6 * j + 3)) & 7;
+      if (act == CO_TAP_NONE) continue;  // uniform
+      float a = (act == CO_TAP_ACC || act == CO_TAP_EMIT) ? pp[slot * 64] : 0.f;
+#pragma unroll
+      for (int e = 0; e < NS; ++e) a = fmaf(wr[j][e], xv[e], a);
+      if (act == CO_TAP_EMIT || act == CO_TAP_EMIT_FRESH) {
+        store_at(yr, yo, k * So * int(esz), from_f32<T>(a + bo));
+        emitted = true;
+      } else {
+        pp[slot * 64] = a;
+      }
+    }
+    if (emitted) ++k;
+  };
+
+  uint32_t xa[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) xa[u] = load(u);
+  for (int t = 0; t < ds.count; t += U) {
+    lds_order();
+#pragma unroll
+    for (int u = 0; u < U; ++u) wp[u * kDwpSlot] = raw_to_f32<T>(xa[u]);
+    lds_order();
+#pragma unroll
+    for (int u = 0; u < U; ++u) xa[u] = load(t + U + u);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (t + u >= ds.count) break;  // (the clip's last, ragged group)
+      eval(t + u, u);
+    }
+    lds_order();
+  }
+  if (ds.update && pl)
+    for (int q = 0; q < g.R; ++q) ring[q * ring_slot + ridx] = pp[q * 64];
+}
+
 // The small-plane kernel's conditions: one lane per input and per output
 // pixel, the padded tile and its sink cell within a slot.
 bool dwp_fits(const ConvGeom& g) {
@@ -464,6 +601,37 @@ hipError_t dw_steps_launch(const ConvGeom& g, const ConvLayout& L, char* state, 
   ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   ds.fd_W = make_fastdiv(uint32_t(g.W));
   const int64_t fbytes = g.S() * esz;
+  if (g.sT != 1 || g.dT != 1) {
+    // step plans: explicit for the call's frames in the stream's first
+    // (kT - 1) dT steps, then one period of sT R steps
+    DwgArgs ga{};
+    const int64_t n_steady = int64_t(g.kT - 1) * g.dT;
+    ga.n_start = int32_t(std::max<int64_t>(0, std::min<int64_t>(count, n_steady - n0)));
+    ga.period = g.sT * g.R;
+    ga.PW = g.W + 2 * g.pW;
+    ga.frame_bytes = int32_t(fbytes);
+    auto pack = [&](int64_t n) {
+      co_step_plan plan;
+      conv_plan(g, n, true, &plan);
+      int32_t code = 0;
+      for (int j = 0; j < g.kT; ++j)
+        code |= (int32_t(plan.action[j]) | (std::max(plan.slot[j], 0) << 3)) << (6 * j);
+      return code;
+    };
+    for (int t = 0; t < ga.n_start; ++t) ga.code_start[t] = pack(n0 + t);
+    // the periodic table starts at the first steady step of the call
+    const int64_t n_first = n0 + ga.n_start;
+    for (int q = 0; q < ga.period; ++q) ga.code_period[q] = pack(n_first + q);
+    ga.ph0 = 0;
+    // output frame of the call's first emission: emissions go out in order
+    hipLaunchKernelGGL((conv_steps_dwg_kernel<T, KH, KW, KT>),
+                       dim3(unsigned((int64_t(g.B) * g.Cout + kDwpWaves - 1) / kDwpWaves)),
+                       dim3(64 * kDwpWaves), 0, s, g, ds, ga, static_cast<const T*>(x), x_bc,
+                       static_cast<T*>(y), y_bc, reinterpret_cast<const float*>(state + L.weight),
+                       reinterpret_cast<const float*>(state + L.bias),
+                       reinterpret_cast<float*>(state + L.ring), L.ring_slot_elems);
+    return hipGetLastError();
+  }
   if (dwp_fits(g)) {
     DwpArgs pa;
     pa.PW = g.W + 2 * g.pW;
@@ -533,7 +701,11 @@ bool dw_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   const bool fits = int64_t(g.B) * g.Cin * x_frames * g.S() * esz < (int64_t(1) << 31) &&
                     int64_t(g.B) * g.Cout * y_frames * g.So() * esz < (int64_t(1) << 31);
-  return g.algo == CO_ALGO_DEPTHWISE && g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 &&
+  // temporal stride or dilation above 1: the plan-driven small-plane kernel
+  const bool strided = g.sT != 1 || g.dT != 1;
+  const bool general = dwp_fits(g) && g.R <= kDwgMaxR && int64_t(g.sT) * g.R <= kDwgPeriod &&
+                       int64_t(g.kT - 1) * g.dT <= kDwgStart;
+  return g.algo == CO_ALGO_DEPTHWISE && (!strided || general) && g.kT >= 1 && g.kT <= 5 &&
          ((g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1)) && fits;
 }
 

@@ -482,10 +482,17 @@ DW_STEPS_CASES = [
     (2, 7, 3, (3, 3), (7, 7), (0, 2, 2), "f32", (1, 1), (2, 2)),    # dilation 2: 11 x 11 tile
     (2, 6, 2, (3, 3), (8, 8), (0, 2, 2), "bf16", (1, 1), (2, 2)),   # 12 x 12 tile: thread per output
     (1, 5, 3, (3, 3), (6, 6), (2, 1, 1), "bf16", (1, 2), (1, 1)),   # stride in one axis only
+    # temporal stride / dilation (plan-driven kernel): ..., sT, dT
+    (2, 8, 3, (3, 3), (7, 7), (1, 1, 1), "bf16", (1, 1), (1, 1), 2, 1),  # temporal stride 2
+    (2, 6, 3, (3, 3), (6, 6), (2, 1, 1), "f32", (1, 1), (1, 1), 1, 2),   # temporal dilation 2
+    (1, 5, 5, (3, 3), (5, 5), (4, 0, 0), "bf16", (1, 1), (1, 1), 3, 1),  # stride 3, kT 5
+    (2, 4, 2, (1, 1), (4, 4), (0, 0, 0), "f32", (1, 1), (1, 1), 2, 3),   # 1x1, stride 2, dilation 3
+    (2, 9, 3, (3, 3), (7, 7), (1, 1, 1), "bf16", (1, 1), (1, 1), 2, 2),  # stride and dilation 2
 ]
 
 
-@pytest.mark.parametrize("case", DW_STEPS_CASES, ids=lambda c: "dwsteps_" + "_".join(map(str, c[:3])))
+@pytest.mark.parametrize("case", DW_STEPS_CASES, ids=lambda c: "dwsteps_" + "_".join(map(str, c[:3])) + (
+    f"_s{c[9]}d{c[10]}" if len(c) > 9 else ""))
 def test_depthwise_forward_steps_persistent(case):
     """The depthwise forward_steps runs as one persistent launch (partial sums
     in registers across frames).  Against the oracle with end padding, and
@@ -493,8 +500,8 @@ def test_depthwise_forward_steps_persistent(case):
     when a clip continues a state left by single steps, after clean_state
     (stale ring contents) and with update_state=False."""
     B, C, kT, ks, size, p, dt = case[:7]
-    st = (1,) + (case[7] if len(case) > 7 else (1, 1))
-    dil = (1,) + (case[8] if len(case) > 8 else (1, 1))
+    st = (case[9] if len(case) > 9 else 1,) + (case[7] if len(case) > 7 else (1, 1))
+    dil = (case[10] if len(case) > 10 else 1,) + (case[8] if len(case) > 8 else (1, 1))
     say("depthwise steps", case)
     spec = synth.ConvSpec(batch=B, in_channels=C, out_channels=C, kernel=(kT,) + ks, in_size=size,
                           stride=st, padding=p, dilation=dil, groups=C, dtype=dt)
@@ -522,15 +529,14 @@ def test_depthwise_forward_steps_persistent(case):
         assert torch.equal(ys2, torch.stack(outs, dim=2))
     # a clip that continues single steps, and single steps after a clip
     co3, co4 = make(), make()
-    for t in range(3):
-        co3.forward_step(xd[:, :, t].contiguous())
+    heads = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(3)]
     mid = co3.forward_steps(xd[:, :, 3:9].contiguous())
     tail = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(9, x.shape[2])]
     seq = [co4.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
     seq = [s_.clone() for s_ in seq if s_ is not None]
     got = ([mid[:, :, k] for k in range(mid.shape[2])] if mid is not None else []) + \
         [t_ for t_ in tail if t_ is not None]
-    n_first = sum(1 for t in range(3) if t >= co3.delay)
+    n_first = sum(1 for h_ in heads if h_ is not None)  # (a temporal stride skips steps)
     assert len(got) == len(seq) - n_first
     for g_, s_ in zip(got, seq[n_first:]):
         assert torch.equal(g_, s_)
