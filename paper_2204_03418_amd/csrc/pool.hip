@@ -373,6 +373,8 @@ constexpr int kPgFrames = 32;  // frames per block, lanes 0..31
 struct PoolGlobalArgs {
   int32_t nblk;       // blocks of the call: ceil(count / kPgFrames)
   int32_t lds_bytes;  // per wave: a block, its alignment and 64 elements of over-read
+  int32_t F;          // window span f = (kT - 1) dT + 1: FIFO slots
+  int64_t tau0;       // output index of the call's first emission
 };
 
 // Value of `cur` in lane (lane - k) of this block, or of `prev` in the
@@ -404,15 +406,16 @@ __global__ __launch_bounds__(64) void pool_steps_global_kernel(
   const int yplane = int(uint32_t(bc) * uint32_t(y_bc) * esz);
 
   // the previous block's reduced frames and validity by lane; before the
-  // first block, lanes kPgFrames - (KT - 1) + q hold the FIFO's frame
-  // n0 - (KT - 1) + q
+  // first block, lanes kPgFrames - (F - 1) + q hold the FIFO's frame
+  // n0 - (F - 1) + q (the window spans F = (kT - 1) dT + 1 frames)
+  const int F = pa.F;
   float prev = neutral, prevok = 0.f;
   {
-    const int q = lane - (kPgFrames - (KT - 1));
-    const int64_t rf = ps.n0 - (KT - 1) + q;
+    const int q = lane - (kPgFrames - (F - 1));
+    const int64_t rf = ps.n0 - (F - 1) + q;
     if (q >= 0 && lane < kPgFrames && rf >= 0) {
-      prev = fifo[(rf % KT) * fifo_slot + bc];
-      prevok = valid[rf % KT];
+      prev = fifo[(rf % F) * fifo_slot + bc];
+      prevok = valid[rf % F];
     }
   }
 
@@ -508,20 +511,21 @@ __global__ __launch_bounds__(64) void pool_steps_global_kernel(
     const float curok = real ? 1.f : 0.f;
     __syncthreads();  // the reads are done before the next block's writes
 
-    // the window of step n = n0 + t: frames n - (KT - 1) + q, q = 0..KT-1
+    // the window of step n = n0 + t: frames n - (KT - 1 - q) dT, q = 0..KT-1
+    // (the temporal stride only decides which steps emit)
     const int64_t n = ps.n0 + t;
     float fv[KT], fok[KT];
     fv[KT - 1] = cur;
     fok[KT - 1] = curok;
 #pragma unroll
     for (int q = 0; q + 1 < KT; ++q) {
-      fv[q] = lane_back(cur, prev, lane, KT - 1 - q);
-      fok[q] = lane_back(curok, prevok, lane, KT - 1 - q);
+      fv[q] = lane_back(cur, prev, lane, (KT - 1 - q) * g.dT);
+      fok[q] = lane_back(curok, prevok, lane, (KT - 1 - q) * g.dT);
     }
     float tv[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const bool in = q < KT && n - (KT - 1) + q >= 0;
+      const bool in = q < KT && n - int64_t(KT - 1 - q) * g.dT >= 0;
       tv[q] = in ? fv[q < KT ? q : 0] : neutral;
     }
 #pragma unroll
@@ -539,7 +543,7 @@ __global__ __launch_bounds__(64) void pool_steps_global_kernel(
         float tc[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-          const bool in = q < KT && n - (KT - 1) + q >= 0;
+          const bool in = q < KT && n - int64_t(KT - 1 - q) * g.dT >= 0;
           tc[q] = in ? fok[q < KT ? q : 0] : 0.f;
         }
 #pragma unroll
@@ -554,12 +558,13 @@ __global__ __launch_bounds__(64) void pool_steps_global_kernel(
       }
       out = div > 0.f ? out / div : 0.f;
     }
-    const bool emits = live && t < ps.count && n >= g.d;
-    store_at(yr, emits ? yplane : kOutOfRange, emits ? int((n - ps.emit0) * int64_t(esz)) : 0,
+    const bool emits = live && t < ps.count && n >= g.d && (n - g.d) % g.sT == 0;
+    const int64_t k = emits ? (n - g.d) / g.sT - pa.tau0 : 0;  // the call's k-th output
+    store_at(yr, emits ? yplane : kOutOfRange, emits ? int(k * int64_t(esz)) : 0,
              from_f32<T>(out));
-    // the call's last KT - 1 frames go to their FIFO slots
-    if (ps.update && live && t < ps.count && t >= ps.count - (KT - 1))
-      fifo[(n % KT) * fifo_slot + bc] = cur;
+    // the call's last F - 1 frames go to their FIFO slots
+    if (ps.update && live && t < ps.count && t >= ps.count - (F - 1))
+      fifo[(n % F) * fifo_slot + bc] = cur;
     prev = cur;
     prevok = curok;
   }
@@ -696,6 +701,9 @@ hipError_t pool_global_launch(const PoolGeom& g, const PoolLayout& L, char* stat
   ps.fstride = int32_t(g.S() * esz);
   PoolGlobalArgs pa;
   pa.nblk = int32_t((int64_t(count) + kPgFrames - 1) / kPgFrames);
+  pa.F = g.R;  // the FIFO holds the window's span
+  const int64_t lo = n0 > g.d ? n0 : g.d;
+  pa.tau0 = (lo - g.d + g.sT - 1) / g.sT;
   // the block, its alignment shift and the 64-element over-read of the last lane
   pa.lds_bytes = int32_t(((kPgFrames * g.S() + 64) * esz + 16 + 15) / 16 * 16);
   if (pa.lds_bytes > 64 * 16 * (esz == 2 ? 5 : 9)) return hipErrorInvalidValue;  // NU units
@@ -746,7 +754,11 @@ hipError_t launch_pool_valid(float* valid, int32_t R, int64_t n0, int32_t count,
 
 bool pool_steps_supported(const PoolGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
-  return g.sT == 1 && g.dT == 1 && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64 &&  // (kT <= 8: tree)
+  // temporal stride or dilation above 1: the frames-in-lanes global pool,
+  // whose window reaches (kT - 1) dT lanes back across one block
+  const bool strided = g.sT != 1 || g.dT != 1;
+  const bool general = pool_global_fits(g) && int64_t(g.kT - 1) * g.dT < kPgFrames;
+  return (!strided || general) && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64 &&  // (kT <= 8: tree)
          int64_t(g.B) * g.C * x_frames * g.S() * esz < (int64_t(1) << 31) &&
          int64_t(g.B) * g.C * y_frames * g.So() * esz < (int64_t(1) << 31);
 }

@@ -784,17 +784,23 @@ POOL_STEPS_CASES = [
     ("avg", (2, 5, 5), (5, 5), (1, 5, 5), (0, 0, 0), True, "bf16", 33),
     ("avg", (5, 8, 8), (8, 8), (1, 1, 1), (2, 0, 0), False, "f32", 70),
     ("max", (4, 7, 7), (7, 7), (1, 7, 7), (0, 0, 0), True, "bf16", 64),
+    # temporal stride / dilation on the global pool: ..., frames, temporal dilation
+    ("avg", (3, 7, 7), (7, 7), (2, 7, 7), (0, 0, 0), True, "bf16", 40, 1),
+    ("avg", (4, 6, 6), (6, 6), (3, 1, 1), (2, 0, 0), False, "f32", 45, 1),
+    ("max", (3, 5, 5), (5, 5), (1, 5, 5), (1, 0, 0), True, "bf16", 50, 3),
+    ("max", (2, 7, 7), (7, 7), (2, 7, 7), (0, 0, 0), True, "bf16", 70, 4),
 ]
 
 
 @pytest.mark.parametrize("case", POOL_STEPS_CASES, ids=lambda c: "poolsteps_" + c[0] + str(c[1][0]) + (
-    f"_T{c[7]}" if len(c) > 7 else ""))
+    f"_T{c[7]}" if len(c) > 7 else "") + (f"_s{c[3][0]}d{c[8]}" if len(c) > 8 else ""))
 def test_pool_forward_steps_persistent(case):
     """Pool forward_steps as one persistent launch against the oracle (end
     padding), bitwise against per-frame steps, continuing a state left by
     single steps, and with update_state=False."""
     kind, ks, size, ss, ps, cip, dt = case[:7]
     T = case[7] if len(case) > 7 else 12
+    dil = (case[8] if len(case) > 8 else 1, 1, 1)
     say("pool steps", case)
     tdt = synth.torch_dtype(dt)
     x = synth.normal((3, 6, T) + size, 7700 + ks[0] + T, dtype=dt)
@@ -802,23 +808,23 @@ def test_pool_forward_steps_persistent(case):
 
     def make():
         return coinf.CoPool(kind, batch=3, channels=6, kernel=ks, in_size=size, stride=ss,
-                            padding=ps, count_include_pad=cip, dtype=tdt)
+                            padding=ps, dilation=dil, count_include_pad=cip, dtype=tdt)
 
     po = make()
+    assert po.steps_fused(T)
     ys = po.forward_steps(xd, pad_end=True)
-    r = oracle.ContinualPool(kind, ks, ss, ps, (1, 1, 1), cip, spatial_dims=2).forward_steps(
+    r = oracle.ContinualPool(kind, ks, ss, ps, dil, cip, spatial_dims=2).forward_steps(
         np64(x), pad_end=True)
     assert_close(np64(ys), r, tdt, "persistent pool steps", terms=window_terms(ks))
     po2, po3 = make(), make()
     seq = [po2.forward_step(xd[:, :, t].contiguous()) for t in range(x.shape[2])]
     seq = [s_.clone() for s_ in seq if s_ is not None]
-    for t in range(2):
-        po3.forward_step(xd[:, :, t].contiguous())
+    heads = [po3.forward_step(xd[:, :, t].contiguous()) for t in range(2)]
     mid = po3.forward_steps(xd[:, :, 2:8].contiguous())
     tail = [po3.forward_step(xd[:, :, t].contiguous()) for t in range(8, x.shape[2])]
     got = ([mid[:, :, k] for k in range(mid.shape[2])] if mid is not None else []) + \
         [t_ for t_ in tail if t_ is not None]
-    n_first = sum(1 for t in range(2) if t >= po3.delay)
+    n_first = sum(1 for h_ in heads if h_ is not None)  # (a temporal stride skips steps)
     assert len(got) == len(seq) - n_first
     for g_, s_ in zip(got, seq[n_first:]):
         assert torch.equal(g_, s_)
