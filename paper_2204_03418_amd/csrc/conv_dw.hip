@@ -439,29 +439,17 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwp_kernel(
 // Temporal stride or dilation above 1 (Principle 5): which output a tap
 // feeds, and whether it starts, continues or completes it, now depends on the
 // frame.  The kernel follows the host's step plans (the ones the per-frame
-// step launches take), packed per frame as 6 bits a tap: action (3 bits, the
-// CO_TAP_ codes) and ring slot (3 bits).  They are explicit for the call's
-// frames in a stream's first (kT - 1) dT steps, where start padding and
-// missing outputs matter, and periodic afterwards: from then on the plan of
-// step n + sT R equals that of step n (slots cycle with the output index
-// mod R).  Each lane keeps the R partial sums of its pixel in LDS, where a
+// step launches take, packed as a PlanTable).  Each lane keeps the R partial sums of its pixel in LDS, where a
 // slot chosen at run time costs no more than a fixed one; frames go through
 // zero-haloed LDS tiles as in the kernel above.  Per tap the arithmetic is
 // the step kernel's: from the ring value (ACC, EMIT) or zero, the 3x3 chain,
 // then back to the slot or out with the bias.
-constexpr int kDwgMaxR = 8;       // ring slots (3-bit slot field)
-constexpr int kDwgStart = 32;     // explicit plans: stream-start frames of a call
-constexpr int kDwgPeriod = 64;    // periodic plans: sT R steps
-constexpr int kDwgU = 4;          // frames per group
+constexpr int kDwgU = 4;  // frames per group
 
 struct DwgArgs {
-  int32_t n_start;  // frames of the call that take explicit plans
-  int32_t period;   // sT * R
-  int32_t ph0;      // phase of frame n_start in the periodic table
-  int32_t PW;       // padded tile width
+  PlanTable pt;
+  int32_t PW;  // padded tile width
   int32_t frame_bytes;
-  int32_t code_start[kDwgStart];
-  int32_t code_period[kDwgPeriod];
 };
 
 template <typename T, int KH, int KW, int KT>
@@ -473,7 +461,7 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwg_kernel(
   constexpr int U = kDwgU;
   constexpr uint32_t esz = sizeof(T);
   __shared__ float lds[kDwpWaves][U][kDwpSlot];
-  __shared__ float parts[kDwpWaves][kDwgMaxR][64];
+  __shared__ float parts[kDwpWaves][kPlanMaxR][64];
   const int lane = int(threadIdx.x) & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
   const int bc = int(blockIdx.x) * kDwpWaves + wave;
@@ -522,14 +510,14 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwg_kernel(
     return load_raw_at<T>(xr, real ? xin : kOutOfRange, real ? t * ga.frame_bytes : 0);
   };
   int k = 0;          // outputs emitted so far in the call
-  int ph = ga.ph0;    // phase of the next periodic frame
+  int ph = 0;         // phase of the next periodic frame
   auto eval = [&](int t, int u) {
-    int code;
-    if (t < ga.n_start) {
-      code = ga.code_start[t];
+    uint64_t code;
+    if (t < ga.pt.n_start) {
+      code = ga.pt.code_start[t];
     } else {
-      code = ga.code_period[ph];
-      ph = ph + 1 == ga.period ? 0 : ph + 1;
+      code = ga.pt.code_period[ph];
+      ph = ph + 1 == ga.pt.period ? 0 : ph + 1;
     }
     float xv[NS];
 #pragma unroll
@@ -537,7 +525,7 @@ __global__ __launch_bounds__(64 * kDwpWaves) void conv_steps_dwg_kernel(
     bool emitted = false;
 #pragma unroll
     for (int j = KT - 1; j >= 0; --j) {
-      const int act = (code >> (6 * j)) & 7, slot = (code >> (6 * j + 3)) & 7;
+      const int act = int(code >> (6 * j)) & 7, slot = int(code >> (6 * j + 3)) & 7;
       if (act == CO_TAP_NONE) continue;  // uniform
       float a = (act == CO_TAP_ACC || act == CO_TAP_EMIT) ? pp[slot * 64] : 0.f;
 #pragma unroll
@@ -605,25 +593,9 @@ hipError_t dw_steps_launch(const ConvGeom& g, const ConvLayout& L, char* state, 
     // step plans: explicit for the call's frames in the stream's first
     // (kT - 1) dT steps, then one period of sT R steps
     DwgArgs ga{};
-    const int64_t n_steady = int64_t(g.kT - 1) * g.dT;
-    ga.n_start = int32_t(std::max<int64_t>(0, std::min<int64_t>(count, n_steady - n0)));
-    ga.period = g.sT * g.R;
+    plan_table(g, n0, count, &ga.pt);
     ga.PW = g.W + 2 * g.pW;
     ga.frame_bytes = int32_t(fbytes);
-    auto pack = [&](int64_t n) {
-      co_step_plan plan;
-      conv_plan(g, n, true, &plan);
-      int32_t code = 0;
-      for (int j = 0; j < g.kT; ++j)
-        code |= (int32_t(plan.action[j]) | (std::max(plan.slot[j], 0) << 3)) << (6 * j);
-      return code;
-    };
-    for (int t = 0; t < ga.n_start; ++t) ga.code_start[t] = pack(n0 + t);
-    // the periodic table starts at the first steady step of the call
-    const int64_t n_first = n0 + ga.n_start;
-    for (int q = 0; q < ga.period; ++q) ga.code_period[q] = pack(n_first + q);
-    ga.ph0 = 0;
-    // output frame of the call's first emission: emissions go out in order
     hipLaunchKernelGGL((conv_steps_dwg_kernel<T, KH, KW, KT>),
                        dim3(unsigned((int64_t(g.B) * g.Cout + kDwpWaves - 1) / kDwpWaves)),
                        dim3(64 * kDwpWaves), 0, s, g, ds, ga, static_cast<const T*>(x), x_bc,
@@ -703,8 +675,7 @@ bool dw_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
                     int64_t(g.B) * g.Cout * y_frames * g.So() * esz < (int64_t(1) << 31);
   // temporal stride or dilation above 1: the plan-driven small-plane kernel
   const bool strided = g.sT != 1 || g.dT != 1;
-  const bool general = dwp_fits(g) && g.R <= kDwgMaxR && int64_t(g.sT) * g.R <= kDwgPeriod &&
-                       int64_t(g.kT - 1) * g.dT <= kDwgStart;
+  const bool general = dwp_fits(g) && plan_table_fits(g);
   return g.algo == CO_ALGO_DEPTHWISE && (!strided || general) && g.kT >= 1 && g.kT <= 5 &&
          ((g.kH == 3 && g.kW == 3) || (g.kH == 1 && g.kW == 1)) && fits;
 }

@@ -918,6 +918,248 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   }
 }
 
+// Temporal stride or dilation above 1 (Principle 5) on the staged 1x1
+// shapes.  Which output a tap feeds, and whether it starts, continues or
+// completes it, depends on the frame, so the frame loop follows the host's
+// step plans (a PlanTable: explicit for a stream's first frames, periodic
+// after).  A lane's R partial sums (four output channels of one pixel) sit
+// in LDS and are addressed by the plan's slot; per tap the arithmetic is the
+// step kernel's: the matrix chain accumulates onto the slot (ACC, EMIT) or
+// zero (START, EMIT_FRESH), and the sum goes back to the slot or out with the
+// bias.  The ring's R slots are read once and written back once, stale ones
+// included.  Time segments start rp.warm frames early, enough for every
+// output they store to take all its taps inside the segment and for every
+// slot to start afresh inside the last one.
+struct RegPlan {
+  PlanTable pt;
+  int32_t warm;  // warm-up frames of a segment after the first
+  int32_t t_e0;  // first emitting frame of the call (count if none)
+};
+
+template <typename T, int CSMAX, int KTM>
+__global__ __launch_bounds__(64 * kRegStgWaves)
+void conv_steps_regp_kernel(ConvGeom g, RegSteps rs, RegPlan rp, const T* __restrict__ x,
+                            int64_t x_bc, T* __restrict__ y, const uint4* __restrict__ wp,
+                            const float* __restrict__ bias, float* __restrict__ ring) {
+  constexpr bool kBF = sizeof(T) == 2;
+  constexpr int CL = kBF ? 8 : 1;
+  constexpr int CKS = 4 * CL;
+  constexpr int CSUMAX = kBF ? CSMAX : (CSMAX + 3) / 4;
+  constexpr uint32_t esz = sizeof(T);
+  using AReg = typename std::conditional<kBF, uint4, float>::type;
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  const int lrow = lane & 15, lgrp = lane >> 4;
+  const int bid = int(blockIdx.x);
+  int lb = (bid & 7) * rs.blocks_per_xcd + (bid >> 3);
+  const int seg = lb / rs.wgs;
+  if (seg >= rs.nseg) return;  // whole workgroups
+  lb -= seg * rs.wgs;
+  if (lb >= rs.m_frags * rs.o_groups) return;
+  const int s0 = seg * rs.seg_len, s1 = min(rs.count, s0 + rs.seg_len);
+  const int tw = seg == 0 ? 0 : s0 - rp.warm;
+  const int mf = fdiv(lb, rs.fd_og);
+  const int of = (lb - mf * rs.o_groups) * kRegStgWaves + wave;
+  const int kT = g.kT;
+
+  // ---- weights, as in the kernel above (one spatial tap)
+  const int o = of * 16 + lrow;
+  const bool ocol = o < g.Cout;
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(wp, rs.w_bytes);
+  uint4 wreg[KTM][CSUMAX];
+#pragma unroll
+  for (int j = 0; j < KTM; ++j) {
+    const int n = j * g.Cout + o;
+    const int nf = n >> 4, r = n & 15;
+#pragma unroll
+    for (int cq = 0; cq < CSUMAX; ++cq) {
+      const bool ok = ocol & (j < kT) & (cq < rs.CSU);
+      const int off = ((nf * rs.CSU + cq) << 10) + (lgrp * 16 + r) * 16;
+      const auto w4 = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? off : kOutOfRange, 0, 0);
+      wreg[j][cq] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    }
+  }
+  // ---- outputs of this lane: channels oc + r of pixel Po
+  const int oc = of * 16 + lgrp * 4;
+  const int Po = mf * 16 + lrow;
+  const __amdgpu_buffer_rsrc_t br = make_rsrc(bias, g.Cout * 4);
+  float bo[4];
+  int yoff[4], roff[4];
+  {
+    const bool pok = Po < rs.M;
+    const int b = fdiv(pok ? Po : 0, rs.fd_So), p = (pok ? Po : 0) - b * rs.So;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int orow = oc + r;
+      const bool ok = pok & (orow < g.Cout);
+      bo[r] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(br, orow < g.Cout ? orow * 4 : kOutOfRange, 0, 0));
+      yoff[r] = ok ? int((uint32_t(b * g.Cout + orow) * uint32_t(rs.y_bc) + uint32_t(p)) * esz)
+                   : kOutOfRange;
+      roff[r] = ok ? orow * rs.M + Po : -1;
+    }
+  }
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(y, rs.y_bytes);
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(ring, rs.ring_bytes);
+
+  // ---- partial sums: slot q of this lane at pp[q * 64]
+  __shared__ v4f parts[kRegStgWaves][kPlanMaxR][64];
+  v4f* const pp = &parts[wave][0][lane];
+  if (seg == 0) {
+    for (int q = 0; q < g.R; ++q) {
+      v4f a;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        a[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+            rr, roff[r] >= 0 ? (q * rs.ring_slot + roff[r]) * 4 : kOutOfRange, 0, 0));
+      pp[q * 64] = a;
+    }
+  }
+
+  // ---- staging: each frame's 16-pixel tile, channels-last in LDS, double
+  // buffered, as in the kernel above
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, rs.x_bytes);
+  const uint32_t plane_b = uint32_t(x_bc) * esz;
+  constexpr int SCH = CSMAX * CKS;
+  constexpr int SQ = (SCH / 4 + 15) / 16;
+  constexpr int PU = SCH * int(esz) / 16 + 1;
+  constexpr int SPF = SQ <= 2 ? 4 : 2;  // frames in flight
+  __shared__ uint4 stg[2][16 * PU];
+  uint32_t sraw[SPF][SQ][4];
+  const int tid = int(threadIdx.x);
+  const int spx = tid & 15, sq0 = tid >> 4;
+  const int Ps = mf * 16 + spx;
+  const bool ps_ok = Ps < rs.M;
+  const int sb = fdiv(ps_ok ? Ps : 0, rs.fd_So), sp = (ps_ok ? Ps : 0) - sb * rs.So;
+  const uint32_t s_base = uint32_t(sb) * uint32_t(g.Cin) * plane_b + uint32_t(sp) * esz;
+  auto load_stage = [&](int t, uint32_t (&a)[SQ][4]) {
+    const bool real = t < rs.T;  // uniform
+    const int fo = real ? t * rs.fstride : 0;
+#pragma unroll
+    for (int k = 0; k < SQ; ++k) {
+      const int qd = sq0 + 16 * k;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * qd + e;
+        const bool ok = real & ps_ok & (c < g.Cin);
+        a[k][e] = load_raw_at<T>(xr, ok ? int(s_base + uint32_t(c) * plane_b) : kOutOfRange, fo);
+      }
+    }
+  };
+  auto write_stage = [&](int buf, const uint32_t (&a)[SQ][4]) {
+    uint4* row = &stg[buf][spx * PU];
+#pragma unroll
+    for (int k = 0; k < SQ; ++k) {
+      const int qd = sq0 + 16 * k;
+      if ((SCH / 4) % 16 == 0 || qd < SCH / 4) {
+        if constexpr (kBF)
+          reinterpret_cast<uint2*>(row)[qd] =
+              make_uint2(a[k][0] | (a[k][1] << 16), a[k][2] | (a[k][3] << 16));
+        else
+          row[qd] = make_uint4(a[k][0], a[k][1], a[k][2], a[k][3]);
+      }
+    }
+  };
+  auto staged_operand = [&](int buf, int cb) -> AReg {
+    const uint4* row = &stg[buf][lrow * PU];
+    if constexpr (kBF)
+      return row[cb * 4 + lgrp];
+    else
+      return reinterpret_cast<const float*>(row)[cb * 4 + lgrp];
+  };
+  AReg aq[CSMAX];
+#pragma unroll
+  for (int u = 0; u < SPF; ++u) {
+    load_stage(tw + u, sraw[u]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  write_stage(tw & 1, sraw[0]);
+  load_stage(tw + SPF, sraw[0]);
+  __syncthreads();
+#pragma unroll
+  for (int cb = 0; cb < CSMAX; ++cb) aq[cb] = staged_operand(tw & 1, cb);
+
+  // plan position and emission count at frame tw
+  int ph = tw > rp.pt.n_start ? (tw - rp.pt.n_start) % rp.pt.period : 0;
+  int k = tw > rp.t_e0 ? (tw - rp.t_e0 + g.sT - 1) / g.sT : 0;
+  uint32_t touched = 0;  // slots written in this segment (uniform)
+  auto frame = [&](int t, int u) {
+    const bool dead = t >= s1;  // workgroup-uniform
+    uint64_t code = 0;
+    if (!dead) {
+      if (t < rp.pt.n_start) {
+        code = rp.pt.code_start[t];
+      } else {
+        code = rp.pt.code_period[ph];
+        ph = ph + 1 == rp.pt.period ? 0 : ph + 1;
+      }
+    }
+    const bool stores = t >= s0;  // (a segment's warm-up frames store nothing)
+    bool emitted = false;
+#pragma unroll
+    for (int j = 0; j < KTM; ++j) {
+      if (j >= kT) break;  // uniform
+      const int act = int(code >> (6 * j)) & 7, sl = int(code >> (6 * j + 3)) & 7;
+      if (act == CO_TAP_NONE) continue;  // uniform
+      v4f c = (act == CO_TAP_ACC || act == CO_TAP_EMIT) ? pp[sl * 64] : v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cb = 0; cb < CSMAX; ++cb) {
+        if constexpr (kBF) {
+          c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, wreg[j][cb]),
+                                                      __builtin_bit_cast(v8bf, aq[cb]), c, 0, 0, 0);
+        } else {
+          const uint4 u4 = wreg[j][cb / 4];
+          const uint32_t bw = (cb & 3) == 0 ? u4.x : (cb & 3) == 1 ? u4.y : (cb & 3) == 2 ? u4.z : u4.w;
+          c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bw), aq[cb], c, 0, 0, 0);
+        }
+      }
+      if (act == CO_TAP_EMIT || act == CO_TAP_EMIT_FRESH) {
+        const int fo = stores ? k * rs.So * int(esz) : 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float val = c[r] + bo[r];
+          const int yo = stores ? yoff[r] : kOutOfRange;
+          if constexpr (kBF)
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, __bf16(val)), yr,
+                                                  yo, fo, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), yr, yo, fo, 0);
+        }
+        emitted = true;
+      } else {
+        pp[sl * 64] = c;
+        touched |= 1u << sl;
+      }
+    }
+    if (emitted) ++k;
+    // frame t + 1 into LDS (as in the kernel above)
+    const int un = (u + 1) % SPF;
+    write_stage((t + 1) & 1, sraw[un]);
+    load_stage(t + 1 + SPF, sraw[un]);
+    __syncthreads();
+#pragma unroll
+    for (int cb = 0; cb < CSMAX; ++cb) aq[cb] = staged_operand((t + 1) & 1, cb);
+  };
+  for (int t0 = tw; t0 < s1; t0 += SPF) {
+#pragma unroll
+    for (int u = 0; u < SPF; ++u) frame(t0 + u, u);
+  }
+
+  // (a later segment's untouched slots hold nothing it read: with kT = 1
+  // no slot is ever written, and otherwise every slot starts afresh in it)
+  if (rs.update && s1 == rs.count) {
+    for (int q = 0; q < g.R; ++q) {
+      if (seg != 0 && !((touched >> q) & 1)) continue;  // uniform
+      const v4f a = pp[q * 64];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        __builtin_amdgcn_raw_buffer_store_b32(
+            __float_as_uint(a[r]), rr, roff[r] >= 0 ? (q * rs.ring_slot + roff[r]) * 4 : kOutOfRange,
+            0, 0);
+    }
+  }
+}
+
 // Instantiations: (step-kernel shape id, largest kT).  Registers hold
 // kT x taps x channel blocks of weights, so deep temporal kernels go with
 // 1x1 spatial taps only.
@@ -992,6 +1234,31 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.nseg = int32_t(ceil_div(count, rs.seg_len));
   rs.wgs = int32_t(wgs);
   rs.blocks_per_xcd = int32_t(ceil_div(wgs * rs.nseg, 8));
+  if constexpr (STG) {
+    if (g.sT != 1 || g.dT != 1) {
+      // plan-driven: segments take max((kT - 1) dT, sT R) warm-up frames and
+      // hold at least four times as many
+      RegPlan rp;
+      plan_table(g, n0, count, &rp.pt);
+      rp.warm = std::max((g.kT - 1) * g.dT, g.sT * g.R);
+      const int64_t te = n0 >= g.d ? (g.sT - (n0 - g.d) % g.sT) % g.sT : g.d - n0;
+      rp.t_e0 = int32_t(std::min<int64_t>(te, count));
+      // (every instantiation fits two waves per SIMD)
+      int64_t ns = (2 * kSimds) / std::max<int64_t>(wgs * kRegStgWaves, 1);
+      ns = std::min<int64_t>(ns, count / (4 * int64_t(rp.warm)));
+      ns = std::max<int64_t>(1, std::min<int64_t>(ns, 64));
+      rs.seg_len = int32_t(ceil_div(count, ns));
+      rs.nseg = int32_t(ceil_div(count, rs.seg_len));
+      rs.blocks_per_xcd = int32_t(ceil_div(wgs * rs.nseg, 8));
+      hipLaunchKernelGGL((conv_steps_regp_kernel<T, CSMAX, KTM>),
+                         dim3(unsigned(8 * rs.blocks_per_xcd)), dim3(64 * kRegStgWaves), 0, s, g,
+                         rs, rp, static_cast<const T*>(x), x_bc, static_cast<T*>(y),
+                         reinterpret_cast<const uint4*>(state + L.weight),
+                         reinterpret_cast<const float*>(state + L.bias),
+                         reinterpret_cast<float*>(state + L.ring));
+      return hipGetLastError();
+    }
+  }
   auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true, STG>
                           : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false, STG>;
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)),
@@ -1038,9 +1305,12 @@ hipError_t launch_conv_step_reg(const ConvGeom& g, const ConvLayout& L, char* st
 }
 
 bool reg_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
-  if (g.algo != CO_ALGO_GEMM_REG || g.sT != 1 || g.dT != 1 || reg_steps_ktm(g) == 0) return false;
+  if (g.algo != CO_ALGO_GEMM_REG || reg_steps_ktm(g) == 0) return false;
   RegConfig c;
   if (!reg_config(g, g.cfg, &c)) return false;
+  // temporal stride or dilation: the plan-driven kernel, staged 1x1 shapes
+  const bool staged = c.id == 0 || c.id == 1 || c.id == 5 || c.id == 6;
+  if ((g.sT != 1 || g.dT != 1) && !(staged && plan_table_fits(g))) return false;
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   const int64_t lim = int64_t(1) << 31;
   return int64_t(g.B) * g.Cin * x_frames * g.S() * esz < lim &&

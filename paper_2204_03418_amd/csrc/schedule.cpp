@@ -497,6 +497,29 @@ void conv_plan(const ConvGeom& g, int64_t n, bool update_state, co_step_plan* p)
   }
 }
 
+bool plan_table_fits(const ConvGeom& g) {
+  return g.kT >= 1 && g.kT <= 10 && g.R <= kPlanMaxR && int64_t(g.sT) * g.R <= kPlanPeriod &&
+         int64_t(g.kT - 1) * g.dT <= kPlanStart;
+}
+
+void plan_table(const ConvGeom& g, int64_t n0, int64_t count, PlanTable* t) {
+  auto pack = [&](int64_t n) {
+    co_step_plan plan;
+    conv_plan(g, n, true, &plan);
+    uint64_t code = 0;
+    for (int j = 0; j < g.kT; ++j)
+      code |= uint64_t(plan.action[j] | (std::max(plan.slot[j], 0) << 3)) << (6 * j);
+    return code;
+  };
+  std::memset(t, 0, sizeof(*t));
+  const int64_t n_steady = int64_t(g.kT - 1) * g.dT;
+  t->n_start = int32_t(std::max<int64_t>(0, std::min<int64_t>(count, n_steady - n0)));
+  t->period = g.sT * g.R;
+  for (int i = 0; i < t->n_start; ++i) t->code_start[i] = pack(n0 + i);
+  // the periodic table starts at the call's first steady frame
+  for (int q = 0; q < t->period; ++q) t->code_period[q] = pack(n0 + t->n_start + q);
+}
+
 int64_t conv_emissions(const ConvGeom& g, int64_t n, int64_t count) {
   // emissions at steps m with m >= d and (m - d) % sT == 0, m in [n, n + count)
   const int64_t lo = n > g.d ? n : g.d;

@@ -210,6 +210,27 @@ ConvLayout conv_layout(const ConvGeom& g);
 uint64_t conv_hash(const ConvGeom& g);
 // Tap plan of step n (see co_conv_plan_step).
 void conv_plan(const ConvGeom& g, int64_t n, bool update_state, co_step_plan* plan);
+
+// Step plans of a forward_steps call for the plan-driven persistent kernels
+// (temporal stride or dilation above 1), packed per frame as 6 bits a tap:
+// the CO_TAP_ action (3 bits) and the ring slot (3 bits).  Explicit for the
+// call's frames within a stream's first (kT - 1) dT steps, where start
+// padding and missing outputs matter; after those the plan of step n + sT R
+// equals that of step n (slots cycle with the output index mod R), so one
+// period covers the rest of the call.
+constexpr int kPlanStart = 32;   // explicit plans
+constexpr int kPlanPeriod = 64;  // periodic plans: sT R steps
+constexpr int kPlanMaxR = 8;     // ring slots a 3-bit field addresses
+struct PlanTable {
+  int32_t n_start;  // frames of the call that take explicit plans
+  int32_t period;   // sT * R
+  uint64_t code_start[kPlanStart];
+  uint64_t code_period[kPlanPeriod];
+};
+// Whether a layer's plans fit a PlanTable (kT <= 10 taps of 6 bits, R <= 8,
+// a period of at most kPlanPeriod steps).
+bool plan_table_fits(const ConvGeom& g);
+void plan_table(const ConvGeom& g, int64_t n0, int64_t count, PlanTable* t);
 // Number of non-empty outputs of steps n .. n + count - 1.
 int64_t conv_emissions(const ConvGeom& g, int64_t n, int64_t count);
 

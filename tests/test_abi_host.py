@@ -222,6 +222,56 @@ def test_conv_plan_update_state_false_keeps_only_completing_tap(k, s, dil, p):
                 assert b.action[j] == C.CO_TAP_NONE
 
 
+STRIDED_GRID = [g for g in PLAN_GRID if g[1] > 1 or g[2] > 1]
+
+
+@pytest.mark.parametrize("k,s,dil,p", STRIDED_GRID)
+def test_strided_plan_tables_and_segment_warmup(k, s, dil, p):
+    """The bookkeeping of the plan-driven persistent kernels (temporal stride
+    or dilation above 1), against the step plans themselves: (a) after a
+    stream's first (k - 1) dil steps the plan of step n + s R equals that
+    of step n, so explicit plans for a call's frames before that point plus
+    one period of s R plans cover any call; (b) a time segment that starts
+    max((k - 1) dil, s R) frames before its first stored frame, with every
+    ring slot unknown, completes every output it stores from slots it
+    started itself, and ends with every slot started inside it (k >= 2;
+    with k = 1 no slot is ever written), so the last segment's write-back
+    is the state stepping leaves; (c) the
+    emission count at a segment's first frame follows from the call's
+    first emitting frame."""
+    d = desc1d(k=k, s=s, p=p, d=dil)
+    R = C.conv_query(d).ring_slots
+    delay = C.conv_query(d).delay
+    period, warm = s * R, max((k - 1) * dil, s * R)
+
+    def key(n):
+        pl = C.conv_plan(d, n, True)
+        return tuple((pl.action[j], pl.slot[j]) for j in range(k)), bool(pl.emit)
+
+    for n0 in (0, 1, 5, 37):
+        count = 24 * warm
+        n_start = max(0, min(count, (k - 1) * dil - n0))
+        for t in range(n_start, count):
+            assert key(n0 + t) == key(n0 + n_start + (t - n_start) % period), (n0, t)
+        emits = [t for t in range(count) if key(n0 + t)[1]]
+        t_e0 = (s - (n0 - delay) % s) % s if n0 >= delay else delay - n0
+        assert not emits or emits[0] == min(t_e0, count)
+        for s0 in range(4 * warm, count, 3):
+            tw = s0 - warm
+            before = sum(1 for t in emits if t < tw)
+            assert before == ((tw - t_e0 + s - 1) // s if tw > t_e0 else 0), (n0, s0)
+            known = [False] * R
+            for t in range(tw, count):
+                pl = C.conv_plan(d, n0 + t, True)
+                for j in range(k):
+                    a, sl = pl.action[j], pl.slot[j]
+                    if a == C.CO_TAP_START:
+                        known[sl] = True
+                    elif a == C.CO_TAP_EMIT and t >= s0:
+                        assert known[sl], (n0, s0, t, j)
+            assert all(known) if k > 1 else not any(known), (n0, s0)
+
+
 POOL_PLAN_GRID = [(k, s, dil, p) for k in (1, 2, 3, 4, 7) for s in (1, 2, 3) for dil in (1, 2)
                   for p in range(0, k // 2 + 1)]
 

@@ -553,9 +553,11 @@ def test_depthwise_forward_steps_persistent(case):
 def _check_fused_steps(make, x, ref, tdt, what):
     """forward_steps as one persistent launch: against the oracle with end
     padding; bitwise against per-frame forward_step (same per-tap arithmetic
-    order), also after clean_state (stale ring contents); a clip continuing a
-    state left by single steps and single steps continuing a clip; and
-    update_state=False (same outputs, state unchanged)."""
+    order), also after clean_state (stale ring contents); a clip from the
+    stream's start followed by single steps (the partial sums the clip
+    leaves are those stepping leaves), a clip continuing a state left by
+    single steps and single steps continuing a clip; and update_state=False
+    (same outputs, state unchanged)."""
     xd = x.to(DEV)
     T = x.shape[2]
     co = make()
@@ -570,16 +572,23 @@ def _check_fused_steps(make, x, ref, tdt, what):
     ys2 = co.forward_steps(xd)
     if outs:
         assert torch.equal(ys2, torch.stack(outs, dim=2)), what
+    co5 = make()
+    head = co5.forward_steps(xd[:, :, :T - 5].contiguous())
+    rest = [co5.forward_step(xd[:, :, t].contiguous()) for t in range(T - 5, T)]
+    got = ([head[:, :, i] for i in range(head.shape[2])] if head is not None else []) + \
+        [r_ for r_ in rest if r_ is not None]
+    assert len(got) == len(outs), what
+    for g_, s_ in zip(got, outs):
+        assert torch.equal(g_, s_), what
     co3, co4 = make(), make()
-    for t in range(3):
-        co3.forward_step(xd[:, :, t].contiguous())
+    heads = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(3)]
     mid = co3.forward_steps(xd[:, :, 3:9].contiguous())
     tail = [co3.forward_step(xd[:, :, t].contiguous()) for t in range(9, T)]
     seq = [co4.forward_step(xd[:, :, t].contiguous()) for t in range(T)]
     seq = [s_.clone() for s_ in seq if s_ is not None]
     got = ([mid[:, :, k] for k in range(mid.shape[2])] if mid is not None else []) + \
         [t_ for t_ in tail if t_ is not None]
-    n_first = sum(1 for t in range(3) if t >= co3.delay)
+    n_first = sum(1 for h_ in heads if h_ is not None)  # (a temporal stride skips steps)
     assert len(got) == len(seq) - n_first
     for g_, s_ in zip(got, seq[n_first:]):
         assert torch.equal(g_, s_), what
@@ -622,6 +631,44 @@ def test_reg_forward_steps_persistent(case):
     assert make().algo.startswith("gemm_reg")
     ones = (1,) * len(k)
     _check_fused_steps(make, x, oracle_conv(w, b, ones, p, ones, 1), tdt, "reg steps")
+
+
+REG_STRIDED_CASES = [
+    # B, C_in, C_out, kernel (time first), in_size, padding, dtype, frames, sT, dT
+    # (sizes chosen so that the picker lands on the staged 1x1 shapes)
+    (3, 40, 20, (3, 1), (13,), (1, 0), "f32", 14, 2, 1),             # temporal stride 2
+    (32, 96, 128, (9, 1), (25,), (4, 0), "bf16", 14, 2, 1),          # skeleton-style, kT = 9
+    (32, 64, 256, (3, 1), (25,), (2, 0), "bf16", 13, 1, 2),          # temporal dilation 2
+    (2, 40, 32, (3, 1), (9,), (0, 0), "f32", 15, 3, 2),              # stride 3, dilation 2
+    (2, 100, 72, (2, 1), (11,), (1, 0), "f32", 12, 2, 3),            # 32-channel-block shape
+    (3, 40, 20, (3, 1), (13,), (1, 0), "f32", 64, 2, 1),             # long clip: time segments
+    (32, 64, 256, (3, 1), (25,), (1, 0), "bf16", 64, 2, 1),          # segments, bf16
+]
+
+
+@pytest.mark.parametrize("case", REG_STRIDED_CASES, ids=lambda c: "regstrided_" + "_".join(
+    map(str, c[:3])) + f"_{c[6]}_T{c[7]}_s{c[8]}d{c[9]}")
+def test_reg_forward_steps_strided(case):
+    """Temporal stride or dilation above 1 on the register GEMM's 1x1
+    spatial shapes: forward_steps as one plan-driven persistent launch
+    (partial sums in LDS slots, the host's step plans); the long clip is
+    split into time segments, so the clip-then-steps check covers the last
+    segment's write-back of the ring."""
+    B, cin, cout, k, size, p, dt, T, sT, dT = case
+    st = (sT,) + (1,) * (len(k) - 1)
+    dil = (dT,) + (1,) * (len(k) - 1)
+    say("reg strided steps", case)
+    spec = synth.ConvSpec(batch=B, in_channels=cin, out_channels=cout, kernel=k, in_size=size,
+                          stride=st, padding=p, dilation=dil, dtype=dt)
+    x, w, b = synth.conv_inputs(spec, T, 98000 + 3 * cin + cout + T, "kaiming")
+
+    def make():
+        return coinf.CoConv(w.to(DEV), b.to(DEV), batch=B, in_size=size, stride=st, padding=p,
+                            dilation=dil, algo="gemm_reg")
+
+    assert make().algo.startswith("gemm_reg")
+    _check_fused_steps(make, x, oracle_conv(w, b, st, p, dil, 1), synth.torch_dtype(dt),
+                       "reg strided steps")
 
 
 DIRECT_STEPS_CASES = [
