@@ -477,11 +477,12 @@ struct RegSteps {
 };
 
 // Waves per SIMD an instantiation is compiled for: two where its registers
-// allow it without spilling (the bf16 1x1 shape with two channel blocks),
-// so that time segments can put two waves on every SIMD.
-template <typename T, int CSMAX, bool STG>
+// allow it without spilling (the bf16 1x1 shape with two channel blocks, in
+// its compile-time form: the runtime-kT form needs more), so that time
+// segments can put two waves on every SIMD.
+template <typename T, int CSMAX, bool STG, bool FULL>
 constexpr int reg_steps_wpe() {
-  return (STG && sizeof(T) == 2 && CSMAX == 2) ? 2 : 1;
+  return (STG && FULL && sizeof(T) == 2 && CSMAX == 2) ? 2 : 1;
 }
 
 // STG (1x1 spatial taps, one chain per tile): the kRegStgWaves waves of a
@@ -497,7 +498,8 @@ constexpr int kRegStgWaves = 4;
 
 template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL, bool STG>
 __global__ __launch_bounds__(64 * (STG ? kRegStgWaves : KSPLIT * kRegTiles))
-__attribute__((amdgpu_waves_per_eu(reg_steps_wpe<T, CSMAX, STG>(), reg_steps_wpe<T, CSMAX, STG>())))
+__attribute__((amdgpu_waves_per_eu(reg_steps_wpe<T, CSMAX, STG, FULL>(),
+                                    reg_steps_wpe<T, CSMAX, STG, FULL>())))
 void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
                            T* __restrict__ y, const uint4* __restrict__ wp,
                            const float* __restrict__ bias, float* __restrict__ ring) {
@@ -693,7 +695,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   // divisor of it, at most SPF0
   constexpr int FPG_S = KTM * ((SPF0 + KTM - 1) / KTM);
   constexpr int SPF = !STG                                  ? 1
-                      : reg_steps_wpe<T, CSMAX, STG>() == 1 ? FPG_S
+                      : reg_steps_wpe<T, CSMAX, STG, FULL>() == 1 ? FPG_S
                       : FPG_S % 4 == 0                      ? 4
                       : FPG_S % 3 == 0                      ? 3
                       : FPG_S % 2 == 0                      ? 2
@@ -1227,7 +1229,9 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   const int64_t wgs = STG ? int64_t(rs.m_frags) * rs.o_groups : blocks;
   const int64_t waves = wgs * (STG ? kRegStgWaves : KSPLIT * kRegTiles);
   constexpr int64_t kSimds = 1024;
-  int64_t nseg = (reg_steps_wpe<T, CSMAX, STG>() * kSimds) / std::max<int64_t>(waves, 1);
+  const int wpe = g.kT == KTM ? reg_steps_wpe<T, CSMAX, STG, true>()
+                              : reg_steps_wpe<T, CSMAX, STG, false>();
+  int64_t nseg = (wpe * kSimds) / std::max<int64_t>(waves, 1);
   if (g.kT > 1) nseg = std::min<int64_t>(nseg, count / (4 * (g.kT - 1)));
   nseg = std::max<int64_t>(1, std::min<int64_t>(nseg, 64));
   rs.seg_len = int32_t(ceil_div(count, nseg));
