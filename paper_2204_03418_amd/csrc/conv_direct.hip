@@ -238,10 +238,20 @@ constexpr int kDirStepsKT = 4;   // temporal taps held in registers
 // KX: reduction positions held (4, 8 or 16); PF: frames in flight (16, 8 or
 // 4, so a thread holds 64 raw inputs either way).  The loop is bound by the
 // latency of its frame loads, so a small layer keeps more frames in flight.
-template <typename T, int KX, int PF>
+//
+// PLAN (temporal stride or dilation above 1, Principle 5): which output a
+// tap feeds, and whether it starts, continues or completes it, depends on
+// the frame, so the loop follows the host's step plans (a PlanTable:
+// explicit for a stream's first frames, periodic after) and each thread
+// keeps its R partial sums in LDS, addressed by the plan's slot.  Per tap
+// the arithmetic is the step kernel's: the tap's product, added to the slot
+// (ACC, EMIT) or not (START, EMIT_FRESH), back to the slot or out with the
+// bias.  The ring's R slots are read once and written back once, stale ones
+// included.
+template <typename T, int KX, int PF, bool PLAN>
 __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
-    ConvGeom g, DirSteps ds, const T* __restrict__ x, int64_t x_bc, T* __restrict__ y,
-    int64_t y_bc, const float* __restrict__ w, const float* __restrict__ bias,
+    ConvGeom g, DirSteps ds, PlanTable pt, const T* __restrict__ x, int64_t x_bc,
+    T* __restrict__ y, int64_t y_bc, const float* __restrict__ w, const float* __restrict__ bias,
     float* __restrict__ ring, int64_t ring_slot) {
   constexpr int KTM = kDirStepsKT;
   constexpr uint32_t esz = sizeof(T);
@@ -282,12 +292,20 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
   const float bo_ = bias[o];
   const int R = g.R;
   float part[KTM];
+  __shared__ float pslot[PLAN ? kPlanMaxR : 1][PLAN ? kBlock : 1];
+  float* const pp = &pslot[0][PLAN ? threadIdx.x : 0];  // + slot * kBlock
+  if constexpr (PLAN) {
+    for (int q = 0; q < R; ++q) pp[q * kBlock] = ring[int64_t(q) * ring_slot + ridx];
+  } else {
 #pragma unroll
-  for (int j = 1; j < KTM; ++j) {
-    part[j] = 0.f;
-    const int tau = ds.v0 - j;
-    if (j < kT && tau >= 0) part[j] = ring[int64_t((ds.slot_v0 - j + R) % R) * ring_slot + ridx];
+    for (int j = 1; j < KTM; ++j) {
+      part[j] = 0.f;
+      const int tau = ds.v0 - j;
+      if (j < kT && tau >= 0) part[j] = ring[int64_t((ds.slot_v0 - j + R) % R) * ring_slot + ridx];
+    }
   }
+  int ph = 0;  // (PLAN) phase of the next periodic frame
+  int k = 0;   // (PLAN) outputs emitted so far in the call
 
   const int fstride = ds.fstride;
   auto load_frame = [&](int t, uint32_t (&xv)[KX]) {
@@ -318,6 +336,35 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
 #pragma unroll
         for (int j = 0; j < KTM; ++j) cj[j] = fmaf(wr[e][j], raw_to_f32<T>(xq[u][e]), cj[j]);
       load_frame(t + PF, xq[u]);
+      if constexpr (PLAN) {
+        uint64_t code;
+        if (t < pt.n_start) {
+          code = pt.code_start[t];
+        } else {
+          code = pt.code_period[ph];
+          ph = ph + 1 == pt.period ? 0 : ph + 1;
+        }
+        float yv = 0.f;
+        bool emitted = false;
+#pragma unroll
+        for (int j = 0; j < KTM; ++j) {
+          if (j >= kT) break;  // uniform
+          const int act = int(code >> (6 * j)) & 7, sl = int(code >> (6 * j + 3)) & 7;
+          if (act == CO_TAP_NONE) continue;  // uniform
+          const bool with = act == CO_TAP_ACC || act == CO_TAP_EMIT;
+          const float a = with ? pp[sl * kBlock] + cj[j] : cj[j];
+          if (act == CO_TAP_EMIT || act == CO_TAP_EMIT_FRESH) {
+            yv = a;
+            emitted = true;
+          } else {
+            pp[sl * kBlock] = a;
+          }
+        }
+        store_at(yr, emitted ? yoff : kOutOfRange, emitted ? k * So * int32_t(esz) : 0,
+                 from_f32<T>(yv + bo_));
+        if (emitted) ++k;
+        continue;
+      }
       // fold each tap's product into its output without a branch: a missing
       // output (tau < 0) or an unused tap only selects zero, and the one
       // store is always issued, to the out-of-range offset unless tap kT - 1
@@ -340,7 +387,9 @@ __global__ __launch_bounds__(kBlock) void conv_steps_direct_kernel(
       for (int j = KTM - 1; j >= 1; --j) part[j] = nxt[j - 1];
     }
   }
-  if (ds.update) {
+  if (PLAN && ds.update) {
+    for (int q = 0; q < R; ++q) ring[int64_t(q) * ring_slot + ridx] = pp[q * kBlock];
+  } else if (ds.update) {
     const int v1 = ds.v0 + ds.count;
     const int s1 = (ds.slot_v0 + ds.count) % R;
 #pragma unroll
@@ -371,11 +420,19 @@ hipError_t direct_steps_t(const ConvGeom& g, const ConvLayout& L, char* state, c
   ds.fd_Cout = make_fastdiv(uint32_t(g.Cout));
   ds.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   const int64_t nk = int64_t(g.Cg) * g.kH * g.kW;
-  auto kern = nk <= 4   ? conv_steps_direct_kernel<T, 4, 16>
-              : nk <= 8 ? conv_steps_direct_kernel<T, 8, 8>
-                        : conv_steps_direct_kernel<T, kDirStepsKX, 4>;
+  const bool plan = g.sT != 1 || g.dT != 1;
+  PlanTable pt{};
+  if (plan) plan_table(g, n0, count, &pt);
+  // (the plan-driven frame body is larger: 16 frames in flight would not
+  // unroll, and a frame register indexed at run time goes to scratch)
+  auto kern = plan ? (nk <= 4   ? conv_steps_direct_kernel<T, 4, 8, true>
+                      : nk <= 8 ? conv_steps_direct_kernel<T, 8, 8, true>
+                                : conv_steps_direct_kernel<T, kDirStepsKX, 4, true>)
+                   : (nk <= 4   ? conv_steps_direct_kernel<T, 4, 16, false>
+                      : nk <= 8 ? conv_steps_direct_kernel<T, 8, 8, false>
+                                : conv_steps_direct_kernel<T, kDirStepsKX, 4, false>);
   hipLaunchKernelGGL(kern, dim3(grid_for(g.out_frame_elems())),
-                     dim3(kBlock), 0, s, g, ds, static_cast<const T*>(x), x_bc,
+                     dim3(kBlock), 0, s, g, ds, pt, static_cast<const T*>(x), x_bc,
                      static_cast<T*>(y), y_bc, reinterpret_cast<const float*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
                      reinterpret_cast<float*>(state + L.ring), L.ring_slot_elems);
@@ -470,7 +527,9 @@ hipError_t launch_conv_step_staged(const ConvGeom& g, const ConvLayout& L, char*
 
 bool direct_steps_supported(const ConvGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
-  return g.algo == CO_ALGO_DIRECT && g.sT == 1 && g.dT == 1 && g.kT <= kDirStepsKT &&
+  // temporal stride or dilation: the plan-driven form (R <= 8 slots)
+  return g.algo == CO_ALGO_DIRECT && ((g.sT == 1 && g.dT == 1) || plan_table_fits(g)) &&
+         g.kT <= kDirStepsKT &&
          int64_t(g.Cg) * g.kH * g.kW <= kDirStepsKX &&
          int64_t(g.B) * g.Cin * x_frames * g.S() * esz < (int64_t(1) << 31) &&
          int64_t(g.B) * g.Cout * y_frames * g.So() * esz < (int64_t(1) << 31);

@@ -186,6 +186,8 @@ struct PoolSteps {
   int32_t count;  // frames: T real, then end padding
   int32_t T;
   int64_t emit0;  // first emitting step of the call: max(n0, d)
+  int32_t sT;     // temporal stride: steps from n = d on emit every sT
+  int32_t t_e0;   // first emitting frame of the call (count if none)
   int32_t update;
   int32_t x_bytes;  // bytes of the clip reachable from x
   int32_t y_bytes;  // bytes of the output clip
@@ -273,7 +275,11 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
     __builtin_amdgcn_sched_barrier(0);  // in frame order
   }
   // whole groups of PF frames with no exit inside: frames past the call
-  // (the last group's tail) store nothing and leave the window as it is
+  // (the last group's tail) store nothing and leave the window as it is.
+  // With a temporal stride the window is still the last kT frames; only
+  // every sT-th step from the first emitting one emits (ep: its phase, ko:
+  // the outputs so far).
+  int ep = 0, ko = 0;
   for (int t0 = 0; t0 < ps.count; t0 += PF) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
@@ -331,9 +337,12 @@ __global__ __launch_bounds__(kBlock) void pool_steps_kernel(
           const float div = g.count_include_pad ? float(KT * kHW) : tcount * float(vh * vw);
           out = div > 0.f ? acc / div : 0.f;
         }
-        const bool emits = (n >= g.d) & !dead;  // uniform
+        const bool on = (t >= ps.t_e0) & !dead;  // uniform
+        const bool emits = on & (ep == 0);
         store_at(yr, (emits && r == 0) ? yoff : kOutOfRange,
-                 emits ? int((n - ps.emit0) * So * int64_t(sizeof(T))) : 0, from_f32<T>(out));
+                 emits ? int(int64_t(ko) * So * int64_t(sizeof(T))) : 0, from_f32<T>(out));
+        ko += emits ? 1 : 0;
+        ep = on ? (ep + 1 == ps.sT ? 0 : ep + 1) : ep;
       }
       // (a dead frame's value went into the last place only, which the next
       // frame overwrites; the call ends after the group anyway)
@@ -656,6 +665,11 @@ hipError_t pool_steps_launch(const PoolGeom& g, const PoolLayout& L, char* state
   ps.count = count;
   ps.T = nreal;
   ps.emit0 = n0 > g.d ? n0 : g.d;
+  ps.sT = g.sT;
+  {
+    const int64_t te = n0 >= g.d ? (g.sT - (n0 - g.d) % g.sT) % g.sT : g.d - n0;
+    ps.t_e0 = int32_t(std::min<int64_t>(te, count));
+  }
   ps.update = update ? 1 : 0;
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   ps.x_bytes = int32_t(((int64_t(g.B) * g.C - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
@@ -689,11 +703,12 @@ template <typename T, int KT>
 hipError_t pool_global_launch(const PoolGeom& g, const PoolLayout& L, char* state, const void* x,
                               int64_t x_bc, int32_t nreal, int32_t count, void* y, int64_t y_bc,
                               int64_t n0, bool update, hipStream_t s) {
-  PoolSteps ps;
+  PoolSteps ps{};  // (the emission fields go in pa)
   ps.n0 = n0;
   ps.count = count;
   ps.T = nreal;
   ps.emit0 = n0 > g.d ? n0 : g.d;
+  ps.sT = g.sT;
   ps.update = update ? 1 : 0;
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   ps.x_bytes = int32_t(((int64_t(g.B) * g.C - 1) * x_bc + int64_t(nreal) * g.S()) * esz);
@@ -755,9 +770,10 @@ hipError_t launch_pool_valid(float* valid, int32_t R, int64_t n0, int32_t count,
 bool pool_steps_supported(const PoolGeom& g, int64_t x_frames, int64_t y_frames) {
   const int64_t esz = g.dtype == CO_BF16 ? 2 : 4;
   // temporal stride or dilation above 1: the frames-in-lanes global pool,
-  // whose window reaches (kT - 1) dT lanes back across one block
+  // whose window reaches (kT - 1) dT lanes back across one block; the lane
+  // group kernel, whose window is the last kT frames, takes a stride alone
   const bool strided = g.sT != 1 || g.dT != 1;
-  const bool general = pool_global_fits(g) && int64_t(g.kT - 1) * g.dT < kPgFrames;
+  const bool general = pool_global_fits(g) ? int64_t(g.kT - 1) * g.dT < kPgFrames : g.dT == 1;
   return (!strided || general) && g.kT >= 1 && g.kT <= 5 && g.kH * g.kW <= 64 &&  // (kT <= 8: tree)
          int64_t(g.B) * g.C * x_frames * g.S() * esz < (int64_t(1) << 31) &&
          int64_t(g.B) * g.C * y_frames * g.So() * esz < (int64_t(1) << 31);

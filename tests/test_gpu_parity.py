@@ -679,11 +679,16 @@ DIRECT_STEPS_CASES = [
     (3, 4, 4, 2, (4, 2, 2), (5, 6), (1, 1, 1), (3, 0, 1), (1, 1, 1), "f32"),  # kT = 4, delay 0
     (2, 16, 5, 1, (1, 1, 1), (4, 4), (1, 1, 1), (0, 0, 0), (1, 1, 1), "f32"),  # 16 positions, kT = 1
     (2, 1, 4, 1, (3, 3, 3), (9, 8), (1, 2, 1), (1, 1, 0), (1, 1, 2), "f32"),  # spatial stride, dilation
+    # temporal stride / dilation (plan-driven form)
+    (1, 4, 8, 1, (3,), (), (2,), (1,), (1,), "f32"),                       # 1-D, stride 2
+    (2, 6, 9, 3, (2, 3), (7,), (1, 1), (1, 1), (2, 1), "bf16"),            # grouped, dilation 2
+    (3, 4, 4, 2, (4, 2, 2), (5, 6), (3, 1, 1), (3, 0, 1), (1, 1, 1), "f32"),  # stride 3, kT = 4
+    (2, 16, 5, 1, (3, 1, 1), (4, 4), (2, 1, 1), (2, 0, 0), (2, 1, 1), "f32"),  # stride and dilation 2
 ]
 
 
 @pytest.mark.parametrize("case", DIRECT_STEPS_CASES, ids=lambda c: "dirsteps_" + "_".join(
-    map(str, c[:4])) + "_" + c[9])
+    map(str, c[:4])) + "_" + c[9] + f"_s{c[6][0]}d{c[8][0]}")
 def test_direct_forward_steps_persistent(case):
     """The direct family's forward_steps as one persistent launch (small
     layers: weights, partial sums and prefetched inputs in registers)."""
@@ -837,6 +842,10 @@ POOL_STEPS_CASES = [
     ("avg", (4, 6, 6), (6, 6), (3, 1, 1), (2, 0, 0), False, "f32", 45, 1),
     ("max", (3, 5, 5), (5, 5), (1, 5, 5), (1, 0, 0), True, "bf16", 50, 3),
     ("max", (2, 7, 7), (7, 7), (2, 7, 7), (0, 0, 0), True, "bf16", 70, 4),
+    # temporal stride on the lane-group pool (windows smaller than the frame)
+    ("max", (3, 3, 3), (8, 8), (2, 2, 2), (1, 1, 1), True, "bf16", 21, 1),
+    ("avg", (2, 3, 2), (7, 6), (3, 2, 1), (1, 1, 0), False, "f32", 26, 1),
+    ("avg", (5, 2, 2), (4, 4), (2, 2, 2), (2, 0, 0), True, "bf16", 30, 1),
 ]
 
 
