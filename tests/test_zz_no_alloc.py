@@ -118,23 +118,27 @@ def test_noalloc_rejects_calls_beyond_the_scratch():
     CO_ESCRATCH, nothing enqueued, the handle unchanged."""
     cap = coinf.i64()
     assert coinf.co_conv_scratch_bytes(ctypes.byref(cap)) == coinf.CO_OK
-    # ring: 2 slots x 4096 channels x 8192 positions x 4 B = 256 MiB > 64 MiB
-    spec = synth.ConvSpec(batch=1, in_channels=1, out_channels=4096, kernel=(3, 1),
-                          in_size=(8192,), stride=(2, 1), dtype="f32")
+    # temporal dilation 4 with kT = 3: nine ring slots, beyond the persistent
+    # kernels' plan tables, so the call loops over step launches; ring:
+    # 9 slots x 2048 channels x 4096 positions x 4 B = 288 MiB > 64 MiB
+    spec = synth.ConvSpec(batch=1, in_channels=1, out_channels=2048, kernel=(3, 1),
+                          in_size=(4096,), dilation=(4, 1), dtype="f32")
     say("noalloc rejection case")
     co, x, _, _ = _layer(spec, "direct", seed=7200)
-    assert co.info.ring_slots * 4096 * 8192 * 4 > cap.value
-    xd = x[:, :, :4].contiguous().to(DEV)
-    y = torch.empty((1, 4096, 4, 8192), dtype=torch.float32, device=DEV)
+    assert co.info.ring_slots == 9 and not co.steps_fused(10)
+    assert co.info.ring_slots * 2048 * 4096 * 4 > cap.value
+    xd = x[:, :, :10].contiguous().to(DEV)
+    y = torch.empty((1, 2048, 10, 4096), dtype=torch.float32, device=DEV)
     n = coinf.i32(-7)
     st = coinf.co_conv_forward_steps_noalloc(
-        co.handle, ctypes.c_void_p(xd.data_ptr()), 4, ctypes.c_void_p(y.data_ptr()), 4, 0, 0,
+        co.handle, ctypes.c_void_p(xd.data_ptr()), 10, ctypes.c_void_p(y.data_ptr()), 10, 0, 0,
         ctypes.c_void_p(torch.cuda.current_stream().cuda_stream), ctypes.byref(n))
     assert st == coinf.CO_ESCRATCH, coinf.co_status_str(st)
     assert n.value == -7 and co.steps == 0
-    # with update_state = 1 no backup is needed: the same call runs
+    # with update_state = 1 no backup is needed: the same call runs (delay 8:
+    # steps 8 and 9 emit)
     st = coinf.co_conv_forward_steps_noalloc(
-        co.handle, ctypes.c_void_p(xd.data_ptr()), 4, ctypes.c_void_p(y.data_ptr()), 4, 0, 1,
+        co.handle, ctypes.c_void_p(xd.data_ptr()), 10, ctypes.c_void_p(y.data_ptr()), 10, 0, 1,
         ctypes.c_void_p(torch.cuda.current_stream().cuda_stream), ctypes.byref(n))
     torch.cuda.synchronize()
-    assert st == coinf.CO_OK and n.value == 1 and co.steps == 4
+    assert st == coinf.CO_OK and n.value == 2 and co.steps == 10
