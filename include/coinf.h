@@ -284,9 +284,14 @@ co_status co_conv_scratch_bytes(int64_t* bytes);
 /*
  * How co_conv_forward_steps runs a call over T frames into y_cap_frames
  * output frames: *fused = 1 when the whole call is one persistent kernel
- * launch that keeps the partial sums on chip across frames (temporal stride
- * and dilation 1, on the depthwise and register-GEMM kernel families), 0 when
- * it enqueues one step per frame.  Both give the same outputs.  Host-only.
+ * launch that keeps the partial sums on chip across frames, 0 when it
+ * enqueues one step per frame.  Both give the same outputs, bit for bit.
+ * With temporal stride and dilation 1 the depthwise, direct, register-GEMM
+ * and bf16 GEMM families run fused within their kernels' size limits; with
+ * a temporal stride or dilation above 1 (Principle 5) the depthwise family
+ * on planes of at most 64 pixels, the direct family and the register GEMM's
+ * 1x1-spatial shapes do, following the step plans, when the ring has at most
+ * 8 slots, kT <= 10, sT R <= 64 and (kT - 1) dT <= 32.  Host-only.
  */
 co_status co_conv_steps_fused(const co_conv_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused);
@@ -446,7 +451,10 @@ co_status co_pool_forward_steps(co_pool_handle* h, const void* x, int32_t T, voi
                                 int32_t y_cap_frames, int32_t pad_end, int32_t update_state,
                                 void* stream, int32_t* n_out);
 
-/* As co_conv_steps_fused, for co_pool_forward_steps. */
+/* As co_conv_steps_fused, for co_pool_forward_steps: fused for kT <= 5
+ * and windows of at most 64 positions; with a temporal stride or dilation
+ * above 1, global spatial pools over frames of 17 to 64 positions with
+ * (kT - 1) dT < 32, and the other windows with a temporal stride alone. */
 co_status co_pool_steps_fused(const co_pool_handle* h, int32_t T, int32_t y_cap_frames,
                               int32_t* fused);
 
