@@ -469,7 +469,7 @@ struct RegSteps {
   int32_t v0;       // virtual time of the first frame, capped at 2^29
   int32_t slot_v0;  // v0 mod R (uncapped)
   int32_t count, T, k0, update;
-  int32_t o_groups;  // STG: workgroups per pixel fragment, ceil(o_frags / kRegStgWaves)
+  int32_t o_groups;  // STG: workgroups per pixel fragment, ceil(o_frags / staging waves)
   int32_t nseg;      // time segments of the call
   int32_t seg_len;   // frames per segment (the last may be shorter)
   int32_t wgs;       // workgroups per segment
@@ -485,9 +485,9 @@ constexpr int reg_steps_wpe() {
   return (STG && FULL && sizeof(T) == 2 && CSMAX == 2) ? 2 : 1;
 }
 
-// STG (1x1 spatial taps, one chain per tile): the kRegStgWaves waves of a
-// workgroup share one 16-pixel fragment and take consecutive 16-channel
-// output fragments.  Each frame's input tile (16 pixels x every input
+// STG (1x1 spatial taps, one chain per tile): the waves of a workgroup (4,
+// or 8 where two waves share a SIMD) share one 16-pixel fragment and take
+// consecutive 16-channel output fragments.  Each frame's input tile (16 pixels x every input
 // channel) is gathered once per workgroup -- four consecutive channels of one
 // pixel per thread -- and staged channels-last in LDS (double buffered, one
 // barrier per frame); each wave reads its operands from there with one
@@ -495,9 +495,16 @@ constexpr int reg_steps_wpe() {
 // wave gathered the same tile in 2-byte pieces, and the vector L1 stalled on
 // the requests.  The operands, and so the results, are the same.
 constexpr int kRegStgWaves = 4;
+// Staging waves of a stride-1 instantiation: eight where it runs two waves
+// per SIMD (a workgroup then fills both, and two workgroups instead of four
+// gather each pixel fragment's frames), else kRegStgWaves.
+template <typename T, int CSMAX, bool FULL>
+constexpr int reg_stg_waves() {
+  return reg_steps_wpe<T, CSMAX, true, FULL>() == 2 ? 2 * kRegStgWaves : kRegStgWaves;
+}
 
 template <typename T, int TAPS, int CSMAX, int KSPLIT, int KTM, bool FULL, bool STG>
-__global__ __launch_bounds__(64 * (STG ? kRegStgWaves : KSPLIT * kRegTiles))
+__global__ __launch_bounds__(64 * (STG ? reg_stg_waves<T, CSMAX, FULL>() : KSPLIT * kRegTiles))
 __attribute__((amdgpu_waves_per_eu(reg_steps_wpe<T, CSMAX, STG, FULL>(),
                                     reg_steps_wpe<T, CSMAX, STG, FULL>())))
 void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int64_t x_bc,
@@ -543,7 +550,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
     // every store masked (their channels are past C_out)
     if (lb >= rs.m_frags * rs.o_groups) return;  // whole workgroups
     mf = fdiv(lb, rs.fd_og);
-    of = (lb - mf * rs.o_groups) * kRegStgWaves + wave;
+    of = (lb - mf * rs.o_groups) * reg_stg_waves<T, CSMAX, FULL>() + wave;
     owner = true;
   } else {
     const int tile_raw = lb * TPW + wslot;
@@ -682,11 +689,16 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       return __uint_as_float(r[0]);
   };
 
-  // ---- staging (STG): thread (px, quad) gathers channels 4 (quad + 16 k)
-  // .. + 3 of pixel mf * 16 + px; out-of-range reads (pixels past M,
-  // channels past C_in, frames past the clip) return zero
+  // ---- staging (STG): thread (px, q) gathers channels CPT (q + TQ k) ..
+  // + CPT - 1 of pixel mf * 16 + px (TQ: the workgroup's threads over its 16
+  // pixels); out-of-range reads (pixels past M, channels past C_in, frames
+  // past the clip) return zero
   constexpr int SCH = CSMAX * CKS;            // staged channels (upper bound)
-  constexpr int SQ = (SCH / 4 + 15) / 16;     // channel quads per thread
+  constexpr int TQ = 4 * (STG ? reg_stg_waves<T, CSMAX, FULL>() : 1);  // unit slots
+  // channels per thread and unit: four, or two where four would leave threads
+  // without a unit (bf16: 64 channels over the 32 slots of eight waves)
+  constexpr int CPT = (kBF && SCH / 4 < TQ) ? 2 : 4;
+  constexpr int SQ = (SCH / CPT + TQ - 1) / TQ;  // units per thread
   constexpr int PU = SCH * int(esz) / 16 + 1;  // LDS row pitch, 16-byte units
   constexpr int SPF0 = SQ <= 2 ? 4 : 2;
   // frames per group: whole periods of the partial sums' rotation, so a
@@ -713,26 +725,28 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
     const int fo = real ? t * rs.fstride : 0;
 #pragma unroll
     for (int k = 0; k < SQ; ++k) {
-      const int qd = sq0 + 16 * k;
+      const int qd = sq0 + TQ * k;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int c = 4 * qd + e;
+      for (int e = 0; e < CPT; ++e) {
+        const int c = CPT * qd + e;
         const bool ok = real & ps_ok & (c < g.Cin);
         a[k][e] = load_raw_at<T>(xr, ok ? int(s_base + uint32_t(c) * plane_b) : kOutOfRange, fo);
       }
     }
   };
   auto write_stage = [&](int buf, const uint32_t (&a)[STG ? SQ : 1][4]) {
-    // every quad of the row, also those past C_in (the k-steps past the
+    // every unit of the row, also those past C_in (the k-steps past the
     // layer's multiply them, as zeros, by zero weights)
     uint4* row = &stg[buf][spx * PU];
 #pragma unroll
     for (int k = 0; k < SQ; ++k) {
-      const int qd = sq0 + 16 * k;
-      // (a compile-time test where the quads fill the threads: a divergent
+      const int qd = sq0 + TQ * k;
+      // (a compile-time test where the units fill the threads: a divergent
       // branch here would split the frame loop into blocks)
-      if ((SCH / 4) % 16 == 0 || qd < SCH / 4) {
-        if constexpr (kBF)
+      if ((SCH / CPT) % TQ == 0 || qd < SCH / CPT) {
+        if constexpr (kBF && CPT == 2)
+          reinterpret_cast<uint32_t*>(row)[qd] = a[k][0] | (a[k][1] << 16);
+        else if constexpr (kBF)
           reinterpret_cast<uint2*>(row)[qd] =
               make_uint2(a[k][0] | (a[k][1] << 16), a[k][2] | (a[k][3] << 16));
         else
@@ -1023,7 +1037,8 @@ void conv_steps_regp_kernel(ConvGeom g, RegSteps rs, RegPlan rp, const T* __rest
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, rs.x_bytes);
   const uint32_t plane_b = uint32_t(x_bc) * esz;
   constexpr int SCH = CSMAX * CKS;
-  constexpr int SQ = (SCH / 4 + 15) / 16;
+  constexpr int TQ = 4 * kRegStgWaves;  // quad slots: threads / 16 pixels
+  constexpr int SQ = (SCH / 4 + TQ - 1) / TQ;
   constexpr int PU = SCH * int(esz) / 16 + 1;
   constexpr int SPF = SQ <= 2 ? 4 : 2;  // frames in flight
   __shared__ uint4 stg[2][16 * PU];
@@ -1039,7 +1054,7 @@ void conv_steps_regp_kernel(ConvGeom g, RegSteps rs, RegPlan rp, const T* __rest
     const int fo = real ? t * rs.fstride : 0;
 #pragma unroll
     for (int k = 0; k < SQ; ++k) {
-      const int qd = sq0 + 16 * k;
+      const int qd = sq0 + TQ * k;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int c = 4 * qd + e;
@@ -1052,8 +1067,8 @@ void conv_steps_regp_kernel(ConvGeom g, RegSteps rs, RegPlan rp, const T* __rest
     uint4* row = &stg[buf][spx * PU];
 #pragma unroll
     for (int k = 0; k < SQ; ++k) {
-      const int qd = sq0 + 16 * k;
-      if ((SCH / 4) % 16 == 0 || qd < SCH / 4) {
+      const int qd = sq0 + TQ * k;
+      if ((SCH / 4) % TQ == 0 || qd < SCH / 4) {
         if constexpr (kBF)
           reinterpret_cast<uint2*>(row)[qd] =
               make_uint2(a[k][0] | (a[k][1] << 16), a[k][2] | (a[k][3] << 16));
@@ -1221,13 +1236,19 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   rs.fd_Wo = make_fastdiv(uint32_t(g.Wo));
   rs.fd_ofr = make_fastdiv(uint32_t(rs.o_frags));
   constexpr bool STG = TAPS == 1 && KSPLIT == 1;
-  rs.o_groups = int32_t(ceil_div(rs.o_frags, kRegStgWaves));
+  // staging waves per workgroup: the plan-driven kernel's, or the stride-1
+  // instantiation's that this call runs
+  const bool plan = STG && (g.sT != 1 || g.dT != 1);
+  const int sw = plan || !STG ? kRegStgWaves
+                 : g.kT == KTM ? reg_stg_waves<T, CSMAX, true>()
+                               : reg_stg_waves<T, CSMAX, false>();
+  rs.o_groups = int32_t(ceil_div(rs.o_frags, sw));
   rs.fd_og = make_fastdiv(uint32_t(rs.o_groups));
   // time segments: as many as keep every wave resident at the waves per
   // SIMD the instantiation is compiled for (1024 SIMDs), with each
   // segment's warm-up (kT - 1 frames) at most a quarter of its frames
   const int64_t wgs = STG ? int64_t(rs.m_frags) * rs.o_groups : blocks;
-  const int64_t waves = wgs * (STG ? kRegStgWaves : KSPLIT * kRegTiles);
+  const int64_t waves = wgs * (STG ? sw : KSPLIT * kRegTiles);
   constexpr int64_t kSimds = 1024;
   const int wpe = g.kT == KTM ? reg_steps_wpe<T, CSMAX, STG, true>()
                               : reg_steps_wpe<T, CSMAX, STG, false>();
@@ -1266,7 +1287,7 @@ hipError_t reg_steps_launch(const ConvGeom& g, const RegConfig& c, const ConvLay
   auto kern = g.kT == KTM ? conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, true, STG>
                           : conv_steps_reg_kernel<T, TAPS, CSMAX, KSPLIT, KTM, false, STG>;
   hipLaunchKernelGGL(kern, dim3(unsigned(8 * rs.blocks_per_xcd)),
-                     dim3(64 * (STG ? kRegStgWaves : KSPLIT * kRegTiles)),
+                     dim3(64 * (STG ? sw : KSPLIT * kRegTiles)),
                      0, s, g, rs, static_cast<const T*>(x), x_bc, static_cast<T*>(y),
                      reinterpret_cast<const uint4*>(state + L.weight),
                      reinterpret_cast<const float*>(state + L.bias),
