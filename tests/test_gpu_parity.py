@@ -610,6 +610,7 @@ REG_STEPS_CASES = [
     (3, 40, 20, (3, 1), (13,), (1, 0), "f32", 14),            # 1x1 spatial, small
     (32, 96, 128, (9, 1), (25,), (4, 0), "bf16", 14),         # deep temporal kernel, bf16
     (64, 64, 256, (5, 1), (25,), (2, 0), "bf16", 12),         # kT = 5 on the 9-tap shape (runtime kT)
+    (64, 64, 256, (3, 1), (25,), (1, 0), "bf16", 12),         # 3-tap shape, eight staging waves
     (2, 7, 17, (1, 3, 3), (6, 9), (0, 1, 1), "f32", 12),      # kT = 1: no ring
 ]
 
