@@ -706,21 +706,27 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
   // flight: the group, or where two waves share a SIMD (registers for two) a
   // divisor of it, at most SPF0
   constexpr int FPG_S = KTM * ((SPF0 + KTM - 1) / KTM);
+  // (two channels per staging thread leave registers for the whole group:
+  // vector memory operations complete in issue order, so a frame's wait
+  // for its staged loads also waits for every output store issued before
+  // them, and loads issued a whole group ahead put that wait on stores a
+  // group old)
   constexpr int SPF = !STG                                  ? 1
                       : reg_steps_wpe<T, CSMAX, STG, FULL>() == 1 ? FPG_S
+                      : CPT == 2                            ? FPG_S
                       : FPG_S % 4 == 0                      ? 4
                       : FPG_S % 3 == 0                      ? 3
                       : FPG_S % 2 == 0                      ? 2
                                                             : FPG_S;
   __shared__ uint4 stg[STG ? 2 : 1][STG ? 16 * PU : 1];
-  uint32_t sraw[SPF][STG ? SQ : 1][4];
+  uint32_t sraw[SPF][STG ? SQ : 1][CPT];
   const int tid = int(threadIdx.x);
   const int spx = tid & 15, sq0 = tid >> 4;
   const int Ps = mf * 16 + spx;
   const bool ps_ok = Ps < rs.M;
   const int sb = fdiv(ps_ok ? Ps : 0, rs.fd_So), sp = (ps_ok ? Ps : 0) - sb * rs.So;
   const uint32_t s_base = uint32_t(sb) * uint32_t(g.Cin) * plane_b + uint32_t(sp) * esz;
-  auto load_stage = [&](int t, uint32_t (&a)[STG ? SQ : 1][4]) {
+  auto load_stage = [&](int t, uint32_t (&a)[STG ? SQ : 1][CPT]) {
     const bool real = t < rs.T;  // uniform
     const int fo = real ? t * rs.fstride : 0;
 #pragma unroll
@@ -734,7 +740,7 @@ void conv_steps_reg_kernel(ConvGeom g, RegSteps rs, const T* __restrict__ x, int
       }
     }
   };
-  auto write_stage = [&](int buf, const uint32_t (&a)[STG ? SQ : 1][4]) {
+  auto write_stage = [&](int buf, const uint32_t (&a)[STG ? SQ : 1][CPT]) {
     // every unit of the row, also those past C_in (the k-steps past the
     // layer's multiply them, as zeros, by zero weights)
     uint4* row = &stg[buf][spx * PU];
